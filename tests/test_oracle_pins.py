@@ -1,0 +1,448 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests compares the oracle with itself: each uses a hand-worked
+value, a table of the paper, brute force, a closed form, an invariant, or a
+special case that reduces to a library routine (scipy, scikit-learn).
+"""
+import numpy as np
+import pytest
+from scipy.special import expit
+from scipy.stats import rankdata
+
+from oracle import fbdt_oracle as O
+from tests.golden_io import read_fixture
+
+
+# ---------------------------------------------------------------- SplitMix64
+def test_splitmix64_published_outputs():
+    # Reference outputs of SplitMix64 (Steele, Lea & Flood 2014) as published
+    # with the reference C implementation: seed 0 and seed 1234567.
+    assert int(O.splitmix64(0, [0])[0]) == 0xE220A8397B1DCDAF
+    got = [int(z) for z in O.splitmix64(1234567, np.arange(5))]
+    assert got == [6457827717110365317, 3203168211198807973, 9817491932198370423,
+                   4593380528125082431, 16408922859458223821]
+
+
+def test_subsample_mask_statistics():
+    n, alpha = 200_000, 0.5
+    m0 = O.subsample_mask(7, 0, n, alpha)
+    m1 = O.subsample_mask(7, 1, n, alpha)
+    sd = np.sqrt(n * alpha * (1 - alpha))
+    assert abs(m0.sum() - n * alpha) < 5 * sd
+    # trees draw independent samples: the overlap is alpha^2
+    assert abs((m0 & m1).sum() - n * alpha * alpha) < 5 * np.sqrt(n * 0.25 * 0.75)
+    u = O.uniform53(3, np.arange(100_000))
+    assert 0.0 <= u.min() and u.max() < 1.0
+    assert abs(u.mean() - 0.5) < 5 * np.sqrt(1 / 12 / u.size)
+    assert O.subsample_mask(9, 4, 1000, 1.0).all()
+    m = O.subsample_mask(9, 4, 100_000, 0.2)
+    assert abs(m.mean() - 0.2) < 0.01
+
+
+# ------------------------------------------------------------------- binning
+def _brute_bins(col, n_bins):
+    s = sorted(float(v) for v in col)
+    n = len(s)
+    b = [s[(k * n) // n_bins] for k in range(1, n_bins)]
+    return b, [sum(1 for bk in b if bk <= float(v)) for v in col]
+
+
+@pytest.mark.parametrize("n,n_bins,seed", [(37, 4, 0), (64, 8, 1), (100, 16, 2), (9, 2, 3)])
+def test_binning_brute_force(n, n_bins, seed):
+    rng = np.random.default_rng(seed)
+    col = rng.normal(size=n).astype(np.float32)
+    col[: n // 5] = col[n // 5]                         # a block of ties
+    b_ref, bins_ref = _brute_bins(col, n_bins)
+    b = O.quantile_boundaries(col, n_bins)
+    assert np.array_equal(b, np.array(b_ref, np.float32))
+    assert O.encode(col, b).tolist() == bins_ref
+
+
+def test_binning_equal_counts_for_distinct_values():
+    # section 2.2 / Fig. 3: equal-frequency bins hold equal counts
+    for n, n_bins in [(1000, 16), (1003, 7), (65_537, 256), (500, 256)]:
+        col = np.random.default_rng(n).permutation(n).astype(np.float32)
+        _, codes = O.bin_features(col[None, :], n_bins)
+        counts = np.bincount(codes[0], minlength=n_bins)
+        assert set(counts.tolist()) <= {n // n_bins, -(-n // n_bins)}
+        assert counts.sum() == n
+
+
+def test_binning_ties_share_a_bin_and_empty_bins_are_kept():
+    col = np.repeat(np.array([0.0, 1.0, 2.0], np.float32), [500, 300, 200])
+    b, codes = O.bin_features(col[None, :], 16)
+    for value in (0.0, 1.0, 2.0):
+        assert len(set(codes[0][col == value].tolist())) == 1
+    assert len(set(codes[0].tolist())) == 3
+    # values below every boundary go to bin 0, +-inf to the ends
+    assert O.encode(np.array([-np.inf, np.inf], np.float32), b[0]).tolist() == [0, 15]
+    with pytest.raises(ValueError):
+        O.encode(np.array([np.nan], np.float32), b[0])
+
+
+def test_binning_monotone_transform_invariance():
+    # section 2.2: trees only use the order statistic of the features
+    rng = np.random.default_rng(5)
+    x = rng.normal(size=(3, 2000)).astype(np.float32)
+    x[1, :300] = 0.25
+    ranks = np.stack([rankdata(x[j], method="min") for j in range(3)]).astype(np.float32)
+    for xt in (x * np.float32(2.0), ranks):
+        _, c0 = O.bin_features(x, 32)
+        _, c1 = O.bin_features(xt, 32)
+        assert np.array_equal(c0, c1)
+
+
+# --------------------------------------------------------- XOR, Table 3
+def test_xor_table3():
+    rows, ex = read_fixture("xor_table3.txt")
+    rows = np.array(rows)
+    x = rows[:, :2].T.astype(np.float32)
+    y = np.where(rows[:, 2] > 0, 1, -1).astype(np.int8)
+    _, xb = O.bin_features(x, 2)
+    assert np.array_equal(xb, x.astype(np.uint8))
+    m = O.fit(xb, y, np.ones(4, np.float32), depth=2, n_trees=1, shrinkage=1.0,
+              subsample=1.0, seed=0, n_bins=2)
+    assert (m.cut_feature[0, 0], m.cut_bin[0, 0]) == tuple(int(v) for v in ex["root_cut"])
+    assert m.gain[0, 0] == ex["root_gain"][0]
+    for k in (1, 2):
+        assert (m.cut_feature[0, k], m.cut_bin[0, k]) == tuple(int(v) for v in ex["layer2_cut"])
+        assert m.gain[0, k] == ex["layer2_gain"][0]
+    p, _ = O.apply(m, xb)
+    sig = y > 0
+    assert np.allclose(p[sig], ex["p_signal"][0], rtol=0, atol=1e-7)
+    assert np.allclose(p[~sig], ex["p_background"][0], rtol=0, atol=1e-7)
+    assert np.allclose(O.feature_importance(m), ex["importance"])
+
+
+# ------------------------------------------------ hand-worked depth-1 example
+def _hand_case():
+    _, ex = read_fixture("hand_depth1.txt")
+    x = np.array(ex["x"], np.float32)[None, :]
+    y = np.array(ex["y"], np.int8)
+    return x, y, ex
+
+
+def test_hand_example_binning_histograms_gains():
+    x, y, ex = _hand_case()
+    b, xb = O.bin_features(x, 4)
+    assert b[0].tolist() == ex["boundaries"]
+    assert xb[0].tolist() == ex["bins"]
+    w = np.ones(8, np.float32)
+    H = O.histogram(xb, np.ones(8, np.int64), w, y > 0, 0, 4)
+    assert H[0, 0, :, 0].tolist() == ex["hist_signal"]
+    assert H[0, 0, :, 1].tolist() == ex["hist_background"]
+    S, Bk = O.cumulative(H)
+    assert S[0, 0].tolist() == ex["cph_signal"]
+    assert Bk[0, 0].tolist() == ex["cph_background"]
+    g = O.split_gains(S, Bk)
+    assert np.allclose(g[0, 0], ex["tree1_gains"], rtol=0, atol=1e-15)
+    f, c, _ = O.best_cuts(g)
+    assert (int(f[0]), int(c[0])) == (0, int(ex["tree1_cut"][0]))
+
+
+@pytest.mark.parametrize("eta", [1.0, 0.1])
+def test_hand_example_two_trees(eta):
+    x, y, ex = _hand_case()
+    _, xb = O.bin_features(x, 4)
+    trace = []
+    m = O.fit(xb, y, np.ones(8, np.float32), depth=1, n_trees=2, shrinkage=eta,
+              subsample=1.0, seed=0, n_bins=4, trace=trace)
+    assert m.f0 == 0.0
+    assert int(m.cut_bin[0, 0]) == int(ex["tree1_cut"][0])
+    assert np.allclose(m.leaf[0] / eta, ex["tree1_leaves"], rtol=1e-15)
+    g2 = O.split_gains(*O.cumulative(trace[1]["H"]))[0, 0]
+    if eta == 1.0:
+        p1, _ = O.apply(m, xb, n_trees=1)
+        assert np.allclose(p1[[0, 7]], ex["tree1_p_eta1"], atol=1e-7)
+        assert np.allclose(g2, ex["tree2_gains_eta1"], atol=1e-6)
+        assert int(m.cut_bin[1, 0]) == int(ex["tree2_cut_eta1"][0])
+        assert np.allclose(m.leaf[1], ex["tree2_leaves_eta1"], atol=1e-6)
+        p2, _ = O.apply(m, xb)
+        assert np.allclose(p2[[0, 2, 4]], ex["tree2_p_eta1"], atol=1e-6)
+    else:
+        p1, _ = O.apply(m, xb, n_trees=1)
+        assert np.allclose(p1[[0, 7]], ex["tree1_p_eta01"], atol=1e-6)
+        assert np.allclose(g2, ex["tree2_gains_eta01"], atol=1e-6)
+        assert int(m.cut_bin[1, 0]) == int(ex["tree2_cut_eta01"][0])
+
+
+# ------------------------------------------------------------- histograms
+def _brute_hist(xb, node, w, y, layer, n_bins):
+    d, n = xb.shape
+    H = np.zeros((1 << layer, d, n_bins, 2))
+    for i in range(n):
+        for j in range(d):
+            H[node[i] - (1 << layer), j, xb[j, i], 0 if y[i] > 0 else 1] += float(w[i])
+    return H
+
+
+@pytest.mark.parametrize("layer", [0, 1, 2])
+def test_histogram_brute_force_and_totals(layer):
+    rng = np.random.default_rng(layer)
+    n, d, nb = 300, 3, 8
+    xb = rng.integers(0, nb, (d, n)).astype(np.uint8)
+    y = np.where(rng.random(n) < 0.4, 1, -1).astype(np.int8)
+    w = rng.uniform(0, 2, n).astype(np.float32)
+    w[rng.random(n) < 0.5] = 0                          # unsampled events
+    node = rng.integers(1 << layer, 2 << layer, n)
+    H = O.histogram(xb, node, w, y > 0, layer, nb)
+    assert np.allclose(H, _brute_hist(xb, node, w, y, layer, nb), rtol=1e-14, atol=0)
+    tot = H.sum(axis=2)                                 # [node][feature][class]
+    for k in range(1 << layer):
+        for c, sel in ((0, y > 0), (1, y < 0)):
+            ref = float(np.sum(w[(node == (1 << layer) + k) & sel].astype(np.float64)))
+            assert np.allclose(tot[k, :, c], ref, rtol=1e-13, atol=1e-300)
+
+
+# ------------------------------------------------------------- best cuts
+def _brute_best(xb, w, y, n_bins):
+    """Enumerate every (feature, cut) by partitioning the events directly."""
+    d, n = xb.shape
+
+    def G(s, b):
+        return 0.0 if s + b == 0 else s * b / (s + b)
+
+    ST = sum(float(w[i]) for i in range(n) if y[i] > 0)
+    BT = sum(float(w[i]) for i in range(n) if y[i] < 0)
+    best = (-np.inf, None)
+    gains = {}
+    for j in range(d):
+        for c in range(1, n_bins):
+            sl = sum(float(w[i]) for i in range(n) if y[i] > 0 and xb[j, i] < c)
+            bl = sum(float(w[i]) for i in range(n) if y[i] < 0 and xb[j, i] < c)
+            sr = sum(float(w[i]) for i in range(n) if y[i] > 0 and xb[j, i] >= c)
+            br = sum(float(w[i]) for i in range(n) if y[i] < 0 and xb[j, i] >= c)
+            g = G(ST, BT) - G(sl, bl) - G(sr, br)
+            gains[(j, c)] = g
+            if g > best[0] + 1e-12:
+                best = (g, (j, c))
+    return best, gains
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_best_cut_brute_force(seed):
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(2, 64))
+    d = int(rng.integers(1, 5))
+    nb = int(rng.integers(2, 9))
+    xb = rng.integers(0, nb, (d, n)).astype(np.uint8)
+    y = np.where(rng.random(n) < 0.5, 1, -1).astype(np.int8)
+    w = rng.uniform(0.1, 2, n).astype(np.float32)
+    (gbest, jc), gains = _brute_best(xb, w, y, nb)
+    g = O.split_gains(*O.cumulative(O.histogram(xb, np.ones(n, int), w, y > 0, 0, nb)))
+    for (j, c), ref in gains.items():
+        assert abs(g[0, j, c - 1] - ref) <= 1e-12 * max(1.0, abs(ref))
+    f, c, best = O.best_cuts(g)
+    assert abs(best[0] - gbest) <= 1e-12 * max(1.0, abs(gbest))
+    # the oracle's choice is the lowest (feature, cut) among the best
+    near = sorted(k for k, v in gains.items() if v >= gbest - 1e-12 * max(1.0, abs(gbest)))
+    assert (int(f[0]), int(c[0])) == near[0]
+
+
+def test_weighted_gini_stump_matches_sklearn():
+    # the gain is the weighted Gini decrease: a depth-1 scikit-learn tree with
+    # the same sample weights picks the same partition
+    from sklearn.tree import DecisionTreeClassifier
+    for seed in range(5):
+        rng = np.random.default_rng(seed)
+        n, d, nb = 3000, 5, 32
+        xb = rng.integers(0, nb, (d, n)).astype(np.uint8)
+        logit = 0.08 * (xb[0].astype(float) - 16) - 0.05 * (xb[3].astype(float) - 16)
+        y = np.where(rng.random(n) < expit(logit), 1, -1).astype(np.int8)
+        w = rng.uniform(0.05, 3.0, n).astype(np.float32)
+        g = O.split_gains(*O.cumulative(O.histogram(xb, np.ones(n, int), w, y > 0, 0, nb)))
+        f, c, _ = O.best_cuts(g)
+        clf = DecisionTreeClassifier(criterion="gini", max_depth=1, random_state=0)
+        clf.fit(xb.T.astype(np.float64), y, sample_weight=w.astype(np.float64))
+        assert clf.tree_.feature[0] == f[0]
+        thr = clf.tree_.threshold[0]
+        col = xb[f[0]]
+        assert np.array_equal(col < c[0], col <= thr)
+
+
+def test_first_tree_matches_sklearn_classifier():
+    # first boosting step, F0 = 0, unit weights, no sub-sampling: every weight
+    # is 1 and the terminal boost weight is (S - B) / (S + B) = 2 p_signal - 1
+    from sklearn.tree import DecisionTreeClassifier
+    rng = np.random.default_rng(11)
+    n, d, nb, D = 4000, 4, 64, 3
+    xb = rng.integers(0, nb, (d, n)).astype(np.uint8)
+    logit = 0.05 * (xb[1].astype(float) - 32) + 0.04 * (xb[2].astype(float) - 32) ** 2 / 32
+    score = logit + rng.logistic(size=n)
+    y = np.where(score > np.median(score), 1, -1).astype(np.int8)   # exactly 50/50: F0 = 0
+    m = O.fit(xb, y, np.ones(n, np.float32), depth=D, n_trees=1, shrinkage=1.0,
+              subsample=1.0, seed=0, n_bins=nb)
+    assert m.f0 == 0.0
+    clf = DecisionTreeClassifier(criterion="gini", max_depth=D, random_state=0)
+    clf.fit(xb.T.astype(np.float64), y)
+    tr = clf.tree_
+    # walk both trees together and compare every partition scikit-learn makes
+    stack = [(1, 0, np.arange(n))]
+    while stack:
+        k, s, idx = stack.pop()
+        if tr.children_left[s] < 0:
+            continue
+        f, c = int(m.cut_feature[0, k - 1]), int(m.cut_bin[0, k - 1])
+        assert f == tr.feature[s]
+        left = xb[f, idx] < c
+        assert np.array_equal(left, xb[f, idx] <= tr.threshold[s])
+        stack.append((2 * k, tr.children_left[s], idx[left]))
+        stack.append((2 * k + 1, tr.children_right[s], idx[~left]))
+    _, F = O.apply(m, xb)
+    proba = clf.predict_proba(xb.T.astype(np.float64))[:, list(clf.classes_).index(1)]
+    assert np.allclose(F, 2 * proba - 1, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------- boosting recursion
+def test_pseudo_response_is_scaled_logistic_residual():
+    rng = np.random.default_rng(2)
+    F = rng.normal(0, 2, 1000)
+    y = np.where(rng.random(1000) < 0.5, 1, -1)
+    y01 = (y > 0).astype(float)
+    assert np.allclose(O.pseudo_response(y, F), 2 * (y01 - expit(2 * F)), rtol=1e-13, atol=1e-15)
+
+
+def test_boosting_matches_sklearn_gradient_boosting_one_binary_feature():
+    # With one binary feature every tree has the same single partition, so
+    # the scores of scikit-learn's log-loss gradient boosting (raw score 2F,
+    # Newton-step leaves, log-odds prior) must equal 2F of this method
+    # (Friedman's two-class LK_TreeBoost) for every tree and weight choice.
+    from sklearn.ensemble import GradientBoostingClassifier
+    rng = np.random.default_rng(4)
+    n, T, eta = 2000, 6, 0.3
+    xb = rng.integers(0, 2, (1, n)).astype(np.uint8)
+    y = np.where(rng.random(n) < np.where(xb[0] == 1, 0.7, 0.35), 1, -1).astype(np.int8)
+    v = rng.uniform(0.2, 2.0, n).astype(np.float32)
+    m, Ffit = O.fit(xb, y, v, depth=1, n_trees=T, shrinkage=eta, subsample=1.0, seed=0,
+                    n_bins=2, final_score=True)
+    gb = GradientBoostingClassifier(loss="log_loss", learning_rate=eta, n_estimators=T,
+                                    max_depth=1, subsample=1.0, random_state=0)
+    X = xb.T.astype(np.float64)
+    gb.fit(X, y, sample_weight=v.astype(np.float64))
+    raw = gb.decision_function(X)
+    assert np.allclose(2 * Ffit, raw, rtol=1e-9, atol=1e-12)
+    p, F = O.apply(m, xb)
+    assert np.allclose(p, gb.predict_proba(X)[:, 1], rtol=0, atol=2e-7)
+    assert np.allclose(2 * m.f0, np.log(v[y > 0].sum(dtype=np.float64) / v[y < 0].sum(dtype=np.float64)))
+
+
+def test_first_tree_closed_form_leaves():
+    rng = np.random.default_rng(8)
+    n, d, nb = 1000, 3, 16
+    xb = rng.integers(0, nb, (d, n)).astype(np.uint8)
+    y = np.where(np.arange(n) % 2 == 0, 1, -1).astype(np.int8)
+    m = O.fit(xb, y, np.ones(n, np.float32), depth=2, n_trees=1, shrinkage=1.0,
+              subsample=1.0, seed=0, n_bins=nb)
+    node = np.ones(n, int)
+    for layer in range(2):
+        lo = (1 << layer) - 1
+        node = O.route(node, xb, m.cut_feature[0, lo:lo + (1 << layer)],
+                       m.cut_bin[0, lo:lo + (1 << layer)], layer)
+    for leaf in range(4):
+        sel = node == 4 + leaf
+        s, b = int(np.sum(y[sel] > 0)), int(np.sum(y[sel] < 0))
+        ref = 0.0 if s + b == 0 else (s - b) / (s + b)
+        assert abs(m.leaf[0, leaf] - ref) < 1e-15
+
+
+# ----------------------------------------------------------- invariants
+def _fit_small(xb, y, v, seed=3, alpha=0.5, T=5, D=3, nb=16):
+    return O.fit(xb, y, v, depth=D, n_trees=T, shrinkage=0.1, subsample=alpha, seed=seed,
+                 n_bins=nb, final_score=True)
+
+
+def _small_problem(seed=1):
+    rng = np.random.default_rng(seed)
+    n, d, nb = 3000, 4, 16
+    xb = rng.integers(0, nb, (d, n)).astype(np.uint8)
+    y = np.where(rng.random(n) < expit(0.2 * (xb[0].astype(float) - 8)), 1, -1).astype(np.int8)
+    v = rng.uniform(0.5, 1.5, n).astype(np.float32)
+    return xb, y, v
+
+
+def test_label_swap_symmetry():
+    xb, y, v = _small_problem()
+    m1, F1 = _fit_small(xb, y, v)
+    m2, F2 = _fit_small(xb, (-y).astype(np.int8), v)
+    assert np.array_equal(m1.cut_feature, m2.cut_feature)
+    assert np.array_equal(m1.cut_bin, m2.cut_bin)
+    assert np.allclose(F1, -F2, rtol=1e-12, atol=1e-14)
+    p1, _ = O.apply(m1, xb)
+    p2, _ = O.apply(m2, xb)
+    assert np.allclose(p1, 1 - p2, atol=1e-7)
+
+
+def test_weight_scale_invariance():
+    xb, y, v = _small_problem()
+    m1, F1 = _fit_small(xb, y, v)
+    m2, F2 = _fit_small(xb, y, v * np.float32(4))
+    assert np.array_equal(m1.cut_bin, m2.cut_bin)
+    assert np.array_equal(m1.cut_feature, m2.cut_feature)
+    assert np.array_equal(m1.leaf, m2.leaf)
+    assert np.array_equal(F1, F2)
+
+
+def test_no_subsampling_removes_randomness():
+    xb, y, v = _small_problem()
+    m1, _ = _fit_small(xb, y, v, seed=1, alpha=1.0)
+    m2, _ = _fit_small(xb, y, v, seed=99, alpha=1.0)
+    assert np.array_equal(m1.leaf, m2.leaf)
+    m3, _ = _fit_small(xb, y, v, seed=1, alpha=0.5)
+    m4, _ = _fit_small(xb, y, v, seed=99, alpha=0.5)
+    assert not np.array_equal(m3.leaf, m4.leaf)
+
+
+def test_apply_reproduces_fit_score():
+    xb, y, v = _small_problem()
+    m, F = _fit_small(xb, y, v, T=8)
+    _, Fa = O.apply(m, xb)
+    assert np.array_equal(F, Fa)
+
+
+def test_model_invariant_under_monotone_feature_transform():
+    rng = np.random.default_rng(6)
+    x = rng.normal(size=(3, 2000)).astype(np.float32)
+    y = np.where(rng.random(2000) < expit(x[0] - 0.5 * x[2]), 1, -1).astype(np.int8)
+    v = np.ones(2000, np.float32)
+    _, xb1 = O.bin_features(x, 16)
+    ranks = np.stack([rankdata(x[j], method="min") for j in range(3)]).astype(np.float32)
+    m1 = O.fit(xb1, y, v, 3, 4, 0.1, 0.5, 0, 16)
+    for xt in (x * np.float32(2.0), ranks):
+        _, xb2 = O.bin_features(xt, 16)
+        m2 = O.fit(xb2, y, v, 3, 4, 0.1, 0.5, 0, 16)
+        assert np.array_equal(m1.cut_bin, m2.cut_bin) and np.array_equal(m1.leaf, m2.leaf)
+
+
+def test_empty_node_takes_first_cut_and_zero_leaves():
+    # all events share one bin of every feature: no cut separates anything,
+    # every gain is 0, so every node takes (feature 0, cut 1); the side that
+    # receives no event gets boost weight 0
+    n = 50
+    xb = np.full((2, n), 3, np.uint8)
+    y = np.where(np.arange(n) % 3 == 0, 1, -1).astype(np.int8)
+    m = O.fit(xb, y, np.ones(n, np.float32), depth=2, n_trees=1, shrinkage=1.0,
+              subsample=1.0, seed=0, n_bins=8)
+    assert m.cut_feature[0].tolist() == [0, 0, 0]
+    assert m.cut_bin[0].tolist() == [1, 1, 1]
+    assert np.all(m.gain[0] == 0.0)
+    assert m.leaf[0, 0] == 0.0 and m.leaf[0, 1] == 0.0 and m.leaf[0, 2] == 0.0
+    assert m.leaf[0, 3] != 0.0
+
+
+def test_apply_hand_built_forest():
+    # a depth-2 tree written by hand, traced as in Fig. 1 (left = bin < cut)
+    m = O.Model(depth=2, n_bins=8, n_features=2, f0=0.25,
+                cut_feature=np.array([[0, 1, 0]], np.uint8),
+                cut_bin=np.array([[3, 5, 2]], np.uint8),
+                gain=np.zeros((1, 3)),
+                leaf=np.array([[0.1, 0.2, 0.3, 0.4]]))
+    xb = np.array([[0, 2, 3, 7, 1], [4, 5, 0, 7, 6]], np.uint8)
+    # event 0: f0=0<3 -> node 2: f1=4<5 -> leaf 4 (0.1)
+    # event 1: f0=2<3 -> node 2: f1=5>=5 -> leaf 5 (0.2)
+    # event 2: f0=3>=3 -> node 3: f0=3>=2 -> leaf 7 (0.4)
+    # event 3: f0=7>=3 -> node 3: f0=7>=2 -> leaf 7 (0.4)
+    # event 4: f0=1<3 -> node 2: f1=6>=5 -> leaf 5 (0.2)
+    p, F = O.apply(m, xb)
+    ref = 0.25 + np.array([0.1, 0.2, 0.4, 0.4, 0.2])
+    assert np.allclose(F, ref, rtol=0, atol=1e-15)
+    assert np.allclose(p, expit(2 * ref), rtol=0, atol=1e-7)
