@@ -1,0 +1,226 @@
+/*
+ * fbdt.h -- C ABI of libfbdt, a HIP implementation for AMD gfx950 (MI355X)
+ * of the fitting and application hot path of FastBDT, the stochastic
+ * gradient-boosted decision trees of T. Keck, "FastBDT: A speed-optimized
+ * and cache-friendly implementation of stochastic gradient-boosted decision
+ * trees for multivariate classification", arXiv:1609.06119.
+ *
+ * Conventions for every call
+ *  - Arrays marked "device" are device pointers that the caller allocates
+ *    and owns (e.g. torch tensors on the current HIP device); arrays marked
+ *    "host" are ordinary host memory.
+ *  - Features are feature-major: element (j, i) of a float array with row
+ *    stride ldx is x[j * ldx + i]; binned codes use row stride ldb.
+ *    ldb must be a multiple of 16, ldb >= n, and the code buffer must be
+ *    16-byte aligned and hold d * ldb bytes.  Bytes of a row beyond n are
+ *    read but never influence a result.
+ *  - Labels are int8: +1 signal, -1 background (section 1).  Weights are
+ *    float32, finite and >= 0; NULL means unit weights.
+ *  - stream is a hipStream_t (NULL = the null stream).  Calls are
+ *    stream-ordered; the ones documented as synchronising also wait for it.
+ *  - Return value: FBDT_OK (0) or a negative FBDT_E_* code.  On error the
+ *    outputs are left untouched where the call checks before it writes (all
+ *    argument checks), and fbdt_last_error() describes the failure.
+ *  - Calls on distinct models and streams may run concurrently; calls that
+ *    fit on the same device serialise on the library's scratch memory.
+ *
+ * Notation: N events, d features, B bins, D depth, T trees, eta shrinkage,
+ * alpha sub-sampling rate.  Node ids are heap-ordered: the root is 1, layer
+ * l (0-based) holds nodes [2^l, 2^(l+1)), leaves are [2^D, 2^(D+1)).  A cut
+ * (f, c) sends an event to the left child 2n if its bin of feature f is < c
+ * and to the right child 2n+1 otherwise (Fig. 1).
+ */
+#ifndef FBDT_H
+#define FBDT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum fbdt_status {
+    FBDT_OK = 0,
+    FBDT_E_INVAL = -1,  /* null pointer, size or parameter out of range      */
+    FBDT_E_LABEL = -2,  /* a label not in {+1, -1}, or a class with no weight */
+    FBDT_E_NAN = -3,    /* NaN among the float features                       */
+    FBDT_E_WEIGHT = -4, /* a weight < 0 or not finite                         */
+    FBDT_E_SHAPE = -5,  /* too few features for the model                     */
+    FBDT_E_DEVICE = -6  /* HIP runtime error or out of device memory          */
+};
+
+typedef struct fbdt_model fbdt_model; /* opaque, owned by the library */
+
+/* Hyper-parameters of a fit (sections 1.1-1.4). */
+typedef struct {
+    int32_t depth;     /* D, number of cut layers, 1..7                        */
+    int32_t n_trees;   /* T >= 1, number of boosting steps                     */
+    double shrinkage;  /* eta > 0, multiplies every terminal boost weight      */
+    double subsample;  /* alpha in (0, 1], per-tree sampling rate              */
+    uint64_t seed;     /* seed of the sub-sample generator (SplitMix64)        */
+} fbdt_fit_params;
+
+/* A model laid out in plain host arrays (heap order: node k at index k-1). */
+typedef struct {
+    int32_t n_trees, depth, n_features, n_bins;
+    double f0;                  /* initial score: half the weighted log-odds */
+    const uint8_t *cut_feature; /* host [T][2^D - 1]                         */
+    const uint8_t *cut_bin;     /* host [T][2^D - 1], each in 1..B-1          */
+    const double *gain;         /* host [T][2^D - 1] separation gain, or NULL */
+    const double *leaf;         /* host [T][2^D], boost weight times eta      */
+    const float *boundaries;    /* host [d][B - 1] bin boundaries, or NULL    */
+} fbdt_model_view;
+
+/*
+ * Equal-frequency binning of a training sample (section 2.2, Fig. 3).
+ * For each feature j, with s the ascending sort of x[j][0..n), boundary k
+ * (k = 1..B-1) is s[floor(k n / B)] and a value goes to bin
+ * #{k : boundary_k <= value}.  Tied values share a bin; repeated boundaries
+ * leave empty bins.  x: device float32 [d][ldx]; boundaries: host float32
+ * [d][B-1] (output); xb: device uint8 [d][ldb] (output).  1 <= d <= 255,
+ * 2 <= n_bins <= 256, n >= 1.  The sort runs on the host; the call
+ * synchronises the stream.  Returns FBDT_E_NAN if any value is NaN.
+ */
+int fbdt_bin(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
+             float *boundaries, uint8_t *xb, int64_t ldb, void *stream);
+
+/*
+ * Bin fresh events with the boundaries of a training sample (section 2.2).
+ * Same layouts as fbdt_bin; boundaries is host input.  Synchronises the
+ * stream to report NaN inputs (FBDT_E_NAN).
+ */
+int fbdt_bin_transform(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
+                       const float *boundaries, uint8_t *xb, int64_t ldb, void *stream);
+
+/*
+ * Fit T trees of depth D by stochastic gradient boosting (sections 1.1-1.4,
+ * 2.1) on binned features: two-class LK_TreeBoost with a SplitMix64
+ * Bernoulli sub-sample per tree, per-layer signal/background histograms of
+ * all nodes and features in one pass, cumulative histograms, weighted Gini
+ * separation gain, lowest-(feature, bin) argmax, and Newton-step terminal
+ * weights.  xb: device uint8 [d][ldb]; y: device int8 [n]; w: device
+ * float32 [n] or NULL; score_out: optional device float64 [n] that receives
+ * the final score F of every event.  *out receives a new model (free with
+ * fbdt_model_free).  Synchronises the stream before returning.
+ */
+int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bins,
+             const int8_t *y, const float *w, const fbdt_fit_params *params,
+             fbdt_model **out, double *score_out, void *stream);
+
+/*
+ * Score events (Fig. 1, section 1.3): F = f0 + sum over trees of the leaf
+ * reached, accumulated in float64 in tree order; prob = 1 / (1 + exp(-2F))
+ * rounded to float32.  xb: device uint8 [d][ldb] with d >= the model's
+ * feature count (else FBDT_E_SHAPE); prob: device float32 [n] (output);
+ * score: optional device float64 [n] (output).  Stream-ordered.
+ */
+int fbdt_apply(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
+               float *prob, double *score, void *stream);
+
+/* Borrowed host view of a model, valid until fbdt_model_free. */
+int fbdt_model_export(const fbdt_model *m, fbdt_model_view *view);
+
+/* New model from host arrays (copied); gain and boundaries may be NULL. */
+int fbdt_model_import(const fbdt_model_view *view, fbdt_model **out);
+
+void fbdt_model_free(fbdt_model *m);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *fbdt_last_error(void);
+
+/* ---- The steps of one boosting iteration, callable one at a time ------- */
+
+/*
+ * Re-weighting of one tree (sections 1.3, 1.4): for every event,
+ * y~ = 2y / (1 + exp(2 y F)); sampled iff the (tree * n + i)-th SplitMix64
+ * output of seed, top 53 bits over 2^53, is < alpha; w_out = fl32(v |y~|)
+ * if sampled, else 0, carrying the class in its sign (+ signal,
+ * - background).  y, v (NULL = unit), F: device [n]; w_out: device float32
+ * [n].  Stream-ordered.
+ */
+int fbdt_tree_weights(const int8_t *y, const float *v, const double *F, int64_t n,
+                      uint64_t seed, int32_t tree, double alpha, float *w_out, void *stream);
+
+/*
+ * Signal/background histograms of every node and feature of one layer
+ * (sections 1.1, 2.1): hist[k][j][b][c] = sum of |w_i| over events with
+ * node_i = 2^layer + k, bin b in feature j, class c (0 = signal, w > 0;
+ * 1 = background, w < 0); events with w = 0 are skipped.  node: device
+ * uint8 [n] heap ids of the layer; w: device float32 [n] as produced by
+ * fbdt_tree_weights; hist: device float64 [2^layer][d][B][2] (output,
+ * overwritten).  0 <= layer <= 6.  Stream-ordered.
+ */
+int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bins,
+                   const uint8_t *node, const float *w, int32_t layer, double *hist,
+                   void *stream);
+
+/*
+ * Cumulative histograms, separation gains and best cut of every node of a
+ * layer (section 1.1).  For node k and feature j with cumulative sums S(c),
+ * B(c) of the bins below c and totals S_T, B_T:
+ *   gain(c) = (G(S_T, B_T) - G(S(c), B(c))) - G(S_T - S(c), B_T - B(c)),
+ *   G(s, b) = s b / (s + b), 0 when s + b = 0, for c = 1..B-1;
+ * the cut is the highest gain, ties to the lowest feature, then bin.
+ * hist: device float64 [n_nodes][d][B][2]; cut_feature, cut_bin: device
+ * uint8 [n_nodes]; gain: device float64 [n_nodes].  Stream-ordered.
+ */
+int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bins,
+                   uint8_t *cut_feature, uint8_t *cut_bin, double *gain, void *stream);
+
+/*
+ * Route every event one layer down (section 1.1): node <- 2 node +
+ * [xb[f][i] >= c] with (f, c) the cut of its node.  node: device uint8 [n],
+ * updated in place (ids of `layer` on entry); cut_feature, cut_bin: device
+ * uint8 [2^layer].  Stream-ordered.
+ */
+int fbdt_route(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, uint8_t *node,
+               const uint8_t *cut_feature, const uint8_t *cut_bin, int32_t layer,
+               void *stream);
+
+/*
+ * Terminal boost weights of one tree (section 1.3, Friedman's Newton step):
+ * leaf[j] = eta * sum(v y~) / sum(v |y~| (2 - |y~|)) over the sampled
+ * events of leaf j (0 if the denominator is 0), with y~ and the sample as
+ * in fbdt_tree_weights.  node: device uint8 [n] leaf heap ids (2^D..);
+ * leaf: device float64 [2^D] (output).  Stream-ordered.
+ */
+int fbdt_leaf_values(const uint8_t *node, const int8_t *y, const float *v, const double *F,
+                     int64_t n, int32_t depth, uint64_t seed, int32_t tree, double alpha,
+                     double eta, double *leaf, void *stream);
+
+/* ---- Measurement and tuning -------------------------------------------- */
+
+enum fbdt_kernel_kind {
+    FBDT_K_HISTOGRAM = 0, /* per-layer histogram pass (with fused routing)   */
+    FBDT_K_BEST_CUTS = 1, /* CPH scan, gain and argmax of one layer          */
+    FBDT_K_TREE_PREP = 2, /* score update and re-weighting of one tree       */
+    FBDT_K_LEAF = 3,      /* last routing and terminal boost weights          */
+    FBDT_K_APPLY = 4,     /* forest traversal                                */
+    FBDT_K_ENCODE = 5,    /* float -> bin code                                */
+    FBDT_K_COUNT = 6
+};
+
+/*
+ * Kernel timing with HIP events recorded on the launching stream around
+ * every launch of the selected kinds (bit k of `kinds` selects kind k;
+ * 0 turns timing off, the default).  The call resets the tallies.
+ * fbdt_timing_read waits for the recorded events and returns
+ * the number of launches of a kind, their summed duration in milliseconds
+ * and, for the histogram kind, the summed algorithmic bytes those launches
+ * move (features, node ids, weights, routing and the histogram written).
+ */
+int fbdt_timing_enable(int32_t kinds);
+int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *bytes);
+
+/*
+ * Launch-shape overrides for sweeps; value 0 restores the default.
+ * Names: "hist_features_per_group", "hist_event_chunks", "hist_threads",
+ * "apply_threads".  Returns FBDT_E_INVAL for an unknown name.
+ */
+int fbdt_set_option(const char *name, int64_t value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FBDT_H */

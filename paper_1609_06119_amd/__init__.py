@@ -1,0 +1,23 @@
+"""FastBDT's fit and apply hot path on AMD gfx950 (MI355X) through libfbdt.
+
+Import is light: the HIP library is loaded on the first call.
+"""
+from .api import (  # noqa: F401
+    Codes,
+    FbdtError,
+    Model,
+    apply,
+    best_cuts,
+    bin,
+    bin_transform,
+    fit,
+    histogram,
+    leaf_values,
+    padded_stride,
+    route,
+    set_option,
+    timing_enable,
+    timing_read,
+    tree_weights,
+)
+from ._lib import EXPORTED, LIB_PATH, lib  # noqa: F401

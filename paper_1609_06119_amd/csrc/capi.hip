@@ -1,0 +1,796 @@
+// C ABI of libfbdt (declared in include/fbdt.h) and the host runtime around
+// the kernels: argument checks, per-device scratch, the stream-ordered
+// boosting loop, model storage and kernel timing.
+#include "fbdt.h"
+#include "fbdt_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <vector>
+
+using namespace fbdt;
+
+struct fbdt_model {
+    int32_t n_trees = 0, depth = 0, n_features = 0, n_bins = 0;
+    double f0 = 0.0;
+    std::vector<uint8_t> cut_feature, cut_bin;
+    std::vector<double> gain, leaf;
+    std::vector<float> boundaries;
+    // device copies of the forest for apply, one per device used
+    struct DeviceCopy {
+        int device;
+        uint16_t *cuts;
+        double *leaves;
+    };
+    std::mutex mu;
+    std::vector<DeviceCopy> copies;
+};
+
+namespace {
+
+thread_local std::string g_error;
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                    \
+    do {                                                                                 \
+        hipError_t e_ = (expr);                                                          \
+        if (e_ != hipSuccess)                                                            \
+            return fail(FBDT_E_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));   \
+    } while (0)
+
+struct DeviceInfo {
+    int cu_count = 0;
+    size_t max_lds = 0;
+};
+
+std::mutex g_dev_mu;
+std::vector<DeviceInfo> g_dev_info(64);
+
+int device_info(int dev, DeviceInfo *out) {
+    if (dev < 0 || dev >= 64) return fail(FBDT_E_DEVICE, "device id %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    DeviceInfo &di = g_dev_info[dev];
+    if (di.cu_count == 0) {
+        int cu = 0, lds = 0;
+        HIP_TRY(hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev));
+        HIP_TRY(hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
+        di.cu_count = cu;
+        di.max_lds = (size_t)lds;
+    }
+    *out = di;
+    return FBDT_OK;
+}
+
+// ---- options --------------------------------------------------------------
+std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0},
+    opt_apply_threads{0};
+
+// ---- timing ---------------------------------------------------------------
+struct PendingTiming {
+    int kind;
+    hipEvent_t start, stop;
+    double bytes;
+};
+std::mutex g_t_mu;
+std::atomic<int> g_timing{0};   // bit k set: time launches of kind k
+std::vector<PendingTiming> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+int64_t g_t_launches[FBDT_K_COUNT];
+double g_t_ms[FBDT_K_COUNT];
+double g_t_bytes[FBDT_K_COUNT];
+
+hipEvent_t take_event() {
+    std::lock_guard<std::mutex> lk(g_t_mu);
+    if (!g_event_pool.empty()) {
+        hipEvent_t e = g_event_pool.back();
+        g_event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Brackets one kernel launch with events when timing is on.
+struct Timed {
+    int kind;
+    double bytes;
+    hipStream_t s;
+    hipEvent_t a = nullptr;
+    Timed(int k, hipStream_t st, double b = 0.0) : kind(k), bytes(b), s(st) {
+        if ((g_timing.load(std::memory_order_relaxed) >> k) & 1) {
+            a = take_event();
+            if (a && hipEventRecord(a, s) != hipSuccess) a = nullptr;
+        }
+    }
+    void done() {
+        if (!a) return;
+        hipEvent_t b = take_event();
+        if (!b || hipEventRecord(b, s) != hipSuccess) return;
+        std::lock_guard<std::mutex> lk(g_t_mu);
+        g_pending.push_back({kind, a, b, bytes});
+        a = nullptr;
+    }
+};
+
+// ---- per-device scratch ---------------------------------------------------
+struct Arena {
+    std::mutex mu;
+    void *ptr = nullptr;
+    size_t size = 0;
+};
+Arena g_arena[64];
+
+int arena_reserve(Arena &a, size_t bytes) {
+    if (bytes <= a.size) return FBDT_OK;
+    if (a.ptr) {
+        HIP_TRY(hipFree(a.ptr));
+        a.ptr = nullptr;
+        a.size = 0;
+    }
+    size_t want = bytes + bytes / 4 + (1 << 20);
+    HIP_TRY(hipMalloc(&a.ptr, want));
+    a.size = want;
+    return FBDT_OK;
+}
+
+// Carves 256-byte aligned sub-buffers out of one allocation.
+struct Carver {
+    size_t off = 0;
+    std::vector<std::pair<void **, size_t>> items;
+    template <typename T>
+    void add(T **p, size_t count) {
+        items.push_back({reinterpret_cast<void **>(p), count * sizeof(T)});
+        off += (count * sizeof(T) + 255) & ~(size_t)255;
+    }
+    void assign(void *base) {
+        size_t o = 0;
+        for (auto &it : items) {
+            *it.first = static_cast<char *>(base) + o;
+            o += (it.second + 255) & ~(size_t)255;
+        }
+    }
+};
+
+// ---- argument checks ------------------------------------------------------
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_codes(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb) {
+    if (!xb) return fail(FBDT_E_INVAL, "xb is NULL");
+    if (n < 1) return fail(FBDT_E_INVAL, "n = %lld must be >= 1", (long long)n);
+    if (n > (int64_t)1 << 40) return fail(FBDT_E_INVAL, "n = %lld too large", (long long)n);
+    if (d < 1 || d > 255) return fail(FBDT_E_INVAL, "d = %d must be in [1, 255]", d);
+    if (ldb < n || ldb % 16 != 0)
+        return fail(FBDT_E_INVAL, "ldb = %lld must be a multiple of 16 and >= n = %lld",
+                    (long long)ldb, (long long)n);
+    if (!aligned16(xb)) return fail(FBDT_E_INVAL, "xb must be 16-byte aligned");
+    return FBDT_OK;
+}
+
+int check_bins(int32_t n_bins) {
+    if (n_bins < 2 || n_bins > 256)
+        return fail(FBDT_E_INVAL, "n_bins = %d must be in [2, 256]", n_bins);
+    return FBDT_OK;
+}
+
+int current_device(int *dev, DeviceInfo *di) {
+    HIP_TRY(hipGetDevice(dev));
+    return device_info(*dev, di);
+}
+
+int read_err(int *err_dev, hipStream_t s, int *out) {
+    HIP_TRY(hipMemcpyAsync(out, err_dev, sizeof(int), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    return FBDT_OK;
+}
+
+double hist_algorithmic_bytes(int64_t n, int d, int n_bins, int layer, bool routed) {
+    double b = (double)n * d + 4.0 * n;                 // bin codes + weights
+    if (routed) {
+        if (layer >= 2) b += (double)n;                 // parent ids
+        if (layer >= 1) b += 2.0 * n;                   // routing code + ids written
+    } else {
+        b += (double)n;                                 // node ids
+    }
+    b += (double)(1 << layer) * d * n_bins * 2 * 8;     // the layer's histogram
+    return b;
+}
+
+}  // namespace
+
+// ===========================================================================
+extern "C" {
+
+const char *fbdt_last_error(void) { return g_error.c_str(); }
+
+int fbdt_set_option(const char *name, int64_t value) {
+    if (!name) return fail(FBDT_E_INVAL, "option name is NULL");
+    if (value < 0) return fail(FBDT_E_INVAL, "option %s: value must be >= 0", name);
+    if (!strcmp(name, "hist_features_per_group")) {
+        opt_hist_fpg = value;
+    } else if (!strcmp(name, "hist_event_chunks")) {
+        opt_hist_chunks = value;
+    } else if (!strcmp(name, "hist_threads")) {
+        if (value != 0 && (value % 64 != 0 || value > 1024))
+            return fail(FBDT_E_INVAL, "hist_threads must be a multiple of 64, <= 1024");
+        opt_hist_threads = value;
+    } else if (!strcmp(name, "apply_threads")) {
+        if (value != 0 && (value % 64 != 0 || value > 1024))
+            return fail(FBDT_E_INVAL, "apply_threads must be a multiple of 64, <= 1024");
+        opt_apply_threads = value;
+    } else {
+        return fail(FBDT_E_INVAL, "unknown option %s", name);
+    }
+    return FBDT_OK;
+}
+
+int fbdt_timing_enable(int32_t kinds) {
+    std::lock_guard<std::mutex> lk(g_t_mu);
+    for (auto &p : g_pending) {
+        (void)hipEventSynchronize(p.stop);
+        g_event_pool.push_back(p.start);
+        g_event_pool.push_back(p.stop);
+    }
+    g_pending.clear();
+    for (int k = 0; k < FBDT_K_COUNT; ++k) {
+        g_t_launches[k] = 0;
+        g_t_ms[k] = 0.0;
+        g_t_bytes[k] = 0.0;
+    }
+    g_timing = kinds & ((1 << FBDT_K_COUNT) - 1);
+    return FBDT_OK;
+}
+
+int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *bytes) {
+    if (kind < 0 || kind >= FBDT_K_COUNT) return fail(FBDT_E_INVAL, "kernel kind %d", kind);
+    std::lock_guard<std::mutex> lk(g_t_mu);
+    for (auto &p : g_pending) {
+        HIP_TRY(hipEventSynchronize(p.stop));
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, p.start, p.stop));
+        g_t_launches[p.kind] += 1;
+        g_t_ms[p.kind] += ms;
+        g_t_bytes[p.kind] += p.bytes;
+        g_event_pool.push_back(p.start);
+        g_event_pool.push_back(p.stop);
+    }
+    g_pending.clear();
+    if (launches) *launches = g_t_launches[kind];
+    if (total_ms) *total_ms = g_t_ms[kind];
+    if (bytes) *bytes = g_t_bytes[kind];
+    return FBDT_OK;
+}
+
+// ---- binning --------------------------------------------------------------
+static int encode_with(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
+                       const float *host_bounds, uint8_t *xb, int64_t ldb, hipStream_t s) {
+    int dev;
+    DeviceInfo di;
+    int rc = current_device(&dev, &di);
+    if (rc) return rc;
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    const size_t nb = (size_t)d * (n_bins - 1);
+    Carver cv;
+    float *bounds;
+    int *err;
+    cv.add(&bounds, std::max<size_t>(nb, 1));
+    cv.add(&err, 1);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+    HIP_TRY(hipMemcpyAsync(bounds, host_bounds, nb * sizeof(float), hipMemcpyHostToDevice, s));
+    HIP_TRY(launch_fill_u32(err, 0u, 1, s));
+    {
+        Timed t(FBDT_K_ENCODE, s, (double)n * d * 5.0);
+        HIP_TRY(launch_encode(x, ldx, n, d, bounds, n_bins, xb, ldb, err, s));
+        t.done();
+    }
+    int h_err = 0;
+    if ((rc = read_err(err, s, &h_err))) return rc;
+    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values");
+    return FBDT_OK;
+}
+
+static int check_float_input(const float *x, int64_t n, int32_t d, int64_t ldx) {
+    if (!x) return fail(FBDT_E_INVAL, "x is NULL");
+    if (ldx < n) return fail(FBDT_E_INVAL, "ldx = %lld < n", (long long)ldx);
+    (void)d;
+    return FBDT_OK;
+}
+
+int fbdt_bin(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
+             float *boundaries, uint8_t *xb, int64_t ldb, void *stream) {
+    int rc;
+    if ((rc = check_codes(xb, n, d, ldb)) || (rc = check_bins(n_bins)) ||
+        (rc = check_float_input(x, n, d, ldx)))
+        return rc;
+    if (!boundaries) return fail(FBDT_E_INVAL, "boundaries is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    std::vector<float> host((size_t)n * d);
+    HIP_TRY(hipMemcpy2DAsync(host.data(), (size_t)n * sizeof(float), x, (size_t)ldx * sizeof(float),
+                             (size_t)n * sizeof(float), (size_t)d, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    // Exact order statistics: boundary k of feature j is the value of rank
+    // floor(k n / B) of the feature (section 2.2).  Sorted on the host.
+    std::vector<float> bounds((size_t)d * (n_bins - 1));
+    std::atomic<int> nan_seen{0};
+    unsigned hw = std::thread::hardware_concurrency();
+    int nthreads = (int)std::min<unsigned>(std::max(1u, hw), 16u);
+    nthreads = std::min(nthreads, (int)d);
+    auto work = [&](int tid) {
+        std::vector<float> col;
+        for (int j = tid; j < d; j += nthreads) {
+            const float *src = host.data() + (size_t)j * n;
+            col.assign(src, src + n);
+            for (float v : col)
+                if (v != v) {
+                    nan_seen = 1;
+                    return;
+                }
+            std::sort(col.begin(), col.end());
+            for (int k = 1; k < n_bins; ++k)
+                bounds[(size_t)j * (n_bins - 1) + (k - 1)] =
+                    col[(size_t)(((int64_t)k * n) / n_bins)];
+        }
+    };
+    std::vector<std::thread> pool;
+    for (int t = 1; t < nthreads; ++t) pool.emplace_back(work, t);
+    work(0);
+    for (auto &th : pool) th.join();
+    if (nan_seen) return fail(FBDT_E_NAN, "NaN among the feature values");
+    if ((rc = encode_with(x, n, d, ldx, n_bins, bounds.data(), xb, ldb, s))) return rc;
+    std::memcpy(boundaries, bounds.data(), bounds.size() * sizeof(float));
+    return FBDT_OK;
+}
+
+int fbdt_bin_transform(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
+                       const float *boundaries, uint8_t *xb, int64_t ldb, void *stream) {
+    int rc;
+    if ((rc = check_codes(xb, n, d, ldb)) || (rc = check_bins(n_bins)) ||
+        (rc = check_float_input(x, n, d, ldx)))
+        return rc;
+    if (!boundaries) return fail(FBDT_E_INVAL, "boundaries is NULL");
+    for (int j = 0; j < d; ++j)
+        for (int k = 1; k < n_bins - 1; ++k)
+            if (!(boundaries[(size_t)j * (n_bins - 1) + k - 1] <=
+                  boundaries[(size_t)j * (n_bins - 1) + k]))
+                return fail(FBDT_E_INVAL, "boundaries of feature %d are not ascending", j);
+    return encode_with(x, n, d, ldx, n_bins, boundaries, xb, ldb, static_cast<hipStream_t>(stream));
+}
+
+// ---- fit ------------------------------------------------------------------
+int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bins,
+             const int8_t *y, const float *w, const fbdt_fit_params *p, fbdt_model **out,
+             double *score_out, void *stream) {
+    int rc;
+    if ((rc = check_codes(xb, n, d, ldb)) || (rc = check_bins(n_bins))) return rc;
+    if (!y) return fail(FBDT_E_INVAL, "y is NULL");
+    if (!p) return fail(FBDT_E_INVAL, "params is NULL");
+    if (!out) return fail(FBDT_E_INVAL, "out is NULL");
+    if (p->depth < 1 || p->depth > 7) return fail(FBDT_E_INVAL, "depth %d not in [1, 7]", p->depth);
+    if (p->n_trees < 1) return fail(FBDT_E_INVAL, "n_trees %d < 1", p->n_trees);
+    if (!(p->shrinkage > 0.0) || !std::isfinite(p->shrinkage))
+        return fail(FBDT_E_INVAL, "shrinkage must be finite and > 0");
+    if (!(p->subsample > 0.0 && p->subsample <= 1.0))
+        return fail(FBDT_E_INVAL, "subsample must be in (0, 1]");
+
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int D = p->depth, T = p->n_trees;
+    const int nin = (1 << D) - 1, nleaf = 1 << D;
+    const int64_t npad = (n + 15) & ~(int64_t)15;
+
+    std::vector<HistShape> plans(D);
+    size_t partial_elems = 0;
+    for (int l = 0; l < D; ++l) {
+        plans[l] = plan_histogram(n, d, n_bins, l, di.cu_count, di.max_lds, (int)opt_hist_fpg.load(),
+                                  (int)opt_hist_chunks.load(), (int)opt_hist_threads.load());
+        partial_elems = std::max(partial_elems,
+                                 (size_t)plans[l].chunks * ((size_t)1 << l) * d * n_bins * 2);
+    }
+    const int lblocks = leaf_blocks(n, di.cu_count);
+    const int max_nodes = 1 << (D - 1);
+
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    FitBuffers fb{};
+    Carver cv;
+    cv.add(&fb.F, npad);
+    cv.add(&fb.w, npad);
+    cv.add(&fb.node[0], npad);
+    cv.add(&fb.node[1], npad);
+    cv.add(&fb.partial, partial_elems);
+    cv.add(&fb.cand_gain, (size_t)max_nodes * d);
+    cv.add(&fb.cand_cut, (size_t)max_nodes * d);
+    cv.add(&fb.node_ticket, max_nodes);
+    cv.add(&fb.leaf_partial, (size_t)lblocks * 2 * nleaf);
+    cv.add(&fb.leaf_ticket, 1);
+    cv.add(&fb.class_partial, 2 * kValidateBlocks);
+    cv.add(&fb.f0, 1);
+    cv.add(&fb.err, 1);
+    cv.add(&fb.cut_feature, (size_t)T * nin);
+    cv.add(&fb.cut_bin, (size_t)T * nin);
+    cv.add(&fb.gain, (size_t)T * nin);
+    cv.add(&fb.leaf, (size_t)T * nleaf);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+
+    HIP_TRY(launch_fill_u32(fb.node_ticket, 0u, max_nodes, s));
+    HIP_TRY(launch_fill_u32(fb.leaf_ticket, 0u, 1, s));
+    HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
+    HIP_TRY(launch_validate(y, w, n, fb.class_partial, fb.err, s));
+    HIP_TRY(launch_initial_score(fb.class_partial, fb.f0, fb.err, s));
+    int h_err = 0;
+    if ((rc = read_err(fb.err, s, &h_err))) return rc;
+    if (h_err & kErrLabel) return fail(FBDT_E_LABEL, "labels must be +1 or -1");
+    if (h_err & kErrWeight) return fail(FBDT_E_WEIGHT, "weights must be finite and >= 0");
+    if (h_err & kErrClass) return fail(FBDT_E_LABEL, "a class has zero total weight");
+
+    const uint64_t seed = p->seed;
+    const double alpha = p->subsample, eta = p->shrinkage;
+    for (int t = 0; t < T; ++t) {
+        {
+            Timed tm(FBDT_K_TREE_PREP, s, (double)n * 30.0);
+            HIP_TRY(launch_tree_prep(y, w, fb.F, t == 0 ? fb.f0 : nullptr,
+                                     t == 0 ? nullptr : fb.node[D & 1],
+                                     t == 0 ? nullptr : fb.leaf + (size_t)(t - 1) * nleaf, D, n,
+                                     seed, t, alpha, fb.w, nullptr, s));
+            tm.done();
+        }
+        uint8_t *cf = fb.cut_feature + (size_t)t * nin;
+        uint8_t *cc = fb.cut_bin + (size_t)t * nin;
+        double *cg = fb.gain + (size_t)t * nin;
+        for (int l = 0; l < D; ++l) {
+            const int lo = (1 << l) - 1;            // index of the layer's first node
+            const int plo = l >= 1 ? (1 << (l - 1)) - 1 : 0;
+            {
+                Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, l, true));
+                HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
+                                         l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
+                                         l >= 1 ? fb.node[l & 1] : nullptr, fb.w, cf + plo,
+                                         cc + plo, l, true, fb.partial, fb.err, s));
+                tm.done();
+            }
+            {
+                Timed tm(FBDT_K_BEST_CUTS, s);
+                HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, 1 << l, d, n_bins,
+                                         fb.cand_gain, fb.cand_cut, fb.node_ticket, cf + lo,
+                                         cc + lo, cg + lo, s));
+                tm.done();
+            }
+        }
+        {
+            const int plo = (1 << (D - 1)) - 1;
+            Timed tm(FBDT_K_LEAF, s);
+            HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
+                                fb.node[D & 1], cf + plo, cc + plo, D, true, y, w, fb.F, seed, t,
+                                alpha, eta, lblocks, fb.leaf_partial, fb.leaf_ticket,
+                                fb.leaf + (size_t)t * nleaf, fb.err, s));
+            tm.done();
+        }
+    }
+    if (score_out)
+        HIP_TRY(launch_tree_prep(y, w, fb.F, nullptr, fb.node[D & 1],
+                                 fb.leaf + (size_t)(T - 1) * nleaf, D, n, seed, T, alpha, nullptr,
+                                 score_out, s));
+
+    fbdt_model *m = new (std::nothrow) fbdt_model;
+    if (!m) return fail(FBDT_E_DEVICE, "out of host memory");
+    m->n_trees = T;
+    m->depth = D;
+    m->n_features = d;
+    m->n_bins = n_bins;
+    m->cut_feature.resize((size_t)T * nin);
+    m->cut_bin.resize((size_t)T * nin);
+    m->gain.resize((size_t)T * nin);
+    m->leaf.resize((size_t)T * nleaf);
+    auto cleanup = [&](int code) {
+        delete m;
+        return code;
+    };
+    if (hipMemcpyAsync(m->cut_feature.data(), fb.cut_feature, (size_t)T * nin,
+                       hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(m->cut_bin.data(), fb.cut_bin, (size_t)T * nin, hipMemcpyDeviceToHost,
+                       s) != hipSuccess ||
+        hipMemcpyAsync(m->gain.data(), fb.gain, (size_t)T * nin * sizeof(double),
+                       hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(m->leaf.data(), fb.leaf, (size_t)T * nleaf * sizeof(double),
+                       hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(&m->f0, fb.f0, sizeof(double), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(&h_err, fb.err, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess) {
+        return cleanup(fail(FBDT_E_DEVICE, "copying the model to the host failed: %s",
+                            hipGetErrorString(hipGetLastError())));
+    }
+    hipError_t se = hipStreamSynchronize(s);
+    if (se != hipSuccess)
+        return cleanup(fail(FBDT_E_DEVICE, "fit failed: %s", hipGetErrorString(se)));
+    if (h_err & kErrBin) return cleanup(fail(FBDT_E_INVAL, "a bin code is >= n_bins"));
+    if (h_err & kErrRoute) return cleanup(fail(FBDT_E_DEVICE, "internal routing error"));
+    *out = m;
+    return FBDT_OK;
+}
+
+// ---- model ----------------------------------------------------------------
+int fbdt_model_export(const fbdt_model *m, fbdt_model_view *v) {
+    if (!m || !v) return fail(FBDT_E_INVAL, "NULL argument");
+    v->n_trees = m->n_trees;
+    v->depth = m->depth;
+    v->n_features = m->n_features;
+    v->n_bins = m->n_bins;
+    v->f0 = m->f0;
+    v->cut_feature = m->cut_feature.data();
+    v->cut_bin = m->cut_bin.data();
+    v->gain = m->gain.data();
+    v->leaf = m->leaf.data();
+    v->boundaries = m->boundaries.empty() ? nullptr : m->boundaries.data();
+    return FBDT_OK;
+}
+
+int fbdt_model_import(const fbdt_model_view *v, fbdt_model **out) {
+    if (!v || !out) return fail(FBDT_E_INVAL, "NULL argument");
+    if (v->n_trees < 1 || v->depth < 1 || v->depth > 7 || v->n_features < 1 ||
+        v->n_features > 255 || v->n_bins < 2 || v->n_bins > 256)
+        return fail(FBDT_E_INVAL, "model dimensions out of range");
+    if (!v->cut_feature || !v->cut_bin || !v->leaf)
+        return fail(FBDT_E_INVAL, "cut_feature, cut_bin and leaf are required");
+    if (!std::isfinite(v->f0)) return fail(FBDT_E_INVAL, "f0 is not finite");
+    const size_t T = v->n_trees, nin = ((size_t)1 << v->depth) - 1, nleaf = (size_t)1 << v->depth;
+    for (size_t k = 0; k < T * nin; ++k) {
+        if (v->cut_feature[k] >= v->n_features)
+            return fail(FBDT_E_INVAL, "cut feature %d >= n_features", (int)v->cut_feature[k]);
+        if (v->cut_bin[k] < 1 || v->cut_bin[k] >= v->n_bins)
+            return fail(FBDT_E_INVAL, "cut bin %d not in [1, n_bins)", (int)v->cut_bin[k]);
+    }
+    fbdt_model *m = new (std::nothrow) fbdt_model;
+    if (!m) return fail(FBDT_E_DEVICE, "out of host memory");
+    m->n_trees = v->n_trees;
+    m->depth = v->depth;
+    m->n_features = v->n_features;
+    m->n_bins = v->n_bins;
+    m->f0 = v->f0;
+    m->cut_feature.assign(v->cut_feature, v->cut_feature + T * nin);
+    m->cut_bin.assign(v->cut_bin, v->cut_bin + T * nin);
+    if (v->gain)
+        m->gain.assign(v->gain, v->gain + T * nin);
+    else
+        m->gain.assign(T * nin, 0.0);
+    m->leaf.assign(v->leaf, v->leaf + T * nleaf);
+    if (v->boundaries)
+        m->boundaries.assign(v->boundaries,
+                             v->boundaries + (size_t)v->n_features * (v->n_bins - 1));
+    *out = m;
+    return FBDT_OK;
+}
+
+void fbdt_model_free(fbdt_model *m) {
+    if (!m) return;
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    for (auto &c : m->copies) {
+        if (hipSetDevice(c.device) == hipSuccess) {
+            (void)hipFree(c.cuts);
+            (void)hipFree(c.leaves);
+        }
+    }
+    if (cur >= 0) (void)hipSetDevice(cur);
+    delete m;
+}
+
+// ---- apply ----------------------------------------------------------------
+int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
+               float *prob, double *score, void *stream) {
+    int rc;
+    if (!mc) return fail(FBDT_E_INVAL, "model is NULL");
+    if ((rc = check_codes(xb, n, d, ldb))) return rc;
+    if (!prob) return fail(FBDT_E_INVAL, "prob is NULL");
+    fbdt_model *m = const_cast<fbdt_model *>(mc);
+    if (d < m->n_features)
+        return fail(FBDT_E_SHAPE, "d = %d < the model's %d features", d, m->n_features);
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = m->n_trees, D = m->depth;
+    const size_t nin = ((size_t)1 << D) - 1, nleaf = (size_t)1 << D;
+    uint16_t *cuts = nullptr;
+    double *leaves = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(m->mu);
+        for (auto &c : m->copies)
+            if (c.device == dev) {
+                cuts = c.cuts;
+                leaves = c.leaves;
+            }
+        if (!cuts) {
+            std::vector<uint16_t> packed((size_t)T * nin);
+            for (size_t k = 0; k < packed.size(); ++k)
+                packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
+            HIP_TRY(hipMalloc(&cuts, packed.size() * sizeof(uint16_t)));
+            if (hipMalloc(&leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
+                (void)hipFree(cuts);
+                return fail(FBDT_E_DEVICE, "out of device memory");
+            }
+            HIP_TRY(hipMemcpy(cuts, packed.data(), packed.size() * sizeof(uint16_t),
+                              hipMemcpyHostToDevice));
+            HIP_TRY(hipMemcpy(leaves, m->leaf.data(), (size_t)T * nleaf * sizeof(double),
+                              hipMemcpyHostToDevice));
+            m->copies.push_back({dev, cuts, leaves});
+        }
+    }
+    ApplyShape as = plan_apply(n, m->n_features, T, D, di.cu_count, di.max_lds,
+                               (int)opt_apply_threads.load());
+    Timed tm(FBDT_K_APPLY, s, (double)n * (m->n_features + 4));
+    HIP_TRY(launch_apply(as, xb, ldb, n, cuts, leaves, T, D, m->f0, prob, score, s));
+    tm.done();
+    return FBDT_OK;
+}
+
+// ---- single steps -----------------------------------------------------------
+int fbdt_tree_weights(const int8_t *y, const float *v, const double *F, int64_t n, uint64_t seed,
+                      int32_t tree, double alpha, float *w_out, void *stream) {
+    if (!y || !F || !w_out) return fail(FBDT_E_INVAL, "NULL argument");
+    if (n < 1) return fail(FBDT_E_INVAL, "n must be >= 1");
+    if (tree < 0) return fail(FBDT_E_INVAL, "tree must be >= 0");
+    if (!(alpha > 0.0 && alpha <= 1.0)) return fail(FBDT_E_INVAL, "alpha must be in (0, 1]");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    Timed tm(FBDT_K_TREE_PREP, s, (double)n * 17.0);
+    HIP_TRY(launch_tree_prep(y, v, const_cast<double *>(F), nullptr, nullptr, nullptr, 1, n, seed,
+                             tree, alpha, w_out, nullptr, s));
+    tm.done();
+    return FBDT_OK;
+}
+
+int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bins,
+                   const uint8_t *node, const float *w, int32_t layer, double *hist,
+                   void *stream) {
+    int rc;
+    if ((rc = check_codes(xb, n, d, ldb)) || (rc = check_bins(n_bins))) return rc;
+    if (!node || !w || !hist) return fail(FBDT_E_INVAL, "NULL argument");
+    if (!aligned16(node) || !aligned16(w))
+        return fail(FBDT_E_INVAL, "node and w must be 16-byte aligned");
+    if (layer < 0 || layer > 6) return fail(FBDT_E_INVAL, "layer %d not in [0, 6]", layer);
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HistShape hs = plan_histogram(n, d, n_bins, layer, di.cu_count, di.max_lds,
+                                  (int)opt_hist_fpg.load(), (int)opt_hist_chunks.load(),
+                                  (int)opt_hist_threads.load());
+    const size_t count = ((size_t)1 << layer) * d * n_bins * 2;
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    Carver cv;
+    double *partial;
+    int *err;
+    cv.add(&partial, (size_t)hs.chunks * count);
+    cv.add(&err, 1);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+    HIP_TRY(launch_fill_u32(err, 0u, 1, s));
+    {
+        Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, layer, false));
+        HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node, nullptr, w, nullptr, nullptr,
+                                 layer, false, partial, err, s));
+        tm.done();
+    }
+    HIP_TRY(launch_merge_partials(partial, hs.chunks, count, hist, s));
+    int h_err = 0;
+    if ((rc = read_err(err, s, &h_err))) return rc;
+    if (h_err & kErrBin) return fail(FBDT_E_INVAL, "a bin code is >= n_bins");
+    return FBDT_OK;
+}
+
+int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bins,
+                   uint8_t *cut_feature, uint8_t *cut_bin, double *gain, void *stream) {
+    int rc;
+    if (!hist || !cut_feature || !cut_bin || !gain) return fail(FBDT_E_INVAL, "NULL argument");
+    if (n_nodes < 1 || n_nodes > 64) return fail(FBDT_E_INVAL, "n_nodes not in [1, 64]");
+    if (d < 1 || d > 255) return fail(FBDT_E_INVAL, "d not in [1, 255]");
+    if ((rc = check_bins(n_bins))) return rc;
+    if ((reinterpret_cast<uintptr_t>(hist) & 15u) != 0)
+        return fail(FBDT_E_INVAL, "hist must be 16-byte aligned");
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    Carver cv;
+    double *cg;
+    int *cc;
+    unsigned *tk;
+    cv.add(&cg, (size_t)n_nodes * d);
+    cv.add(&cc, (size_t)n_nodes * d);
+    cv.add(&tk, n_nodes);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+    HIP_TRY(launch_fill_u32(tk, 0u, n_nodes, s));
+    Timed tm(FBDT_K_BEST_CUTS, s);
+    HIP_TRY(launch_best_cuts(hist, 1, n_nodes, d, n_bins, cg, cc, tk, cut_feature, cut_bin, gain,
+                             s));
+    tm.done();
+    HIP_TRY(hipStreamSynchronize(s));
+    return FBDT_OK;
+}
+
+int fbdt_route(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, uint8_t *node,
+               const uint8_t *cut_feature, const uint8_t *cut_bin, int32_t layer, void *stream) {
+    int rc;
+    if ((rc = check_codes(xb, n, d, ldb))) return rc;
+    if (!node || !cut_feature || !cut_bin) return fail(FBDT_E_INVAL, "NULL argument");
+    if (layer < 0 || layer > 6) return fail(FBDT_E_INVAL, "layer %d not in [0, 6]", layer);
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    Carver cv;
+    int *err;
+    cv.add(&err, 1);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+    HIP_TRY(launch_fill_u32(err, 0u, 1, s));
+    HIP_TRY(launch_route(xb, ldb, n, d, node, cut_feature, cut_bin, layer, err, s));
+    int h_err = 0;
+    if ((rc = read_err(err, s, &h_err))) return rc;
+    if (h_err & kErrRoute)
+        return fail(FBDT_E_INVAL, "a node id or cut feature is out of range (events skipped)");
+    return FBDT_OK;
+}
+
+int fbdt_leaf_values(const uint8_t *node, const int8_t *y, const float *v, const double *F,
+                     int64_t n, int32_t depth, uint64_t seed, int32_t tree, double alpha,
+                     double eta, double *leaf, void *stream) {
+    int rc;
+    if (!node || !y || !F || !leaf) return fail(FBDT_E_INVAL, "NULL argument");
+    if (n < 1) return fail(FBDT_E_INVAL, "n must be >= 1");
+    if (depth < 1 || depth > 7) return fail(FBDT_E_INVAL, "depth not in [1, 7]");
+    if (!(alpha > 0.0 && alpha <= 1.0)) return fail(FBDT_E_INVAL, "alpha must be in (0, 1]");
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int blocks = leaf_blocks(n, di.cu_count);
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    Carver cv;
+    double *lp;
+    unsigned *tk;
+    int *err;
+    cv.add(&lp, (size_t)blocks * 2 * (1 << depth));
+    cv.add(&tk, 1);
+    cv.add(&err, 1);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+    HIP_TRY(launch_fill_u32(tk, 0u, 1, s));
+    HIP_TRY(launch_fill_u32(err, 0u, 1, s));
+    HIP_TRY(launch_leaf(nullptr, 0, n, 1, node, nullptr, nullptr, nullptr, depth, false, y, v, F,
+                        seed, tree, alpha, eta, blocks, lp, tk, leaf, err, s));
+    int h_err = 0;
+    if ((rc = read_err(err, s, &h_err))) return rc;
+    if (h_err & kErrRoute) return fail(FBDT_E_INVAL, "a node id is not a leaf id (skipped)");
+    return FBDT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,125 @@
+// Internal launch interface between the C ABI (capi.hip) and the kernels
+// (kernels.hip).  Nothing here is exported from libfbdt.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace fbdt {
+
+// Bits of the device-side error word that kernels raise.
+enum : int {
+    kErrLabel = 1,     // label not in {+1, -1}
+    kErrWeight = 2,    // weight < 0 or not finite
+    kErrNan = 4,       // NaN feature value
+    kErrBin = 8,       // bin code >= n_bins met by a histogram pass
+    kErrRoute = 16,    // cut or node id out of range met while routing
+    kErrClass = 32,    // a class has zero total weight
+};
+
+// Launch shape of one histogram pass.
+struct HistShape {
+    int features_per_group;   // features whose histograms one workgroup keeps in LDS
+    int feature_groups;       // ceil(d / features_per_group)
+    int nodes_per_group;      // nodes whose histograms one workgroup keeps in LDS
+    int node_groups;          // ceil(2^layer / nodes_per_group)
+    int chunks;               // event chunks, each merged once per layer
+    int64_t chunk_events;     // events per chunk (a multiple of 4)
+    int threads;              // threads per workgroup
+    int blocks;               // grid size (chunks * groups, rounded up to the XCD count)
+    size_t lds_bytes;         // dynamic LDS per workgroup
+};
+
+// Device-side scratch of one fit.
+struct FitBuffers {
+    double *F;            // [npad] score
+    float *w;             // [npad] signed re-weighted sample
+    uint8_t *node[2];     // [npad] node ids, double-buffered across layers
+    double *partial;      // histogram partials [chunks][nodes][d][B][2]
+    double *cand_gain;    // [max nodes][d]
+    int *cand_cut;        // [max nodes][d]
+    unsigned *node_ticket;  // [max nodes]
+    double *leaf_partial;   // [leaf blocks][2^D][2]
+    unsigned *leaf_ticket;  // [1]
+    double *class_partial;  // [validate blocks][2]
+    double *f0;             // [1]
+    int *err;               // [1]
+    uint8_t *cut_feature;   // [T][2^D - 1]
+    uint8_t *cut_bin;       // [T][2^D - 1]
+    double *gain;           // [T][2^D - 1]
+    double *leaf;           // [T][2^D]
+};
+
+constexpr int kXcds = 8;            // gfx950: 8 XCDs, workgroups dispatched round-robin
+constexpr int kValidateBlocks = 256;
+
+hipError_t launch_fill_u32(void *p, uint32_t value, size_t count, hipStream_t s);
+
+hipError_t launch_validate(const int8_t *y, const float *v, int64_t n, double *class_partial,
+                           int *err, hipStream_t s);
+hipError_t launch_initial_score(const double *class_partial, double *f0, int *err,
+                                hipStream_t s);
+
+// Score update of the previous tree (if any) and re-weighting of tree `tree`.
+//  update_from_leaf: F += leaf_prev[leaf_node - 2^depth]; else if f0 != null: F = *f0.
+//  w may be null (score update only); score_out (optional) receives F.
+hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const double *f0,
+                            const uint8_t *leaf_node, const double *leaf_prev, int depth,
+                            int64_t n, uint64_t seed, int tree, double alpha, float *w,
+                            double *score_out, hipStream_t s);
+
+// fpg, chunks, threads: launch-shape overrides (0 = default).
+HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
+                         size_t max_lds, int fpg, int chunks, int threads);
+
+// Histogram pass.  routed = true: node_in holds the ids of layer-1 (null for
+// layer <= 1, all events at the root), the pass routes them with the cuts of
+// layer-1 and (first feature group only) writes the layer's ids to node_out.
+// routed = false: node_in holds the ids of the layer itself.
+hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
+                            int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
+                            const float *w, const uint8_t *cut_f, const uint8_t *cut_c,
+                            int layer, bool routed, double *partial, int *err, hipStream_t s);
+
+// hist[i] = sum over chunks of partial[chunk][i], in chunk order.
+hipError_t launch_merge_partials(const double *partial, int chunks, size_t count, double *out,
+                                 hipStream_t s);
+
+hipError_t launch_best_cuts(const double *partial, int chunks, int n_nodes, int d, int n_bins,
+                            double *cand_gain, int *cand_cut, unsigned *ticket,
+                            uint8_t *out_f, uint8_t *out_c, double *out_g, hipStream_t s);
+
+// Last routing (routed = true, from layer depth-1 to the leaves) or none
+// (node_in already holds leaf ids), then terminal boost weights.
+int leaf_blocks(int64_t n, int cu_count);
+hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
+                       uint8_t *node_out, const uint8_t *cut_f, const uint8_t *cut_c, int depth,
+                       bool routed, const int8_t *y, const float *v, const double *F,
+                       uint64_t seed, int tree, double alpha, double eta, int blocks,
+                       double *leaf_partial, unsigned *ticket, double *leaf_out, int *err,
+                       hipStream_t s);
+
+hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *node,
+                        const uint8_t *cut_f, const uint8_t *cut_c, int layer, int *err,
+                        hipStream_t s);
+
+// Forest traversal.  cuts: [T][2^D-1] packed (feature | bin << 8).
+struct ApplyShape {
+    int threads;
+    int blocks;
+    int trees_per_chunk;
+    int d_used;
+    size_t lds_bytes;
+};
+ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_count,
+                      size_t max_lds, int threads);
+hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
+                        const uint16_t *cuts, const double *leaves, int n_trees, int depth,
+                        double f0, float *prob, double *score, hipStream_t s);
+
+hipError_t launch_encode(const float *x, int64_t ldx, int64_t n, int d, const float *bounds,
+                         int n_bins, uint8_t *xb, int64_t ldb, int *err, hipStream_t s);
+
+}  // namespace fbdt

@@ -1,0 +1,900 @@
+// HIP kernels of libfbdt for gfx950 (CDNA4, wave64).
+//
+// The fit and apply path of FastBDT (Keck, arXiv:1609.06119):
+//   tree_prep      score update + gradient re-weighting + sub-sample (sections 1.3, 1.4)
+//   hist           one pass over the sample builds the signal/background
+//                  histograms of all nodes and features of a layer (sections 1.1, 2.1),
+//                  routing every event from the previous layer on the way (Fig. 1)
+//   best_cuts      cumulative histograms, separation gain, best cut (section 1.1)
+//   leaf           last routing + Newton-step terminal boost weights (section 1.3)
+//   apply          forest traversal and sigmoid of the summed boost weights (section 1.3)
+//   encode         equal-frequency bin codes from boundaries (section 2.2)
+//
+// Data layout in HBM: binned features are feature-major uint8 rows (row
+// stride ldb, a multiple of 16), so a wavefront reads 64 consecutive events
+// of one feature as one 256-byte run; per-event state (node id uint8, signed
+// float32 weight, float64 score) lives in separate arrays.
+#include "fbdt_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+namespace fbdt {
+namespace {
+
+constexpr int kWave = 64;
+
+// SplitMix64 (Steele, Lea & Flood, OOPSLA 2014): output number k (0-based)
+// of the generator seeded with `seed` mixes the state seed + (k + 1) * gamma.
+__device__ __forceinline__ uint64_t splitmix64_at(uint64_t seed, uint64_t k) {
+    uint64_t z = seed + (k + 1ull) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Event i of tree t is in the sub-sample iff the top 53 bits of output
+// t * n + i, over 2^53, are below alpha (section 1.4).
+__device__ __forceinline__ bool in_subsample(uint64_t seed, int tree, int64_t n, int64_t i,
+                                             double alpha) {
+    const uint64_t k = (uint64_t)tree * (uint64_t)n + (uint64_t)i;
+    const double u = (double)(splitmix64_at(seed, k) >> 11) * 0x1.0p-53;
+    return u < alpha;
+}
+
+// Pseudo-response of the binomial deviance with F half the log-odds
+// (section 1.3, Friedman's two-class LK_TreeBoost): 2y / (1 + exp(2yF)).
+__device__ __forceinline__ double pseudo_response(double yf, double F) {
+    return 2.0 * yf / (1.0 + exp(2.0 * yf * F));
+}
+
+// Weighted Gini impurity G(s, b) = s b / (s + b), zero for an empty side.
+__device__ __forceinline__ double gini(double s, double b) {
+    const double t = s + b;
+    return t == 0.0 ? 0.0 : (s * b) / t;
+}
+
+template <typename T>
+__device__ __forceinline__ T load_agent(const T *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+__global__ void fill_u32_kernel(uint32_t *p, uint32_t value, size_t count) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < count;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = value;
+}
+
+// ---------------------------------------------------------------------------
+// Label/weight checks and per-class weight sums (deterministic order:
+// fixed grid, grid-stride per thread, fixed reduction tree).
+__global__ __launch_bounds__(256) void validate_kernel(const int8_t *__restrict__ y,
+                                                       const float *__restrict__ v, int64_t n,
+                                                       double *__restrict__ class_partial,
+                                                       int *__restrict__ err) {
+    double s = 0.0, b = 0.0;
+    int e = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int yi = y[i];
+        const float vi = v ? v[i] : 1.0f;
+        if (yi != 1 && yi != -1) e |= kErrLabel;
+        if (!(vi >= 0.0f) || isinf(vi)) e |= kErrWeight;
+        if (yi > 0)
+            s += (double)vi;
+        else if (yi < 0)
+            b += (double)vi;
+    }
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        s += __shfl_down(s, off);
+        b += __shfl_down(b, off);
+    }
+    __shared__ double ws[256 / kWave][2];
+    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+    if (lane == 0) {
+        ws[wid][0] = s;
+        ws[wid][1] = b;
+    }
+    if (e) atomicOr(err, e);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double ts = 0.0, tb = 0.0;
+        for (int k = 0; k < (int)(blockDim.x / kWave); ++k) {
+            ts += ws[k][0];
+            tb += ws[k][1];
+        }
+        class_partial[2 * blockIdx.x] = ts;
+        class_partial[2 * blockIdx.x + 1] = tb;
+    }
+}
+
+// F0 = 1/2 ln(sum of signal weight / sum of background weight).
+__global__ __launch_bounds__(256) void initial_score_kernel(const double *__restrict__ cp,
+                                                            int nblocks, double *__restrict__ f0,
+                                                            int *__restrict__ err) {
+    __shared__ double sh[256][2];
+    double s = 0.0, b = 0.0;
+    for (int k = threadIdx.x; k < nblocks; k += blockDim.x) {
+        s += cp[2 * k];
+        b += cp[2 * k + 1];
+    }
+    sh[threadIdx.x][0] = s;
+    sh[threadIdx.x][1] = b;
+    __syncthreads();
+    for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            sh[threadIdx.x][0] += sh[threadIdx.x + off][0];
+            sh[threadIdx.x][1] += sh[threadIdx.x + off][1];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const double ts = sh[0][0], tb = sh[0][1];
+        if (!(ts > 0.0 && tb > 0.0))
+            atomicOr(err, kErrClass);
+        else
+            *f0 = 0.5 * log(ts / tb);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// One elementwise pass per tree: add the previous tree's boost weight to F
+// (or set F = F0 for the first tree), then the histogram weight of every
+// event: fl32(v |y~|) if sampled else 0, class in the sign bit.
+__global__ __launch_bounds__(256) void tree_prep_kernel(
+    const int8_t *__restrict__ y, const float *__restrict__ v, double *__restrict__ F,
+    const double *__restrict__ f0, const uint8_t *__restrict__ leaf_node,
+    const double *__restrict__ leaf_prev, int depth, int64_t n, uint64_t seed, int tree,
+    double alpha, float *__restrict__ w, double *__restrict__ score_out) {
+    const unsigned nleaf = 1u << depth;
+    const double f0v = (f0 && !leaf_prev) ? *f0 : 0.0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        double Fi;
+        if (leaf_prev) {
+            unsigned li = (unsigned)leaf_node[i] - nleaf;
+            if (li >= nleaf) li = 0;  // unreachable: leaf ids come from the leaf pass
+            Fi = F[i] + leaf_prev[li];
+            F[i] = Fi;
+        } else if (f0) {
+            Fi = f0v;
+            F[i] = Fi;
+        } else {
+            Fi = F[i];
+        }
+        if (score_out) score_out[i] = Fi;
+        if (w) {
+            const double yf = (double)y[i];
+            const double yt = pseudo_response(yf, Fi);
+            const double vi = v ? (double)v[i] : 1.0;
+            const float wi = in_subsample(seed, tree, n, i, alpha) ? (float)(vi * fabs(yt)) : 0.0f;
+            w[i] = yf > 0.0 ? wi : -wi;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Layer histogram.  Workgroup (chunk p, feature group g, node group h) keeps
+// H[node in h][feature in g][bin][class] in LDS as float64, adds every
+// sampled event of its event chunk with ds_add_f64, and writes its partial
+// histogram once at the end; best_cuts sums the chunk partials in a fixed
+// order.  Each thread handles 4 consecutive events per step: one float4 of
+// weights, one dword of node ids and one dword of bin codes per feature.
+// Routed mode computes each event's node of this layer from its parent
+// (layer - 1) and the parent's cut on the way; the first feature group
+// stores the new ids.
+template <bool ROUTED>
+__global__ __launch_bounds__(1024) void hist_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
+    const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
+    const float *__restrict__ w, const uint8_t *__restrict__ cut_f,
+    const uint8_t *__restrict__ cut_c, int layer, int fpg, int G, int npg, int NG, int chunks,
+    int64_t chunk_events, double *__restrict__ partial, int *__restrict__ err) {
+    extern __shared__ double lds[];
+    __shared__ uint8_t s_cf[64], s_cc[64];
+
+    // Consecutive work items (same event chunk, different feature groups) go
+    // to the same XCD so that the chunk's node ids and weights are fetched
+    // into that XCD's L2 once and re-read from there.
+    const int per_xcd = gridDim.x / kXcds;
+    const int q = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    const int groups = G * NG;
+    if (q >= chunks * groups) return;
+    const int p = q / groups;
+    const int r = q - p * groups;
+    const int h = r / G;
+    const int g = r - h * G;
+
+    const int nodes = 1 << layer;
+    const int half = nodes >> 1;
+    const int j0 = g * fpg;
+    const int nf = min(fpg, d - j0);
+    const int k0 = h * npg;
+    const int nk = min(npg, nodes - k0);
+    const int lds_n = npg * fpg * nbins * 2;
+
+    for (int t = threadIdx.x; t < lds_n; t += blockDim.x) lds[t] = 0.0;
+    if (ROUTED && layer >= 1)
+        for (int t = threadIdx.x; t < half; t += blockDim.x) {
+            s_cf[t] = cut_f[t];
+            s_cc[t] = cut_c[t];
+        }
+    __syncthreads();
+
+    const int64_t start = (int64_t)p * chunk_events;
+    const int64_t end = min(n, start + chunk_events);
+    const bool writer = ROUTED && layer >= 1 && g == 0 && h == 0 && node_out != nullptr;
+    int eflag = 0;
+
+    for (int64_t i0 = start + 4 * (int64_t)threadIdx.x; i0 < end; i0 += 4 * (int64_t)blockDim.x) {
+        const bool full = i0 + 4 <= n;
+        float wv[4];
+        int nd[4];
+        if (full) {
+            const float4 t4 = *reinterpret_cast<const float4 *>(w + i0);
+            wv[0] = t4.x; wv[1] = t4.y; wv[2] = t4.z; wv[3] = t4.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) wv[e] = (i0 + e < n) ? w[i0 + e] : 0.0f;
+        }
+        if (!ROUTED) {
+            if (full) {
+                const uint32_t t4 = *reinterpret_cast<const uint32_t *>(node_in + i0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) nd[e] = (t4 >> (8 * e)) & 0xff;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) nd[e] = (i0 + e < n) ? node_in[i0 + e] : 0;
+            }
+        } else if (layer == 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) nd[e] = 1;
+        } else {
+            int par[4];
+            if (layer == 1) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) par[e] = 1;
+            } else if (full) {
+                const uint32_t t4 = *reinterpret_cast<const uint32_t *>(node_in + i0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) par[e] = (t4 >> (8 * e)) & 0xff;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) par[e] = (i0 + e < n) ? node_in[i0 + e] : half;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                unsigned k = (unsigned)(par[e] - half);
+                if (k >= (unsigned)half) {  // unreachable for ids written by this library
+                    eflag |= kErrRoute;
+                    k = 0;
+                    par[e] = half;
+                }
+                int f = s_cf[k];
+                if (f >= d) {
+                    eflag |= kErrRoute;
+                    f = 0;
+                }
+                const uint8_t x = xb[(int64_t)f * ldb + i0 + e];  // i0 + e < ldb
+                nd[e] = 2 * par[e] + (x >= s_cc[k] ? 1 : 0);
+            }
+            if (writer) {
+                if (full) {
+                    const uint32_t packed = (uint32_t)nd[0] | ((uint32_t)nd[1] << 8) |
+                                            ((uint32_t)nd[2] << 16) | ((uint32_t)nd[3] << 24);
+                    *reinterpret_cast<uint32_t *>(node_out + i0) = packed;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (i0 + e < n) node_out[i0 + e] = (uint8_t)nd[e];
+                }
+            }
+        }
+        for (int f = 0; f < nf; ++f) {
+            const uint32_t xv =
+                *reinterpret_cast<const uint32_t *>(xb + (int64_t)(j0 + f) * ldb + i0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (wv[e] != 0.0f) {
+                    const unsigned loc = (unsigned)(nd[e] - nodes - k0);
+                    const unsigned bin = (xv >> (8 * e)) & 0xffu;
+                    if (bin >= (unsigned)nbins) {
+                        eflag |= kErrBin;
+                    } else if (loc < (unsigned)nk) {
+                        const int idx = (((int)loc * fpg + f) * nbins + (int)bin) * 2 +
+                                        (wv[e] < 0.0f ? 1 : 0);
+                        atomicAdd(&lds[idx], (double)fabsf(wv[e]));
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    const int per_nf = nbins * 2;
+    double *out = partial + (size_t)p * nodes * d * per_nf;
+    for (int t = threadIdx.x; t < lds_n; t += blockDim.x) {
+        const int k = t / (fpg * per_nf);
+        const int rem = t - k * fpg * per_nf;
+        const int f = rem / per_nf;
+        const int rr = rem - f * per_nf;
+        if (k < nk && f < nf) out[((size_t)(k0 + k) * d + j0 + f) * per_nf + rr] = lds[t];
+    }
+    if (eflag) atomicOr(err, eflag);
+}
+
+// Sum of chunk partials into one histogram (fixed order over chunks).
+__global__ __launch_bounds__(256) void merge_partials_kernel(const double *__restrict__ partial,
+                                                             int chunks, size_t count,
+                                                             double *__restrict__ out) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < count;
+         i += (size_t)gridDim.x * blockDim.x) {
+        double s = 0.0;
+        for (int p = 0; p < chunks; ++p) s += partial[(size_t)p * count + i];
+        out[i] = s;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Best cut of every node of a layer.  One wavefront per (node, feature):
+// lane l owns bins 4l..4l+3, sums the chunk partials, builds the cumulative
+// histograms with an in-lane prefix plus a wavefront scan, evaluates the
+// separation gain of each candidate cut and reduces to the best (gain
+// highest, then lowest bin).  The last wavefront to finish a node reduces
+// over features (gain highest, then lowest feature) and writes the cut.
+//
+// Exactness rules shared with the plain definition: a cut whose left or
+// right side holds no event has gain exactly 0 (as the definition gives
+// with exact zero sums); a cut c >= 2 whose bin c-1 is empty makes the same
+// partition as cut c-1, has the same gain in exact arithmetic, and is
+// skipped so that the lower cut wins the tie independently of rounding.
+__global__ __launch_bounds__(256) void best_cuts_kernel(
+    const double *__restrict__ partial, int chunks, int nodes, int d, int nbins,
+    double *__restrict__ cand_gain, int *__restrict__ cand_cut, unsigned *__restrict__ ticket,
+    uint8_t *__restrict__ out_f, uint8_t *__restrict__ out_c, double *__restrict__ out_g) {
+#pragma clang fp contract(off)
+    const int lane = threadIdx.x % kWave;
+    const int pair = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (pair >= nodes * d) return;
+    const int k = pair / d;
+    const int j = pair - k * d;
+
+    double hs[4] = {0.0, 0.0, 0.0, 0.0}, hb[4] = {0.0, 0.0, 0.0, 0.0};
+    const int b0 = 4 * lane;
+    if (b0 < nbins) {
+        const size_t stride_p = (size_t)nodes * d * nbins * 2;
+        const double *base = partial + ((size_t)k * d + j) * nbins * 2 + 2 * b0;
+        const int nb = min(4, nbins - b0);
+        for (int p = 0; p < chunks; ++p) {
+            const double *src = base + (size_t)p * stride_p;
+            if (nb == 4) {
+                const double2 a0 = reinterpret_cast<const double2 *>(src)[0];
+                const double2 a1 = reinterpret_cast<const double2 *>(src)[1];
+                const double2 a2 = reinterpret_cast<const double2 *>(src)[2];
+                const double2 a3 = reinterpret_cast<const double2 *>(src)[3];
+                hs[0] += a0.x; hb[0] += a0.y;
+                hs[1] += a1.x; hb[1] += a1.y;
+                hs[2] += a2.x; hb[2] += a2.y;
+                hs[3] += a3.x; hb[3] += a3.y;
+            } else {
+                for (int e = 0; e < nb; ++e) {
+                    hs[e] += src[2 * e];
+                    hb[e] += src[2 * e + 1];
+                }
+            }
+        }
+    }
+    bool ne[4];
+    int first = 0x7fffffff, last = -1;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        ne[e] = (hs[e] != 0.0) || (hb[e] != 0.0);
+        if (ne[e]) {
+            first = min(first, b0 + e);
+            last = max(last, b0 + e);
+        }
+    }
+    // in-lane inclusive prefix
+    double ps[4], pb[4];
+    ps[0] = hs[0];
+    pb[0] = hb[0];
+#pragma unroll
+    for (int e = 1; e < 4; ++e) {
+        ps[e] = ps[e - 1] + hs[e];
+        pb[e] = pb[e - 1] + hb[e];
+    }
+    // wavefront inclusive scan of the lane totals
+    double is = ps[3], ib = pb[3];
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const double us = __shfl_up(is, off);
+        const double ub = __shfl_up(ib, off);
+        if (lane >= off) {
+            is += us;
+            ib += ub;
+        }
+    }
+    double xs = __shfl_up(is, 1), xbk = __shfl_up(ib, 1);
+    if (lane == 0) {
+        xs = 0.0;
+        xbk = 0.0;
+    }
+    const double ST = __shfl(is, kWave - 1);
+    const double BT = __shfl(ib, kWave - 1);
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        first = min(first, __shfl_xor(first, off));
+        last = max(last, __shfl_xor(last, off));
+    }
+    const bool prev_ne = __shfl_up(ne[3] ? 1 : 0, 1) != 0;
+    const double gp = gini(ST, BT);
+
+    double best = -INFINITY;
+    int bestc = 0x7fffffff;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int c = b0 + e;
+        if (c < 1 || c > nbins - 1) continue;
+        const bool below_ne = e > 0 ? ne[e - 1] : prev_ne;
+        if (c >= 2 && !below_ne) continue;
+        double g;
+        if (c <= first || c > last) {
+            g = 0.0;
+        } else {
+            const double S = e > 0 ? xs + ps[e - 1] : xs;
+            const double B = e > 0 ? xbk + pb[e - 1] : xbk;
+            g = (gp - gini(S, B)) - gini(ST - S, BT - B);
+        }
+        if (g > best) {
+            best = g;
+            bestc = c;
+        }
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const double og = __shfl_xor(best, off);
+        const int oc = __shfl_xor(bestc, off);
+        if (og > best || (og == best && oc < bestc)) {
+            best = og;
+            bestc = oc;
+        }
+    }
+    if (lane == 0) {
+        cand_gain[pair] = best;
+        cand_cut[pair] = bestc;
+    }
+    __threadfence();
+    unsigned prev = 0;
+    if (lane == 0) prev = atomicAdd(&ticket[k], 1u);
+    prev = __shfl(prev, 0);
+    if (prev != (unsigned)(d - 1)) return;
+
+    // last wavefront of node k: best over features
+    __threadfence();
+    double bg = -INFINITY;
+    int bj = 0x7fffffff, bc = 1;
+    for (int jj = lane; jj < d; jj += kWave) {
+        const double gg = load_agent(&cand_gain[(size_t)k * d + jj]);
+        if (gg > bg) {
+            bg = gg;
+            bj = jj;
+            bc = load_agent(&cand_cut[(size_t)k * d + jj]);
+        }
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const double og = __shfl_xor(bg, off);
+        const int oj = __shfl_xor(bj, off);
+        const int oc = __shfl_xor(bc, off);
+        if (og > bg || (og == bg && oj < bj)) {
+            bg = og;
+            bj = oj;
+            bc = oc;
+        }
+    }
+    if (lane == 0) {
+        out_f[k] = (uint8_t)bj;
+        out_c[k] = (uint8_t)bc;
+        out_g[k] = bg;
+        ticket[k] = 0u;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Terminal boost weights (section 1.3): per leaf, sum(v y~) and
+// sum(v |y~| (2 - |y~|)) over the sampled events, in LDS per workgroup; the
+// last workgroup sums the workgroup partials in block order and writes
+// eta * num / den (0 when den = 0).  Routed mode first sends every event
+// from layer depth-1 to its leaf and stores the leaf id.
+template <bool ROUTED>
+__global__ __launch_bounds__(256) void leaf_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
+    const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
+    const uint8_t *__restrict__ cut_f, const uint8_t *__restrict__ cut_c, int depth,
+    const int8_t *__restrict__ y, const float *__restrict__ v, const double *__restrict__ F,
+    uint64_t seed, int tree, double alpha, double eta, double *__restrict__ leaf_partial,
+    unsigned *__restrict__ ticket, double *__restrict__ leaf_out, int *__restrict__ err) {
+#pragma clang fp contract(off)
+    __shared__ double acc[2 * 128];
+    __shared__ uint8_t s_cf[64], s_cc[64];
+    __shared__ unsigned s_last;
+    const int nleaf = 1 << depth;
+    const int half = nleaf >> 1;
+    for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x) acc[t] = 0.0;
+    if (ROUTED)
+        for (int t = threadIdx.x; t < half; t += blockDim.x) {
+            s_cf[t] = cut_f[t];
+            s_cc[t] = cut_c[t];
+        }
+    __syncthreads();
+    int eflag = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int leaf;
+        if (ROUTED) {
+            int par = node_in ? (int)node_in[i] : 1;
+            unsigned k = (unsigned)(par - half);
+            if (k >= (unsigned)half) {
+                eflag |= kErrRoute;
+                k = 0;
+                par = half;
+            }
+            int f = s_cf[k];
+            if (f >= d) {
+                eflag |= kErrRoute;
+                f = 0;
+            }
+            const uint8_t x = xb[(int64_t)f * ldb + i];
+            leaf = 2 * par + (x >= s_cc[k] ? 1 : 0);
+            node_out[i] = (uint8_t)leaf;
+        } else {
+            leaf = node_in[i];
+            if ((unsigned)(leaf - nleaf) >= (unsigned)nleaf) {
+                eflag |= kErrRoute;
+                continue;
+            }
+        }
+        if (in_subsample(seed, tree, n, i, alpha)) {
+            const double yf = (double)y[i];
+            const double yt = pseudo_response(yf, F[i]);
+            const double vi = v ? (double)v[i] : 1.0;
+            const double a = fabs(yt);
+            const int li = leaf - nleaf;
+            atomicAdd(&acc[2 * li], vi * yt);
+            atomicAdd(&acc[2 * li + 1], vi * a * (2.0 - a));
+        }
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x)
+        leaf_partial[(size_t)blockIdx.x * 2 * nleaf + t] = acc[t];
+    if (eflag) atomicOr(err, eflag);
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = (atomicAdd(ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    for (int t = threadIdx.x; t < nleaf; t += blockDim.x) {
+        double num = 0.0, den = 0.0;
+        for (unsigned b = 0; b < gridDim.x; ++b) {
+            num += load_agent(&leaf_partial[(size_t)b * 2 * nleaf + 2 * t]);
+            den += load_agent(&leaf_partial[(size_t)b * 2 * nleaf + 2 * t + 1]);
+        }
+        leaf_out[t] = den == 0.0 ? 0.0 : eta * (num / den);
+    }
+    if (threadIdx.x == 0) *ticket = 0u;
+}
+
+// node <- 2 node + [xb[f][i] >= c] with (f, c) the cut of the node.
+__global__ __launch_bounds__(256) void route_kernel(const uint8_t *__restrict__ xb, int64_t ldb,
+                                                    int64_t n, int d, uint8_t *__restrict__ node,
+                                                    const uint8_t *__restrict__ cut_f,
+                                                    const uint8_t *__restrict__ cut_c, int layer,
+                                                    int *__restrict__ err) {
+    const int lo = 1 << layer;
+    int eflag = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int nd = node[i];
+        const unsigned k = (unsigned)(nd - lo);
+        if (k >= (unsigned)lo) {
+            eflag |= kErrRoute;
+            continue;
+        }
+        const int f = cut_f[k];
+        if (f >= d) {
+            eflag |= kErrRoute;
+            continue;
+        }
+        node[i] = (uint8_t)(2 * nd + (xb[(int64_t)f * ldb + i] >= cut_c[k] ? 1 : 0));
+    }
+    if (eflag) atomicOr(err, eflag);
+}
+
+// ---------------------------------------------------------------------------
+// Forest traversal.  A workgroup stages a tile of `blockDim.x` events (all
+// model features, padded rows to spread LDS banks) and a chunk of trees in
+// LDS; each thread walks its event through every tree (left = bin < cut,
+// Fig. 1), adds the leaf's boost weight to F in float64 in tree order, and
+// writes 1 / (1 + exp(-2F)) as float32.
+__global__ __launch_bounds__(1024) void apply_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d_used,
+    const uint16_t *__restrict__ cuts, const double *__restrict__ leaves, int T, int depth,
+    int tpc, double f0, float *__restrict__ prob, double *__restrict__ score) {
+    extern __shared__ double smem[];
+    const int nin = (1 << depth) - 1;
+    const int nleaf = 1 << depth;
+    double *s_leaf = smem;
+    uint16_t *s_cut = reinterpret_cast<uint16_t *>(s_leaf + (size_t)tpc * nleaf);
+    uint8_t *s_x = reinterpret_cast<uint8_t *>(s_cut + (((size_t)tpc * nin + 3) & ~(size_t)3));
+    const int XS = blockDim.x + 4;
+    const int nchunks = (T + tpc - 1) / tpc;
+    const int64_t ntiles = (n + blockDim.x - 1) / blockDim.x;
+    bool staged = false;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t i = tile * blockDim.x + threadIdx.x;
+        __syncthreads();
+        for (int f = 0; f < d_used; ++f)
+            s_x[f * XS + threadIdx.x] = i < n ? xb[(int64_t)f * ldb + i] : 0;
+        double Fv = f0;
+        for (int ch = 0; ch < nchunks; ++ch) {
+            const int t0 = ch * tpc;
+            const int tc = min(tpc, T - t0);
+            if (nchunks > 1 || !staged) {
+                __syncthreads();
+                for (int q = threadIdx.x; q < tc * nleaf; q += blockDim.x)
+                    s_leaf[q] = leaves[(size_t)t0 * nleaf + q];
+                for (int q = threadIdx.x; q < tc * nin; q += blockDim.x)
+                    s_cut[q] = cuts[(size_t)t0 * nin + q];
+                staged = true;
+            }
+            __syncthreads();
+            for (int t = 0; t < tc; ++t) {
+                int node = 1;
+                for (int lvl = 0; lvl < depth; ++lvl) {
+                    const uint16_t cc = s_cut[t * nin + node - 1];
+                    const int f = cc & 0xff;
+                    const int c = cc >> 8;
+                    node = 2 * node + (s_x[f * XS + threadIdx.x] >= c ? 1 : 0);
+                }
+                Fv += s_leaf[t * nleaf + node - nleaf];
+            }
+        }
+        if (i < n) {
+            prob[i] = (float)(1.0 / (1.0 + exp(-2.0 * Fv)));
+            if (score) score[i] = Fv;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Bin code of a float: number of boundaries <= value (upper bound by binary
+// search over the feature's boundaries in LDS).  Row padding [n, ldb) is
+// written as 0.
+__global__ __launch_bounds__(256) void encode_kernel(const float *__restrict__ x, int64_t ldx,
+                                                     int64_t n, int d,
+                                                     const float *__restrict__ bounds, int nbins,
+                                                     uint8_t *__restrict__ xb, int64_t ldb,
+                                                     int *__restrict__ err) {
+    __shared__ float sb[256];
+    const int j = blockIdx.y;
+    const int nb = nbins - 1;
+    for (int k = threadIdx.x; k < nb; k += blockDim.x) sb[k] = bounds[(size_t)j * nb + k];
+    __syncthreads();
+    int eflag = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < ldb;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        uint8_t code = 0;
+        if (i < n) {
+            const float val = x[(int64_t)j * ldx + i];
+            if (val != val) {
+                eflag |= kErrNan;
+            } else {
+                int lo = 0, len = nb;
+                while (len > 0) {
+                    const int hh = len >> 1;
+                    if (sb[lo + hh] <= val) {
+                        lo += hh + 1;
+                        len -= hh + 1;
+                    } else {
+                        len = hh;
+                    }
+                }
+                code = (uint8_t)lo;
+            }
+        }
+        xb[(int64_t)j * ldb + i] = code;
+    }
+    if (eflag) atomicOr(err, eflag);
+}
+
+int grid_for(int64_t n, int threads, int cap) {
+    int64_t g = (n + threads - 1) / threads;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (int)g;
+}
+
+// Raises a kernel's dynamic-LDS limit above 64 KiB when a launch needs it;
+// a launch beyond the device limit then fails and reports its own error.
+template <typename K>
+void allow_lds(K kernel, size_t bytes) {
+    if (bytes <= 65536) return;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) (void)hipGetLastError();
+}
+
+}  // namespace
+
+// ===========================================================================
+hipError_t launch_fill_u32(void *p, uint32_t value, size_t count, hipStream_t s) {
+    if (count == 0) return hipSuccess;
+    fill_u32_kernel<<<grid_for((int64_t)count, 256, 1024), 256, 0, s>>>(
+        static_cast<uint32_t *>(p), value, count);
+    return hipGetLastError();
+}
+
+hipError_t launch_validate(const int8_t *y, const float *v, int64_t n, double *class_partial,
+                           int *err, hipStream_t s) {
+    validate_kernel<<<kValidateBlocks, 256, 0, s>>>(y, v, n, class_partial, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_initial_score(const double *class_partial, double *f0, int *err,
+                                hipStream_t s) {
+    initial_score_kernel<<<1, 256, 0, s>>>(class_partial, kValidateBlocks, f0, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const double *f0,
+                            const uint8_t *leaf_node, const double *leaf_prev, int depth,
+                            int64_t n, uint64_t seed, int tree, double alpha, float *w,
+                            double *score_out, hipStream_t s) {
+    tree_prep_kernel<<<grid_for(n, 256, 4096), 256, 0, s>>>(
+        y, v, F, f0, leaf_node, leaf_prev, depth, n, seed, tree, alpha, w, score_out);
+    return hipGetLastError();
+}
+
+HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
+                         size_t max_lds, int fpg, int chunks, int threads) {
+    HistShape hs{};
+    const int nodes = 1 << layer;
+    const size_t per_node_feature = (size_t)n_bins * 2 * sizeof(double);
+    int npg = (int)(max_lds / per_node_feature);
+    if (npg < 1) npg = 1;
+    if (npg > nodes) npg = nodes;
+    hs.nodes_per_group = npg;
+    hs.node_groups = (nodes + npg - 1) / npg;
+    int f = fpg > 0 ? fpg : 1;
+    if (f > d) f = d;
+    while (f > 1 && (size_t)npg * f * per_node_feature > max_lds) --f;
+    hs.features_per_group = f;
+    hs.feature_groups = (d + f - 1) / f;
+    hs.threads = threads > 0 ? threads : 256;
+    const int groups = hs.feature_groups * hs.node_groups;
+    int64_t c = chunks > 0 ? chunks : (2 * (int64_t)cu_count + groups - 1) / groups;
+    const int64_t min_events = 4LL * hs.threads;
+    const int64_t cmax = (n + min_events - 1) / min_events;
+    if (c > cmax) c = cmax;
+    if (c < 1) c = 1;
+    int64_t ce = (n + c - 1) / c;
+    ce = (ce + 3) & ~(int64_t)3;
+    hs.chunk_events = ce;
+    hs.chunks = (int)((n + ce - 1) / ce);
+    const int64_t work = (int64_t)hs.chunks * groups;
+    hs.blocks = (int)((work + kXcds - 1) / kXcds * kXcds);
+    hs.lds_bytes = (size_t)npg * f * per_node_feature;
+    return hs;
+}
+
+hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
+                            int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
+                            const float *w, const uint8_t *cut_f, const uint8_t *cut_c,
+                            int layer, bool routed, double *partial, int *err, hipStream_t s) {
+    if (routed) {
+        allow_lds(hist_kernel<true>, hs.lds_bytes);
+        hist_kernel<true><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+            xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f, cut_c, layer,
+            hs.features_per_group, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
+            hs.chunks, hs.chunk_events, partial, err);
+    } else {
+        allow_lds(hist_kernel<false>, hs.lds_bytes);
+        hist_kernel<false><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+            xb, ldb, n, d, n_bins, node_in, nullptr, w, nullptr, nullptr, layer,
+            hs.features_per_group, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
+            hs.chunks, hs.chunk_events, partial, err);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_merge_partials(const double *partial, int chunks, size_t count, double *out,
+                                 hipStream_t s) {
+    merge_partials_kernel<<<grid_for((int64_t)count, 256, 2048), 256, 0, s>>>(partial, chunks,
+                                                                             count, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_best_cuts(const double *partial, int chunks, int n_nodes, int d, int n_bins,
+                            double *cand_gain, int *cand_cut, unsigned *ticket, uint8_t *out_f,
+                            uint8_t *out_c, double *out_g, hipStream_t s) {
+    const int waves_per_block = 4;
+    const int pairs = n_nodes * d;
+    const int blocks = (pairs + waves_per_block - 1) / waves_per_block;
+    best_cuts_kernel<<<blocks, waves_per_block * kWave, 0, s>>>(
+        partial, chunks, n_nodes, d, n_bins, cand_gain, cand_cut, ticket, out_f, out_c, out_g);
+    return hipGetLastError();
+}
+
+int leaf_blocks(int64_t n, int cu_count) { return grid_for(n, 256, 2 * cu_count); }
+
+hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
+                       uint8_t *node_out, const uint8_t *cut_f, const uint8_t *cut_c, int depth,
+                       bool routed, const int8_t *y, const float *v, const double *F,
+                       uint64_t seed, int tree, double alpha, double eta, int blocks,
+                       double *leaf_partial, unsigned *ticket, double *leaf_out, int *err,
+                       hipStream_t s) {
+    if (routed)
+        leaf_kernel<true><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, node_out, cut_f, cut_c,
+                                                 depth, y, v, F, seed, tree, alpha, eta,
+                                                 leaf_partial, ticket, leaf_out, err);
+    else
+        leaf_kernel<false><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, nullptr, nullptr,
+                                                  nullptr, depth, y, v, F, seed, tree, alpha,
+                                                  eta, leaf_partial, ticket, leaf_out, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *node,
+                        const uint8_t *cut_f, const uint8_t *cut_c, int layer, int *err,
+                        hipStream_t s) {
+    route_kernel<<<grid_for(n, 256, 4096), 256, 0, s>>>(xb, ldb, n, d, node, cut_f, cut_c, layer,
+                                                       err);
+    return hipGetLastError();
+}
+
+ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_count,
+                      size_t max_lds, int threads) {
+    ApplyShape as{};
+    as.threads = threads > 0 ? threads : 256;
+    as.d_used = d_used;
+    const int nin = (1 << depth) - 1, nleaf = 1 << depth;
+    const size_t xtile = (size_t)d_used * (as.threads + 4);
+    const size_t per_tree = (size_t)nleaf * 8 + (size_t)nin * 2;
+    size_t budget = 65536;
+    if (budget < xtile + per_tree + 64) budget = max_lds;
+    size_t room = budget > xtile + 64 ? budget - xtile - 64 : 0;
+    int64_t tpc = (int64_t)(room / per_tree);
+    if (tpc < 1) tpc = 1;
+    if (tpc > n_trees) tpc = n_trees;
+    as.trees_per_chunk = (int)tpc;
+    as.lds_bytes = (size_t)tpc * nleaf * 8 + ((((size_t)tpc * nin) + 3) & ~(size_t)3) * 2 + xtile;
+    const int64_t ntiles = (n + as.threads - 1) / as.threads;
+    int64_t blocks = (int64_t)cu_count * 8;
+    if (blocks > ntiles) blocks = ntiles;
+    if (blocks < 1) blocks = 1;
+    as.blocks = (int)blocks;
+    return as;
+}
+
+hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
+                        const uint16_t *cuts, const double *leaves, int n_trees, int depth,
+                        double f0, float *prob, double *score, hipStream_t s) {
+    allow_lds(apply_kernel, as.lds_bytes);
+    apply_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(xb, ldb, n, as.d_used, cuts, leaves,
+                                                            n_trees, depth, as.trees_per_chunk,
+                                                            f0, prob, score);
+    return hipGetLastError();
+}
+
+hipError_t launch_encode(const float *x, int64_t ldx, int64_t n, int d, const float *bounds,
+                         int n_bins, uint8_t *xb, int64_t ldb, int *err, hipStream_t s) {
+    dim3 grid(grid_for(ldb, 256, 1024), d);
+    encode_kernel<<<grid, 256, 0, s>>>(x, ldx, n, d, bounds, n_bins, xb, ldb, err);
+    return hipGetLastError();
+}
+
+}  // namespace fbdt

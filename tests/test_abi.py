@@ -1,0 +1,53 @@
+"""The C ABI library loads on the CPU host and exports every declared symbol."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fbdt.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fbdt_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("fbdt_bin", "fbdt_bin_transform", "fbdt_fit", "fbdt_apply",
+                     "fbdt_model_export", "fbdt_model_import", "fbdt_model_free",
+                     "fbdt_last_error", "fbdt_histogram", "fbdt_best_cuts", "fbdt_route",
+                     "fbdt_tree_weights", "fbdt_leaf_values"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_1609_06119_amd._lib import EXPORTED, LIB_PATH
+    if not os.path.exists(LIB_PATH):
+        pytest.fail("libfbdt.so is not built (run __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert missing == []
+    assert sorted(EXPORTED) == declared_functions()
+
+
+def test_argument_errors_need_no_device():
+    # checks that run before any HIP call
+    from paper_1609_06119_amd._lib import FitParams, lib
+    L = lib()
+    h = ctypes.c_void_p()
+    p = FitParams(3, 10, 0.1, 0.5, 0)
+    assert L.fbdt_fit(None, 10, 2, 16, 16, None, None, ctypes.byref(p), ctypes.byref(h), None,
+                      None) == -1
+    assert b"xb" in L.fbdt_last_error()
+    buf = ctypes.create_string_buffer(64)
+    aligned = (ctypes.addressof(buf) + 15) // 16 * 16
+    assert L.fbdt_fit(ctypes.c_void_p(aligned), 10, 2, 15, 16, None, None, ctypes.byref(p),
+                      ctypes.byref(h), None, None) == -1
+    assert b"ldb" in L.fbdt_last_error()
+    assert L.fbdt_set_option(b"no_such_option", 1) == -1
+    assert L.fbdt_set_option(b"hist_threads", 100) == -1
+    assert L.fbdt_set_option(b"hist_threads", 0) == 0

@@ -1,0 +1,374 @@
+"""Parity of the HIP library (through its C ABI) with the CPU oracle.
+
+Tolerances: bin codes, boundaries, sub-sample masks, node ids, cut features
+and cut bins are compared exactly (tree structure only up to near-ties of
+the oracle's gains, relative 1e-6, adopted and counted); histogram sums to
+relative 1e-5 (also checked at 1e-12, the float64 accumulation level);
+probabilities to |dP| <= 1e-5; scores, gains and boost weights to relative
+1e-9 (float64 sums taken in a different order).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_1609_06119_amd as fb
+from oracle import fbdt_oracle as O
+from synth import CONFIGS, make_apply_chunk, make_training_set, random_forest
+
+pytestmark = pytest.mark.gpu
+
+HIST_RTOL = 1e-5
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def max_rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    den = np.maximum(np.abs(b), 1e-300)
+    return float(np.max(np.where(a == b, 0.0, np.abs(a - b) / den))) if a.size else 0.0
+
+
+@pytest.fixture(autouse=True)
+def _defaults():
+    for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads",
+                 "apply_threads"):
+        fb.set_option(name, 0)
+    yield
+    for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads",
+                 "apply_threads"):
+        fb.set_option(name, 0)
+
+
+# ------------------------------------------------------------------ binning
+def _bin_cases():
+    rng = np.random.default_rng(0)
+    cases = [("config1", make_training_set(1)["x"], 16),
+             ("config2-100k", make_training_set(2, n_events=100_003)["x"], 256),
+             ("config4-50k", make_training_set(4, n_events=50_001)["x"], 256)]
+    x = rng.normal(size=(3, 1001)).astype(np.float32)
+    x[0, :10] = np.inf
+    x[1, :10] = -np.inf
+    x[2, ::3] = 0.0
+    x[2, 1::3] = -0.0
+    cases.append(("inf-and-signed-zero", x, 32))
+    cases.append(("one-event", np.array([[1.5]], np.float32), 2))
+    cases.append(("more-bins-than-events", rng.normal(size=(2, 5)).astype(np.float32), 256))
+    return cases
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_bin_matches_oracle(case):
+    name, x, B = _bin_cases()[case]
+    say(f"bin parity: {name} d={x.shape[0]} n={x.shape[1]} B={B}")
+    bounds, codes = fb.bin(dev(x), B)
+    ob, oc = O.bin_features(x, B)
+    assert np.array_equal(bounds, ob)
+    assert np.array_equal(codes.numpy(), oc)
+    pad = codes.data[:, codes.n:].cpu().numpy()
+    assert not pad.any()
+
+
+def test_bin_with_row_stride_and_transform():
+    ds = make_training_set(1)
+    x = ds["x"]
+    wide = np.zeros((x.shape[0], x.shape[1] + 37), np.float32)
+    wide[:, : x.shape[1]] = x
+    xw = dev(wide)[:, : x.shape[1]]
+    say("bin with ldx > n")
+    bounds, codes = fb.bin(xw, 16)
+    ob, oc = O.bin_features(x, 16)
+    assert np.array_equal(bounds, ob) and np.array_equal(codes.numpy(), oc)
+    fresh = make_apply_chunk(0, 30_001)["x"][:8]
+    say("bin_transform of fresh events")
+    c2 = fb.bin_transform(dev(fresh), bounds)
+    ref = np.stack([O.encode(fresh[j], ob[j]) for j in range(8)])
+    assert np.array_equal(c2.numpy(), ref)
+
+
+def test_bin_rejects_nan():
+    x = np.ones((2, 100), np.float32)
+    x[1, 50] = np.nan
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.bin(dev(x), 16)
+    assert ei.value.status == "FBDT_E_NAN"
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.bin_transform(dev(x), np.zeros((2, 15), np.float32))
+    assert ei.value.status == "FBDT_E_NAN"
+
+
+# ------------------------------------------------------------ single steps
+def test_tree_weights_match_oracle():
+    rng = np.random.default_rng(1)
+    n = 100_003
+    y = np.where(rng.random(n) < 0.5, 1, -1).astype(np.int8)
+    v = rng.uniform(0, 2, n).astype(np.float32)
+    v[:100] = 0
+    F = rng.normal(0, 2, n)
+    for tree, alpha in ((0, 0.5), (7, 0.3), (2, 1.0)):
+        say(f"tree_weights tree={tree} alpha={alpha}")
+        w = fb.tree_weights(dev(y), dev(v), dev(F), seed=99, tree=tree, alpha=alpha).cpu().numpy()
+        mask = O.subsample_mask(99, tree, n, alpha)
+        ow = O.histogram_weights(y, v, O.pseudo_response(y, F), mask)
+        ows = np.where(y > 0, ow, -ow).astype(np.float32)
+        assert np.array_equal(w != 0, ows != 0)
+        assert np.array_equal(np.signbit(w[w != 0]), np.signbit(ows[ows != 0]))
+        np.testing.assert_array_max_ulp(w, ows, maxulp=1)
+        if alpha < 1.0:
+            sampled = (w != 0) | (v == 0) & mask
+            assert np.array_equal(sampled[v != 0], mask[v != 0])
+
+
+@pytest.mark.parametrize("layer,n_bins,d,n", [(0, 256, 7, 65_539), (1, 16, 3, 1000),
+                                              (2, 256, 20, 100_001), (3, 64, 5, 20_000),
+                                              (5, 256, 4, 50_003), (6, 256, 2, 30_001),
+                                              (0, 2, 1, 1), (4, 256, 9, 7)])
+def test_histogram_matches_oracle(layer, n_bins, d, n):
+    rng = np.random.default_rng(layer * 31 + n_bins)
+    xb = rng.integers(0, n_bins, (d, n)).astype(np.uint8)
+    node = rng.integers(1 << layer, 2 << layer, n).astype(np.uint8)
+    y = np.where(rng.random(n) < 0.45, 1, -1).astype(np.int8)
+    wa = rng.uniform(0, 2, n).astype(np.float32)
+    wa[rng.random(n) < 0.5] = 0
+    ws = np.where(y > 0, wa, -wa).astype(np.float32)
+    ref = O.histogram(xb, node.astype(np.int64), wa, y > 0, layer, n_bins)
+    codes = fb.Codes.from_numpy(xb)
+    for chunks in (0, 1, 3, 17):
+        fb.set_option("hist_event_chunks", chunks)
+        say(f"histogram layer={layer} B={n_bins} d={d} n={n} chunks={chunks}")
+        H = fb.histogram(codes, dev(node), dev(ws), layer, n_bins).cpu().numpy()
+        assert np.array_equal(H == 0, ref == 0)
+        err = max_rel(H, ref)
+        assert err <= HIST_RTOL
+        assert err <= 1e-12, err
+
+
+def test_histogram_feature_groups_and_threads():
+    rng = np.random.default_rng(3)
+    n, d, B, layer = 40_001, 11, 256, 2
+    xb = rng.integers(0, B, (d, n)).astype(np.uint8)
+    node = rng.integers(4, 8, n).astype(np.uint8)
+    y = np.where(rng.random(n) < 0.5, 1, -1).astype(np.int8)
+    wa = rng.uniform(0.1, 1, n).astype(np.float32)
+    ws = np.where(y > 0, wa, -wa).astype(np.float32)
+    ref = O.histogram(xb, node.astype(np.int64), wa, y > 0, layer, B)
+    codes = fb.Codes.from_numpy(xb)
+    for fpg, threads in ((2, 256), (3, 512), (5, 1024), (11, 128)):
+        fb.set_option("hist_features_per_group", fpg)
+        fb.set_option("hist_threads", threads)
+        say(f"histogram fpg={fpg} threads={threads}")
+        H = fb.histogram(codes, dev(node), dev(ws), layer, B).cpu().numpy()
+        assert max_rel(H, ref) <= 1e-12
+
+
+def _check_cuts(H, f, c, g):
+    S, Bk = O.cumulative(H)
+    gains = O.split_gains(S, Bk)
+    of, oc, og = O.best_cuts(gains)
+    n_bins = H.shape[2]
+    parent = O.gini(S[:, 0, n_bins], Bk[:, 0, n_bins])
+    ties = 0
+    for k in range(H.shape[0]):
+        if (f[k], c[k]) != (of[k], oc[k]):
+            other = gains[k, f[k], c[k] - 1]
+            assert O.is_near_tie(og[k], other, parent[k]), (k, (f[k], c[k]), (of[k], oc[k]))
+            ties += 1
+        assert abs(g[k] - gains[k, f[k], c[k] - 1]) <= 1e-12 * max(abs(parent[k]), 1e-300)
+    return ties
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_best_cuts_match_oracle(seed):
+    rng = np.random.default_rng(seed)
+    n_nodes = [1, 2, 4, 8, 32, 64][seed]
+    d = [1, 3, 5, 20, 7, 2][seed]
+    B = [2, 16, 256, 256, 64, 256][seed]
+    H = rng.uniform(0, 5, (n_nodes, d, B, 2))
+    H[rng.random(H.shape) < 0.3] = 0.0              # empty bins
+    if n_nodes > 1:
+        H[1] = 0.0                                   # an empty node
+        H[0, :, :, 1] = 0.0                          # a pure node
+    say(f"best_cuts nodes={n_nodes} d={d} B={B}")
+    f, c, g = (t.cpu().numpy() for t in fb.best_cuts(dev(H)))
+    _check_cuts(H, f, c, g)
+    if n_nodes > 1:
+        assert (f[1], c[1], g[1]) == (0, 1, 0.0)
+        assert (f[0], c[0], g[0]) == (0, 1, 0.0)
+
+
+def test_best_cuts_exact_ties_take_lowest_feature_and_bin():
+    # XOR root (Table 3, section 4.3): every gain is exactly 0
+    H = np.zeros((1, 2, 2, 2))
+    H[0, :, :, :] = 1.0
+    f, c, g = (t.cpu().numpy() for t in fb.best_cuts(dev(H)))
+    assert (f[0], c[0], g[0]) == (0, 1, 0.0)
+    # two identical features: the lower wins; duplicate bins: the lower cut wins
+    H = np.zeros((1, 3, 8, 2))
+    H[0, :, 2, 0] = 3.0
+    H[0, :, 6, 1] = 2.0
+    H[0, 0, :, :] = 0.0
+    H[0, 0, 0, 0] = 5.0
+    f, c, g = (t.cpu().numpy() for t in fb.best_cuts(dev(H)))
+    assert (f[0], c[0]) == (1, 3)
+
+
+def test_route_matches_oracle():
+    rng = np.random.default_rng(4)
+    n, d, B = 70_001, 6, 32
+    xb = rng.integers(0, B, (d, n)).astype(np.uint8)
+    codes = fb.Codes.from_numpy(xb)
+    for layer in (0, 1, 3, 6):
+        node = rng.integers(1 << layer, 2 << layer, n).astype(np.uint8)
+        cf = rng.integers(0, d, 1 << layer).astype(np.uint8)
+        cc = rng.integers(1, B, 1 << layer).astype(np.uint8)
+        say(f"route layer={layer}")
+        got = fb.route(codes, dev(node), dev(cf), dev(cc), layer).cpu().numpy()
+        ref = O.route(node.astype(np.int64), xb, cf, cc, layer)
+        assert np.array_equal(got.astype(np.int64), ref)
+
+
+def test_leaf_values_match_oracle():
+    rng = np.random.default_rng(5)
+    n = 90_001
+    for depth in (1, 3, 6, 7):
+        leaf_id = rng.integers(1 << depth, 2 << depth, n).astype(np.uint8)
+        leaf_id[leaf_id == (1 << depth) + 1] = 1 << depth     # one empty leaf
+        y = np.where(rng.random(n) < 0.5, 1, -1).astype(np.int8)
+        v = rng.uniform(0.2, 2, n).astype(np.float32)
+        F = rng.normal(0, 1.5, n)
+        say(f"leaf_values depth={depth}")
+        got = fb.leaf_values(dev(leaf_id), dev(y), dev(v), dev(F), depth, seed=7, tree=3,
+                             alpha=0.5, eta=0.1).cpu().numpy()
+        mask = O.subsample_mask(7, 3, n, 0.5)
+        ref = 0.1 * O.leaf_values(leaf_id.astype(np.int64) - (1 << depth),
+                                  O.pseudo_response(y, F), v, mask, 1 << depth)
+        assert got[1] == 0.0 and ref[1] == 0.0
+        assert max_rel(got, ref) <= 1e-12
+
+
+# --------------------------------------------------------------- full fit
+def _oracle_model(m):
+    return O.Model(m["depth"], m["n_bins"], m["n_features"], m["f0"], m["cut_feature"],
+                   m["cut_bin"], m["gain"], m["leaf"])
+
+
+FIT_CASES = {
+    "config1": dict(cfg=1),
+    "config2-full": dict(cfg=2),
+    "config3-100k-20trees": dict(cfg=3, n_events=100_000, n_trees=20),
+    "config4-200k-3trees": dict(cfg=4, n_events=200_000, n_trees=3),
+    "ragged-depth1-B2": dict(cfg=1, n_events=1237, depth=1, n_bins=2, n_trees=5),
+    "depth7-B128": dict(cfg=3, n_events=40_013, depth=7, n_bins=128, n_trees=2, subsample=1.0),
+    "weighted-alpha0.8": dict(cfg=2, n_events=30_011, n_trees=8, weights=True, subsample=0.8),
+}
+
+
+@pytest.mark.parametrize("case", list(FIT_CASES))
+def test_fit_and_apply_match_oracle(case):
+    c = FIT_CASES[case]
+    spec = CONFIGS[c["cfg"]]
+    ds = make_training_set(c["cfg"], n_events=c.get("n_events"))
+    n = ds["x"].shape[1]
+    B = c.get("n_bins", spec.n_bins)
+    D = c.get("depth", spec.depth)
+    T = c.get("n_trees", spec.n_trees)
+    alpha = c.get("subsample", spec.subsample)
+    eta = spec.shrinkage
+    seed = spec.fit_seed
+    v = ds["v"]
+    if c.get("weights"):
+        v = np.random.default_rng(9).uniform(0.2, 3.0, n).astype(np.float32)
+    say(f"fit parity {case}: n={n} d={ds['x'].shape[0]} B={B} D={D} T={T} alpha={alpha}")
+    bounds, codes = fb.bin(dev(ds["x"]), B)
+    ob, xb = O.bin_features(ds["x"], B)
+    assert np.array_equal(codes.numpy(), xb)
+    score = torch.empty(n, dtype=torch.float64, device="cuda")
+    model = fb.fit(codes, dev(ds["y"]), B, D, T, eta, alpha, seed, w=dev(v), score_out=score)
+    gm = model.export()
+    say(f"  oracle fit {case}")
+    log = O.TieLog()
+    om, F = O.fit(xb, ds["y"], v, D, T, eta, alpha, seed, B, reference=_oracle_model(gm),
+                  tie_log=log, final_score=True)
+    say(f"  near-ties adopted: {len(log.adopted)}  rejected: {len(log.rejected)}")
+    assert log.rejected == []
+    assert np.array_equal(gm["cut_feature"], om.cut_feature)
+    assert np.array_equal(gm["cut_bin"], om.cut_bin)
+    assert abs(gm["f0"] - om.f0) <= 1e-12
+    assert np.allclose(gm["leaf"], om.leaf, rtol=1e-9, atol=1e-13)
+    assert np.allclose(gm["gain"], om.gain, rtol=1e-9, atol=1e-12 * n)
+    Fg = score.cpu().numpy()
+    assert np.allclose(Fg, F, rtol=1e-9, atol=1e-12)
+    say(f"  apply {case}")
+    ascore = torch.empty(n, dtype=torch.float64, device="cuda")
+    p = fb.apply(model, codes, score=ascore).cpu().numpy()
+    assert np.array_equal(ascore.cpu().numpy(), Fg)          # apply reproduces the fit's F
+    op, oF = O.apply(om, xb)
+    assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
+    assert np.allclose(ascore.cpu().numpy(), oF, rtol=1e-9, atol=1e-12)
+
+
+# ------------------------------------------------------------------ apply
+@pytest.mark.parametrize("T,D,d,n", [(400, 3, 40, 100_003), (100, 6, 40, 50_001),
+                                     (1, 1, 1, 1), (50, 7, 255, 3001), (3, 2, 5, 255)])
+def test_apply_random_forest_matches_oracle(T, D, d, n):
+    B = 256
+    f = random_forest(T, D, d, B, seed=T + D)
+    rng = np.random.default_rng(d)
+    xb = rng.integers(0, B, (d, n)).astype(np.uint8)
+    say(f"apply T={T} D={D} d={d} n={n}")
+    model = fb.Model.from_arrays(f["cut_feature"], f["cut_bin"], f["leaf"], f["f0"], d, B)
+    codes = fb.Codes.from_numpy(xb)
+    score = torch.empty(n, dtype=torch.float64, device="cuda")
+    p = fb.apply(model, codes, score=score).cpu().numpy()
+    om = O.Model(D, B, d, f["f0"], f["cut_feature"], f["cut_bin"], np.zeros_like(f["leaf"][:, 1:]),
+                 f["leaf"])
+    op, oF = O.apply(om, xb)
+    assert np.array_equal(score.cpu().numpy(), oF)     # same leaves, same order
+    assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
+    np.testing.assert_array_max_ulp(p, op, maxulp=1)
+
+
+# ------------------------------------------------------------------ errors
+def test_errors_are_reported():
+    n, d, B = 1000, 3, 16
+    rng = np.random.default_rng(0)
+    codes = fb.Codes.from_numpy(rng.integers(0, B, (d, n)).astype(np.uint8))
+    y = np.where(np.arange(n) % 2 == 0, 1, -1).astype(np.int8)
+    bad = y.copy()
+    bad[5] = 0
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, dev(bad), B, 2, 2)
+    assert ei.value.status == "FBDT_E_LABEL"
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, dev(np.ones(n, np.int8)), B, 2, 2)
+    assert ei.value.status == "FBDT_E_LABEL"
+    w = np.ones(n, np.float32)
+    w[3] = -1
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, dev(y), B, 2, 2, w=dev(w))
+    assert ei.value.status == "FBDT_E_WEIGHT"
+    w[3] = np.nan
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, dev(y), B, 2, 2, w=dev(w))
+    assert ei.value.status == "FBDT_E_WEIGHT"
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, dev(y), 8, 2, 2)                  # codes up to 15 with n_bins = 8
+    assert ei.value.status == "FBDT_E_INVAL"
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, dev(y), B, 8, 2)
+    assert ei.value.status == "FBDT_E_INVAL"
+    model = fb.fit(codes, dev(y), B, 2, 2)
+    small = fb.Codes.from_numpy(np.zeros((2, 10), np.uint8))
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.apply(model, small)
+    assert ei.value.status == "FBDT_E_SHAPE"
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.Model.from_arrays(np.array([[5]], np.uint8), np.array([[1]], np.uint8),
+                             np.zeros((1, 2)), 0.0, 3, 16)
+    assert ei.value.status == "FBDT_E_INVAL"
