@@ -104,8 +104,10 @@ hipEvent_t take_event() {
         g_event_pool.pop_back();
         return e;
     }
+    // timing-only events: no system-scope fence (no cache write-back and
+    // invalidate around the timed kernel)
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
 }
 
@@ -407,6 +409,9 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                                   (int)opt_hist_chunks.load(), (int)opt_hist_threads.load());
         partial_elems = std::max(partial_elems,
                                  (size_t)plans[l].chunks * ((size_t)1 << l) * d * n_bins * 2);
+        if (plans[l].lds_bytes + kHistStaticLdsReserve > di.max_lds)
+            return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", l,
+                        plans[l].lds_bytes, di.max_lds);
     }
     const int lblocks = leaf_blocks(n, di.cu_count);
     const int max_nodes = 1 << (D - 1);
@@ -639,6 +644,9 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     }
     ApplyShape as = plan_apply(n, m->n_features, T, D, di.cu_count, di.max_lds,
                                (int)opt_apply_threads.load());
+    if (as.lds_bytes > di.max_lds)
+        return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
+                    "apply_threads)", as.lds_bytes, di.max_lds);
     Timed tm(FBDT_K_APPLY, s, (double)n * (m->n_features + 4));
     HIP_TRY(launch_apply(as, xb, ldb, n, cuts, leaves, T, D, m->f0, prob, score, s));
     tm.done();
@@ -676,6 +684,9 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     HistShape hs = plan_histogram(n, d, n_bins, layer, di.cu_count, di.max_lds,
                                   (int)opt_hist_fpg.load(), (int)opt_hist_chunks.load(),
                                   (int)opt_hist_threads.load());
+    if (hs.lds_bytes + kHistStaticLdsReserve > di.max_lds)
+        return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", layer,
+                    hs.lds_bytes, di.max_lds);
     const size_t count = ((size_t)1 << layer) * d * n_bins * 2;
     Arena &a = g_arena[dev];
     std::lock_guard<std::mutex> lk(a.mu);

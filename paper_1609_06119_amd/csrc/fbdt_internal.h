@@ -54,6 +54,9 @@ struct FitBuffers {
 
 constexpr int kXcds = 8;            // gfx950: 8 XCDs, workgroups dispatched round-robin
 constexpr int kValidateBlocks = 256;
+// LDS kept aside for a kernel's static shared arrays when sizing its
+// dynamic LDS (the histogram kernel's cut table takes 128 bytes)
+constexpr size_t kHistStaticLdsReserve = 1024;
 
 hipError_t launch_fill_u32(void *p, uint32_t value, size_t count, hipStream_t s);
 

@@ -181,12 +181,22 @@ __global__ __launch_bounds__(256) void tree_prep_kernel(
 // H[node in h][feature in g][bin][class] in LDS as float64, adds every
 // sampled event of its event chunk with ds_add_f64, and writes its partial
 // histogram once at the end; best_cuts sums the chunk partials in a fixed
-// order.  Each thread handles 4 consecutive events per step: one float4 of
-// weights, one dword of node ids and one dword of bin codes per feature.
-// Routed mode computes each event's node of this layer from its parent
+// order.  Each thread handles 16 consecutive events per step: four float4
+// loads of weights, one 16-byte load of node ids and one 16-byte load of
+// codes per feature, all independent of each other.
+//
+// Routed mode computes every event's node of this layer from its parent
 // (layer - 1) and the parent's cut on the way; the first feature group
-// stores the new ids.
-template <bool ROUTED>
+// stores the new ids.  With NP > 0 (NP = number of parents) the code rows of
+// the parents' cut features are loaded for the same 16 events up front, so
+// routing costs no dependent load; with NP = 0 each event's routing code is
+// gathered after its parent id arrives (deep layers).
+__device__ __forceinline__ uint32_t byte_of(const uint4 &v, int e) {
+    const uint32_t w = e < 4 ? v.x : e < 8 ? v.y : e < 12 ? v.z : v.w;
+    return (w >> (8 * (e & 3))) & 0xffu;
+}
+
+template <bool ROUTED, int NP>
 __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
@@ -219,97 +229,124 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     for (int t = threadIdx.x; t < lds_n; t += blockDim.x) lds[t] = 0.0;
     if (ROUTED && layer >= 1)
         for (int t = threadIdx.x; t < half; t += blockDim.x) {
-            s_cf[t] = cut_f[t];
+            s_cf[t] = cut_f[t] < d ? cut_f[t] : 0;
             s_cc[t] = cut_c[t];
         }
     __syncthreads();
+    int eflag = 0;
+    if (ROUTED && layer >= 1 && threadIdx.x < half && cut_f[threadIdx.x] >= d) eflag |= kErrRoute;
 
     const int64_t start = (int64_t)p * chunk_events;
     const int64_t end = min(n, start + chunk_events);
     const bool writer = ROUTED && layer >= 1 && g == 0 && h == 0 && node_out != nullptr;
-    int eflag = 0;
 
-    for (int64_t i0 = start + 4 * (int64_t)threadIdx.x; i0 < end; i0 += 4 * (int64_t)blockDim.x) {
-        const bool full = i0 + 4 <= n;
-        float wv[4];
-        int nd[4];
+    for (int64_t i0 = start + 16 * (int64_t)threadIdx.x; i0 < end;
+         i0 += 16 * (int64_t)blockDim.x) {
+        const bool full = i0 + 16 <= n;
+        float wv[16];
         if (full) {
-            const float4 t4 = *reinterpret_cast<const float4 *>(w + i0);
-            wv[0] = t4.x; wv[1] = t4.y; wv[2] = t4.z; wv[3] = t4.w;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const float4 t4 = reinterpret_cast<const float4 *>(w + i0)[q4];
+                wv[4 * q4] = t4.x;
+                wv[4 * q4 + 1] = t4.y;
+                wv[4 * q4 + 2] = t4.z;
+                wv[4 * q4 + 3] = t4.w;
+            }
         } else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) wv[e] = (i0 + e < n) ? w[i0 + e] : 0.0f;
+            for (int e = 0; e < 16; ++e) wv[e] = (i0 + e < n) ? w[i0 + e] : 0.0f;
         }
+        // node ids of this layer, one byte per event
+        uint4 nd;
         if (!ROUTED) {
             if (full) {
-                const uint32_t t4 = *reinterpret_cast<const uint32_t *>(node_in + i0);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) nd[e] = (t4 >> (8 * e)) & 0xff;
+                nd = *reinterpret_cast<const uint4 *>(node_in + i0);
             } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) nd[e] = (i0 + e < n) ? node_in[i0 + e] : 0;
+                uint32_t t4[4] = {0, 0, 0, 0};
+                for (int e = 0; e < 16; ++e)
+                    if (i0 + e < n) t4[e >> 2] |= (uint32_t)node_in[i0 + e] << (8 * (e & 3));
+                nd = make_uint4(t4[0], t4[1], t4[2], t4[3]);
             }
         } else if (layer == 0) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) nd[e] = 1;
+            nd = make_uint4(0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u);
         } else {
-            int par[4];
+            uint4 par;
             if (layer == 1) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) par[e] = 1;
+                par = make_uint4(0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u);
             } else if (full) {
-                const uint32_t t4 = *reinterpret_cast<const uint32_t *>(node_in + i0);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) par[e] = (t4 >> (8 * e)) & 0xff;
+                par = *reinterpret_cast<const uint4 *>(node_in + i0);
             } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) par[e] = (i0 + e < n) ? node_in[i0 + e] : half;
+                uint32_t t4[4];
+                for (int k4 = 0; k4 < 4; ++k4) t4[k4] = (uint32_t)half * 0x01010101u;
+                for (int e = 0; e < 16; ++e)
+                    if (i0 + e < n)
+                        t4[e >> 2] = (t4[e >> 2] & ~(0xffu << (8 * (e & 3)))) |
+                                     ((uint32_t)node_in[i0 + e] << (8 * (e & 3)));
+                par = make_uint4(t4[0], t4[1], t4[2], t4[3]);
             }
+            uint4 rows[NP > 0 ? NP : 1];
+            if (NP > 0) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                unsigned k = (unsigned)(par[e] - half);
+                for (int kk = 0; kk < NP; ++kk)   // i0 + 15 < ldb: in bounds
+                    rows[kk] = *reinterpret_cast<const uint4 *>(
+                        xb + (int64_t)min((int)s_cf[kk], d - 1) * ldb + i0);
+            }
+            uint32_t o4[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                int pe = (int)byte_of(par, e);
+                unsigned k = (unsigned)(pe - half);
                 if (k >= (unsigned)half) {  // unreachable for ids written by this library
                     eflag |= kErrRoute;
                     k = 0;
-                    par[e] = half;
+                    pe = half;
                 }
-                int f = s_cf[k];
-                if (f >= d) {
-                    eflag |= kErrRoute;
-                    f = 0;
+                uint32_t code;
+                if (NP > 0) {
+                    code = byte_of(rows[0], e);
+#pragma unroll
+                    for (int kk = 1; kk < NP; ++kk)
+                        if (k == (unsigned)kk) code = byte_of(rows[kk], e);
+                } else {
+                    code = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i0 + e];
                 }
-                const uint8_t x = xb[(int64_t)f * ldb + i0 + e];  // i0 + e < ldb
-                nd[e] = 2 * par[e] + (x >= s_cc[k] ? 1 : 0);
+                const uint32_t ne = 2u * (uint32_t)pe + (code >= s_cc[k] ? 1u : 0u);
+                o4[e >> 2] |= ne << (8 * (e & 3));
             }
+            nd = make_uint4(o4[0], o4[1], o4[2], o4[3]);
             if (writer) {
                 if (full) {
-                    const uint32_t packed = (uint32_t)nd[0] | ((uint32_t)nd[1] << 8) |
-                                            ((uint32_t)nd[2] << 16) | ((uint32_t)nd[3] << 24);
-                    *reinterpret_cast<uint32_t *>(node_out + i0) = packed;
+                    *reinterpret_cast<uint4 *>(node_out + i0) = nd;
                 } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (i0 + e < n) node_out[i0 + e] = (uint8_t)nd[e];
+                    for (int e = 0; e < 16; ++e)
+                        if (i0 + e < n) node_out[i0 + e] = (uint8_t)byte_of(nd, e);
                 }
             }
         }
-        for (int f = 0; f < nf; ++f) {
-            const uint32_t xv =
-                *reinterpret_cast<const uint32_t *>(xb + (int64_t)(j0 + f) * ldb + i0);
+        // per event: LDS offset of its (node, class) block and |w| as float64;
+        // events outside this group's nodes or unsampled get base < 0
+        int base[16];
+        double aw[16];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (wv[e] != 0.0f) {
-                    const unsigned loc = (unsigned)(nd[e] - nodes - k0);
-                    const unsigned bin = (xv >> (8 * e)) & 0xffu;
-                    if (bin >= (unsigned)nbins) {
-                        eflag |= kErrBin;
-                    } else if (loc < (unsigned)nk) {
-                        const int idx = (((int)loc * fpg + f) * nbins + (int)bin) * 2 +
-                                        (wv[e] < 0.0f ? 1 : 0);
-                        atomicAdd(&lds[idx], (double)fabsf(wv[e]));
-                    }
-                }
+        for (int e = 0; e < 16; ++e) {
+            const unsigned loc = byte_of(nd, e) - (unsigned)(nodes + k0);
+            const bool take = wv[e] != 0.0f && loc < (unsigned)nk;
+            base[e] = take ? (int)loc * fpg * nbins * 2 + (wv[e] < 0.0f ? 1 : 0) : -1;
+            aw[e] = (double)fabsf(wv[e]);
+        }
+        for (int f = 0; f < nf; ++f) {
+            const uint4 xv = *reinterpret_cast<const uint4 *>(xb + (int64_t)(j0 + f) * ldb + i0);
+            const int fofs = f * nbins * 2;
+            unsigned bad = 0;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const unsigned bin = byte_of(xv, e);
+                const bool oor = bin >= (unsigned)nbins;
+                bad |= (oor && base[e] >= 0) ? 1u : 0u;
+                if (base[e] >= 0 && !oor) atomicAdd(&lds[base[e] + fofs + 2 * (int)bin], aw[e]);
             }
+            if (bad) eflag |= kErrBin;
         }
     }
     __syncthreads();
@@ -356,9 +393,12 @@ __global__ __launch_bounds__(256) void best_cuts_kernel(
     double *__restrict__ cand_gain, int *__restrict__ cand_cut, unsigned *__restrict__ ticket,
     uint8_t *__restrict__ out_f, uint8_t *__restrict__ out_c, double *__restrict__ out_g) {
 #pragma clang fp contract(off)
+    // one workgroup of 4 wavefronts per (node, feature); wavefront w sums the
+    // chunk partials w, w + 4, ...; wavefront 0 adds the four sums in order
+    __shared__ double red[4][kWave][8];
     const int lane = threadIdx.x % kWave;
-    const int pair = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    if (pair >= nodes * d) return;
+    const int wave = threadIdx.x / kWave;
+    const int pair = blockIdx.x;
     const int k = pair / d;
     const int j = pair - k * d;
 
@@ -368,24 +408,47 @@ __global__ __launch_bounds__(256) void best_cuts_kernel(
         const size_t stride_p = (size_t)nodes * d * nbins * 2;
         const double *base = partial + ((size_t)k * d + j) * nbins * 2 + 2 * b0;
         const int nb = min(4, nbins - b0);
-        for (int p = 0; p < chunks; ++p) {
-            const double *src = base + (size_t)p * stride_p;
-            if (nb == 4) {
-                const double2 a0 = reinterpret_cast<const double2 *>(src)[0];
-                const double2 a1 = reinterpret_cast<const double2 *>(src)[1];
-                const double2 a2 = reinterpret_cast<const double2 *>(src)[2];
-                const double2 a3 = reinterpret_cast<const double2 *>(src)[3];
-                hs[0] += a0.x; hb[0] += a0.y;
-                hs[1] += a1.x; hb[1] += a1.y;
-                hs[2] += a2.x; hb[2] += a2.y;
-                hs[3] += a3.x; hb[3] += a3.y;
-            } else {
+        if (nb == 4) {
+            int p = wave;
+            for (; p + 4 < chunks; p += 8) {   // two chunks per step, loads issued together
+                const double2 *s0 = reinterpret_cast<const double2 *>(base + (size_t)p * stride_p);
+                const double2 *s1 =
+                    reinterpret_cast<const double2 *>(base + (size_t)(p + 4) * stride_p);
+                const double2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
+                const double2 c0 = s1[0], c1 = s1[1], c2 = s1[2], c3 = s1[3];
+                hs[0] += a0.x; hb[0] += a0.y; hs[1] += a1.x; hb[1] += a1.y;
+                hs[2] += a2.x; hb[2] += a2.y; hs[3] += a3.x; hb[3] += a3.y;
+                hs[0] += c0.x; hb[0] += c0.y; hs[1] += c1.x; hb[1] += c1.y;
+                hs[2] += c2.x; hb[2] += c2.y; hs[3] += c3.x; hb[3] += c3.y;
+            }
+            if (p < chunks) {
+                const double2 *s0 = reinterpret_cast<const double2 *>(base + (size_t)p * stride_p);
+                const double2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
+                hs[0] += a0.x; hb[0] += a0.y; hs[1] += a1.x; hb[1] += a1.y;
+                hs[2] += a2.x; hb[2] += a2.y; hs[3] += a3.x; hb[3] += a3.y;
+            }
+        } else {
+            for (int p = wave; p < chunks; p += 4) {
+                const double *src = base + (size_t)p * stride_p;
                 for (int e = 0; e < nb; ++e) {
                     hs[e] += src[2 * e];
                     hb[e] += src[2 * e + 1];
                 }
             }
         }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        red[wave][lane][e] = hs[e];
+        red[wave][lane][4 + e] = hb[e];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        hs[e] = ((red[0][lane][e] + red[1][lane][e]) + red[2][lane][e]) + red[3][lane][e];
+        hb[e] = ((red[0][lane][4 + e] + red[1][lane][4 + e]) + red[2][lane][4 + e]) +
+                red[3][lane][4 + e];
     }
     bool ne[4];
     int first = 0x7fffffff, last = -1;
@@ -505,11 +568,20 @@ __global__ __launch_bounds__(256) void best_cuts_kernel(
 
 // ---------------------------------------------------------------------------
 // Terminal boost weights (section 1.3): per leaf, sum(v y~) and
-// sum(v |y~| (2 - |y~|)) over the sampled events, in LDS per workgroup; the
-// last workgroup sums the workgroup partials in block order and writes
-// eta * num / den (0 when den = 0).  Routed mode first sends every event
-// from layer depth-1 to its leaf and stores the leaf id.
-template <bool ROUTED>
+// sum(v |y~| (2 - |y~|)) over the sampled events.  With NL > 0 leaves every
+// thread keeps the 2 NL sums in registers, then a wavefront reduction and an
+// in-order sum over wavefronts give the workgroup's partial (no atomics, a
+// fixed order); with NL = 0 (deep trees) threads add into LDS accumulators.
+// The last workgroup to finish sums the workgroup partials (all threads,
+// fixed order) and writes eta * num / den (0 when den = 0).  Routed mode
+// first sends every event from layer depth-1 to its leaf and stores it.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+template <bool ROUTED, int NL>
 __global__ __launch_bounds__(256) void leaf_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
@@ -519,11 +591,16 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     unsigned *__restrict__ ticket, double *__restrict__ leaf_out, int *__restrict__ err) {
 #pragma clang fp contract(off)
     __shared__ double acc[2 * 128];
+    __shared__ double red[256];
     __shared__ uint8_t s_cf[64], s_cc[64];
     __shared__ unsigned s_last;
     const int nleaf = 1 << depth;
     const int half = nleaf >> 1;
-    for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x) acc[t] = 0.0;
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    const int nwaves = blockDim.x / kWave;
+    if (NL == 0)
+        for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x) acc[t] = 0.0;
     if (ROUTED)
         for (int t = threadIdx.x; t < half; t += blockDim.x) {
             s_cf[t] = cut_f[t];
@@ -531,6 +608,9 @@ __global__ __launch_bounds__(256) void leaf_kernel(
         }
     __syncthreads();
     int eflag = 0;
+    double an[NL > 0 ? NL : 1], ad[NL > 0 ? NL : 1];
+#pragma unroll
+    for (int l = 0; l < (NL > 0 ? NL : 1); ++l) an[l] = ad[l] = 0.0;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
         int leaf;
@@ -557,19 +637,47 @@ __global__ __launch_bounds__(256) void leaf_kernel(
                 continue;
             }
         }
-        if (in_subsample(seed, tree, n, i, alpha)) {
-            const double yf = (double)y[i];
-            const double yt = pseudo_response(yf, F[i]);
-            const double vi = v ? (double)v[i] : 1.0;
-            const double a = fabs(yt);
-            const int li = leaf - nleaf;
-            atomicAdd(&acc[2 * li], vi * yt);
-            atomicAdd(&acc[2 * li + 1], vi * a * (2.0 - a));
+        if (!in_subsample(seed, tree, n, i, alpha)) continue;
+        const double yf = (double)y[i];
+        const double yt = pseudo_response(yf, F[i]);
+        const double vi = v ? (double)v[i] : 1.0;
+        const double a = fabs(yt);
+        const double gnum = vi * yt;
+        const double gden = vi * a * (2.0 - a);
+        const int li = leaf - nleaf;
+        if (NL > 0) {
+#pragma unroll
+            for (int l = 0; l < (NL > 0 ? NL : 1); ++l) {
+                an[l] += li == l ? gnum : 0.0;
+                ad[l] += li == l ? gden : 0.0;
+            }
+        } else {
+            atomicAdd(&acc[2 * li], gnum);
+            atomicAdd(&acc[2 * li + 1], gden);
         }
     }
-    __syncthreads();
-    for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x)
-        leaf_partial[(size_t)blockIdx.x * 2 * nleaf + t] = acc[t];
+    if (NL > 0) {
+        // red[wave][2 NL] (2 NL * nwaves <= 256 doubles for NL <= 16, 256 threads)
+#pragma unroll
+        for (int l = 0; l < (NL > 0 ? NL : 1); ++l) {
+            const double sn = wave_sum(an[l]);
+            const double sd = wave_sum(ad[l]);
+            if (lane == 0) {
+                red[wave * 2 * NL + 2 * l] = sn;
+                red[wave * 2 * NL + 2 * l + 1] = sd;
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x < 2 * NL) {
+            double sum = 0.0;
+            for (int wv = 0; wv < nwaves; ++wv) sum += red[wv * 2 * NL + threadIdx.x];
+            leaf_partial[(size_t)blockIdx.x * 2 * nleaf + threadIdx.x] = sum;
+        }
+    } else {
+        __syncthreads();
+        for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x)
+            leaf_partial[(size_t)blockIdx.x * 2 * nleaf + t] = acc[t];
+    }
     if (eflag) atomicOr(err, eflag);
     __threadfence();
     __syncthreads();
@@ -577,15 +685,28 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     __syncthreads();
     if (!s_last) return;
     __threadfence();
-    for (int t = threadIdx.x; t < nleaf; t += blockDim.x) {
+    // the last workgroup: thread t sums value t % nv over blocks t / nv,
+    // t / nv + stripes, ...; then the stripes are added in order
+    const int nv = 2 * nleaf;
+    const int stripes = blockDim.x / nv;
+    const int t = threadIdx.x;
+    if (t < stripes * nv) {
+        const int val = t % nv, st = t / nv;
+        double sum = 0.0;
+        for (unsigned b = st; b < gridDim.x; b += stripes)
+            sum += leaf_partial[(size_t)b * nv + val];
+        red[t] = sum;
+    }
+    __syncthreads();
+    if (t < nleaf) {
         double num = 0.0, den = 0.0;
-        for (unsigned b = 0; b < gridDim.x; ++b) {
-            num += load_agent(&leaf_partial[(size_t)b * 2 * nleaf + 2 * t]);
-            den += load_agent(&leaf_partial[(size_t)b * 2 * nleaf + 2 * t + 1]);
+        for (int st = 0; st < stripes; ++st) {
+            num += red[st * nv + 2 * t];
+            den += red[st * nv + 2 * t + 1];
         }
         leaf_out[t] = den == 0.0 ? 0.0 : eta * (num / den);
     }
-    if (threadIdx.x == 0) *ticket = 0u;
+    if (t == 0) *ticket = 0u;
 }
 
 // node <- 2 node + [xb[f][i] >= c] with (f, c) the cut of the node.
@@ -722,7 +843,7 @@ int grid_for(int64_t n, int threads, int cap) {
 // a launch beyond the device limit then fails and reports its own error.
 template <typename K>
 void allow_lds(K kernel, size_t bytes) {
-    if (bytes <= 65536) return;
+    if (bytes + kHistStaticLdsReserve <= 65536) return;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess) (void)hipGetLastError();
@@ -764,25 +885,57 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
     HistShape hs{};
     const int nodes = 1 << layer;
     const size_t per_node_feature = (size_t)n_bins * 2 * sizeof(double);
+    // the kernel's static LDS (cut table) shares the workgroup's LDS limit
+    max_lds = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
     int npg = (int)(max_lds / per_node_feature);
     if (npg < 1) npg = 1;
     if (npg > nodes) npg = nodes;
     hs.nodes_per_group = npg;
     hs.node_groups = (nodes + npg - 1) / npg;
-    int f = fpg > 0 ? fpg : 1;
-    if (f > d) f = d;
+    // Features per workgroup.  Estimated time of a launch shape, with about
+    // one workgroup per CU: every feature group re-reads the chunk's node
+    // ids and weights (5 bytes per event, mostly from L2), every event chunk
+    // writes one partial histogram that best_cuts reads again, and the LDS
+    // atomics of a workgroup run at a few per clock per CU.
+    const int t_threads = threads > 0 ? threads : (n >= (1 << 20) ? 1024 : 512);
+    int f;
+    if (fpg > 0) {
+        f = fpg < d ? fpg : d;
+    } else {
+        const double hbytes = (double)nodes * d * per_node_feature;
+        const double cmax = (double)n / (16.0 * t_threads);
+        double best = -1.0;
+        f = 1;
+        for (int cand = 1; cand <= d; ++cand) {
+            if ((size_t)npg * cand * per_node_feature > max_lds) break;
+            const int g = ((d + cand - 1) / cand) * ((nodes + npg - 1) / npg);
+            double c = (double)cu_count / g;
+            if (c > cmax) c = cmax;
+            if (c < 1.0) c = 1.0;
+            const double wgs = c * g < cu_count ? c * g : (double)cu_count;
+            const double mem = ((double)n * d + 5.0 * n * g + 2.0 * c * hbytes) / 5.0e12;
+            const double atom = 0.5 * n * d / (wgs * 2.0 * 2.4e9);
+            const double cost = mem > atom ? mem : atom;
+            if (best < 0.0 || cost < best) {
+                best = cost;
+                f = cand;
+            }
+        }
+    }
     while (f > 1 && (size_t)npg * f * per_node_feature > max_lds) --f;
     hs.features_per_group = f;
     hs.feature_groups = (d + f - 1) / f;
-    hs.threads = threads > 0 ? threads : 256;
+    hs.threads = t_threads;
     const int groups = hs.feature_groups * hs.node_groups;
-    int64_t c = chunks > 0 ? chunks : (2 * (int64_t)cu_count + groups - 1) / groups;
-    const int64_t min_events = 4LL * hs.threads;
+    // one workgroup per CU by default: every extra event chunk adds one more
+    // partial histogram to write and to sum
+    int64_t c = chunks > 0 ? chunks : ((int64_t)cu_count + groups - 1) / groups;
+    const int64_t min_events = 16LL * hs.threads;
     const int64_t cmax = (n + min_events - 1) / min_events;
-    if (c > cmax) c = cmax;
+    if (chunks <= 0 && c > cmax) c = cmax;
     if (c < 1) c = 1;
     int64_t ce = (n + c - 1) / c;
-    ce = (ce + 3) & ~(int64_t)3;
+    ce = (ce + 15) & ~(int64_t)15;
     hs.chunk_events = ce;
     hs.chunks = (int)((n + ce - 1) / ce);
     const int64_t work = (int64_t)hs.chunks * groups;
@@ -791,24 +944,42 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
     return hs;
 }
 
+template <bool ROUTED, int NP>
+hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
+                          int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
+                          const uint8_t *cut_f, const uint8_t *cut_c, int layer, double *partial,
+                          int *err, hipStream_t s) {
+    allow_lds(hist_kernel<ROUTED, NP>, hs.lds_bytes);
+    hist_kernel<ROUTED, NP><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+        xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f, cut_c, layer, hs.features_per_group,
+        hs.feature_groups, hs.nodes_per_group, hs.node_groups, hs.chunks, hs.chunk_events,
+        partial, err);
+    return hipGetLastError();
+}
+
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                             const float *w, const uint8_t *cut_f, const uint8_t *cut_c,
                             int layer, bool routed, double *partial, int *err, hipStream_t s) {
-    if (routed) {
-        allow_lds(hist_kernel<true>, hs.lds_bytes);
-        hist_kernel<true><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
-            xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f, cut_c, layer,
-            hs.features_per_group, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
-            hs.chunks, hs.chunk_events, partial, err);
-    } else {
-        allow_lds(hist_kernel<false>, hs.lds_bytes);
-        hist_kernel<false><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
-            xb, ldb, n, d, n_bins, node_in, nullptr, w, nullptr, nullptr, layer,
-            hs.features_per_group, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
-            hs.chunks, hs.chunk_events, partial, err);
+    if (!routed)
+        return launch_hist_np<false, 0>(hs, xb, ldb, n, d, n_bins, node_in, nullptr, w, nullptr,
+                                        nullptr, layer, partial, err, s);
+    const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
+    switch (parents) {
+    case 0:
+    case 1:
+        return launch_hist_np<true, 1>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
+                                       cut_c, layer, partial, err, s);
+    case 2:
+        return launch_hist_np<true, 2>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
+                                       cut_c, layer, partial, err, s);
+    case 4:
+        return launch_hist_np<true, 4>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
+                                       cut_c, layer, partial, err, s);
+    default:
+        return launch_hist_np<true, 0>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
+                                       cut_c, layer, partial, err, s);
     }
-    return hipGetLastError();
 }
 
 hipError_t launch_merge_partials(const double *partial, int chunks, size_t count, double *out,
@@ -821,15 +992,43 @@ hipError_t launch_merge_partials(const double *partial, int chunks, size_t count
 hipError_t launch_best_cuts(const double *partial, int chunks, int n_nodes, int d, int n_bins,
                             double *cand_gain, int *cand_cut, unsigned *ticket, uint8_t *out_f,
                             uint8_t *out_c, double *out_g, hipStream_t s) {
-    const int waves_per_block = 4;
-    const int pairs = n_nodes * d;
-    const int blocks = (pairs + waves_per_block - 1) / waves_per_block;
-    best_cuts_kernel<<<blocks, waves_per_block * kWave, 0, s>>>(
-        partial, chunks, n_nodes, d, n_bins, cand_gain, cand_cut, ticket, out_f, out_c, out_g);
+    best_cuts_kernel<<<n_nodes * d, 4 * kWave, 0, s>>>(partial, chunks, n_nodes, d, n_bins,
+                                                       cand_gain, cand_cut, ticket, out_f, out_c,
+                                                       out_g);
     return hipGetLastError();
 }
 
 int leaf_blocks(int64_t n, int cu_count) { return grid_for(n, 256, 2 * cu_count); }
+
+template <bool ROUTED, int NL>
+void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
+             const uint8_t *node_in, uint8_t *node_out, const uint8_t *cut_f,
+             const uint8_t *cut_c, int depth, const int8_t *y, const float *v, const double *F,
+             uint64_t seed, int tree, double alpha, double eta, double *leaf_partial,
+             unsigned *ticket, double *leaf_out, int *err) {
+    leaf_kernel<ROUTED, NL><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, node_out, cut_f,
+                                                   cut_c, depth, y, v, F, seed, tree, alpha, eta,
+                                                   leaf_partial, ticket, leaf_out, err);
+}
+
+template <bool ROUTED>
+void leaf_dispatch(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
+                   const uint8_t *node_in, uint8_t *node_out, const uint8_t *cut_f,
+                   const uint8_t *cut_c, int depth, const int8_t *y, const float *v,
+                   const double *F, uint64_t seed, int tree, double alpha, double eta,
+                   double *leaf_partial, unsigned *ticket, double *leaf_out, int *err) {
+#define FBDT_LEAF_CASE(NLV)                                                                      \
+    leaf_go<ROUTED, NLV>(blocks, s, xb, ldb, n, d, node_in, node_out, cut_f, cut_c, depth, y, v, \
+                         F, seed, tree, alpha, eta, leaf_partial, ticket, leaf_out, err)
+    switch (depth) {
+    case 1: FBDT_LEAF_CASE(2); break;
+    case 2: FBDT_LEAF_CASE(4); break;
+    case 3: FBDT_LEAF_CASE(8); break;
+    case 4: FBDT_LEAF_CASE(16); break;
+    default: FBDT_LEAF_CASE(0); break;
+    }
+#undef FBDT_LEAF_CASE
+}
 
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
                        uint8_t *node_out, const uint8_t *cut_f, const uint8_t *cut_c, int depth,
@@ -838,13 +1037,12 @@ hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const u
                        double *leaf_partial, unsigned *ticket, double *leaf_out, int *err,
                        hipStream_t s) {
     if (routed)
-        leaf_kernel<true><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, node_out, cut_f, cut_c,
-                                                 depth, y, v, F, seed, tree, alpha, eta,
-                                                 leaf_partial, ticket, leaf_out, err);
+        leaf_dispatch<true>(blocks, s, xb, ldb, n, d, node_in, node_out, cut_f, cut_c, depth, y,
+                            v, F, seed, tree, alpha, eta, leaf_partial, ticket, leaf_out, err);
     else
-        leaf_kernel<false><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, nullptr, nullptr,
-                                                  nullptr, depth, y, v, F, seed, tree, alpha,
-                                                  eta, leaf_partial, ticket, leaf_out, err);
+        leaf_dispatch<false>(blocks, s, xb, ldb, n, d, node_in, nullptr, nullptr, nullptr, depth,
+                             y, v, F, seed, tree, alpha, eta, leaf_partial, ticket, leaf_out,
+                             err);
     return hipGetLastError();
 }
 
