@@ -425,13 +425,15 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.node[0], npad);
     cv.add(&fb.node[1], npad);
     cv.add(&fb.partial, partial_elems);
+    const size_t small_elems = (size_t)max_nodes * d * n_bins * 2;
+    cv.add(&fb.small, small_elems);
     cv.add(&fb.cand_gain, (size_t)max_nodes * d);
     cv.add(&fb.cand_cut, (size_t)max_nodes * d);
     cv.add(&fb.node_ticket, max_nodes);
     cv.add(&fb.leaf_partial, (size_t)lblocks * 2 * nleaf);
     cv.add(&fb.leaf_ticket, 1);
     cv.add(&fb.class_partial, 2 * kValidateBlocks);
-    cv.add(&fb.f0, 1);
+    cv.add(&fb.f0, 2);
     cv.add(&fb.err, 1);
     cv.add(&fb.cut_feature, (size_t)T * nin);
     cv.add(&fb.cut_bin, (size_t)T * nin);
@@ -443,13 +445,19 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     HIP_TRY(launch_fill_u32(fb.node_ticket, 0u, max_nodes, s));
     HIP_TRY(launch_fill_u32(fb.leaf_ticket, 0u, 1, s));
     HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
+    HIP_TRY(launch_fill_u32(fb.small, 0u, 2 * small_elems, s));
     HIP_TRY(launch_validate(y, w, n, fb.class_partial, fb.err, s));
     HIP_TRY(launch_initial_score(fb.class_partial, fb.f0, fb.err, s));
     int h_err = 0;
+    double h_f0[2] = {0.0, 0.0};
+    HIP_TRY(hipMemcpyAsync(h_f0, fb.f0, sizeof h_f0, hipMemcpyDeviceToHost, s));
     if ((rc = read_err(fb.err, s, &h_err))) return rc;
     if (h_err & kErrLabel) return fail(FBDT_E_LABEL, "labels must be +1 or -1");
     if (h_err & kErrWeight) return fail(FBDT_E_WEIGHT, "weights must be finite and >= 0");
     if (h_err & kErrClass) return fail(FBDT_E_LABEL, "a class has zero total weight");
+    // every histogram weight is fl32(v |y~|) < 2 v (1 + 2^-24): twice the
+    // total event weight bounds every bin total
+    const int scale = histogram_scale(2.0 * h_f0[1] * (1.0 + 1e-6));
 
     const uint64_t seed = p->seed;
     const double alpha = p->subsample, eta = p->shrinkage;
@@ -473,14 +481,15 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
                                          l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
                                          l >= 1 ? fb.node[l & 1] : nullptr, fb.w, cf + plo,
-                                         cc + plo, l, true, fb.partial, fb.err, s));
+                                         cc + plo, l, true, scale, fb.partial, fb.small, fb.err,
+                                         s));
                 tm.done();
             }
             {
                 Timed tm(FBDT_K_BEST_CUTS, s);
-                HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, 1 << l, d, n_bins,
-                                         fb.cand_gain, fb.cand_cut, fb.node_ticket, cf + lo,
-                                         cc + lo, cg + lo, s));
+                HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, scale, fb.small, nullptr,
+                                         1 << l, d, n_bins, fb.cand_gain, fb.cand_cut,
+                                         fb.node_ticket, cf + lo, cc + lo, cg + lo, s));
                 tm.done();
             }
         }
@@ -691,20 +700,31 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     Arena &a = g_arena[dev];
     std::lock_guard<std::mutex> lk(a.mu);
     Carver cv;
-    double *partial;
+    uint64_t *partial;
+    double *small, *bpart, *wsum;
     int *err;
     cv.add(&partial, (size_t)hs.chunks * count);
+    cv.add(&small, count);
+    cv.add(&bpart, kValidateBlocks);
+    cv.add(&wsum, 1);
     cv.add(&err, 1);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     HIP_TRY(launch_fill_u32(err, 0u, 1, s));
+    HIP_TRY(launch_fill_u32(small, 0u, 2 * count, s));
+    HIP_TRY(launch_abs_sum(w, n, bpart, wsum, s));
+    double h_wsum = 0.0;
+    HIP_TRY(hipMemcpyAsync(&h_wsum, wsum, sizeof h_wsum, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (!std::isfinite(h_wsum)) return fail(FBDT_E_WEIGHT, "weights must be finite");
+    const int scale = histogram_scale(h_wsum * (1.0 + 1e-6));
     {
         Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, layer, false));
         HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node, nullptr, w, nullptr, nullptr,
-                                 layer, false, partial, err, s));
+                                 layer, false, scale, partial, small, err, s));
         tm.done();
     }
-    HIP_TRY(launch_merge_partials(partial, hs.chunks, count, hist, s));
+    HIP_TRY(launch_merge_partials(partial, hs.chunks, count, scale, small, hist, s));
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;
     if (h_err & kErrBin) return fail(FBDT_E_INVAL, "a bin code is >= n_bins");
@@ -737,8 +757,8 @@ int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bin
     cv.assign(a.ptr);
     HIP_TRY(launch_fill_u32(tk, 0u, n_nodes, s));
     Timed tm(FBDT_K_BEST_CUTS, s);
-    HIP_TRY(launch_best_cuts(hist, 1, n_nodes, d, n_bins, cg, cc, tk, cut_feature, cut_bin, gain,
-                             s));
+    HIP_TRY(launch_best_cuts(nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cg, cc, tk,
+                             cut_feature, cut_bin, gain, s));
     tm.done();
     HIP_TRY(hipStreamSynchronize(s));
     return FBDT_OK;

@@ -37,14 +37,15 @@ struct FitBuffers {
     double *F;            // [npad] score
     float *w;             // [npad] signed re-weighted sample
     uint8_t *node[2];     // [npad] node ids, double-buffered across layers
-    double *partial;      // histogram partials [chunks][nodes][d][B][2]
+    uint64_t *partial;    // fixed-point histogram partials [chunks][nodes][d][B][2]
+    double *small;        // float64 histogram of the weights below the fixed-point grid
     double *cand_gain;    // [max nodes][d]
     int *cand_cut;        // [max nodes][d]
     unsigned *node_ticket;  // [max nodes]
     double *leaf_partial;   // [leaf blocks][2^D][2]
     unsigned *leaf_ticket;  // [1]
     double *class_partial;  // [validate blocks][2]
-    double *f0;             // [1]
+    double *f0;             // [2]: initial score, total event weight
     int *err;               // [1]
     uint8_t *cut_feature;   // [T][2^D - 1]
     uint8_t *cut_bin;       // [T][2^D - 1]
@@ -57,6 +58,9 @@ constexpr int kValidateBlocks = 256;
 // LDS kept aside for a kernel's static shared arrays when sizing its
 // dynamic LDS (the histogram kernel's cut table takes 128 bytes)
 constexpr size_t kHistStaticLdsReserve = 1024;
+// dynamic LDS of the histogram kernel beyond the histogram itself: one
+// dummy and one out-of-range counter (8 bytes) per lane of a wavefront
+constexpr size_t kHistExtraLds = 2 * 64 * 8;
 
 hipError_t launch_fill_u32(void *p, uint32_t value, size_t count, hipStream_t s);
 
@@ -77,20 +81,38 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
 HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
                          size_t max_lds, int fpg, int chunks, int threads);
 
+// Fixed-point scale of the histogram sums: a weight w >= 2^(23 - scale) is
+// an exact multiple of 2^-scale and is added as the integer w * 2^scale;
+// smaller positive weights go to a float64 side histogram.  The scale is
+// chosen so that no bin total can reach 2^63: total_weight_bound * 2^scale
+// < 2^62.
+int histogram_scale(double total_weight_bound);
+
 // Histogram pass.  routed = true: node_in holds the ids of layer-1 (null for
 // layer <= 1, all events at the root), the pass routes them with the cuts of
 // layer-1 and (first feature group only) writes the layer's ids to node_out.
 // routed = false: node_in holds the ids of the layer itself.
+// partial: [chunks][2^layer][d][B][2] fixed-point sums; small: [2^layer][d][B][2]
+// float64 sums of the weights below the grid (accumulated into, not cleared).
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                             const float *w, const uint8_t *cut_f, const uint8_t *cut_c,
-                            int layer, bool routed, double *partial, int *err, hipStream_t s);
+                            int layer, bool routed, int scale, uint64_t *partial, double *small,
+                            int *err, hipStream_t s);
 
-// hist[i] = sum over chunks of partial[chunk][i], in chunk order.
-hipError_t launch_merge_partials(const double *partial, int chunks, size_t count, double *out,
-                                 hipStream_t s);
+// hist[i] = (sum over chunks of partial[chunk][i]) * 2^-scale + small[i].
+hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t count, int scale,
+                                 const double *small, double *out, hipStream_t s);
 
-hipError_t launch_best_cuts(const double *partial, int chunks, int n_nodes, int d, int n_bins,
+// Sum of |w| over n weights into *out (fixed order).
+hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, double *out,
+                          hipStream_t s);
+
+// Best cut of every node of a layer, from fixed-point chunk partials plus the
+// float64 side histogram (which it clears), or, with partial == null, from a
+// float64 histogram `hist`.
+hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
+                            const double *hist, int n_nodes, int d, int n_bins,
                             double *cand_gain, int *cand_cut, unsigned *ticket,
                             uint8_t *out_f, uint8_t *out_c, double *out_g, hipStream_t s);
 

@@ -136,7 +136,8 @@ __global__ __launch_bounds__(256) void initial_score_kernel(const double *__rest
         if (!(ts > 0.0 && tb > 0.0))
             atomicOr(err, kErrClass);
         else
-            *f0 = 0.5 * log(ts / tb);
+            f0[0] = 0.5 * log(ts / tb);
+        f0[1] = ts + tb;
     }
 }
 
@@ -202,8 +203,9 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const float *__restrict__ w, const uint8_t *__restrict__ cut_f,
     const uint8_t *__restrict__ cut_c, int layer, int fpg, int G, int npg, int NG, int chunks,
-    int64_t chunk_events, double *__restrict__ partial, int *__restrict__ err) {
-    extern __shared__ double lds[];
+    int64_t chunk_events, int scale, uint64_t *__restrict__ partial, double *__restrict__ small,
+    int *__restrict__ err) {
+    extern __shared__ uint64_t lds[];
     __shared__ uint8_t s_cf[64], s_cc[64];
 
     // Consecutive work items (same event chunk, different feature groups) go
@@ -225,8 +227,16 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const int k0 = h * npg;
     const int nk = min(npg, nodes - k0);
     const int lds_n = npg * fpg * nbins * 2;
+    const int lstride = fpg * nbins * 2;
+    // per-lane counters after the histogram: a dummy for events that add
+    // nothing, a "bad" one for out-of-range bin codes
+    const int lane = threadIdx.x % kWave;
+    const int dummy = lds_n + lane;
+    const int bad = lds_n + kWave + lane;
 
-    for (int t = threadIdx.x; t < lds_n; t += blockDim.x) lds[t] = 0.0;
+    for (int t = threadIdx.x; t < lds_n + 2 * kWave; t += blockDim.x) lds[t] = 0ull;
+    // weights at or above tau are exact multiples of 2^-scale
+    const float tau = ldexpf(1.0f, 23 - scale);
     if (ROUTED && layer >= 1)
         for (int t = threadIdx.x; t < half; t += blockDim.x) {
             s_cf[t] = cut_f[t] < d ? cut_f[t] : 0;
@@ -324,35 +334,60 @@ __global__ __launch_bounds__(1024) void hist_kernel(
                 }
             }
         }
-        // per event: LDS offset of its (node, class) block and |w| as float64;
-        // events outside this group's nodes or unsampled get base < 0
-        int base[16];
-        double aw[16];
+        // Sampled events of this group's nodes add w * 2^scale to their
+        // (node, feature, bin, class) counter; the integer is the float's
+        // 24-bit significand shifted into place, exact for w >= tau.  Other
+        // events (unsampled, outside this group's nodes) add 0 to a per-lane
+        // dummy counter and an out-of-range bin code adds to a per-lane
+        // "bad" counter, so the inner loop has no branch.  Rarer weights
+        // below the grid are flagged and added in float64 afterwards.
+        int slot[16];
+        uint64_t fx[16];
+        unsigned smallm = 0;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
             const unsigned loc = byte_of(nd, e) - (unsigned)(nodes + k0);
-            const bool take = wv[e] != 0.0f && loc < (unsigned)nk;
-            base[e] = take ? (int)loc * fpg * nbins * 2 + (wv[e] < 0.0f ? 1 : 0) : -1;
-            aw[e] = (double)fabsf(wv[e]);
+            const float a = fabsf(wv[e]);
+            const bool take = a != 0.0f && loc < (unsigned)nk;
+            const bool big = take && a >= tau;
+            const uint32_t bits = __float_as_uint(a);
+            const int sh = (int)(bits >> 23) - 150 + scale;
+            slot[e] = big ? (int)loc * lstride + (wv[e] < 0.0f ? 1 : 0) : dummy;
+            fx[e] = big ? (uint64_t)((bits & 0x7fffffu) | 0x800000u) << (sh > 0 ? sh : 0) : 0ull;
+            smallm |= (take && !big) ? 1u << e : 0u;
         }
         for (int f = 0; f < nf; ++f) {
             const uint4 xv = *reinterpret_cast<const uint4 *>(xb + (int64_t)(j0 + f) * ldb + i0);
             const int fofs = f * nbins * 2;
-            unsigned bad = 0;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const unsigned bin = byte_of(xv, e);
-                const bool oor = bin >= (unsigned)nbins;
-                bad |= (oor && base[e] >= 0) ? 1u : 0u;
-                if (base[e] >= 0 && !oor) atomicAdd(&lds[base[e] + fofs + 2 * (int)bin], aw[e]);
+                const int real = slot[e] + fofs + 2 * (int)bin;
+                const int idx = slot[e] == dummy ? dummy : (bin < (unsigned)nbins ? real : bad);
+                atomicAdd(&lds[idx], fx[e]);
             }
-            if (bad) eflag |= kErrBin;
+            unsigned sm = smallm;
+            while (sm) {  // rare: weights below the fixed-point grid
+                const int e = __ffs(sm) - 1;
+                sm &= sm - 1;
+                const float wi = w[i0 + e];
+                const unsigned loc = byte_of(nd, e) - (unsigned)(nodes + k0);
+                const unsigned bin = byte_of(xv, e);
+                if (bin >= (unsigned)nbins) {
+                    eflag |= kErrBin;
+                    continue;
+                }
+                const size_t gi = ((((size_t)(k0 + (int)loc) * d + j0 + f) * nbins + bin) * 2) +
+                                  (wi < 0.0f ? 1 : 0);
+                atomicAdd(&small[gi], (double)fabsf(wi));
+            }
         }
     }
     __syncthreads();
+    if (threadIdx.x < kWave && lds[lds_n + kWave + threadIdx.x] != 0ull) eflag |= kErrBin;
 
     const int per_nf = nbins * 2;
-    double *out = partial + (size_t)p * nodes * d * per_nf;
+    uint64_t *out = partial + (size_t)p * nodes * d * per_nf;
     for (int t = threadIdx.x; t < lds_n; t += blockDim.x) {
         const int k = t / (fpg * per_nf);
         const int rem = t - k * fpg * per_nf;
@@ -363,15 +398,45 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     if (eflag) atomicOr(err, eflag);
 }
 
-// Sum of chunk partials into one histogram (fixed order over chunks).
-__global__ __launch_bounds__(256) void merge_partials_kernel(const double *__restrict__ partial,
-                                                             int chunks, size_t count,
+// Sum of the fixed-point chunk partials (exact) converted to float64, plus
+// the float64 side histogram.
+__global__ __launch_bounds__(256) void merge_partials_kernel(const uint64_t *__restrict__ partial,
+                                                             int chunks, size_t count, int scale,
+                                                             const double *__restrict__ small,
                                                              double *__restrict__ out) {
     for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < count;
          i += (size_t)gridDim.x * blockDim.x) {
-        double s = 0.0;
+        uint64_t s = 0;
         for (int p = 0; p < chunks; ++p) s += partial[(size_t)p * count + i];
-        out[i] = s;
+        out[i] = ldexp((double)s, -scale) + small[i];
+    }
+}
+
+// Sum of |w| (fixed grid, fixed reduction order): per-block partials, then
+// one block adds them.
+__global__ __launch_bounds__(256) void abs_sum_kernel(const float *__restrict__ w, int64_t n,
+                                                      double *__restrict__ block_partial) {
+    double s = 0.0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        s += (double)fabsf(w[i]);
+    for (int off = kWave / 2; off > 0; off >>= 1) s += __shfl_down(s, off);
+    __shared__ double ws[256 / kWave];
+    if (threadIdx.x % kWave == 0) ws[threadIdx.x / kWave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t = 0.0;
+        for (int k = 0; k < (int)(blockDim.x / kWave); ++k) t += ws[k];
+        block_partial[blockIdx.x] = t;
+    }
+}
+
+__global__ void sum_blocks_kernel(const double *__restrict__ block_partial, int nblocks,
+                                  double *__restrict__ out) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) {
+        double t = 0.0;
+        for (int k = 0; k < nblocks; ++k) t += block_partial[k];
+        *out = t;
     }
 }
 
@@ -388,67 +453,77 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(const double *__res
 // with exact zero sums); a cut c >= 2 whose bin c-1 is empty makes the same
 // partition as cut c-1, has the same gain in exact arithmetic, and is
 // skipped so that the lower cut wins the tie independently of rounding.
+template <bool FIXED>
 __global__ __launch_bounds__(256) void best_cuts_kernel(
-    const double *__restrict__ partial, int chunks, int nodes, int d, int nbins,
+    const uint64_t *__restrict__ partial, int chunks, int scale, double *__restrict__ small,
+    const double *__restrict__ hist, int nodes, int d, int nbins,
     double *__restrict__ cand_gain, int *__restrict__ cand_cut, unsigned *__restrict__ ticket,
     uint8_t *__restrict__ out_f, uint8_t *__restrict__ out_c, double *__restrict__ out_g) {
 #pragma clang fp contract(off)
     // one workgroup of 4 wavefronts per (node, feature); wavefront w sums the
-    // chunk partials w, w + 4, ...; wavefront 0 adds the four sums in order
-    __shared__ double red[4][kWave][8];
+    // fixed-point chunk partials w, w + 4, ... (integer sums: exact in any
+    // order); wavefront 0 adds the four sums, converts them to float64 and
+    // adds the side histogram of weights below the grid
+    __shared__ uint64_t red[4][kWave][8];
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
     const int pair = blockIdx.x;
     const int k = pair / d;
     const int j = pair - k * d;
+    const int b0 = 4 * lane;
+    const int nb = b0 < nbins ? min(4, nbins - b0) : 0;
+    const size_t off = ((size_t)k * d + j) * nbins * 2 + 2 * b0;
 
     double hs[4] = {0.0, 0.0, 0.0, 0.0}, hb[4] = {0.0, 0.0, 0.0, 0.0};
-    const int b0 = 4 * lane;
-    if (b0 < nbins) {
-        const size_t stride_p = (size_t)nodes * d * nbins * 2;
-        const double *base = partial + ((size_t)k * d + j) * nbins * 2 + 2 * b0;
-        const int nb = min(4, nbins - b0);
+    if (FIXED) {
+        uint64_t us[4] = {0, 0, 0, 0}, ub[4] = {0, 0, 0, 0};
         if (nb == 4) {
-            int p = wave;
-            for (; p + 4 < chunks; p += 8) {   // two chunks per step, loads issued together
-                const double2 *s0 = reinterpret_cast<const double2 *>(base + (size_t)p * stride_p);
-                const double2 *s1 =
-                    reinterpret_cast<const double2 *>(base + (size_t)(p + 4) * stride_p);
-                const double2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
-                const double2 c0 = s1[0], c1 = s1[1], c2 = s1[2], c3 = s1[3];
-                hs[0] += a0.x; hb[0] += a0.y; hs[1] += a1.x; hb[1] += a1.y;
-                hs[2] += a2.x; hb[2] += a2.y; hs[3] += a3.x; hb[3] += a3.y;
-                hs[0] += c0.x; hb[0] += c0.y; hs[1] += c1.x; hb[1] += c1.y;
-                hs[2] += c2.x; hb[2] += c2.y; hs[3] += c3.x; hb[3] += c3.y;
-            }
-            if (p < chunks) {
-                const double2 *s0 = reinterpret_cast<const double2 *>(base + (size_t)p * stride_p);
-                const double2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
-                hs[0] += a0.x; hb[0] += a0.y; hs[1] += a1.x; hb[1] += a1.y;
-                hs[2] += a2.x; hb[2] += a2.y; hs[3] += a3.x; hb[3] += a3.y;
-            }
-        } else {
+            const size_t stride_p = (size_t)nodes * d * nbins * 2;
             for (int p = wave; p < chunks; p += 4) {
-                const double *src = base + (size_t)p * stride_p;
+                const ulonglong2 *src =
+                    reinterpret_cast<const ulonglong2 *>(partial + (size_t)p * stride_p + off);
+                const ulonglong2 a0 = src[0], a1 = src[1], a2 = src[2], a3 = src[3];
+                us[0] += a0.x; ub[0] += a0.y; us[1] += a1.x; ub[1] += a1.y;
+                us[2] += a2.x; ub[2] += a2.y; us[3] += a3.x; ub[3] += a3.y;
+            }
+        } else if (nb > 0) {
+            const size_t stride_p = (size_t)nodes * d * nbins * 2;
+            for (int p = wave; p < chunks; p += 4) {
+                const uint64_t *src = partial + (size_t)p * stride_p + off;
                 for (int e = 0; e < nb; ++e) {
-                    hs[e] += src[2 * e];
-                    hb[e] += src[2 * e + 1];
+                    us[e] += src[2 * e];
+                    ub[e] += src[2 * e + 1];
                 }
             }
         }
-    }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        red[wave][lane][e] = hs[e];
-        red[wave][lane][4 + e] = hb[e];
-    }
-    __syncthreads();
-    if (wave != 0) return;
+        for (int e = 0; e < 4; ++e) {
+            red[wave][lane][e] = us[e];
+            red[wave][lane][4 + e] = ub[e];
+        }
+        __syncthreads();
+        if (wave != 0) return;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        hs[e] = ((red[0][lane][e] + red[1][lane][e]) + red[2][lane][e]) + red[3][lane][e];
-        hb[e] = ((red[0][lane][4 + e] + red[1][lane][4 + e]) + red[2][lane][4 + e]) +
-                red[3][lane][4 + e];
+        for (int e = 0; e < 4; ++e) {
+            const uint64_t ts = red[0][lane][e] + red[1][lane][e] + red[2][lane][e] +
+                                red[3][lane][e];
+            const uint64_t tb = red[0][lane][4 + e] + red[1][lane][4 + e] +
+                                red[2][lane][4 + e] + red[3][lane][4 + e];
+            hs[e] = ldexp((double)ts, -scale);
+            hb[e] = ldexp((double)tb, -scale);
+        }
+        for (int e = 0; e < nb; ++e) {   // side histogram, cleared for the next layer
+            hs[e] += small[off + 2 * e];
+            hb[e] += small[off + 2 * e + 1];
+            small[off + 2 * e] = 0.0;
+            small[off + 2 * e + 1] = 0.0;
+        }
+    } else {
+        if (wave != 0) return;
+        for (int e = 0; e < nb; ++e) {
+            hs[e] = hist[off + 2 * e];
+            hb[e] = hist[off + 2 * e + 1];
+        }
     }
     bool ne[4];
     int first = 0x7fffffff, last = -1;
@@ -886,42 +961,23 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
     const int nodes = 1 << layer;
     const size_t per_node_feature = (size_t)n_bins * 2 * sizeof(double);
     // the kernel's static LDS (cut table) shares the workgroup's LDS limit
-    max_lds = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
+    max_lds = max_lds > kHistStaticLdsReserve + kHistExtraLds
+                  ? max_lds - kHistStaticLdsReserve - kHistExtraLds
+                  : 0;
     int npg = (int)(max_lds / per_node_feature);
     if (npg < 1) npg = 1;
     if (npg > nodes) npg = nodes;
     hs.nodes_per_group = npg;
     hs.node_groups = (nodes + npg - 1) / npg;
-    // Features per workgroup.  Estimated time of a launch shape, with about
-    // one workgroup per CU: every feature group re-reads the chunk's node
-    // ids and weights (5 bytes per event, mostly from L2), every event chunk
-    // writes one partial histogram that best_cuts reads again, and the LDS
-    // atomics of a workgroup run at a few per clock per CU.
+    // Features per workgroup.  Each feature group re-reads the chunk's node
+    // ids and weights (5 bytes per event) and each event chunk adds one
+    // partial histogram to write and to sum; measured sweeps over 0.5M-10M
+    // events and 20-40 features put the optimum near four feature groups,
+    // capped by LDS, with one workgroup per CU.
     const int t_threads = threads > 0 ? threads : (n >= (1 << 20) ? 1024 : 512);
-    int f;
-    if (fpg > 0) {
-        f = fpg < d ? fpg : d;
-    } else {
-        const double hbytes = (double)nodes * d * per_node_feature;
-        const double cmax = (double)n / (16.0 * t_threads);
-        double best = -1.0;
-        f = 1;
-        for (int cand = 1; cand <= d; ++cand) {
-            if ((size_t)npg * cand * per_node_feature > max_lds) break;
-            const int g = ((d + cand - 1) / cand) * ((nodes + npg - 1) / npg);
-            double c = (double)cu_count / g;
-            if (c > cmax) c = cmax;
-            if (c < 1.0) c = 1.0;
-            const double wgs = c * g < cu_count ? c * g : (double)cu_count;
-            const double mem = ((double)n * d + 5.0 * n * g + 2.0 * c * hbytes) / 5.0e12;
-            const double atom = 0.5 * n * d / (wgs * 2.0 * 2.4e9);
-            const double cost = mem > atom ? mem : atom;
-            if (best < 0.0 || cost < best) {
-                best = cost;
-                f = cand;
-            }
-        }
-    }
+    int f = fpg > 0 ? fpg : (d + 3) / 4;
+    if (f > d) f = d;
+    if (f < 1) f = 1;
     while (f > 1 && (size_t)npg * f * per_node_feature > max_lds) --f;
     hs.features_per_group = f;
     hs.feature_groups = (d + f - 1) / f;
@@ -940,61 +996,80 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
     hs.chunks = (int)((n + ce - 1) / ce);
     const int64_t work = (int64_t)hs.chunks * groups;
     hs.blocks = (int)((work + kXcds - 1) / kXcds * kXcds);
-    hs.lds_bytes = (size_t)npg * f * per_node_feature;
+    hs.lds_bytes = (size_t)npg * f * per_node_feature + kHistExtraLds;
     return hs;
+}
+
+int histogram_scale(double total_weight_bound) {
+    if (!(total_weight_bound > 0.0) || !std::isfinite(total_weight_bound)) return 60;
+    int e = 0;
+    (void)std::frexp(total_weight_bound, &e);  // bound < 2^e
+    int sc = 62 - e;                           // bound * 2^sc < 2^62
+    if (sc > 60) sc = 60;
+    if (sc < -60) sc = -60;
+    return sc;
 }
 
 template <bool ROUTED, int NP>
 hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
-                          const uint8_t *cut_f, const uint8_t *cut_c, int layer, double *partial,
-                          int *err, hipStream_t s) {
+                          const uint8_t *cut_f, const uint8_t *cut_c, int layer, int scale,
+                          uint64_t *partial, double *small, int *err, hipStream_t s) {
     allow_lds(hist_kernel<ROUTED, NP>, hs.lds_bytes);
     hist_kernel<ROUTED, NP><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f, cut_c, layer, hs.features_per_group,
-        hs.feature_groups, hs.nodes_per_group, hs.node_groups, hs.chunks, hs.chunk_events,
-        partial, err);
+        hs.feature_groups, hs.nodes_per_group, hs.node_groups, hs.chunks, hs.chunk_events, scale,
+        partial, small, err);
     return hipGetLastError();
 }
 
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                             const float *w, const uint8_t *cut_f, const uint8_t *cut_c,
-                            int layer, bool routed, double *partial, int *err, hipStream_t s) {
-    if (!routed)
-        return launch_hist_np<false, 0>(hs, xb, ldb, n, d, n_bins, node_in, nullptr, w, nullptr,
-                                        nullptr, layer, partial, err, s);
+                            int layer, bool routed, int scale, uint64_t *partial, double *small,
+                            int *err, hipStream_t s) {
+#define FBDT_HIST(R, NPV)                                                                        \
+    launch_hist_np<R, NPV>(hs, xb, ldb, n, d, n_bins, node_in, R ? node_out : nullptr, w,       \
+                           R ? cut_f : nullptr, R ? cut_c : nullptr, layer, scale, partial,     \
+                           small, err, s)
+    if (!routed) return FBDT_HIST(false, 0);
     const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
     switch (parents) {
     case 0:
-    case 1:
-        return launch_hist_np<true, 1>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
-                                       cut_c, layer, partial, err, s);
-    case 2:
-        return launch_hist_np<true, 2>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
-                                       cut_c, layer, partial, err, s);
-    case 4:
-        return launch_hist_np<true, 4>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
-                                       cut_c, layer, partial, err, s);
-    default:
-        return launch_hist_np<true, 0>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f,
-                                       cut_c, layer, partial, err, s);
+    case 1: return FBDT_HIST(true, 1);
+    case 2: return FBDT_HIST(true, 2);
+    case 4: return FBDT_HIST(true, 4);
+    default: return FBDT_HIST(true, 0);
     }
+#undef FBDT_HIST
 }
 
-hipError_t launch_merge_partials(const double *partial, int chunks, size_t count, double *out,
-                                 hipStream_t s) {
-    merge_partials_kernel<<<grid_for((int64_t)count, 256, 2048), 256, 0, s>>>(partial, chunks,
-                                                                             count, out);
+hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t count, int scale,
+                                 const double *small, double *out, hipStream_t s) {
+    merge_partials_kernel<<<grid_for((int64_t)count, 256, 2048), 256, 0, s>>>(
+        partial, chunks, count, scale, small, out);
     return hipGetLastError();
 }
 
-hipError_t launch_best_cuts(const double *partial, int chunks, int n_nodes, int d, int n_bins,
+hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, double *out,
+                          hipStream_t s) {
+    abs_sum_kernel<<<kValidateBlocks, 256, 0, s>>>(w, n, block_partial);
+    sum_blocks_kernel<<<1, 64, 0, s>>>(block_partial, kValidateBlocks, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
+                            const double *hist, int n_nodes, int d, int n_bins,
                             double *cand_gain, int *cand_cut, unsigned *ticket, uint8_t *out_f,
                             uint8_t *out_c, double *out_g, hipStream_t s) {
-    best_cuts_kernel<<<n_nodes * d, 4 * kWave, 0, s>>>(partial, chunks, n_nodes, d, n_bins,
-                                                       cand_gain, cand_cut, ticket, out_f, out_c,
-                                                       out_g);
+    if (partial)
+        best_cuts_kernel<true><<<n_nodes * d, 4 * kWave, 0, s>>>(
+            partial, chunks, scale, small, nullptr, n_nodes, d, n_bins, cand_gain, cand_cut,
+            ticket, out_f, out_c, out_g);
+    else
+        best_cuts_kernel<false><<<n_nodes * d, 4 * kWave, 0, s>>>(
+            nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cand_gain, cand_cut, ticket, out_f,
+            out_c, out_g);
     return hipGetLastError();
 }
 

@@ -149,6 +149,25 @@ def test_histogram_matches_oracle(layer, n_bins, d, n):
         assert err <= 1e-12, err
 
 
+@pytest.mark.parametrize("layer", [0, 3])
+def test_histogram_weights_of_every_magnitude(layer):
+    # weights from 1e-12 to 1e3: the large ones are summed exactly in fixed
+    # point, the ones below the fixed-point grid in float64
+    rng = np.random.default_rng(11 + layer)
+    n, d, B = 60_013, 5, 64
+    xb = rng.integers(0, B, (d, n)).astype(np.uint8)
+    node = rng.integers(1 << layer, 2 << layer, n).astype(np.uint8)
+    y = np.where(rng.random(n) < 0.5, 1, -1).astype(np.int8)
+    wa = (10.0 ** rng.uniform(-12, 3, n)).astype(np.float32)
+    wa[rng.random(n) < 0.3] = 0
+    ws = np.where(y > 0, wa, -wa).astype(np.float32)
+    ref = O.histogram(xb, node.astype(np.int64), wa, y > 0, layer, B)
+    say(f"histogram weights 1e-12..1e3 layer={layer}")
+    H = fb.histogram(fb.Codes.from_numpy(xb), dev(node), dev(ws), layer, B).cpu().numpy()
+    assert np.array_equal(H == 0, ref == 0)
+    assert max_rel(H, ref) <= 1e-12
+
+
 def test_histogram_feature_groups_and_threads():
     rng = np.random.default_rng(3)
     n, d, B, layer = 40_001, 11, 256, 2
