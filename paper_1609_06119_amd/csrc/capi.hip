@@ -429,9 +429,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.small, small_elems);
     cv.add(&fb.cand_gain, (size_t)max_nodes * d);
     cv.add(&fb.cand_cut, (size_t)max_nodes * d);
-    cv.add(&fb.node_ticket, max_nodes);
     cv.add(&fb.leaf_partial, (size_t)lblocks * 2 * nleaf);
-    cv.add(&fb.leaf_ticket, 1);
     cv.add(&fb.class_partial, 2 * kValidateBlocks);
     cv.add(&fb.f0, 2);
     cv.add(&fb.err, 1);
@@ -442,8 +440,6 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
 
-    HIP_TRY(launch_fill_u32(fb.node_ticket, 0u, max_nodes, s));
-    HIP_TRY(launch_fill_u32(fb.leaf_ticket, 0u, 1, s));
     HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
     HIP_TRY(launch_fill_u32(fb.small, 0u, 2 * small_elems, s));
     HIP_TRY(launch_validate(y, w, n, fb.class_partial, fb.err, s));
@@ -474,32 +470,35 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
         uint8_t *cc = fb.cut_bin + (size_t)t * nin;
         double *cg = fb.gain + (size_t)t * nin;
         for (int l = 0; l < D; ++l) {
-            const int lo = (1 << l) - 1;            // index of the layer's first node
+            // the previous layer's candidates give the cuts this pass routes
+            // with; workgroup 0 records them in the model
             const int plo = l >= 1 ? (1 << (l - 1)) - 1 : 0;
+            ParentCuts pc;
+            if (l >= 1) pc = ParentCuts{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
             {
                 Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, l, true));
                 HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
                                          l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
-                                         l >= 1 ? fb.node[l & 1] : nullptr, fb.w, cf + plo,
-                                         cc + plo, l, true, scale, fb.partial, fb.small, fb.err,
-                                         s));
+                                         l >= 1 ? fb.node[l & 1] : nullptr, fb.w, pc, l, true,
+                                         scale, fb.partial, fb.small, fb.err, s));
                 tm.done();
             }
             {
                 Timed tm(FBDT_K_BEST_CUTS, s);
                 HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, scale, fb.small, nullptr,
-                                         1 << l, d, n_bins, fb.cand_gain, fb.cand_cut,
-                                         fb.node_ticket, cf + lo, cc + lo, cg + lo, s));
+                                         1 << l, d, n_bins, fb.cand_gain, fb.cand_cut, s));
                 tm.done();
             }
         }
         {
             const int plo = (1 << (D - 1)) - 1;
+            const ParentCuts pc{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
             Timed tm(FBDT_K_LEAF, s);
             HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
-                                fb.node[D & 1], cf + plo, cc + plo, D, true, y, w, fb.F, seed, t,
-                                alpha, eta, lblocks, fb.leaf_partial, fb.leaf_ticket,
-                                fb.leaf + (size_t)t * nleaf, fb.err, s));
+                                fb.node[D & 1], pc, D, true, y, w, fb.F, seed, t, alpha, lblocks,
+                                fb.leaf_partial, fb.err, s));
+            HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, eta,
+                                         fb.leaf + (size_t)t * nleaf, s));
             tm.done();
         }
     }
@@ -720,7 +719,7 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     const int scale = histogram_scale(h_wsum * (1.0 + 1e-6));
     {
         Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, layer, false));
-        HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node, nullptr, w, nullptr, nullptr,
+        HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node, nullptr, w, ParentCuts{},
                                  layer, false, scale, partial, small, err, s));
         tm.done();
     }
@@ -749,16 +748,13 @@ int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bin
     Carver cv;
     double *cg;
     int *cc;
-    unsigned *tk;
     cv.add(&cg, (size_t)n_nodes * d);
     cv.add(&cc, (size_t)n_nodes * d);
-    cv.add(&tk, n_nodes);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
-    HIP_TRY(launch_fill_u32(tk, 0u, n_nodes, s));
     Timed tm(FBDT_K_BEST_CUTS, s);
-    HIP_TRY(launch_best_cuts(nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cg, cc, tk,
-                             cut_feature, cut_bin, gain, s));
+    HIP_TRY(launch_best_cuts(nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cg, cc, s));
+    HIP_TRY(launch_select_cuts(cg, cc, n_nodes, d, cut_feature, cut_bin, gain, s));
     tm.done();
     HIP_TRY(hipStreamSynchronize(s));
     return FBDT_OK;
@@ -807,17 +803,15 @@ int fbdt_leaf_values(const uint8_t *node, const int8_t *y, const float *v, const
     std::lock_guard<std::mutex> lk(a.mu);
     Carver cv;
     double *lp;
-    unsigned *tk;
     int *err;
     cv.add(&lp, (size_t)blocks * 2 * (1 << depth));
-    cv.add(&tk, 1);
     cv.add(&err, 1);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
-    HIP_TRY(launch_fill_u32(tk, 0u, 1, s));
     HIP_TRY(launch_fill_u32(err, 0u, 1, s));
-    HIP_TRY(launch_leaf(nullptr, 0, n, 1, node, nullptr, nullptr, nullptr, depth, false, y, v, F,
-                        seed, tree, alpha, eta, blocks, lp, tk, leaf, err, s));
+    HIP_TRY(launch_leaf(nullptr, 0, n, 1, node, nullptr, ParentCuts{}, depth, false, y, v, F,
+                        seed, tree, alpha, blocks, lp, err, s));
+    HIP_TRY(launch_leaf_finalize(lp, blocks, depth, eta, leaf, s));
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;
     if (h_err & kErrRoute) return fail(FBDT_E_INVAL, "a node id is not a leaf id (skipped)");

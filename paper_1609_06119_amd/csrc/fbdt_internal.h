@@ -39,11 +39,9 @@ struct FitBuffers {
     uint8_t *node[2];     // [npad] node ids, double-buffered across layers
     uint64_t *partial;    // fixed-point histogram partials [chunks][nodes][d][B][2]
     double *small;        // float64 histogram of the weights below the fixed-point grid
-    double *cand_gain;    // [max nodes][d]
-    int *cand_cut;        // [max nodes][d]
-    unsigned *node_ticket;  // [max nodes]
+    double *cand_gain;    // [max nodes][d] best gain of every (node, feature)
+    int *cand_cut;        // [max nodes][d] and its bin
     double *leaf_partial;   // [leaf blocks][2^D][2]
-    unsigned *leaf_ticket;  // [1]
     double *class_partial;  // [validate blocks][2]
     double *f0;             // [2]: initial score, total event weight
     int *err;               // [1]
@@ -81,6 +79,17 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
 HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
                          size_t max_lds, int fpg, int chunks, int threads);
 
+// Candidate cuts of a layer's nodes, one per (node, feature), from which a
+// routed pass takes each parent's cut (best gain, then lowest feature);
+// rec_* (optional) receive those cuts for the model (written by workgroup 0).
+struct ParentCuts {
+    const double *cand_gain = nullptr;
+    const int *cand_cut = nullptr;
+    uint8_t *rec_f = nullptr;
+    uint8_t *rec_c = nullptr;
+    double *rec_g = nullptr;
+};
+
 // Fixed-point scale of the histogram sums: a weight w >= 2^(23 - scale) is
 // an exact multiple of 2^-scale and is added as the integer w * 2^scale;
 // smaller positive weights go to a float64 side histogram.  The scale is
@@ -90,15 +99,16 @@ int histogram_scale(double total_weight_bound);
 
 // Histogram pass.  routed = true: node_in holds the ids of layer-1 (null for
 // layer <= 1, all events at the root), the pass routes them with the cuts of
-// layer-1 and (first feature group only) writes the layer's ids to node_out.
+// layer-1 (from pc) and (first feature group only) writes the layer's ids to
+// node_out.
 // routed = false: node_in holds the ids of the layer itself.
 // partial: [chunks][2^layer][d][B][2] fixed-point sums; small: [2^layer][d][B][2]
 // float64 sums of the weights below the grid (accumulated into, not cleared).
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
-                            const float *w, const uint8_t *cut_f, const uint8_t *cut_c,
-                            int layer, bool routed, int scale, uint64_t *partial, double *small,
-                            int *err, hipStream_t s);
+                            const float *w, const ParentCuts &pc, int layer, bool routed,
+                            int scale, uint64_t *partial, double *small, int *err,
+                            hipStream_t s);
 
 // hist[i] = (sum over chunks of partial[chunk][i]) * 2^-scale + small[i].
 hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t count, int scale,
@@ -108,23 +118,28 @@ hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t cou
 hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, double *out,
                           hipStream_t s);
 
-// Best cut of every node of a layer, from fixed-point chunk partials plus the
-// float64 side histogram (which it clears), or, with partial == null, from a
-// float64 histogram `hist`.
+// Best cut of every (node, feature) of a layer into cand_gain/cand_cut, from
+// fixed-point chunk partials plus the float64 side histogram (which it
+// clears), or, with partial == null, from a float64 histogram `hist`.
 hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
                             const double *hist, int n_nodes, int d, int n_bins,
-                            double *cand_gain, int *cand_cut, unsigned *ticket,
-                            uint8_t *out_f, uint8_t *out_c, double *out_g, hipStream_t s);
+                            double *cand_gain, int *cand_cut, hipStream_t s);
 
-// Last routing (routed = true, from layer depth-1 to the leaves) or none
-// (node_in already holds leaf ids), then terminal boost weights.
+// Best cut of each node over its features.
+hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,
+                              uint8_t *out_f, uint8_t *out_c, double *out_g, hipStream_t s);
+
+// Last routing (routed = true, from layer depth-1 to the leaves with the
+// cuts from pc) or none (node_in already holds leaf ids), then the per-block
+// partial sums of the terminal boost weights; launch_leaf_finalize adds the
+// partials and writes eta * num / den per leaf.
 int leaf_blocks(int64_t n, int cu_count);
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
-                       uint8_t *node_out, const uint8_t *cut_f, const uint8_t *cut_c, int depth,
-                       bool routed, const int8_t *y, const float *v, const double *F,
-                       uint64_t seed, int tree, double alpha, double eta, int blocks,
-                       double *leaf_partial, unsigned *ticket, double *leaf_out, int *err,
-                       hipStream_t s);
+                       uint8_t *node_out, const ParentCuts &pc, int depth, bool routed,
+                       const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
+                       double alpha, int blocks, double *leaf_partial, int *err, hipStream_t s);
+hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, double eta,
+                                double *leaf_out, hipStream_t s);
 
 hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *node,
                         const uint8_t *cut_f, const uint8_t *cut_c, int layer, int *err,

@@ -178,6 +178,85 @@ __global__ __launch_bounds__(256) void tree_prep_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Best candidate of one node over its features (gain highest, then lowest
+// feature), by one wavefront; lane 0 returns it.  An unusable result
+// (no finite gain) falls back to feature 0 and reports it.
+__device__ __forceinline__ void node_best(const double *__restrict__ cand_gain,
+                                          const int *__restrict__ cand_cut, int d, int k,
+                                          int lane, int *bf, int *bc, double *bg, bool *ok) {
+    double g = -INFINITY;
+    int j = 0x7fffffff, c = 1;
+    for (int jj = lane; jj < d; jj += kWave) {
+        const double gg = cand_gain[(size_t)k * d + jj];
+        if (gg > g) {
+            g = gg;
+            j = jj;
+            c = cand_cut[(size_t)k * d + jj];
+        }
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const double og = __shfl_xor(g, off);
+        const int oj = __shfl_xor(j, off);
+        const int oc = __shfl_xor(c, off);
+        if (og > g || (og == g && oj < j)) {
+            g = og;
+            j = oj;
+            c = oc;
+        }
+    }
+    *ok = j < d && c >= 1 && c <= 255;
+    *bf = *ok ? j : 0;
+    *bc = *ok ? c : 1;
+    *bg = g;
+}
+
+// Prologue of a routed pass: the cut of every parent node from the previous
+// layer's candidates, into the LDS cut table; workgroup 0 also records the
+// cuts in the model.
+__device__ void load_parent_cuts(const double *__restrict__ cand_gain,
+                                 const int *__restrict__ cand_cut, int d, int half,
+                                 uint8_t *s_cf, uint8_t *s_cc, uint8_t *__restrict__ rec_f,
+                                 uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
+                                 int *eflag) {
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nw = blockDim.x / kWave;
+    for (int k = wave; k < half; k += nw) {
+        int bf, bc;
+        double bg;
+        bool ok;
+        node_best(cand_gain, cand_cut, d, k, lane, &bf, &bc, &bg, &ok);
+        if (lane == 0) {
+            s_cf[k] = (uint8_t)bf;
+            s_cc[k] = (uint8_t)bc;
+            if (!ok) atomicOr(eflag, kErrRoute);
+            if (blockIdx.x == 0 && rec_f) {
+                rec_f[k] = (uint8_t)bf;
+                rec_c[k] = (uint8_t)bc;
+                rec_g[k] = bg;
+            }
+        }
+    }
+}
+
+// Cuts of n_nodes nodes from their candidates (one wavefront per node).
+__global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restrict__ cand_gain,
+                                                         const int *__restrict__ cand_cut, int d,
+                                                         uint8_t *__restrict__ out_f,
+                                                         uint8_t *__restrict__ out_c,
+                                                         double *__restrict__ out_g) {
+    int bf, bc;
+    double bg;
+    bool ok;
+    node_best(cand_gain, cand_cut, d, blockIdx.x, threadIdx.x, &bf, &bc, &bg, &ok);
+    if (threadIdx.x == 0) {
+        out_f[blockIdx.x] = (uint8_t)bf;
+        out_c[blockIdx.x] = (uint8_t)bc;
+        out_g[blockIdx.x] = bg;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Layer histogram.  Workgroup (chunk p, feature group g, node group h) keeps
 // H[node in h][feature in g][bin][class] in LDS as float64, adds every
 // sampled event of its event chunk with ds_add_f64, and writes its partial
@@ -201,8 +280,9 @@ template <bool ROUTED, int NP>
 __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
-    const float *__restrict__ w, const uint8_t *__restrict__ cut_f,
-    const uint8_t *__restrict__ cut_c, int layer, int fpg, int G, int npg, int NG, int chunks,
+    const float *__restrict__ w, const double *__restrict__ cand_gain,
+    const int *__restrict__ cand_cut, uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c,
+    double *__restrict__ rec_g, int layer, int fpg, int G, int npg, int NG, int chunks,
     int64_t chunk_events, int scale, uint64_t *__restrict__ partial, double *__restrict__ small,
     int *__restrict__ err) {
     extern __shared__ uint64_t lds[];
@@ -237,14 +317,13 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     for (int t = threadIdx.x; t < lds_n + 2 * kWave; t += blockDim.x) lds[t] = 0ull;
     // weights at or above tau are exact multiples of 2^-scale
     const float tau = ldexpf(1.0f, 23 - scale);
-    if (ROUTED && layer >= 1)
-        for (int t = threadIdx.x; t < half; t += blockDim.x) {
-            s_cf[t] = cut_f[t] < d ? cut_f[t] : 0;
-            s_cc[t] = cut_c[t];
-        }
+    __shared__ int s_eflag;
+    if (threadIdx.x == 0) s_eflag = 0;
     __syncthreads();
-    int eflag = 0;
-    if (ROUTED && layer >= 1 && threadIdx.x < half && cut_f[threadIdx.x] >= d) eflag |= kErrRoute;
+    if (ROUTED && layer >= 1)
+        load_parent_cuts(cand_gain, cand_cut, d, half, s_cf, s_cc, rec_f, rec_c, rec_g, &s_eflag);
+    __syncthreads();
+    int eflag = threadIdx.x == 0 ? s_eflag : 0;
 
     const int64_t start = (int64_t)p * chunk_events;
     const int64_t end = min(n, start + chunk_events);
@@ -445,8 +524,9 @@ __global__ void sum_blocks_kernel(const double *__restrict__ block_partial, int 
 // lane l owns bins 4l..4l+3, sums the chunk partials, builds the cumulative
 // histograms with an in-lane prefix plus a wavefront scan, evaluates the
 // separation gain of each candidate cut and reduces to the best (gain
-// highest, then lowest bin).  The last wavefront to finish a node reduces
-// over features (gain highest, then lowest feature) and writes the cut.
+// highest, then lowest bin).  The reduction of a node's candidates
+// over features (gain highest, then lowest feature) is left to the next
+// pass (load_parent_cuts) or to select_cuts_kernel.
 //
 // Exactness rules shared with the plain definition: a cut whose left or
 // right side holds no event has gain exactly 0 (as the definition gives
@@ -457,8 +537,7 @@ template <bool FIXED>
 __global__ __launch_bounds__(256) void best_cuts_kernel(
     const uint64_t *__restrict__ partial, int chunks, int scale, double *__restrict__ small,
     const double *__restrict__ hist, int nodes, int d, int nbins,
-    double *__restrict__ cand_gain, int *__restrict__ cand_cut, unsigned *__restrict__ ticket,
-    uint8_t *__restrict__ out_f, uint8_t *__restrict__ out_c, double *__restrict__ out_g) {
+    double *__restrict__ cand_gain, int *__restrict__ cand_cut) {
 #pragma clang fp contract(off)
     // one workgroup of 4 wavefronts per (node, feature); wavefront w sums the
     // fixed-point chunk partials w, w + 4, ... (integer sums: exact in any
@@ -479,7 +558,19 @@ __global__ __launch_bounds__(256) void best_cuts_kernel(
         uint64_t us[4] = {0, 0, 0, 0}, ub[4] = {0, 0, 0, 0};
         if (nb == 4) {
             const size_t stride_p = (size_t)nodes * d * nbins * 2;
-            for (int p = wave; p < chunks; p += 4) {
+            // four chunks per step so that their loads are in flight together
+            int p = wave;
+            for (; p + 12 < chunks; p += 16) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(
+                        partial + (size_t)(p + 4 * q) * stride_p + off);
+                    const ulonglong2 a0 = src[0], a1 = src[1], a2 = src[2], a3 = src[3];
+                    us[0] += a0.x; ub[0] += a0.y; us[1] += a1.x; ub[1] += a1.y;
+                    us[2] += a2.x; ub[2] += a2.y; us[3] += a3.x; ub[3] += a3.y;
+                }
+            }
+            for (; p < chunks; p += 4) {
                 const ulonglong2 *src =
                     reinterpret_cast<const ulonglong2 *>(partial + (size_t)p * stride_p + off);
                 const ulonglong2 a0 = src[0], a1 = src[1], a2 = src[2], a3 = src[3];
@@ -604,52 +695,18 @@ __global__ __launch_bounds__(256) void best_cuts_kernel(
         cand_gain[pair] = best;
         cand_cut[pair] = bestc;
     }
-    __threadfence();
-    unsigned prev = 0;
-    if (lane == 0) prev = atomicAdd(&ticket[k], 1u);
-    prev = __shfl(prev, 0);
-    if (prev != (unsigned)(d - 1)) return;
-
-    // last wavefront of node k: best over features
-    __threadfence();
-    double bg = -INFINITY;
-    int bj = 0x7fffffff, bc = 1;
-    for (int jj = lane; jj < d; jj += kWave) {
-        const double gg = load_agent(&cand_gain[(size_t)k * d + jj]);
-        if (gg > bg) {
-            bg = gg;
-            bj = jj;
-            bc = load_agent(&cand_cut[(size_t)k * d + jj]);
-        }
-    }
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        const double og = __shfl_xor(bg, off);
-        const int oj = __shfl_xor(bj, off);
-        const int oc = __shfl_xor(bc, off);
-        if (og > bg || (og == bg && oj < bj)) {
-            bg = og;
-            bj = oj;
-            bc = oc;
-        }
-    }
-    if (lane == 0) {
-        out_f[k] = (uint8_t)bj;
-        out_c[k] = (uint8_t)bc;
-        out_g[k] = bg;
-        ticket[k] = 0u;
-    }
 }
 
 // ---------------------------------------------------------------------------
 // Terminal boost weights (section 1.3): per leaf, sum(v y~) and
-// sum(v |y~| (2 - |y~|)) over the sampled events.  With NL > 0 leaves every
-// thread keeps the 2 NL sums in registers, then a wavefront reduction and an
-// in-order sum over wavefronts give the workgroup's partial (no atomics, a
-// fixed order); with NL = 0 (deep trees) threads add into LDS accumulators.
-// The last workgroup to finish sums the workgroup partials (all threads,
-// fixed order) and writes eta * num / den (0 when den = 0).  Routed mode
-// first sends every event from layer depth-1 to its leaf and stores it.
+// sum(v |y~| (2 - |y~|)) over the sampled events, one partial per
+// workgroup.  With NL > 0 leaves every thread keeps the 2 NL sums in
+// registers, then a wavefront reduction and an in-order sum over wavefronts
+// give the workgroup's partial (no atomics, fixed order); with NL = 0 (deep
+// trees) threads add into LDS accumulators.  leaf_finalize_kernel adds the
+// partials.  Routed mode first takes the last layer's cuts from their
+// candidates, sends every event from layer depth-1 to its leaf and stores
+// the leaf id.
 __device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
@@ -660,15 +717,16 @@ template <bool ROUTED, int NL>
 __global__ __launch_bounds__(256) void leaf_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
-    const uint8_t *__restrict__ cut_f, const uint8_t *__restrict__ cut_c, int depth,
-    const int8_t *__restrict__ y, const float *__restrict__ v, const double *__restrict__ F,
-    uint64_t seed, int tree, double alpha, double eta, double *__restrict__ leaf_partial,
-    unsigned *__restrict__ ticket, double *__restrict__ leaf_out, int *__restrict__ err) {
+    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut,
+    uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
+    int depth, const int8_t *__restrict__ y, const float *__restrict__ v,
+    const double *__restrict__ F, uint64_t seed, int tree, double alpha,
+    double *__restrict__ leaf_partial, int *__restrict__ err) {
 #pragma clang fp contract(off)
     __shared__ double acc[2 * 128];
     __shared__ double red[256];
     __shared__ uint8_t s_cf[64], s_cc[64];
-    __shared__ unsigned s_last;
+    __shared__ int s_eflag;
     const int nleaf = 1 << depth;
     const int half = nleaf >> 1;
     const int lane = threadIdx.x % kWave;
@@ -676,13 +734,12 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     const int nwaves = blockDim.x / kWave;
     if (NL == 0)
         for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x) acc[t] = 0.0;
-    if (ROUTED)
-        for (int t = threadIdx.x; t < half; t += blockDim.x) {
-            s_cf[t] = cut_f[t];
-            s_cc[t] = cut_c[t];
-        }
+    if (threadIdx.x == 0) s_eflag = 0;
     __syncthreads();
-    int eflag = 0;
+    if (ROUTED)
+        load_parent_cuts(cand_gain, cand_cut, d, half, s_cf, s_cc, rec_f, rec_c, rec_g, &s_eflag);
+    __syncthreads();
+    int eflag = threadIdx.x == 0 ? s_eflag : 0;
     double an[NL > 0 ? NL : 1], ad[NL > 0 ? NL : 1];
 #pragma unroll
     for (int l = 0; l < (NL > 0 ? NL : 1); ++l) an[l] = ad[l] = 0.0;
@@ -697,11 +754,7 @@ __global__ __launch_bounds__(256) void leaf_kernel(
                 k = 0;
                 par = half;
             }
-            int f = s_cf[k];
-            if (f >= d) {
-                eflag |= kErrRoute;
-                f = 0;
-            }
+            const int f = min((int)s_cf[k], d - 1);
             const uint8_t x = xb[(int64_t)f * ldb + i];
             leaf = 2 * par + (x >= s_cc[k] ? 1 : 0);
             node_out[i] = (uint8_t)leaf;
@@ -754,23 +807,32 @@ __global__ __launch_bounds__(256) void leaf_kernel(
             leaf_partial[(size_t)blockIdx.x * 2 * nleaf + t] = acc[t];
     }
     if (eflag) atomicOr(err, eflag);
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) s_last = (atomicAdd(ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    // the last workgroup: thread t sums value t % nv over blocks t / nv,
-    // t / nv + stripes, ...; then the stripes are added in order
+}
+
+// Sum of the workgroup partials of the leaf pass (one workgroup; thread t
+// adds value t % nv over blocks t / nv, t / nv + stripes, ...; the stripes
+// are then added in order) and the boost weights eta * num / den (0 when
+// den = 0).
+__global__ __launch_bounds__(256) void leaf_finalize_kernel(const double *__restrict__ leaf_partial,
+                                                            int nblocks, int nleaf, double eta,
+                                                            double *__restrict__ leaf_out) {
+#pragma clang fp contract(off)
+    __shared__ double red[256];
     const int nv = 2 * nleaf;
     const int stripes = blockDim.x / nv;
     const int t = threadIdx.x;
     if (t < stripes * nv) {
         const int val = t % nv, st = t / nv;
-        double sum = 0.0;
-        for (unsigned b = st; b < gridDim.x; b += stripes)
-            sum += leaf_partial[(size_t)b * nv + val];
-        red[t] = sum;
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        int b = st;
+        for (; b + 3 * stripes < nblocks; b += 4 * stripes) {
+            s0 += leaf_partial[(size_t)b * nv + val];
+            s1 += leaf_partial[(size_t)(b + stripes) * nv + val];
+            s2 += leaf_partial[(size_t)(b + 2 * stripes) * nv + val];
+            s3 += leaf_partial[(size_t)(b + 3 * stripes) * nv + val];
+        }
+        for (; b < nblocks; b += stripes) s0 += leaf_partial[(size_t)b * nv + val];
+        red[t] = (s0 + s1) + (s2 + s3);
     }
     __syncthreads();
     if (t < nleaf) {
@@ -781,7 +843,6 @@ __global__ __launch_bounds__(256) void leaf_kernel(
         }
         leaf_out[t] = den == 0.0 ? 0.0 : eta * (num / den);
     }
-    if (t == 0) *ticket = 0u;
 }
 
 // node <- 2 node + [xb[f][i] >= c] with (f, c) the cut of the node.
@@ -1013,25 +1074,25 @@ int histogram_scale(double total_weight_bound) {
 template <bool ROUTED, int NP>
 hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
-                          const uint8_t *cut_f, const uint8_t *cut_c, int layer, int scale,
-                          uint64_t *partial, double *small, int *err, hipStream_t s) {
+                          const ParentCuts &pc, int layer, int scale, uint64_t *partial,
+                          double *small, int *err, hipStream_t s) {
     allow_lds(hist_kernel<ROUTED, NP>, hs.lds_bytes);
     hist_kernel<ROUTED, NP><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
-        xb, ldb, n, d, n_bins, node_in, node_out, w, cut_f, cut_c, layer, hs.features_per_group,
-        hs.feature_groups, hs.nodes_per_group, hs.node_groups, hs.chunks, hs.chunk_events, scale,
-        partial, small, err);
+        xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.rec_f,
+        pc.rec_c, pc.rec_g, layer, hs.features_per_group, hs.feature_groups, hs.nodes_per_group,
+        hs.node_groups, hs.chunks, hs.chunk_events, scale, partial, small, err);
     return hipGetLastError();
 }
 
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
-                            const float *w, const uint8_t *cut_f, const uint8_t *cut_c,
-                            int layer, bool routed, int scale, uint64_t *partial, double *small,
-                            int *err, hipStream_t s) {
+                            const float *w, const ParentCuts &pc, int layer, bool routed,
+                            int scale, uint64_t *partial, double *small, int *err,
+                            hipStream_t s) {
+    const ParentCuts none{};
 #define FBDT_HIST(R, NPV)                                                                        \
     launch_hist_np<R, NPV>(hs, xb, ldb, n, d, n_bins, node_in, R ? node_out : nullptr, w,       \
-                           R ? cut_f : nullptr, R ? cut_c : nullptr, layer, scale, partial,     \
-                           small, err, s)
+                           R ? pc : none, layer, scale, partial, small, err, s)
     if (!routed) return FBDT_HIST(false, 0);
     const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
     switch (parents) {
@@ -1060,16 +1121,19 @@ hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, doub
 
 hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
                             const double *hist, int n_nodes, int d, int n_bins,
-                            double *cand_gain, int *cand_cut, unsigned *ticket, uint8_t *out_f,
-                            uint8_t *out_c, double *out_g, hipStream_t s) {
+                            double *cand_gain, int *cand_cut, hipStream_t s) {
     if (partial)
         best_cuts_kernel<true><<<n_nodes * d, 4 * kWave, 0, s>>>(
-            partial, chunks, scale, small, nullptr, n_nodes, d, n_bins, cand_gain, cand_cut,
-            ticket, out_f, out_c, out_g);
+            partial, chunks, scale, small, nullptr, n_nodes, d, n_bins, cand_gain, cand_cut);
     else
         best_cuts_kernel<false><<<n_nodes * d, 4 * kWave, 0, s>>>(
-            nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cand_gain, cand_cut, ticket, out_f,
-            out_c, out_g);
+            nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cand_gain, cand_cut);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,
+                              uint8_t *out_f, uint8_t *out_c, double *out_g, hipStream_t s) {
+    select_cuts_kernel<<<n_nodes, kWave, 0, s>>>(cand_gain, cand_cut, d, out_f, out_c, out_g);
     return hipGetLastError();
 }
 
@@ -1077,24 +1141,23 @@ int leaf_blocks(int64_t n, int cu_count) { return grid_for(n, 256, 2 * cu_count)
 
 template <bool ROUTED, int NL>
 void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
-             const uint8_t *node_in, uint8_t *node_out, const uint8_t *cut_f,
-             const uint8_t *cut_c, int depth, const int8_t *y, const float *v, const double *F,
-             uint64_t seed, int tree, double alpha, double eta, double *leaf_partial,
-             unsigned *ticket, double *leaf_out, int *err) {
-    leaf_kernel<ROUTED, NL><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, node_out, cut_f,
-                                                   cut_c, depth, y, v, F, seed, tree, alpha, eta,
-                                                   leaf_partial, ticket, leaf_out, err);
+             const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
+             const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
+             double alpha, double *leaf_partial, int *err) {
+    leaf_kernel<ROUTED, NL><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain,
+                                                   pc.cand_cut, pc.rec_f, pc.rec_c, pc.rec_g,
+                                                   depth, y, v, F, seed, tree, alpha,
+                                                   leaf_partial, err);
 }
 
 template <bool ROUTED>
 void leaf_dispatch(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
-                   const uint8_t *node_in, uint8_t *node_out, const uint8_t *cut_f,
-                   const uint8_t *cut_c, int depth, const int8_t *y, const float *v,
-                   const double *F, uint64_t seed, int tree, double alpha, double eta,
-                   double *leaf_partial, unsigned *ticket, double *leaf_out, int *err) {
+                   const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
+                   const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
+                   double alpha, double *leaf_partial, int *err) {
 #define FBDT_LEAF_CASE(NLV)                                                                      \
-    leaf_go<ROUTED, NLV>(blocks, s, xb, ldb, n, d, node_in, node_out, cut_f, cut_c, depth, y, v, \
-                         F, seed, tree, alpha, eta, leaf_partial, ticket, leaf_out, err)
+    leaf_go<ROUTED, NLV>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, y, v, F, seed,  \
+                         tree, alpha, leaf_partial, err)
     switch (depth) {
     case 1: FBDT_LEAF_CASE(2); break;
     case 2: FBDT_LEAF_CASE(4); break;
@@ -1106,18 +1169,22 @@ void leaf_dispatch(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, in
 }
 
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
-                       uint8_t *node_out, const uint8_t *cut_f, const uint8_t *cut_c, int depth,
-                       bool routed, const int8_t *y, const float *v, const double *F,
-                       uint64_t seed, int tree, double alpha, double eta, int blocks,
-                       double *leaf_partial, unsigned *ticket, double *leaf_out, int *err,
-                       hipStream_t s) {
+                       uint8_t *node_out, const ParentCuts &pc, int depth, bool routed,
+                       const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
+                       double alpha, int blocks, double *leaf_partial, int *err, hipStream_t s) {
+    const ParentCuts none{};
     if (routed)
-        leaf_dispatch<true>(blocks, s, xb, ldb, n, d, node_in, node_out, cut_f, cut_c, depth, y,
-                            v, F, seed, tree, alpha, eta, leaf_partial, ticket, leaf_out, err);
+        leaf_dispatch<true>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, y, v, F, seed,
+                            tree, alpha, leaf_partial, err);
     else
-        leaf_dispatch<false>(blocks, s, xb, ldb, n, d, node_in, nullptr, nullptr, nullptr, depth,
-                             y, v, F, seed, tree, alpha, eta, leaf_partial, ticket, leaf_out,
-                             err);
+        leaf_dispatch<false>(blocks, s, xb, ldb, n, d, node_in, nullptr, none, depth, y, v, F,
+                             seed, tree, alpha, leaf_partial, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, double eta,
+                                double *leaf_out, hipStream_t s) {
+    leaf_finalize_kernel<<<1, 256, 0, s>>>(leaf_partial, blocks, 1 << depth, eta, leaf_out);
     return hipGetLastError();
 }
 
