@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdlib>
 #include <cstdint>
 
 namespace fbdt {
@@ -1030,23 +1031,45 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
     if (npg > nodes) npg = nodes;
     hs.nodes_per_group = npg;
     hs.node_groups = (nodes + npg - 1) / npg;
-    // Features per workgroup.  Each feature group re-reads the chunk's node
-    // ids and weights (5 bytes per event) and each event chunk adds one
-    // partial histogram to write and to sum; measured sweeps over 0.5M-10M
-    // events and 20-40 features put the optimum near four feature groups,
-    // capped by LDS, with one workgroup per CU.
-    const int t_threads = threads > 0 ? threads : (n >= (1 << 20) ? 1024 : 512);
-    int f = fpg > 0 ? fpg : (d + 3) / 4;
-    if (f > d) f = d;
-    if (f < 1) f = 1;
+    // Features per workgroup.  A 1024-thread workgroup fills a CU, so the
+    // pass runs as one round of at most cu_count workgroups: groups * chunks
+    // with chunks <= cu_count / groups and at least 16 events per thread.
+    // Take the feature-group size that brings the most workgroups, ties to
+    // about eight feature groups (each group re-reads the chunk's node ids
+    // and weights; each chunk writes one more partial histogram).
+    const int t_threads = threads > 0 ? threads : 1024;
+    int f = 1;
+    if (fpg > 0) {
+        f = fpg < d ? fpg : d;
+    } else {
+        const int64_t cmax = n / (16LL * t_threads) > 0 ? n / (16LL * t_threads) : 1;
+        int64_t best_w = -1;
+        int best_dist = 1 << 30;
+        for (int cand = 1; cand <= d; ++cand) {
+            if ((size_t)npg * cand * per_node_feature > max_lds) break;
+            const int g = ((d + cand - 1) / cand) * hs.node_groups;
+            int64_t c = cu_count / g;
+            if (c > cmax) c = cmax;
+            if (c < 1) c = 1;
+            const int64_t wgs = c * g;
+            const int dist = std::abs((d + cand - 1) / cand - 8);
+            if (wgs <= cu_count && (wgs > best_w || (wgs == best_w && dist < best_dist))) {
+                best_w = wgs;
+                best_dist = dist;
+                f = cand;
+            }
+        }
+    }
     while (f > 1 && (size_t)npg * f * per_node_feature > max_lds) --f;
     hs.features_per_group = f;
     hs.feature_groups = (d + f - 1) / f;
     hs.threads = t_threads;
     const int groups = hs.feature_groups * hs.node_groups;
-    // one workgroup per CU by default: every extra event chunk adds one more
-    // partial histogram to write and to sum
-    int64_t c = chunks > 0 ? chunks : ((int64_t)cu_count + groups - 1) / groups;
+    // at most one workgroup per CU by default (a 1024-thread workgroup fills
+    // a CU): a few workgroups more than CUs run as a second round and nearly
+    // double the pass; every extra event chunk also adds one more partial
+    // histogram to write and to sum
+    int64_t c = chunks > 0 ? chunks : (int64_t)cu_count / groups;
     const int64_t min_events = 16LL * hs.threads;
     const int64_t cmax = (n + min_events - 1) / min_events;
     if (chunks <= 0 && c > cmax) c = cmax;
