@@ -215,7 +215,14 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
 /*
  * Launch-shape overrides for sweeps; value 0 restores the default.
  * Names: "hist_features_per_group", "hist_event_chunks", "hist_threads",
- * "apply_threads".  Returns FBDT_E_INVAL for an unknown name.
+ * "apply_threads".
+ * "fit_graphs" (default 1): fbdt_fit records the kernel launches of its
+ * boosting loop as a HIP graph on first use of an argument set (device,
+ * buffer addresses, sizes, parameters, launch shapes) and replays it on later
+ * calls with the same set; up to 4 graphs per device are kept, and growing the
+ * device workspace drops them.  0 launches every kernel one by one.  Graphs
+ * are not used while any fit kernel kind is being timed.
+ * Returns FBDT_E_INVAL for an unknown name.
  */
 int fbdt_set_option(const char *name, int64_t value);
 

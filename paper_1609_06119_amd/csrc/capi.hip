@@ -72,6 +72,7 @@ int device_info(int dev, DeviceInfo *out) {
         int cu = 0, lds = 0;
         HIP_TRY(hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev));
         HIP_TRY(hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
+        HIP_TRY(prepare_kernels((size_t)lds));
         di.cu_count = cu;
         di.max_lds = (size_t)lds;
     }
@@ -81,7 +82,7 @@ int device_info(int dev, DeviceInfo *out) {
 
 // ---- options --------------------------------------------------------------
 std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0},
-    opt_apply_threads{0};
+    opt_apply_threads{0}, opt_fit_graphs{1};
 
 // ---- timing ---------------------------------------------------------------
 struct PendingTiming {
@@ -134,15 +135,41 @@ struct Timed {
 };
 
 // ---- per-device scratch ---------------------------------------------------
+// Launch sequence of a fit's boosting loop, captured once per distinct set
+// of arguments and replayed (kernel launches only).
+struct GraphKey {
+    const void *xb, *y, *w;
+    int64_t n, ldb;
+    int d, n_bins, depth, n_trees, scale, lblocks;
+    double eta, alpha;
+    uint64_t seed;
+    int64_t fpg, chunks, threads;
+    bool operator==(const GraphKey &o) const {
+        return xb == o.xb && y == o.y && w == o.w && n == o.n && ldb == o.ldb && d == o.d &&
+               n_bins == o.n_bins && depth == o.depth && n_trees == o.n_trees &&
+               scale == o.scale && lblocks == o.lblocks && eta == o.eta && alpha == o.alpha &&
+               seed == o.seed && fpg == o.fpg && chunks == o.chunks && threads == o.threads;
+    }
+};
+
 struct Arena {
     std::mutex mu;
     void *ptr = nullptr;
     size_t size = 0;
+    std::vector<std::pair<GraphKey, hipGraphExec_t>> graphs;  // oldest first
+    hipStream_t capture = nullptr;  // records launches only; never runs work
 };
 Arena g_arena[64];
+constexpr size_t kMaxGraphs = 4;
+
+void drop_graphs(Arena &a) {
+    for (auto &g : a.graphs) (void)hipGraphExecDestroy(g.second);
+    a.graphs.clear();
+}
 
 int arena_reserve(Arena &a, size_t bytes) {
     if (bytes <= a.size) return FBDT_OK;
+    drop_graphs(a);  // captured launches point into the old allocation
     if (a.ptr) {
         HIP_TRY(hipFree(a.ptr));
         a.ptr = nullptr;
@@ -234,6 +261,8 @@ int fbdt_set_option(const char *name, int64_t value) {
         if (value != 0 && (value % 64 != 0 || value > 1024))
             return fail(FBDT_E_INVAL, "hist_threads must be a multiple of 64, <= 1024");
         opt_hist_threads = value;
+    } else if (!strcmp(name, "fit_graphs")) {
+        opt_fit_graphs = value != 0;
     } else if (!strcmp(name, "apply_threads")) {
         if (value != 0 && (value % 64 != 0 || value > 1024))
             return fail(FBDT_E_INVAL, "apply_threads must be a multiple of 64, <= 1024");
@@ -457,50 +486,92 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
 
     const uint64_t seed = p->seed;
     const double alpha = p->subsample, eta = p->shrinkage;
-    for (int t = 0; t < T; ++t) {
-        {
-            Timed tm(FBDT_K_TREE_PREP, s, (double)n * 30.0);
-            HIP_TRY(launch_tree_prep(y, w, fb.F, t == 0 ? fb.f0 : nullptr,
-                                     t == 0 ? nullptr : fb.node[D & 1],
-                                     t == 0 ? nullptr : fb.leaf + (size_t)(t - 1) * nleaf, D, n,
-                                     seed, t, alpha, fb.w, nullptr, s));
-            tm.done();
-        }
-        uint8_t *cf = fb.cut_feature + (size_t)t * nin;
-        uint8_t *cc = fb.cut_bin + (size_t)t * nin;
-        double *cg = fb.gain + (size_t)t * nin;
-        for (int l = 0; l < D; ++l) {
-            // the previous layer's candidates give the cuts this pass routes
-            // with; workgroup 0 records them in the model
-            const int plo = l >= 1 ? (1 << (l - 1)) - 1 : 0;
-            ParentCuts pc;
-            if (l >= 1) pc = ParentCuts{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
+    // every launch of the boosting loop, in stream order (no host sync)
+    auto enqueue_trees = [&](hipStream_t st) -> int {
+        for (int t = 0; t < T; ++t) {
             {
-                Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, l, true));
-                HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
-                                         l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
-                                         l >= 1 ? fb.node[l & 1] : nullptr, fb.w, pc, l, true,
-                                         scale, fb.partial, fb.small, fb.err, s));
+                Timed tm(FBDT_K_TREE_PREP, st, (double)n * 30.0);
+                HIP_TRY(launch_tree_prep(y, w, fb.F, t == 0 ? fb.f0 : nullptr,
+                                         t == 0 ? nullptr : fb.node[D & 1],
+                                         t == 0 ? nullptr : fb.leaf + (size_t)(t - 1) * nleaf, D, n,
+                                         seed, t, alpha, fb.w, nullptr, st));
                 tm.done();
             }
+            uint8_t *cf = fb.cut_feature + (size_t)t * nin;
+            uint8_t *cc = fb.cut_bin + (size_t)t * nin;
+            double *cg = fb.gain + (size_t)t * nin;
+            for (int l = 0; l < D; ++l) {
+                // the previous layer's candidates give the cuts this pass routes
+                // with; workgroup 0 records them in the model
+                const int plo = l >= 1 ? (1 << (l - 1)) - 1 : 0;
+                ParentCuts pc;
+                if (l >= 1) pc = ParentCuts{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
+                {
+                    Timed tm(FBDT_K_HISTOGRAM, st, hist_algorithmic_bytes(n, d, n_bins, l, true));
+                    HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
+                                             l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
+                                             l >= 1 ? fb.node[l & 1] : nullptr, fb.w, pc, l, true,
+                                             scale, fb.partial, fb.small, fb.err, st));
+                    tm.done();
+                }
+                {
+                    Timed tm(FBDT_K_BEST_CUTS, st);
+                    HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, scale, fb.small, nullptr,
+                                             1 << l, d, n_bins, fb.cand_gain, fb.cand_cut, st));
+                    tm.done();
+                }
+            }
             {
-                Timed tm(FBDT_K_BEST_CUTS, s);
-                HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, scale, fb.small, nullptr,
-                                         1 << l, d, n_bins, fb.cand_gain, fb.cand_cut, s));
+                const int plo = (1 << (D - 1)) - 1;
+                const ParentCuts pc{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
+                Timed tm(FBDT_K_LEAF, st);
+                HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
+                                    fb.node[D & 1], pc, D, true, y, w, fb.F, seed, t, alpha, lblocks,
+                                    fb.leaf_partial, fb.err, st));
+                HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, eta,
+                                             fb.leaf + (size_t)t * nleaf, st));
                 tm.done();
             }
         }
-        {
-            const int plo = (1 << (D - 1)) - 1;
-            const ParentCuts pc{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
-            Timed tm(FBDT_K_LEAF, s);
-            HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
-                                fb.node[D & 1], pc, D, true, y, w, fb.F, seed, t, alpha, lblocks,
-                                fb.leaf_partial, fb.err, s));
-            HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, eta,
-                                         fb.leaf + (size_t)t * nleaf, s));
-            tm.done();
+        return FBDT_OK;
+    };
+    const int timed_kinds = (1 << FBDT_K_TREE_PREP) | (1 << FBDT_K_HISTOGRAM) |
+                            (1 << FBDT_K_BEST_CUTS) | (1 << FBDT_K_LEAF);
+    if (opt_fit_graphs.load() && !(g_timing.load() & timed_kinds)) {
+        const GraphKey key{xb, y, w, n, ldb, d, n_bins, D, T, scale, lblocks, eta, alpha, seed,
+                           opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load()};
+        hipGraphExec_t exec = nullptr;
+        for (auto &g : a.graphs)
+            if (g.first == key) exec = g.second;
+        if (!exec) {
+            // captured on a stream of the library's own, since the caller's may
+            // be the null stream, which cannot be captured; the graph then runs
+            // on the caller's stream
+            if (!a.capture) HIP_TRY(hipStreamCreateWithFlags(&a.capture, hipStreamNonBlocking));
+            HIP_TRY(hipStreamBeginCapture(a.capture, hipStreamCaptureModeThreadLocal));
+            const int qrc = enqueue_trees(a.capture);
+            hipGraph_t graph = nullptr;
+            const hipError_t ce = hipStreamEndCapture(a.capture, &graph);
+            if (qrc != FBDT_OK || ce != hipSuccess) {
+                if (graph) (void)hipGraphDestroy(graph);
+                if (qrc != FBDT_OK) return qrc;
+                return fail(FBDT_E_DEVICE, "capturing the boosting loop failed: %s",
+                            hipGetErrorString(ce));
+            }
+            const hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+            (void)hipGraphDestroy(graph);
+            if (ie != hipSuccess)
+                return fail(FBDT_E_DEVICE, "instantiating the boosting loop failed: %s",
+                            hipGetErrorString(ie));
+            if (a.graphs.size() >= kMaxGraphs) {
+                (void)hipGraphExecDestroy(a.graphs.front().second);
+                a.graphs.erase(a.graphs.begin());
+            }
+            a.graphs.push_back({key, exec});
         }
+        HIP_TRY(hipGraphLaunch(exec, s));
+    } else if ((rc = enqueue_trees(s))) {
+        return rc;
     }
     if (score_out)
         HIP_TRY(launch_tree_prep(y, w, fb.F, nullptr, fb.node[D & 1],
@@ -652,7 +723,7 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     }
     ApplyShape as = plan_apply(n, m->n_features, T, D, di.cu_count, di.max_lds,
                                (int)opt_apply_threads.load());
-    if (as.lds_bytes > di.max_lds)
+    if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
         return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
                     "apply_threads)", as.lds_bytes, di.max_lds);
     Timed tm(FBDT_K_APPLY, s, (double)n * (m->n_features + 4));

@@ -60,6 +60,11 @@ constexpr size_t kHistStaticLdsReserve = 1024;
 // dummy and one out-of-range counter (8 bytes) per lane of a wavefront
 constexpr size_t kHistExtraLds = 2 * 64 * 8;
 
+// Sets the per-kernel attributes the launchers rely on (dynamic LDS above
+// 64 KiB) for the current device; called once per device before any launch,
+// so that a launch sequence holds nothing but kernel launches.
+hipError_t prepare_kernels(size_t max_lds);
+
 hipError_t launch_fill_u32(void *p, uint32_t value, size_t count, hipStream_t s);
 
 hipError_t launch_validate(const int8_t *y, const float *v, int64_t n, double *class_partial,

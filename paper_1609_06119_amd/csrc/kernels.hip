@@ -26,6 +26,7 @@ namespace fbdt {
 namespace {
 
 constexpr int kWave = 64;
+constexpr int kBcWaves = 16;   // wavefronts per (node, feature) in best_cuts
 
 // SplitMix64 (Steele, Lea & Flood, OOPSLA 2014): output number k (0-based)
 // of the generator seeded with `seed` mixes the state seed + (k + 1) * gamma.
@@ -259,10 +260,11 @@ __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restric
 
 // ---------------------------------------------------------------------------
 // Layer histogram.  Workgroup (chunk p, feature group g, node group h) keeps
-// H[node in h][feature in g][bin][class] in LDS as float64, adds every
-// sampled event of its event chunk with ds_add_f64, and writes its partial
-// histogram once at the end; best_cuts sums the chunk partials in a fixed
-// order.  Each thread handles 16 consecutive events per step: four float4
+// H[node in h][feature in g][bin][class] in LDS as 64-bit fixed point
+// (weight * 2^scale), adds every sampled event of its event chunk with a
+// 64-bit integer LDS atomic, and writes its partial histogram once at the
+// end; integer sums are exact, so the result is independent of the order of
+// the adds, and best_cuts sums the chunk partials.  Each thread handles 16 consecutive events per step: four float4
 // loads of weights, one 16-byte load of node ids and one 16-byte load of
 // codes per feature, all independent of each other.
 //
@@ -535,16 +537,17 @@ __global__ void sum_blocks_kernel(const double *__restrict__ block_partial, int 
 // partition as cut c-1, has the same gain in exact arithmetic, and is
 // skipped so that the lower cut wins the tie independently of rounding.
 template <bool FIXED>
-__global__ __launch_bounds__(256) void best_cuts_kernel(
+__global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
     const uint64_t *__restrict__ partial, int chunks, int scale, double *__restrict__ small,
     const double *__restrict__ hist, int nodes, int d, int nbins,
     double *__restrict__ cand_gain, int *__restrict__ cand_cut) {
 #pragma clang fp contract(off)
-    // one workgroup of 4 wavefronts per (node, feature); wavefront w sums the
-    // fixed-point chunk partials w, w + 4, ... (integer sums: exact in any
-    // order); wavefront 0 adds the four sums, converts them to float64 and
-    // adds the side histogram of weights below the grid
-    __shared__ uint64_t red[4][kWave][8];
+    // one workgroup of kBcWaves wavefronts per (node, feature); wavefront w
+    // sums the fixed-point chunk partials w, w + kBcWaves, ... (integer sums:
+    // exact in any order), so that all chunk loads are in flight together;
+    // wavefront 0 adds the sums, converts them to float64 and adds the side
+    // histogram of weights below the grid
+    __shared__ uint64_t red[kBcWaves][kWave][8];
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
     const int pair = blockIdx.x;
@@ -557,30 +560,28 @@ __global__ __launch_bounds__(256) void best_cuts_kernel(
     double hs[4] = {0.0, 0.0, 0.0, 0.0}, hb[4] = {0.0, 0.0, 0.0, 0.0};
     if (FIXED) {
         uint64_t us[4] = {0, 0, 0, 0}, ub[4] = {0, 0, 0, 0};
+        const size_t stride_p = (size_t)nodes * d * nbins * 2;
         if (nb == 4) {
-            const size_t stride_p = (size_t)nodes * d * nbins * 2;
-            // four chunks per step so that their loads are in flight together
             int p = wave;
-            for (; p + 12 < chunks; p += 16) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(
-                        partial + (size_t)(p + 4 * q) * stride_p + off);
-                    const ulonglong2 a0 = src[0], a1 = src[1], a2 = src[2], a3 = src[3];
-                    us[0] += a0.x; ub[0] += a0.y; us[1] += a1.x; ub[1] += a1.y;
-                    us[2] += a2.x; ub[2] += a2.y; us[3] += a3.x; ub[3] += a3.y;
-                }
-            }
-            for (; p < chunks; p += 4) {
-                const ulonglong2 *src =
+            for (; p + kBcWaves < chunks; p += 2 * kBcWaves) {   // two chunks in flight
+                const ulonglong2 *s0 =
                     reinterpret_cast<const ulonglong2 *>(partial + (size_t)p * stride_p + off);
-                const ulonglong2 a0 = src[0], a1 = src[1], a2 = src[2], a3 = src[3];
+                const ulonglong2 *s1 = reinterpret_cast<const ulonglong2 *>(
+                    partial + (size_t)(p + kBcWaves) * stride_p + off);
+                const ulonglong2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
+                const ulonglong2 c0 = s1[0], c1 = s1[1], c2 = s1[2], c3 = s1[3];
+                us[0] += a0.x + c0.x; ub[0] += a0.y + c0.y; us[1] += a1.x + c1.x; ub[1] += a1.y + c1.y;
+                us[2] += a2.x + c2.x; ub[2] += a2.y + c2.y; us[3] += a3.x + c3.x; ub[3] += a3.y + c3.y;
+            }
+            if (p < chunks) {
+                const ulonglong2 *s0 =
+                    reinterpret_cast<const ulonglong2 *>(partial + (size_t)p * stride_p + off);
+                const ulonglong2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
                 us[0] += a0.x; ub[0] += a0.y; us[1] += a1.x; ub[1] += a1.y;
                 us[2] += a2.x; ub[2] += a2.y; us[3] += a3.x; ub[3] += a3.y;
             }
         } else if (nb > 0) {
-            const size_t stride_p = (size_t)nodes * d * nbins * 2;
-            for (int p = wave; p < chunks; p += 4) {
+            for (int p = wave; p < chunks; p += kBcWaves) {
                 const uint64_t *src = partial + (size_t)p * stride_p + off;
                 for (int e = 0; e < nb; ++e) {
                     us[e] += src[2 * e];
@@ -595,14 +596,18 @@ __global__ __launch_bounds__(256) void best_cuts_kernel(
         }
         __syncthreads();
         if (wave != 0) return;
+        uint64_t ts[4] = {0, 0, 0, 0}, tb[4] = {0, 0, 0, 0};
+        for (int wv = 0; wv < kBcWaves; ++wv) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                ts[e] += red[wv][lane][e];
+                tb[e] += red[wv][lane][4 + e];
+            }
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const uint64_t ts = red[0][lane][e] + red[1][lane][e] + red[2][lane][e] +
-                                red[3][lane][e];
-            const uint64_t tb = red[0][lane][4 + e] + red[1][lane][4 + e] +
-                                red[2][lane][4 + e] + red[3][lane][4 + e];
-            hs[e] = ldexp((double)ts, -scale);
-            hb[e] = ldexp((double)tb, -scale);
+            hs[e] = ldexp((double)ts[e], -scale);
+            hb[e] = ldexp((double)tb[e], -scale);
         }
         for (int e = 0; e < nb; ++e) {   // side histogram, cleared for the next layer
             hs[e] += small[off + 2 * e];
@@ -814,11 +819,11 @@ __global__ __launch_bounds__(256) void leaf_kernel(
 // adds value t % nv over blocks t / nv, t / nv + stripes, ...; the stripes
 // are then added in order) and the boost weights eta * num / den (0 when
 // den = 0).
-__global__ __launch_bounds__(256) void leaf_finalize_kernel(const double *__restrict__ leaf_partial,
-                                                            int nblocks, int nleaf, double eta,
-                                                            double *__restrict__ leaf_out) {
+__global__ __launch_bounds__(1024) void leaf_finalize_kernel(const double *__restrict__ leaf_partial,
+                                                             int nblocks, int nleaf, double eta,
+                                                             double *__restrict__ leaf_out) {
 #pragma clang fp contract(off)
-    __shared__ double red[256];
+    __shared__ double red[1024];
     const int nv = 2 * nleaf;
     const int stripes = blockDim.x / nv;
     const int t = threadIdx.x;
@@ -976,19 +981,29 @@ int grid_for(int64_t n, int threads, int cap) {
     return (int)g;
 }
 
-// Raises a kernel's dynamic-LDS limit above 64 KiB when a launch needs it;
-// a launch beyond the device limit then fails and reports its own error.
+// Raises a kernel's dynamic-LDS limit to what the device allows beside the
+// kernel's static LDS.
 template <typename K>
-void allow_lds(K kernel, size_t bytes) {
-    if (bytes + kHistStaticLdsReserve <= 65536) return;
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e != hipSuccess) (void)hipGetLastError();
+hipError_t allow_lds(K kernel, size_t max_lds) {
+    if (max_lds <= kHistStaticLdsReserve) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)(max_lds - kHistStaticLdsReserve));
 }
 
 }  // namespace
 
 // ===========================================================================
+hipError_t prepare_kernels(size_t max_lds) {
+    const hipError_t e[] = {
+        allow_lds(hist_kernel<false, 0>, max_lds), allow_lds(hist_kernel<true, 0>, max_lds),
+        allow_lds(hist_kernel<true, 1>, max_lds),  allow_lds(hist_kernel<true, 2>, max_lds),
+        allow_lds(hist_kernel<true, 4>, max_lds),  allow_lds(apply_kernel, max_lds)};
+    for (hipError_t x : e)
+        if (x != hipSuccess) return x;
+    return hipSuccess;
+}
+
 hipError_t launch_fill_u32(void *p, uint32_t value, size_t count, hipStream_t s) {
     if (count == 0) return hipSuccess;
     fill_u32_kernel<<<grid_for((int64_t)count, 256, 1024), 256, 0, s>>>(
@@ -1099,7 +1114,6 @@ hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, i
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
                           const ParentCuts &pc, int layer, int scale, uint64_t *partial,
                           double *small, int *err, hipStream_t s) {
-    allow_lds(hist_kernel<ROUTED, NP>, hs.lds_bytes);
     hist_kernel<ROUTED, NP><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.rec_f,
         pc.rec_c, pc.rec_g, layer, hs.features_per_group, hs.feature_groups, hs.nodes_per_group,
@@ -1146,10 +1160,10 @@ hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, doub
                             const double *hist, int n_nodes, int d, int n_bins,
                             double *cand_gain, int *cand_cut, hipStream_t s) {
     if (partial)
-        best_cuts_kernel<true><<<n_nodes * d, 4 * kWave, 0, s>>>(
+        best_cuts_kernel<true><<<n_nodes * d, kBcWaves * kWave, 0, s>>>(
             partial, chunks, scale, small, nullptr, n_nodes, d, n_bins, cand_gain, cand_cut);
     else
-        best_cuts_kernel<false><<<n_nodes * d, 4 * kWave, 0, s>>>(
+        best_cuts_kernel<false><<<n_nodes * d, kBcWaves * kWave, 0, s>>>(
             nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cand_gain, cand_cut);
     return hipGetLastError();
 }
@@ -1207,7 +1221,7 @@ hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const u
 
 hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, double eta,
                                 double *leaf_out, hipStream_t s) {
-    leaf_finalize_kernel<<<1, 256, 0, s>>>(leaf_partial, blocks, 1 << depth, eta, leaf_out);
+    leaf_finalize_kernel<<<1, 1024, 0, s>>>(leaf_partial, blocks, 1 << depth, eta, leaf_out);
     return hipGetLastError();
 }
 
@@ -1228,7 +1242,8 @@ ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_coun
     const size_t xtile = (size_t)d_used * (as.threads + 4);
     const size_t per_tree = (size_t)nleaf * 8 + (size_t)nin * 2;
     size_t budget = 65536;
-    if (budget < xtile + per_tree + 64) budget = max_lds;
+    if (budget < xtile + per_tree + 64)
+        budget = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
     size_t room = budget > xtile + 64 ? budget - xtile - 64 : 0;
     int64_t tpc = (int64_t)(room / per_tree);
     if (tpc < 1) tpc = 1;
@@ -1246,7 +1261,6 @@ ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_coun
 hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
                         const uint16_t *cuts, const double *leaves, int n_trees, int depth,
                         double f0, float *prob, double *score, hipStream_t s) {
-    allow_lds(apply_kernel, as.lds_bytes);
     apply_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(xb, ldb, n, as.d_used, cuts, leaves,
                                                             n_trees, depth, as.trees_per_chunk,
                                                             f0, prob, score);

@@ -40,10 +40,12 @@ def _defaults():
     for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads",
                  "apply_threads"):
         fb.set_option(name, 0)
+    fb.set_option("fit_graphs", 1)
     yield
     for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads",
                  "apply_threads"):
         fb.set_option(name, 0)
+    fb.set_option("fit_graphs", 1)
 
 
 # ------------------------------------------------------------------ binning
@@ -330,6 +332,45 @@ def test_fit_and_apply_match_oracle(case):
     op, oF = O.apply(om, xb)
     assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
     assert np.allclose(ascore.cpu().numpy(), oF, rtol=1e-9, atol=1e-12)
+
+
+def test_fit_graph_replays_match_eager_fit():
+    """The boosting loop is captured once per argument set and replayed; every
+    replay, with other device work and other fits in between, gives the model
+    and scores of a fit that launches its kernels one by one."""
+    spec = CONFIGS[2]
+    ds = make_training_set(2, n_events=60_013)
+    n = ds["x"].shape[1]
+    _, codes = fb.bin(dev(ds["x"]), spec.n_bins)
+    y = dev(ds["y"])
+    args = (spec.n_bins, 3, 12, spec.shrinkage, spec.subsample)
+
+    def run(seed):
+        score = torch.empty(n, dtype=torch.float64, device="cuda")
+        m = fb.fit(codes, y, *args, seed, score_out=score).export()
+        return m, score.cpu().numpy()
+
+    def same(a, b):
+        (ma, fa), (mb, fb_) = a, b
+        for k in ("cut_feature", "cut_bin", "gain", "leaf"):
+            assert np.array_equal(ma[k], mb[k]), k
+        assert ma["f0"] == mb["f0"]
+        assert np.array_equal(fa, fb_)
+
+    fb.set_option("fit_graphs", 0)
+    eager = {s: run(s) for s in (11, 12, 13, 14, 15)}
+    fb.set_option("fit_graphs", 1)
+    junk = torch.randn(1 << 20, device="cuda")
+    for rep in range(3):
+        say(f"graph replay {rep}")
+        same(run(11), eager[11])
+        junk.mul_(1.0001).add_(0.5)             # eager work between replays
+        torch.cuda.synchronize()
+        same(run(12), eager[12])
+    for s in (13, 14, 15, 11):                  # more keys than the cache holds
+        same(run(s), eager[s])
+    fb.set_option("fit_graphs", 0)              # eager again after replays
+    same(run(11), eager[11])
 
 
 # ------------------------------------------------------------------ apply
