@@ -443,6 +443,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                         plans[l].lds_bytes, di.max_lds);
     }
     const int lblocks = leaf_blocks(n, di.cu_count);
+    const bool fused = D <= kFusedLeafDepth;
     const int max_nodes = 1 << (D - 1);
 
     Arena &a = g_arena[dev];
@@ -491,10 +492,15 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
         for (int t = 0; t < T; ++t) {
             {
                 Timed tm(FBDT_K_TREE_PREP, st, (double)n * 30.0);
+                // the previous tree's boost weights: summed here from the leaf
+                // pass partials (shallow trees; workgroup 0 records them), or
+                // from the model after leaf_finalize
+                double *prev = t == 0 ? nullptr : fb.leaf + (size_t)(t - 1) * nleaf;
                 HIP_TRY(launch_tree_prep(y, w, fb.F, t == 0 ? fb.f0 : nullptr,
-                                         t == 0 ? nullptr : fb.node[D & 1],
-                                         t == 0 ? nullptr : fb.leaf + (size_t)(t - 1) * nleaf, D, n,
-                                         seed, t, alpha, fb.w, nullptr, st));
+                                         t == 0 ? nullptr : fb.node[D & 1], fused ? nullptr : prev,
+                                         t > 0 && fused ? fb.leaf_partial : nullptr, lblocks, eta,
+                                         fused ? prev : nullptr, D, n, seed, t, alpha, fb.w,
+                                         nullptr, di.cu_count, st));
                 tm.done();
             }
             uint8_t *cf = fb.cut_feature + (size_t)t * nin;
@@ -528,8 +534,9 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
                                     fb.node[D & 1], pc, D, true, y, w, fb.F, seed, t, alpha, lblocks,
                                     fb.leaf_partial, fb.err, st));
-                HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, eta,
-                                             fb.leaf + (size_t)t * nleaf, st));
+                if (!fused || t == T - 1)
+                    HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, eta,
+                                                 fb.leaf + (size_t)t * nleaf, st));
                 tm.done();
             }
         }
@@ -575,8 +582,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     }
     if (score_out)
         HIP_TRY(launch_tree_prep(y, w, fb.F, nullptr, fb.node[D & 1],
-                                 fb.leaf + (size_t)(T - 1) * nleaf, D, n, seed, T, alpha, nullptr,
-                                 score_out, s));
+                                 fb.leaf + (size_t)(T - 1) * nleaf, nullptr, 0, 0.0, nullptr, D, n,
+                                 seed, T, alpha, nullptr, score_out, di.cu_count, s));
 
     fbdt_model *m = new (std::nothrow) fbdt_model;
     if (!m) return fail(FBDT_E_DEVICE, "out of host memory");
@@ -739,10 +746,14 @@ int fbdt_tree_weights(const int8_t *y, const float *v, const double *F, int64_t 
     if (n < 1) return fail(FBDT_E_INVAL, "n must be >= 1");
     if (tree < 0) return fail(FBDT_E_INVAL, "tree must be >= 0");
     if (!(alpha > 0.0 && alpha <= 1.0)) return fail(FBDT_E_INVAL, "alpha must be in (0, 1]");
+    int rc, dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     Timed tm(FBDT_K_TREE_PREP, s, (double)n * 17.0);
-    HIP_TRY(launch_tree_prep(y, v, const_cast<double *>(F), nullptr, nullptr, nullptr, 1, n, seed,
-                             tree, alpha, w_out, nullptr, s));
+    HIP_TRY(launch_tree_prep(y, v, const_cast<double *>(F), nullptr, nullptr, nullptr, nullptr, 0,
+                             0.0, nullptr, 1, n, seed, tree, alpha, w_out, nullptr, di.cu_count,
+                             s));
     tm.done();
     return FBDT_OK;
 }

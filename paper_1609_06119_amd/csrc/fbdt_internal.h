@@ -26,7 +26,7 @@ struct HistShape {
     int nodes_per_group;      // nodes whose histograms one workgroup keeps in LDS
     int node_groups;          // ceil(2^layer / nodes_per_group)
     int chunks;               // event chunks, each merged once per layer
-    int64_t chunk_events;     // events per chunk (a multiple of 4)
+    int64_t chunk_events;     // events per chunk (a multiple of kHistE = 8)
     int threads;              // threads per workgroup
     int blocks;               // grid size (chunks * groups, rounded up to the XCD count)
     size_t lds_bytes;         // dynamic LDS per workgroup
@@ -56,9 +56,9 @@ constexpr int kValidateBlocks = 256;
 // LDS kept aside for a kernel's static shared arrays when sizing its
 // dynamic LDS (the histogram kernel's cut table takes 128 bytes)
 constexpr size_t kHistStaticLdsReserve = 1024;
-// dynamic LDS of the histogram kernel beyond the histogram itself: one
-// dummy and one out-of-range counter (8 bytes) per lane of a wavefront
-constexpr size_t kHistExtraLds = 2 * 64 * 8;
+// features whose codes one histogram workgroup holds in registers per step
+// (the most features a workgroup takes)
+constexpr int kHistFMax = 8;
 
 // Sets the per-kernel attributes the launchers rely on (dynamic LDS above
 // 64 KiB) for the current device; called once per device before any launch,
@@ -72,13 +72,22 @@ hipError_t launch_validate(const int8_t *y, const float *v, int64_t n, double *c
 hipError_t launch_initial_score(const double *class_partial, double *f0, int *err,
                                 hipStream_t s);
 
+// Deepest tree whose boost weights tree_prep sums from the leaf-pass
+// partials itself (2^depth leaves, two sums each, per workgroup partial).
+constexpr int kFusedLeafDepth = 4;
+
 // Score update of the previous tree (if any) and re-weighting of tree `tree`.
-//  update_from_leaf: F += leaf_prev[leaf_node - 2^depth]; else if f0 != null: F = *f0.
+//  leaf_partial != null (depth <= kFusedLeafDepth): the previous tree's boost
+//    weights are summed from the leaf-pass partials (lblocks of them) and
+//    eta; leaf_rec (optional) receives them;
+//  else leaf_prev != null: the previous tree's boost weights;
+//  either way F += weight[leaf_node - 2^depth]; else if f0 != null: F = *f0.
 //  w may be null (score update only); score_out (optional) receives F.
 hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const double *f0,
-                            const uint8_t *leaf_node, const double *leaf_prev, int depth,
-                            int64_t n, uint64_t seed, int tree, double alpha, float *w,
-                            double *score_out, hipStream_t s);
+                            const uint8_t *leaf_node, const double *leaf_prev,
+                            const double *leaf_partial, int lblocks, double eta, double *leaf_rec,
+                            int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
+                            double *score_out, int cu_count, hipStream_t s);
 
 // fpg, chunks, threads: launch-shape overrides (0 = default).
 HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,

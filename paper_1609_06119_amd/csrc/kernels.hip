@@ -27,6 +27,7 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kBcWaves = 16;   // wavefronts per (node, feature) in best_cuts
+constexpr int kHistE = 8;      // events per thread and step of the histogram pass
 
 // SplitMix64 (Steele, Lea & Flood, OOPSLA 2014): output number k (0-based)
 // of the generator seeded with `seed` mixes the state seed + (k + 1) * gamma.
@@ -144,23 +145,81 @@ __global__ __launch_bounds__(256) void initial_score_kernel(const double *__rest
 }
 
 // ---------------------------------------------------------------------------
+// Sum of the workgroup partials of the leaf pass in a fixed order by a
+// workgroup of kLeafReduceThreads threads (thread t adds value t % nv over
+// blocks t / nv, t / nv + stripes, ...; the stripes are then added
+// pairwise), and the boost weights eta * num / den (0 when den = 0) into
+// s_leaf[0, nleaf).  Every thread of the workgroup calls it; red holds
+// kLeafReduceThreads doubles of LDS.  The same order everywhere gives the
+// same weights in every workgroup that calls it.
+constexpr int kLeafReduceThreads = 1024;
+
+__device__ void reduce_leaf_partials(const double *__restrict__ leaf_partial, int nblocks,
+                                     int nleaf, double eta, double *red, double *s_leaf) {
+#pragma clang fp contract(off)
+    const int nv = 2 * nleaf;
+    const int stripes = kLeafReduceThreads / nv;
+    const int t = threadIdx.x;
+    if (t < stripes * nv) {
+        const int val = t % nv, st = t / nv;
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        int b = st;
+        for (; b + 3 * stripes < nblocks; b += 4 * stripes) {
+            s0 += leaf_partial[(size_t)b * nv + val];
+            s1 += leaf_partial[(size_t)(b + stripes) * nv + val];
+            s2 += leaf_partial[(size_t)(b + 2 * stripes) * nv + val];
+            s3 += leaf_partial[(size_t)(b + 3 * stripes) * nv + val];
+        }
+        for (; b < nblocks; b += stripes) s0 += leaf_partial[(size_t)b * nv + val];
+        red[t] = (s0 + s1) + (s2 + s3);
+    }
+    __syncthreads();
+    // stripes (a power of two) added pairwise: red[st] += red[st + half]
+    for (int half = stripes / 2; half >= 1; half >>= 1) {
+        if (t < half * nv) red[t] += red[t + half * nv];
+        __syncthreads();
+    }
+    if (t < nleaf) {
+        const double num = red[2 * t], den = red[2 * t + 1];
+        s_leaf[t] = den == 0.0 ? 0.0 : eta * (num / den);
+    }
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
 // One elementwise pass per tree: add the previous tree's boost weight to F
 // (or set F = F0 for the first tree), then the histogram weight of every
-// event: fl32(v |y~|) if sampled else 0, class in the sign bit.
-__global__ __launch_bounds__(256) void tree_prep_kernel(
+// event: fl32(v |y~|) if sampled else 0, class in the sign bit.  The
+// previous tree's boost weights come either from the model (leaf_prev) or
+// straight from the leaf pass partials (leaf_partial, depth <= 4), which
+// every workgroup sums itself in the fixed order of leaf_finalize_kernel;
+// workgroup 0 then records them in the model (leaf_rec).
+__global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     const int8_t *__restrict__ y, const float *__restrict__ v, double *__restrict__ F,
     const double *__restrict__ f0, const uint8_t *__restrict__ leaf_node,
-    const double *__restrict__ leaf_prev, int depth, int64_t n, uint64_t seed, int tree,
-    double alpha, float *__restrict__ w, double *__restrict__ score_out) {
+    const double *__restrict__ leaf_prev, const double *__restrict__ leaf_partial,
+    int lblocks, double eta, double *__restrict__ leaf_rec, int depth, int64_t n,
+    uint64_t seed, int tree, double alpha, float *__restrict__ w,
+    double *__restrict__ score_out) {
+    __shared__ double red[kLeafReduceThreads];
+    __shared__ double s_leaf[128];
     const unsigned nleaf = 1u << depth;
-    const double f0v = (f0 && !leaf_prev) ? *f0 : 0.0;
+    const bool have_leaf = leaf_prev || leaf_partial;
+    if (leaf_partial) {
+        reduce_leaf_partials(leaf_partial, lblocks, (int)nleaf, eta, red, s_leaf);
+        if (blockIdx.x == 0 && leaf_rec && threadIdx.x < nleaf) leaf_rec[threadIdx.x] = s_leaf[threadIdx.x];
+    } else if (leaf_prev) {
+        for (unsigned t = threadIdx.x; t < nleaf; t += blockDim.x) s_leaf[t] = leaf_prev[t];
+        __syncthreads();
+    }
+    const double f0v = (f0 && !have_leaf) ? *f0 : 0.0;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
         double Fi;
-        if (leaf_prev) {
+        if (have_leaf) {
             unsigned li = (unsigned)leaf_node[i] - nleaf;
             if (li >= nleaf) li = 0;  // unreachable: leaf ids come from the leaf pass
-            Fi = F[i] + leaf_prev[li];
+            Fi = F[i] + s_leaf[li];
             F[i] = Fi;
         } else if (f0) {
             Fi = f0v;
@@ -182,18 +241,41 @@ __global__ __launch_bounds__(256) void tree_prep_kernel(
 // ---------------------------------------------------------------------------
 // Best candidate of one node over its features (gain highest, then lowest
 // feature), by one wavefront; lane 0 returns it.  An unusable result
-// (no finite gain) falls back to feature 0 and reports it.
-__device__ __forceinline__ void node_best(const double *__restrict__ cand_gain,
-                                          const int *__restrict__ cand_cut, int d, int k,
-                                          int lane, int *bf, int *bc, double *bg, bool *ok) {
+// (no finite gain) falls back to feature 0 and reports it.  Split into the
+// loads (lane l holds features l, l + 64, ... < 256) and the reduction, so
+// that a kernel can issue the loads early.
+struct CandRegs {
+    double g[4];
+    int c[4];
+};
+
+__device__ __forceinline__ void cand_load(const double *__restrict__ cand_gain,
+                                          const int *__restrict__ cand_cut, int d, int k, int lane,
+                                          CandRegs &r) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int jj = lane + kWave * q;
+        if (jj < d) {
+            r.g[q] = cand_gain[(size_t)k * d + jj];
+            r.c[q] = cand_cut[(size_t)k * d + jj];
+        } else {
+            r.g[q] = -INFINITY;
+            r.c[q] = 1;
+        }
+    }
+}
+
+__device__ __forceinline__ void cand_reduce(const CandRegs &r, int d, int lane, int *bf, int *bc,
+                                            double *bg, bool *ok) {
     double g = -INFINITY;
     int j = 0x7fffffff, c = 1;
-    for (int jj = lane; jj < d; jj += kWave) {
-        const double gg = cand_gain[(size_t)k * d + jj];
-        if (gg > g) {
-            g = gg;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int jj = lane + kWave * q;
+        if (jj < d && r.g[q] > g) {
+            g = r.g[q];
             j = jj;
-            c = cand_cut[(size_t)k * d + jj];
+            c = r.c[q];
         }
     }
 #pragma unroll
@@ -213,33 +295,14 @@ __device__ __forceinline__ void node_best(const double *__restrict__ cand_gain,
     *bg = g;
 }
 
-// Prologue of a routed pass: the cut of every parent node from the previous
-// layer's candidates, into the LDS cut table; workgroup 0 also records the
-// cuts in the model.
-__device__ void load_parent_cuts(const double *__restrict__ cand_gain,
-                                 const int *__restrict__ cand_cut, int d, int half,
-                                 uint8_t *s_cf, uint8_t *s_cc, uint8_t *__restrict__ rec_f,
-                                 uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
-                                 int *eflag) {
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int nw = blockDim.x / kWave;
-    for (int k = wave; k < half; k += nw) {
-        int bf, bc;
-        double bg;
-        bool ok;
-        node_best(cand_gain, cand_cut, d, k, lane, &bf, &bc, &bg, &ok);
-        if (lane == 0) {
-            s_cf[k] = (uint8_t)bf;
-            s_cc[k] = (uint8_t)bc;
-            if (!ok) atomicOr(eflag, kErrRoute);
-            if (blockIdx.x == 0 && rec_f) {
-                rec_f[k] = (uint8_t)bf;
-                rec_c[k] = (uint8_t)bc;
-                rec_g[k] = bg;
-            }
-        }
-    }
+__device__ __forceinline__ void node_best(const double *__restrict__ cand_gain,
+                                          const int *__restrict__ cand_cut, int d, int k,
+                                          int lane, int *bf, int *bc, double *bg, bool *ok) {
+    CandRegs r;
+    cand_load(cand_gain, cand_cut, d, k, lane, r);
+    cand_reduce(r, d, lane, bf, bc, bg, ok);
 }
+
 
 // Cuts of n_nodes nodes from their candidates (one wavefront per node).
 __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restrict__ cand_gain,
@@ -264,22 +327,178 @@ __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restric
 // (weight * 2^scale), adds every sampled event of its event chunk with a
 // 64-bit integer LDS atomic, and writes its partial histogram once at the
 // end; integer sums are exact, so the result is independent of the order of
-// the adds, and best_cuts sums the chunk partials.  Each thread handles 16 consecutive events per step: four float4
-// loads of weights, one 16-byte load of node ids and one 16-byte load of
-// codes per feature, all independent of each other.
+// the adds, and best_cuts sums the chunk partials.
+//
+// Each thread handles kHistE consecutive events per step and loads the next
+// step's weights, node ids, routing rows and feature codes (all features of
+// the group) before it adds the current step's events, so every load of a
+// step is in flight while the LDS atomics of the previous one run.
 //
 // Routed mode computes every event's node of this layer from its parent
 // (layer - 1) and the parent's cut on the way; the first feature group
 // stores the new ids.  With NP > 0 (NP = number of parents) the code rows of
-// the parents' cut features are loaded for the same 16 events up front, so
-// routing costs no dependent load; with NP = 0 each event's routing code is
+// the parents' cut features are loaded for the step up front, so routing
+// costs no dependent load; with NP = 0 each event's routing code is
 // gathered after its parent id arrives (deep layers).
-__device__ __forceinline__ uint32_t byte_of(const uint4 &v, int e) {
-    const uint32_t w = e < 4 ? v.x : e < 8 ? v.y : e < 12 ? v.z : v.w;
+//
+// LDS row of (node, feature): `fstride` bins x 2 classes, fstride = 256 for
+// 256 bins (the row offset of feature f is then a compile-time constant of
+// the atomic), else n_bins + 1 with the extra bin collecting codes >= n_bins
+// (reported as an error).
+__device__ __forceinline__ uint32_t byte8(const uint2 &v, int e) {
+    const uint32_t w = e < 4 ? v.x : v.y;
     return (w >> (8 * (e & 3))) & 0xffu;
 }
 
+// kHistE bytes at p[i0..]; bytes at i >= n read as `fill`.
+__device__ __forceinline__ uint2 load_bytes8(const uint8_t *__restrict__ p, int64_t i0,
+                                             int64_t n, bool full, uint32_t fill) {
+    if (full) return *reinterpret_cast<const uint2 *>(p + i0);
+    uint32_t t[2] = {fill * 0x01010101u, fill * 0x01010101u};
+    for (int e = 0; e < kHistE; ++e)
+        if (i0 + e < n)
+            t[e >> 2] = (t[e >> 2] & ~(0xffu << (8 * (e & 3)))) |
+                        ((uint32_t)p[i0 + e] << (8 * (e & 3)));
+    return make_uint2(t[0], t[1]);
+}
+
+template <int NP>
+struct HistStep {
+    float w[kHistE];
+    uint2 node;                       // parent ids (routed, layer >= 2) or node ids
+    uint2 rows[NP > 0 ? NP : 1];      // codes of the parents' cut features
+    uint2 codes[kHistFMax];           // codes of the group's features
+};
+
+// codes of the parents' cut features (the cut table must be in LDS)
 template <bool ROUTED, int NP>
+__device__ __forceinline__ void hist_load_rows(HistStep<NP> &st, const uint8_t *__restrict__ xb,
+                                               int64_t ldb, int d, const uint8_t *s_cf, int layer,
+                                               int64_t i0) {
+    if (ROUTED && NP > 0 && layer >= 1) {
+        // rows are padded to ldb >= i0 + kHistE: always in bounds
+#pragma unroll
+        for (int kk = 0; kk < (NP > 0 ? NP : 1); ++kk)
+            st.rows[kk] = *reinterpret_cast<const uint2 *>(
+                xb + (int64_t)min((int)s_cf[kk], d - 1) * ldb + i0);
+    }
+}
+
+template <bool ROUTED, int NP>
+__device__ __forceinline__ void hist_load(HistStep<NP> &st, const uint8_t *__restrict__ xb,
+                                          int64_t ldb, int64_t n, int d, int j0, int nf,
+                                          const uint8_t *__restrict__ node_in,
+                                          const float *__restrict__ w, const uint8_t *s_cf,
+                                          int layer, int half, int64_t i0, bool with_rows) {
+    const bool full = i0 + kHistE <= n;
+    if (full) {
+        const float4 a = reinterpret_cast<const float4 *>(w + i0)[0];
+        const float4 b = reinterpret_cast<const float4 *>(w + i0)[1];
+        st.w[0] = a.x; st.w[1] = a.y; st.w[2] = a.z; st.w[3] = a.w;
+        st.w[4] = b.x; st.w[5] = b.y; st.w[6] = b.z; st.w[7] = b.w;
+    } else {
+#pragma unroll
+        for (int e = 0; e < kHistE; ++e) st.w[e] = (i0 + e < n) ? w[i0 + e] : 0.0f;
+    }
+    if (!ROUTED)
+        st.node = load_bytes8(node_in, i0, n, full, 0u);
+    else if (layer >= 2)
+        st.node = load_bytes8(node_in, i0, n, full, (uint32_t)half);
+#pragma unroll
+    for (int ff = 0; ff < kHistFMax; ++ff)
+        if (ff < nf)
+            st.codes[ff] = *reinterpret_cast<const uint2 *>(xb + (int64_t)(j0 + ff) * ldb + i0);
+    if (with_rows) hist_load_rows<ROUTED, NP>(st, xb, ldb, d, s_cf, layer, i0);
+}
+
+template <bool ROUTED, int NP, bool FULLB>
+__device__ __forceinline__ void hist_add(
+    const HistStep<NP> &st, uint64_t *lds, const uint8_t *__restrict__ xb, int64_t ldb,
+    int64_t n, int d, int nbins, uint8_t *__restrict__ node_out, bool writer,
+    const float *__restrict__ w, const uint8_t *s_cf, const uint8_t *s_cc, int layer, int nodes,
+    int half, int j0, int nf, int k0, int nk, int fpg, int fstride, float tau, int scale,
+    double *__restrict__ small, int64_t i0, int &eflag) {
+    // node ids of this layer
+    uint2 nd;
+    if (!ROUTED) {
+        nd = st.node;
+    } else if (layer == 0) {
+        nd = make_uint2(0x01010101u, 0x01010101u);
+    } else {
+        const uint2 par = layer == 1 ? make_uint2(0x01010101u, 0x01010101u) : st.node;
+        uint32_t o[2] = {0u, 0u};
+#pragma unroll
+        for (int e = 0; e < kHistE; ++e) {
+            int pe = (int)byte8(par, e);
+            unsigned k = (unsigned)(pe - half);
+            if (k >= (unsigned)half) {  // unreachable for ids written by this library
+                eflag |= kErrRoute;
+                k = 0;
+                pe = half;
+            }
+            uint32_t code;
+            if (NP > 0) {
+                code = byte8(st.rows[0], e);
+#pragma unroll
+                for (int kk = 1; kk < (NP > 0 ? NP : 1); ++kk)
+                    if (k == (unsigned)kk) code = byte8(st.rows[kk], e);
+            } else {
+                code = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i0 + e];
+            }
+            const uint32_t ne = 2u * (uint32_t)pe + (code >= s_cc[k] ? 1u : 0u);
+            o[e >> 2] |= ne << (8 * (e & 3));
+        }
+        nd = make_uint2(o[0], o[1]);
+        if (writer) {
+            if (i0 + kHistE <= n) {
+                *reinterpret_cast<uint2 *>(node_out + i0) = nd;
+            } else {
+                for (int e = 0; e < kHistE; ++e)
+                    if (i0 + e < n) node_out[i0 + e] = (uint8_t)byte8(nd, e);
+            }
+        }
+    }
+    // Sampled events of this group's nodes add w * 2^scale to their
+    // (node, feature, bin, class) counter: the float's 24-bit significand
+    // shifted into place, exact for w >= tau.  Weights below the grid are
+    // added in float64 to the side histogram.
+    const int rowc = 2 * fstride;   // counters per (node, feature)
+#pragma unroll
+    for (int e = 0; e < kHistE; ++e) {
+        const uint32_t bits = __float_as_uint(st.w[e]);
+        const uint32_t ab = bits & 0x7fffffffu;
+        const float a = __uint_as_float(ab);
+        const uint32_t loc = byte8(nd, e) - (uint32_t)(nodes + k0);
+        if (loc < (uint32_t)nk && a >= tau) {
+            const int sh = (int)(ab >> 23) - 150 + scale;   // >= 0 for a >= tau
+            const uint64_t fx = (uint64_t)((ab & 0x7fffffu) | 0x800000u) << sh;
+            const int slot = (int)loc * fpg * rowc + (int)(bits >> 31);
+#pragma unroll
+            for (int ff = 0; ff < kHistFMax; ++ff) {
+                if (ff < nf) {
+                    uint32_t bin = byte8(st.codes[ff], e);
+                    if (!FULLB) bin = min(bin, (uint32_t)nbins);
+                    atomicAdd(&lds[slot + ff * (FULLB ? 512 : rowc) + 2 * (int)bin], fx);
+                }
+            }
+        } else if (loc < (uint32_t)nk && ab != 0u) {   // rare: below the fixed-point grid
+#pragma unroll
+            for (int ff = 0; ff < kHistFMax; ++ff) {
+                if (ff >= nf) break;
+                const uint32_t bin = byte8(st.codes[ff], e);
+                if (bin >= (uint32_t)nbins) {
+                    eflag |= kErrBin;
+                    continue;
+                }
+                const size_t gi =
+                    ((((size_t)(k0 + (int)loc) * d + j0 + ff) * nbins + bin) * 2) + (bits >> 31);
+                atomicAdd(&small[gi], (double)a);
+            }
+        }
+    }
+}
+
+template <bool ROUTED, int NP, bool FULLB>
 __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
@@ -309,173 +528,93 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const int nf = min(fpg, d - j0);
     const int k0 = h * npg;
     const int nk = min(npg, nodes - k0);
-    const int lds_n = npg * fpg * nbins * 2;
-    const int lstride = fpg * nbins * 2;
-    // per-lane counters after the histogram: a dummy for events that add
-    // nothing, a "bad" one for out-of-range bin codes
-    const int lane = threadIdx.x % kWave;
-    const int dummy = lds_n + lane;
-    const int bad = lds_n + kWave + lane;
-
-    for (int t = threadIdx.x; t < lds_n + 2 * kWave; t += blockDim.x) lds[t] = 0ull;
-    // weights at or above tau are exact multiples of 2^-scale
-    const float tau = ldexpf(1.0f, 23 - scale);
-    __shared__ int s_eflag;
-    if (threadIdx.x == 0) s_eflag = 0;
-    __syncthreads();
-    if (ROUTED && layer >= 1)
-        load_parent_cuts(cand_gain, cand_cut, d, half, s_cf, s_cc, rec_f, rec_c, rec_g, &s_eflag);
-    __syncthreads();
-    int eflag = threadIdx.x == 0 ? s_eflag : 0;
+    const int fstride = FULLB ? 256 : nbins + 1;
+    const int lds_n = npg * fpg * 2 * fstride;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nwaves = blockDim.x / kWave;
+    int eflag = 0;
 
     const int64_t start = (int64_t)p * chunk_events;
     const int64_t end = min(n, start + chunk_events);
     const bool writer = ROUTED && layer >= 1 && g == 0 && h == 0 && node_out != nullptr;
+    const int64_t stride = (int64_t)kHistE * blockDim.x;
 
-    for (int64_t i0 = start + 16 * (int64_t)threadIdx.x; i0 < end;
-         i0 += 16 * (int64_t)blockDim.x) {
-        const bool full = i0 + 16 <= n;
-        float wv[16];
-        if (full) {
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const float4 t4 = reinterpret_cast<const float4 *>(w + i0)[q4];
-                wv[4 * q4] = t4.x;
-                wv[4 * q4 + 1] = t4.y;
-                wv[4 * q4 + 2] = t4.z;
-                wv[4 * q4 + 3] = t4.w;
-            }
-        } else {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) wv[e] = (i0 + e < n) ? w[i0 + e] : 0.0f;
-        }
-        // node ids of this layer, one byte per event
-        uint4 nd;
-        if (!ROUTED) {
-            if (full) {
-                nd = *reinterpret_cast<const uint4 *>(node_in + i0);
-            } else {
-                uint32_t t4[4] = {0, 0, 0, 0};
-                for (int e = 0; e < 16; ++e)
-                    if (i0 + e < n) t4[e >> 2] |= (uint32_t)node_in[i0 + e] << (8 * (e & 3));
-                nd = make_uint4(t4[0], t4[1], t4[2], t4[3]);
-            }
-        } else if (layer == 0) {
-            nd = make_uint4(0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u);
-        } else {
-            uint4 par;
-            if (layer == 1) {
-                par = make_uint4(0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u);
-            } else if (full) {
-                par = *reinterpret_cast<const uint4 *>(node_in + i0);
-            } else {
-                uint32_t t4[4];
-                for (int k4 = 0; k4 < 4; ++k4) t4[k4] = (uint32_t)half * 0x01010101u;
-                for (int e = 0; e < 16; ++e)
-                    if (i0 + e < n)
-                        t4[e >> 2] = (t4[e >> 2] & ~(0xffu << (8 * (e & 3)))) |
-                                     ((uint32_t)node_in[i0 + e] << (8 * (e & 3)));
-                par = make_uint4(t4[0], t4[1], t4[2], t4[3]);
-            }
-            uint4 rows[NP > 0 ? NP : 1];
-            if (NP > 0) {
-#pragma unroll
-                for (int kk = 0; kk < NP; ++kk)   // i0 + 15 < ldb: in bounds
-                    rows[kk] = *reinterpret_cast<const uint4 *>(
-                        xb + (int64_t)min((int)s_cf[kk], d - 1) * ldb + i0);
-            }
-            uint32_t o4[4] = {0, 0, 0, 0};
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                int pe = (int)byte_of(par, e);
-                unsigned k = (unsigned)(pe - half);
-                if (k >= (unsigned)half) {  // unreachable for ids written by this library
-                    eflag |= kErrRoute;
-                    k = 0;
-                    pe = half;
+    // Loads in flight together: the candidates of this wavefront's parent
+    // node (the cut table of a routed pass) first, then the first step's
+    // weights, node ids and codes; the candidates are reduced while the
+    // event data arrives, and the step's routing rows follow once the cut
+    // table is in LDS.  (Loads complete in issue order, so the candidates
+    // come first.)
+    CandRegs cr;
+    const bool pwave = ROUTED && layer >= 1 && wave < half;
+    if (pwave) cand_load(cand_gain, cand_cut, d, wave, lane, cr);
+    HistStep<NP> A, B;
+    int64_t ia = start + (int64_t)kHistE * threadIdx.x;
+    if (ia < end) hist_load<ROUTED, NP>(A, xb, ldb, n, d, j0, nf, node_in, w, s_cf, layer, half, ia, false);
+
+    for (int t = threadIdx.x; t < lds_n; t += blockDim.x) lds[t] = 0ull;
+    // weights at or above tau are exact multiples of 2^-scale
+    const float tau = ldexpf(1.0f, 23 - scale);
+    if (ROUTED && layer >= 1) {
+        // cut of parent k from its candidates; workgroup 0 records it in the model
+        for (int k = wave; k < half; k += nwaves) {
+            int bf, bc;
+            double bg;
+            bool ok;
+            if (k == wave)
+                cand_reduce(cr, d, lane, &bf, &bc, &bg, &ok);
+            else
+                node_best(cand_gain, cand_cut, d, k, lane, &bf, &bc, &bg, &ok);
+            if (lane == 0) {
+                s_cf[k] = (uint8_t)bf;
+                s_cc[k] = (uint8_t)bc;
+                if (!ok) eflag |= kErrRoute;
+                if (blockIdx.x == 0 && rec_f) {
+                    rec_f[k] = (uint8_t)bf;
+                    rec_c[k] = (uint8_t)bc;
+                    rec_g[k] = bg;
                 }
-                uint32_t code;
-                if (NP > 0) {
-                    code = byte_of(rows[0], e);
-#pragma unroll
-                    for (int kk = 1; kk < NP; ++kk)
-                        if (k == (unsigned)kk) code = byte_of(rows[kk], e);
-                } else {
-                    code = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i0 + e];
-                }
-                const uint32_t ne = 2u * (uint32_t)pe + (code >= s_cc[k] ? 1u : 0u);
-                o4[e >> 2] |= ne << (8 * (e & 3));
-            }
-            nd = make_uint4(o4[0], o4[1], o4[2], o4[3]);
-            if (writer) {
-                if (full) {
-                    *reinterpret_cast<uint4 *>(node_out + i0) = nd;
-                } else {
-                    for (int e = 0; e < 16; ++e)
-                        if (i0 + e < n) node_out[i0 + e] = (uint8_t)byte_of(nd, e);
-                }
-            }
-        }
-        // Sampled events of this group's nodes add w * 2^scale to their
-        // (node, feature, bin, class) counter; the integer is the float's
-        // 24-bit significand shifted into place, exact for w >= tau.  Other
-        // events (unsampled, outside this group's nodes) add 0 to a per-lane
-        // dummy counter and an out-of-range bin code adds to a per-lane
-        // "bad" counter, so the inner loop has no branch.  Rarer weights
-        // below the grid are flagged and added in float64 afterwards.
-        int slot[16];
-        uint64_t fx[16];
-        unsigned smallm = 0;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const unsigned loc = byte_of(nd, e) - (unsigned)(nodes + k0);
-            const float a = fabsf(wv[e]);
-            const bool take = a != 0.0f && loc < (unsigned)nk;
-            const bool big = take && a >= tau;
-            const uint32_t bits = __float_as_uint(a);
-            const int sh = (int)(bits >> 23) - 150 + scale;
-            slot[e] = big ? (int)loc * lstride + (wv[e] < 0.0f ? 1 : 0) : dummy;
-            fx[e] = big ? (uint64_t)((bits & 0x7fffffu) | 0x800000u) << (sh > 0 ? sh : 0) : 0ull;
-            smallm |= (take && !big) ? 1u << e : 0u;
-        }
-        for (int f = 0; f < nf; ++f) {
-            const uint4 xv = *reinterpret_cast<const uint4 *>(xb + (int64_t)(j0 + f) * ldb + i0);
-            const int fofs = f * nbins * 2;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const unsigned bin = byte_of(xv, e);
-                const int real = slot[e] + fofs + 2 * (int)bin;
-                const int idx = slot[e] == dummy ? dummy : (bin < (unsigned)nbins ? real : bad);
-                atomicAdd(&lds[idx], fx[e]);
-            }
-            unsigned sm = smallm;
-            while (sm) {  // rare: weights below the fixed-point grid
-                const int e = __ffs(sm) - 1;
-                sm &= sm - 1;
-                const float wi = w[i0 + e];
-                const unsigned loc = byte_of(nd, e) - (unsigned)(nodes + k0);
-                const unsigned bin = byte_of(xv, e);
-                if (bin >= (unsigned)nbins) {
-                    eflag |= kErrBin;
-                    continue;
-                }
-                const size_t gi = ((((size_t)(k0 + (int)loc) * d + j0 + f) * nbins + bin) * 2) +
-                                  (wi < 0.0f ? 1 : 0);
-                atomicAdd(&small[gi], (double)fabsf(wi));
             }
         }
     }
     __syncthreads();
-    if (threadIdx.x < kWave && lds[lds_n + kWave + threadIdx.x] != 0ull) eflag |= kErrBin;
 
+    // two steps in flight: the loads of step s + 1 are issued before the
+    // adds of step s
+    if (ia < end) {
+        hist_load_rows<ROUTED, NP>(A, xb, ldb, d, s_cf, layer, ia);
+        for (;;) {
+            const int64_t ib = ia + stride;
+            if (ib < end)
+                hist_load<ROUTED, NP>(B, xb, ldb, n, d, j0, nf, node_in, w, s_cf, layer, half, ib, true);
+            hist_add<ROUTED, NP, FULLB>(A, lds, xb, ldb, n, d, nbins, node_out, writer, w, s_cf,
+                                        s_cc, layer, nodes, half, j0, nf, k0, nk, fpg, fstride,
+                                        tau, scale, small, ia, eflag);
+            if (ib >= end) break;
+            ia = ib + stride;
+            if (ia < end)
+                hist_load<ROUTED, NP>(A, xb, ldb, n, d, j0, nf, node_in, w, s_cf, layer, half, ia, true);
+            hist_add<ROUTED, NP, FULLB>(B, lds, xb, ldb, n, d, nbins, node_out, writer, w, s_cf,
+                                        s_cc, layer, nodes, half, j0, nf, k0, nk, fpg, fstride,
+                                        tau, scale, small, ib, eflag);
+            if (ia >= end) break;
+        }
+    }
+    __syncthreads();
+    if (!FULLB)   // counters of codes >= n_bins
+        for (int t = threadIdx.x; t < npg * fpg * 2; t += blockDim.x)
+            if (lds[(t >> 1) * 2 * fstride + 2 * nbins + (t & 1)] != 0ull) eflag |= kErrBin;
+
+    // partial[p][node][feature][bin][class]: one (node, feature) row per
+    // wavefront step, lanes over bins and classes
     const int per_nf = nbins * 2;
     uint64_t *out = partial + (size_t)p * nodes * d * per_nf;
-    for (int t = threadIdx.x; t < lds_n; t += blockDim.x) {
-        const int k = t / (fpg * per_nf);
-        const int rem = t - k * fpg * per_nf;
-        const int f = rem / per_nf;
-        const int rr = rem - f * per_nf;
-        if (k < nk && f < nf) out[((size_t)(k0 + k) * d + j0 + f) * per_nf + rr] = lds[t];
+    for (int kf = wave; kf < nk * nf; kf += nwaves) {
+        const int k = kf / nf;
+        const int f = kf - k * nf;
+        uint64_t *dst = out + ((size_t)(k0 + k) * d + j0 + f) * per_nf;
+        const uint64_t *src = lds + (k * fpg + f) * 2 * fstride;
+        for (int t = lane; t < per_nf; t += kWave) dst[t] = src[t];
     }
     if (eflag) atomicOr(err, eflag);
 }
@@ -529,7 +668,7 @@ __global__ void sum_blocks_kernel(const double *__restrict__ block_partial, int 
 // separation gain of each candidate cut and reduces to the best (gain
 // highest, then lowest bin).  The reduction of a node's candidates
 // over features (gain highest, then lowest feature) is left to the next
-// pass (load_parent_cuts) or to select_cuts_kernel.
+// pass (its prologue) or to select_cuts_kernel.
 //
 // Exactness rules shared with the plain definition: a cut whose left or
 // right side holds no event has gain exactly 0 (as the definition gives
@@ -709,18 +848,82 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
 // workgroup.  With NL > 0 leaves every thread keeps the 2 NL sums in
 // registers, then a wavefront reduction and an in-order sum over wavefronts
 // give the workgroup's partial (no atomics, fixed order); with NL = 0 (deep
-// trees) threads add into LDS accumulators.  leaf_finalize_kernel adds the
-// partials.  Routed mode first takes the last layer's cuts from their
-// candidates, sends every event from layer depth-1 to its leaf and stores
-// the leaf id.
-__device__ __forceinline__ double wave_sum(double v) {
+// trees) threads add into LDS accumulators.  Routed mode first takes the
+// last layer's cuts from their candidates (loaded before the event data, so
+// both latencies overlap), sends every event from layer depth-1 to its leaf
+// and stores the leaf id; with at most four parents the code rows of the
+// parents' cut features are loaded with the event's other data, so routing
+// costs no dependent load.  One event per thread and step, the next step's
+// loads issued before the current step's arithmetic.
+// Sums V values (a power of two <= 64) over a wavefront in few shuffles:
+// each halving step exchanges half of the values with the lane across bit b
+// (b = 5, 4, ...) and keeps the half that bit selects, so lane l ends with
+// value idx(l) = its kept halves summed over the lanes that agree with l in
+// those bits; plain butterflies over the lower bits then complete the sums.
+// Returns the total of value *idx in every lane (fixed order: deterministic).
+template <int H>
+__device__ __forceinline__ void transpose_sum_step(double *x, int lane, int bit, int &id) {
+    const bool hi = (lane >> bit) & 1;
 #pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    return v;
+    for (int j = 0; j < H; ++j) {
+        const double mine = hi ? x[H + j] : x[j];
+        const double other = hi ? x[j] : x[H + j];
+        x[j] = mine + __shfl_xor(other, 1 << bit);
+    }
+    id += hi ? H : 0;
+    if constexpr (H > 1) transpose_sum_step<H / 2>(x, lane, bit - 1, id);
+}
+
+template <int V>
+__device__ __forceinline__ double wave_transpose_sum(double (&x)[V], int lane, int *idx) {
+    static_assert(V >= 2 && V <= 64 && (V & (V - 1)) == 0, "V: a power of two in [2, 64]");
+    int id = 0;
+    transpose_sum_step<V / 2>(x, lane, 5, id);
+    double r = x[0];
+    constexpr int lower = 6 - __builtin_ctz(V);   // bits 5 .. 6 - log2(V) are used
+#pragma unroll
+    for (int bit = lower - 1; bit >= 0; --bit) r += __shfl_xor(r, 1 << bit);
+    *idx = id;
+    return r;
+}
+
+struct LeafStep {
+    int node;        // parent id (routed) or leaf id
+    uint32_t rows;   // codes of up to four parents' cut features, one byte each
+    int yv;
+    double F;
+    float v;
+};
+
+// codes of the parents' cut features (the cut table must be in LDS)
+template <bool ROUTED, bool ROWS>
+__device__ __forceinline__ void leaf_load_rows(LeafStep &st, const uint8_t *__restrict__ xb,
+                                               int64_t ldb, int d, int half, const uint8_t *s_cf,
+                                               int64_t i) {
+    if (ROUTED && ROWS) {
+        uint32_t r = 0;
+        for (int k = 0; k < half; ++k)
+            r |= (uint32_t)xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i] << (8 * k);
+        st.rows = r;
+    }
+}
+
+template <bool ROUTED, bool ROWS>
+__device__ __forceinline__ void leaf_load(LeafStep &st, const uint8_t *__restrict__ xb,
+                                          int64_t ldb, int d, const uint8_t *__restrict__ node_in,
+                                          const int8_t *__restrict__ y,
+                                          const float *__restrict__ v,
+                                          const double *__restrict__ F, int half,
+                                          const uint8_t *s_cf, int64_t i, bool with_rows) {
+    st.node = node_in ? (int)node_in[i] : 1;
+    st.yv = y[i];
+    st.F = F[i];
+    st.v = v ? v[i] : 1.0f;
+    if (with_rows) leaf_load_rows<ROUTED, ROWS>(st, xb, ldb, d, half, s_cf, i);
 }
 
 template <bool ROUTED, int NL>
-__global__ __launch_bounds__(256) void leaf_kernel(
+__global__ __launch_bounds__(1024) void leaf_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut,
@@ -729,52 +932,80 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     const double *__restrict__ F, uint64_t seed, int tree, double alpha,
     double *__restrict__ leaf_partial, int *__restrict__ err) {
 #pragma clang fp contract(off)
+    constexpr bool ROWS = NL > 0 && NL <= 8;   // at most four parents
     __shared__ double acc[2 * 128];
-    __shared__ double red[256];
+    __shared__ double red[2 * 16 * 16];
     __shared__ uint8_t s_cf[64], s_cc[64];
-    __shared__ int s_eflag;
     const int nleaf = 1 << depth;
     const int half = nleaf >> 1;
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
     const int nwaves = blockDim.x / kWave;
+    int eflag = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t ia = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+
+    CandRegs cr;
+    const bool pwave = ROUTED && wave < half;
+    if (pwave) cand_load(cand_gain, cand_cut, d, wave, lane, cr);
+    LeafStep A, B;
+    if (ia < n) leaf_load<ROUTED, ROWS>(A, xb, ldb, d, node_in, y, v, F, half, s_cf, ia, false);
     if (NL == 0)
         for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x) acc[t] = 0.0;
-    if (threadIdx.x == 0) s_eflag = 0;
+    if (ROUTED) {
+        for (int k = wave; k < half; k += nwaves) {
+            int bf, bc;
+            double bg;
+            bool ok;
+            if (k == wave)
+                cand_reduce(cr, d, lane, &bf, &bc, &bg, &ok);
+            else
+                node_best(cand_gain, cand_cut, d, k, lane, &bf, &bc, &bg, &ok);
+            if (lane == 0) {
+                s_cf[k] = (uint8_t)bf;
+                s_cc[k] = (uint8_t)bc;
+                if (!ok) eflag |= kErrRoute;
+                if (blockIdx.x == 0 && rec_f) {
+                    rec_f[k] = (uint8_t)bf;
+                    rec_c[k] = (uint8_t)bc;
+                    rec_g[k] = bg;
+                }
+            }
+        }
+    }
     __syncthreads();
-    if (ROUTED)
-        load_parent_cuts(cand_gain, cand_cut, d, half, s_cf, s_cc, rec_f, rec_c, rec_g, &s_eflag);
-    __syncthreads();
-    int eflag = threadIdx.x == 0 ? s_eflag : 0;
+
     double an[NL > 0 ? NL : 1], ad[NL > 0 ? NL : 1];
 #pragma unroll
     for (int l = 0; l < (NL > 0 ? NL : 1); ++l) an[l] = ad[l] = 0.0;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
+    auto add = [&](const LeafStep &st, int64_t i) {
         int leaf;
         if (ROUTED) {
-            int par = node_in ? (int)node_in[i] : 1;
+            int par = st.node;
             unsigned k = (unsigned)(par - half);
-            if (k >= (unsigned)half) {
+            if (k >= (unsigned)half) {  // unreachable for ids written by this library
                 eflag |= kErrRoute;
                 k = 0;
                 par = half;
             }
-            const int f = min((int)s_cf[k], d - 1);
-            const uint8_t x = xb[(int64_t)f * ldb + i];
+            uint32_t x;
+            if (ROWS)
+                x = (st.rows >> (8 * k)) & 0xffu;
+            else
+                x = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i];
             leaf = 2 * par + (x >= s_cc[k] ? 1 : 0);
             node_out[i] = (uint8_t)leaf;
         } else {
-            leaf = node_in[i];
+            leaf = st.node;
             if ((unsigned)(leaf - nleaf) >= (unsigned)nleaf) {
                 eflag |= kErrRoute;
-                continue;
+                return;
             }
         }
-        if (!in_subsample(seed, tree, n, i, alpha)) continue;
-        const double yf = (double)y[i];
-        const double yt = pseudo_response(yf, F[i]);
-        const double vi = v ? (double)v[i] : 1.0;
+        if (!in_subsample(seed, tree, n, i, alpha)) return;
+        const double yf = (double)st.yv;
+        const double yt = pseudo_response(yf, st.F);
+        const double vi = (double)st.v;
         const double a = fabs(yt);
         const double gnum = vi * yt;
         const double gden = vi * a * (2.0 - a);
@@ -789,18 +1020,32 @@ __global__ __launch_bounds__(256) void leaf_kernel(
             atomicAdd(&acc[2 * li], gnum);
             atomicAdd(&acc[2 * li + 1], gden);
         }
+    };
+    if (ia < n) {
+        leaf_load_rows<ROUTED, ROWS>(A, xb, ldb, d, half, s_cf, ia);
+        for (;;) {
+            const int64_t ib = ia + stride;
+            if (ib < n) leaf_load<ROUTED, ROWS>(B, xb, ldb, d, node_in, y, v, F, half, s_cf, ib, true);
+            add(A, ia);
+            if (ib >= n) break;
+            ia = ib + stride;
+            if (ia < n) leaf_load<ROUTED, ROWS>(A, xb, ldb, d, node_in, y, v, F, half, s_cf, ia, true);
+            add(B, ib);
+            if (ia >= n) break;
+        }
     }
     if (NL > 0) {
-        // red[wave][2 NL] (2 NL * nwaves <= 256 doubles for NL <= 16, 256 threads)
+        // red[wave][2 NL]: 2 NL * nwaves <= 512 doubles for NL <= 16, 16 waves
+        constexpr int V = 2 * (NL > 0 ? NL : 1);
+        double x[V];
 #pragma unroll
-        for (int l = 0; l < (NL > 0 ? NL : 1); ++l) {
-            const double sn = wave_sum(an[l]);
-            const double sd = wave_sum(ad[l]);
-            if (lane == 0) {
-                red[wave * 2 * NL + 2 * l] = sn;
-                red[wave * 2 * NL + 2 * l + 1] = sd;
-            }
+        for (int l = 0; l < V / 2; ++l) {
+            x[2 * l] = an[l];
+            x[2 * l + 1] = ad[l];
         }
+        int idx;
+        const double sum = wave_transpose_sum<V>(x, lane, &idx);
+        if ((lane & (kWave / V - 1)) == 0) red[wave * V + idx] = sum;
         __syncthreads();
         if (threadIdx.x < 2 * NL) {
             double sum = 0.0;
@@ -815,40 +1060,13 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     if (eflag) atomicOr(err, eflag);
 }
 
-// Sum of the workgroup partials of the leaf pass (one workgroup; thread t
-// adds value t % nv over blocks t / nv, t / nv + stripes, ...; the stripes
-// are then added in order) and the boost weights eta * num / den (0 when
-// den = 0).
-__global__ __launch_bounds__(1024) void leaf_finalize_kernel(const double *__restrict__ leaf_partial,
-                                                             int nblocks, int nleaf, double eta,
-                                                             double *__restrict__ leaf_out) {
-#pragma clang fp contract(off)
-    __shared__ double red[1024];
-    const int nv = 2 * nleaf;
-    const int stripes = blockDim.x / nv;
-    const int t = threadIdx.x;
-    if (t < stripes * nv) {
-        const int val = t % nv, st = t / nv;
-        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-        int b = st;
-        for (; b + 3 * stripes < nblocks; b += 4 * stripes) {
-            s0 += leaf_partial[(size_t)b * nv + val];
-            s1 += leaf_partial[(size_t)(b + stripes) * nv + val];
-            s2 += leaf_partial[(size_t)(b + 2 * stripes) * nv + val];
-            s3 += leaf_partial[(size_t)(b + 3 * stripes) * nv + val];
-        }
-        for (; b < nblocks; b += stripes) s0 += leaf_partial[(size_t)b * nv + val];
-        red[t] = (s0 + s1) + (s2 + s3);
-    }
-    __syncthreads();
-    if (t < nleaf) {
-        double num = 0.0, den = 0.0;
-        for (int st = 0; st < stripes; ++st) {
-            num += red[st * nv + 2 * t];
-            den += red[st * nv + 2 * t + 1];
-        }
-        leaf_out[t] = den == 0.0 ? 0.0 : eta * (num / den);
-    }
+__global__ __launch_bounds__(kLeafReduceThreads) void leaf_finalize_kernel(
+    const double *__restrict__ leaf_partial, int nblocks, int nleaf, double eta,
+    double *__restrict__ leaf_out) {
+    __shared__ double red[kLeafReduceThreads];
+    __shared__ double s_leaf[128];
+    reduce_leaf_partials(leaf_partial, nblocks, nleaf, eta, red, s_leaf);
+    if ((int)threadIdx.x < nleaf) leaf_out[threadIdx.x] = s_leaf[threadIdx.x];
 }
 
 // node <- 2 node + [xb[f][i] >= c] with (f, c) the cut of the node.
@@ -996,9 +1214,17 @@ hipError_t allow_lds(K kernel, size_t max_lds) {
 // ===========================================================================
 hipError_t prepare_kernels(size_t max_lds) {
     const hipError_t e[] = {
-        allow_lds(hist_kernel<false, 0>, max_lds), allow_lds(hist_kernel<true, 0>, max_lds),
-        allow_lds(hist_kernel<true, 1>, max_lds),  allow_lds(hist_kernel<true, 2>, max_lds),
-        allow_lds(hist_kernel<true, 4>, max_lds),  allow_lds(apply_kernel, max_lds)};
+        allow_lds(hist_kernel<false, 0, true>, max_lds),
+        allow_lds(hist_kernel<true, 0, true>, max_lds),
+        allow_lds(hist_kernel<true, 1, true>, max_lds),
+        allow_lds(hist_kernel<true, 2, true>, max_lds),
+        allow_lds(hist_kernel<true, 4, true>, max_lds),
+        allow_lds(hist_kernel<false, 0, false>, max_lds),
+        allow_lds(hist_kernel<true, 0, false>, max_lds),
+        allow_lds(hist_kernel<true, 1, false>, max_lds),
+        allow_lds(hist_kernel<true, 2, false>, max_lds),
+        allow_lds(hist_kernel<true, 4, false>, max_lds),
+        allow_lds(apply_kernel, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -1024,11 +1250,14 @@ hipError_t launch_initial_score(const double *class_partial, double *f0, int *er
 }
 
 hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const double *f0,
-                            const uint8_t *leaf_node, const double *leaf_prev, int depth,
-                            int64_t n, uint64_t seed, int tree, double alpha, float *w,
-                            double *score_out, hipStream_t s) {
-    tree_prep_kernel<<<grid_for(n, 256, 4096), 256, 0, s>>>(
-        y, v, F, f0, leaf_node, leaf_prev, depth, n, seed, tree, alpha, w, score_out);
+                            const uint8_t *leaf_node, const double *leaf_prev,
+                            const double *leaf_partial, int lblocks, double eta, double *leaf_rec,
+                            int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
+                            double *score_out, int cu_count, hipStream_t s) {
+    if (leaf_partial && depth > kFusedLeafDepth) return hipErrorInvalidValue;
+    tree_prep_kernel<<<grid_for(n, kLeafReduceThreads, cu_count), kLeafReduceThreads, 0, s>>>(
+        y, v, F, f0, leaf_node, leaf_prev, leaf_partial, lblocks, eta, leaf_rec, depth, n, seed,
+        tree, alpha, w, score_out);
     return hipGetLastError();
 }
 
@@ -1036,41 +1265,53 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
                          size_t max_lds, int fpg, int chunks, int threads) {
     HistShape hs{};
     const int nodes = 1 << layer;
-    const size_t per_node_feature = (size_t)n_bins * 2 * sizeof(double);
+    // LDS row of one (node, feature): 256 bins, or n_bins + 1 with the
+    // out-of-range counter, times two classes
+    const int fstride = n_bins == 256 ? 256 : n_bins + 1;
+    const size_t per_node_feature = (size_t)fstride * 2 * sizeof(uint64_t);
     // the kernel's static LDS (cut table) shares the workgroup's LDS limit
-    max_lds = max_lds > kHistStaticLdsReserve + kHistExtraLds
-                  ? max_lds - kHistStaticLdsReserve - kHistExtraLds
-                  : 0;
+    max_lds = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
     int npg = (int)(max_lds / per_node_feature);
     if (npg < 1) npg = 1;
     if (npg > nodes) npg = nodes;
     hs.nodes_per_group = npg;
     hs.node_groups = (nodes + npg - 1) / npg;
-    // Features per workgroup.  A 1024-thread workgroup fills a CU, so the
-    // pass runs as one round of at most cu_count workgroups: groups * chunks
-    // with chunks <= cu_count / groups and at least 16 events per thread.
-    // Take the feature-group size that brings the most workgroups, ties to
-    // about eight feature groups (each group re-reads the chunk's node ids
-    // and weights; each chunk writes one more partial histogram).
+    // Features per workgroup (at most kHistFMax).  A 1024-thread workgroup
+    // fills a CU, so the pass runs as one round of at most cu_count
+    // workgroups: groups * chunks with chunks <= cu_count / groups and at
+    // least one full step (kHistE events) per thread.  Among the
+    // feature-group sizes whose launch fills at least 95% of the most
+    // workgroups any size reaches, take the one with the fewest event
+    // chunks: every chunk writes one more partial histogram that best_cuts
+    // reads back.
     const int t_threads = threads > 0 ? threads : 1024;
+    const int64_t min_events = (int64_t)kHistE * t_threads;
+    const int fmax = d < kHistFMax ? d : kHistFMax;
     int f = 1;
     if (fpg > 0) {
-        f = fpg < d ? fpg : d;
+        f = fpg < fmax ? fpg : fmax;
     } else {
-        const int64_t cmax = n / (16LL * t_threads) > 0 ? n / (16LL * t_threads) : 1;
-        int64_t best_w = -1;
-        int best_dist = 1 << 30;
-        for (int cand = 1; cand <= d; ++cand) {
+        const int64_t cmax = n / min_events > 0 ? n / min_events : 1;
+        int64_t wgs_of[kHistFMax + 1] = {0}, ch_of[kHistFMax + 1] = {0};
+        int64_t most = 0;
+        int last = 0;
+        for (int cand = 1; cand <= fmax; ++cand) {
             if ((size_t)npg * cand * per_node_feature > max_lds) break;
             const int g = ((d + cand - 1) / cand) * hs.node_groups;
             int64_t c = cu_count / g;
             if (c > cmax) c = cmax;
             if (c < 1) c = 1;
-            const int64_t wgs = c * g;
-            const int dist = std::abs((d + cand - 1) / cand - 8);
-            if (wgs <= cu_count && (wgs > best_w || (wgs == best_w && dist < best_dist))) {
-                best_w = wgs;
-                best_dist = dist;
+            ch_of[cand] = c;
+            wgs_of[cand] = c * g;
+            if (wgs_of[cand] > most) most = wgs_of[cand];
+            last = cand;
+        }
+        int64_t best_c = -1;
+        for (int cand = 1; cand <= last; ++cand) {
+            if (wgs_of[cand] * 100 < most * 95) continue;
+            if (best_c < 0 || ch_of[cand] < best_c ||
+                (ch_of[cand] == best_c && wgs_of[cand] > wgs_of[f])) {
+                best_c = ch_of[cand];
                 f = cand;
             }
         }
@@ -1085,17 +1326,16 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
     // double the pass; every extra event chunk also adds one more partial
     // histogram to write and to sum
     int64_t c = chunks > 0 ? chunks : (int64_t)cu_count / groups;
-    const int64_t min_events = 16LL * hs.threads;
     const int64_t cmax = (n + min_events - 1) / min_events;
     if (chunks <= 0 && c > cmax) c = cmax;
     if (c < 1) c = 1;
     int64_t ce = (n + c - 1) / c;
-    ce = (ce + 15) & ~(int64_t)15;
+    ce = (ce + kHistE - 1) / kHistE * kHistE;
     hs.chunk_events = ce;
     hs.chunks = (int)((n + ce - 1) / ce);
     const int64_t work = (int64_t)hs.chunks * groups;
     hs.blocks = (int)((work + kXcds - 1) / kXcds * kXcds);
-    hs.lds_bytes = (size_t)npg * f * per_node_feature + kHistExtraLds;
+    hs.lds_bytes = (size_t)npg * f * per_node_feature;
     return hs;
 }
 
@@ -1109,12 +1349,12 @@ int histogram_scale(double total_weight_bound) {
     return sc;
 }
 
-template <bool ROUTED, int NP>
+template <bool ROUTED, int NP, bool FULLB>
 hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
                           const ParentCuts &pc, int layer, int scale, uint64_t *partial,
                           double *small, int *err, hipStream_t s) {
-    hist_kernel<ROUTED, NP><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+    hist_kernel<ROUTED, NP, FULLB><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.rec_f,
         pc.rec_c, pc.rec_g, layer, hs.features_per_group, hs.feature_groups, hs.nodes_per_group,
         hs.node_groups, hs.chunks, hs.chunk_events, scale, partial, small, err);
@@ -1127,18 +1367,21 @@ hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb,
                             int scale, uint64_t *partial, double *small, int *err,
                             hipStream_t s) {
     const ParentCuts none{};
-#define FBDT_HIST(R, NPV)                                                                        \
-    launch_hist_np<R, NPV>(hs, xb, ldb, n, d, n_bins, node_in, R ? node_out : nullptr, w,       \
-                           R ? pc : none, layer, scale, partial, small, err, s)
-    if (!routed) return FBDT_HIST(false, 0);
+    if (hs.features_per_group < 1 || hs.features_per_group > kHistFMax) return hipErrorInvalidValue;
+#define FBDT_HIST(R, NPV, FB)                                                                    \
+    launch_hist_np<R, NPV, FB>(hs, xb, ldb, n, d, n_bins, node_in, R ? node_out : nullptr, w,   \
+                               R ? pc : none, layer, scale, partial, small, err, s)
+#define FBDT_HIST_B(R, NPV) (n_bins == 256 ? FBDT_HIST(R, NPV, true) : FBDT_HIST(R, NPV, false))
+    if (!routed) return FBDT_HIST_B(false, 0);
     const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
     switch (parents) {
     case 0:
-    case 1: return FBDT_HIST(true, 1);
-    case 2: return FBDT_HIST(true, 2);
-    case 4: return FBDT_HIST(true, 4);
-    default: return FBDT_HIST(true, 0);
+    case 1: return FBDT_HIST_B(true, 1);
+    case 2: return FBDT_HIST_B(true, 2);
+    case 4: return FBDT_HIST_B(true, 4);
+    default: return FBDT_HIST_B(true, 0);
     }
+#undef FBDT_HIST_B
 #undef FBDT_HIST
 }
 
@@ -1174,14 +1417,14 @@ hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int 
     return hipGetLastError();
 }
 
-int leaf_blocks(int64_t n, int cu_count) { return grid_for(n, 256, 2 * cu_count); }
+int leaf_blocks(int64_t n, int cu_count) { return grid_for(n, 1024, cu_count); }
 
 template <bool ROUTED, int NL>
 void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
              const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
              const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
              double alpha, double *leaf_partial, int *err) {
-    leaf_kernel<ROUTED, NL><<<blocks, 256, 0, s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain,
+    leaf_kernel<ROUTED, NL><<<blocks, 1024, 0, s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain,
                                                    pc.cand_cut, pc.rec_f, pc.rec_c, pc.rec_g,
                                                    depth, y, v, F, seed, tree, alpha,
                                                    leaf_partial, err);
@@ -1221,7 +1464,8 @@ hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const u
 
 hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, double eta,
                                 double *leaf_out, hipStream_t s) {
-    leaf_finalize_kernel<<<1, 1024, 0, s>>>(leaf_partial, blocks, 1 << depth, eta, leaf_out);
+    leaf_finalize_kernel<<<1, kLeafReduceThreads, 0, s>>>(leaf_partial, blocks, 1 << depth, eta,
+                                                          leaf_out);
     return hipGetLastError();
 }
 
