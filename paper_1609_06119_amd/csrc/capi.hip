@@ -239,7 +239,10 @@ double hist_algorithmic_bytes(int64_t n, int d, int n_bins, int layer, bool rout
     } else {
         b += (double)n;                                 // node ids
     }
-    b += (double)(1 << layer) * d * n_bins * 2 * 8;     // the layer's histogram
+    // the histograms written: below the root a routed pass writes one child
+    // per parent (the other is parent - child)
+    const int hnodes = routed && layer >= 1 ? 1 << (layer - 1) : 1 << layer;
+    b += (double)hnodes * d * n_bins * 2 * 8;
     return b;
 }
 
@@ -434,10 +437,13 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     std::vector<HistShape> plans(D);
     size_t partial_elems = 0;
     for (int l = 0; l < D; ++l) {
-        plans[l] = plan_histogram(n, d, n_bins, l, di.cu_count, di.max_lds, (int)opt_hist_fpg.load(),
-                                  (int)opt_hist_chunks.load(), (int)opt_hist_threads.load());
+        // below the root the routed pass histograms one child per parent
+        plans[l] = plan_histogram(n, d, n_bins, l, true, di.cu_count, di.max_lds,
+                                  (int)opt_hist_fpg.load(), (int)opt_hist_chunks.load(),
+                                  (int)opt_hist_threads.load());
+        const size_t hnodes = l >= 1 ? (size_t)1 << (l - 1) : 1;
         partial_elems = std::max(partial_elems,
-                                 (size_t)plans[l].chunks * ((size_t)1 << l) * d * n_bins * 2);
+                                 (size_t)plans[l].chunks * hnodes * d * n_bins * 2);
         if (plans[l].lds_bytes + kHistStaticLdsReserve > di.max_lds)
             return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", l,
                         plans[l].lds_bytes, di.max_lds);
@@ -455,6 +461,10 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.node[0], npad);
     cv.add(&fb.node[1], npad);
     cv.add(&fb.partial, partial_elems);
+    // summed histograms of the layers that have children (all but the last)
+    const size_t hfull_elems = D >= 2 ? ((size_t)1 << (D - 2)) * d * n_bins * 2 : 1;
+    cv.add(&fb.hfull[0], hfull_elems);
+    cv.add(&fb.hfull[1], hfull_elems);
     const size_t small_elems = (size_t)max_nodes * d * n_bins * 2;
     cv.add(&fb.small, small_elems);
     cv.add(&fb.cand_gain, (size_t)max_nodes * d);
@@ -522,8 +532,11 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 }
                 {
                     Timed tm(FBDT_K_BEST_CUTS, st);
+                    // right children below the root: parent - left child
                     HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, scale, fb.small, nullptr,
-                                             1 << l, d, n_bins, fb.cand_gain, fb.cand_cut, st));
+                                             l >= 1 ? 1 << (l - 1) : 1, d, n_bins, fb.cand_gain,
+                                             fb.cand_cut, l >= 1 ? fb.hfull[(l - 1) & 1] : nullptr,
+                                             l + 1 < D ? fb.hfull[l & 1] : nullptr, st));
                     tm.done();
                 }
             }
@@ -771,7 +784,7 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     DeviceInfo di;
     if ((rc = current_device(&dev, &di))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    HistShape hs = plan_histogram(n, d, n_bins, layer, di.cu_count, di.max_lds,
+    HistShape hs = plan_histogram(n, d, n_bins, layer, false, di.cu_count, di.max_lds,
                                   (int)opt_hist_fpg.load(), (int)opt_hist_chunks.load(),
                                   (int)opt_hist_threads.load());
     if (hs.lds_bytes + kHistStaticLdsReserve > di.max_lds)
@@ -835,7 +848,8 @@ int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bin
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     Timed tm(FBDT_K_BEST_CUTS, s);
-    HIP_TRY(launch_best_cuts(nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cg, cc, s));
+    HIP_TRY(launch_best_cuts(nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cg, cc, nullptr,
+                             nullptr, s));
     HIP_TRY(launch_select_cuts(cg, cc, n_nodes, d, cut_feature, cut_bin, gain, s));
     tm.done();
     HIP_TRY(hipStreamSynchronize(s));

@@ -37,7 +37,9 @@ struct FitBuffers {
     double *F;            // [npad] score
     float *w;             // [npad] signed re-weighted sample
     uint8_t *node[2];     // [npad] node ids, double-buffered across layers
-    uint64_t *partial;    // fixed-point histogram partials [chunks][nodes][d][B][2]
+    uint64_t *partial;    // fixed-point histogram partials [chunks][histogrammed nodes][d][B][2]
+    uint64_t *hfull[2];   // summed fixed-point histograms of every node of a layer
+                          // [nodes][d][B][2], by layer parity (the next layer's parents)
     double *small;        // float64 histogram of the weights below the fixed-point grid
     double *cand_gain;    // [max nodes][d] best gain of every (node, feature)
     int *cand_cut;        // [max nodes][d] and its bin
@@ -89,8 +91,9 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
                             int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
                             double *score_out, int cu_count, hipStream_t s);
 
-// fpg, chunks, threads: launch-shape overrides (0 = default).
-HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
+// fpg, chunks, threads: launch-shape overrides (0 = default).  sibling: the
+// routed fit pass, which for layer >= 1 histograms one child per parent.
+HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, int cu_count,
                          size_t max_lds, int fpg, int chunks, int threads);
 
 // Candidate cuts of a layer's nodes, one per (node, feature), from which a
@@ -114,10 +117,13 @@ int histogram_scale(double total_weight_bound);
 // Histogram pass.  routed = true: node_in holds the ids of layer-1 (null for
 // layer <= 1, all events at the root), the pass routes them with the cuts of
 // layer-1 (from pc) and (first feature group only) writes the layer's ids to
-// node_out.
-// routed = false: node_in holds the ids of the layer itself.
-// partial: [chunks][2^layer][d][B][2] fixed-point sums; small: [2^layer][d][B][2]
-// float64 sums of the weights below the grid (accumulated into, not cleared).
+// node_out; for layer >= 1 it histograms only the left child of every
+// parent (the right child is the parent minus the left child, formed by
+// best_cuts): partial: [chunks][2^(layer-1)][d][B][2], indexed by parent.
+// routed = false: node_in holds the ids of the layer itself; partial:
+// [chunks][2^layer][d][B][2].
+// small: [2^layer][d][B][2] float64 sums of the weights below the grid, for
+// every node of the layer (accumulated into, not cleared).
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                             const float *w, const ParentCuts &pc, int layer, bool routed,
@@ -135,9 +141,16 @@ hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, doub
 // Best cut of every (node, feature) of a layer into cand_gain/cand_cut, from
 // fixed-point chunk partials plus the float64 side histogram (which it
 // clears), or, with partial == null, from a float64 histogram `hist`.
+// n_nodes: histogrammed nodes (one workgroup per node and feature).  With
+// hparent != null (fixed-point path, layer >= 1) the partials are the left
+// children of n_nodes parents and hparent [n_nodes][d][B][2] their summed
+// histograms: the right child is parent - left, exactly, and both children
+// get candidates (layer index 2k, 2k + 1 for parent k).  hout (optional)
+// receives the summed fixed-point histogram of every node of the layer.
 hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
                             const double *hist, int n_nodes, int d, int n_bins,
-                            double *cand_gain, int *cand_cut, hipStream_t s);
+                            double *cand_gain, int *cand_cut, const uint64_t *hparent,
+                            uint64_t *hout, hipStream_t s);
 
 // Best cut of each node over its features.
 hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,

@@ -194,6 +194,13 @@ __device__ void reduce_leaf_partials(const double *__restrict__ leaf_partial, in
 // straight from the leaf pass partials (leaf_partial, depth <= 4), which
 // every workgroup sums itself in the fixed order of leaf_finalize_kernel;
 // workgroup 0 then records them in the model (leaf_rec).
+struct PrepStep {
+    int yv;
+    uint32_t leaf;
+    float v;
+    double F;
+};
+
 __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     const int8_t *__restrict__ y, const float *__restrict__ v, double *__restrict__ F,
     const double *__restrict__ f0, const uint8_t *__restrict__ leaf_node,
@@ -205,6 +212,19 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     __shared__ double s_leaf[128];
     const unsigned nleaf = 1u << depth;
     const bool have_leaf = leaf_prev || leaf_partial;
+    const bool read_F = have_leaf || !f0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t ia = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    // one event per thread and step; the first step's loads are in flight
+    // while the boost weights are summed, later steps are loaded one ahead
+    auto load = [&](PrepStep &st, int64_t i) {
+        st.yv = y[i];
+        st.v = v ? v[i] : 1.0f;
+        st.leaf = have_leaf ? (uint32_t)leaf_node[i] : 0u;
+        st.F = read_F ? F[i] : 0.0;
+    };
+    PrepStep A, B;
+    if (ia < n) load(A, ia);
     if (leaf_partial) {
         reduce_leaf_partials(leaf_partial, lblocks, (int)nleaf, eta, red, s_leaf);
         if (blockIdx.x == 0 && leaf_rec && threadIdx.x < nleaf) leaf_rec[threadIdx.x] = s_leaf[threadIdx.x];
@@ -213,27 +233,38 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
         __syncthreads();
     }
     const double f0v = (f0 && !have_leaf) ? *f0 : 0.0;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
+    auto step = [&](const PrepStep &st, int64_t i) {
         double Fi;
         if (have_leaf) {
-            unsigned li = (unsigned)leaf_node[i] - nleaf;
+            unsigned li = st.leaf - nleaf;
             if (li >= nleaf) li = 0;  // unreachable: leaf ids come from the leaf pass
-            Fi = F[i] + s_leaf[li];
+            Fi = st.F + s_leaf[li];
             F[i] = Fi;
         } else if (f0) {
             Fi = f0v;
             F[i] = Fi;
         } else {
-            Fi = F[i];
+            Fi = st.F;
         }
         if (score_out) score_out[i] = Fi;
         if (w) {
-            const double yf = (double)y[i];
+            const double yf = (double)st.yv;
             const double yt = pseudo_response(yf, Fi);
-            const double vi = v ? (double)v[i] : 1.0;
+            const double vi = (double)st.v;
             const float wi = in_subsample(seed, tree, n, i, alpha) ? (float)(vi * fabs(yt)) : 0.0f;
             w[i] = yf > 0.0 ? wi : -wi;
+        }
+    };
+    if (ia < n) {
+        for (;;) {
+            const int64_t ib = ia + stride;
+            if (ib < n) load(B, ib);
+            step(A, ia);
+            if (ib >= n) break;
+            ia = ib + stride;
+            if (ia < n) load(A, ia);
+            step(B, ib);
+            if (ia >= n) break;
         }
     }
 }
@@ -463,13 +494,22 @@ __device__ __forceinline__ void hist_add(
     // shifted into place, exact for w >= tau.  Weights below the grid are
     // added in float64 to the side histogram.
     const int rowc = 2 * fstride;   // counters per (node, feature)
+    // Routed passes below the root histogram the left child of every parent
+    // only (slot = parent index); the right child's fixed-point histogram is
+    // parent - left.  Weights below the grid go to the side histogram of
+    // every node, left or right.
+    const bool left_only = ROUTED && layer >= 1;
 #pragma unroll
     for (int e = 0; e < kHistE; ++e) {
         const uint32_t bits = __float_as_uint(st.w[e]);
         const uint32_t ab = bits & 0x7fffffffu;
         const float a = __uint_as_float(ab);
-        const uint32_t loc = byte8(nd, e) - (uint32_t)(nodes + k0);
+        const uint32_t node = byte8(nd, e);
+        const uint32_t loc = left_only ? (node >> 1) - (uint32_t)(half + k0)
+                                       : node - (uint32_t)(nodes + k0);
+        const bool counted = !left_only || (node & 1u) == 0u;
         if (loc < (uint32_t)nk && a >= tau) {
+            if (!counted) continue;
             const int sh = (int)(ab >> 23) - 150 + scale;   // >= 0 for a >= tau
             const uint64_t fx = (uint64_t)((ab & 0x7fffffu) | 0x800000u) << sh;
             const int slot = (int)loc * fpg * rowc + (int)(bits >> 31);
@@ -491,7 +531,8 @@ __device__ __forceinline__ void hist_add(
                     continue;
                 }
                 const size_t gi =
-                    ((((size_t)(k0 + (int)loc) * d + j0 + ff) * nbins + bin) * 2) + (bits >> 31);
+                    ((((size_t)(node - (uint32_t)nodes) * d + j0 + ff) * nbins + bin) * 2) +
+                    (bits >> 31);
                 atomicAdd(&small[gi], (double)a);
             }
         }
@@ -524,10 +565,11 @@ __global__ __launch_bounds__(1024) void hist_kernel(
 
     const int nodes = 1 << layer;
     const int half = nodes >> 1;
+    const int hnodes = ROUTED && layer >= 1 ? half : nodes;   // histogrammed nodes
     const int j0 = g * fpg;
     const int nf = min(fpg, d - j0);
     const int k0 = h * npg;
-    const int nk = min(npg, nodes - k0);
+    const int nk = min(npg, hnodes - k0);
     const int fstride = FULLB ? 256 : nbins + 1;
     const int lds_n = npg * fpg * 2 * fstride;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
@@ -608,7 +650,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     // partial[p][node][feature][bin][class]: one (node, feature) row per
     // wavefront step, lanes over bins and classes
     const int per_nf = nbins * 2;
-    uint64_t *out = partial + (size_t)p * nodes * d * per_nf;
+    uint64_t *out = partial + (size_t)p * hnodes * d * per_nf;
     for (int kf = wave; kf < nk * nf; kf += nwaves) {
         const int k = kf / nf;
         const int f = kf - k * nf;
@@ -679,14 +721,17 @@ template <bool FIXED>
 __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
     const uint64_t *__restrict__ partial, int chunks, int scale, double *__restrict__ small,
     const double *__restrict__ hist, int nodes, int d, int nbins,
-    double *__restrict__ cand_gain, int *__restrict__ cand_cut) {
+    double *__restrict__ cand_gain, int *__restrict__ cand_cut,
+    const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout) {
 #pragma clang fp contract(off)
-    // one workgroup of kBcWaves wavefronts per (node, feature); wavefront w
-    // sums the fixed-point chunk partials w, w + kBcWaves, ... (integer sums:
-    // exact in any order), so that all chunk loads are in flight together;
-    // wavefront 0 adds the sums, converts them to float64 and adds the side
-    // histogram of weights below the grid
-    __shared__ uint64_t red[kBcWaves][kWave][8];
+    // one workgroup of kBcWaves wavefronts per (histogrammed node, feature);
+    // wavefront w sums the fixed-point chunk partials w, w + kBcWaves, ...
+    // (integer sums: exact in any order), so that all chunk loads are in
+    // flight together; wavefront 0 (and, for a left child, wavefront 1 with
+    // the right child = parent - left) converts the sums to float64 and adds
+    // the side histogram of weights below the grid
+    __shared__ uint64_t red[kBcWaves][8][kWave];   // lane fastest: no bank conflicts
+    __shared__ double side[2][8][kWave];
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
     const int pair = blockIdx.x;
@@ -694,12 +739,23 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
     const int j = pair - k * d;
     const int b0 = 4 * lane;
     const int nb = b0 < nbins ? min(4, nbins - b0) : 0;
-    const size_t off = ((size_t)k * d + j) * nbins * 2 + 2 * b0;
+    const size_t row = (size_t)nbins * 2;
+    const size_t off = ((size_t)k * d + j) * row + 2 * b0;   // histogrammed node k
+    const bool sib = FIXED && hparent != nullptr;
+    // node of this wavefront's candidate, as an index within the layer
+    const int node = sib ? 2 * k + (wave & 1) : k;
+    const size_t noff = ((size_t)node * d + j) * row + 2 * b0;
 
     double hs[4] = {0.0, 0.0, 0.0, 0.0}, hb[4] = {0.0, 0.0, 0.0, 0.0};
     if (FIXED) {
+        uint64_t ps[4] = {0, 0, 0, 0}, pb[4] = {0, 0, 0, 0};
+        if (sib && wave == 1)   // the parent's summed histogram, for the right child
+            for (int e = 0; e < nb; ++e) {
+                ps[e] = hparent[off + 2 * e];
+                pb[e] = hparent[off + 2 * e + 1];
+            }
         uint64_t us[4] = {0, 0, 0, 0}, ub[4] = {0, 0, 0, 0};
-        const size_t stride_p = (size_t)nodes * d * nbins * 2;
+        const size_t stride_p = (size_t)nodes * d * row;
         if (nb == 4) {
             int p = wave;
             for (; p + kBcWaves < chunks; p += 2 * kBcWaves) {   // two chunks in flight
@@ -730,29 +786,66 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            red[wave][lane][e] = us[e];
-            red[wave][lane][4 + e] = ub[e];
+            red[wave][e][lane] = us[e];
+            red[wave][4 + e][lane] = ub[e];
         }
-        __syncthreads();
-        if (wave != 0) return;
-        uint64_t ts[4] = {0, 0, 0, 0}, tb[4] = {0, 0, 0, 0};
-        for (int wv = 0; wv < kBcWaves; ++wv) {
+        if (wave >= kBcWaves - 2 && (sib || wave == kBcWaves - 1)) {
+            // side histograms of weights below the grid: the last wavefront
+            // loads the left (or only) node's, the one before it the right's
+            const int c = sib ? wave - (kBcWaves - 2) : 0;
+            const size_t so = ((size_t)(sib ? 2 * k + c : k) * d + j) * row + 2 * b0;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                ts[e] += red[wv][lane][e];
-                tb[e] += red[wv][lane][4 + e];
+                side[c][e][lane] = e < nb ? small[so + 2 * e] : 0.0;
+                side[c][4 + e][lane] = e < nb ? small[so + 2 * e + 1] : 0.0;
             }
         }
+        __syncthreads();
+        // the wavefront sums: value (e, l) over wavefronts [h kBcWaves / 2,
+        // (h + 1) kBcWaves / 2) by thread 512 h + 64 e + l, all reads in flight
+        // together; the candidate wavefronts add the two halves
+        {
+            const int vi = threadIdx.x % (8 * kWave), hh = threadIdx.x / (8 * kWave);
+            const int e = vi / kWave, l = vi % kWave;
+            uint64_t t = 0;
+            if (hh < 2) {
+#pragma unroll
+                for (int wv = 0; wv < kBcWaves / 2; ++wv) t += red[hh * (kBcWaves / 2) + wv][e][l];
+            }
+            __syncthreads();
+            if (hh < 2) red[hh][e][l] = t;
+            __syncthreads();
+        }
+        if (wave >= (sib ? 2 : 1)) return;
+        uint64_t ts[4], tb[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            ts[e] = red[0][e][lane] + red[1][e][lane];
+            tb[e] = red[0][4 + e][lane] + red[1][4 + e][lane];
+        }
+        if (sib && wave == 1) {   // right child = parent - left child (exact)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                ts[e] = ps[e] - ts[e];
+                tb[e] = pb[e] - tb[e];
+            }
+        }
+        if (hout)
+            for (int e = 0; e < nb; ++e) {
+                hout[noff + 2 * e] = ts[e];
+                hout[noff + 2 * e + 1] = tb[e];
+            }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             hs[e] = ldexp((double)ts[e], -scale);
             hb[e] = ldexp((double)tb[e], -scale);
         }
+        const int c = sib ? wave : 0;
         for (int e = 0; e < nb; ++e) {   // side histogram, cleared for the next layer
-            hs[e] += small[off + 2 * e];
-            hb[e] += small[off + 2 * e + 1];
-            small[off + 2 * e] = 0.0;
-            small[off + 2 * e + 1] = 0.0;
+            hs[e] += side[c][e][lane];
+            hb[e] += side[c][4 + e][lane];
+            small[noff + 2 * e] = 0.0;
+            small[noff + 2 * e + 1] = 0.0;
         }
     } else {
         if (wave != 0) return;
@@ -837,8 +930,8 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
         }
     }
     if (lane == 0) {
-        cand_gain[pair] = best;
-        cand_cut[pair] = bestc;
+        cand_gain[(size_t)node * d + j] = best;
+        cand_cut[(size_t)node * d + j] = bestc;
     }
 }
 
@@ -1261,10 +1354,10 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
     return hipGetLastError();
 }
 
-HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, int cu_count,
+HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, int cu_count,
                          size_t max_lds, int fpg, int chunks, int threads) {
     HistShape hs{};
-    const int nodes = 1 << layer;
+    const int nodes = sibling && layer >= 1 ? 1 << (layer - 1) : 1 << layer;
     // LDS row of one (node, feature): 256 bins, or n_bins + 1 with the
     // out-of-range counter, times two classes
     const int fstride = n_bins == 256 ? 256 : n_bins + 1;
@@ -1401,13 +1494,16 @@ hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, doub
 
 hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
                             const double *hist, int n_nodes, int d, int n_bins,
-                            double *cand_gain, int *cand_cut, hipStream_t s) {
+                            double *cand_gain, int *cand_cut, const uint64_t *hparent,
+                            uint64_t *hout, hipStream_t s) {
     if (partial)
         best_cuts_kernel<true><<<n_nodes * d, kBcWaves * kWave, 0, s>>>(
-            partial, chunks, scale, small, nullptr, n_nodes, d, n_bins, cand_gain, cand_cut);
+            partial, chunks, scale, small, nullptr, n_nodes, d, n_bins, cand_gain, cand_cut,
+            hparent, hout);
     else
         best_cuts_kernel<false><<<n_nodes * d, kBcWaves * kWave, 0, s>>>(
-            nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cand_gain, cand_cut);
+            nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cand_gain, cand_cut, nullptr,
+            nullptr);
     return hipGetLastError();
 }
 
