@@ -257,6 +257,8 @@ int fbdt_set_option(const char *name, int64_t value) {
     if (!name) return fail(FBDT_E_INVAL, "option name is NULL");
     if (value < 0) return fail(FBDT_E_INVAL, "option %s: value must be >= 0", name);
     if (!strcmp(name, "hist_features_per_group")) {
+        if (value != 0 && !hist_fpg_supported((int)value))
+            return fail(FBDT_E_INVAL, "hist_features_per_group must be 0, 1, 2, 4, 5 or 8");
         opt_hist_fpg = value;
     } else if (!strcmp(name, "hist_event_chunks")) {
         opt_hist_chunks = value;
@@ -482,6 +484,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
 
     HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
     HIP_TRY(launch_fill_u32(fb.small, 0u, 2 * small_elems, s));
+    // the histogram passes read whole steps of events: padded events weigh 0
+    HIP_TRY(launch_fill_u32(fb.w, 0u, (size_t)npad, s));
     HIP_TRY(launch_validate(y, w, n, fb.class_partial, fb.err, s));
     HIP_TRY(launch_initial_score(fb.class_partial, fb.f0, fb.err, s));
     int h_err = 0;
@@ -791,12 +795,19 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
         return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", layer,
                     hs.lds_bytes, di.max_lds);
     const size_t count = ((size_t)1 << layer) * d * n_bins * 2;
+    // the pass reads whole steps of events: node ids and weights are copied
+    // into buffers padded with zero weights
+    const int64_t npad = (n + 15) & ~(int64_t)15;
     Arena &a = g_arena[dev];
     std::lock_guard<std::mutex> lk(a.mu);
     Carver cv;
     uint64_t *partial;
     double *small, *bpart, *wsum;
     int *err;
+    uint8_t *node_pad;
+    float *w_pad;
+    cv.add(&node_pad, (size_t)npad);
+    cv.add(&w_pad, (size_t)npad);
     cv.add(&partial, (size_t)hs.chunks * count);
     cv.add(&small, count);
     cv.add(&bpart, kValidateBlocks);
@@ -806,6 +817,10 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     cv.assign(a.ptr);
     HIP_TRY(launch_fill_u32(err, 0u, 1, s));
     HIP_TRY(launch_fill_u32(small, 0u, 2 * count, s));
+    HIP_TRY(launch_fill_u32(node_pad, 0u, (size_t)npad / 4, s));
+    HIP_TRY(launch_fill_u32(w_pad, 0u, (size_t)npad, s));
+    HIP_TRY(hipMemcpyAsync(node_pad, node, (size_t)n, hipMemcpyDeviceToDevice, s));
+    HIP_TRY(hipMemcpyAsync(w_pad, w, (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, s));
     HIP_TRY(launch_abs_sum(w, n, bpart, wsum, s));
     double h_wsum = 0.0;
     HIP_TRY(hipMemcpyAsync(&h_wsum, wsum, sizeof h_wsum, hipMemcpyDeviceToHost, s));
@@ -814,8 +829,8 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     const int scale = histogram_scale(h_wsum * (1.0 + 1e-6));
     {
         Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, layer, false));
-        HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node, nullptr, w, ParentCuts{},
-                                 layer, false, scale, partial, small, err, s));
+        HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node_pad, nullptr, w_pad,
+                                 ParentCuts{}, layer, false, scale, partial, small, err, s));
         tm.done();
     }
     HIP_TRY(launch_merge_partials(partial, hs.chunks, count, scale, small, hist, s));

@@ -58,9 +58,11 @@ constexpr int kValidateBlocks = 256;
 // LDS kept aside for a kernel's static shared arrays when sizing its
 // dynamic LDS (the histogram kernel's cut table takes 128 bytes)
 constexpr size_t kHistStaticLdsReserve = 1024;
-// features whose codes one histogram workgroup holds in registers per step
-// (the most features a workgroup takes)
+// features per histogram workgroup the kernels are built for (a workgroup
+// holds the codes of all of them in registers per step)
+constexpr int kHistFpgSizes[] = {1, 2, 4, 5, 8};
 constexpr int kHistFMax = 8;
+bool hist_fpg_supported(int f);
 
 // Sets the per-kernel attributes the launchers rely on (dynamic LDS above
 // 64 KiB) for the current device; called once per device before any launch,
@@ -124,6 +126,10 @@ int histogram_scale(double total_weight_bound);
 // [chunks][2^layer][d][B][2].
 // small: [2^layer][d][B][2] float64 sums of the weights below the grid, for
 // every node of the layer (accumulated into, not cleared).
+// Every step reads kHistE = 8 whole events: w and node_in must hold
+// round_up(n, 8) elements, with weight 0 beyond n (those events count
+// nowhere), code rows ldb >= round_up(n, 8) bytes, and node_out room for
+// round_up(n, 8) ids (the padded events are routed too).
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                             const float *w, const ParentCuts &pc, int layer, bool routed,

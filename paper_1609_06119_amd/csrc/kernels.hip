@@ -355,15 +355,18 @@ __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restric
 // ---------------------------------------------------------------------------
 // Layer histogram.  Workgroup (chunk p, feature group g, node group h) keeps
 // H[node in h][feature in g][bin][class] in LDS as 64-bit fixed point
-// (weight * 2^scale), adds every sampled event of its event chunk with a
+// (weight * 2^scale), adds every counted event of its event chunk with a
 // 64-bit integer LDS atomic, and writes its partial histogram once at the
 // end; integer sums are exact, so the result is independent of the order of
 // the adds, and best_cuts sums the chunk partials.
 //
 // Each thread handles kHistE consecutive events per step and loads the next
-// step's weights, node ids, routing rows and feature codes (all features of
-// the group) before it adds the current step's events, so every load of a
-// step is in flight while the LDS atomics of the previous one run.
+// step's weights, node ids, routing rows and the codes of the group's FPG
+// features before it adds the current step's events.  Per event it forms
+// once its node of this layer (routing), the LDS offset of its (node, class)
+// counters, the fixed-point value and whether it counts; one branch per
+// event then covers its FPG atomics, whose feature-row offsets are
+// immediates of the LDS instruction.
 //
 // Routed mode computes every event's node of this layer from its parent
 // (layer - 1) and the parent's cut on the way; the first feature group
@@ -372,180 +375,196 @@ __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restric
 // costs no dependent load; with NP = 0 each event's routing code is
 // gathered after its parent id arrives (deep layers).
 //
-// LDS row of (node, feature): `fstride` bins x 2 classes, fstride = 256 for
-// 256 bins (the row offset of feature f is then a compile-time constant of
-// the atomic), else n_bins + 1 with the extra bin collecting codes >= n_bins
-// (reported as an error).
+// An LDS row of (node, feature) holds 256 bins x 2 classes (4 KiB) whatever
+// n_bins; codes >= n_bins land in bins that are checked at the end and
+// reported as an error.  The last feature group may run past feature d - 1:
+// its missing features load the codes of feature d - 1 and add them into
+// rows that are never written out, so the inner loop has no feature test.
+constexpr int kRow = 256 * 2;                        // counters per LDS row
+constexpr int kRowBytes = kRow * (int)sizeof(uint64_t);
+
 __device__ __forceinline__ uint32_t byte8(const uint2 &v, int e) {
     const uint32_t w = e < 4 ? v.x : v.y;
     return (w >> (8 * (e & 3))) & 0xffu;
 }
 
-// kHistE bytes at p[i0..]; bytes at i >= n read as `fill`.
-__device__ __forceinline__ uint2 load_bytes8(const uint8_t *__restrict__ p, int64_t i0,
-                                             int64_t n, bool full, uint32_t fill) {
-    if (full) return *reinterpret_cast<const uint2 *>(p + i0);
-    uint32_t t[2] = {fill * 0x01010101u, fill * 0x01010101u};
-    for (int e = 0; e < kHistE; ++e)
-        if (i0 + e < n)
-            t[e >> 2] = (t[e >> 2] & ~(0xffu << (8 * (e & 3)))) |
-                        ((uint32_t)p[i0 + e] << (8 * (e & 3)));
-    return make_uint2(t[0], t[1]);
-}
-
-template <int NP>
+template <int NP, int FPG>
 struct HistStep {
-    float w[kHistE];
+    uint32_t w[kHistE];               // weight bits (class in the sign bit)
     uint2 node;                       // parent ids (routed, layer >= 2) or node ids
     uint2 rows[NP > 0 ? NP : 1];      // codes of the parents' cut features
-    uint2 codes[kHistFMax];           // codes of the group's features
+    uint2 codes[FPG];                 // codes of the group's features
+};
+
+// Uniform per-workgroup arguments of the histogram pass.
+struct HistArgs {
+    const uint8_t *xb;
+    int64_t ldb, n;
+    int d, nbins, layer, nodes, half, j0, nf, k0, nk, scale;
+    uint32_t tau_bits;                // bits of the smallest weight on the fixed-point grid
+    const uint8_t *node_in;
+    uint8_t *node_out;
+    const float *w;
+    double *small;
 };
 
 // codes of the parents' cut features (the cut table must be in LDS)
-template <bool ROUTED, int NP>
-__device__ __forceinline__ void hist_load_rows(HistStep<NP> &st, const uint8_t *__restrict__ xb,
-                                               int64_t ldb, int d, const uint8_t *s_cf, int layer,
-                                               int64_t i0) {
-    if (ROUTED && NP > 0 && layer >= 1) {
+template <bool ROUTED, int NP, int FPG>
+__device__ __forceinline__ void hist_load_rows(HistStep<NP, FPG> &st, const HistArgs &a,
+                                               const uint8_t *s_cf, int64_t i0) {
+    if (ROUTED && NP > 0 && a.layer >= 1) {
         // rows are padded to ldb >= i0 + kHistE: always in bounds
 #pragma unroll
         for (int kk = 0; kk < (NP > 0 ? NP : 1); ++kk)
             st.rows[kk] = *reinterpret_cast<const uint2 *>(
-                xb + (int64_t)min((int)s_cf[kk], d - 1) * ldb + i0);
+                a.xb + (int64_t)min((int)s_cf[kk], a.d - 1) * a.ldb + i0);
     }
 }
 
-template <bool ROUTED, int NP>
-__device__ __forceinline__ void hist_load(HistStep<NP> &st, const uint8_t *__restrict__ xb,
-                                          int64_t ldb, int64_t n, int d, int j0, int nf,
-                                          const uint8_t *__restrict__ node_in,
-                                          const float *__restrict__ w, const uint8_t *s_cf,
-                                          int layer, int half, int64_t i0, bool with_rows) {
-    const bool full = i0 + kHistE <= n;
-    if (full) {
-        const float4 a = reinterpret_cast<const float4 *>(w + i0)[0];
-        const float4 b = reinterpret_cast<const float4 *>(w + i0)[1];
-        st.w[0] = a.x; st.w[1] = a.y; st.w[2] = a.z; st.w[3] = a.w;
-        st.w[4] = b.x; st.w[5] = b.y; st.w[6] = b.z; st.w[7] = b.w;
-    } else {
+// The per-event arrays (weights, node ids) are padded to a multiple of
+// kHistE with zero weights, and code rows to ldb >= that padding, so every
+// step loads kHistE whole events; padded events weigh 0 and count nowhere.
+template <bool ROUTED, int NP, int FPG>
+__device__ __forceinline__ void hist_load(HistStep<NP, FPG> &st, const HistArgs &a,
+                                          const uint8_t *s_cf, int64_t i0, bool with_rows) {
+    const uint4 x = reinterpret_cast<const uint4 *>(a.w + i0)[0];
+    const uint4 y = reinterpret_cast<const uint4 *>(a.w + i0)[1];
+    st.w[0] = x.x; st.w[1] = x.y; st.w[2] = x.z; st.w[3] = x.w;
+    st.w[4] = y.x; st.w[5] = y.y; st.w[6] = y.z; st.w[7] = y.w;
+    if (!ROUTED || a.layer >= 2) st.node = *reinterpret_cast<const uint2 *>(a.node_in + i0);
 #pragma unroll
-        for (int e = 0; e < kHistE; ++e) st.w[e] = (i0 + e < n) ? w[i0 + e] : 0.0f;
-    }
-    if (!ROUTED)
-        st.node = load_bytes8(node_in, i0, n, full, 0u);
-    else if (layer >= 2)
-        st.node = load_bytes8(node_in, i0, n, full, (uint32_t)half);
-#pragma unroll
-    for (int ff = 0; ff < kHistFMax; ++ff)
-        if (ff < nf)
-            st.codes[ff] = *reinterpret_cast<const uint2 *>(xb + (int64_t)(j0 + ff) * ldb + i0);
-    if (with_rows) hist_load_rows<ROUTED, NP>(st, xb, ldb, d, s_cf, layer, i0);
+    for (int ff = 0; ff < FPG; ++ff)
+        st.codes[ff] = *reinterpret_cast<const uint2 *>(
+            a.xb + (int64_t)min(a.j0 + ff, a.d - 1) * a.ldb + i0);
+    if (with_rows) hist_load_rows<ROUTED, NP, FPG>(st, a, s_cf, i0);
 }
 
-template <bool ROUTED, int NP, bool FULLB>
-__device__ __forceinline__ void hist_add(
-    const HistStep<NP> &st, uint64_t *lds, const uint8_t *__restrict__ xb, int64_t ldb,
-    int64_t n, int d, int nbins, uint8_t *__restrict__ node_out, bool writer,
-    const float *__restrict__ w, const uint8_t *s_cf, const uint8_t *s_cc, int layer, int nodes,
-    int half, int j0, int nf, int k0, int nk, int fpg, int fstride, float tau, int scale,
-    double *__restrict__ small, int64_t i0, int &eflag) {
-    // node ids of this layer
-    uint2 nd;
-    if (!ROUTED) {
-        nd = st.node;
-    } else if (layer == 0) {
-        nd = make_uint2(0x01010101u, 0x01010101u);
-    } else {
-        const uint2 par = layer == 1 ? make_uint2(0x01010101u, 0x01010101u) : st.node;
-        uint32_t o[2] = {0u, 0u};
-#pragma unroll
-        for (int e = 0; e < kHistE; ++e) {
-            int pe = (int)byte8(par, e);
-            unsigned k = (unsigned)(pe - half);
-            if (k >= (unsigned)half) {  // unreachable for ids written by this library
-                eflag |= kErrRoute;
-                k = 0;
-                pe = half;
-            }
-            uint32_t code;
-            if (NP > 0) {
-                code = byte8(st.rows[0], e);
-#pragma unroll
-                for (int kk = 1; kk < (NP > 0 ? NP : 1); ++kk)
-                    if (k == (unsigned)kk) code = byte8(st.rows[kk], e);
-            } else {
-                code = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i0 + e];
-            }
-            const uint32_t ne = 2u * (uint32_t)pe + (code >= s_cc[k] ? 1u : 0u);
-            o[e >> 2] |= ne << (8 * (e & 3));
-        }
-        nd = make_uint2(o[0], o[1]);
-        if (writer) {
-            if (i0 + kHistE <= n) {
-                *reinterpret_cast<uint2 *>(node_out + i0) = nd;
-            } else {
-                for (int e = 0; e < kHistE; ++e)
-                    if (i0 + e < n) node_out[i0 + e] = (uint8_t)byte8(nd, e);
-            }
-        }
-    }
-    // Sampled events of this group's nodes add w * 2^scale to their
-    // (node, feature, bin, class) counter: the float's 24-bit significand
-    // shifted into place, exact for w >= tau.  Weights below the grid are
-    // added in float64 to the side histogram.
-    const int rowc = 2 * fstride;   // counters per (node, feature)
+template <bool ROUTED, int NP, int FPG>
+__device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const HistArgs &a,
+                                         uint64_t *lds, bool writer, const uint8_t *s_cf,
+                                         const uint8_t *s_cc, const uint32_t (&cut)[4],
+                                         int64_t i0, int &eflag) {
+    // Per event: slot = index of the histogrammed node within the group
+    // (>= nk: not this group's), nl = node of this layer - nodes (side
+    // histogram index), counted = the event's node is histogrammed here.
     // Routed passes below the root histogram the left child of every parent
     // only (slot = parent index); the right child's fixed-point histogram is
     // parent - left.  Weights below the grid go to the side histogram of
     // every node, left or right.
-    const bool left_only = ROUTED && layer >= 1;
+    uint32_t slot[kHistE], nl[kHistE];
+    bool counted[kHistE];
+    uint32_t bad = 0u;
+    if (!ROUTED) {
 #pragma unroll
-    for (int e = 0; e < kHistE; ++e) {
-        const uint32_t bits = __float_as_uint(st.w[e]);
-        const uint32_t ab = bits & 0x7fffffffu;
-        const float a = __uint_as_float(ab);
-        const uint32_t node = byte8(nd, e);
-        const uint32_t loc = left_only ? (node >> 1) - (uint32_t)(half + k0)
-                                       : node - (uint32_t)(nodes + k0);
-        const bool counted = !left_only || (node & 1u) == 0u;
-        if (loc < (uint32_t)nk && a >= tau) {
-            if (!counted) continue;
-            const int sh = (int)(ab >> 23) - 150 + scale;   // >= 0 for a >= tau
-            const uint64_t fx = (uint64_t)((ab & 0x7fffffu) | 0x800000u) << sh;
-            const int slot = (int)loc * fpg * rowc + (int)(bits >> 31);
+        for (int e = 0; e < kHistE; ++e) {
+            const uint32_t node = byte8(st.node, e);
+            nl[e] = node - (uint32_t)a.nodes;
+            slot[e] = nl[e] - (uint32_t)a.k0;
+            counted[e] = true;
+        }
+    } else if (a.layer == 0) {
 #pragma unroll
-            for (int ff = 0; ff < kHistFMax; ++ff) {
-                if (ff < nf) {
-                    uint32_t bin = byte8(st.codes[ff], e);
-                    if (!FULLB) bin = min(bin, (uint32_t)nbins);
-                    atomicAdd(&lds[slot + ff * (FULLB ? 512 : rowc) + 2 * (int)bin], fx);
+        for (int e = 0; e < kHistE; ++e) {
+            nl[e] = 0u;
+            slot[e] = 0u;
+            counted[e] = true;
+        }
+    } else {
+        uint32_t o[2] = {0u, 0u};
+#pragma unroll
+        for (int e = 0; e < kHistE; ++e) {
+            uint32_t par, k, code, c;
+            if (NP == 1) {   // layer 1: the root is the only parent
+                par = 1u;
+                k = 0u;
+                code = byte8(st.rows[0], e);
+                c = cut[0];
+            } else {
+                par = byte8(st.node, e);
+                k = par - (uint32_t)a.half;
+                if (k >= (uint32_t)a.half) {   // unreachable for ids written by this library
+                    bad = 1u;
+                    k = 0u;
+                    par = (uint32_t)a.half;
+                }
+                if (NP > 0) {
+                    code = byte8(st.rows[0], e);
+                    c = cut[0];
+#pragma unroll
+                    for (int kk = 1; kk < (NP > 0 ? NP : 1); ++kk) {
+                        if (k == (uint32_t)kk) {
+                            code = byte8(st.rows[kk], e);
+                            c = cut[kk];
+                        }
+                    }
+                } else {
+                    code = a.xb[(int64_t)min((int)s_cf[k], a.d - 1) * a.ldb + i0 + e];
+                    c = s_cc[k];
                 }
             }
-        } else if (loc < (uint32_t)nk && ab != 0u) {   // rare: below the fixed-point grid
+            const uint32_t right = code >= c ? 1u : 0u;
+            const uint32_t ne = 2u * par + right;
+            o[e >> 2] |= ne << (8 * (e & 3));
+            nl[e] = ne - (uint32_t)a.nodes;
+            slot[e] = k - (uint32_t)a.k0;
+            counted[e] = right == 0u;
+        }
+        // padded events get ids too, so that the next layer reads valid parents
+        if (writer) *reinterpret_cast<uint2 *>(a.node_out + i0) = make_uint2(o[0], o[1]);
+    }
+    if (bad) eflag |= kErrRoute;
+    // Counted events of this group's nodes add w * 2^scale to their
+    // (node, feature, bin, class) counter: the float's 24-bit significand
+    // shifted into place, exact for weights on the grid (>= tau).
+    char *ldsb = reinterpret_cast<char *>(lds);
+    uint32_t below = 0u;
 #pragma unroll
-            for (int ff = 0; ff < kHistFMax; ++ff) {
-                if (ff >= nf) break;
-                const uint32_t bin = byte8(st.codes[ff], e);
-                if (bin >= (uint32_t)nbins) {
-                    eflag |= kErrBin;
-                    continue;
+    for (int e = 0; e < kHistE; ++e) {
+        const uint32_t bits = st.w[e];
+        const uint32_t ab = bits & 0x7fffffffu;
+        const bool mine = slot[e] < (uint32_t)a.nk;
+        if (mine && (ab - 1u) < a.tau_bits - 1u) below |= 1u << e;   // 0 < w < tau: rare
+        if (mine && counted[e] && ab >= a.tau_bits) {
+            const int sh = (int)(ab >> 23) - 150 + a.scale;   // >= 0 on the grid
+            const uint64_t fx = (uint64_t)((ab & 0x7fffffu) | 0x800000u) << sh;
+            const uint32_t base = slot[e] * (uint32_t)(FPG * kRowBytes) + ((bits >> 28) & 8u);
+#pragma unroll
+            for (int ff = 0; ff < FPG; ++ff) {
+                const uint32_t off = base + (byte8(st.codes[ff], e) << 4);
+                atomicAdd(reinterpret_cast<uint64_t *>(ldsb + off) + ff * kRow, fx);
+            }
+        }
+    }
+    if (below) {   // weights below the grid: float64 side histogram of the event's node
+        // (indices stay compile-time constants so that the step stays in registers)
+#pragma unroll
+        for (int e = 0; e < kHistE; ++e) {
+            if ((below >> e) & 1u) {
+                const uint32_t bits = st.w[e];
+                const double wa = (double)__uint_as_float(bits & 0x7fffffffu);
+#pragma unroll
+                for (int ff = 0; ff < FPG; ++ff) {
+                    const uint32_t bin = byte8(st.codes[ff], e);
+                    if (ff < a.nf && bin >= (uint32_t)a.nbins) eflag |= kErrBin;
+                    if (ff < a.nf && bin < (uint32_t)a.nbins) {
+                        const size_t gi =
+                            ((((size_t)nl[e] * a.d + a.j0 + ff) * a.nbins + bin) * 2) +
+                            (bits >> 31);
+                        atomicAdd(&a.small[gi], wa);
+                    }
                 }
-                const size_t gi =
-                    ((((size_t)(node - (uint32_t)nodes) * d + j0 + ff) * nbins + bin) * 2) +
-                    (bits >> 31);
-                atomicAdd(&small[gi], (double)a);
             }
         }
     }
 }
 
-template <bool ROUTED, int NP, bool FULLB>
+template <bool ROUTED, int NP, int FPG>
 __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const float *__restrict__ w, const double *__restrict__ cand_gain,
     const int *__restrict__ cand_cut, uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c,
-    double *__restrict__ rec_g, int layer, int fpg, int G, int npg, int NG, int chunks,
+    double *__restrict__ rec_g, int layer, int G, int npg, int NG, int chunks,
     int64_t chunk_events, int scale, uint64_t *__restrict__ partial, double *__restrict__ small,
     int *__restrict__ err) {
     extern __shared__ uint64_t lds[];
@@ -563,15 +582,28 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const int h = r / G;
     const int g = r - h * G;
 
-    const int nodes = 1 << layer;
-    const int half = nodes >> 1;
-    const int hnodes = ROUTED && layer >= 1 ? half : nodes;   // histogrammed nodes
-    const int j0 = g * fpg;
-    const int nf = min(fpg, d - j0);
-    const int k0 = h * npg;
-    const int nk = min(npg, hnodes - k0);
-    const int fstride = FULLB ? 256 : nbins + 1;
-    const int lds_n = npg * fpg * 2 * fstride;
+    HistArgs a;
+    a.xb = xb;
+    a.ldb = ldb;
+    a.n = n;
+    a.d = d;
+    a.nbins = nbins;
+    a.layer = layer;
+    a.nodes = 1 << layer;
+    a.half = a.nodes >> 1;
+    const int hnodes = ROUTED && layer >= 1 ? a.half : a.nodes;   // histogrammed nodes
+    a.j0 = g * FPG;
+    a.nf = min(FPG, d - a.j0);
+    a.k0 = h * npg;
+    a.nk = min(npg, hnodes - a.k0);
+    a.scale = scale;
+    // weights at or above tau = 2^(23 - scale) are exact multiples of 2^-scale
+    a.tau_bits = __float_as_uint(ldexpf(1.0f, 23 - scale));
+    a.node_in = node_in;
+    a.node_out = node_out;
+    a.w = w;
+    a.small = small;
+    const int lds_n = npg * FPG * kRow;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int nwaves = blockDim.x / kWave;
     int eflag = 0;
@@ -585,21 +617,21 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     // node (the cut table of a routed pass) first, then the first step's
     // weights, node ids and codes; the candidates are reduced while the
     // event data arrives, and the step's routing rows follow once the cut
-    // table is in LDS.  (Loads complete in issue order, so the candidates
-    // come first.)
+    // table is in LDS.
     CandRegs cr;
-    const bool pwave = ROUTED && layer >= 1 && wave < half;
+    const bool pwave = ROUTED && layer >= 1 && wave < a.half;
     if (pwave) cand_load(cand_gain, cand_cut, d, wave, lane, cr);
-    HistStep<NP> A, B;
+    HistStep<NP, FPG> A, B;
     int64_t ia = start + (int64_t)kHistE * threadIdx.x;
-    if (ia < end) hist_load<ROUTED, NP>(A, xb, ldb, n, d, j0, nf, node_in, w, s_cf, layer, half, ia, false);
+    if (ia < end) hist_load<ROUTED, NP, FPG>(A, a, s_cf, ia, false);
 
-    for (int t = threadIdx.x; t < lds_n; t += blockDim.x) lds[t] = 0ull;
-    // weights at or above tau are exact multiples of 2^-scale
-    const float tau = ldexpf(1.0f, 23 - scale);
+    {
+        uint4 *l4 = reinterpret_cast<uint4 *>(lds);
+        for (int t = threadIdx.x; t < lds_n / 2; t += blockDim.x) l4[t] = make_uint4(0u, 0u, 0u, 0u);
+    }
     if (ROUTED && layer >= 1) {
         // cut of parent k from its candidates; workgroup 0 records it in the model
-        for (int k = wave; k < half; k += nwaves) {
+        for (int k = wave; k < a.half; k += nwaves) {
             int bf, bc;
             double bg;
             bool ok;
@@ -620,43 +652,47 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         }
     }
     __syncthreads();
+    uint32_t cut[4] = {0u, 0u, 0u, 0u};
+    if (ROUTED && NP > 0 && layer >= 1) {
+#pragma unroll
+        for (int kk = 0; kk < (NP > 0 ? NP : 1); ++kk) cut[kk] = s_cc[kk];
+    }
 
     // two steps in flight: the loads of step s + 1 are issued before the
-    // adds of step s
+    // adds of step s.  They are issued unconditionally (the last step
+    // reloads its own events) so that the waits for step s never cover them.
     if (ia < end) {
-        hist_load_rows<ROUTED, NP>(A, xb, ldb, d, s_cf, layer, ia);
+        hist_load_rows<ROUTED, NP, FPG>(A, a, s_cf, ia);
         for (;;) {
             const int64_t ib = ia + stride;
-            if (ib < end)
-                hist_load<ROUTED, NP>(B, xb, ldb, n, d, j0, nf, node_in, w, s_cf, layer, half, ib, true);
-            hist_add<ROUTED, NP, FULLB>(A, lds, xb, ldb, n, d, nbins, node_out, writer, w, s_cf,
-                                        s_cc, layer, nodes, half, j0, nf, k0, nk, fpg, fstride,
-                                        tau, scale, small, ia, eflag);
-            if (ib >= end) break;
+            const bool more_b = ib < end;
+            hist_load<ROUTED, NP, FPG>(B, a, s_cf, more_b ? ib : ia, true);
+            hist_add<ROUTED, NP, FPG>(A, a, lds, writer, s_cf, s_cc, cut, ia, eflag);
+            if (!more_b) break;
             ia = ib + stride;
-            if (ia < end)
-                hist_load<ROUTED, NP>(A, xb, ldb, n, d, j0, nf, node_in, w, s_cf, layer, half, ia, true);
-            hist_add<ROUTED, NP, FULLB>(B, lds, xb, ldb, n, d, nbins, node_out, writer, w, s_cf,
-                                        s_cc, layer, nodes, half, j0, nf, k0, nk, fpg, fstride,
-                                        tau, scale, small, ib, eflag);
-            if (ia >= end) break;
+            const bool more_a = ia < end;
+            hist_load<ROUTED, NP, FPG>(A, a, s_cf, more_a ? ia : ib, true);
+            hist_add<ROUTED, NP, FPG>(B, a, lds, writer, s_cf, s_cc, cut, ib, eflag);
+            if (!more_a) break;
         }
     }
     __syncthreads();
-    if (!FULLB)   // counters of codes >= n_bins
-        for (int t = threadIdx.x; t < npg * fpg * 2; t += blockDim.x)
-            if (lds[(t >> 1) * 2 * fstride + 2 * nbins + (t & 1)] != 0ull) eflag |= kErrBin;
 
     // partial[p][node][feature][bin][class]: one (node, feature) row per
-    // wavefront step, lanes over bins and classes
-    const int per_nf = nbins * 2;
-    uint64_t *out = partial + (size_t)p * hnodes * d * per_nf;
-    for (int kf = wave; kf < nk * nf; kf += nwaves) {
-        const int k = kf / nf;
-        const int f = kf - k * nf;
-        uint64_t *dst = out + ((size_t)(k0 + k) * d + j0 + f) * per_nf;
-        const uint64_t *src = lds + (k * fpg + f) * 2 * fstride;
-        for (int t = lane; t < per_nf; t += kWave) dst[t] = src[t];
+    // wavefront step, lanes over bins (16 bytes: both classes); bins >=
+    // n_bins must be empty
+    const int nrows = a.nk * a.nf;
+    uint4 *out = reinterpret_cast<uint4 *>(partial + (size_t)p * hnodes * d * nbins * 2);
+    for (int rr = wave; rr < nrows; rr += nwaves) {
+        const int k = rr / a.nf;
+        const int f = rr - k * a.nf;
+        const uint4 *src = reinterpret_cast<const uint4 *>(lds + (k * FPG + f) * kRow);
+        uint4 *dst = out + ((size_t)(a.k0 + k) * d + a.j0 + f) * nbins;
+        for (int t = lane; t < nbins; t += kWave) dst[t] = src[t];
+        for (int t = nbins + lane; t < 256; t += kWave) {
+            const uint4 v = src[t];
+            if (v.x | v.y | v.z | v.w) eflag |= kErrBin;
+        }
     }
     if (eflag) atomicOr(err, eflag);
 }
@@ -1305,19 +1341,22 @@ hipError_t allow_lds(K kernel, size_t max_lds) {
 }  // namespace
 
 // ===========================================================================
+template <int FPG>
+hipError_t allow_hist_lds(size_t max_lds) {
+    const hipError_t e[] = {allow_lds(hist_kernel<false, 0, FPG>, max_lds),
+                            allow_lds(hist_kernel<true, 0, FPG>, max_lds),
+                            allow_lds(hist_kernel<true, 1, FPG>, max_lds),
+                            allow_lds(hist_kernel<true, 2, FPG>, max_lds),
+                            allow_lds(hist_kernel<true, 4, FPG>, max_lds)};
+    for (hipError_t x : e)
+        if (x != hipSuccess) return x;
+    return hipSuccess;
+}
+
 hipError_t prepare_kernels(size_t max_lds) {
-    const hipError_t e[] = {
-        allow_lds(hist_kernel<false, 0, true>, max_lds),
-        allow_lds(hist_kernel<true, 0, true>, max_lds),
-        allow_lds(hist_kernel<true, 1, true>, max_lds),
-        allow_lds(hist_kernel<true, 2, true>, max_lds),
-        allow_lds(hist_kernel<true, 4, true>, max_lds),
-        allow_lds(hist_kernel<false, 0, false>, max_lds),
-        allow_lds(hist_kernel<true, 0, false>, max_lds),
-        allow_lds(hist_kernel<true, 1, false>, max_lds),
-        allow_lds(hist_kernel<true, 2, false>, max_lds),
-        allow_lds(hist_kernel<true, 4, false>, max_lds),
-        allow_lds(apply_kernel, max_lds)};
+    const hipError_t e[] = {allow_hist_lds<1>(max_lds), allow_hist_lds<2>(max_lds),
+                            allow_hist_lds<4>(max_lds), allow_hist_lds<5>(max_lds),
+                            allow_hist_lds<8>(max_lds), allow_lds(apply_kernel, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -1354,14 +1393,19 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
     return hipGetLastError();
 }
 
+bool hist_fpg_supported(int f) {
+    for (int c : kHistFpgSizes)
+        if (c == f) return true;
+    return false;
+}
+
 HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, int cu_count,
                          size_t max_lds, int fpg, int chunks, int threads) {
+    (void)n_bins;
     HistShape hs{};
     const int nodes = sibling && layer >= 1 ? 1 << (layer - 1) : 1 << layer;
-    // LDS row of one (node, feature): 256 bins, or n_bins + 1 with the
-    // out-of-range counter, times two classes
-    const int fstride = n_bins == 256 ? 256 : n_bins + 1;
-    const size_t per_node_feature = (size_t)fstride * 2 * sizeof(uint64_t);
+    // an LDS row of one (node, feature) holds 256 bins x 2 classes
+    const size_t per_node_feature = (size_t)kRowBytes;
     // the kernel's static LDS (cut table) shares the workgroup's LDS limit
     max_lds = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
     int npg = (int)(max_lds / per_node_feature);
@@ -1369,47 +1413,37 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     if (npg > nodes) npg = nodes;
     hs.nodes_per_group = npg;
     hs.node_groups = (nodes + npg - 1) / npg;
-    // Features per workgroup (at most kHistFMax).  A 1024-thread workgroup
-    // fills a CU, so the pass runs as one round of at most cu_count
-    // workgroups: groups * chunks with chunks <= cu_count / groups and at
-    // least one full step (kHistE events) per thread.  Among the
-    // feature-group sizes whose launch fills at least 95% of the most
-    // workgroups any size reaches, take the one with the fewest event
-    // chunks: every chunk writes one more partial histogram that best_cuts
-    // reads back.
+    // Features per workgroup, one of kHistFpgSizes.  A 1024-thread
+    // workgroup fills a CU, so the pass runs as one round of at most
+    // cu_count workgroups: groups * chunks with chunks <= cu_count / groups
+    // and at least one full step (kHistE events) per thread.  Among the
+    // sizes whose launch fills at least 95% of the most workgroups any size
+    // reaches, take the largest: every feature group repeats the per-event
+    // work (weights, routing) of its chunk.
     const int t_threads = threads > 0 ? threads : 1024;
     const int64_t min_events = (int64_t)kHistE * t_threads;
-    const int fmax = d < kHistFMax ? d : kHistFMax;
     int f = 1;
     if (fpg > 0) {
-        f = fpg < fmax ? fpg : fmax;
+        f = fpg;
     } else {
         const int64_t cmax = n / min_events > 0 ? n / min_events : 1;
-        int64_t wgs_of[kHistFMax + 1] = {0}, ch_of[kHistFMax + 1] = {0};
+        int64_t wgs_of[kHistFMax + 1] = {0};
         int64_t most = 0;
-        int last = 0;
-        for (int cand = 1; cand <= fmax; ++cand) {
-            if ((size_t)npg * cand * per_node_feature > max_lds) break;
+        for (int cand : kHistFpgSizes) {
+            if ((size_t)npg * cand * per_node_feature > max_lds) continue;
             const int g = ((d + cand - 1) / cand) * hs.node_groups;
             int64_t c = cu_count / g;
             if (c > cmax) c = cmax;
             if (c < 1) c = 1;
-            ch_of[cand] = c;
             wgs_of[cand] = c * g;
             if (wgs_of[cand] > most) most = wgs_of[cand];
-            last = cand;
         }
-        int64_t best_c = -1;
-        for (int cand = 1; cand <= last; ++cand) {
-            if (wgs_of[cand] * 100 < most * 95) continue;
-            if (best_c < 0 || ch_of[cand] < best_c ||
-                (ch_of[cand] == best_c && wgs_of[cand] > wgs_of[f])) {
-                best_c = ch_of[cand];
-                f = cand;
-            }
-        }
+        for (int cand : kHistFpgSizes)
+            if (wgs_of[cand] > 0 && wgs_of[cand] * 100 >= most * 95 && cand <= d) f = cand;
     }
-    while (f > 1 && (size_t)npg * f * per_node_feature > max_lds) --f;
+    while (npg > 1 && (size_t)npg * f * per_node_feature > max_lds) --npg;
+    hs.nodes_per_group = npg;
+    hs.node_groups = (nodes + npg - 1) / npg;
     hs.features_per_group = f;
     hs.feature_groups = (d + f - 1) / f;
     hs.threads = t_threads;
@@ -1442,16 +1476,40 @@ int histogram_scale(double total_weight_bound) {
     return sc;
 }
 
-template <bool ROUTED, int NP, bool FULLB>
+template <bool ROUTED, int NP, int FPG>
 hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
                           const ParentCuts &pc, int layer, int scale, uint64_t *partial,
                           double *small, int *err, hipStream_t s) {
-    hist_kernel<ROUTED, NP, FULLB><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+    hist_kernel<ROUTED, NP, FPG><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.rec_f,
-        pc.rec_c, pc.rec_g, layer, hs.features_per_group, hs.feature_groups, hs.nodes_per_group,
-        hs.node_groups, hs.chunks, hs.chunk_events, scale, partial, small, err);
+        pc.rec_c, pc.rec_g, layer, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
+        hs.chunks, hs.chunk_events, scale, partial, small, err);
     return hipGetLastError();
+}
+
+template <int FPG>
+hipError_t launch_hist_fpg(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
+                           int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
+                           const float *w, const ParentCuts &pc, int layer, bool routed,
+                           int scale, uint64_t *partial, double *small, int *err,
+                           hipStream_t s) {
+    const ParentCuts none{};
+    if (!routed)
+        return launch_hist_np<false, 0, FPG>(hs, xb, ldb, n, d, n_bins, node_in, nullptr, w, none,
+                                             layer, scale, partial, small, err, s);
+    const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
+#define FBDT_HIST(NPV)                                                                          \
+    launch_hist_np<true, NPV, FPG>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, pc, layer,   \
+                                   scale, partial, small, err, s)
+    switch (parents) {
+    case 0:
+    case 1: return FBDT_HIST(1);
+    case 2: return FBDT_HIST(2);
+    case 4: return FBDT_HIST(4);
+    default: return FBDT_HIST(0);
+    }
+#undef FBDT_HIST
 }
 
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
@@ -1459,23 +1517,18 @@ hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb,
                             const float *w, const ParentCuts &pc, int layer, bool routed,
                             int scale, uint64_t *partial, double *small, int *err,
                             hipStream_t s) {
-    const ParentCuts none{};
-    if (hs.features_per_group < 1 || hs.features_per_group > kHistFMax) return hipErrorInvalidValue;
-#define FBDT_HIST(R, NPV, FB)                                                                    \
-    launch_hist_np<R, NPV, FB>(hs, xb, ldb, n, d, n_bins, node_in, R ? node_out : nullptr, w,   \
-                               R ? pc : none, layer, scale, partial, small, err, s)
-#define FBDT_HIST_B(R, NPV) (n_bins == 256 ? FBDT_HIST(R, NPV, true) : FBDT_HIST(R, NPV, false))
-    if (!routed) return FBDT_HIST_B(false, 0);
-    const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
-    switch (parents) {
-    case 0:
-    case 1: return FBDT_HIST_B(true, 1);
-    case 2: return FBDT_HIST_B(true, 2);
-    case 4: return FBDT_HIST_B(true, 4);
-    default: return FBDT_HIST_B(true, 0);
+#define FBDT_HIST_F(F)                                                                          \
+    launch_hist_fpg<F>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, pc, layer, routed,      \
+                       scale, partial, small, err, s)
+    switch (hs.features_per_group) {
+    case 1: return FBDT_HIST_F(1);
+    case 2: return FBDT_HIST_F(2);
+    case 4: return FBDT_HIST_F(4);
+    case 5: return FBDT_HIST_F(5);
+    case 8: return FBDT_HIST_F(8);
+    default: return hipErrorInvalidValue;
     }
-#undef FBDT_HIST_B
-#undef FBDT_HIST
+#undef FBDT_HIST_F
 }
 
 hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t count, int scale,

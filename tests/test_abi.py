@@ -51,3 +51,7 @@ def test_argument_errors_need_no_device():
     assert L.fbdt_set_option(b"no_such_option", 1) == -1
     assert L.fbdt_set_option(b"hist_threads", 100) == -1
     assert L.fbdt_set_option(b"hist_threads", 0) == 0
+    # the histogram kernels are built for 1, 2, 4, 5 or 8 features per workgroup
+    assert L.fbdt_set_option(b"hist_features_per_group", 3) == -1
+    assert L.fbdt_set_option(b"hist_features_per_group", 5) == 0
+    assert L.fbdt_set_option(b"hist_features_per_group", 0) == 0

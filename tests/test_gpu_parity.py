@@ -180,7 +180,7 @@ def test_histogram_feature_groups_and_threads():
     ws = np.where(y > 0, wa, -wa).astype(np.float32)
     ref = O.histogram(xb, node.astype(np.int64), wa, y > 0, layer, B)
     codes = fb.Codes.from_numpy(xb)
-    for fpg, threads in ((2, 256), (3, 512), (5, 1024), (11, 128)):
+    for fpg, threads in ((2, 256), (4, 512), (5, 1024), (8, 128), (1, 64)):
         fb.set_option("hist_features_per_group", fpg)
         fb.set_option("hist_threads", threads)
         say(f"histogram fpg={fpg} threads={threads}")
