@@ -467,10 +467,14 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     const size_t hfull_elems = D >= 2 ? ((size_t)1 << (D - 2)) * d * n_bins * 2 : 1;
     cv.add(&fb.hfull[0], hfull_elems);
     cv.add(&fb.hfull[1], hfull_elems);
+    // side histograms of the weights below the fixed-point grid, by the
+    // parity of the layer's index in the whole fit (tree * D + layer)
     const size_t small_elems = (size_t)max_nodes * d * n_bins * 2;
-    cv.add(&fb.small, small_elems);
-    cv.add(&fb.cand_gain, (size_t)max_nodes * d);
-    cv.add(&fb.cand_cut, (size_t)max_nodes * d);
+    cv.add(&fb.small[0], small_elems);
+    cv.add(&fb.small[1], small_elems);
+    const int S = cut_slices(n_bins);
+    cv.add(&fb.cand_gain, (size_t)max_nodes * d * S);
+    cv.add(&fb.cand_cut, (size_t)max_nodes * d * S);
     cv.add(&fb.leaf_partial, (size_t)lblocks * 2 * nleaf);
     cv.add(&fb.class_partial, 2 * kValidateBlocks);
     cv.add(&fb.f0, 2);
@@ -483,7 +487,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.assign(a.ptr);
 
     HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
-    HIP_TRY(launch_fill_u32(fb.small, 0u, 2 * small_elems, s));
+    HIP_TRY(launch_fill_u32(fb.small[0], 0u, 2 * small_elems, s));
+    HIP_TRY(launch_fill_u32(fb.small[1], 0u, 2 * small_elems, s));
     // the histogram passes read whole steps of events: padded events weigh 0
     HIP_TRY(launch_fill_u32(fb.w, 0u, (size_t)npad, s));
     HIP_TRY(launch_validate(y, w, n, fb.class_partial, fb.err, s));
@@ -525,28 +530,36 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 // with; workgroup 0 records them in the model
                 const int plo = l >= 1 ? (1 << (l - 1)) - 1 : 0;
                 ParentCuts pc;
-                if (l >= 1) pc = ParentCuts{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
+                if (l >= 1)
+                    pc = ParentCuts{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
+                const int gl = t * D + l;   // side histograms alternate by gl's parity
                 {
                     Timed tm(FBDT_K_HISTOGRAM, st, hist_algorithmic_bytes(n, d, n_bins, l, true));
                     HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
                                              l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
                                              l >= 1 ? fb.node[l & 1] : nullptr, fb.w, pc, l, true,
-                                             scale, fb.partial, fb.small, fb.err, st));
+                                             scale, fb.partial, fb.small[gl & 1], fb.err, st));
                     tm.done();
                 }
                 {
                     Timed tm(FBDT_K_BEST_CUTS, st);
-                    // right children below the root: parent - left child
-                    HIP_TRY(launch_best_cuts(fb.partial, plans[l].chunks, scale, fb.small, nullptr,
-                                             l >= 1 ? 1 << (l - 1) : 1, d, n_bins, fb.cand_gain,
-                                             fb.cand_cut, l >= 1 ? fb.hfull[(l - 1) & 1] : nullptr,
-                                             l + 1 < D ? fb.hfull[l & 1] : nullptr, st));
+                    // right children below the root: parent - left child; the
+                    // next layer's side histogram (next tree's root after the
+                    // last layer) is cleared on the way
+                    const size_t next_count =
+                        (size_t)(l + 1 < D ? 1 << (l + 1) : 1) * d * n_bins * 2;
+                    HIP_TRY(launch_cut_scan(fb.partial, plans[l].chunks, scale, fb.small[gl & 1],
+                                            fb.small[(gl + 1) & 1], next_count,
+                                            l >= 1 ? 1 << (l - 1) : 1, d, n_bins, l >= 1,
+                                            fb.cand_gain, fb.cand_cut,
+                                            l >= 1 ? fb.hfull[(l - 1) & 1] : nullptr,
+                                            l + 1 < D ? fb.hfull[l & 1] : nullptr, st));
                     tm.done();
                 }
             }
             {
                 const int plo = (1 << (D - 1)) - 1;
-                const ParentCuts pc{fb.cand_gain, fb.cand_cut, cf + plo, cc + plo, cg + plo};
+                const ParentCuts pc{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
                 Timed tm(FBDT_K_LEAF, st);
                 HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
                                     fb.node[D & 1], pc, D, true, y, w, fb.F, seed, t, alpha, lblocks,
@@ -863,9 +876,8 @@ int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bin
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     Timed tm(FBDT_K_BEST_CUTS, s);
-    HIP_TRY(launch_best_cuts(nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cg, cc, nullptr,
-                             nullptr, s));
-    HIP_TRY(launch_select_cuts(cg, cc, n_nodes, d, cut_feature, cut_bin, gain, s));
+    HIP_TRY(launch_best_cuts_f64(hist, n_nodes, d, n_bins, cg, cc, s));
+    HIP_TRY(launch_select_cuts(cg, cc, n_nodes, d, 1, cut_feature, cut_bin, gain, s));
     tm.done();
     HIP_TRY(hipStreamSynchronize(s));
     return FBDT_OK;

@@ -40,9 +40,10 @@ struct FitBuffers {
     uint64_t *partial;    // fixed-point histogram partials [chunks][histogrammed nodes][d][B][2]
     uint64_t *hfull[2];   // summed fixed-point histograms of every node of a layer
                           // [nodes][d][B][2], by layer parity (the next layer's parents)
-    double *small;        // float64 histogram of the weights below the fixed-point grid
-    double *cand_gain;    // [max nodes][d] best gain of every (node, feature)
-    int *cand_cut;        // [max nodes][d] and its bin
+    double *small[2];     // float64 histograms of the weights below the fixed-point grid,
+                          // [nodes][d][B][2], by the parity of tree * D + layer
+    double *cand_gain;    // [max nodes][d * slices] best gain of every (node, feature, slice)
+    int *cand_cut;        // [max nodes][d * slices] and its bin
     double *leaf_partial;   // [leaf blocks][2^D][2]
     double *class_partial;  // [validate blocks][2]
     double *f0;             // [2]: initial score, total event weight
@@ -102,8 +103,9 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
 // routed pass takes each parent's cut (best gain, then lowest feature);
 // rec_* (optional) receive those cuts for the model (written by workgroup 0).
 struct ParentCuts {
-    const double *cand_gain = nullptr;
+    const double *cand_gain = nullptr;   // [nodes][d * slices]
     const int *cand_cut = nullptr;
+    int slices = 1;
     uint8_t *rec_f = nullptr;
     uint8_t *rec_c = nullptr;
     double *rec_g = nullptr;
@@ -144,23 +146,33 @@ hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t cou
 hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, double *out,
                           hipStream_t s);
 
-// Best cut of every (node, feature) of a layer into cand_gain/cand_cut, from
-// fixed-point chunk partials plus the float64 side histogram (which it
-// clears), or, with partial == null, from a float64 histogram `hist`.
-// n_nodes: histogrammed nodes (one workgroup per node and feature).  With
-// hparent != null (fixed-point path, layer >= 1) the partials are the left
-// children of n_nodes parents and hparent [n_nodes][d][B][2] their summed
-// histograms: the right child is parent - left, exactly, and both children
-// get candidates (layer index 2k, 2k + 1 for parent k).  hout (optional)
-// receives the summed fixed-point histogram of every node of the layer.
-hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
-                            const double *hist, int n_nodes, int d, int n_bins,
-                            double *cand_gain, int *cand_cut, const uint64_t *hparent,
-                            uint64_t *hout, hipStream_t s);
+// Slices of the candidate cuts of one (node, feature) row: ceil((B-1)/31).
+int cut_slices(int n_bins);
 
-// Best cut of each node over its features.
+// Best cut of every (node, feature) of a float64 histogram hist
+// [n_nodes][d][B][2] into cand_gain/cand_cut [n_nodes][d] (one slice per
+// feature).
+hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bins,
+                                double *cand_gain, int *cand_cut, hipStream_t s);
+
+// Best cuts of a layer in the fit from the prefix-summed fixed-point chunk
+// partials of the routed histogram pass (hnodes histogrammed nodes, chunks
+// partials) plus the float64 side histogram `small` of the layer, into
+// cand_gain/cand_cut [layer nodes][d * cut_slices(B)].  sibling (layers
+// below the root): the partials are the left children of hnodes parents and
+// hparent [hnodes][d][B][2] their summed prefix rows; the right child is
+// parent - left.  hout (optional) receives the summed prefix rows of every
+// node of the layer.  Clears small_next[0, small_next_count) (the next
+// layer's side histogram).
+hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
+                           double *small_next, size_t small_next_count, int hnodes, int d,
+                           int n_bins, bool sibling, double *cand_gain, int *cand_cut,
+                           const uint64_t *hparent, uint64_t *hout, hipStream_t s);
+
+// Best cut of each node over its candidates (d features x slices entries).
 hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,
-                              uint8_t *out_f, uint8_t *out_c, double *out_g, hipStream_t s);
+                              int slices, uint8_t *out_f, uint8_t *out_c, double *out_g,
+                              hipStream_t s);
 
 // Last routing (routed = true, from layer depth-1 to the leaves with the
 // cuts from pc) or none (node_in already holds leaf ids), then the per-block

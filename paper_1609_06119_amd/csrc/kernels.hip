@@ -26,7 +26,6 @@ namespace fbdt {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kBcWaves = 16;   // wavefronts per (node, feature) in best_cuts
 constexpr int kHistE = 8;      // events per thread and step of the histogram pass
 
 // SplitMix64 (Steele, Lea & Flood, OOPSLA 2014): output number k (0-based)
@@ -270,25 +269,36 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Best candidate of one node over its features (gain highest, then lowest
-// feature), by one wavefront; lane 0 returns it.  An unusable result
-// (no finite gain) falls back to feature 0 and reports it.  Split into the
-// loads (lane l holds features l, l + 64, ... < 256) and the reduction, so
-// that a kernel can issue the loads early.
-struct CandRegs {
-    double g[4];
-    int c[4];
+// Candidate cuts of a layer: entry e = j * S + q of node k holds the best cut
+// (gain, bin) of feature j among the bins of slice q (S slices per feature,
+// bins rising with q), so that the entry order is the (feature, bin) order.
+// The best candidate of a node (gain highest, then lowest entry: lowest
+// feature, then lowest bin) is found by one wavefront; lane 0 returns it.  An
+// unusable result (no finite gain) falls back to feature 0 and reports it.
+// Split into the loads of the first kCandRegs * 64 entries and the
+// reduction, so that a kernel can issue the loads early.
+struct CandSet {
+    const double *gain;   // [nodes][E]
+    const int *cut;       // [nodes][E]
+    int d;                // features
+    int S;                // slices per feature; E = d * S entries per node
 };
 
-__device__ __forceinline__ void cand_load(const double *__restrict__ cand_gain,
-                                          const int *__restrict__ cand_cut, int d, int k, int lane,
-                                          CandRegs &r) {
+constexpr int kCandRegs = 8;
+
+struct CandRegs {
+    double g[kCandRegs];
+    int c[kCandRegs];
+};
+
+__device__ __forceinline__ void cand_load(const CandSet &cs, int k, int lane, CandRegs &r) {
+    const int E = cs.d * cs.S;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int jj = lane + kWave * q;
-        if (jj < d) {
-            r.g[q] = cand_gain[(size_t)k * d + jj];
-            r.c[q] = cand_cut[(size_t)k * d + jj];
+    for (int q = 0; q < kCandRegs; ++q) {
+        const int e = lane + kWave * q;
+        if (e < E) {
+            r.g[q] = cs.gain[(size_t)k * E + e];
+            r.c[q] = cs.cut[(size_t)k * E + e];
         } else {
             r.g[q] = -INFINITY;
             r.c[q] = 1;
@@ -296,55 +306,64 @@ __device__ __forceinline__ void cand_load(const double *__restrict__ cand_gain,
     }
 }
 
-__device__ __forceinline__ void cand_reduce(const CandRegs &r, int d, int lane, int *bf, int *bc,
-                                            double *bg, bool *ok) {
+__device__ __forceinline__ void cand_reduce(const CandRegs &r, const CandSet &cs, int k, int lane,
+                                            int *bf, int *bc, double *bg, bool *ok) {
+    const int E = cs.d * cs.S;
     double g = -INFINITY;
-    int j = 0x7fffffff, c = 1;
+    int idx = 0x7fffffff, c = 1;
+    // each lane visits its entries in rising order: a strict > keeps the lowest
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int jj = lane + kWave * q;
-        if (jj < d && r.g[q] > g) {
+    for (int q = 0; q < kCandRegs; ++q) {
+        const int e = lane + kWave * q;
+        if (e < E && r.g[q] > g) {
             g = r.g[q];
-            j = jj;
+            idx = e;
             c = r.c[q];
+        }
+    }
+    for (int e = lane + kWave * kCandRegs; e < E; e += kWave) {
+        const double x = cs.gain[(size_t)k * E + e];
+        if (x > g) {
+            g = x;
+            idx = e;
+            c = cs.cut[(size_t)k * E + e];
         }
     }
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) {
         const double og = __shfl_xor(g, off);
-        const int oj = __shfl_xor(j, off);
+        const int oi = __shfl_xor(idx, off);
         const int oc = __shfl_xor(c, off);
-        if (og > g || (og == g && oj < j)) {
+        if (og > g || (og == g && oi < idx)) {
             g = og;
-            j = oj;
+            idx = oi;
             c = oc;
         }
     }
-    *ok = j < d && c >= 1 && c <= 255;
+    const int j = idx < E ? idx / cs.S : cs.d;
+    *ok = j < cs.d && c >= 1 && c <= 255;
     *bf = *ok ? j : 0;
     *bc = *ok ? c : 1;
     *bg = g;
 }
 
-__device__ __forceinline__ void node_best(const double *__restrict__ cand_gain,
-                                          const int *__restrict__ cand_cut, int d, int k,
-                                          int lane, int *bf, int *bc, double *bg, bool *ok) {
+__device__ __forceinline__ void node_best(const CandSet &cs, int k, int lane, int *bf, int *bc,
+                                          double *bg, bool *ok) {
     CandRegs r;
-    cand_load(cand_gain, cand_cut, d, k, lane, r);
-    cand_reduce(r, d, lane, bf, bc, bg, ok);
+    cand_load(cs, k, lane, r);
+    cand_reduce(r, cs, k, lane, bf, bc, bg, ok);
 }
-
 
 // Cuts of n_nodes nodes from their candidates (one wavefront per node).
 __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restrict__ cand_gain,
                                                          const int *__restrict__ cand_cut, int d,
-                                                         uint8_t *__restrict__ out_f,
+                                                         int S, uint8_t *__restrict__ out_f,
                                                          uint8_t *__restrict__ out_c,
                                                          double *__restrict__ out_g) {
     int bf, bc;
     double bg;
     bool ok;
-    node_best(cand_gain, cand_cut, d, blockIdx.x, threadIdx.x, &bf, &bc, &bg, &ok);
+    node_best(CandSet{cand_gain, cand_cut, d, S}, blockIdx.x, threadIdx.x, &bf, &bc, &bg, &ok);
     if (threadIdx.x == 0) {
         out_f[blockIdx.x] = (uint8_t)bf;
         out_c[blockIdx.x] = (uint8_t)bc;
@@ -380,6 +399,29 @@ __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restric
 // reported as an error.  The last feature group may run past feature d - 1:
 // its missing features load the codes of feature d - 1 and add them into
 // rows that are never written out, so the inner loop has no feature test.
+// Inclusive prefix sum of a 64-bit value over the 64 lanes of a wavefront
+// with DPP lane moves (no LDS round trip): a Hillis-Steele scan within each
+// row of 16 lanes (row_shr 1, 2, 4, 8), then the last lane of row 0 and 2
+// added to rows 1 and 3 (row_bcast 15) and the last lane of row 1 to rows 2
+// and 3 (row_bcast 31).  Lanes that a move does not reach receive 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long x) {
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, ROW_MASK, 0xf, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, ROW_MASK, 0xf,
+                                               true);
+    return ((unsigned long long)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ unsigned long long wave_inclusive_scan_u64(unsigned long long x) {
+    x += dpp_u64<0x111, 0xf>(x);   // row_shr:1
+    x += dpp_u64<0x112, 0xf>(x);   // row_shr:2
+    x += dpp_u64<0x114, 0xf>(x);   // row_shr:4
+    x += dpp_u64<0x118, 0xf>(x);   // row_shr:8
+    x += dpp_u64<0x142, 0xa>(x);   // row_bcast:15 into rows 1, 3
+    x += dpp_u64<0x143, 0xc>(x);   // row_bcast:31 into rows 2, 3
+    return x;
+}
+
 constexpr int kRow = 256 * 2;                        // counters per LDS row
 constexpr int kRowBytes = kRow * (int)sizeof(uint64_t);
 
@@ -563,10 +605,10 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const float *__restrict__ w, const double *__restrict__ cand_gain,
-    const int *__restrict__ cand_cut, uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c,
-    double *__restrict__ rec_g, int layer, int G, int npg, int NG, int chunks,
-    int64_t chunk_events, int scale, uint64_t *__restrict__ partial, double *__restrict__ small,
-    int *__restrict__ err) {
+    const int *__restrict__ cand_cut, int cslices, uint8_t *__restrict__ rec_f,
+    uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, int G, int npg, int NG,
+    int chunks, int64_t chunk_events, int scale, uint64_t *__restrict__ partial,
+    double *__restrict__ small, int *__restrict__ err) {
     extern __shared__ uint64_t lds[];
     __shared__ uint8_t s_cf[64], s_cc[64];
 
@@ -619,8 +661,9 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     // event data arrives, and the step's routing rows follow once the cut
     // table is in LDS.
     CandRegs cr;
+    const CandSet cs{cand_gain, cand_cut, d, cslices};
     const bool pwave = ROUTED && layer >= 1 && wave < a.half;
-    if (pwave) cand_load(cand_gain, cand_cut, d, wave, lane, cr);
+    if (pwave) cand_load(cs, wave, lane, cr);
     HistStep<NP, FPG> A, B;
     int64_t ia = start + (int64_t)kHistE * threadIdx.x;
     if (ia < end) hist_load<ROUTED, NP, FPG>(A, a, s_cf, ia, false);
@@ -636,9 +679,9 @@ __global__ __launch_bounds__(1024) void hist_kernel(
             double bg;
             bool ok;
             if (k == wave)
-                cand_reduce(cr, d, lane, &bf, &bc, &bg, &ok);
+                cand_reduce(cr, cs, k, lane, &bf, &bc, &bg, &ok);
             else
-                node_best(cand_gain, cand_cut, d, k, lane, &bf, &bc, &bg, &ok);
+                node_best(cs, k, lane, &bf, &bc, &bg, &ok);
             if (lane == 0) {
                 s_cf[k] = (uint8_t)bf;
                 s_cc[k] = (uint8_t)bc;
@@ -679,8 +722,12 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     __syncthreads();
 
     // partial[p][node][feature][bin][class]: one (node, feature) row per
-    // wavefront step, lanes over bins (16 bytes: both classes); bins >=
-    // n_bins must be empty
+    // wavefront step; bins >= n_bins must be empty.  Routed (fit) passes
+    // write every row as inclusive prefix sums over bins, P(b) = sum of the
+    // bins <= b per class: summed over chunks these are the cumulative
+    // histograms, which best_cuts then reads slice by slice.  Lane l holds
+    // bins 4l..4l+3 (both classes), prefix in the lane, then an exclusive
+    // scan of the lane totals across the wavefront.
     const int nrows = a.nk * a.nf;
     uint4 *out = reinterpret_cast<uint4 *>(partial + (size_t)p * hnodes * d * nbins * 2);
     for (int rr = wave; rr < nrows; rr += nwaves) {
@@ -688,11 +735,24 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         const int f = rr - k * a.nf;
         const uint4 *src = reinterpret_cast<const uint4 *>(lds + (k * FPG + f) * kRow);
         uint4 *dst = out + ((size_t)(a.k0 + k) * d + a.j0 + f) * nbins;
-        for (int t = lane; t < nbins; t += kWave) dst[t] = src[t];
         for (int t = nbins + lane; t < 256; t += kWave) {
             const uint4 v = src[t];
             if (v.x | v.y | v.z | v.w) eflag |= kErrBin;
         }
+        if (ROUTED) {   // the row is scanned in place (this wavefront's row only)
+            ulonglong2 *s2 = reinterpret_cast<ulonglong2 *>(lds + (k * FPG + f) * kRow) + 4 * lane;
+            ulonglong2 v[4] = {s2[0], s2[1], s2[2], s2[3]};
+#pragma unroll
+            for (int e = 1; e < 4; ++e) {
+                v[e].x += v[e - 1].x;
+                v[e].y += v[e - 1].y;
+            }
+            const unsigned long long xs = wave_inclusive_scan_u64(v[3].x) - v[3].x;   // exclusive
+            const unsigned long long xb = wave_inclusive_scan_u64(v[3].y) - v[3].y;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) s2[e] = make_ulonglong2(v[e].x + xs, v[e].y + xb);
+        }
+        for (int t = lane; t < nbins; t += kWave) dst[t] = src[t];
     }
     if (eflag) atomicOr(err, eflag);
 }
@@ -740,155 +800,32 @@ __global__ void sum_blocks_kernel(const double *__restrict__ block_partial, int 
 }
 
 // ---------------------------------------------------------------------------
-// Best cut of every node of a layer.  One wavefront per (node, feature):
-// lane l owns bins 4l..4l+3, sums the chunk partials, builds the cumulative
-// histograms with an in-lane prefix plus a wavefront scan, evaluates the
-// separation gain of each candidate cut and reduces to the best (gain
-// highest, then lowest bin).  The reduction of a node's candidates
-// over features (gain highest, then lowest feature) is left to the next
-// pass (its prologue) or to select_cuts_kernel.
+// Best cut of every (node, feature) of a float64 histogram (the standalone
+// step): one wavefront per (node, feature); lane l owns bins 4l..4l+3, builds
+// the cumulative histograms with an in-lane prefix plus a wavefront scan,
+// evaluates the separation gain of each candidate cut and reduces to the best
+// (gain highest, then lowest bin) as entry [node][feature] of a candidate set
+// with one slice per feature.
 //
 // Exactness rules shared with the plain definition: a cut whose left or
 // right side holds no event has gain exactly 0 (as the definition gives
 // with exact zero sums); a cut c >= 2 whose bin c-1 is empty makes the same
 // partition as cut c-1, has the same gain in exact arithmetic, and is
 // skipped so that the lower cut wins the tie independently of rounding.
-template <bool FIXED>
-__global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
-    const uint64_t *__restrict__ partial, int chunks, int scale, double *__restrict__ small,
-    const double *__restrict__ hist, int nodes, int d, int nbins,
-    double *__restrict__ cand_gain, int *__restrict__ cand_cut,
-    const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout) {
+__global__ __launch_bounds__(kWave) void best_cuts_f64_kernel(const double *__restrict__ hist,
+                                                              int d, int nbins,
+                                                              double *__restrict__ cand_gain,
+                                                              int *__restrict__ cand_cut) {
 #pragma clang fp contract(off)
-    // one workgroup of kBcWaves wavefronts per (histogrammed node, feature);
-    // wavefront w sums the fixed-point chunk partials w, w + kBcWaves, ...
-    // (integer sums: exact in any order), so that all chunk loads are in
-    // flight together; wavefront 0 (and, for a left child, wavefront 1 with
-    // the right child = parent - left) converts the sums to float64 and adds
-    // the side histogram of weights below the grid
-    __shared__ uint64_t red[kBcWaves][8][kWave];   // lane fastest: no bank conflicts
-    __shared__ double side[2][8][kWave];
-    const int lane = threadIdx.x % kWave;
-    const int wave = threadIdx.x / kWave;
-    const int pair = blockIdx.x;
-    const int k = pair / d;
-    const int j = pair - k * d;
+    const int lane = threadIdx.x;
+    const int pair = blockIdx.x;   // node * d + feature
     const int b0 = 4 * lane;
     const int nb = b0 < nbins ? min(4, nbins - b0) : 0;
-    const size_t row = (size_t)nbins * 2;
-    const size_t off = ((size_t)k * d + j) * row + 2 * b0;   // histogrammed node k
-    const bool sib = FIXED && hparent != nullptr;
-    // node of this wavefront's candidate, as an index within the layer
-    const int node = sib ? 2 * k + (wave & 1) : k;
-    const size_t noff = ((size_t)node * d + j) * row + 2 * b0;
-
+    const size_t off = (size_t)pair * nbins * 2 + 2 * b0;
     double hs[4] = {0.0, 0.0, 0.0, 0.0}, hb[4] = {0.0, 0.0, 0.0, 0.0};
-    if (FIXED) {
-        uint64_t ps[4] = {0, 0, 0, 0}, pb[4] = {0, 0, 0, 0};
-        if (sib && wave == 1)   // the parent's summed histogram, for the right child
-            for (int e = 0; e < nb; ++e) {
-                ps[e] = hparent[off + 2 * e];
-                pb[e] = hparent[off + 2 * e + 1];
-            }
-        uint64_t us[4] = {0, 0, 0, 0}, ub[4] = {0, 0, 0, 0};
-        const size_t stride_p = (size_t)nodes * d * row;
-        if (nb == 4) {
-            int p = wave;
-            for (; p + kBcWaves < chunks; p += 2 * kBcWaves) {   // two chunks in flight
-                const ulonglong2 *s0 =
-                    reinterpret_cast<const ulonglong2 *>(partial + (size_t)p * stride_p + off);
-                const ulonglong2 *s1 = reinterpret_cast<const ulonglong2 *>(
-                    partial + (size_t)(p + kBcWaves) * stride_p + off);
-                const ulonglong2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
-                const ulonglong2 c0 = s1[0], c1 = s1[1], c2 = s1[2], c3 = s1[3];
-                us[0] += a0.x + c0.x; ub[0] += a0.y + c0.y; us[1] += a1.x + c1.x; ub[1] += a1.y + c1.y;
-                us[2] += a2.x + c2.x; ub[2] += a2.y + c2.y; us[3] += a3.x + c3.x; ub[3] += a3.y + c3.y;
-            }
-            if (p < chunks) {
-                const ulonglong2 *s0 =
-                    reinterpret_cast<const ulonglong2 *>(partial + (size_t)p * stride_p + off);
-                const ulonglong2 a0 = s0[0], a1 = s0[1], a2 = s0[2], a3 = s0[3];
-                us[0] += a0.x; ub[0] += a0.y; us[1] += a1.x; ub[1] += a1.y;
-                us[2] += a2.x; ub[2] += a2.y; us[3] += a3.x; ub[3] += a3.y;
-            }
-        } else if (nb > 0) {
-            for (int p = wave; p < chunks; p += kBcWaves) {
-                const uint64_t *src = partial + (size_t)p * stride_p + off;
-                for (int e = 0; e < nb; ++e) {
-                    us[e] += src[2 * e];
-                    ub[e] += src[2 * e + 1];
-                }
-            }
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            red[wave][e][lane] = us[e];
-            red[wave][4 + e][lane] = ub[e];
-        }
-        if (wave >= kBcWaves - 2 && (sib || wave == kBcWaves - 1)) {
-            // side histograms of weights below the grid: the last wavefront
-            // loads the left (or only) node's, the one before it the right's
-            const int c = sib ? wave - (kBcWaves - 2) : 0;
-            const size_t so = ((size_t)(sib ? 2 * k + c : k) * d + j) * row + 2 * b0;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                side[c][e][lane] = e < nb ? small[so + 2 * e] : 0.0;
-                side[c][4 + e][lane] = e < nb ? small[so + 2 * e + 1] : 0.0;
-            }
-        }
-        __syncthreads();
-        // the wavefront sums: value (e, l) over wavefronts [h kBcWaves / 2,
-        // (h + 1) kBcWaves / 2) by thread 512 h + 64 e + l, all reads in flight
-        // together; the candidate wavefronts add the two halves
-        {
-            const int vi = threadIdx.x % (8 * kWave), hh = threadIdx.x / (8 * kWave);
-            const int e = vi / kWave, l = vi % kWave;
-            uint64_t t = 0;
-            if (hh < 2) {
-#pragma unroll
-                for (int wv = 0; wv < kBcWaves / 2; ++wv) t += red[hh * (kBcWaves / 2) + wv][e][l];
-            }
-            __syncthreads();
-            if (hh < 2) red[hh][e][l] = t;
-            __syncthreads();
-        }
-        if (wave >= (sib ? 2 : 1)) return;
-        uint64_t ts[4], tb[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            ts[e] = red[0][e][lane] + red[1][e][lane];
-            tb[e] = red[0][4 + e][lane] + red[1][4 + e][lane];
-        }
-        if (sib && wave == 1) {   // right child = parent - left child (exact)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                ts[e] = ps[e] - ts[e];
-                tb[e] = pb[e] - tb[e];
-            }
-        }
-        if (hout)
-            for (int e = 0; e < nb; ++e) {
-                hout[noff + 2 * e] = ts[e];
-                hout[noff + 2 * e + 1] = tb[e];
-            }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            hs[e] = ldexp((double)ts[e], -scale);
-            hb[e] = ldexp((double)tb[e], -scale);
-        }
-        const int c = sib ? wave : 0;
-        for (int e = 0; e < nb; ++e) {   // side histogram, cleared for the next layer
-            hs[e] += side[c][e][lane];
-            hb[e] += side[c][4 + e][lane];
-            small[noff + 2 * e] = 0.0;
-            small[noff + 2 * e + 1] = 0.0;
-        }
-    } else {
-        if (wave != 0) return;
-        for (int e = 0; e < nb; ++e) {
-            hs[e] = hist[off + 2 * e];
-            hb[e] = hist[off + 2 * e + 1];
-        }
+    for (int e = 0; e < nb; ++e) {
+        hs[e] = hist[off + 2 * e];
+        hb[e] = hist[off + 2 * e + 1];
     }
     bool ne[4];
     int first = 0x7fffffff, last = -1;
@@ -900,8 +837,7 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
             last = max(last, b0 + e);
         }
     }
-    // in-lane inclusive prefix
-    double ps[4], pb[4];
+    double ps[4], pb[4];   // in-lane inclusive prefix
     ps[0] = hs[0];
     pb[0] = hb[0];
 #pragma unroll
@@ -909,13 +845,12 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
         ps[e] = ps[e - 1] + hs[e];
         pb[e] = pb[e - 1] + hb[e];
     }
-    // wavefront inclusive scan of the lane totals
-    double is = ps[3], ib = pb[3];
+    double is = ps[3], ib = pb[3];   // wavefront inclusive scan of the lane totals
 #pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const double us = __shfl_up(is, off);
-        const double ub = __shfl_up(ib, off);
-        if (lane >= off) {
+    for (int o = 1; o < kWave; o <<= 1) {
+        const double us = __shfl_up(is, o);
+        const double ub = __shfl_up(ib, o);
+        if (lane >= o) {
             is += us;
             ib += ub;
         }
@@ -928,13 +863,12 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
     const double ST = __shfl(is, kWave - 1);
     const double BT = __shfl(ib, kWave - 1);
 #pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        first = min(first, __shfl_xor(first, off));
-        last = max(last, __shfl_xor(last, off));
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        first = min(first, __shfl_xor(first, o));
+        last = max(last, __shfl_xor(last, o));
     }
     const bool prev_ne = __shfl_up(ne[3] ? 1 : 0, 1) != 0;
     const double gp = gini(ST, BT);
-
     double best = -INFINITY;
     int bestc = 0x7fffffff;
 #pragma unroll
@@ -957,17 +891,221 @@ __global__ __launch_bounds__(kBcWaves * 64) void best_cuts_kernel(
         }
     }
 #pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        const double og = __shfl_xor(best, off);
-        const int oc = __shfl_xor(bestc, off);
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const double og = __shfl_xor(best, o);
+        const int oc = __shfl_xor(bestc, o);
         if (og > best || (og == best && oc < bestc)) {
             best = og;
             bestc = oc;
         }
     }
     if (lane == 0) {
-        cand_gain[(size_t)node * d + j] = best;
-        cand_cut[(size_t)node * d + j] = bestc;
+        cand_gain[pair] = best;
+        cand_cut[pair] = bestc;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Best cuts of a layer in the fit (cumulative histograms, separation gain,
+// argmax; section 1.1), from the prefix-summed fixed-point chunk partials of
+// the routed histogram pass: summed over chunks, the partial row of a
+// (node, feature) is P(b) = the node's histogram summed over bins <= b, per
+// class, exactly (64-bit integers).  Cut c (1 <= c <= B-1) sends bins < c
+// left, so S(c) = P_sig(c-1) and B(c) = P_bkg(c-1); the totals are P(B-1).
+//
+// The cuts of a row are split into slices of kCutSlice cuts, one workgroup
+// per (histogrammed node, feature, slice): slice q holds cuts
+// kCutSlice q + 1 .. kCutSlice (q + 1) and needs P at bins
+// kCutSlice q - 1 .. kCutSlice q + kCutSlice - 1 (P(c-1) of its cuts and, for
+// the empty-bin rule, P(c-2)): lane l holds window bin l >> 1, class l & 1.
+// The workgroup's wavefronts sum the chunks round-robin (integer sums: exact
+// in any order); wavefront 0 then evaluates the slice's cuts and writes the
+// slice's candidate (entry j * S + q of the node, gain highest, then lowest
+// bin).  With SIB (layers below the root) the partials are the left children
+// of the parents and wavefront 1 evaluates the right child, parent - left,
+// from the parents' summed rows (hparent).  hout receives the summed rows of
+// every node of the layer (the next layer's parents).
+//
+// The side histogram (float64 sums of the weights below the fixed-point
+// grid, per node of the layer, plain bins) is added after a prefix scan when
+// any of a row's values is non-zero.  Every workgroup also clears its share
+// of the next layer's side histogram (small_next), which no kernel reads in
+// the meantime.
+//
+// Exactness rules (those of the plain definition, decided here on the exact
+// sums): a cut with an empty side has gain exactly 0; a cut c >= 2 whose bin
+// c-1 is empty makes the same partition as cut c-1 and is skipped, so the
+// lower cut wins that tie whatever the rounding.
+constexpr int kCutSlice = 31;
+constexpr int kCutWaves = 4;
+
+template <bool SIB>
+__global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
+    const uint64_t *__restrict__ partial, int chunks, int scale, const double *__restrict__ small,
+    double *__restrict__ small_next, size_t small_next_count, int hnodes, int d, int nbins, int S,
+    double *__restrict__ cand_gain, int *__restrict__ cand_cut,
+    const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout) {
+#pragma clang fp contract(off)
+    __shared__ uint64_t red[kCutWaves][kWave + 2];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int q = blockIdx.x % S;
+    const int kj = blockIdx.x / S;
+    const int j = kj % d;
+    const int k = kj / d;   // histogrammed node (the parent with SIB)
+    const size_t row = (size_t)nbins * 2;
+    const int wi = lane >> 1, cls = lane & 1;
+    const int b = kCutSlice * q - 1 + wi;   // this lane's window bin
+    const bool inb = b >= 0 && b < nbins;
+    const size_t off = ((size_t)k * d + j) * row;
+    const size_t offv = off + (size_t)(inb ? b : 0) * 2 + cls;
+    const size_t offt = off + (size_t)(nbins - 1) * 2 + cls;
+    const size_t stride_p = (size_t)hnodes * d * row;
+    // node of this wavefront's candidates, as an index within the layer
+    const int node = SIB ? 2 * k + (wave & 1) : k;
+    const size_t noff = ((size_t)node * d + j) * row;
+
+    // side histogram row of the candidate wavefronts' node: lane l holds bins
+    // 4l..4l+3, both classes (loaded first, in flight with the chunk sums)
+    double sd[8];
+    const bool cwave = wave < (SIB ? 2 : 1);
+    if (cwave) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int bb = 4 * lane + (e >> 1);
+            sd[e] = bb < nbins ? small[noff + 2 * bb + (e & 1)] : 0.0;
+        }
+    }
+    uint64_t pv = 0, pt = 0;   // parent row (right child = parent - left)
+    if (SIB && wave == 1) {
+        pv = hparent[offv];
+        pt = hparent[offt];
+    }
+    // chunk sums: wavefront w takes chunks w, w + kCutWaves, ...
+    uint64_t v = 0, vt = 0;
+    {
+        int p = wave;
+        for (; p + 3 * kCutWaves < chunks; p += 4 * kCutWaves) {
+            const uint64_t *b0 = partial + (size_t)p * stride_p;
+            const uint64_t *b1 = b0 + kCutWaves * stride_p;
+            const uint64_t *b2 = b1 + kCutWaves * stride_p;
+            const uint64_t *b3 = b2 + kCutWaves * stride_p;
+            const uint64_t x0 = b0[offv], x1 = b1[offv], x2 = b2[offv], x3 = b3[offv];
+            const uint64_t t0 = b0[offt], t1 = b1[offt], t2 = b2[offt], t3 = b3[offt];
+            v += (x0 + x1) + (x2 + x3);
+            vt += (t0 + t1) + (t2 + t3);
+        }
+        for (; p < chunks; p += kCutWaves) {
+            v += partial[(size_t)p * stride_p + offv];
+            vt += partial[(size_t)p * stride_p + offt];
+        }
+    }
+    red[wave][lane] = v;
+    if (lane < 2) red[wave][kWave + lane] = vt;
+    // this workgroup's share of the next layer's side histogram
+    {
+        const size_t per = (small_next_count + gridDim.x - 1) / gridDim.x;
+        const size_t lo = per * blockIdx.x;
+        const size_t hi = min(small_next_count, lo + per);
+        for (size_t t = lo + threadIdx.x; t < hi; t += blockDim.x) small_next[t] = 0.0;
+    }
+    __syncthreads();
+    if (!cwave) return;
+    uint64_t P = 0, T = 0;
+#pragma unroll
+    for (int w = 0; w < kCutWaves; ++w) {
+        P += red[w][lane];
+        T += red[w][kWave + cls];
+    }
+    if (!inb) P = 0;
+    if (SIB && wave == 1) {   // right child = parent - left child (exact)
+        P = (inb ? pv : 0) - P;
+        T = pt - T;
+    }
+    if (hout && wi >= 1 && inb) hout[noff + 2 * b + cls] = P;
+    // the row total P(B-1), which the windows do not reach when B > 31 S
+    if (hout && q == S - 1 && lane < 2) hout[noff + 2 * (nbins - 1) + cls] = T;
+
+    // side histogram: inclusive prefix over bins (per class) when the row
+    // holds anything, picked at this lane's window bin; sb = the bin itself
+    double sp = 0.0, sb = 0.0, stot = 0.0;
+    bool any = false;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) any |= sd[e] != 0.0;
+    if (__any(any)) {
+        double pr[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pr[e] = sd[e] + (e >= 2 ? pr[e - 2] : 0.0);
+        double xs = pr[6], xb = pr[7];   // lane totals, inclusive scan
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const double us = __shfl_up(xs, o), ub = __shfl_up(xb, o);
+            if (lane >= o) {
+                xs += us;
+                xb += ub;
+            }
+        }
+        const double es = xs - pr[6], eb = xb - pr[7];   // exclusive
+        const int src = inb ? b >> 2 : 0, el = inb ? b & 3 : 0;
+        double cand_p = 0.0, cand_b = 0.0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const double ps = __shfl(pr[2 * e] + es, src), pbk = __shfl(pr[2 * e + 1] + eb, src);
+            const double vs = __shfl(sd[2 * e], src), vb = __shfl(sd[2 * e + 1], src);
+            if (el == e) {
+                cand_p = cls ? pbk : ps;
+                cand_b = cls ? vb : vs;
+            }
+        }
+        sp = inb ? cand_p : 0.0;
+        sb = inb ? cand_b : 0.0;
+        const double tS = __shfl(xs, kWave - 1), tB = __shfl(xb, kWave - 1);
+        stot = cls ? tB : tS;
+    }
+
+    // cut c = kCutSlice q + wi evaluated by the even lane of pair wi >= 1:
+    // this pair holds bin c-1, the pair below bin c-2
+    const unsigned long long Ps = __shfl((unsigned long long)P, lane & ~1);
+    const unsigned long long Pb = __shfl((unsigned long long)P, lane | 1);
+    const unsigned long long Qs = __shfl((unsigned long long)P, max((lane & ~1) - 2, 0));
+    const unsigned long long Qb = __shfl((unsigned long long)P, max((lane & ~1) - 1, 1));
+    const unsigned long long Ts = __shfl((unsigned long long)T, 0);
+    const unsigned long long Tb = __shfl((unsigned long long)T, 1);
+    const double sPs = __shfl(sp, lane & ~1), sPb = __shfl(sp, lane | 1);
+    const double sBs = __shfl(sb, lane & ~1), sBb = __shfl(sb, lane | 1);
+    const double sTs = __shfl(stot, 0), sTb = __shfl(stot, 1);
+    const int c = kCutSlice * q + wi;
+    double g = -INFINITY;
+    if (cls == 0 && wi >= 1 && c <= nbins - 1) {
+        const bool left_empty = Ps == 0 && Pb == 0 && sPs == 0.0 && sPb == 0.0;
+        const bool right_empty = Ps == Ts && Pb == Tb && sPs == sTs && sPb == sTb;
+        const bool bin_empty = Ps == Qs && Pb == Qb && sBs == 0.0 && sBb == 0.0;
+        if (c >= 2 && bin_empty) {
+            g = -INFINITY;   // same partition as cut c-1
+        } else if (left_empty || right_empty) {
+            g = 0.0;
+        } else {
+            const double SS = ldexp((double)Ps, -scale) + sPs;
+            const double BB = ldexp((double)Pb, -scale) + sPb;
+            const double ST = ldexp((double)Ts, -scale) + sTs;
+            const double BT = ldexp((double)Tb, -scale) + sTb;
+            g = (gini(ST, BT) - gini(SS, BB)) - gini(ST - SS, BT - BB);
+        }
+    }
+    double best = g;
+    int bestc = g > -INFINITY ? c : 0x7fffffff;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const double og = __shfl_xor(best, o);
+        const int oc = __shfl_xor(bestc, o);
+        if (og > best || (og == best && oc < bestc)) {
+            best = og;
+            bestc = oc;
+        }
+    }
+    if (lane == 0) {
+        const size_t e = (size_t)node * d * S + (size_t)j * S + q;
+        cand_gain[e] = best;
+        cand_cut[e] = bestc;
     }
 }
 
@@ -1055,7 +1193,7 @@ template <bool ROUTED, int NL>
 __global__ __launch_bounds__(1024) void leaf_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
-    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut,
+    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
     int depth, const int8_t *__restrict__ y, const float *__restrict__ v,
     const double *__restrict__ F, uint64_t seed, int tree, double alpha,
@@ -1075,8 +1213,9 @@ __global__ __launch_bounds__(1024) void leaf_kernel(
     int64_t ia = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
 
     CandRegs cr;
+    const CandSet cs{cand_gain, cand_cut, d, cslices};
     const bool pwave = ROUTED && wave < half;
-    if (pwave) cand_load(cand_gain, cand_cut, d, wave, lane, cr);
+    if (pwave) cand_load(cs, wave, lane, cr);
     LeafStep A, B;
     if (ia < n) leaf_load<ROUTED, ROWS>(A, xb, ldb, d, node_in, y, v, F, half, s_cf, ia, false);
     if (NL == 0)
@@ -1087,9 +1226,9 @@ __global__ __launch_bounds__(1024) void leaf_kernel(
             double bg;
             bool ok;
             if (k == wave)
-                cand_reduce(cr, d, lane, &bf, &bc, &bg, &ok);
+                cand_reduce(cr, cs, k, lane, &bf, &bc, &bg, &ok);
             else
-                node_best(cand_gain, cand_cut, d, k, lane, &bf, &bc, &bg, &ok);
+                node_best(cs, k, lane, &bf, &bc, &bg, &ok);
             if (lane == 0) {
                 s_cf[k] = (uint8_t)bf;
                 s_cc[k] = (uint8_t)bc;
@@ -1482,8 +1621,8 @@ hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, i
                           const ParentCuts &pc, int layer, int scale, uint64_t *partial,
                           double *small, int *err, hipStream_t s) {
     hist_kernel<ROUTED, NP, FPG><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
-        xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.rec_f,
-        pc.rec_c, pc.rec_g, layer, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
+        xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.slices,
+        pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
         hs.chunks, hs.chunk_events, scale, partial, small, err);
     return hipGetLastError();
 }
@@ -1545,24 +1684,36 @@ hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, doub
     return hipGetLastError();
 }
 
-hipError_t launch_best_cuts(const uint64_t *partial, int chunks, int scale, double *small,
-                            const double *hist, int n_nodes, int d, int n_bins,
-                            double *cand_gain, int *cand_cut, const uint64_t *hparent,
-                            uint64_t *hout, hipStream_t s) {
-    if (partial)
-        best_cuts_kernel<true><<<n_nodes * d, kBcWaves * kWave, 0, s>>>(
-            partial, chunks, scale, small, nullptr, n_nodes, d, n_bins, cand_gain, cand_cut,
-            hparent, hout);
+int cut_slices(int n_bins) { return (n_bins - 1 + kCutSlice - 1) / kCutSlice; }
+
+hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bins,
+                                double *cand_gain, int *cand_cut, hipStream_t s) {
+    best_cuts_f64_kernel<<<n_nodes * d, kWave, 0, s>>>(hist, d, n_bins, cand_gain, cand_cut);
+    return hipGetLastError();
+}
+
+hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
+                           double *small_next, size_t small_next_count, int hnodes, int d,
+                           int n_bins, bool sibling, double *cand_gain, int *cand_cut,
+                           const uint64_t *hparent, uint64_t *hout, hipStream_t s) {
+    const int S = cut_slices(n_bins);
+    const int blocks = hnodes * d * S;
+    if (sibling)
+        cut_scan_kernel<true><<<blocks, kCutWaves * kWave, 0, s>>>(
+            partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,
+            cand_gain, cand_cut, hparent, hout);
     else
-        best_cuts_kernel<false><<<n_nodes * d, kBcWaves * kWave, 0, s>>>(
-            nullptr, 1, 0, nullptr, hist, n_nodes, d, n_bins, cand_gain, cand_cut, nullptr,
-            nullptr);
+        cut_scan_kernel<false><<<blocks, kCutWaves * kWave, 0, s>>>(
+            partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,
+            cand_gain, cand_cut, nullptr, hout);
     return hipGetLastError();
 }
 
 hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,
-                              uint8_t *out_f, uint8_t *out_c, double *out_g, hipStream_t s) {
-    select_cuts_kernel<<<n_nodes, kWave, 0, s>>>(cand_gain, cand_cut, d, out_f, out_c, out_g);
+                              int slices, uint8_t *out_f, uint8_t *out_c, double *out_g,
+                              hipStream_t s) {
+    select_cuts_kernel<<<n_nodes, kWave, 0, s>>>(cand_gain, cand_cut, d, slices, out_f, out_c,
+                                                 out_g);
     return hipGetLastError();
 }
 
@@ -1574,7 +1725,8 @@ void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t 
              const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
              double alpha, double *leaf_partial, int *err) {
     leaf_kernel<ROUTED, NL><<<blocks, 1024, 0, s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain,
-                                                   pc.cand_cut, pc.rec_f, pc.rec_c, pc.rec_g,
+                                                   pc.cand_cut, pc.slices, pc.rec_f, pc.rec_c,
+                                                   pc.rec_g,
                                                    depth, y, v, F, seed, tree, alpha,
                                                    leaf_partial, err);
 }
