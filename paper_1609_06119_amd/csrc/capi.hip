@@ -450,7 +450,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
             return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", l,
                         plans[l].lds_bytes, di.max_lds);
     }
-    const int lblocks = leaf_blocks(n, di.cu_count);
+    const int lblocks = leaf_blocks(n, D, di.cu_count);
     const bool fused = D <= kFusedLeafDepth;
     const int max_nodes = 1 << (D - 1);
 
@@ -460,6 +460,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     Carver cv;
     cv.add(&fb.F, npad);
     cv.add(&fb.w, npad);
+    cv.add(&fb.yts, npad);
+    if (w) cv.add(&fb.v, npad);
     cv.add(&fb.node[0], npad);
     cv.add(&fb.node[1], npad);
     cv.add(&fb.partial, partial_elems);
@@ -489,8 +491,14 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
     HIP_TRY(launch_fill_u32(fb.small[0], 0u, 2 * small_elems, s));
     HIP_TRY(launch_fill_u32(fb.small[1], 0u, 2 * small_elems, s));
-    // the histogram passes read whole steps of events: padded events weigh 0
+    // the histogram and leaf passes read whole steps of events: padded events
+    // weigh 0 and have no pseudo-response
     HIP_TRY(launch_fill_u32(fb.w, 0u, (size_t)npad, s));
+    HIP_TRY(launch_fill_u32(fb.yts, 0u, 2 * (size_t)npad, s));
+    if (w) {
+        HIP_TRY(launch_fill_u32(fb.v, 0u, (size_t)npad, s));
+        HIP_TRY(hipMemcpyAsync(fb.v, w, (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, s));
+    }
     HIP_TRY(launch_validate(y, w, n, fb.class_partial, fb.err, s));
     HIP_TRY(launch_initial_score(fb.class_partial, fb.f0, fb.err, s));
     int h_err = 0;
@@ -519,7 +527,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                                          t == 0 ? nullptr : fb.node[D & 1], fused ? nullptr : prev,
                                          t > 0 && fused ? fb.leaf_partial : nullptr, lblocks, eta,
                                          fused ? prev : nullptr, D, n, seed, t, alpha, fb.w,
-                                         nullptr, di.cu_count, st));
+                                         fb.yts, nullptr, di.cu_count, st));
                 tm.done();
             }
             uint8_t *cf = fb.cut_feature + (size_t)t * nin;
@@ -562,7 +570,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 const ParentCuts pc{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
                 Timed tm(FBDT_K_LEAF, st);
                 HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
-                                    fb.node[D & 1], pc, D, true, y, w, fb.F, seed, t, alpha, lblocks,
+                                    fb.node[D & 1], pc, D, true, fb.v, fb.yts, lblocks,
                                     fb.leaf_partial, fb.err, st));
                 if (!fused || t == T - 1)
                     HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, eta,
@@ -613,7 +621,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     if (score_out)
         HIP_TRY(launch_tree_prep(y, w, fb.F, nullptr, fb.node[D & 1],
                                  fb.leaf + (size_t)(T - 1) * nleaf, nullptr, 0, 0.0, nullptr, D, n,
-                                 seed, T, alpha, nullptr, score_out, di.cu_count, s));
+                                 seed, T, alpha, nullptr, nullptr, score_out, di.cu_count, s));
 
     fbdt_model *m = new (std::nothrow) fbdt_model;
     if (!m) return fail(FBDT_E_DEVICE, "out of host memory");
@@ -782,8 +790,8 @@ int fbdt_tree_weights(const int8_t *y, const float *v, const double *F, int64_t 
     hipStream_t s = static_cast<hipStream_t>(stream);
     Timed tm(FBDT_K_TREE_PREP, s, (double)n * 17.0);
     HIP_TRY(launch_tree_prep(y, v, const_cast<double *>(F), nullptr, nullptr, nullptr, nullptr, 0,
-                             0.0, nullptr, 1, n, seed, tree, alpha, w_out, nullptr, di.cu_count,
-                             s));
+                             0.0, nullptr, 1, n, seed, tree, alpha, w_out, nullptr, nullptr,
+                             di.cu_count, s));
     tm.done();
     return FBDT_OK;
 }
@@ -921,19 +929,38 @@ int fbdt_leaf_values(const uint8_t *node, const int8_t *y, const float *v, const
     DeviceInfo di;
     if ((rc = current_device(&dev, &di))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int blocks = leaf_blocks(n, di.cu_count);
+    const int blocks = leaf_blocks(n, depth, di.cu_count);
+    // the leaf pass reads whole steps of events: padded copies of the leaf
+    // ids and weights, and y~ of the sampled events (0 beyond n) from the
+    // re-weighting pass
+    const int64_t npad = (n + 15) & ~(int64_t)15;
     Arena &a = g_arena[dev];
     std::lock_guard<std::mutex> lk(a.mu);
     Carver cv;
-    double *lp;
+    double *lp, *yts;
+    uint8_t *node_pad;
+    float *v_pad = nullptr;
     int *err;
     cv.add(&lp, (size_t)blocks * 2 * (1 << depth));
+    cv.add(&yts, (size_t)npad);
+    cv.add(&node_pad, (size_t)npad);
+    if (v) cv.add(&v_pad, (size_t)npad);
     cv.add(&err, 1);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     HIP_TRY(launch_fill_u32(err, 0u, 1, s));
-    HIP_TRY(launch_leaf(nullptr, 0, n, 1, node, nullptr, ParentCuts{}, depth, false, y, v, F,
-                        seed, tree, alpha, blocks, lp, err, s));
+    HIP_TRY(launch_fill_u32(yts, 0u, 2 * (size_t)npad, s));
+    HIP_TRY(launch_fill_u32(node_pad, 0u, (size_t)npad / 4, s));
+    HIP_TRY(hipMemcpyAsync(node_pad, node, (size_t)n, hipMemcpyDeviceToDevice, s));
+    if (v) {
+        HIP_TRY(launch_fill_u32(v_pad, 0u, (size_t)npad, s));
+        HIP_TRY(hipMemcpyAsync(v_pad, v, (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, s));
+    }
+    HIP_TRY(launch_tree_prep(y, v, const_cast<double *>(F), nullptr, nullptr, nullptr, nullptr, 0,
+                             0.0, nullptr, depth, n, seed, tree, alpha, nullptr, yts, nullptr,
+                             di.cu_count, s));
+    HIP_TRY(launch_leaf(nullptr, 0, n, 1, node_pad, nullptr, ParentCuts{}, depth, false, v_pad,
+                        yts, blocks, lp, err, s));
     HIP_TRY(launch_leaf_finalize(lp, blocks, depth, eta, leaf, s));
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;

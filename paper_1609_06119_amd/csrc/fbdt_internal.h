@@ -36,6 +36,8 @@ struct HistShape {
 struct FitBuffers {
     double *F;            // [npad] score
     float *w;             // [npad] signed re-weighted sample
+    double *yts;          // [npad] y~ of the sampled events, 0 for the others
+    float *v;             // [npad] caller's event weights, padded (null: unit weights)
     uint8_t *node[2];     // [npad] node ids, double-buffered across layers
     uint64_t *partial;    // fixed-point histogram partials [chunks][histogrammed nodes][d][B][2]
     uint64_t *hfull[2];   // summed fixed-point histograms of every node of a layer
@@ -87,12 +89,13 @@ constexpr int kFusedLeafDepth = 4;
 //    eta; leaf_rec (optional) receives them;
 //  else leaf_prev != null: the previous tree's boost weights;
 //  either way F += weight[leaf_node - 2^depth]; else if f0 != null: F = *f0.
-//  w may be null (score update only); score_out (optional) receives F.
+//  w may be null (score update only); yts (optional) receives y~ of the
+//  sampled events and 0 for the others; score_out (optional) receives F.
 hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const double *f0,
                             const uint8_t *leaf_node, const double *leaf_prev,
                             const double *leaf_partial, int lblocks, double eta, double *leaf_rec,
                             int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
-                            double *score_out, int cu_count, hipStream_t s);
+                            double *yts, double *score_out, int cu_count, hipStream_t s);
 
 // fpg, chunks, threads: launch-shape overrides (0 = default).  sibling: the
 // routed fit pass, which for layer >= 1 histograms one child per parent.
@@ -176,13 +179,16 @@ hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int 
 
 // Last routing (routed = true, from layer depth-1 to the leaves with the
 // cuts from pc) or none (node_in already holds leaf ids), then the per-block
-// partial sums of the terminal boost weights; launch_leaf_finalize adds the
-// partials and writes eta * num / den per leaf.
-int leaf_blocks(int64_t n, int cu_count);
+// partial sums of the terminal boost weights from yts (y~ of the sampled
+// events, 0 for the others); launch_leaf_finalize adds the partials and
+// writes eta * num / den per leaf.  node_in, v (or null: unit weights) and
+// yts hold round_up(n, 8) elements with yts = 0 beyond n; node_out receives
+// round_up(n, 8) ids.
+int leaf_blocks(int64_t n, int depth, int cu_count);
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
                        uint8_t *node_out, const ParentCuts &pc, int depth, bool routed,
-                       const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
-                       double alpha, int blocks, double *leaf_partial, int *err, hipStream_t s);
+                       const float *v, const double *yts, int blocks, double *leaf_partial,
+                       int *err, hipStream_t s);
 hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, double eta,
                                 double *leaf_out, hipStream_t s);
 

@@ -28,6 +28,15 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kHistE = 8;      // events per thread and step of the histogram pass
 
+// Workgroup barrier that orders LDS only: this wavefront's LDS operations
+// complete before it (s_waitcnt lgkmcnt(0)), while its global loads and
+// stores may stay in flight across it (the compiler still waits for a
+// loaded register where it is used).  For barriers that publish LDS data
+// only, so that prefetched event data keeps arriving and stores keep draining.
+__device__ __forceinline__ void lds_barrier() {
+    __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // SplitMix64 (Steele, Lea & Flood, OOPSLA 2014): output number k (0-based)
 // of the generator seeded with `seed` mixes the state seed + (k + 1) * gamma.
 __device__ __forceinline__ uint64_t splitmix64_at(uint64_t seed, uint64_t k) {
@@ -145,20 +154,53 @@ __global__ __launch_bounds__(256) void initial_score_kernel(const double *__rest
 
 // ---------------------------------------------------------------------------
 // Sum of the workgroup partials of the leaf pass in a fixed order by a
-// workgroup of kLeafReduceThreads threads (thread t adds value t % nv over
-// blocks t / nv, t / nv + stripes, ...; the stripes are then added
-// pairwise), and the boost weights eta * num / den (0 when den = 0) into
-// s_leaf[0, nleaf).  Every thread of the workgroup calls it; red holds
-// kLeafReduceThreads doubles of LDS.  The same order everywhere gives the
-// same weights in every workgroup that calls it.
+// workgroup of kLeafReduceThreads threads, and the boost weights
+// eta * num / den (0 when den = 0) into s_leaf[0, nleaf).  Every thread of
+// the workgroup calls it; red holds kLeafReduceThreads doubles of LDS.  The
+// same order everywhere gives the same weights in every workgroup that calls
+// it.  With nv = 2 nleaf <= 64 values: lane l of wavefront w takes value
+// l % nv and stripe s = w (64 / nv) + l / nv of the S = 16 (64 / nv) stripes,
+// sums blocks s, s + S, ... in order, the wavefront adds its stripes with
+// xor shuffles (fixed tree), and 16 wavefront sums are added in order.
+// Larger nv: thread t takes value t % nv over stripes of kLeafReduceThreads
+// / nv, then the stripes are added pairwise.
 constexpr int kLeafReduceThreads = 1024;
 
 __device__ void reduce_leaf_partials(const double *__restrict__ leaf_partial, int nblocks,
                                      int nleaf, double eta, double *red, double *s_leaf) {
 #pragma clang fp contract(off)
     const int nv = 2 * nleaf;
-    const int stripes = kLeafReduceThreads / nv;
     const int t = threadIdx.x;
+    if (nv <= kWave) {
+        const int lane = t % kWave, wave = t / kWave;
+        const int per_wave = kWave / nv;
+        const int stripes = (kLeafReduceThreads / kWave) * per_wave;
+        const int val = lane % nv, st = wave * per_wave + lane / nv;
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        int b = st;
+        for (; b + 3 * stripes < nblocks; b += 4 * stripes) {
+            s0 += leaf_partial[(size_t)b * nv + val];
+            s1 += leaf_partial[(size_t)(b + stripes) * nv + val];
+            s2 += leaf_partial[(size_t)(b + 2 * stripes) * nv + val];
+            s3 += leaf_partial[(size_t)(b + 3 * stripes) * nv + val];
+        }
+        for (; b < nblocks; b += stripes) s0 += leaf_partial[(size_t)b * nv + val];
+        double x = (s0 + s1) + (s2 + s3);
+        for (int o = nv; o < kWave; o <<= 1) x += __shfl_xor(x, o);
+        if (lane < nv) red[wave * nv + lane] = x;
+        lds_barrier();
+        if (t < nleaf) {
+            double num = 0.0, den = 0.0;
+            for (int w = 0; w < kLeafReduceThreads / kWave; ++w) {
+                num += red[w * nv + 2 * t];
+                den += red[w * nv + 2 * t + 1];
+            }
+            s_leaf[t] = den == 0.0 ? 0.0 : eta * (num / den);
+        }
+        lds_barrier();
+        return;
+    }
+    const int stripes = kLeafReduceThreads / nv;
     if (t < stripes * nv) {
         const int val = t % nv, st = t / nv;
         double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
@@ -188,7 +230,8 @@ __device__ void reduce_leaf_partials(const double *__restrict__ leaf_partial, in
 // ---------------------------------------------------------------------------
 // One elementwise pass per tree: add the previous tree's boost weight to F
 // (or set F = F0 for the first tree), then the histogram weight of every
-// event: fl32(v |y~|) if sampled else 0, class in the sign bit.  The
+// event: fl32(v |y~|) if sampled else 0, class in the sign bit, and (yts)
+// the pseudo-response y~ of the sampled events, 0 for the others.  The
 // previous tree's boost weights come either from the model (leaf_prev) or
 // straight from the leaf pass partials (leaf_partial, depth <= 4), which
 // every workgroup sums itself in the fixed order of leaf_finalize_kernel;
@@ -198,6 +241,7 @@ struct PrepStep {
     uint32_t leaf;
     float v;
     double F;
+    bool sampled;   // depends on (seed, tree, i) only: decided while the loads fly
 };
 
 __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
@@ -205,7 +249,7 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     const double *__restrict__ f0, const uint8_t *__restrict__ leaf_node,
     const double *__restrict__ leaf_prev, const double *__restrict__ leaf_partial,
     int lblocks, double eta, double *__restrict__ leaf_rec, int depth, int64_t n,
-    uint64_t seed, int tree, double alpha, float *__restrict__ w,
+    uint64_t seed, int tree, double alpha, float *__restrict__ w, double *__restrict__ yts,
     double *__restrict__ score_out) {
     __shared__ double red[kLeafReduceThreads];
     __shared__ double s_leaf[128];
@@ -216,11 +260,13 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     int64_t ia = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     // one event per thread and step; the first step's loads are in flight
     // while the boost weights are summed, later steps are loaded one ahead
+    const bool need_sample = w || yts;
     auto load = [&](PrepStep &st, int64_t i) {
         st.yv = y[i];
         st.v = v ? v[i] : 1.0f;
         st.leaf = have_leaf ? (uint32_t)leaf_node[i] : 0u;
         st.F = read_F ? F[i] : 0.0;
+        st.sampled = need_sample && in_subsample(seed, tree, n, i, alpha);
     };
     PrepStep A, B;
     if (ia < n) load(A, ia);
@@ -229,7 +275,7 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
         if (blockIdx.x == 0 && leaf_rec && threadIdx.x < nleaf) leaf_rec[threadIdx.x] = s_leaf[threadIdx.x];
     } else if (leaf_prev) {
         for (unsigned t = threadIdx.x; t < nleaf; t += blockDim.x) s_leaf[t] = leaf_prev[t];
-        __syncthreads();
+        lds_barrier();
     }
     const double f0v = (f0 && !have_leaf) ? *f0 : 0.0;
     auto step = [&](const PrepStep &st, int64_t i) {
@@ -246,12 +292,16 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
             Fi = st.F;
         }
         if (score_out) score_out[i] = Fi;
-        if (w) {
+        if (w || yts) {
             const double yf = (double)st.yv;
             const double yt = pseudo_response(yf, Fi);
-            const double vi = (double)st.v;
-            const float wi = in_subsample(seed, tree, n, i, alpha) ? (float)(vi * fabs(yt)) : 0.0f;
-            w[i] = yf > 0.0 ? wi : -wi;
+            const bool sampled = st.sampled;
+            if (w) {
+                const double vi = (double)st.v;
+                const float wi = sampled ? (float)(vi * fabs(yt)) : 0.0f;
+                w[i] = yf > 0.0 ? wi : -wi;
+            }
+            if (yts) yts[i] = sampled ? yt : 0.0;
         }
     };
     if (ia < n) {
@@ -694,7 +744,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
     uint32_t cut[4] = {0u, 0u, 0u, 0u};
     if (ROUTED && NP > 0 && layer >= 1) {
 #pragma unroll
@@ -719,7 +769,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
             if (!more_a) break;
         }
     }
-    __syncthreads();
+    lds_barrier();
 
     // partial[p][node][feature][bin][class]: one (node, feature) row per
     // wavefront step; bins >= n_bins must be empty.  Routed (fit) passes
@@ -1008,7 +1058,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         const size_t hi = min(small_next_count, lo + per);
         for (size_t t = lo + threadIdx.x; t < hi; t += blockDim.x) small_next[t] = 0.0;
     }
-    __syncthreads();
+    lds_barrier();
     if (!cwave) return;
     uint64_t P = 0, T = 0;
 #pragma unroll
@@ -1112,114 +1162,103 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
 // ---------------------------------------------------------------------------
 // Terminal boost weights (section 1.3): per leaf, sum(v y~) and
 // sum(v |y~| (2 - |y~|)) over the sampled events, one partial per
-// workgroup.  With NL > 0 leaves every thread keeps the 2 NL sums in
-// registers, then a wavefront reduction and an in-order sum over wavefronts
-// give the workgroup's partial (no atomics, fixed order); with NL = 0 (deep
-// trees) threads add into LDS accumulators.  Routed mode first takes the
-// last layer's cuts from their candidates (loaded before the event data, so
-// both latencies overlap), sends every event from layer depth-1 to its leaf
+// workgroup, from yts (y~ of the sampled events, 0 for the others, written
+// by the re-weighting pass).  Routed mode first takes the last layer's cuts
+// from their candidates, sends every event from layer depth-1 to its leaf
 // and stores the leaf id; with at most four parents the code rows of the
-// parents' cut features are loaded with the event's other data, so routing
-// costs no dependent load.  One event per thread and step, the next step's
-// loads issued before the current step's arithmetic.
-// Sums V values (a power of two <= 64) over a wavefront in few shuffles:
-// each halving step exchanges half of the values with the lane across bit b
-// (b = 5, 4, ...) and keeps the half that bit selects, so lane l ends with
-// value idx(l) = its kept halves summed over the lanes that agree with l in
-// those bits; plain butterflies over the lower bits then complete the sums.
-// Returns the total of value *idx in every lane (fixed order: deterministic).
-template <int H>
-__device__ __forceinline__ void transpose_sum_step(double *x, int lane, int bit, int &id) {
-    const bool hi = (lane >> bit) & 1;
-#pragma unroll
-    for (int j = 0; j < H; ++j) {
-        const double mine = hi ? x[H + j] : x[j];
-        const double other = hi ? x[j] : x[H + j];
-        x[j] = mine + __shfl_xor(other, 1 << bit);
-    }
-    id += hi ? H : 0;
-    if constexpr (H > 1) transpose_sum_step<H / 2>(x, lane, bit - 1, id);
+// parents' cut features are loaded with the step's other data, so routing
+// costs no dependent load.
+//
+// Every thread owns the 2 * 2^depth accumulators of its column of the
+// LDS array acc[value][thread] and adds its events in order (non-returning
+// LDS float64 adds on addresses no other thread touches: exact order, no
+// bank conflicts); the workgroup then adds its columns in a fixed order.
+// kLeafE consecutive events per thread and step on padded arrays (weights,
+// yts, node ids: zero pseudo-response beyond n), the next step's loads
+// issued before the current step's arithmetic.
+constexpr int kLeafE = 8;
+
+__host__ __device__ constexpr int leaf_threads(int depth) {
+    // acc takes threads * 2^(depth + 1) doubles: at most 128 KiB
+    return depth <= 5 ? 256 : depth == 6 ? 128 : 64;
 }
 
-template <int V>
-__device__ __forceinline__ double wave_transpose_sum(double (&x)[V], int lane, int *idx) {
-    static_assert(V >= 2 && V <= 64 && (V & (V - 1)) == 0, "V: a power of two in [2, 64]");
-    int id = 0;
-    transpose_sum_step<V / 2>(x, lane, 5, id);
-    double r = x[0];
-    constexpr int lower = 6 - __builtin_ctz(V);   // bits 5 .. 6 - log2(V) are used
-#pragma unroll
-    for (int bit = lower - 1; bit >= 0; --bit) r += __shfl_xor(r, 1 << bit);
-    *idx = id;
-    return r;
-}
-
+template <int NP>
 struct LeafStep {
-    int node;        // parent id (routed) or leaf id
-    uint32_t rows;   // codes of up to four parents' cut features, one byte each
-    int yv;
-    double F;
-    float v;
+    uint2 node;                     // parent ids (routed) or leaf ids
+    uint2 rows[NP > 0 ? NP : 1];    // codes of the parents' cut features
+    double yt[kLeafE];
+    float v[kLeafE];
 };
 
-// codes of the parents' cut features (the cut table must be in LDS)
-template <bool ROUTED, bool ROWS>
-__device__ __forceinline__ void leaf_load_rows(LeafStep &st, const uint8_t *__restrict__ xb,
-                                               int64_t ldb, int d, int half, const uint8_t *s_cf,
-                                               int64_t i) {
-    if (ROUTED && ROWS) {
-        uint32_t r = 0;
-        for (int k = 0; k < half; ++k)
-            r |= (uint32_t)xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i] << (8 * k);
-        st.rows = r;
+template <bool ROUTED, int NP>
+__device__ __forceinline__ void leaf_load_rows(LeafStep<NP> &st, const uint8_t *__restrict__ xb,
+                                               int64_t ldb, int d, const uint8_t *s_cf,
+                                               int64_t i0) {
+    if (ROUTED && NP > 0) {
+#pragma unroll
+        for (int k = 0; k < (NP > 0 ? NP : 1); ++k)
+            st.rows[k] =
+                *reinterpret_cast<const uint2 *>(xb + (int64_t)min((int)s_cf[k], d - 1) * ldb + i0);
     }
 }
 
-template <bool ROUTED, bool ROWS>
-__device__ __forceinline__ void leaf_load(LeafStep &st, const uint8_t *__restrict__ xb,
+template <bool ROUTED, int NP>
+__device__ __forceinline__ void leaf_load(LeafStep<NP> &st, const uint8_t *__restrict__ xb,
                                           int64_t ldb, int d, const uint8_t *__restrict__ node_in,
-                                          const int8_t *__restrict__ y,
                                           const float *__restrict__ v,
-                                          const double *__restrict__ F, int half,
-                                          const uint8_t *s_cf, int64_t i, bool with_rows) {
-    st.node = node_in ? (int)node_in[i] : 1;
-    st.yv = y[i];
-    st.F = F[i];
-    st.v = v ? v[i] : 1.0f;
-    if (with_rows) leaf_load_rows<ROUTED, ROWS>(st, xb, ldb, d, half, s_cf, i);
+                                          const double *__restrict__ yts, const uint8_t *s_cf,
+                                          int64_t i0, bool with_rows) {
+    st.node = node_in ? *reinterpret_cast<const uint2 *>(node_in + i0)
+                      : make_uint2(0x01010101u, 0x01010101u);
+#pragma unroll
+    for (int e = 0; e < kLeafE; e += 2) {
+        const double2 y2 = *reinterpret_cast<const double2 *>(yts + i0 + e);
+        st.yt[e] = y2.x;
+        st.yt[e + 1] = y2.y;
+    }
+    if (v) {
+        const float4 a = reinterpret_cast<const float4 *>(v + i0)[0];
+        const float4 b = reinterpret_cast<const float4 *>(v + i0)[1];
+        st.v[0] = a.x; st.v[1] = a.y; st.v[2] = a.z; st.v[3] = a.w;
+        st.v[4] = b.x; st.v[5] = b.y; st.v[6] = b.z; st.v[7] = b.w;
+    } else {
+#pragma unroll
+        for (int e = 0; e < kLeafE; ++e) st.v[e] = 1.0f;
+    }
+    if (with_rows) leaf_load_rows<ROUTED, NP>(st, xb, ldb, d, s_cf, i0);
 }
 
-template <bool ROUTED, int NL>
-__global__ __launch_bounds__(1024) void leaf_kernel(
+template <bool ROUTED, int NP>
+__global__ __launch_bounds__(256) void leaf_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
-    int depth, const int8_t *__restrict__ y, const float *__restrict__ v,
-    const double *__restrict__ F, uint64_t seed, int tree, double alpha,
+    int depth, const float *__restrict__ v, const double *__restrict__ yts,
     double *__restrict__ leaf_partial, int *__restrict__ err) {
 #pragma clang fp contract(off)
-    constexpr bool ROWS = NL > 0 && NL <= 8;   // at most four parents
-    __shared__ double acc[2 * 128];
-    __shared__ double red[2 * 16 * 16];
+    extern __shared__ double acc[];   // [2 nleaf][T + 1], then the segment sums
     __shared__ uint8_t s_cf[64], s_cc[64];
+    const int T = blockDim.x;
     const int nleaf = 1 << depth;
+    const int nv = 2 * nleaf;
     const int half = nleaf >> 1;
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
-    const int nwaves = blockDim.x / kWave;
+    const int nwaves = T / kWave;
     int eflag = 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t ia = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * T * kLeafE;
+    int64_t ia = ((int64_t)blockIdx.x * T + threadIdx.x) * kLeafE;
 
     CandRegs cr;
     const CandSet cs{cand_gain, cand_cut, d, cslices};
     const bool pwave = ROUTED && wave < half;
     if (pwave) cand_load(cs, wave, lane, cr);
-    LeafStep A, B;
-    if (ia < n) leaf_load<ROUTED, ROWS>(A, xb, ldb, d, node_in, y, v, F, half, s_cf, ia, false);
-    if (NL == 0)
-        for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x) acc[t] = 0.0;
+    LeafStep<NP> A, B;
+    if (ia < n) leaf_load<ROUTED, NP>(A, xb, ldb, d, node_in, v, yts, s_cf, ia, false);
+    const int TP = T + 1;   // row stride: rows start two LDS banks apart
+    for (int t = threadIdx.x; t < nv * TP; t += T) acc[t] = 0.0;
     if (ROUTED) {
         for (int k = wave; k < half; k += nwaves) {
             int bf, bc;
@@ -1241,89 +1280,99 @@ __global__ __launch_bounds__(1024) void leaf_kernel(
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
+    uint32_t cut[4] = {0u, 0u, 0u, 0u};
+    if (ROUTED && NP > 0) {
+#pragma unroll
+        for (int k = 0; k < (NP > 0 ? NP : 1); ++k) cut[k] = s_cc[k];
+    }
+    double *mine = acc + threadIdx.x;   // this thread's column, value stride TP
 
-    double an[NL > 0 ? NL : 1], ad[NL > 0 ? NL : 1];
+    auto add = [&](const LeafStep<NP> &st, int64_t i0) {
+        uint32_t o[2] = {0u, 0u};
 #pragma unroll
-    for (int l = 0; l < (NL > 0 ? NL : 1); ++l) an[l] = ad[l] = 0.0;
-    auto add = [&](const LeafStep &st, int64_t i) {
-        int leaf;
-        if (ROUTED) {
-            int par = st.node;
-            unsigned k = (unsigned)(par - half);
-            if (k >= (unsigned)half) {  // unreachable for ids written by this library
-                eflag |= kErrRoute;
-                k = 0;
-                par = half;
+        for (int e = 0; e < kLeafE; ++e) {
+            uint32_t leaf;
+            if (ROUTED) {
+                uint32_t par = byte8(st.node, e);
+                uint32_t k = par - (uint32_t)half;
+                if (k >= (uint32_t)half) {   // unreachable for ids written by this library
+                    eflag |= kErrRoute;
+                    k = 0u;
+                    par = (uint32_t)half;
+                }
+                uint32_t x, c;
+                if (NP > 0) {
+                    x = byte8(st.rows[0], e);
+                    c = cut[0];
+#pragma unroll
+                    for (int kk = 1; kk < (NP > 0 ? NP : 1); ++kk) {
+                        if (k == (uint32_t)kk) {
+                            x = byte8(st.rows[kk], e);
+                            c = cut[kk];
+                        }
+                    }
+                } else {
+                    x = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i0 + e];
+                    c = s_cc[k];
+                }
+                leaf = 2u * par + (x >= c ? 1u : 0u);
+                o[e >> 2] |= leaf << (8 * (e & 3));
+            } else {
+                leaf = byte8(st.node, e);
             }
-            uint32_t x;
-            if (ROWS)
-                x = (st.rows >> (8 * k)) & 0xffu;
-            else
-                x = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i];
-            leaf = 2 * par + (x >= s_cc[k] ? 1 : 0);
-            node_out[i] = (uint8_t)leaf;
-        } else {
-            leaf = st.node;
-            if ((unsigned)(leaf - nleaf) >= (unsigned)nleaf) {
-                eflag |= kErrRoute;
-                return;
+            const uint32_t li = leaf - (uint32_t)nleaf;
+            const double yt = st.yt[e];
+            if (yt != 0.0) {   // sampled
+                if (li >= (uint32_t)nleaf) {   // unreachable for ids written by this library
+                    eflag |= kErrRoute;
+                    continue;
+                }
+                const double vi = (double)st.v[e];
+                const double a = fabs(yt);
+                unsafeAtomicAdd(mine + (size_t)(2 * li) * TP, vi * yt);
+                unsafeAtomicAdd(mine + (size_t)(2 * li + 1) * TP, vi * a * (2.0 - a));
             }
         }
-        if (!in_subsample(seed, tree, n, i, alpha)) return;
-        const double yf = (double)st.yv;
-        const double yt = pseudo_response(yf, st.F);
-        const double vi = (double)st.v;
-        const double a = fabs(yt);
-        const double gnum = vi * yt;
-        const double gden = vi * a * (2.0 - a);
-        const int li = leaf - nleaf;
-        if (NL > 0) {
-#pragma unroll
-            for (int l = 0; l < (NL > 0 ? NL : 1); ++l) {
-                an[l] += li == l ? gnum : 0.0;
-                ad[l] += li == l ? gden : 0.0;
-            }
-        } else {
-            atomicAdd(&acc[2 * li], gnum);
-            atomicAdd(&acc[2 * li + 1], gden);
-        }
+        // padded events get leaf ids too (the arrays hold whole steps)
+        if (ROUTED) *reinterpret_cast<uint2 *>(node_out + i0) = make_uint2(o[0], o[1]);
     };
     if (ia < n) {
-        leaf_load_rows<ROUTED, ROWS>(A, xb, ldb, d, half, s_cf, ia);
+        leaf_load_rows<ROUTED, NP>(A, xb, ldb, d, s_cf, ia);
         for (;;) {
             const int64_t ib = ia + stride;
-            if (ib < n) leaf_load<ROUTED, ROWS>(B, xb, ldb, d, node_in, y, v, F, half, s_cf, ib, true);
+            const bool more_b = ib < n;
+            leaf_load<ROUTED, NP>(B, xb, ldb, d, node_in, v, yts, s_cf, more_b ? ib : ia, true);
             add(A, ia);
-            if (ib >= n) break;
+            if (!more_b) break;
             ia = ib + stride;
-            if (ia < n) leaf_load<ROUTED, ROWS>(A, xb, ldb, d, node_in, y, v, F, half, s_cf, ia, true);
+            const bool more_a = ia < n;
+            leaf_load<ROUTED, NP>(A, xb, ldb, d, node_in, v, yts, s_cf, more_a ? ia : ib, true);
             add(B, ib);
-            if (ia >= n) break;
+            if (!more_a) break;
         }
     }
-    if (NL > 0) {
-        // red[wave][2 NL]: 2 NL * nwaves <= 512 doubles for NL <= 16, 16 waves
-        constexpr int V = 2 * (NL > 0 ? NL : 1);
-        double x[V];
-#pragma unroll
-        for (int l = 0; l < V / 2; ++l) {
-            x[2 * l] = an[l];
-            x[2 * l + 1] = ad[l];
+    lds_barrier();
+    // columns added in a fixed order: G segments of T / G columns per value,
+    // then the G segment sums
+    const int G = T >= nv ? T / nv : 1;
+    const int seg = T / G;
+    double *segsum = acc + (size_t)nv * TP;   // [G][nv]
+    for (int idx = threadIdx.x; idx < nv * G; idx += T) {
+        const int val = idx % nv, g = idx / nv;
+        const double *col = acc + (size_t)val * TP + g * seg;
+        double s0 = 0.0, s1 = 0.0;
+        for (int c = 0; c < seg; c += 2) {
+            s0 += col[c];
+            s1 += col[c + 1];
         }
-        int idx;
-        const double sum = wave_transpose_sum<V>(x, lane, &idx);
-        if ((lane & (kWave / V - 1)) == 0) red[wave * V + idx] = sum;
-        __syncthreads();
-        if (threadIdx.x < 2 * NL) {
-            double sum = 0.0;
-            for (int wv = 0; wv < nwaves; ++wv) sum += red[wv * 2 * NL + threadIdx.x];
-            leaf_partial[(size_t)blockIdx.x * 2 * nleaf + threadIdx.x] = sum;
-        }
-    } else {
-        __syncthreads();
-        for (int t = threadIdx.x; t < 2 * nleaf; t += blockDim.x)
-            leaf_partial[(size_t)blockIdx.x * 2 * nleaf + t] = acc[t];
+        segsum[g * nv + val] = s0 + s1;
+    }
+    lds_barrier();
+    for (int val = threadIdx.x; val < nv; val += T) {
+        double sum = 0.0;
+        for (int g = 0; g < G; ++g) sum += segsum[g * nv + val];
+        leaf_partial[(size_t)blockIdx.x * nv + val] = sum;
     }
     if (eflag) atomicOr(err, eflag);
 }
@@ -1495,7 +1544,12 @@ hipError_t allow_hist_lds(size_t max_lds) {
 hipError_t prepare_kernels(size_t max_lds) {
     const hipError_t e[] = {allow_hist_lds<1>(max_lds), allow_hist_lds<2>(max_lds),
                             allow_hist_lds<4>(max_lds), allow_hist_lds<5>(max_lds),
-                            allow_hist_lds<8>(max_lds), allow_lds(apply_kernel, max_lds)};
+                            allow_hist_lds<8>(max_lds), allow_lds(apply_kernel, max_lds),
+                            allow_lds(leaf_kernel<false, 0>, max_lds),
+                            allow_lds(leaf_kernel<true, 0>, max_lds),
+                            allow_lds(leaf_kernel<true, 1>, max_lds),
+                            allow_lds(leaf_kernel<true, 2>, max_lds),
+                            allow_lds(leaf_kernel<true, 4>, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -1524,11 +1578,11 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
                             const uint8_t *leaf_node, const double *leaf_prev,
                             const double *leaf_partial, int lblocks, double eta, double *leaf_rec,
                             int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
-                            double *score_out, int cu_count, hipStream_t s) {
+                            double *yts, double *score_out, int cu_count, hipStream_t s) {
     if (leaf_partial && depth > kFusedLeafDepth) return hipErrorInvalidValue;
     tree_prep_kernel<<<grid_for(n, kLeafReduceThreads, cu_count), kLeafReduceThreads, 0, s>>>(
         y, v, F, f0, leaf_node, leaf_prev, leaf_partial, lblocks, eta, leaf_rec, depth, n, seed,
-        tree, alpha, w, score_out);
+        tree, alpha, w, yts, score_out);
     return hipGetLastError();
 }
 
@@ -1717,49 +1771,39 @@ hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int 
     return hipGetLastError();
 }
 
-int leaf_blocks(int64_t n, int cu_count) { return grid_for(n, 1024, cu_count); }
-
-template <bool ROUTED, int NL>
-void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
-             const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
-             const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
-             double alpha, double *leaf_partial, int *err) {
-    leaf_kernel<ROUTED, NL><<<blocks, 1024, 0, s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain,
-                                                   pc.cand_cut, pc.slices, pc.rec_f, pc.rec_c,
-                                                   pc.rec_g,
-                                                   depth, y, v, F, seed, tree, alpha,
-                                                   leaf_partial, err);
+int leaf_blocks(int64_t n, int depth, int cu_count) {
+    return grid_for((n + kLeafE - 1) / kLeafE, leaf_threads(depth), cu_count);
 }
 
-template <bool ROUTED>
-void leaf_dispatch(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
-                   const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
-                   const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
-                   double alpha, double *leaf_partial, int *err) {
-#define FBDT_LEAF_CASE(NLV)                                                                      \
-    leaf_go<ROUTED, NLV>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, y, v, F, seed,  \
-                         tree, alpha, leaf_partial, err)
-    switch (depth) {
-    case 1: FBDT_LEAF_CASE(2); break;
-    case 2: FBDT_LEAF_CASE(4); break;
-    case 3: FBDT_LEAF_CASE(8); break;
-    case 4: FBDT_LEAF_CASE(16); break;
-    default: FBDT_LEAF_CASE(0); break;
-    }
-#undef FBDT_LEAF_CASE
+size_t leaf_lds_bytes(int depth) {
+    const size_t T = (size_t)leaf_threads(depth), nv = (size_t)2 << depth;
+    return (nv * (T + 1) + (T >= nv ? T : nv)) * sizeof(double);
+}
+
+template <bool ROUTED, int NP>
+void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
+             const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
+             const float *v, const double *yts, double *leaf_partial, int *err) {
+    leaf_kernel<ROUTED, NP><<<blocks, leaf_threads(depth), leaf_lds_bytes(depth), s>>>(
+        xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut, pc.slices, pc.rec_f,
+        pc.rec_c, pc.rec_g, depth, v, yts, leaf_partial, err);
 }
 
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
                        uint8_t *node_out, const ParentCuts &pc, int depth, bool routed,
-                       const int8_t *y, const float *v, const double *F, uint64_t seed, int tree,
-                       double alpha, int blocks, double *leaf_partial, int *err, hipStream_t s) {
-    const ParentCuts none{};
-    if (routed)
-        leaf_dispatch<true>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, y, v, F, seed,
-                            tree, alpha, leaf_partial, err);
-    else
-        leaf_dispatch<false>(blocks, s, xb, ldb, n, d, node_in, nullptr, none, depth, y, v, F,
-                             seed, tree, alpha, leaf_partial, err);
+                       const float *v, const double *yts, int blocks, double *leaf_partial,
+                       int *err, hipStream_t s) {
+    if (!routed) {
+        leaf_go<false, 0>(blocks, s, xb, ldb, n, d, node_in, nullptr, ParentCuts{}, depth, v, yts,
+                          leaf_partial, err);
+    } else {
+        switch (1 << (depth - 1)) {   // parents of the leaves
+        case 1: leaf_go<true, 1>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
+        case 2: leaf_go<true, 2>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
+        case 4: leaf_go<true, 4>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
+        default: leaf_go<true, 0>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
+        }
+    }
     return hipGetLastError();
 }
 
