@@ -25,8 +25,10 @@ struct HistShape {
     int feature_groups;       // ceil(d / features_per_group)
     int nodes_per_group;      // nodes whose histograms one workgroup keeps in LDS
     int node_groups;          // ceil(2^layer / nodes_per_group)
-    int chunks;               // event chunks, each merged once per layer
+    int chunks;               // event chunks, each merged once per layer: the same number
+                              // in each XCD's event range (a multiple of kXcds)
     int64_t chunk_events;     // events per chunk (a multiple of kHistE = 8)
+    int64_t xcd_events;       // events of an XCD's range, xcd_range(n)
     int threads;              // threads per workgroup
     int blocks;               // grid size (chunks * groups, rounded up to the XCD count)
     size_t lds_bytes;         // dynamic LDS per workgroup
@@ -57,6 +59,13 @@ struct FitBuffers {
 };
 
 constexpr int kXcds = 8;            // gfx950: 8 XCDs, workgroups dispatched round-robin
+constexpr int kXcdQuantum = 64;     // XCD event ranges are whole multiples of this
+
+// Every per-event pass of a fit gives the events [x R, min(n, (x + 1) R)),
+// R = xcd_range(n), to workgroups on XCD x (workgroup b runs on XCD b % 8),
+// so that the per-event arrays one pass writes stay in that XCD's L2 for the
+// next pass: R = ceil(n / 8) rounded up to kXcdQuantum.
+int64_t xcd_range(int64_t n);
 constexpr int kValidateBlocks = 256;
 // LDS kept aside for a kernel's static shared arrays when sizing its
 // dynamic LDS (the histogram kernel's cut table takes 128 bytes)

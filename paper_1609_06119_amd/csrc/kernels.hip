@@ -250,14 +250,17 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     const double *__restrict__ leaf_prev, const double *__restrict__ leaf_partial,
     int lblocks, double eta, double *__restrict__ leaf_rec, int depth, int64_t n,
     uint64_t seed, int tree, double alpha, float *__restrict__ w, double *__restrict__ yts,
-    double *__restrict__ score_out) {
+    double *__restrict__ score_out, int64_t xcd_events) {
     __shared__ double red[kLeafReduceThreads];
     __shared__ double s_leaf[128];
     const unsigned nleaf = 1u << depth;
     const bool have_leaf = leaf_prev || leaf_partial;
     const bool read_F = have_leaf || !f0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t ia = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
+    const int64_t xlo = (int64_t)(blockIdx.x % kXcds) * xcd_events;
+    const int64_t xend = min(n, xlo + xcd_events);
+    const int64_t stride = (int64_t)(gridDim.x / kXcds) * blockDim.x;
+    int64_t ia = xlo + (int64_t)(blockIdx.x / kXcds) * blockDim.x + threadIdx.x;
     // one event per thread and step; the first step's loads are in flight
     // while the boost weights are summed, later steps are loaded one ahead
     const bool need_sample = w || yts;
@@ -269,7 +272,7 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
         st.sampled = need_sample && in_subsample(seed, tree, n, i, alpha);
     };
     PrepStep A, B;
-    if (ia < n) load(A, ia);
+    if (ia < xend) load(A, ia);
     if (leaf_partial) {
         reduce_leaf_partials(leaf_partial, lblocks, (int)nleaf, eta, red, s_leaf);
         if (blockIdx.x == 0 && leaf_rec && threadIdx.x < nleaf) leaf_rec[threadIdx.x] = s_leaf[threadIdx.x];
@@ -304,16 +307,16 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
             if (yts) yts[i] = sampled ? yt : 0.0;
         }
     };
-    if (ia < n) {
+    if (ia < xend) {
         for (;;) {
             const int64_t ib = ia + stride;
-            if (ib < n) load(B, ib);
+            if (ib < xend) load(B, ib);
             step(A, ia);
-            if (ib >= n) break;
+            if (ib >= xend) break;
             ia = ib + stride;
-            if (ia < n) load(A, ia);
+            if (ia < xend) load(A, ia);
             step(B, ib);
-            if (ia >= n) break;
+            if (ia >= xend) break;
         }
     }
 }
@@ -657,8 +660,8 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const float *__restrict__ w, const double *__restrict__ cand_gain,
     const int *__restrict__ cand_cut, int cslices, uint8_t *__restrict__ rec_f,
     uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, int G, int npg, int NG,
-    int chunks, int64_t chunk_events, int scale, uint64_t *__restrict__ partial,
-    double *__restrict__ small, int *__restrict__ err) {
+    int chunks, int64_t chunk_events, int64_t xcd_events, int scale,
+    uint64_t *__restrict__ partial, double *__restrict__ small, int *__restrict__ err) {
     extern __shared__ uint64_t lds[];
     __shared__ uint8_t s_cf[64], s_cc[64];
 
@@ -700,8 +703,12 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const int nwaves = blockDim.x / kWave;
     int eflag = 0;
 
-    const int64_t start = (int64_t)p * chunk_events;
-    const int64_t end = min(n, start + chunk_events);
+    // chunk p is chunk k of XCD x's event range [x R, (x + 1) R) (the range
+    // every per-event pass of the fit gives that XCD)
+    const int cpx = chunks / kXcds;
+    const int64_t xlo = (int64_t)(p / cpx) * xcd_events;
+    const int64_t start = xlo + (int64_t)(p % cpx) * chunk_events;
+    const int64_t end = min(min(n, xlo + xcd_events), start + chunk_events);
     const bool writer = ROUTED && layer >= 1 && g == 0 && h == 0 && node_out != nullptr;
     const int64_t stride = (int64_t)kHistE * blockDim.x;
 
@@ -1236,7 +1243,7 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
     int depth, const float *__restrict__ v, const double *__restrict__ yts,
-    double *__restrict__ leaf_partial, int *__restrict__ err) {
+    double *__restrict__ leaf_partial, int *__restrict__ err, int64_t xcd_events) {
 #pragma clang fp contract(off)
     extern __shared__ double acc[];   // [2 nleaf][T + 1], then the segment sums
     __shared__ uint8_t s_cf[64], s_cc[64];
@@ -1248,15 +1255,18 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     const int wave = threadIdx.x / kWave;
     const int nwaves = T / kWave;
     int eflag = 0;
-    const int64_t stride = (int64_t)gridDim.x * T * kLeafE;
-    int64_t ia = ((int64_t)blockIdx.x * T + threadIdx.x) * kLeafE;
+    // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
+    const int64_t xlo = (int64_t)(blockIdx.x % kXcds) * xcd_events;
+    const int64_t xend = min(n, xlo + xcd_events);
+    const int64_t stride = (int64_t)(gridDim.x / kXcds) * T * kLeafE;
+    int64_t ia = xlo + ((int64_t)(blockIdx.x / kXcds) * T + threadIdx.x) * kLeafE;
 
     CandRegs cr;
     const CandSet cs{cand_gain, cand_cut, d, cslices};
     const bool pwave = ROUTED && wave < half;
     if (pwave) cand_load(cs, wave, lane, cr);
     LeafStep<NP> A, B;
-    if (ia < n) leaf_load<ROUTED, NP>(A, xb, ldb, d, node_in, v, yts, s_cf, ia, false);
+    if (ia < xend) leaf_load<ROUTED, NP>(A, xb, ldb, d, node_in, v, yts, s_cf, ia, false);
     const int TP = T + 1;   // row stride: rows start two LDS banks apart
     for (int t = threadIdx.x; t < nv * TP; t += T) acc[t] = 0.0;
     if (ROUTED) {
@@ -1337,16 +1347,16 @@ __global__ __launch_bounds__(256) void leaf_kernel(
         // padded events get leaf ids too (the arrays hold whole steps)
         if (ROUTED) *reinterpret_cast<uint2 *>(node_out + i0) = make_uint2(o[0], o[1]);
     };
-    if (ia < n) {
+    if (ia < xend) {
         leaf_load_rows<ROUTED, NP>(A, xb, ldb, d, s_cf, ia);
         for (;;) {
             const int64_t ib = ia + stride;
-            const bool more_b = ib < n;
+            const bool more_b = ib < xend;
             leaf_load<ROUTED, NP>(B, xb, ldb, d, node_in, v, yts, s_cf, more_b ? ib : ia, true);
             add(A, ia);
             if (!more_b) break;
             ia = ib + stride;
-            const bool more_a = ia < n;
+            const bool more_a = ia < xend;
             leaf_load<ROUTED, NP>(A, xb, ldb, d, node_in, v, yts, s_cf, more_a ? ia : ib, true);
             add(B, ib);
             if (!more_a) break;
@@ -1509,6 +1519,25 @@ __global__ __launch_bounds__(256) void encode_kernel(const float *__restrict__ x
     if (eflag) atomicOr(err, eflag);
 }
 
+}  // namespace
+
+int64_t xcd_range(int64_t n) {
+    const int64_t r = (n + kXcds - 1) / kXcds;
+    return (r + kXcdQuantum - 1) / kXcdQuantum * kXcdQuantum;
+}
+
+namespace {
+
+// Workgroups of a per-event pass: the same number on each XCD (a multiple
+// of kXcds), at most one round of cu_count, as many as the XCD range needs.
+int xcd_grid(int64_t n, int64_t events_per_block, int cu_count) {
+    int64_t per = (xcd_range(n) + events_per_block - 1) / events_per_block;
+    const int64_t cap = cu_count / kXcds > 0 ? cu_count / kXcds : 1;
+    if (per > cap) per = cap;
+    if (per < 1) per = 1;
+    return (int)(kXcds * per);
+}
+
 int grid_for(int64_t n, int threads, int cap) {
     int64_t g = (n + threads - 1) / threads;
     if (g < 1) g = 1;
@@ -1580,9 +1609,9 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
                             int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
                             double *yts, double *score_out, int cu_count, hipStream_t s) {
     if (leaf_partial && depth > kFusedLeafDepth) return hipErrorInvalidValue;
-    tree_prep_kernel<<<grid_for(n, kLeafReduceThreads, cu_count), kLeafReduceThreads, 0, s>>>(
+    tree_prep_kernel<<<xcd_grid(n, kLeafReduceThreads, cu_count), kLeafReduceThreads, 0, s>>>(
         y, v, F, f0, leaf_node, leaf_prev, leaf_partial, lblocks, eta, leaf_rec, depth, n, seed,
-        tree, alpha, w, yts, score_out);
+        tree, alpha, w, yts, score_out, xcd_range(n));
     return hipGetLastError();
 }
 
@@ -1609,7 +1638,7 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     // Features per workgroup, one of kHistFpgSizes.  A 1024-thread
     // workgroup fills a CU, so the pass runs as one round of at most
     // cu_count workgroups: groups * chunks with chunks <= cu_count / groups
-    // and at least one full step (kHistE events) per thread.  Among the
+    // and at least half a step of events (kHistE per thread) per chunk.  Among the
     // sizes whose launch fills at least 95% of the most workgroups any size
     // reaches, take the largest: every feature group repeats the per-event
     // work (weights, routing) of its chunk.
@@ -1619,16 +1648,17 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     if (fpg > 0) {
         f = fpg;
     } else {
-        const int64_t cmax = n / min_events > 0 ? n / min_events : 1;
+        const int64_t R = xcd_range(n);
+        const int64_t c8max = R / (min_events / 2) > 0 ? R / (min_events / 2) : 1;
         int64_t wgs_of[kHistFMax + 1] = {0};
         int64_t most = 0;
         for (int cand : kHistFpgSizes) {
             if ((size_t)npg * cand * per_node_feature > max_lds) continue;
             const int g = ((d + cand - 1) / cand) * hs.node_groups;
-            int64_t c = cu_count / g;
-            if (c > cmax) c = cmax;
-            if (c < 1) c = 1;
-            wgs_of[cand] = c * g;
+            int64_t c8 = cu_count / kXcds / g;
+            if (c8 > c8max) c8 = c8max;
+            if (c8 < 1) c8 = 1;
+            wgs_of[cand] = kXcds * c8 * g;
             if (wgs_of[cand] > most) most = wgs_of[cand];
         }
         for (int cand : kHistFpgSizes)
@@ -1641,20 +1671,25 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     hs.feature_groups = (d + f - 1) / f;
     hs.threads = t_threads;
     const int groups = hs.feature_groups * hs.node_groups;
-    // at most one workgroup per CU by default (a 1024-thread workgroup fills
-    // a CU): a few workgroups more than CUs run as a second round and nearly
-    // double the pass; every extra event chunk also adds one more partial
-    // histogram to write and to sum
-    int64_t c = chunks > 0 ? chunks : (int64_t)cu_count / groups;
-    const int64_t cmax = (n + min_events - 1) / min_events;
-    if (chunks <= 0 && c > cmax) c = cmax;
-    if (c < 1) c = 1;
-    int64_t ce = (n + c - 1) / c;
+    // Chunks: the same number in each XCD's event range [x R, (x + 1) R), so
+    // that the workgroups of a chunk, which the launch places on that XCD,
+    // read event data that the fit's other per-event passes wrote there (it
+    // stays in the XCD's L2 across kernels).  At most one workgroup per CU
+    // by default (a 1024-thread workgroup fills a CU): a few workgroups more
+    // than CUs run as a second round and nearly double the pass; every extra
+    // event chunk also adds one more partial histogram to write and to sum.
+    const int64_t R = xcd_range(n);
+    int64_t c8 = chunks > 0 ? (chunks + kXcds - 1) / kXcds : (int64_t)cu_count / kXcds / groups;
+    const int64_t c8max = R / (min_events / 2) > 0 ? R / (min_events / 2) : 1;
+    if (chunks <= 0 && c8 > c8max) c8 = c8max;
+    if (c8 < 1) c8 = 1;
+    int64_t ce = (R + c8 - 1) / c8;
     ce = (ce + kHistE - 1) / kHistE * kHistE;
+    c8 = (R + ce - 1) / ce;
     hs.chunk_events = ce;
-    hs.chunks = (int)((n + ce - 1) / ce);
-    const int64_t work = (int64_t)hs.chunks * groups;
-    hs.blocks = (int)((work + kXcds - 1) / kXcds * kXcds);
+    hs.xcd_events = R;
+    hs.chunks = (int)(kXcds * c8);
+    hs.blocks = hs.chunks * groups;
     hs.lds_bytes = (size_t)npg * f * per_node_feature;
     return hs;
 }
@@ -1677,7 +1712,7 @@ hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, i
     hist_kernel<ROUTED, NP, FPG><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.slices,
         pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
-        hs.chunks, hs.chunk_events, scale, partial, small, err);
+        hs.chunks, hs.chunk_events, hs.xcd_events, scale, partial, small, err);
     return hipGetLastError();
 }
 
@@ -1772,7 +1807,7 @@ hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int 
 }
 
 int leaf_blocks(int64_t n, int depth, int cu_count) {
-    return grid_for((n + kLeafE - 1) / kLeafE, leaf_threads(depth), cu_count);
+    return xcd_grid(n, (int64_t)kLeafE * leaf_threads(depth), cu_count);
 }
 
 size_t leaf_lds_bytes(int depth) {
@@ -1786,7 +1821,7 @@ void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t 
              const float *v, const double *yts, double *leaf_partial, int *err) {
     leaf_kernel<ROUTED, NP><<<blocks, leaf_threads(depth), leaf_lds_bytes(depth), s>>>(
         xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut, pc.slices, pc.rec_f,
-        pc.rec_c, pc.rec_g, depth, v, yts, leaf_partial, err);
+        pc.rec_c, pc.rec_g, depth, v, yts, leaf_partial, err, xcd_range(n));
 }
 
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
