@@ -56,10 +56,59 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--cpu-trees", type=int, default=100,
                     help="trees of the CPU-oracle baseline sample")
+    ap.add_argument("--apply-events", type=int, default=50_000_000,
+                    help="fresh events of the apply workload (0 skips it)")
+    ap.add_argument("--apply-steps", type=int, default=3,
+                    help="timed applies of the 400-tree forest to the fresh events")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this size on the device three "
                          "times (reference kernel for hardware byte counters)")
     return ap.parse_args()
+
+
+def measure_apply_workload(args, apply_x, fb, torch):
+    """Workload 5: a 400-tree depth-3 forest fitted on workload 3's 2M x 40
+    sample (256 bins), applied to the fresh events (binned with the training
+    boundaries, chunk by chunk, into one code buffer).  Returns events/s of
+    fbdt_apply from HIP events around each timed launch."""
+    from synth import CONFIGS, make_training_set
+    s3, s5 = CONFIGS[3], CONFIGS[5]
+    t0 = time.time()
+    ds = make_training_set(3)
+    x3 = torch.from_numpy(ds["x"]).cuda()
+    y3 = torch.from_numpy(ds["y"]).cuda()
+    bounds, codes3 = fb.bin(x3, s5.n_bins)
+    del x3
+    model = fb.fit(codes3, y3, s5.n_bins, s5.depth, s5.n_trees, s5.shrinkage, s5.subsample,
+                   s5.fit_seed)
+    torch.cuda.synchronize()
+    fit_s = time.time() - t0
+    n = sum(x.shape[1] for _, x in apply_x)
+    d = apply_x[0][1].shape[0]
+    codes = fb.Codes.empty(d, n)
+    for off, x in apply_x:
+        m = x.shape[1]
+        part = fb.bin_transform(torch.from_numpy(x).cuda(), bounds)
+        codes.data[:, off:off + m].copy_(part.data[:, :m])
+    del part
+    prob = torch.empty(n, dtype=torch.float32, device="cuda")
+    fb.apply(model, codes, prob=prob)   # warm-up
+    torch.cuda.synchronize()
+    fb.timing_enable(("apply",))
+    for _ in range(max(1, args.apply_steps)):
+        fb.apply(model, codes, prob=prob)
+    torch.cuda.synchronize()
+    launches, ms, _ = fb.timing_read("apply")
+    fb.timing_enable(())
+    mean_ms = ms / max(launches, 1)
+    return {"events_per_s": n / (mean_ms / 1e3), "launches": launches,
+            "mean_launch_us": mean_ms * 1e3,
+            "bytes_per_event": d + 4,
+            "hbm_gbs": n * (d + 4) / (mean_ms / 1e3) / 1e9,
+            "workload": f"{s5.n_trees}-tree depth-{s5.depth} forest fitted on workload 3 "
+                        f"({s3.n_events} x {s3.n_features}, {s5.n_bins} bins) applied to {n} "
+                        f"fresh events x {d} uint8 codes; prob float32 out",
+            "setup_s": round(fit_s, 1)}
 
 
 def main():
@@ -70,10 +119,20 @@ def main():
         sys.exit(2)
 
     import numpy as np
+    from synth import CONFIGS, apply_chunks, digest, make_training_set
+
+    # The apply workload's fresh events are drawn first, in worker processes,
+    # before this process touches the GPU.
+    apply_x = []
+    if args.apply_events > 0:
+        t0 = time.time()
+        apply_x = list(apply_chunks(args.apply_events, workers=16))
+        print(f"# apply workload: {args.apply_events} fresh events drawn in "
+              f"{time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
     import torch
 
     import paper_1609_06119_amd as fb
-    from synth import CONFIGS, digest, make_training_set
 
     spec = CONFIGS[2]
     t0 = time.time()
@@ -135,6 +194,12 @@ def main():
     cpu_s = time.perf_counter() - tc
     cpu_value = n * d * D * cpu_T / cpu_s
 
+    apply_out = {"events_per_s": apply_events_per_s, "launches": a_launches,
+                 "mean_launch_us": a_ms * 1e3 / max(a_launches, 1),
+                 "workload": f"{n} binned events x {T} trees of depth {D} (the step's apply)"}
+    if apply_x:
+        apply_out = measure_apply_workload(args, apply_x, fb, torch)
+
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20
         src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
@@ -177,9 +242,7 @@ def main():
             "mean_launch_us": hist_avg_ms * 1e3,
             "algorithmic_bytes_per_launch": hist_avg_bytes,
         },
-        "apply": {"events_per_s": apply_events_per_s, "launches": a_launches,
-                  "mean_launch_us": a_ms * 1e3 / max(a_launches, 1),
-                  "workload": "500k binned events x 100 trees of depth 3"},
+        "apply": apply_out,
         "bin_ms": bin_ms,
         "cpu_baseline": {
             "value": cpu_value,

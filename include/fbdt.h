@@ -13,7 +13,8 @@
  *    stride ldx is x[j * ldx + i]; binned codes use row stride ldb.
  *    ldb must be a multiple of 16, ldb >= n, and the code buffer must be
  *    16-byte aligned and hold d * ldb bytes.  Bytes of a row beyond n are
- *    read but never influence a result.
+ *    read but never influence a result; the binning calls write the first n
+ *    bytes of each row only.
  *  - Labels are int8: +1 signal, -1 background (section 1).  Weights are
  *    float32, finite and >= 0; NULL means unit weights.
  *  - stream is a hipStream_t (NULL = the null stream).  Calls are

@@ -1493,26 +1493,25 @@ __global__ __launch_bounds__(256) void encode_kernel(const float *__restrict__ x
     for (int k = threadIdx.x; k < nb; k += blockDim.x) sb[k] = bounds[(size_t)j * nb + k];
     __syncthreads();
     int eflag = 0;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < ldb;
+    // the n codes of row j only: bytes of the row beyond n are not written
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
         uint8_t code = 0;
-        if (i < n) {
-            const float val = x[(int64_t)j * ldx + i];
-            if (val != val) {
-                eflag |= kErrNan;
-            } else {
-                int lo = 0, len = nb;
-                while (len > 0) {
-                    const int hh = len >> 1;
-                    if (sb[lo + hh] <= val) {
-                        lo += hh + 1;
-                        len -= hh + 1;
-                    } else {
-                        len = hh;
-                    }
+        const float val = x[(int64_t)j * ldx + i];
+        if (val != val) {
+            eflag |= kErrNan;
+        } else {
+            int lo = 0, len = nb;
+            while (len > 0) {
+                const int hh = len >> 1;
+                if (sb[lo + hh] <= val) {
+                    lo += hh + 1;
+                    len -= hh + 1;
+                } else {
+                    len = hh;
                 }
-                code = (uint8_t)lo;
             }
+            code = (uint8_t)lo;
         }
         xb[(int64_t)j * ldb + i] = code;
     }
@@ -1893,7 +1892,7 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
 
 hipError_t launch_encode(const float *x, int64_t ldx, int64_t n, int d, const float *bounds,
                          int n_bins, uint8_t *xb, int64_t ldb, int *err, hipStream_t s) {
-    dim3 grid(grid_for(ldb, 256, 1024), d);
+    dim3 grid(grid_for(n, 256, 1024), d);
     encode_kernel<<<grid, 256, 0, s>>>(x, ldx, n, d, bounds, n_bins, xb, ldb, err);
     return hipGetLastError();
 }

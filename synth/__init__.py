@@ -10,6 +10,7 @@ from .generators import (  # noqa: F401
     ConfigSpec,
     make_training_set,
     make_apply_chunk,
+    apply_chunks,
     random_forest,
     random_binned,
     digest,

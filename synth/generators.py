@@ -177,6 +177,34 @@ def make_apply_chunk(chunk_index: int, chunk_events: int, cfg: int = 5):
     return {"x": x, "y": y}
 
 
+def _apply_chunk_x(args):
+    cfg, index, m = args
+    return make_apply_chunk(index, m, cfg)["x"]
+
+
+def apply_chunks(n_events: int, chunk_events: int = 1_000_000, cfg: int = 5, workers: int = 16):
+    """The first ``n_events`` fresh events of the apply workload as a stream.
+
+    Yields ``(offset, x)`` in event order, ``x`` float32 [d][m] being chunk
+    ``offset // chunk_events`` (the last one shortened), each drawn from its own
+    seed exactly as ``make_apply_chunk`` draws it, with up to ``workers``
+    processes drawing chunks ahead of the consumer.
+    """
+    import multiprocessing as mp
+
+    n_chunks = (int(n_events) + chunk_events - 1) // chunk_events
+    sizes = [min(chunk_events, int(n_events) - k * chunk_events) for k in range(n_chunks)]
+    jobs = [(cfg, k, sizes[k]) for k in range(n_chunks)]
+    if workers <= 1 or n_chunks <= 1:
+        for k, job in enumerate(jobs):
+            yield k * chunk_events, _apply_chunk_x(job)
+        return
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(min(workers, n_chunks)) as pool:
+        for k, x in enumerate(pool.imap(_apply_chunk_x, jobs)):
+            yield k * chunk_events, x
+
+
 def random_binned(n: int, d: int, n_bins: int, seed: int, signal_fraction: float = 0.5):
     """Uniform random bin codes, labels and positive weights for unit tests."""
     rng = np.random.default_rng(seed)

@@ -69,12 +69,15 @@ def _bin_cases():
 def test_bin_matches_oracle(case):
     name, x, B = _bin_cases()[case]
     say(f"bin parity: {name} d={x.shape[0]} n={x.shape[1]} B={B}")
-    bounds, codes = fb.bin(dev(x), B)
+    d, n = x.shape
+    # binning writes the first n codes of each row only: padding keeps its bytes
+    pre = torch.full((d, fb.padded_stride(n)), 0xAB, dtype=torch.uint8, device="cuda")
+    bounds, codes = fb.bin(dev(x), B, codes=fb.Codes(pre, n))
     ob, oc = O.bin_features(x, B)
     assert np.array_equal(bounds, ob)
     assert np.array_equal(codes.numpy(), oc)
     pad = codes.data[:, codes.n:].cpu().numpy()
-    assert not pad.any()
+    assert (pad == 0xAB).all()
 
 
 def test_bin_with_row_stride_and_transform():
@@ -392,6 +395,44 @@ def test_apply_random_forest_matches_oracle(T, D, d, n):
     assert np.array_equal(score.cpu().numpy(), oF)     # same leaves, same order
     assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
     np.testing.assert_array_max_ulp(p, op, maxulp=1)
+
+
+def test_apply_workload5_launch_configuration_matches_oracle():
+    """Workload 5's apply path at its launch configuration (every n >= 524k
+    events takes the grid bench.py times on 50M): fresh events from the
+    correlated distribution, binned with workload 3's training boundaries on
+    both sides, then a seeded 400-tree depth-3 forest over the 40 features;
+    all events compared on codes, the first 200k on scores and probabilities."""
+    s3, s5 = CONFIGS[3], CONFIGS[5]
+    B, D, T = s5.n_bins, s5.depth, s5.n_trees
+    say("workload 5: training boundaries (workload 3, 2M x 40)")
+    ds = make_training_set(3)
+    d = ds["x"].shape[0]
+    gb, _ = fb.bin(dev(ds["x"]), B)
+    ob = np.stack([O.quantile_boundaries(ds["x"][j], B) for j in range(d)])
+    assert np.array_equal(gb, ob)
+    del ds
+    n = 1_200_003
+    say(f"workload 5: {n} fresh events")
+    x = make_apply_chunk(7, n)["x"]
+    codes = fb.bin_transform(dev(x), ob)
+    xb = np.stack([O.encode(x[j], ob[j]) for j in range(d)]).astype(np.uint8)
+    assert np.array_equal(codes.numpy(), xb)
+    f = random_forest(T, D, d, B, seed=5)
+    model = fb.Model.from_arrays(f["cut_feature"], f["cut_bin"], f["leaf"], f["f0"], d, B)
+    score = torch.empty(n, dtype=torch.float64, device="cuda")
+    p = fb.apply(model, codes, score=score)
+    m = 200_000
+    om = O.Model(D, B, d, f["f0"], f["cut_feature"], f["cut_bin"], np.zeros_like(f["leaf"][:, 1:]),
+                 f["leaf"])
+    say(f"workload 5: oracle apply of the first {m} events")
+    op, oF = O.apply(om, xb[:, :m])
+    assert np.array_equal(score[:m].cpu().numpy(), oF)
+    pg = p[:m].cpu().numpy()
+    assert np.max(np.abs(pg.astype(np.float64) - op)) <= 1e-5
+    np.testing.assert_array_max_ulp(pg, op, maxulp=1)
+    pa = p.cpu().numpy()
+    assert np.all((pa > 0.0) & (pa < 1.0))
 
 
 # ------------------------------------------------------------------ errors
