@@ -30,6 +30,8 @@ struct fbdt_model {
         int device;
         uint16_t *cuts;
         double *leaves;
+        int nodes_stride;   // tile stride the node records were made for (0: none)
+        uint32_t *nodes;    // [T][16] node records of shallow forests, or null
     };
     std::mutex mu;
     std::vector<DeviceCopy> copies;
@@ -719,6 +721,7 @@ void fbdt_model_free(fbdt_model *m) {
         if (hipSetDevice(c.device) == hipSuccess) {
             (void)hipFree(c.cuts);
             (void)hipFree(c.leaves);
+            if (c.nodes) (void)hipFree(c.nodes);
         }
     }
     if (cur >= 0) (void)hipSetDevice(cur);
@@ -741,38 +744,57 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = m->n_trees, D = m->depth;
     const size_t nin = ((size_t)1 << D) - 1, nleaf = (size_t)1 << D;
-    uint16_t *cuts = nullptr;
-    double *leaves = nullptr;
-    {
-        std::lock_guard<std::mutex> lk(m->mu);
-        for (auto &c : m->copies)
-            if (c.device == dev) {
-                cuts = c.cuts;
-                leaves = c.leaves;
-            }
-        if (!cuts) {
-            std::vector<uint16_t> packed((size_t)T * nin);
-            for (size_t k = 0; k < packed.size(); ++k)
-                packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
-            HIP_TRY(hipMalloc(&cuts, packed.size() * sizeof(uint16_t)));
-            if (hipMalloc(&leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
-                (void)hipFree(cuts);
-                return fail(FBDT_E_DEVICE, "out of device memory");
-            }
-            HIP_TRY(hipMemcpy(cuts, packed.data(), packed.size() * sizeof(uint16_t),
-                              hipMemcpyHostToDevice));
-            HIP_TRY(hipMemcpy(leaves, m->leaf.data(), (size_t)T * nleaf * sizeof(double),
-                              hipMemcpyHostToDevice));
-            m->copies.push_back({dev, cuts, leaves});
-        }
-    }
     ApplyShape as = plan_apply(n, m->n_features, T, D, di.cu_count, di.max_lds,
                                (int)opt_apply_threads.load());
     if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
         return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
                     "apply_threads)", as.lds_bytes, di.max_lds);
+    uint16_t *cuts = nullptr;
+    uint32_t *nodes = nullptr;
+    double *leaves = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(m->mu);
+        fbdt_model::DeviceCopy *copy = nullptr;
+        for (auto &c : m->copies)
+            if (c.device == dev) copy = &c;
+        if (!copy) {
+            std::vector<uint16_t> packed((size_t)T * nin);
+            for (size_t k = 0; k < packed.size(); ++k)
+                packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
+            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr};
+            HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
+            if (hipMalloc(&c.leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
+                (void)hipFree(c.cuts);
+                return fail(FBDT_E_DEVICE, "out of device memory");
+            }
+            m->copies.push_back(c);
+            copy = &m->copies.back();
+            HIP_TRY(hipMemcpy(copy->cuts, packed.data(), packed.size() * sizeof(uint16_t),
+                              hipMemcpyHostToDevice));
+            HIP_TRY(hipMemcpy(copy->leaves, m->leaf.data(), (size_t)T * nleaf * sizeof(double),
+                              hipMemcpyHostToDevice));
+        }
+        if (as.shallow && copy->nodes_stride != apply_node_stride(as)) {
+            // node records for this launch's tile stride
+            const int xs = apply_node_stride(as);
+            std::vector<uint32_t> table((size_t)T * 16, 0u);
+            for (size_t t = 0; t < (size_t)T; ++t)
+                for (size_t k = 0; k < nin; ++k) {
+                    table[t * 16 + k] = (uint32_t)m->cut_feature[t * nin + k] * (uint32_t)xs;
+                    table[t * 16 + 8 + k] = (256u - m->cut_bin[t * nin + k]) * 0x10001u;
+                }
+            if (!copy->nodes)
+                HIP_TRY(hipMalloc(&copy->nodes, table.size() * sizeof(uint32_t)));
+            HIP_TRY(hipMemcpy(copy->nodes, table.data(), table.size() * sizeof(uint32_t),
+                              hipMemcpyHostToDevice));
+            copy->nodes_stride = xs;
+        }
+        cuts = copy->cuts;
+        nodes = copy->nodes;
+        leaves = copy->leaves;
+    }
     Timed tm(FBDT_K_APPLY, s, (double)n * (m->n_features + 4));
-    HIP_TRY(launch_apply(as, xb, ldb, n, cuts, leaves, T, D, m->f0, prob, score, s));
+    HIP_TRY(launch_apply(as, xb, ldb, n, cuts, nodes, leaves, T, D, m->f0, prob, score, s));
     tm.done();
     return FBDT_OK;
 }

@@ -205,19 +205,26 @@ hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_
                         const uint8_t *cut_f, const uint8_t *cut_c, int layer, int *err,
                         hipStream_t s);
 
-// Forest traversal.  cuts: [T][2^D-1] packed (feature | bin << 8).
+// Forest traversal.  cuts: [T][2^D-1] packed (feature | bin << 8), for the
+// general kernel; nodes: [T][16] for depth <= kApplyShallowDepth, for heap
+// node k + 1 word k = feature * apply_node_stride (the LDS row offset in the
+// launch's code tile) and word 8 + k = (256 - bin) * 0x10001.
+constexpr int kApplyShallowDepth = 3;
 struct ApplyShape {
+    bool shallow;          // depth <= kApplyShallowDepth: apply_shallow_kernel
     int threads;
     int blocks;
-    int trees_per_chunk;
+    int trees_per_chunk;   // trees whose leaf values (and cuts) are staged in LDS at once
     int d_used;
     size_t lds_bytes;
 };
 ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_count,
                       size_t max_lds, int threads);
+inline int apply_node_stride(const ApplyShape &as) { return 2 * as.threads + 8; }
 hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
-                        const uint16_t *cuts, const double *leaves, int n_trees, int depth,
-                        double f0, float *prob, double *score, hipStream_t s);
+                        const uint16_t *cuts, const uint32_t *nodes, const double *leaves,
+                        int n_trees, int depth, double f0, float *prob, double *score,
+                        hipStream_t s);
 
 hipError_t launch_encode(const float *x, int64_t ldx, int64_t n, int d, const float *bounds,
                          int n_bins, uint8_t *xb, int64_t ldb, int *err, hipStream_t s);

@@ -1482,6 +1482,140 @@ __global__ __launch_bounds__(1024) void apply_kernel(
 // Bin code of a float: number of boundaries <= value (upper bound by binary
 // search over the feature's boundaries in LDS).  Row padding [n, ldb) is
 // written as 0.
+// Forest traversal for depth <= 3 (the apply workload's forests).  Every
+// thread scores two adjacent events.  The 2^D - 1 cuts of a tree are uniform
+// across the workgroup, so they come as scalar loads of a per-tree record of
+// 16 words: for heap node k + 1, word k = the LDS offset of its feature's row
+// in the code tile (feature * XS) and word 8 + k = (256 - bin) * 0x10001.  All
+// cuts' codes of both events are read up front (one 16-bit LDS read per cut,
+// no chain from one level to the next); v_perm puts the two codes in the low
+// bytes of the two 16-bit halves, and adding word 8 + k sets bit 8 (first
+// event) and bit 24 (second event) exactly when code >= bin (right child).
+// The path is then bitfield selects on those words for both events at once,
+// and each reached leaf's value is one LDS read, added to F in tree order.
+// Leaf values of tpc trees at a time are staged in LDS (all of them when they
+// fit), the codes of a tile of 2 * blockDim events per feature (row stride XS
+// = 2 * blockDim + 8).
+constexpr int kApplyBatch = 4;
+
+// Leaf indices of the two events in a tree of depth D <= 3: the first in
+// bits 0..2, the second in bits 16..18.
+template <int D>
+__device__ __forceinline__ uint32_t shallow_leaf2(const uint8_t *xpair, const uint32_t *off,
+                                                  const uint32_t *add) {
+    constexpr int NIN = (1 << D) - 1;
+    uint32_t w[NIN];
+#pragma unroll
+    for (int k = 0; k < NIN; ++k) {
+        const uint32_t p = *reinterpret_cast<const uint16_t *>(xpair + off[k]);
+        w[k] = __builtin_amdgcn_perm(p, p, 0x0c010c00u) + add[k];
+    }
+    constexpr uint32_t kBits = 0x01000100u;   // the decision bits (8 and 24)
+    const uint32_t r1 = w[0];
+    if (D == 1) return (r1 & kBits) >> 8;
+    const uint32_t r2 = (r1 & w[2]) | (~r1 & w[1]);   // child of the root reached
+    if (D == 2) return ((r1 & kBits) >> 7) | ((r2 & kBits) >> 8);
+    const uint32_t t0 = (r2 & w[4]) | (~r2 & w[3]);
+    const uint32_t t1 = (r2 & w[6]) | (~r2 & w[5]);
+    const uint32_t r3 = (r1 & t1) | (~r1 & t0);
+    return ((r1 & kBits) >> 6) | ((r2 & kBits) >> 7) | ((r3 & kBits) >> 8);
+}
+
+template <int D>
+__global__ __launch_bounds__(1024) void apply_shallow_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d_used,
+    const uint32_t *__restrict__ nodes, const double *__restrict__ leaves, int T, int tpc,
+    double f0, float *__restrict__ prob, double *__restrict__ score) {
+    constexpr int NLEAF = 1 << D;
+    constexpr int NIN = (1 << D) - 1;
+    extern __shared__ double smem[];
+    double *s_leaf = smem;   // [tpc][NLEAF]
+    uint8_t *s_x = reinterpret_cast<uint8_t *>(s_leaf + (size_t)tpc * NLEAF);   // [d_used][XS]
+    const int tile_events = 2 * blockDim.x;
+    const int XS = tile_events + 8;   // the stride the node records were prepared for
+    const int nchunks = (T + tpc - 1) / tpc;
+    const int64_t ntiles = (n + tile_events - 1) / tile_events;
+    const uint8_t *xpair = s_x + 2 * threadIdx.x;
+    bool staged = false;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t i0 = tile * tile_events + 2 * threadIdx.x;   // this thread's events
+        __syncthreads();
+        for (int f = 0; f < d_used; ++f) {
+            const uint8_t *src = xb + (int64_t)f * ldb + i0;
+            uint16_t pair = 0;
+            if (i0 + 1 < n)
+                pair = *reinterpret_cast<const uint16_t *>(src);
+            else if (i0 < n)
+                pair = src[0];
+            *reinterpret_cast<uint16_t *>(s_x + f * XS + 2 * threadIdx.x) = pair;
+        }
+        double Fa = f0, Fb = f0;
+        for (int ch = 0; ch < nchunks; ++ch) {
+            const int t0 = ch * tpc;
+            const int tc = min(tpc, T - t0);
+            if (nchunks > 1 || !staged) {
+                __syncthreads();
+                for (int q = threadIdx.x; q < tc * NLEAF; q += blockDim.x)
+                    s_leaf[q] = leaves[(size_t)t0 * NLEAF + q];
+                staged = true;
+            }
+            __syncthreads();
+            // full batches of kApplyBatch trees: every load of the batch (node
+            // records, codes, leaf values) is issued before its results are
+            // used, then the leaf values are added in tree order
+            int t = 0;
+            for (; t + kApplyBatch <= tc; t += kApplyBatch) {
+                uint32_t off[kApplyBatch][NIN], add[kApplyBatch][NIN];
+#pragma unroll
+                for (int u = 0; u < kApplyBatch; ++u) {
+                    const uint32_t *nt = nodes + (size_t)(t0 + t + u) * 16;
+#pragma unroll
+                    for (int k = 0; k < NIN; ++k) {
+                        off[u][k] = nt[k];
+                        add[u][k] = nt[8 + k];
+                    }
+                }
+                uint32_t idx[kApplyBatch];
+#pragma unroll
+                for (int u = 0; u < kApplyBatch; ++u) idx[u] = shallow_leaf2<D>(xpair, off[u], add[u]);
+                double la[kApplyBatch], lb[kApplyBatch];
+#pragma unroll
+                for (int u = 0; u < kApplyBatch; ++u) {
+                    const double *lt = s_leaf + (t + u) * NLEAF;
+                    la[u] = lt[idx[u] & 0xffffu];
+                    lb[u] = lt[idx[u] >> 16];
+                }
+#pragma unroll
+                for (int u = 0; u < kApplyBatch; ++u) {
+                    Fa += la[u];
+                    Fb += lb[u];
+                }
+            }
+            for (; t < tc; ++t) {
+                const uint32_t *nt = nodes + (size_t)(t0 + t) * 16;
+                uint32_t off[NIN], add[NIN];
+#pragma unroll
+                for (int k = 0; k < NIN; ++k) {
+                    off[k] = nt[k];
+                    add[k] = nt[8 + k];
+                }
+                const uint32_t idx = shallow_leaf2<D>(xpair, off, add);
+                const double *lt = s_leaf + t * NLEAF;
+                Fa += lt[idx & 0xffffu];
+                Fb += lt[idx >> 16];
+            }
+        }
+        if (i0 < n) {
+            prob[i0] = (float)(1.0 / (1.0 + exp(-2.0 * Fa)));
+            if (score) score[i0] = Fa;
+        }
+        if (i0 + 1 < n) {
+            prob[i0 + 1] = (float)(1.0 / (1.0 + exp(-2.0 * Fb)));
+            if (score) score[i0 + 1] = Fb;
+        }
+    }
+}
+
 __global__ __launch_bounds__(256) void encode_kernel(const float *__restrict__ x, int64_t ldx,
                                                      int64_t n, int d,
                                                      const float *__restrict__ bounds, int nbins,
@@ -1577,7 +1711,10 @@ hipError_t prepare_kernels(size_t max_lds) {
                             allow_lds(leaf_kernel<true, 0>, max_lds),
                             allow_lds(leaf_kernel<true, 1>, max_lds),
                             allow_lds(leaf_kernel<true, 2>, max_lds),
-                            allow_lds(leaf_kernel<true, 4>, max_lds)};
+                            allow_lds(leaf_kernel<true, 4>, max_lds),
+                            allow_lds(apply_shallow_kernel<1>, max_lds),
+                            allow_lds(apply_shallow_kernel<2>, max_lds),
+                            allow_lds(apply_shallow_kernel<3>, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -1859,22 +1996,41 @@ hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_
 ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_count,
                       size_t max_lds, int threads) {
     ApplyShape as{};
-    as.threads = threads > 0 ? threads : 256;
     as.d_used = d_used;
     const int nin = (1 << depth) - 1, nleaf = 1 << depth;
-    const size_t xtile = (size_t)d_used * (as.threads + 4);
-    const size_t per_tree = (size_t)nleaf * 8 + (size_t)nin * 2;
-    size_t budget = 65536;
-    if (budget < xtile + per_tree + 64)
-        budget = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
-    size_t room = budget > xtile + 64 ? budget - xtile - 64 : 0;
-    int64_t tpc = (int64_t)(room / per_tree);
-    if (tpc < 1) tpc = 1;
-    if (tpc > n_trees) tpc = n_trees;
-    as.trees_per_chunk = (int)tpc;
-    as.lds_bytes = (size_t)tpc * nleaf * 8 + ((((size_t)tpc * nin) + 3) & ~(size_t)3) * 2 + xtile;
-    const int64_t ntiles = (n + as.threads - 1) / as.threads;
-    int64_t blocks = (int64_t)cu_count * 8;
+    const size_t lds_cap = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
+    as.shallow = depth <= kApplyShallowDepth;
+    if (as.shallow) {
+        // workgroups of 512 threads (two per CU for 40 features and 400
+        // trees of depth 3, measured best); the tile of codes takes at most
+        // 96 KiB, the leaf values of as many trees as fit the rest
+        int t = threads > 0 ? threads : 512;
+        while (t > 64 && (size_t)d_used * (2 * t + 8) > 96 * 1024) t -= 64;
+        as.threads = t;
+        const size_t xtile = (size_t)d_used * (2 * t + 8);
+        const size_t room = lds_cap > xtile + 64 ? lds_cap - xtile - 64 : 0;
+        int64_t tpc = (int64_t)(room / ((size_t)nleaf * 8));
+        if (tpc < 1) tpc = 1;
+        if (tpc > n_trees) tpc = n_trees;
+        as.trees_per_chunk = (int)tpc;
+        as.lds_bytes = (size_t)tpc * nleaf * 8 + xtile;
+    } else {
+        as.threads = threads > 0 ? threads : 256;
+        const size_t xtile = (size_t)d_used * (as.threads + 4);
+        const size_t per_tree = (size_t)nleaf * 8 + (size_t)nin * 2;
+        size_t budget = 65536;
+        if (budget < xtile + per_tree + 64) budget = lds_cap;
+        size_t room = budget > xtile + 64 ? budget - xtile - 64 : 0;
+        int64_t tpc = (int64_t)(room / per_tree);
+        if (tpc < 1) tpc = 1;
+        if (tpc > n_trees) tpc = n_trees;
+        as.trees_per_chunk = (int)tpc;
+        as.lds_bytes =
+            (size_t)tpc * nleaf * 8 + ((((size_t)tpc * nin) + 3) & ~(size_t)3) * 2 + xtile;
+    }
+    const int64_t tile_events = as.shallow ? 2 * (int64_t)as.threads : as.threads;
+    const int64_t ntiles = (n + tile_events - 1) / tile_events;
+    int64_t blocks = (int64_t)cu_count * (as.shallow ? 4 : 8);
     if (blocks > ntiles) blocks = ntiles;
     if (blocks < 1) blocks = 1;
     as.blocks = (int)blocks;
@@ -1882,8 +2038,23 @@ ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_coun
 }
 
 hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
-                        const uint16_t *cuts, const double *leaves, int n_trees, int depth,
-                        double f0, float *prob, double *score, hipStream_t s) {
+                        const uint16_t *cuts, const uint32_t *nodes, const double *leaves,
+                        int n_trees, int depth, double f0, float *prob, double *score,
+                        hipStream_t s) {
+    if (as.shallow) {
+        if (!nodes) return hipErrorInvalidValue;
+#define FBDT_APPLY_S(DV)                                                                        \
+    apply_shallow_kernel<DV><<<as.blocks, as.threads, as.lds_bytes, s>>>(                       \
+        xb, ldb, n, as.d_used, nodes, leaves, n_trees, as.trees_per_chunk, f0, prob, score)
+        switch (depth) {
+        case 1: FBDT_APPLY_S(1); break;
+        case 2: FBDT_APPLY_S(2); break;
+        case 3: FBDT_APPLY_S(3); break;
+        default: return hipErrorInvalidValue;
+        }
+#undef FBDT_APPLY_S
+        return hipGetLastError();
+    }
     apply_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(xb, ldb, n, as.d_used, cuts, leaves,
                                                             n_trees, depth, as.trees_per_chunk,
                                                             f0, prob, score);
