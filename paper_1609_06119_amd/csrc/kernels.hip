@@ -1793,12 +1793,16 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
             const int g = ((d + cand - 1) / cand) * hs.node_groups;
             int64_t c8 = cu_count / kXcds / g;
             if (c8 > c8max) c8 = c8max;
-            if (c8 < 1) c8 = 1;
+            if (c8 < 1) continue;   // even one chunk per XCD needs a second round
             wgs_of[cand] = kXcds * c8 * g;
             if (wgs_of[cand] > most) most = wgs_of[cand];
         }
+        // every size needs more than one round (many nodes or features): the
+        // largest group, which needs the fewest workgroups
+        f = kHistFMax;
         for (int cand : kHistFpgSizes)
             if (wgs_of[cand] > 0 && wgs_of[cand] * 100 >= most * 95 && cand <= d) f = cand;
+        if (most == 0) f = kHistFMax;
     }
     while (npg > 1 && (size_t)npg * f * per_node_feature > max_lds) --npg;
     hs.nodes_per_group = npg;
