@@ -1759,7 +1759,6 @@ bool hist_fpg_supported(int f) {
 
 HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, int cu_count,
                          size_t max_lds, int fpg, int chunks, int threads) {
-    (void)n_bins;
     HistShape hs{};
     const int nodes = sibling && layer >= 1 ? 1 << (layer - 1) : 1 << layer;
     // an LDS row of one (node, feature) holds 256 bins x 2 classes
@@ -1771,38 +1770,53 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     if (npg > nodes) npg = nodes;
     hs.nodes_per_group = npg;
     hs.node_groups = (nodes + npg - 1) / npg;
-    // Features per workgroup, one of kHistFpgSizes.  A 1024-thread
-    // workgroup fills a CU, so the pass runs as one round of at most
-    // cu_count workgroups: groups * chunks with chunks <= cu_count / groups
-    // and at least half a step of events (kHistE per thread) per chunk.  Among the
-    // sizes whose launch fills at least 95% of the most workgroups any size
-    // reaches, take the largest: every feature group repeats the per-event
-    // work (weights, routing) of its chunk.
+    // Features per workgroup f (one of kHistFpgSizes) and event chunks per
+    // XCD c8, from a cost model fitted to launches of this kernel on MI355X
+    // (0.5M-10M events, 20-40 features, 1-16 histogrammed nodes).  The pass
+    // is bound by LDS atomic issue: a ds_add_u64 wavefront instruction costs
+    // ~9 clocks whether half or all of its lanes are active, so a workgroup
+    // pays about kCostAdd us per thousand (event, feature) slots it streams,
+    // sampled or not, counted or not, plus kCostEvent per thousand events;
+    // the launch pays that once per round of workgroups, and every MB of
+    // chunk partials written (and summed again by the cut scan) costs about
+    // kCostPartial us.  With the CUs filled the slots per workgroup are about
+    // equal for every f, so the model takes the fewest chunks (fewest
+    // partials) that still fill the CUs, and it avoids node groups, which
+    // stream every event once per group.
     const int t_threads = threads > 0 ? threads : 1024;
     const int64_t min_events = (int64_t)kHistE * t_threads;
+    const int64_t R = xcd_range(n);
+    const int64_t c8max = R / (min_events / 2) > 0 ? R / (min_events / 2) : 1;
     int f = 1;
+    int64_t c8_pick = 0;
     if (fpg > 0) {
         f = fpg;
     } else {
-        const int64_t R = xcd_range(n);
-        const int64_t c8max = R / (min_events / 2) > 0 ? R / (min_events / 2) : 1;
-        int64_t wgs_of[kHistFMax + 1] = {0};
-        int64_t most = 0;
+        constexpr double kCostEvent = 0.01, kCostAdd = 0.057, kCostPartial = 0.25;
+        double best = 0.0;
         for (int cand : kHistFpgSizes) {
-            if ((size_t)npg * cand * per_node_feature > max_lds) continue;
-            const int g = ((d + cand - 1) / cand) * hs.node_groups;
-            int64_t c8 = cu_count / kXcds / g;
-            if (c8 > c8max) c8 = c8max;
-            if (c8 < 1) continue;   // even one chunk per XCD needs a second round
-            wgs_of[cand] = kXcds * c8 * g;
-            if (wgs_of[cand] > most) most = wgs_of[cand];
+            if (cand > d && cand != kHistFpgSizes[0]) continue;
+            const int np = (int)std::min<size_t>((size_t)nodes, max_lds / ((size_t)cand * per_node_feature));
+            if (np < 1) continue;
+            const int ng = (nodes + np - 1) / np;
+            const int g = ((d + cand - 1) / cand) * ng;
+            int64_t top = cu_count / kXcds / g;
+            if (top > c8max) top = c8max;
+            if (top < 1) top = 1;
+            for (int64_t c8 = 1; c8 <= top; ++c8) {
+                const double ek = (double)((R + c8 - 1) / c8) / 1000.0;
+                const int64_t wgs = kXcds * c8 * g;
+                const double rounds = (double)((wgs + cu_count - 1) / cu_count);
+                const double pmb = (double)(kXcds * c8) * nodes * d * n_bins * 16.0 / 1e6;
+                const double t = rounds * ek * (kCostEvent + kCostAdd * cand) + kCostPartial * pmb;
+                if (c8_pick == 0 || t < best) {
+                    best = t;
+                    f = cand;
+                    c8_pick = c8;
+                }
+            }
         }
-        // every size needs more than one round (many nodes or features): the
-        // largest group, which needs the fewest workgroups
-        f = kHistFMax;
-        for (int cand : kHistFpgSizes)
-            if (wgs_of[cand] > 0 && wgs_of[cand] * 100 >= most * 95 && cand <= d) f = cand;
-        if (most == 0) f = kHistFMax;
+        if (chunks > 0) c8_pick = 0;
     }
     while (npg > 1 && (size_t)npg * f * per_node_feature > max_lds) --npg;
     hs.nodes_per_group = npg;
@@ -1818,9 +1832,8 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     // by default (a 1024-thread workgroup fills a CU): a few workgroups more
     // than CUs run as a second round and nearly double the pass; every extra
     // event chunk also adds one more partial histogram to write and to sum.
-    const int64_t R = xcd_range(n);
-    int64_t c8 = chunks > 0 ? (chunks + kXcds - 1) / kXcds : (int64_t)cu_count / kXcds / groups;
-    const int64_t c8max = R / (min_events / 2) > 0 ? R / (min_events / 2) : 1;
+    int64_t c8 = chunks > 0 ? (chunks + kXcds - 1) / kXcds
+               : c8_pick > 0 ? c8_pick : (int64_t)cu_count / kXcds / groups;
     if (chunks <= 0 && c8 > c8max) c8 = c8max;
     if (c8 < 1) c8 = 1;
     int64_t ce = (R + c8 - 1) / c8;
