@@ -446,3 +446,4 @@ def test_apply_hand_built_forest():
     ref = 0.25 + np.array([0.1, 0.2, 0.4, 0.4, 0.2])
     assert np.allclose(F, ref, rtol=0, atol=1e-15)
     assert np.allclose(p, expit(2 * ref), rtol=0, atol=1e-7)
+
