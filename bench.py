@@ -15,6 +15,10 @@ HBM.  Prints one JSON line:
            records none), against 8 TB/s;
   cpu_baseline = the CPU oracle fitting the first trees of the same
            workload on this host, in the same unit.
+Also reported, outside the step: "apply" = the 400-tree forest applied to 50M
+fresh events (events/s); "fit_workloads" = full fits of the 2M x 40 (200
+trees) and 10M x 40 (depth 6, 100 trees) workloads, with the histogram
+kernel's mean launch and roofline fraction on each.
 """
 from __future__ import annotations
 
@@ -60,10 +64,57 @@ def parse():
                     help="fresh events of the apply workload (0 skips it)")
     ap.add_argument("--apply-steps", type=int, default=3,
                     help="timed applies of the 400-tree forest to the fresh events")
+    ap.add_argument("--fit-workloads", default="3,4",
+                    help="larger fit workloads also timed and reported (comma list, '' for none)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this size on the device three "
                          "times (reference kernel for hardware byte counters)")
     return ap.parse_args()
+
+
+def measure_fit_workload(cfg, fb, torch):
+    """One full fit of a larger workload (all trees), timed twice: once as
+    launched in production (graph replay, no events) for the fit time, once
+    with HIP events around every histogram launch for the kernel's roofline."""
+    from synth import CONFIGS, make_training_set
+    spec = CONFIGS[cfg]
+    t0 = time.time()
+    ds = make_training_set(cfg)
+    d, n = ds["x"].shape
+    x = torch.from_numpy(ds["x"]).cuda()
+    y = torch.from_numpy(ds["y"]).cuda()
+    _, codes = fb.bin(x, spec.n_bins)
+    del x, ds
+    B, D, T = spec.n_bins, spec.depth, spec.n_trees
+
+    def fit():
+        return fb.fit(codes, y, B, D, T, spec.shrinkage, spec.subsample, spec.fit_seed)
+
+    fit()   # warm-up (records the graph)
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
+    fit()
+    torch.cuda.synchronize()
+    fit_s = time.perf_counter() - ts
+    fb.timing_enable(("histogram", "best_cuts"))
+    fit()
+    torch.cuda.synchronize()
+    hl, hms, hb = fb.timing_read("histogram")
+    cl, cms, _ = fb.timing_read("best_cuts")
+    fb.timing_enable(())
+    del codes, y
+    torch.cuda.empty_cache()
+    achieved = hb / (hms / 1e3) / 1e9
+    return {"workload": f"fit {n} x {d}, {B} bins, depth {D}, {T} trees ({spec.name})",
+            "fit_ms": fit_s * 1e3,
+            "value": n * d * D * T / fit_s,
+            "unit": "event*features/s per tree layer",
+            "hist_mean_launch_us": hms * 1e3 / hl,
+            "hist_algorithmic_bytes_per_launch": hb / hl,
+            "hist_achieved_gbs": achieved,
+            "hist_frac": achieved / HBM_PEAK_GBS,
+            "cut_scan_mean_launch_us": cms * 1e3 / max(cl, 1),
+            "setup_s": round(time.time() - t0, 1)}
 
 
 def measure_apply_workload(args, apply_x, fb, torch):
@@ -194,6 +245,12 @@ def main():
     cpu_s = time.perf_counter() - tc
     cpu_value = n * d * D * cpu_T / cpu_s
 
+    fits = {}
+    for c in filter(None, str(args.fit_workloads).split(",")):
+        fits[f"workload{int(c)}"] = measure_fit_workload(int(c), fb, torch)
+        print(f"# fit workload {c}: {fits[f'workload{int(c)}']['fit_ms']:.1f} ms", file=sys.stderr,
+              flush=True)
+
     apply_out = {"events_per_s": apply_events_per_s, "launches": a_launches,
                  "mean_launch_us": a_ms * 1e3 / max(a_launches, 1),
                  "workload": f"{n} binned events x {T} trees of depth {D} (the step's apply)"}
@@ -243,6 +300,7 @@ def main():
             "algorithmic_bytes_per_launch": hist_avg_bytes,
         },
         "apply": apply_out,
+        "fit_workloads": fits,
         "bin_ms": bin_ms,
         "cpu_baseline": {
             "value": cpu_value,
