@@ -216,7 +216,8 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
 /*
  * Launch-shape overrides for sweeps; value 0 restores the default.
  * Names: "hist_features_per_group" (1, 2, 4, 5 or 8), "hist_event_chunks",
- * "hist_threads" (a multiple of 64, at most 1024), "apply_threads".
+ * "hist_threads" (a multiple of 64, at most 1024), "hist_copies" (1, 2 or 4
+ * LDS copies of a workgroup's histograms), "apply_threads".
  * "fit_graphs" (default 1): fbdt_fit records the kernel launches of its
  * boosting loop as a HIP graph on first use of an argument set (device,
  * buffer addresses, sizes, parameters, launch shapes) and replays it on later

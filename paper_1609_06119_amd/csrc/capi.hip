@@ -83,8 +83,17 @@ int device_info(int dev, DeviceInfo *out) {
 }
 
 // ---- options --------------------------------------------------------------
-std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0},
+std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0}, opt_hist_copies{0},
     opt_apply_threads{0}, opt_fit_graphs{1};
+
+HistOverrides hist_overrides() {
+    HistOverrides ov;
+    ov.fpg = (int)opt_hist_fpg.load();
+    ov.chunks = (int)opt_hist_chunks.load();
+    ov.threads = (int)opt_hist_threads.load();
+    ov.copies = (int)opt_hist_copies.load();
+    return ov;
+}
 
 // ---- timing ---------------------------------------------------------------
 struct PendingTiming {
@@ -145,12 +154,13 @@ struct GraphKey {
     int d, n_bins, depth, n_trees, scale, lblocks;
     double eta, alpha;
     uint64_t seed;
-    int64_t fpg, chunks, threads;
+    int64_t fpg, chunks, threads, copies;
     bool operator==(const GraphKey &o) const {
         return xb == o.xb && y == o.y && w == o.w && n == o.n && ldb == o.ldb && d == o.d &&
                n_bins == o.n_bins && depth == o.depth && n_trees == o.n_trees &&
                scale == o.scale && lblocks == o.lblocks && eta == o.eta && alpha == o.alpha &&
-               seed == o.seed && fpg == o.fpg && chunks == o.chunks && threads == o.threads;
+               seed == o.seed && fpg == o.fpg && chunks == o.chunks && threads == o.threads &&
+               copies == o.copies;
     }
 };
 
@@ -268,6 +278,10 @@ int fbdt_set_option(const char *name, int64_t value) {
         if (value != 0 && (value % 64 != 0 || value > 1024))
             return fail(FBDT_E_INVAL, "hist_threads must be a multiple of 64, <= 1024");
         opt_hist_threads = value;
+    } else if (!strcmp(name, "hist_copies")) {
+        if (value != 0 && value != 1 && value != 2 && value != 4)
+            return fail(FBDT_E_INVAL, "hist_copies must be 0, 1, 2 or 4");
+        opt_hist_copies = value;
     } else if (!strcmp(name, "fit_graphs")) {
         opt_fit_graphs = value != 0;
     } else if (!strcmp(name, "apply_threads")) {
@@ -442,9 +456,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     size_t partial_elems = 0;
     for (int l = 0; l < D; ++l) {
         // below the root the routed pass histograms one child per parent
-        plans[l] = plan_histogram(n, d, n_bins, l, true, di.cu_count, di.max_lds,
-                                  (int)opt_hist_fpg.load(), (int)opt_hist_chunks.load(),
-                                  (int)opt_hist_threads.load());
+        plans[l] = plan_histogram(n, d, n_bins, l, true, di.cu_count, di.max_lds, hist_overrides());
         const size_t hnodes = l >= 1 ? (size_t)1 << (l - 1) : 1;
         partial_elems = std::max(partial_elems,
                                  (size_t)plans[l].chunks * hnodes * d * n_bins * 2);
@@ -586,7 +598,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                             (1 << FBDT_K_BEST_CUTS) | (1 << FBDT_K_LEAF);
     if (opt_fit_graphs.load() && !(g_timing.load() & timed_kinds)) {
         const GraphKey key{xb, y, w, n, ldb, d, n_bins, D, T, scale, lblocks, eta, alpha, seed,
-                           opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load()};
+                           opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load(),
+                           opt_hist_copies.load()};
         hipGraphExec_t exec = nullptr;
         for (auto &g : a.graphs)
             if (g.first == key) exec = g.second;
@@ -832,8 +845,7 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     if ((rc = current_device(&dev, &di))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     HistShape hs = plan_histogram(n, d, n_bins, layer, false, di.cu_count, di.max_lds,
-                                  (int)opt_hist_fpg.load(), (int)opt_hist_chunks.load(),
-                                  (int)opt_hist_threads.load());
+                                  hist_overrides());
     if (hs.lds_bytes + kHistStaticLdsReserve > di.max_lds)
         return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", layer,
                     hs.lds_bytes, di.max_lds);

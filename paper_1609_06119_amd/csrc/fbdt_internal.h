@@ -31,7 +31,15 @@ struct HistShape {
     int64_t xcd_events;       // events of an XCD's range, xcd_range(n)
     int threads;              // threads per workgroup
     int blocks;               // grid size (chunks * groups, rounded up to the XCD count)
+    int copies;               // LDS copies of the workgroup's histograms (1, 2 or 4):
+                              // lane l adds into copy l % copies
+    int copy_stride;          // bytes between copies (the histograms plus a bank shift)
     size_t lds_bytes;         // dynamic LDS per workgroup
+};
+
+// Launch-shape overrides of the histogram pass (0 = the planner's choice).
+struct HistOverrides {
+    int fpg = 0, chunks = 0, threads = 0, copies = 0;
 };
 
 // Device-side scratch of one fit.
@@ -70,6 +78,11 @@ constexpr int kValidateBlocks = 256;
 // LDS kept aside for a kernel's static shared arrays when sizing its
 // dynamic LDS (the histogram kernel's cut table takes 128 bytes)
 constexpr size_t kHistStaticLdsReserve = 1024;
+// bytes between LDS copies of the histograms beyond their size: a shift of
+// 16 four-byte banks, so that copy c of a counter sits 16 c banks away
+constexpr size_t kHistCopyShift = 64;
+// chunk length (events per workgroup) from which the planner uses copies
+constexpr int64_t kHistCopiesMinEvents = 131072;
 // features per histogram workgroup the kernels are built for (a workgroup
 // holds the codes of all of them in registers per step)
 constexpr int kHistFpgSizes[] = {1, 2, 4, 5, 8};
@@ -106,10 +119,10 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
                             int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
                             double *yts, double *score_out, int cu_count, hipStream_t s);
 
-// fpg, chunks, threads: launch-shape overrides (0 = default).  sibling: the
+// ov: launch-shape overrides (0 = the planner's choice).  sibling: the
 // routed fit pass, which for layer >= 1 histograms one child per parent.
 HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, int cu_count,
-                         size_t max_lds, int fpg, int chunks, int threads);
+                         size_t max_lds, const HistOverrides &ov);
 
 // Candidate cuts of a layer's nodes, one per (node, feature), from which a
 // routed pass takes each parent's cut (best gain, then lowest feature);

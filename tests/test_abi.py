@@ -55,3 +55,6 @@ def test_argument_errors_need_no_device():
     assert L.fbdt_set_option(b"hist_features_per_group", 3) == -1
     assert L.fbdt_set_option(b"hist_features_per_group", 5) == 0
     assert L.fbdt_set_option(b"hist_features_per_group", 0) == 0
+    assert L.fbdt_set_option(b"hist_copies", 3) == -1
+    assert L.fbdt_set_option(b"hist_copies", 4) == 0
+    assert L.fbdt_set_option(b"hist_copies", 0) == 0

@@ -38,12 +38,12 @@ def max_rel(a, b):
 @pytest.fixture(autouse=True)
 def _defaults():
     for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads",
-                 "apply_threads"):
+                 "hist_copies", "apply_threads"):
         fb.set_option(name, 0)
     fb.set_option("fit_graphs", 1)
     yield
     for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads",
-                 "apply_threads"):
+                 "hist_copies", "apply_threads"):
         fb.set_option(name, 0)
     fb.set_option("fit_graphs", 1)
 
@@ -183,10 +183,30 @@ def test_histogram_feature_groups_and_threads():
     ws = np.where(y > 0, wa, -wa).astype(np.float32)
     ref = O.histogram(xb, node.astype(np.int64), wa, y > 0, layer, B)
     codes = fb.Codes.from_numpy(xb)
-    for fpg, threads in ((2, 256), (4, 512), (5, 1024), (8, 128), (1, 64)):
+    for fpg, threads, copies in ((2, 256, 4), (4, 512, 2), (5, 1024, 1), (8, 128, 4), (1, 64, 2),
+                                 (5, 1024, 4)):
         fb.set_option("hist_features_per_group", fpg)
         fb.set_option("hist_threads", threads)
-        say(f"histogram fpg={fpg} threads={threads}")
+        fb.set_option("hist_copies", copies)
+        say(f"histogram fpg={fpg} threads={threads} copies={copies}")
+        H = fb.histogram(codes, dev(node), dev(ws), layer, B).cpu().numpy()
+        assert max_rel(H, ref) <= 1e-12
+
+
+def test_histogram_copies_with_few_distinct_codes():
+    """Every lane of an instruction hitting the same few counters (a feature
+    with two codes) is summed exactly with one, two or four LDS copies."""
+    rng = np.random.default_rng(4)
+    n, d, B, layer = 70_003, 5, 256, 1
+    xb = rng.integers(0, 2, (d, n)).astype(np.uint8) * 255
+    node = rng.integers(2, 4, n).astype(np.uint8)
+    y = np.where(rng.random(n) < 0.5, 1, -1).astype(np.int8)
+    wa = rng.uniform(0.1, 1, n).astype(np.float32)
+    ws = np.where(y > 0, wa, -wa).astype(np.float32)
+    ref = O.histogram(xb, node.astype(np.int64), wa, y > 0, layer, B)
+    codes = fb.Codes.from_numpy(xb)
+    for copies in (1, 2, 4):
+        fb.set_option("hist_copies", copies)
         H = fb.histogram(codes, dev(node), dev(ws), layer, B).cpu().numpy()
         assert max_rel(H, ref) <= 1e-12
 

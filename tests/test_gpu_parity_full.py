@@ -32,7 +32,7 @@ def dev(a):
 
 @pytest.fixture(autouse=True)
 def _defaults():
-    for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads"):
+    for name in ("hist_features_per_group", "hist_event_chunks", "hist_threads", "hist_copies"):
         fb.set_option(name, 0)
     fb.set_option("fit_graphs", 1)
     yield
