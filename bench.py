@@ -152,6 +152,31 @@ def measure_apply_workload(args, apply_x, fb, torch):
     launches, ms, _ = fb.timing_read("apply")
     fb.timing_enable(())
     mean_ms = ms / max(launches, 1)
+    del codes
+    prob_binned = prob.clone()
+    # the same events as float32 values, tested against value thresholds
+    # (the training boundaries attached to the model)
+    xf = torch.empty((d, n), dtype=torch.float32, device="cuda")
+    for off, x in apply_x:
+        xf[:, off:off + x.shape[1]].copy_(torch.from_numpy(x))
+    model.set_boundaries(bounds)
+    fb.apply_float(model, xf, prob=prob)   # warm-up
+    torch.cuda.synchronize()
+    fb.timing_enable(("apply",))
+    for _ in range(max(1, args.apply_steps)):
+        fb.apply_float(model, xf, prob=prob)
+    torch.cuda.synchronize()
+    fl, fms, _ = fb.timing_read("apply")
+    fb.timing_enable(())
+    same = bool(torch.equal(prob, prob_binned))
+    del xf, prob_binned
+    f_ms = fms / max(fl, 1)
+    float_out = {"events_per_s": n / (f_ms / 1e3), "launches": fl, "mean_launch_us": f_ms * 1e3,
+                 "bytes_per_event": 4 * d + 4,
+                 "hbm_gbs": n * (4 * d + 4) / (f_ms / 1e3) / 1e9,
+                 "workload": f"the same forest and events as float32 values [{d}][{n}], "
+                             "value thresholds (fbdt_apply_float)",
+                 "prob_equal_to_binned_apply": same}
     return {"events_per_s": n / (mean_ms / 1e3), "launches": launches,
             "mean_launch_us": mean_ms * 1e3,
             "bytes_per_event": d + 4,
@@ -159,7 +184,7 @@ def measure_apply_workload(args, apply_x, fb, torch):
             "workload": f"{s5.n_trees}-tree depth-{s5.depth} forest fitted on workload 3 "
                         f"({s3.n_events} x {s3.n_features}, {s5.n_bins} bins) applied to {n} "
                         f"fresh events x {d} uint8 codes; prob float32 out",
-            "setup_s": round(fit_s, 1)}
+            "setup_s": round(fit_s, 1), "float": float_out}
 
 
 def main():

@@ -118,11 +118,36 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
 int fbdt_apply(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
                float *prob, double *score, void *stream);
 
+/*
+ * Score float32 events without binning them (section 2.2, the inverse of the
+ * bin transform): the cut "bin >= c" of feature j is the test
+ * x >= boundaries[j][c - 1], which holds exactly when the value's bin (the
+ * number of boundaries at or below it) is >= c, so the result equals
+ * fbdt_apply on fbdt_bin_transform's codes bit for bit.  The model needs its
+ * boundaries (fbdt_model_set_boundaries or fbdt_model_import), else
+ * FBDT_E_INVAL.  x: device float32 [d][ldx], ldx >= n, d >= the model's
+ * feature count (else FBDT_E_SHAPE); NaN values are not supported (a NaN
+ * fails every test and takes the left branch).  prob, score as for
+ * fbdt_apply.  Stream-ordered.
+ */
+int fbdt_apply_float(const fbdt_model *m, const float *x, int64_t n, int32_t d, int64_t ldx,
+                     float *prob, double *score, void *stream);
+
 /* Borrowed host view of a model, valid until fbdt_model_free. */
 int fbdt_model_export(const fbdt_model *m, fbdt_model_view *view);
 
-/* New model from host arrays (copied); gain and boundaries may be NULL. */
+/* New model from host arrays (copied); gain and boundaries may be NULL.
+ * Boundaries, if given, must hold no NaN and ascend (non-strictly) per
+ * feature, else FBDT_E_INVAL. */
 int fbdt_model_import(const fbdt_model_view *view, fbdt_model **out);
+
+/*
+ * Attach the training sample's bin boundaries (host float32 [d][B - 1], as
+ * fbdt_bin returns them; copied) to a model, for fbdt_apply_float.  They
+ * must hold no NaN and ascend per feature, else FBDT_E_INVAL.  Not to be
+ * called while the model is applied on another thread.
+ */
+int fbdt_model_set_boundaries(fbdt_model *m, const float *boundaries);
 
 void fbdt_model_free(fbdt_model *m);
 

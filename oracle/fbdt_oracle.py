@@ -14,7 +14,8 @@ method at a time, in the order the paper describes it:
   histograms of all nodes and features (sections 1.1 and 2.1), cumulative
   probability histograms, separation gain, best cut, routing (section 1.1,
   Fig. 1) -> terminal boost weights and score update (section 1.3) ->
-  apply: traverse, sum, sigmoid (Fig. 1, section 1.3).
+  apply: traverse, sum, sigmoid (Fig. 1, section 1.3), on bin codes or on
+  raw values with the inverse transform of section 2.2.
 
 Where the paper is silent the reading is stated at the function.  Pins:
 every function is checked by ``tests/test_oracle_*.py`` against something
@@ -367,6 +368,30 @@ def apply(model: Model, xb, n_trees: int | None = None):
             f = model.cut_feature[t][node - 1].astype(np.int64)
             c = model.cut_bin[t][node - 1].astype(np.int64)
             node = 2 * node + (xb[f, rows].astype(np.int64) >= c)
+        F = F + model.leaf[t][node - (1 << model.depth)]
+    p = (1.0 / (1.0 + np.exp(-2.0 * F))).astype(np.float32)
+    return p, F
+
+
+def apply_thresholds(model: Model, x, boundaries, n_trees: int | None = None):
+    """Score float32 events without binning them (section 2.2, the inverse
+    of the bin transform): a value's bin is the number of boundaries at or
+    below it, so the cut "bin >= c" of feature j is the test x >= b_j,c, the
+    c-th smallest training boundary of feature j (boundaries[j][c - 1]).
+    Leaf values summed in tree order in float64, as in ``apply``.
+    Returns (P float32 [N], F float64 [N])."""
+    x = np.asarray(x, dtype=np.float32)
+    b = np.asarray(boundaries, dtype=np.float32)
+    n = x.shape[1]
+    T = model.n_trees if n_trees is None else n_trees
+    F = np.full(n, model.f0)
+    rows = np.arange(n)
+    for t in range(T):
+        node = np.ones(n, dtype=np.int64)
+        for _ in range(model.depth):
+            f = model.cut_feature[t][node - 1].astype(np.int64)
+            c = model.cut_bin[t][node - 1].astype(np.int64)
+            node = 2 * node + (x[f, rows] >= b[f, c - 1])
         F = F + model.leaf[t][node - (1 << model.depth)]
     p = (1.0 / (1.0 + np.exp(-2.0 * F))).astype(np.float32)
     return p, F

@@ -7,6 +7,7 @@ from .api import (  # noqa: F401
     FbdtError,
     Model,
     apply,
+    apply_float,
     best_cuts,
     bin,
     bin_transform,

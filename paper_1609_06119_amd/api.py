@@ -116,6 +116,13 @@ class Model:
                                     np.float32).reshape(v.n_features, v.n_bins - 1)
         return out
 
+    def set_boundaries(self, boundaries) -> "Model":
+        """Attach the training bin boundaries [d][B-1] (for apply_float)."""
+        b = np.ascontiguousarray(boundaries, np.float32)
+        check("fbdt_model_set_boundaries",
+              lib().fbdt_model_set_boundaries(self._h, b.ctypes.data_as(C.c_void_p)))
+        return self
+
     @staticmethod
     def from_arrays(cut_feature, cut_bin, leaf, f0: float, n_features: int, n_bins: int,
                     gain=None, boundaries=None) -> "Model":
@@ -211,6 +218,21 @@ def apply(model: Model, codes: Codes, prob: torch.Tensor | None = None,
         _need(score, torch.float64, "score", n)
     check("fbdt_apply", lib().fbdt_apply(model.handle, _ptr(codes.data), n, codes.d, codes.ldb,
                                          _ptr(prob), _ptr(score), _stream()))
+    return prob
+
+
+def apply_float(model: Model, x: torch.Tensor, prob: torch.Tensor | None = None,
+                score: torch.Tensor | None = None) -> torch.Tensor:
+    """P(signal) float32 [n] of float32 events x [d][n] (row stride x.stride(0)),
+    tested against the model's value thresholds; score float64 [n] optionally."""
+    _need_rows(x)
+    d, n = int(x.shape[0]), int(x.shape[1])
+    prob = prob if prob is not None else torch.empty(n, dtype=torch.float32, device=x.device)
+    _need(prob, torch.float32, "prob", n)
+    if score is not None:
+        _need(score, torch.float64, "score", n)
+    check("fbdt_apply_float", lib().fbdt_apply_float(model.handle, _ptr(x), n, d, x.stride(0),
+                                                     _ptr(prob), _ptr(score), _stream()))
     return prob
 
 

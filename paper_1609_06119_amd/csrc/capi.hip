@@ -32,6 +32,7 @@ struct fbdt_model {
         double *leaves;
         int nodes_stride;   // tile stride the node records were made for (0: none)
         uint32_t *nodes;    // [T][16] node records of shallow forests, or null
+        uint2 *frec;        // [T][2^D - 1] (feature, threshold) for float apply, or null
     };
     std::mutex mu;
     std::vector<DeviceCopy> copies;
@@ -358,6 +359,19 @@ static int encode_with(const float *x, int64_t n, int32_t d, int64_t ldx, int32_
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;
     if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values");
+    return FBDT_OK;
+}
+
+// Training boundaries [d][n_bins - 1]: no NaN, non-decreasing per feature.
+static int check_boundaries(const float *b, int32_t d, int32_t n_bins) {
+    for (int j = 0; j < d; ++j) {
+        const float *r = b + (size_t)j * (n_bins - 1);
+        for (int k = 0; k < n_bins - 1; ++k) {
+            if (std::isnan(r[k])) return fail(FBDT_E_INVAL, "boundary %d of feature %d is NaN", k, j);
+            if (k > 0 && !(r[k - 1] <= r[k]))
+                return fail(FBDT_E_INVAL, "boundaries of feature %d are not ascending", j);
+        }
+    }
     return FBDT_OK;
 }
 
@@ -705,6 +719,10 @@ int fbdt_model_import(const fbdt_model_view *v, fbdt_model **out) {
         if (v->cut_bin[k] < 1 || v->cut_bin[k] >= v->n_bins)
             return fail(FBDT_E_INVAL, "cut bin %d not in [1, n_bins)", (int)v->cut_bin[k]);
     }
+    if (v->boundaries) {
+        const int rc = check_boundaries(v->boundaries, v->n_features, v->n_bins);
+        if (rc) return rc;
+    }
     fbdt_model *m = new (std::nothrow) fbdt_model;
     if (!m) return fail(FBDT_E_DEVICE, "out of host memory");
     m->n_trees = v->n_trees;
@@ -726,6 +744,24 @@ int fbdt_model_import(const fbdt_model_view *v, fbdt_model **out) {
     return FBDT_OK;
 }
 
+int fbdt_model_set_boundaries(fbdt_model *m, const float *boundaries) {
+    int rc;
+    if (!m || !boundaries) return fail(FBDT_E_INVAL, "NULL argument");
+    if ((rc = check_boundaries(boundaries, m->n_features, m->n_bins))) return rc;
+    std::lock_guard<std::mutex> lk(m->mu);
+    m->boundaries.assign(boundaries, boundaries + (size_t)m->n_features * (m->n_bins - 1));
+    // the float-apply records hold thresholds: rebuilt on next use
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    for (auto &c : m->copies)
+        if (c.frec && hipSetDevice(c.device) == hipSuccess) {
+            (void)hipFree(c.frec);
+            c.frec = nullptr;
+        }
+    if (cur >= 0) (void)hipSetDevice(cur);
+    return FBDT_OK;
+}
+
 void fbdt_model_free(fbdt_model *m) {
     if (!m) return;
     int cur = -1;
@@ -735,6 +771,7 @@ void fbdt_model_free(fbdt_model *m) {
             (void)hipFree(c.cuts);
             (void)hipFree(c.leaves);
             if (c.nodes) (void)hipFree(c.nodes);
+            if (c.frec) (void)hipFree(c.frec);
         }
     }
     if (cur >= 0) (void)hipSetDevice(cur);
@@ -774,7 +811,7 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
             std::vector<uint16_t> packed((size_t)T * nin);
             for (size_t k = 0; k < packed.size(); ++k)
                 packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
-            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr};
+            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr};
             HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
             if (hipMalloc(&c.leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
                 (void)hipFree(c.cuts);
@@ -808,6 +845,79 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     }
     Timed tm(FBDT_K_APPLY, s, (double)n * (m->n_features + 4));
     HIP_TRY(launch_apply(as, xb, ldb, n, cuts, nodes, leaves, T, D, m->f0, prob, score, s));
+    tm.done();
+    return FBDT_OK;
+}
+
+int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d, int64_t ldx,
+                     float *prob, double *score, void *stream) {
+    int rc;
+    if (!mc) return fail(FBDT_E_INVAL, "model is NULL");
+    if ((rc = check_float_input(x, n, d, ldx))) return rc;
+    if (n < 1) return fail(FBDT_E_INVAL, "n = %lld must be >= 1", (long long)n);
+    if (!prob) return fail(FBDT_E_INVAL, "prob is NULL");
+    fbdt_model *m = const_cast<fbdt_model *>(mc);
+    if (d < m->n_features)
+        return fail(FBDT_E_SHAPE, "d = %d < the model's %d features", d, m->n_features);
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = m->n_trees, D = m->depth;
+    const size_t nin = ((size_t)1 << D) - 1, nleaf = (size_t)1 << D;
+    const ApplyShape as = plan_apply_float(n, m->n_features, T, D, di.cu_count, di.max_lds,
+                                           (int)opt_apply_threads.load());
+    if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
+        return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
+                    "apply_threads)", as.lds_bytes, di.max_lds);
+    const uint2 *rec = nullptr;
+    const double *leaves = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(m->mu);
+        if (m->boundaries.empty())
+            return fail(FBDT_E_INVAL, "the model has no bin boundaries (fbdt_model_set_boundaries)");
+        fbdt_model::DeviceCopy *copy = nullptr;
+        for (auto &c : m->copies)
+            if (c.device == dev) copy = &c;
+        if (!copy) {
+            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr};
+            std::vector<uint16_t> packed((size_t)T * nin);
+            for (size_t k = 0; k < packed.size(); ++k)
+                packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
+            HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
+            if (hipMalloc(&c.leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
+                (void)hipFree(c.cuts);
+                return fail(FBDT_E_DEVICE, "out of device memory");
+            }
+            m->copies.push_back(c);
+            copy = &m->copies.back();
+            HIP_TRY(hipMemcpy(copy->cuts, packed.data(), packed.size() * sizeof(uint16_t),
+                              hipMemcpyHostToDevice));
+            HIP_TRY(hipMemcpy(copy->leaves, m->leaf.data(), (size_t)T * nleaf * sizeof(double),
+                              hipMemcpyHostToDevice));
+        }
+        if (!copy->frec) {
+            // cut "bin >= c" of feature j = "x >= boundary c of feature j"
+            // (boundary index c - 1 of its row)
+            std::vector<uint2> table((size_t)T * nin);
+            const size_t nb = (size_t)m->n_bins - 1;
+            for (size_t k = 0; k < table.size(); ++k) {
+                const uint32_t f = m->cut_feature[k], c = m->cut_bin[k];
+                float thr;
+                std::memcpy(&thr, &m->boundaries[f * nb + c - 1], sizeof thr);
+                uint32_t bits;
+                std::memcpy(&bits, &thr, sizeof bits);
+                table[k] = make_uint2(f, bits);
+            }
+            HIP_TRY(hipMalloc(&copy->frec, table.size() * sizeof(uint2)));
+            HIP_TRY(hipMemcpy(copy->frec, table.data(), table.size() * sizeof(uint2),
+                              hipMemcpyHostToDevice));
+        }
+        rec = copy->frec;
+        leaves = copy->leaves;
+    }
+    Timed tm(FBDT_K_APPLY, s, (double)n * (4.0 * m->n_features + 4));
+    HIP_TRY(launch_apply_float(as, x, ldx, n, rec, leaves, T, D, m->f0, prob, score, s));
     tm.done();
     return FBDT_OK;
 }

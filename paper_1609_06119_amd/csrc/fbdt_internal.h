@@ -239,6 +239,15 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
                         int n_trees, int depth, double f0, float *prob, double *score,
                         hipStream_t s);
 
+// Traversal of float32 events [d][ldx] with value thresholds.  rec: [T][2^D-1]
+// (feature, float bits of the threshold) per heap node.  as.shallow marks
+// depth <= kApplyShallowDepth (every node tested, records by scalar loads).
+ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, int cu_count,
+                            size_t max_lds, int threads);
+hipError_t launch_apply_float(const ApplyShape &as, const float *x, int64_t ldx, int64_t n,
+                              const uint2 *rec, const double *leaves, int n_trees, int depth,
+                              double f0, float *prob, double *score, hipStream_t s);
+
 hipError_t launch_encode(const float *x, int64_t ldx, int64_t n, int d, const float *bounds,
                          int n_bins, uint8_t *xb, int64_t ldb, int *err, hipStream_t s);
 

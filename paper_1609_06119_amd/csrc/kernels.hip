@@ -1633,6 +1633,106 @@ __global__ __launch_bounds__(1024) void apply_shallow_kernel(
     }
 }
 
+// Leaf (0 .. 2^D - 1) of a tree of depth D <= 3 reached by this thread's
+// event: every node tested (x >= threshold), then the path picked from the
+// decisions; r[k] = (feature, threshold bits) of heap node k + 1.
+template <int D>
+__device__ __forceinline__ uint32_t float_leaf(const float *xme, int XS, const uint2 *r) {
+    constexpr int NIN = (1 << D) - 1;
+    uint32_t b[NIN];
+#pragma unroll
+    for (int k = 0; k < NIN; ++k) b[k] = xme[r[k].x * XS] >= __uint_as_float(r[k].y) ? 1u : 0u;
+    const uint32_t r1 = b[0];
+    if (D == 1) return r1;
+    const uint32_t r2 = r1 ? b[2] : b[1];
+    if (D == 2) return 2u * r1 + r2;
+    const uint32_t r3 = r1 ? (r2 ? b[6] : b[5]) : (r2 ? b[4] : b[3]);
+    return 4u * r1 + 2u * r2 + r3;
+}
+
+// Forest traversal of float32 events with value thresholds (section 2.2:
+// the cut "bin >= c" of feature j is the test x >= b_j,c, the c-th training
+// boundary, since a value's bin counts the boundaries at or below it).  A
+// workgroup stages a tile of one event per thread, feature-major, in LDS.
+// rec: [T][2^D - 1] pairs (feature, threshold bits).  Depth <= 3: every
+// node of a tree is tested (records read with scalar loads, a batch of
+// trees at a time) and the leaf is picked from the decisions without a
+// branch; deeper trees: each event walks its path with records in LDS.
+template <int D>
+__global__ __launch_bounds__(1024) void apply_float_kernel(
+    const float *__restrict__ x, int64_t ldx, int64_t n, int d_used,
+    const uint2 *__restrict__ rec, const double *__restrict__ leaves, int T, int tpc, double f0,
+    float *__restrict__ prob, double *__restrict__ score) {
+    constexpr int NLEAF = 1 << D;
+    constexpr int NIN = (1 << D) - 1;
+    constexpr bool kAll = D <= kApplyShallowDepth;
+    extern __shared__ double smem[];
+    double *s_leaf = smem;                                                    // [tpc][NLEAF]
+    uint2 *s_rec = reinterpret_cast<uint2 *>(s_leaf + (size_t)tpc * NLEAF);   // [tpc][NIN]
+    float *s_x = reinterpret_cast<float *>(s_rec + (kAll ? 0 : (size_t)tpc * NIN));
+    const int XS = blockDim.x;   // [d_used][XS]
+    const int nchunks = (T + tpc - 1) / tpc;
+    const int64_t ntiles = (n + blockDim.x - 1) / blockDim.x;
+    const float *xme = s_x + threadIdx.x;
+    bool staged = false;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t i = tile * blockDim.x + threadIdx.x;
+        __syncthreads();
+        for (int f = 0; f < d_used; ++f) s_x[f * XS + threadIdx.x] = i < n ? x[(int64_t)f * ldx + i] : 0.0f;
+        double Fv = f0;
+        for (int ch = 0; ch < nchunks; ++ch) {
+            const int t0 = ch * tpc;
+            const int tc = min(tpc, T - t0);
+            if (nchunks > 1 || !staged) {
+                __syncthreads();
+                for (int q = threadIdx.x; q < tc * NLEAF; q += blockDim.x)
+                    s_leaf[q] = leaves[(size_t)t0 * NLEAF + q];
+                if (!kAll)
+                    for (int q = threadIdx.x; q < tc * NIN; q += blockDim.x)
+                        s_rec[q] = rec[(size_t)t0 * NIN + q];
+                staged = true;
+            }
+            __syncthreads();
+            if constexpr (kAll) {
+                int t = 0;
+                for (; t + kApplyBatch <= tc; t += kApplyBatch) {
+                    uint2 r[kApplyBatch][NIN];
+#pragma unroll
+                    for (int u = 0; u < kApplyBatch; ++u)
+#pragma unroll
+                        for (int k = 0; k < NIN; ++k) r[u][k] = rec[(size_t)(t0 + t + u) * NIN + k];
+                    double lv[kApplyBatch];
+#pragma unroll
+                    for (int u = 0; u < kApplyBatch; ++u)
+                        lv[u] = s_leaf[(t + u) * NLEAF + float_leaf<D>(xme, XS, r[u])];
+#pragma unroll
+                    for (int u = 0; u < kApplyBatch; ++u) Fv += lv[u];
+                }
+                for (; t < tc; ++t) {
+                    uint2 r[NIN];
+#pragma unroll
+                    for (int k = 0; k < NIN; ++k) r[k] = rec[(size_t)(t0 + t) * NIN + k];
+                    Fv += s_leaf[t * NLEAF + float_leaf<D>(xme, XS, r)];
+                }
+            } else {
+                for (int t = 0; t < tc; ++t) {
+                    int node = 1;
+#pragma unroll
+                    for (int lvl = 0; lvl < D; ++lvl) {
+                        const uint2 r = s_rec[t * NIN + node - 1];
+                        node = 2 * node + (xme[r.x * XS] >= __uint_as_float(r.y) ? 1 : 0);
+                    }
+                    Fv += s_leaf[t * NLEAF + node - NLEAF];
+                }
+            }
+        }
+        if (i < n) {
+            prob[i] = (float)(1.0 / (1.0 + exp(-2.0 * Fv)));
+            if (score) score[i] = Fv;
+        }
+    }
+}
+
 __global__ __launch_bounds__(256) void encode_kernel(const float *__restrict__ x, int64_t ldx,
                                                      int64_t n, int d,
                                                      const float *__restrict__ bounds, int nbins,
@@ -1731,7 +1831,14 @@ hipError_t prepare_kernels(size_t max_lds) {
                             allow_lds(leaf_kernel<true, 4>, max_lds),
                             allow_lds(apply_shallow_kernel<1>, max_lds),
                             allow_lds(apply_shallow_kernel<2>, max_lds),
-                            allow_lds(apply_shallow_kernel<3>, max_lds)};
+                            allow_lds(apply_shallow_kernel<3>, max_lds),
+                            allow_lds(apply_float_kernel<1>, max_lds),
+                            allow_lds(apply_float_kernel<2>, max_lds),
+                            allow_lds(apply_float_kernel<3>, max_lds),
+                            allow_lds(apply_float_kernel<4>, max_lds),
+                            allow_lds(apply_float_kernel<5>, max_lds),
+                            allow_lds(apply_float_kernel<6>, max_lds),
+                            allow_lds(apply_float_kernel<7>, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -2104,6 +2211,53 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
     apply_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(xb, ldb, n, as.d_used, cuts, leaves,
                                                             n_trees, depth, as.trees_per_chunk,
                                                             f0, prob, score);
+    return hipGetLastError();
+}
+
+ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, int cu_count,
+                            size_t max_lds, int threads) {
+    ApplyShape as{};
+    as.d_used = d_used;
+    as.shallow = depth <= kApplyShallowDepth;
+    const int nin = (1 << depth) - 1, nleaf = 1 << depth;
+    const size_t lds_cap = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
+    // one event per thread: the tile of float32 values takes at most 96 KiB
+    int t = threads > 0 ? threads : 512;
+    while (t > 64 && (size_t)d_used * t * 4 > 96 * 1024) t -= 64;
+    as.threads = t;
+    const size_t xtile = (size_t)d_used * t * 4;
+    const size_t per_tree = (size_t)nleaf * 8 + (as.shallow ? 0 : (size_t)nin * 8);
+    const size_t room = lds_cap > xtile + 64 ? lds_cap - xtile - 64 : 0;
+    int64_t tpc = (int64_t)(room / per_tree);
+    if (tpc < 1) tpc = 1;
+    if (tpc > n_trees) tpc = n_trees;
+    as.trees_per_chunk = (int)tpc;
+    as.lds_bytes = (size_t)tpc * per_tree + xtile;
+    const int64_t ntiles = (n + t - 1) / t;
+    int64_t blocks = (int64_t)cu_count * 4;
+    if (blocks > ntiles) blocks = ntiles;
+    if (blocks < 1) blocks = 1;
+    as.blocks = (int)blocks;
+    return as;
+}
+
+hipError_t launch_apply_float(const ApplyShape &as, const float *x, int64_t ldx, int64_t n,
+                              const uint2 *rec, const double *leaves, int n_trees, int depth,
+                              double f0, float *prob, double *score, hipStream_t s) {
+#define FBDT_APPLY_F(DV)                                                                        \
+    apply_float_kernel<DV><<<as.blocks, as.threads, as.lds_bytes, s>>>(                         \
+        x, ldx, n, as.d_used, rec, leaves, n_trees, as.trees_per_chunk, f0, prob, score)
+    switch (depth) {
+    case 1: FBDT_APPLY_F(1); break;
+    case 2: FBDT_APPLY_F(2); break;
+    case 3: FBDT_APPLY_F(3); break;
+    case 4: FBDT_APPLY_F(4); break;
+    case 5: FBDT_APPLY_F(5); break;
+    case 6: FBDT_APPLY_F(6); break;
+    case 7: FBDT_APPLY_F(7); break;
+    default: return hipErrorInvalidValue;
+    }
+#undef FBDT_APPLY_F
     return hipGetLastError();
 }
 

@@ -455,6 +455,78 @@ def test_apply_workload5_launch_configuration_matches_oracle():
     assert np.all((pa > 0.0) & (pa < 1.0))
 
 
+# ----------------------------------------------------------- float apply
+def _edge_events(b, extra, rng):
+    """Every boundary, its float32 neighbours above and below, +-0 and +-inf,
+    then events drawn from a sample; float32 [d][m]."""
+    vals = []
+    for j in range(b.shape[0]):
+        col = np.concatenate([b[j], np.nextafter(b[j], np.float32(np.inf)),
+                              np.nextafter(b[j], np.float32(-np.inf)),
+                              np.array([0.0, -0.0, np.inf, -np.inf], np.float32)])
+        vals.append(col.astype(np.float32))
+    m = max(len(v) for v in vals)
+    x = np.stack([np.resize(v, m) for v in vals]).astype(np.float32)
+    x = np.concatenate([x, extra[:, rng.integers(0, extra.shape[1], 20_000)]], axis=1)
+    return np.ascontiguousarray(x)
+
+
+@pytest.mark.parametrize("T,D", [(50, 1), (400, 3), (30, 4), (20, 7)])
+def test_apply_float_matches_binned_apply_and_oracle(T, D):
+    """Section 2.2's inverse transform: fbdt_apply_float on raw values equals
+    fbdt_apply on the codes of fbdt_bin_transform bit for bit, and the
+    oracle's threshold apply, on values at, just above and just below every
+    boundary of a training sample with tied and discrete features."""
+    B = 256
+    ds = make_training_set(4, n_events=40_001)
+    d = ds["x"].shape[0]
+    rng = np.random.default_rng(T + D)
+    gb, _ = fb.bin(dev(ds["x"]), B)
+    x = _edge_events(gb, ds["x"], rng)
+    n = x.shape[1]
+    say(f"apply_float T={T} D={D} n={n}")
+    f = random_forest(T, D, d, B, seed=3 * T + D)
+    model = fb.Model.from_arrays(f["cut_feature"], f["cut_bin"], f["leaf"], f["f0"], d, B,
+                                 boundaries=gb)
+    xs = dev(x)
+    sf = torch.empty(n, dtype=torch.float64, device="cuda")
+    pf = fb.apply_float(model, xs, score=sf).cpu().numpy()
+    codes = fb.bin_transform(xs, gb)
+    sb = torch.empty(n, dtype=torch.float64, device="cuda")
+    pb = fb.apply(model, codes, score=sb).cpu().numpy()
+    assert np.array_equal(sf.cpu().numpy(), sb.cpu().numpy())
+    assert np.array_equal(pf, pb)
+    om = O.Model(D, B, d, f["f0"], f["cut_feature"], f["cut_bin"], np.zeros_like(f["leaf"][:, 1:]),
+                 f["leaf"])
+    op, oF = O.apply_thresholds(om, x, gb)
+    assert np.array_equal(sf.cpu().numpy(), oF)
+    np.testing.assert_array_max_ulp(pf, op, maxulp=1)
+
+
+def test_apply_float_on_a_fitted_model_with_row_stride():
+    """A fitted model gets its training boundaries; fresh events in a padded
+    row layout (ldx > n) score as their codes do."""
+    spec = CONFIGS[1]
+    ds = make_training_set(1)
+    bounds, codes = fb.bin(dev(ds["x"]), spec.n_bins)
+    model = fb.fit(codes, dev(ds["y"]), spec.n_bins, spec.depth, spec.n_trees, spec.shrinkage,
+                   spec.subsample, spec.fit_seed)
+    with pytest.raises(fb.FbdtError):
+        fb.apply_float(model, dev(ds["x"]))          # no boundaries yet
+    model.set_boundaries(bounds)
+    d, n = ds["x"].shape
+    big = torch.zeros((d, n + 37), dtype=torch.float32, device="cuda")
+    big[:, :n] = dev(ds["x"])
+    xv = big[:, :n]
+    pf = fb.apply_float(model, xv).cpu().numpy()
+    pb = fb.apply(model, codes).cpu().numpy()
+    assert np.array_equal(pf, pb)
+    bad = bounds.copy()
+    bad[0, 3] = bad[0, 2] - 1.0
+    with pytest.raises(fb.FbdtError):
+        model.set_boundaries(bad)
+
+
 # ------------------------------------------------------------------ errors
 def test_errors_are_reported():
     n, d, B = 1000, 3, 16

@@ -166,6 +166,50 @@ def test_hand_example_two_trees(eta):
         assert int(m.cut_bin[1, 0]) == int(ex["tree2_cut_eta01"][0])
 
 
+def test_hand_example_threshold_apply():
+    """The depth-1 hand example's first tree (cut c = 1 at eta = 1) applied
+    to the raw values: the test is x >= the first boundary, 3."""
+    x, y, ex = _hand_case()
+    b, xb = O.bin_features(x, 4)
+    m = O.fit(xb, y, np.ones(8, np.float32), depth=1, n_trees=1, shrinkage=1.0,
+              subsample=1.0, seed=0, n_bins=4)
+    p, _ = O.apply_thresholds(m, x, b)
+    assert np.allclose(p[:2], ex["tree1_p_eta1"][0], atol=1e-7)
+    assert np.allclose(p[2:], ex["tree1_p_eta1"][1], atol=1e-7)
+
+
+def test_threshold_apply_equals_binned_apply_on_edge_values():
+    """Section 2.2's inverse transform: testing x >= b_j,c gives the same leaf
+    as testing bin(x) >= c, with bin(x) = searchsorted(b_j, x, 'right') (the
+    library routine), for values on, just below and just above every
+    boundary, repeated boundaries (tied training values), +-0 and +-inf."""
+    from synth import make_training_set, random_forest
+    xt = make_training_set(4, n_events=3001)["x"][:10]
+    xt[3, :100] = np.inf
+    xt[4, :100] = -np.inf
+    xt[5, ::2] = -0.0
+    B = 32
+    b = np.stack([O.quantile_boundaries(xt[j], B) for j in range(10)])
+    vals = []
+    for j in range(10):
+        col = np.concatenate([b[j], np.nextafter(b[j], np.float32(np.inf)),
+                              np.nextafter(b[j], np.float32(-np.inf)),
+                              np.array([0.0, -0.0, np.inf, -np.inf], np.float32)])
+        vals.append(col.astype(np.float32))
+    m = max(len(v) for v in vals)
+    x = np.stack([np.resize(v, m) for v in vals]).astype(np.float32)
+    rng = np.random.default_rng(1)
+    x = np.concatenate([x, xt[:, rng.integers(0, xt.shape[1], 500)]], axis=1)
+    codes = np.stack([np.searchsorted(b[j], x[j], side="right") for j in range(10)])
+    for D in (1, 3, 6):
+        f = random_forest(20, D, 10, B, seed=D)
+        om = O.Model(D, B, 10, f["f0"], f["cut_feature"], f["cut_bin"],
+                     np.zeros_like(f["leaf"][:, 1:]), f["leaf"])
+        _, Ft = O.apply_thresholds(om, x, b)
+        _, Fb = O.apply(om, codes.astype(np.uint8))
+        assert np.array_equal(Ft, Fb)
+
+
 # ------------------------------------------------------------- histograms
 def _brute_hist(xb, node, w, y, layer, n_bins):
     d, n = xb.shape
