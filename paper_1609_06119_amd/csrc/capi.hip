@@ -14,7 +14,6 @@
 #include <cstring>
 #include <mutex>
 #include <string>
-#include <thread>
 #include <vector>
 
 using namespace fbdt;
@@ -390,40 +389,45 @@ int fbdt_bin(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
         return rc;
     if (!boundaries) return fail(FBDT_E_INVAL, "boundaries is NULL");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    std::vector<float> host((size_t)n * d);
-    HIP_TRY(hipMemcpy2DAsync(host.data(), (size_t)n * sizeof(float), x, (size_t)ldx * sizeof(float),
-                             (size_t)n * sizeof(float), (size_t)d, hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
-    // Exact order statistics: boundary k of feature j is the value of rank
-    // floor(k n / B) of the feature (section 2.2).  Sorted on the host.
-    std::vector<float> bounds((size_t)d * (n_bins - 1));
-    std::atomic<int> nan_seen{0};
-    unsigned hw = std::thread::hardware_concurrency();
-    int nthreads = (int)std::min<unsigned>(std::max(1u, hw), 16u);
-    nthreads = std::min(nthreads, (int)d);
-    auto work = [&](int tid) {
-        std::vector<float> col;
-        for (int j = tid; j < d; j += nthreads) {
-            const float *src = host.data() + (size_t)j * n;
-            col.assign(src, src + n);
-            for (float v : col)
-                if (v != v) {
-                    nan_seen = 1;
-                    return;
-                }
-            std::sort(col.begin(), col.end());
-            for (int k = 1; k < n_bins; ++k)
-                bounds[(size_t)j * (n_bins - 1) + (k - 1)] =
-                    col[(size_t)(((int64_t)k * n) / n_bins)];
-        }
-    };
-    std::vector<std::thread> pool;
-    for (int t = 1; t < nthreads; ++t) pool.emplace_back(work, t);
-    work(0);
-    for (auto &th : pool) th.join();
-    if (nan_seen) return fail(FBDT_E_NAN, "NaN among the feature values");
-    if ((rc = encode_with(x, n, d, ldx, n_bins, bounds.data(), xb, ldb, s))) return rc;
-    std::memcpy(boundaries, bounds.data(), bounds.size() * sizeof(float));
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    // Exact order statistics on the device: boundary k of feature j is the
+    // value of rank floor(k n / B) of the feature (section 2.2), read off a
+    // radix sort of the feature's values; then every value is encoded.
+    QuantileScratch qs;
+    HIP_TRY(quantile_scratch(n, d, &qs));
+    const size_t nb = (size_t)d * (n_bins - 1);
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    Carver cv;
+    uint64_t *keys_a, *keys_b;
+    char *temp;
+    float *bounds;
+    int *err;
+    cv.add(&keys_a, qs.key_elems);
+    cv.add(&keys_b, qs.key_elems);
+    cv.add(&temp, std::max<size_t>(qs.temp_bytes, 1));
+    cv.add(&bounds, nb);
+    cv.add(&err, 1);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+    HIP_TRY(launch_fill_u32(err, 0u, 1, s));
+    HIP_TRY(launch_quantile_boundaries(x, ldx, n, d, n_bins, qs, keys_a, keys_b, temp, bounds, err,
+                                       s));
+    int h_err = 0;
+    if ((rc = read_err(err, s, &h_err))) return rc;
+    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values");
+    {
+        Timed t(FBDT_K_ENCODE, s, (double)n * d * 5.0);
+        HIP_TRY(launch_encode(x, ldx, n, d, bounds, n_bins, xb, ldb, err, s));
+        t.done();
+    }
+    std::vector<float> host(nb);
+    HIP_TRY(hipMemcpyAsync(host.data(), bounds, nb * sizeof(float), hipMemcpyDeviceToHost, s));
+    if ((rc = read_err(err, s, &h_err))) return rc;
+    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values");
+    std::memcpy(boundaries, host.data(), nb * sizeof(float));
     return FBDT_OK;
 }
 

@@ -248,6 +248,24 @@ hipError_t launch_apply_float(const ApplyShape &as, const float *x, int64_t ldx,
                               const uint2 *rec, const double *leaves, int n_trees, int depth,
                               double f0, float *prob, double *score, hipStream_t s);
 
+// Equal-frequency boundaries on the device: for every feature the value of
+// rank floor(k n / B), k = 1 .. B - 1, from a radix sort of the feature's
+// values (batches of features whose keys together stay <= kQuantileBatchKeys).
+constexpr int64_t kQuantileBatchKeys = (int64_t)1 << 27;
+struct QuantileScratch {
+    int batch_features;   // features sorted together
+    size_t key_elems;     // 64-bit keys per buffer (two buffers)
+    size_t temp_bytes;    // sort scratch
+};
+int quantile_batch_features(int64_t n, int d);
+hipError_t quantile_scratch(int64_t n, int d, QuantileScratch *qs);
+// x: device float32 [d][ldx]; bounds: device float32 [d][n_bins - 1]; err
+// receives kErrNan if any value is NaN (the boundaries are then undefined).
+hipError_t launch_quantile_boundaries(const float *x, int64_t ldx, int64_t n, int d, int n_bins,
+                                      const QuantileScratch &qs, uint64_t *keys_a,
+                                      uint64_t *keys_b, void *temp, float *bounds, int *err,
+                                      hipStream_t s);
+
 hipError_t launch_encode(const float *x, int64_t ldx, int64_t n, int d, const float *bounds,
                          int n_bins, uint8_t *xb, int64_t ldb, int *err, hipStream_t s);
 
