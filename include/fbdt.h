@@ -133,6 +133,23 @@ int fbdt_apply(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d, int
 int fbdt_apply_float(const fbdt_model *m, const float *x, int64_t n, int32_t d, int64_t ldx,
                      float *prob, double *score, void *stream);
 
+/*
+ * Global feature importance (section 4.3): the separation gains of all
+ * nodes of all trees summed per cut feature, in tree order then heap order.
+ * importance: host float64 [the model's feature count] (output).
+ */
+int fbdt_feature_importance(const fbdt_model *m, double *importance);
+
+/*
+ * Importance of every feature for every event (section 4.3): the gains of
+ * the nodes on the event's path through the trees summed per cut feature,
+ * tree by tree in float64.  xb: device uint8 [d][ldb] (as fbdt_apply);
+ * importance: device float64 [d][ldi] (output, ldi >= n; rows of features
+ * beyond the model's are zero).  Stream-ordered.
+ */
+int fbdt_event_importance(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d,
+                          int64_t ldb, double *importance, int64_t ldi, void *stream);
+
 /* Borrowed host view of a model, valid until fbdt_model_free. */
 int fbdt_model_export(const fbdt_model *m, fbdt_model_view *view);
 

@@ -11,6 +11,8 @@ from .api import (  # noqa: F401
     best_cuts,
     bin,
     bin_transform,
+    event_importance,
+    feature_importance,
     fit,
     histogram,
     leaf_values,

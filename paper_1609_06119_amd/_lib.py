@@ -25,7 +25,7 @@ KERNEL_KINDS = {"histogram": 0, "best_cuts": 1, "tree_prep": 2, "leaf": 3, "appl
 EXPORTED = (
     "fbdt_bin", "fbdt_bin_transform", "fbdt_fit", "fbdt_apply", "fbdt_apply_float",
     "fbdt_model_export", "fbdt_model_import", "fbdt_model_set_boundaries", "fbdt_model_free",
-    "fbdt_last_error", "fbdt_tree_weights",
+    "fbdt_last_error", "fbdt_tree_weights", "fbdt_feature_importance", "fbdt_event_importance",
     "fbdt_histogram", "fbdt_best_cuts", "fbdt_route", "fbdt_leaf_values",
     "fbdt_timing_enable", "fbdt_timing_read", "fbdt_set_option",
 )
@@ -69,6 +69,8 @@ def _declare(lib):
         "fbdt_apply": (C.c_int, [P, P, I64, I32, I64, P, P, P]),
         "fbdt_apply_float": (C.c_int, [P, P, I64, I32, I64, P, P, P]),
         "fbdt_model_set_boundaries": (C.c_int, [P, P]),
+        "fbdt_feature_importance": (C.c_int, [P, P]),
+        "fbdt_event_importance": (C.c_int, [P, P, I64, I32, I64, P, I64, P]),
         "fbdt_model_export": (C.c_int, [P, C.POINTER(ModelView)]),
         "fbdt_model_import": (C.c_int, [C.POINTER(ModelView), C.POINTER(P)]),
         "fbdt_model_free": (None, [P]),

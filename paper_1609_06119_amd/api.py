@@ -236,6 +236,30 @@ def apply_float(model: Model, x: torch.Tensor, prob: torch.Tensor | None = None,
     return prob
 
 
+def feature_importance(model: Model) -> np.ndarray:
+    """Summed separation gain per feature over every node of every tree."""
+    n_features = model.export()["n_features"]
+    out = np.zeros(n_features, np.float64)
+    check("fbdt_feature_importance",
+          lib().fbdt_feature_importance(model.handle, out.ctypes.data_as(C.c_void_p)))
+    return out
+
+
+def event_importance(model: Model, codes: Codes, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Per-event importance float64 [d][n]: the gains on each event's path,
+    summed per cut feature."""
+    n, d = codes.n, codes.d
+    out = out if out is not None else torch.empty((d, n), dtype=torch.float64,
+                                                  device=codes.data.device)
+    if out.dtype != torch.float64 or out.dim() != 2 or out.shape[0] != d or out.shape[1] < n \
+            or out.stride(1) != 1 or not out.is_cuda:
+        raise ValueError("out must be a float64 CUDA tensor [d][>= n] with unit stride along events")
+    check("fbdt_event_importance",
+          lib().fbdt_event_importance(model.handle, _ptr(codes.data), n, d, codes.ldb, _ptr(out),
+                                      out.stride(0), _stream()))
+    return out
+
+
 def tree_weights(y, v, F, seed: int, tree: int, alpha: float, w_out=None) -> torch.Tensor:
     n = int(y.numel())
     _need(y, torch.int8, "y")

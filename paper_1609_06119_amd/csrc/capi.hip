@@ -32,6 +32,7 @@ struct fbdt_model {
         int nodes_stride;   // tile stride the node records were made for (0: none)
         uint32_t *nodes;    // [T][16] node records of shallow forests, or null
         uint2 *frec;        // [T][2^D - 1] (feature, threshold) for float apply, or null
+        double *gains;      // [T][2^D - 1] separation gains, or null
     };
     std::mutex mu;
     std::vector<DeviceCopy> copies;
@@ -776,6 +777,7 @@ void fbdt_model_free(fbdt_model *m) {
             (void)hipFree(c.leaves);
             if (c.nodes) (void)hipFree(c.nodes);
             if (c.frec) (void)hipFree(c.frec);
+            if (c.gains) (void)hipFree(c.gains);
         }
     }
     if (cur >= 0) (void)hipSetDevice(cur);
@@ -815,7 +817,7 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
             std::vector<uint16_t> packed((size_t)T * nin);
             for (size_t k = 0; k < packed.size(); ++k)
                 packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
-            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr};
+            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
             HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
             if (hipMalloc(&c.leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
                 (void)hipFree(c.cuts);
@@ -853,6 +855,82 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     return FBDT_OK;
 }
 
+// The model's device copy on `dev` (cuts and leaves), created on first use.
+// Call with m->mu held.
+static int device_copy(fbdt_model *m, int dev, fbdt_model::DeviceCopy **out) {
+    for (auto &c : m->copies)
+        if (c.device == dev) {
+            *out = &c;
+            return FBDT_OK;
+        }
+    const size_t T = m->n_trees, nin = ((size_t)1 << m->depth) - 1;
+    const size_t nleaf = (size_t)1 << m->depth;
+    fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
+    std::vector<uint16_t> packed(T * nin);
+    for (size_t k = 0; k < packed.size(); ++k)
+        packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
+    HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
+    if (hipMalloc(&c.leaves, T * nleaf * sizeof(double)) != hipSuccess) {
+        (void)hipFree(c.cuts);
+        return fail(FBDT_E_DEVICE, "out of device memory");
+    }
+    m->copies.push_back(c);
+    fbdt_model::DeviceCopy *cp = &m->copies.back();
+    HIP_TRY(hipMemcpy(cp->cuts, packed.data(), packed.size() * sizeof(uint16_t),
+                      hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(cp->leaves, m->leaf.data(), T * nleaf * sizeof(double),
+                      hipMemcpyHostToDevice));
+    *out = cp;
+    return FBDT_OK;
+}
+
+int fbdt_feature_importance(const fbdt_model *m, double *importance) {
+    if (!m || !importance) return fail(FBDT_E_INVAL, "NULL argument");
+    const size_t nin = ((size_t)1 << m->depth) - 1;
+    std::vector<double> imp((size_t)m->n_features, 0.0);
+    for (size_t k = 0; k < (size_t)m->n_trees * nin; ++k) imp[m->cut_feature[k]] += m->gain[k];
+    std::memcpy(importance, imp.data(), imp.size() * sizeof(double));
+    return FBDT_OK;
+}
+
+int fbdt_event_importance(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d,
+                          int64_t ldb, double *importance, int64_t ldi, void *stream) {
+    int rc;
+    if (!mc) return fail(FBDT_E_INVAL, "model is NULL");
+    if ((rc = check_codes(xb, n, d, ldb))) return rc;
+    if (!importance) return fail(FBDT_E_INVAL, "importance is NULL");
+    if (ldi < n) return fail(FBDT_E_INVAL, "ldi = %lld < n", (long long)ldi);
+    fbdt_model *m = const_cast<fbdt_model *>(mc);
+    if (d < m->n_features)
+        return fail(FBDT_E_SHAPE, "d = %d < the model's %d features", d, m->n_features);
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = m->n_trees, D = m->depth;
+    const size_t nin = ((size_t)1 << D) - 1;
+    const ApplyShape as = plan_importance(n, m->n_features, T, D, di.cu_count, di.max_lds);
+    if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
+        return fail(FBDT_E_INVAL, "event importance needs %zu bytes of LDS, the device has %zu",
+                    as.lds_bytes, di.max_lds);
+    const uint16_t *cuts = nullptr;
+    const double *gains = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(m->mu);
+        fbdt_model::DeviceCopy *copy = nullptr;
+        if ((rc = device_copy(m, dev, &copy))) return rc;
+        if (!copy->gains) {
+            HIP_TRY(hipMalloc(&copy->gains, (size_t)T * nin * sizeof(double)));
+            HIP_TRY(hipMemcpy(copy->gains, m->gain.data(), (size_t)T * nin * sizeof(double),
+                              hipMemcpyHostToDevice));
+        }
+        cuts = copy->cuts;
+        gains = copy->gains;
+    }
+    HIP_TRY(launch_importance(as, xb, ldb, n, cuts, gains, T, D, importance, ldi, d, s));
+    return FBDT_OK;
+}
+
 int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d, int64_t ldx,
                      float *prob, double *score, void *stream) {
     int rc;
@@ -884,7 +962,7 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
         for (auto &c : m->copies)
             if (c.device == dev) copy = &c;
         if (!copy) {
-            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr};
+            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
             std::vector<uint16_t> packed((size_t)T * nin);
             for (size_t k = 0; k < packed.size(); ++k)
                 packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));

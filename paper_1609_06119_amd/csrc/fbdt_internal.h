@@ -239,6 +239,15 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
                         int n_trees, int depth, double f0, float *prob, double *score,
                         hipStream_t s);
 
+// Per-event importance [d_out][ldi] (float64) of binned events: the gains of
+// the nodes on each event's path summed per cut feature, tree by tree.
+// cuts: [T][2^D-1] packed (feature | bin << 8); gains: [T][2^D-1].
+ApplyShape plan_importance(int64_t n, int d_used, int n_trees, int depth, int cu_count,
+                           size_t max_lds);
+hipError_t launch_importance(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
+                             const uint16_t *cuts, const double *gains, int n_trees, int depth,
+                             double *imp, int64_t ldi, int d_out, hipStream_t s);
+
 // Traversal of float32 events [d][ldx] with value thresholds.  rec: [T][2^D-1]
 // (feature, float bits of the threshold) per heap node.  as.shallow marks
 // depth <= kApplyShallowDepth (every node tested, records by scalar loads).

@@ -1633,6 +1633,58 @@ __global__ __launch_bounds__(1024) void apply_shallow_kernel(
     }
 }
 
+// Importance of every feature for every event (section 4.3): each node on
+// an event's path adds its separation gain to the importance of the node's
+// cut feature, tree by tree in float64.  A workgroup stages a tile of codes
+// (one event per thread) and chunks of the forest (packed cut and gain) in
+// LDS; each thread keeps its event's accumulators in an LDS column.
+__global__ __launch_bounds__(256) void importance_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d_used,
+    const uint16_t *__restrict__ cuts, const double *__restrict__ gains, int T, int depth,
+    int tpc, double *__restrict__ imp, int64_t ldi, int d_out) {
+    extern __shared__ double smem[];
+    const int nin = (1 << depth) - 1;
+    const int nt = blockDim.x;
+    double *s_gain = smem;                            // [tpc][nin]
+    double *s_acc = s_gain + (size_t)tpc * nin;       // [d_used][nt]
+    uint16_t *s_cut = reinterpret_cast<uint16_t *>(s_acc + (size_t)d_used * nt);   // [tpc][nin]
+    uint8_t *s_x = reinterpret_cast<uint8_t *>(s_cut + (((size_t)tpc * nin + 3) & ~(size_t)3));
+    const int XS = nt + 4;
+    const int nchunks = (T + tpc - 1) / tpc;
+    const int64_t ntiles = (n + nt - 1) / nt;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t i = tile * nt + threadIdx.x;
+        __syncthreads();
+        for (int f = 0; f < d_used; ++f) {
+            s_x[f * XS + threadIdx.x] = i < n ? xb[(int64_t)f * ldb + i] : 0;
+            s_acc[f * nt + threadIdx.x] = 0.0;
+        }
+        for (int ch = 0; ch < nchunks; ++ch) {
+            const int t0 = ch * tpc;
+            const int tc = min(tpc, T - t0);
+            __syncthreads();
+            for (int q = threadIdx.x; q < tc * nin; q += nt) {
+                s_gain[q] = gains[(size_t)t0 * nin + q];
+                s_cut[q] = cuts[(size_t)t0 * nin + q];
+            }
+            __syncthreads();
+            for (int t = 0; t < tc; ++t) {
+                int node = 1;
+                for (int lvl = 0; lvl < depth; ++lvl) {
+                    const int k = t * nin + node - 1;
+                    const uint16_t cc = s_cut[k];
+                    const int f = cc & 0xff;
+                    s_acc[f * nt + threadIdx.x] += s_gain[k];
+                    node = 2 * node + (s_x[f * XS + threadIdx.x] >= (cc >> 8) ? 1 : 0);
+                }
+            }
+        }
+        if (i < n)
+            for (int f = 0; f < d_out; ++f)
+                imp[(int64_t)f * ldi + i] = f < d_used ? s_acc[f * nt + threadIdx.x] : 0.0;
+    }
+}
+
 // Leaf (0 .. 2^D - 1) of a tree of depth D <= 3 reached by this thread's
 // event: every node tested (x >= threshold), then the path picked from the
 // decisions; r[k] = (feature, threshold bits) of heap node k + 1.
@@ -1840,7 +1892,8 @@ hipError_t prepare_kernels(size_t max_lds) {
                             allow_lds(apply_float_kernel<4>, max_lds),
                             allow_lds(apply_float_kernel<5>, max_lds),
                             allow_lds(apply_float_kernel<6>, max_lds),
-                            allow_lds(apply_float_kernel<7>, max_lds)};
+                            allow_lds(apply_float_kernel<7>, max_lds),
+                            allow_lds(importance_kernel, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -2218,6 +2271,42 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
     apply_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(xb, ldb, n, as.d_used, cuts, leaves,
                                                             n_trees, depth, as.trees_per_chunk,
                                                             f0, prob, score);
+    return hipGetLastError();
+}
+
+ApplyShape plan_importance(int64_t n, int d_used, int n_trees, int depth, int cu_count,
+                           size_t max_lds) {
+    ApplyShape as{};
+    as.d_used = d_used;
+    const int nin = (1 << depth) - 1;
+    const size_t lds_cap = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
+    // one event per thread: its float64 accumulator column and code column
+    // take at most 96 KiB over the workgroup, the forest chunk the rest
+    int t = 256;
+    while (t > 64 && (size_t)d_used * ((size_t)t * 8 + t + 4) > 96 * 1024) t -= 64;
+    as.threads = t;
+    const size_t fixed = (size_t)d_used * ((size_t)t * 8 + t + 4) + 64;
+    const size_t per_tree = (size_t)nin * 10;
+    const size_t room = lds_cap > fixed ? lds_cap - fixed : 0;
+    int64_t tpc = (int64_t)(room / per_tree);
+    if (tpc < 1) tpc = 1;
+    if (tpc > n_trees) tpc = n_trees;
+    as.trees_per_chunk = (int)tpc;
+    as.lds_bytes = (size_t)tpc * nin * 8 + (size_t)d_used * t * 8 +
+                   ((((size_t)tpc * nin) + 3) & ~(size_t)3) * 2 + (size_t)d_used * (t + 4);
+    const int64_t ntiles = (n + t - 1) / t;
+    int64_t blocks = (int64_t)cu_count * 4;
+    if (blocks > ntiles) blocks = ntiles;
+    if (blocks < 1) blocks = 1;
+    as.blocks = (int)blocks;
+    return as;
+}
+
+hipError_t launch_importance(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
+                             const uint16_t *cuts, const double *gains, int n_trees, int depth,
+                             double *imp, int64_t ldi, int d_out, hipStream_t s) {
+    importance_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(
+        xb, ldb, n, as.d_used, cuts, gains, n_trees, depth, as.trees_per_chunk, imp, ldi, d_out);
     return hipGetLastError();
 }
 

@@ -527,6 +527,38 @@ def test_apply_float_on_a_fitted_model_with_row_stride():
         model.set_boundaries(bad)
 
 
+# ------------------------------------------------------------- importance
+def test_feature_and_event_importance_match_oracle():
+    """Section 4.3: global importance (gains summed per feature) and each
+    event's importance (gains on its path) of a fitted model and of a random
+    deep forest, against the oracle, exactly (the same float64 sums in the
+    same order)."""
+    spec = CONFIGS[2]
+    ds = make_training_set(2, n_events=60_013)
+    B = spec.n_bins
+    bounds, codes = fb.bin(dev(ds["x"]), B)
+    model = fb.fit(codes, dev(ds["y"]), B, spec.depth, 30, spec.shrinkage, spec.subsample,
+                   spec.fit_seed)
+    gm = model.export()
+    om = _oracle_model(gm)
+    assert np.array_equal(fb.feature_importance(model), O.feature_importance(om))
+    xb = codes.numpy()
+    ei = fb.event_importance(model, codes).cpu().numpy()
+    assert np.array_equal(ei, O.event_importance(om, xb))
+    rng = np.random.default_rng(11)
+    T, D, d, n = 20, 7, 30, 5003
+    f = random_forest(T, D, d, B, seed=12)
+    gain = rng.exponential(1.0, f["cut_feature"].shape)
+    model = fb.Model.from_arrays(f["cut_feature"], f["cut_bin"], f["leaf"], f["f0"], d, B,
+                                 gain=gain)
+    xr = rng.integers(0, B, (d + 3, n)).astype(np.uint8)     # more rows than features
+    codes = fb.Codes.from_numpy(xr)
+    ei = fb.event_importance(model, codes).cpu().numpy()
+    om = O.Model(D, B, d, f["f0"], f["cut_feature"], f["cut_bin"], gain, f["leaf"])
+    assert np.array_equal(ei[:d], O.event_importance(om, xr[:d]))
+    assert not ei[d:].any()
+
+
 # ------------------------------------------------------------------ errors
 def test_errors_are_reported():
     n, d, B = 1000, 3, 16

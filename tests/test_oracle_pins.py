@@ -112,6 +112,8 @@ def test_xor_table3():
     assert np.allclose(p[sig], ex["p_signal"][0], rtol=0, atol=1e-7)
     assert np.allclose(p[~sig], ex["p_background"][0], rtol=0, atol=1e-7)
     assert np.allclose(O.feature_importance(m), ex["importance"])
+    ei = O.event_importance(m, xb)
+    assert np.allclose(ei, np.array(ex["event_importance"])[:, None])
 
 
 # ------------------------------------------------ hand-worked depth-1 example
@@ -164,6 +166,20 @@ def test_hand_example_two_trees(eta):
         assert np.allclose(p1[[0, 7]], ex["tree1_p_eta01"], atol=1e-6)
         assert np.allclose(g2, ex["tree2_gains_eta01"], atol=1e-6)
         assert int(m.cut_bin[1, 0]) == int(ex["tree2_cut_eta01"][0])
+
+
+def test_hand_example_event_importance():
+    """Depth 1, two trees at eta = 1: every event passes the root of each tree,
+    so its importance is the sum of the two root gains (both on feature 0)."""
+    x, y, ex = _hand_case()
+    _, xb = O.bin_features(x, 4)
+    m = O.fit(xb, y, np.ones(8, np.float32), depth=1, n_trees=2, shrinkage=1.0,
+              subsample=1.0, seed=0, n_bins=4)
+    g1 = ex["tree1_gains"][int(ex["tree1_cut"][0]) - 1]
+    g2 = ex["tree2_gains_eta1"][int(ex["tree2_cut_eta1"][0]) - 1]
+    ei = O.event_importance(m, xb)
+    assert np.allclose(ei[0], g1 + g2, atol=1e-6)
+    assert np.allclose(O.feature_importance(m), [g1 + g2], atol=1e-6)
 
 
 def test_hand_example_threshold_apply():
