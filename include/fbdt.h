@@ -16,7 +16,9 @@
  *    read but never influence a result; the binning calls write the first n
  *    bytes of each row only.
  *  - Labels are int8: +1 signal, -1 background (section 1).  Weights are
- *    float32, finite and >= 0; NULL means unit weights.
+ *    float32 and finite; NULL means unit weights.  fbdt_fit accepts
+ *    negative event weights (section 4.1), as long as each class's total
+ *    weight is positive; the single steps take weights >= 0.
  *  - stream is a hipStream_t (NULL = the null stream).  Calls are
  *    stream-ordered; the ones documented as synchronising also wait for it.
  *  - Return value: FBDT_OK (0) or a negative FBDT_E_* code.  On error the
@@ -45,7 +47,7 @@ enum fbdt_status {
     FBDT_E_INVAL = -1,  /* null pointer, size or parameter out of range      */
     FBDT_E_LABEL = -2,  /* a label not in {+1, -1}, or a class with no weight */
     FBDT_E_NAN = -3,    /* NaN among the float features                       */
-    FBDT_E_WEIGHT = -4, /* a weight < 0 or not finite                         */
+    FBDT_E_WEIGHT = -4, /* a weight not finite                                */
     FBDT_E_SHAPE = -5,  /* too few features for the model                     */
     FBDT_E_DEVICE = -6  /* HIP runtime error or out of device memory          */
 };
@@ -100,7 +102,8 @@ int fbdt_bin_transform(const float *x, int64_t n, int32_t d, int64_t ldx, int32_
  * all nodes and features in one pass, cumulative histograms, weighted Gini
  * separation gain, lowest-(feature, bin) argmax, and Newton-step terminal
  * weights.  xb: device uint8 [d][ldb]; y: device int8 [n]; w: device
- * float32 [n] or NULL; score_out: optional device float64 [n] that receives
+ * float32 [n] or NULL (event weights, any sign; each class's total must be
+ * positive, else FBDT_E_LABEL); score_out: optional device float64 [n] that receives
  * the final score F of every event.  *out receives a new model (free with
  * fbdt_model_free).  Synchronises the stream before returning.
  */
@@ -176,7 +179,7 @@ const char *fbdt_last_error(void);
 /*
  * Re-weighting of one tree (sections 1.3, 1.4): for every event,
  * y~ = 2y / (1 + exp(2 y F)); sampled iff the (tree * n + i)-th SplitMix64
- * output of seed, top 53 bits over 2^53, is < alpha; w_out = fl32(v |y~|)
+ * output of seed, top 53 bits over 2^53, is < alpha; w_out = |fl32(v |y~|)|
  * if sampled, else 0, carrying the class in its sign (+ signal,
  * - background).  y, v (NULL = unit), F: device [n]; w_out: device float32
  * [n].  Stream-ordered.

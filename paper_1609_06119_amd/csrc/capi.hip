@@ -156,12 +156,13 @@ struct GraphKey {
     double eta, alpha;
     uint64_t seed;
     int64_t fpg, chunks, threads, copies;
+    bool signed_w;
     bool operator==(const GraphKey &o) const {
         return xb == o.xb && y == o.y && w == o.w && n == o.n && ldb == o.ldb && d == o.d &&
                n_bins == o.n_bins && depth == o.depth && n_trees == o.n_trees &&
                scale == o.scale && lblocks == o.lblocks && eta == o.eta && alpha == o.alpha &&
                seed == o.seed && fpg == o.fpg && chunks == o.chunks && threads == o.threads &&
-               copies == o.copies;
+               copies == o.copies && signed_w == o.signed_w;
     }
 };
 
@@ -495,6 +496,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.w, npad);
     cv.add(&fb.yts, npad);
     if (w) cv.add(&fb.v, npad);
+    if (w) cv.add(&fb.vsign, npad);
     cv.add(&fb.node[0], npad);
     cv.add(&fb.node[1], npad);
     cv.add(&fb.partial, partial_elems);
@@ -511,7 +513,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.cand_gain, (size_t)max_nodes * d * S);
     cv.add(&fb.cand_cut, (size_t)max_nodes * d * S);
     cv.add(&fb.leaf_partial, (size_t)lblocks * 2 * nleaf);
-    cv.add(&fb.class_partial, 2 * kValidateBlocks);
+    cv.add(&fb.class_partial, 3 * kValidateBlocks);
     cv.add(&fb.f0, 2);
     cv.add(&fb.err, 1);
     cv.add(&fb.cut_feature, (size_t)T * nin);
@@ -539,11 +541,17 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     HIP_TRY(hipMemcpyAsync(h_f0, fb.f0, sizeof h_f0, hipMemcpyDeviceToHost, s));
     if ((rc = read_err(fb.err, s, &h_err))) return rc;
     if (h_err & kErrLabel) return fail(FBDT_E_LABEL, "labels must be +1 or -1");
-    if (h_err & kErrWeight) return fail(FBDT_E_WEIGHT, "weights must be finite and >= 0");
-    if (h_err & kErrClass) return fail(FBDT_E_LABEL, "a class has zero total weight");
-    // every histogram weight is fl32(v |y~|) < 2 v (1 + 2^-24): twice the
-    // total event weight bounds every bin total
+    if (h_err & kErrWeight) return fail(FBDT_E_WEIGHT, "weights must be finite");
+    if (h_err & kErrClass)
+        return fail(FBDT_E_LABEL, "a class has no positive total weight");
+    // every histogram weight has |w| = |fl32(v |y~|)| < 2 |v| (1 + 2^-24):
+    // twice the sum of |v| bounds the magnitude of every (partial) bin sum
     const int scale = histogram_scale(2.0 * h_f0[1] * (1.0 + 1e-6));
+    // negative event weights (section 4.1): their signs travel in bytes
+    // beside the weights, and the histogram passes subtract those events
+    const bool signed_w = (h_err & kNegWeights) != 0;
+    if (signed_w) HIP_TRY(launch_sign_bytes(w, n, npad, fb.vsign, s));
+    const uint8_t *vsign = signed_w ? fb.vsign : nullptr;
 
     const uint64_t seed = p->seed;
     const double alpha = p->subsample, eta = p->shrinkage;
@@ -578,8 +586,9 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                     Timed tm(FBDT_K_HISTOGRAM, st, hist_algorithmic_bytes(n, d, n_bins, l, true));
                     HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
                                              l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
-                                             l >= 1 ? fb.node[l & 1] : nullptr, fb.w, pc, l, true,
-                                             scale, fb.partial, fb.small[gl & 1], fb.err, st));
+                                             l >= 1 ? fb.node[l & 1] : nullptr, fb.w, vsign, pc, l,
+                                             true, scale, fb.partial, fb.small[gl & 1], fb.err,
+                                             st));
                     tm.done();
                 }
                 {
@@ -618,7 +627,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     if (opt_fit_graphs.load() && !(g_timing.load() & timed_kinds)) {
         const GraphKey key{xb, y, w, n, ldb, d, n_bins, D, T, scale, lblocks, eta, alpha, seed,
                            opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load(),
-                           opt_hist_copies.load()};
+                           opt_hist_copies.load(), signed_w};
         hipGraphExec_t exec = nullptr;
         for (auto &g : a.graphs)
             if (g.first == key) exec = g.second;
@@ -1076,7 +1085,7 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     const int scale = histogram_scale(h_wsum * (1.0 + 1e-6));
     {
         Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, layer, false));
-        HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node_pad, nullptr, w_pad,
+        HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node_pad, nullptr, w_pad, nullptr,
                                  ParentCuts{}, layer, false, scale, partial, small, err, s));
         tm.done();
     }

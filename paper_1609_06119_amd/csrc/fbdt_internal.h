@@ -12,11 +12,12 @@ namespace fbdt {
 // Bits of the device-side error word that kernels raise.
 enum : int {
     kErrLabel = 1,     // label not in {+1, -1}
-    kErrWeight = 2,    // weight < 0 or not finite
+    kErrWeight = 2,    // weight not finite
     kErrNan = 4,       // NaN feature value
     kErrBin = 8,       // bin code >= n_bins met by a histogram pass
     kErrRoute = 16,    // cut or node id out of range met while routing
-    kErrClass = 32,    // a class has zero total weight
+    kErrClass = 32,    // a class has no positive total weight
+    kNegWeights = 64,  // (not an error) some event weight is negative
 };
 
 // Launch shape of one histogram pass.
@@ -57,8 +58,9 @@ struct FitBuffers {
     double *cand_gain;    // [max nodes][d * slices] best gain of every (node, feature, slice)
     int *cand_cut;        // [max nodes][d * slices] and its bin
     double *leaf_partial;   // [leaf blocks][2^D][2]
-    double *class_partial;  // [validate blocks][2]
-    double *f0;             // [2]: initial score, total event weight
+    double *class_partial;  // [validate blocks][3]: signal, background, sum of |v|
+    uint8_t *vsign;         // [npad] 1 = negative event weight (fits with negative weights)
+    double *f0;             // [2]: initial score, sum of |v| (bounds every histogram sum)
     int *err;               // [1]
     uint8_t *cut_feature;   // [T][2^D - 1]
     uint8_t *cut_bin;       // [T][2^D - 1]
@@ -157,11 +159,17 @@ int histogram_scale(double total_weight_bound);
 // round_up(n, 8) elements, with weight 0 beyond n (those events count
 // nowhere), code rows ldb >= round_up(n, 8) bytes, and node_out room for
 // round_up(n, 8) ids (the padded events are routed too).
+// vsign (routed passes only, else null): [round_up(n, 8)] bytes, 1 where the
+// event's weight is negative; w then holds |w| with the class in the sign
+// bit and the pass adds -|w| for those events (two's complement fixed point).
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
-                            const float *w, const ParentCuts &pc, int layer, bool routed,
-                            int scale, uint64_t *partial, double *small, int *err,
-                            hipStream_t s);
+                            const float *w, const uint8_t *vsign, const ParentCuts &pc,
+                            int layer, bool routed, int scale, uint64_t *partial, double *small,
+                            int *err, hipStream_t s);
+
+// vs[i] = 1 where v[i] < 0 (i < n), else 0, for i < npad.
+hipError_t launch_sign_bytes(const float *v, int64_t n, int64_t npad, uint8_t *vs, hipStream_t s);
 
 // hist[i] = (sum over chunks of partial[chunk][i]) * 2^-scale + small[i].
 hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t count, int scale,

@@ -86,39 +86,46 @@ __global__ __launch_bounds__(256) void validate_kernel(const int8_t *__restrict_
                                                        const float *__restrict__ v, int64_t n,
                                                        double *__restrict__ class_partial,
                                                        int *__restrict__ err) {
-    double s = 0.0, b = 0.0;
+    // per block: signal total, background total, sum of |v|
+    double s = 0.0, b = 0.0, a = 0.0;
     int e = 0;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
         const int yi = y[i];
         const float vi = v ? v[i] : 1.0f;
         if (yi != 1 && yi != -1) e |= kErrLabel;
-        if (!(vi >= 0.0f) || isinf(vi)) e |= kErrWeight;
+        if (!isfinite(vi)) e |= kErrWeight;
+        if (vi < 0.0f) e |= kNegWeights;
         if (yi > 0)
             s += (double)vi;
         else if (yi < 0)
             b += (double)vi;
+        a += fabs((double)vi);
     }
     for (int off = kWave / 2; off > 0; off >>= 1) {
         s += __shfl_down(s, off);
         b += __shfl_down(b, off);
+        a += __shfl_down(a, off);
     }
-    __shared__ double ws[256 / kWave][2];
+    __shared__ double ws[256 / kWave][3];
     const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
     if (lane == 0) {
         ws[wid][0] = s;
         ws[wid][1] = b;
+        ws[wid][2] = a;
     }
     if (e) atomicOr(err, e);
     __syncthreads();
     if (threadIdx.x == 0) {
-        double ts = 0.0, tb = 0.0;
+        double ts = 0.0, tb = 0.0, ta = 0.0;
         for (int k = 0; k < (int)(blockDim.x / kWave); ++k) {
             ts += ws[k][0];
             tb += ws[k][1];
+            ta += ws[k][2];
         }
-        class_partial[2 * blockIdx.x] = ts;
-        class_partial[2 * blockIdx.x + 1] = tb;
+        class_partial[3 * blockIdx.x] = ts;
+        class_partial[3 * blockIdx.x + 1] = tb;
+        class_partial[3 * blockIdx.x + 2] = ta;
     }
 }
 
@@ -126,19 +133,22 @@ __global__ __launch_bounds__(256) void validate_kernel(const int8_t *__restrict_
 __global__ __launch_bounds__(256) void initial_score_kernel(const double *__restrict__ cp,
                                                             int nblocks, double *__restrict__ f0,
                                                             int *__restrict__ err) {
-    __shared__ double sh[256][2];
-    double s = 0.0, b = 0.0;
+    __shared__ double sh[256][3];
+    double s = 0.0, b = 0.0, a = 0.0;
     for (int k = threadIdx.x; k < nblocks; k += blockDim.x) {
-        s += cp[2 * k];
-        b += cp[2 * k + 1];
+        s += cp[3 * k];
+        b += cp[3 * k + 1];
+        a += cp[3 * k + 2];
     }
     sh[threadIdx.x][0] = s;
     sh[threadIdx.x][1] = b;
+    sh[threadIdx.x][2] = a;
     __syncthreads();
     for (int off = blockDim.x / 2; off > 0; off >>= 1) {
         if ((int)threadIdx.x < off) {
             sh[threadIdx.x][0] += sh[threadIdx.x + off][0];
             sh[threadIdx.x][1] += sh[threadIdx.x + off][1];
+            sh[threadIdx.x][2] += sh[threadIdx.x + off][2];
         }
         __syncthreads();
     }
@@ -148,7 +158,7 @@ __global__ __launch_bounds__(256) void initial_score_kernel(const double *__rest
             atomicOr(err, kErrClass);
         else
             f0[0] = 0.5 * log(ts / tb);
-        f0[1] = ts + tb;
+        f0[1] = sh[0][2];   // sum of |v|: bounds every histogram sum
     }
 }
 
@@ -301,7 +311,9 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
             const bool sampled = st.sampled;
             if (w) {
                 const double vi = (double)st.v;
-                const float wi = sampled ? (float)(vi * fabs(yt)) : 0.0f;
+                // |fl32(v |y~|)| with the class in the sign bit (a negative
+                // v's sign travels in the separate sign bytes of the fit)
+                const float wi = sampled ? fabsf((float)(vi * fabs(yt))) : 0.0f;
                 w[i] = yf > 0.0 ? wi : -wi;
             }
             if (yts) yts[i] = sampled ? yt : 0.0;
@@ -487,6 +499,7 @@ template <int NP, int FPG>
 struct HistStep {
     uint32_t w[kHistE];               // weight bits (class in the sign bit)
     uint2 node;                       // parent ids (routed, layer >= 2) or node ids
+    uint2 vs;                         // 1 where the event's weight is negative (signed fits)
     uint2 rows[NP > 0 ? NP : 1];      // codes of the parents' cut features
     uint2 codes[FPG];                 // codes of the group's features
 };
@@ -500,11 +513,12 @@ struct HistArgs {
     const uint8_t *node_in;
     uint8_t *node_out;
     const float *w;
+    const uint8_t *vsign;             // [padded n] 1 = negative event weight (signed fits)
     double *small;
 };
 
 // codes of the parents' cut features (the cut table must be in LDS)
-template <bool ROUTED, int NP, int FPG>
+template <bool ROUTED, int NP, int FPG, bool SIGNED>
 __device__ __forceinline__ void hist_load_rows(HistStep<NP, FPG> &st, const HistArgs &a,
                                                const uint8_t *s_cf, int64_t i0) {
     if (ROUTED && NP > 0 && a.layer >= 1) {
@@ -519,7 +533,7 @@ __device__ __forceinline__ void hist_load_rows(HistStep<NP, FPG> &st, const Hist
 // The per-event arrays (weights, node ids) are padded to a multiple of
 // kHistE with zero weights, and code rows to ldb >= that padding, so every
 // step loads kHistE whole events; padded events weigh 0 and count nowhere.
-template <bool ROUTED, int NP, int FPG>
+template <bool ROUTED, int NP, int FPG, bool SIGNED>
 __device__ __forceinline__ void hist_load(HistStep<NP, FPG> &st, const HistArgs &a,
                                           const uint8_t *s_cf, int64_t i0, bool with_rows) {
     const uint4 x = reinterpret_cast<const uint4 *>(a.w + i0)[0];
@@ -531,10 +545,11 @@ __device__ __forceinline__ void hist_load(HistStep<NP, FPG> &st, const HistArgs 
     for (int ff = 0; ff < FPG; ++ff)
         st.codes[ff] = *reinterpret_cast<const uint2 *>(
             a.xb + (int64_t)min(a.j0 + ff, a.d - 1) * a.ldb + i0);
-    if (with_rows) hist_load_rows<ROUTED, NP, FPG>(st, a, s_cf, i0);
+    if (SIGNED) st.vs = *reinterpret_cast<const uint2 *>(a.vsign + i0);
+    if (with_rows) hist_load_rows<ROUTED, NP, FPG, SIGNED>(st, a, s_cf, i0);
 }
 
-template <bool ROUTED, int NP, int FPG>
+template <bool ROUTED, int NP, int FPG, bool SIGNED>
 __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const HistArgs &a,
                                          uint64_t *lds, bool writer, const uint8_t *s_cf,
                                          const uint8_t *s_cc, const uint32_t (&cut)[4],
@@ -621,7 +636,8 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
         if (mine && (ab - 1u) < a.tau_bits - 1u) below |= 1u << e;   // 0 < w < tau: rare
         if (mine && counted[e] && ab >= a.tau_bits) {
             const int sh = (int)(ab >> 23) - 150 + a.scale;   // >= 0 on the grid
-            const uint64_t fx = (uint64_t)((ab & 0x7fffffu) | 0x800000u) << sh;
+            uint64_t fx = (uint64_t)((ab & 0x7fffffu) | 0x800000u) << sh;
+            if (SIGNED && byte8(st.vs, e)) fx = 0ull - fx;   // two's complement: sums stay exact
             const uint32_t base = slot[e] * (uint32_t)(FPG * kRowBytes) + ((bits >> 28) & 8u);
 #pragma unroll
             for (int ff = 0; ff < FPG; ++ff) {
@@ -636,7 +652,8 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
         for (int e = 0; e < kHistE; ++e) {
             if ((below >> e) & 1u) {
                 const uint32_t bits = st.w[e];
-                const double wa = (double)__uint_as_float(bits & 0x7fffffffu);
+                double wa = (double)__uint_as_float(bits & 0x7fffffffu);
+                if (SIGNED && byte8(st.vs, e)) wa = -wa;
 #pragma unroll
                 for (int ff = 0; ff < FPG; ++ff) {
                     const uint32_t bin = byte8(st.codes[ff], e);
@@ -653,11 +670,12 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
     }
 }
 
-template <bool ROUTED, int NP, int FPG>
+template <bool ROUTED, int NP, int FPG, bool SIGNED>
 __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
-    const float *__restrict__ w, const double *__restrict__ cand_gain,
+    const float *__restrict__ w, const uint8_t *__restrict__ vsign,
+    const double *__restrict__ cand_gain,
     const int *__restrict__ cand_cut, int cslices, uint8_t *__restrict__ rec_f,
     uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, int G, int npg, int NG,
     int chunks, int64_t chunk_events, int64_t xcd_events, int scale, int copies,
@@ -698,6 +716,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     a.node_in = node_in;
     a.node_out = node_out;
     a.w = w;
+    a.vsign = vsign;
     a.small = small;
     const int lds_n = npg * FPG * kRow;   // counters of one copy
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
@@ -730,7 +749,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     if (pwave) cand_load(cs, wave, lane, cr);
     HistStep<NP, FPG> A, B;
     int64_t ia = start + (int64_t)kHistE * threadIdx.x;
-    if (ia < end) hist_load<ROUTED, NP, FPG>(A, a, s_cf, ia, false);
+    if (ia < end) hist_load<ROUTED, NP, FPG, SIGNED>(A, a, s_cf, ia, false);
 
     {
         uint4 *l4 = reinterpret_cast<uint4 *>(lds);
@@ -770,17 +789,17 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     // adds of step s.  They are issued unconditionally (the last step
     // reloads its own events) so that the waits for step s never cover them.
     if (ia < end) {
-        hist_load_rows<ROUTED, NP, FPG>(A, a, s_cf, ia);
+        hist_load_rows<ROUTED, NP, FPG, SIGNED>(A, a, s_cf, ia);
         for (;;) {
             const int64_t ib = ia + stride;
             const bool more_b = ib < end;
-            hist_load<ROUTED, NP, FPG>(B, a, s_cf, more_b ? ib : ia, true);
-            hist_add<ROUTED, NP, FPG>(A, a, lds_lane, writer, s_cf, s_cc, cut, ia, eflag);
+            hist_load<ROUTED, NP, FPG, SIGNED>(B, a, s_cf, more_b ? ib : ia, true);
+            hist_add<ROUTED, NP, FPG, SIGNED>(A, a, lds_lane, writer, s_cf, s_cc, cut, ia, eflag);
             if (!more_b) break;
             ia = ib + stride;
             const bool more_a = ia < end;
-            hist_load<ROUTED, NP, FPG>(A, a, s_cf, more_a ? ia : ib, true);
-            hist_add<ROUTED, NP, FPG>(B, a, lds_lane, writer, s_cf, s_cc, cut, ib, eflag);
+            hist_load<ROUTED, NP, FPG, SIGNED>(A, a, s_cf, more_a ? ia : ib, true);
+            hist_add<ROUTED, NP, FPG, SIGNED>(B, a, lds_lane, writer, s_cf, s_cc, cut, ib, eflag);
             if (!more_a) break;
         }
     }
@@ -841,7 +860,7 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(const uint64_t *__r
          i += (size_t)gridDim.x * blockDim.x) {
         uint64_t s = 0;
         for (int p = 0; p < chunks; ++p) s += partial[(size_t)p * count + i];
-        out[i] = ldexp((double)s, -scale) + small[i];
+        out[i] = ldexp((double)(long long)s, -scale) + small[i];
     }
 }
 
@@ -1158,10 +1177,11 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         } else if (left_empty || right_empty) {
             g = 0.0;
         } else {
-            const double SS = ldexp((double)Ps, -scale) + sPs;
-            const double BB = ldexp((double)Pb, -scale) + sPb;
-            const double ST = ldexp((double)Ts, -scale) + sTs;
-            const double BT = ldexp((double)Tb, -scale) + sTb;
+            // fixed-point sums as signed integers (negative event weights)
+            const double SS = ldexp((double)(long long)Ps, -scale) + sPs;
+            const double BB = ldexp((double)(long long)Pb, -scale) + sPb;
+            const double ST = ldexp((double)(long long)Ts, -scale) + sTs;
+            const double BT = ldexp((double)(long long)Tb, -scale) + sTb;
             g = (gini(ST, BT) - gini(SS, BB)) - gini(ST - SS, BT - BB);
         }
     }
@@ -1864,11 +1884,15 @@ hipError_t allow_lds(K kernel, size_t max_lds) {
 // ===========================================================================
 template <int FPG>
 hipError_t allow_hist_lds(size_t max_lds) {
-    const hipError_t e[] = {allow_lds(hist_kernel<false, 0, FPG>, max_lds),
-                            allow_lds(hist_kernel<true, 0, FPG>, max_lds),
-                            allow_lds(hist_kernel<true, 1, FPG>, max_lds),
-                            allow_lds(hist_kernel<true, 2, FPG>, max_lds),
-                            allow_lds(hist_kernel<true, 4, FPG>, max_lds)};
+    const hipError_t e[] = {allow_lds(hist_kernel<false, 0, FPG, false>, max_lds),
+                            allow_lds(hist_kernel<true, 0, FPG, false>, max_lds),
+                            allow_lds(hist_kernel<true, 1, FPG, false>, max_lds),
+                            allow_lds(hist_kernel<true, 2, FPG, false>, max_lds),
+                            allow_lds(hist_kernel<true, 4, FPG, false>, max_lds),
+                            allow_lds(hist_kernel<true, 0, FPG, true>, max_lds),
+                            allow_lds(hist_kernel<true, 1, FPG, true>, max_lds),
+                            allow_lds(hist_kernel<true, 2, FPG, true>, max_lds),
+                            allow_lds(hist_kernel<true, 4, FPG, true>, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -2047,33 +2071,29 @@ int histogram_scale(double total_weight_bound) {
     return sc;
 }
 
-template <bool ROUTED, int NP, int FPG>
+template <bool ROUTED, int NP, int FPG, bool SIGNED>
 hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
-                          const ParentCuts &pc, int layer, int scale, uint64_t *partial,
-                          double *small, int *err, hipStream_t s) {
-    hist_kernel<ROUTED, NP, FPG><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
-        xb, ldb, n, d, n_bins, node_in, node_out, w, pc.cand_gain, pc.cand_cut, pc.slices,
+                          const uint8_t *vsign, const ParentCuts &pc, int layer, int scale,
+                          uint64_t *partial, double *small, int *err, hipStream_t s) {
+    hist_kernel<ROUTED, NP, FPG, SIGNED><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+        xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices,
         pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
         hs.chunks, hs.chunk_events, hs.xcd_events, scale, hs.copies, hs.copy_stride, partial, small,
         err);
     return hipGetLastError();
 }
 
-template <int FPG>
-hipError_t launch_hist_fpg(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
-                           int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
-                           const float *w, const ParentCuts &pc, int layer, bool routed,
-                           int scale, uint64_t *partial, double *small, int *err,
-                           hipStream_t s) {
-    const ParentCuts none{};
-    if (!routed)
-        return launch_hist_np<false, 0, FPG>(hs, xb, ldb, n, d, n_bins, node_in, nullptr, w, none,
-                                             layer, scale, partial, small, err, s);
+template <int FPG, bool SIGNED>
+hipError_t launch_hist_routed(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
+                              int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
+                              const float *w, const uint8_t *vsign, const ParentCuts &pc,
+                              int layer, int scale, uint64_t *partial, double *small, int *err,
+                              hipStream_t s) {
     const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
 #define FBDT_HIST(NPV)                                                                          \
-    launch_hist_np<true, NPV, FPG>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, pc, layer,   \
-                                   scale, partial, small, err, s)
+    launch_hist_np<true, NPV, FPG, SIGNED>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,     \
+                                           vsign, pc, layer, scale, partial, small, err, s)
     switch (parents) {
     case 0:
     case 1: return FBDT_HIST(1);
@@ -2084,14 +2104,34 @@ hipError_t launch_hist_fpg(const HistShape &hs, const uint8_t *xb, int64_t ldb, 
 #undef FBDT_HIST
 }
 
+template <int FPG>
+hipError_t launch_hist_fpg(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
+                           int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
+                           const float *w, const uint8_t *vsign, const ParentCuts &pc, int layer,
+                           bool routed, int scale, uint64_t *partial, double *small, int *err,
+                           hipStream_t s) {
+    const ParentCuts none{};
+    if (!routed) {
+        if (vsign) return hipErrorInvalidValue;   // signed weights: routed (fit) passes only
+        return launch_hist_np<false, 0, FPG, false>(hs, xb, ldb, n, d, n_bins, node_in, nullptr,
+                                                    w, nullptr, none, layer, scale, partial,
+                                                    small, err, s);
+    }
+    if (vsign)
+        return launch_hist_routed<FPG, true>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,
+                                             vsign, pc, layer, scale, partial, small, err, s);
+    return launch_hist_routed<FPG, false>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,
+                                          nullptr, pc, layer, scale, partial, small, err, s);
+}
+
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
-                            const float *w, const ParentCuts &pc, int layer, bool routed,
-                            int scale, uint64_t *partial, double *small, int *err,
-                            hipStream_t s) {
+                            const float *w, const uint8_t *vsign, const ParentCuts &pc,
+                            int layer, bool routed, int scale, uint64_t *partial, double *small,
+                            int *err, hipStream_t s) {
 #define FBDT_HIST_F(F)                                                                          \
-    launch_hist_fpg<F>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, pc, layer, routed,      \
-                       scale, partial, small, err, s)
+    launch_hist_fpg<F>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc, layer,       \
+                       routed, scale, partial, small, err, s)
     switch (hs.features_per_group) {
     case 1: return FBDT_HIST_F(1);
     case 2: return FBDT_HIST_F(2);
@@ -2101,6 +2141,19 @@ hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb,
     default: return hipErrorInvalidValue;
     }
 #undef FBDT_HIST_F
+}
+
+// vs[i] = 1 where v[i] < 0, 0 elsewhere and for the padding [n, npad)
+__global__ __launch_bounds__(256) void sign_bytes_kernel(const float *__restrict__ v, int64_t n,
+                                                         int64_t npad, uint8_t *__restrict__ vs) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < npad;
+         i += (int64_t)gridDim.x * blockDim.x)
+        vs[i] = (i < n && v[i] < 0.0f) ? 1 : 0;
+}
+
+hipError_t launch_sign_bytes(const float *v, int64_t n, int64_t npad, uint8_t *vs, hipStream_t s) {
+    sign_bytes_kernel<<<grid_for(npad, 256, 2048), 256, 0, s>>>(v, n, npad, vs);
+    return hipGetLastError();
 }
 
 hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t count, int scale,

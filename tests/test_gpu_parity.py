@@ -310,6 +310,9 @@ FIT_CASES = {
     "ragged-depth1-B2": dict(cfg=1, n_events=1237, depth=1, n_bins=2, n_trees=5),
     "depth7-B128": dict(cfg=3, n_events=40_013, depth=7, n_bins=128, n_trees=2, subsample=1.0),
     "weighted-alpha0.8": dict(cfg=2, n_events=30_011, n_trees=8, weights=True, subsample=0.8),
+    # negative event weights (section 4.1): about a fifth of the events
+    "negative-weights": dict(cfg=2, n_events=30_011, n_trees=8, weights="signed"),
+    "negative-weights-depth6": dict(cfg=4, n_events=60_013, depth=6, n_trees=2, weights="signed"),
 }
 
 
@@ -326,7 +329,9 @@ def test_fit_and_apply_match_oracle(case):
     eta = spec.shrinkage
     seed = spec.fit_seed
     v = ds["v"]
-    if c.get("weights"):
+    if c.get("weights") == "signed":
+        v = np.random.default_rng(9).uniform(-0.6, 2.5, n).astype(np.float32)
+    elif c.get("weights"):
         v = np.random.default_rng(9).uniform(0.2, 3.0, n).astype(np.float32)
     say(f"fit parity {case}: n={n} d={ds['x'].shape[0]} B={B} D={D} T={T} alpha={alpha}")
     bounds, codes = fb.bin(dev(ds["x"]), B)
@@ -574,7 +579,13 @@ def test_errors_are_reported():
         fb.fit(codes, dev(np.ones(n, np.int8)), B, 2, 2)
     assert ei.value.status == "FBDT_E_LABEL"
     w = np.ones(n, np.float32)
-    w[3] = -1
+    w[y > 0] = -0.5                                    # signal total negative
+    w[0] = 1.0
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, dev(y), B, 2, 2, w=dev(w))
+    assert ei.value.status == "FBDT_E_LABEL"
+    w = np.ones(n, np.float32)
+    w[3] = np.inf
     with pytest.raises(fb.FbdtError) as ei:
         fb.fit(codes, dev(y), B, 2, 2, w=dev(w))
     assert ei.value.status == "FBDT_E_WEIGHT"

@@ -226,6 +226,28 @@ def test_threshold_apply_equals_binned_apply_on_edge_values():
         assert np.array_equal(Ft, Fb)
 
 
+def test_negative_weights_cancel_a_positive_copy():
+    """Section 4.1: events may carry negative weights.  Appending a copy of
+    the sample with weight +a and another with weight -a (same features and
+    labels) leaves every histogram, gain, boost weight and score unchanged up
+    to float64 rounding, with alpha = 1 (no sampling)."""
+    from synth import make_training_set
+    ds = make_training_set(1, n_events=2000)
+    _, xb = O.bin_features(ds["x"], 16)
+    n = xb.shape[1]
+    rng = np.random.default_rng(2)
+    a = rng.uniform(0.5, 2.0, n).astype(np.float32)
+    xb3 = np.concatenate([xb, xb, xb], axis=1)
+    y3 = np.concatenate([ds["y"]] * 3)
+    v3 = np.concatenate([ds["v"], a, -a]).astype(np.float32)
+    m1, F1 = O.fit(xb, ds["y"], ds["v"], 3, 4, 0.1, 1.0, 0, 16, final_score=True)
+    m3, F3 = O.fit(xb3, y3, v3, 3, 4, 0.1, 1.0, 0, 16, final_score=True)
+    assert np.array_equal(m1.cut_feature, m3.cut_feature)
+    assert np.array_equal(m1.cut_bin, m3.cut_bin)
+    assert np.allclose(m1.leaf, m3.leaf, rtol=1e-9, atol=1e-12)
+    assert np.allclose(F3[:n], F1, rtol=1e-9, atol=1e-12)
+
+
 # ------------------------------------------------------------- histograms
 def _brute_hist(xb, node, w, y, layer, n_bins):
     d, n = xb.shape
