@@ -81,23 +81,46 @@ def subsample_mask(seed: int, tree: int, n_events: int, alpha: float) -> np.ndar
 # or ceil(N/B) events; tied values share a bin; repeated boundaries leave
 # empty bins, which are kept.  Comparisons are float32, as stored.
 # --------------------------------------------------------------------------
+# Missing values (section 4.2).  NaN marks a value that must not inform the
+# fit.  Reading: NaN takes the reserved code 255 (so B <= 255 bins when the
+# data hold NaN); the boundaries are the order statistics of the feature's
+# other values; a NaN never enters the feature's histograms; an event whose
+# value of a node's cut feature is NaN stops at that node, which acts as its
+# terminal node (its boost weight, computed like a leaf's over the sampled
+# events that reached it, is added to F); apply does the same.
+MISSING = 255
+
+
+def missing_allowed(n_bins: int) -> bool:
+    return n_bins <= MISSING
+
+
 def quantile_boundaries(column, n_bins: int) -> np.ndarray:
+    """b_k = the value of rank floor(k m / B) among the m non-NaN values of
+    the feature (k = 1 .. B - 1); +inf when every value is NaN.  NaN is an
+    error unless B <= 255 (section 4.2)."""
     col = np.asarray(column, dtype=np.float32)
-    if np.isnan(col).any():
-        raise ValueError("NaN feature values are not accepted")
-    s = np.sort(col)
-    n = s.shape[0]
+    nan = np.isnan(col)
+    if nan.any() and not missing_allowed(n_bins):
+        raise ValueError("NaN feature values need n_bins <= 255")
+    s = np.sort(col[~nan])
+    m = s.shape[0]
+    if m == 0:
+        return np.full(n_bins - 1, np.inf, np.float32)
     k = np.arange(1, n_bins, dtype=np.int64)
-    return s[(k * n) // n_bins].astype(np.float32)
+    return s[(k * m) // n_bins].astype(np.float32)
 
 
 def encode(column, boundaries) -> np.ndarray:
-    """Bin code of every value: the number of boundaries at or below it."""
+    """Bin code of every value: the number of boundaries at or below it;
+    NaN takes the reserved code 255 (B <= 255, section 4.2)."""
     col = np.asarray(column, dtype=np.float32)
-    if np.isnan(col).any():
-        raise ValueError("NaN feature values are not accepted")
     b = np.asarray(boundaries, dtype=np.float32)
-    return np.searchsorted(b, col, side="right").astype(np.uint8)
+    nan = np.isnan(col)
+    if nan.any() and not missing_allowed(b.shape[0] + 1):
+        raise ValueError("NaN feature values need n_bins <= 255")
+    code = np.searchsorted(b, col, side="right")
+    return np.where(nan, MISSING, code).astype(np.uint8)
 
 
 def bin_features(x, n_bins: int):
@@ -159,9 +182,14 @@ def histogram(xb, node, w, is_signal, layer: int, n_bins: int) -> np.ndarray:
     cls = np.where(is_signal, 0, 1)
     w64 = np.asarray(w, dtype=np.float32).astype(np.float64)
     H = np.zeros((n_nodes, d, n_bins, 2))
+    # events that stopped at an earlier layer (missing values) are not in
+    # the layer; a missing value of feature j is not in feature j's histogram
+    here = local >= 0
     for j in range(d):
-        idx = (local * n_bins + xb[j].astype(np.int64)) * 2 + cls
-        H[:, j] = np.bincount(idx, weights=w64, minlength=n_nodes * n_bins * 2).reshape(
+        code = xb[j].astype(np.int64)
+        keep = here & (code < n_bins) if missing_allowed(n_bins) else here
+        idx = ((local * n_bins + code) * 2 + cls)[keep]
+        H[:, j] = np.bincount(idx, weights=w64[keep], minlength=n_nodes * n_bins * 2).reshape(
             n_nodes, n_bins, 2)
     return H
 
@@ -222,14 +250,22 @@ def best_cuts(gains):
     return feat, cut, flat[np.arange(n_nodes), arg]
 
 
-def route(node, xb, feat_of_node, cut_of_node, layer: int) -> np.ndarray:
-    """Send every event to a child: node <- 2 node + [bin(f*) >= c*] (section 1.1)."""
+def route(node, xb, feat_of_node, cut_of_node, layer: int, missing: bool = False) -> np.ndarray:
+    """Send every event to a child: node <- 2 node + [bin(f*) >= c*] (section 1.1).
+    With ``missing`` (section 4.2) an event whose code of the cut feature is
+    the missing code stays at its node, and an event that stopped at an
+    earlier layer stays where it is."""
     node = np.asarray(node, dtype=np.int64)
     local = node - (1 << layer)
-    f = np.asarray(feat_of_node, dtype=np.int64)[local]
-    c = np.asarray(cut_of_node, dtype=np.int64)[local]
+    here = local >= 0
+    lc = np.where(here, local, 0)
+    f = np.asarray(feat_of_node, dtype=np.int64)[lc]
+    c = np.asarray(cut_of_node, dtype=np.int64)[lc]
     code = np.asarray(xb)[f, np.arange(node.shape[0])].astype(np.int64)
-    return 2 * node + (code >= c).astype(np.int64)
+    child = 2 * node + (code >= c).astype(np.int64)
+    if not missing:
+        return child
+    return np.where(here & (code != MISSING), child, node)
 
 
 def leaf_values(leaf_local, ytilde, v, mask, n_leaves: int) -> np.ndarray:
@@ -247,6 +283,28 @@ def leaf_values(leaf_local, ytilde, v, mask, n_leaves: int) -> np.ndarray:
     return np.where(den == 0.0, 0.0, g)
 
 
+def node_values(terminal, ytilde, v, mask, depth: int) -> np.ndarray:
+    """Boost weights of every node (section 4.2 reading): for node k the
+    Newton step sum(v y~) / sum(v |y~| (2 - |y~|)) over the sampled events
+    that reached k (those whose terminal node is k or below it), 0 where the
+    denominator is 0.  terminal: heap id of each event's terminal node.
+    Returns float64 [2^(D+1) - 1], node k at index k - 1."""
+    n_nodes = (2 << depth) - 1
+    yt = np.asarray(ytilde, dtype=np.float64)
+    v64 = np.asarray(v, dtype=np.float64)
+    m = np.asarray(mask, dtype=bool)
+    idx = np.asarray(terminal, dtype=np.int64)[m] - 1
+    num = np.bincount(idx, weights=(v64 * yt)[m], minlength=n_nodes)
+    a = np.abs(yt)
+    den = np.bincount(idx, weights=(v64 * a * (2.0 - a))[m], minlength=n_nodes)
+    for k in range((1 << depth) - 1, 0, -1):   # inner nodes, bottom up
+        num[k - 1] += num[2 * k - 1] + num[2 * k]
+        den[k - 1] += den[2 * k - 1] + den[2 * k]
+    with np.errstate(invalid="ignore", divide="ignore"):
+        g = num / den
+    return np.where(den == 0.0, 0.0, g)
+
+
 @dataclasses.dataclass
 class Model:
     """A fitted forest in heap order: node k of tree t at index [t, k - 1]."""
@@ -259,6 +317,8 @@ class Model:
     cut_bin: np.ndarray         # uint8 [T][2^D - 1]
     gain: np.ndarray            # float64 [T][2^D - 1]
     leaf: np.ndarray            # float64 [T][2^D], already multiplied by eta
+    inner: np.ndarray | None = None   # float64 [T][2^D - 1] times eta: the boost
+                                      # weights of inner nodes, for missing values
 
     @property
     def n_trees(self) -> int:
@@ -310,6 +370,9 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
     cut_bin = np.zeros((n_trees, n_inner), np.uint8)
     gain_out = np.zeros((n_trees, n_inner))
     leaf_out = np.zeros((n_trees, 1 << depth))
+    # missing values (section 4.2): NaN codes in data binned with B <= 255
+    missing = missing_allowed(n_bins) and bool((xb == MISSING).any())
+    inner_out = np.zeros((n_trees, (1 << depth) - 1)) if missing else None
     for t in range(n_trees):
         mask = subsample_mask(seed, t, n, subsample)
         yt = pseudo_response(y, F)
@@ -344,12 +407,18 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
             if trace is not None:
                 trace.append({"tree": t, "layer": layer, "H": H, "node": node.copy(),
                               "w": w, "feat": feat.copy(), "cut": cut.copy()})
-            node = route(node, xb, feat, cut, layer)
+            node = route(node, xb, feat, cut, layer, missing)
         leaf_local = node - (1 << depth)
-        gamma = leaf_values(leaf_local, yt, v, mask, 1 << depth)
-        leaf_out[t] = shrinkage * gamma
-        F = F + leaf_out[t][leaf_local]
-    model = Model(depth, n_bins, d, f0, cut_feature, cut_bin, gain_out, leaf_out)
+        if missing:
+            values = shrinkage * node_values(node, yt, v, mask, depth)
+            inner_out[t] = values[:(1 << depth) - 1]
+            leaf_out[t] = values[(1 << depth) - 1:]
+            F = F + values[node - 1]
+        else:
+            gamma = leaf_values(leaf_local, yt, v, mask, 1 << depth)
+            leaf_out[t] = shrinkage * gamma
+            F = F + leaf_out[t][leaf_local]
+    model = Model(depth, n_bins, d, f0, cut_feature, cut_bin, gain_out, leaf_out, inner_out)
     return (model, F) if final_score else model
 
 
@@ -364,13 +433,27 @@ def apply(model: Model, xb, n_trees: int | None = None):
     rows = np.arange(n)
     for t in range(T):
         node = np.ones(n, dtype=np.int64)
+        done = np.zeros(n, dtype=bool)   # stopped at an inner node (missing value)
         for _ in range(model.depth):
             f = model.cut_feature[t][node - 1].astype(np.int64)
             c = model.cut_bin[t][node - 1].astype(np.int64)
-            node = 2 * node + (xb[f, rows].astype(np.int64) >= c)
-        F = F + model.leaf[t][node - (1 << model.depth)]
+            code = xb[f, rows].astype(np.int64)
+            if model.inner is not None:
+                done |= code == MISSING
+            node = np.where(done, node, 2 * node + (code >= c))
+        F = F + _node_value(model, t, node)
     p = (1.0 / (1.0 + np.exp(-2.0 * F))).astype(np.float32)
     return p, F
+
+
+def _node_value(model: Model, t: int, node):
+    """Boost weight (times eta) of heap node ``node`` of tree t: a leaf's, or
+    with missing values an inner node's."""
+    nleaf = 1 << model.depth
+    if model.inner is None:
+        return model.leaf[t][node - nleaf]
+    allv = np.concatenate([model.inner[t], model.leaf[t]])
+    return allv[node - 1]
 
 
 def apply_thresholds(model: Model, x, boundaries, n_trees: int | None = None):
@@ -388,11 +471,15 @@ def apply_thresholds(model: Model, x, boundaries, n_trees: int | None = None):
     rows = np.arange(n)
     for t in range(T):
         node = np.ones(n, dtype=np.int64)
+        done = np.zeros(n, dtype=bool)   # stopped at an inner node (NaN value)
         for _ in range(model.depth):
             f = model.cut_feature[t][node - 1].astype(np.int64)
             c = model.cut_bin[t][node - 1].astype(np.int64)
-            node = 2 * node + (x[f, rows] >= b[f, c - 1])
-        F = F + model.leaf[t][node - (1 << model.depth)]
+            xv = x[f, rows]
+            if model.inner is not None:
+                done |= np.isnan(xv)
+            node = np.where(done, node, 2 * node + (xv >= b[f, c - 1]))
+        F = F + _node_value(model, t, node)
     p = (1.0 / (1.0 + np.exp(-2.0 * F))).astype(np.float32)
     return p, F
 
@@ -416,9 +503,14 @@ def event_importance(model: Model, xb, n_trees: int | None = None) -> np.ndarray
     rows = np.arange(n)
     for t in range(T):
         node = np.ones(n, dtype=np.int64)
+        done = np.zeros(n, dtype=bool)   # stopped at an inner node (missing value)
         for _ in range(model.depth):
             f = model.cut_feature[t][node - 1].astype(np.int64)
             c = model.cut_bin[t][node - 1].astype(np.int64)
-            imp[f, rows] += model.gain[t][node - 1]
-            node = 2 * node + (xb[f, rows].astype(np.int64) >= c)
+            code = xb[f, rows].astype(np.int64)
+            if model.inner is not None:
+                done |= code == MISSING
+            # a node adds its gain to the events its cut applies to
+            imp[f, rows] += np.where(done, 0.0, model.gain[t][node - 1])
+            node = np.where(done, node, 2 * node + (code >= c))
     return imp

@@ -76,8 +76,11 @@ def test_binning_ties_share_a_bin_and_empty_bins_are_kept():
     assert len(set(codes[0].tolist())) == 3
     # values below every boundary go to bin 0, +-inf to the ends
     assert O.encode(np.array([-np.inf, np.inf], np.float32), b[0]).tolist() == [0, 15]
+    # NaN (section 4.2) takes the reserved code 255, which needs B <= 255
+    assert O.encode(np.array([np.nan], np.float32), b[0]).tolist() == [255]
+    b256 = O.quantile_boundaries(np.arange(1000, dtype=np.float32), 256)
     with pytest.raises(ValueError):
-        O.encode(np.array([np.nan], np.float32), b[0])
+        O.encode(np.array([np.nan], np.float32), b256)
 
 
 def test_binning_monotone_transform_invariance():
@@ -166,6 +169,64 @@ def test_hand_example_two_trees(eta):
         assert np.allclose(p1[[0, 7]], ex["tree1_p_eta01"], atol=1e-6)
         assert np.allclose(g2, ex["tree2_gains_eta01"], atol=1e-6)
         assert int(m.cut_bin[1, 0]) == int(ex["tree2_cut_eta01"][0])
+
+
+def test_hand_missing_value_example():
+    """Section 4.2: the hand-worked depth-1 example with one value missing
+    (tests/golden/hand_missing.txt): boundaries over the other values, NaN
+    code 255 out of the histograms, the same gains, the NaN event stopping at
+    the root with the root's boost weight."""
+    _, ex = read_fixture("hand_missing.txt")
+    x = np.array(ex["x"], np.float32)[None, :]
+    y = np.array(ex["y"], np.int8)
+    b, xb = O.bin_features(x, 4)
+    assert b[0].tolist() == ex["boundaries"]
+    assert xb[0].tolist() == [int(v) for v in ex["bins"]]
+    H = O.histogram(xb, np.ones(8, np.int64), np.ones(8, np.float32), y > 0, 0, 4)
+    assert H[0, 0, :, 0].tolist() == ex["hist_signal"]
+    assert H[0, 0, :, 1].tolist() == ex["hist_background"]
+    g = O.split_gains(*O.cumulative(H))[0, 0]
+    assert np.allclose(g, ex["gains"], rtol=0, atol=1e-15)
+    m = O.fit(xb, y, np.ones(8, np.float32), depth=1, n_trees=1, shrinkage=1.0,
+              subsample=1.0, seed=0, n_bins=4)
+    assert int(m.cut_bin[0, 0]) == int(ex["cut"][0])
+    assert np.allclose(m.leaf[0], ex["leaves"], rtol=1e-15)
+    assert m.inner is not None and np.allclose(m.inner[0], ex["root_value"], atol=1e-15)
+    p, _ = O.apply(m, xb)
+    assert np.allclose(p, ex["p"], atol=1e-7)
+    pt, _ = O.apply_thresholds(m, x, b)
+    assert np.array_equal(pt, p)
+    # the missing event's path has no applied cut: no importance
+    assert O.event_importance(m, xb)[0].tolist() == [g[1]] * 3 + [0.0] + [g[1]] * 4
+
+
+def test_missing_values_leave_other_features_and_events_unchanged():
+    """Section 4.2: NaN values are ignored.  A feature that is NaN for every
+    event never moves an event (all stop at the root when it is cut on), so
+    a sample with one extra all-NaN feature placed last, on which the best
+    cut never falls when the other features separate, fits the same trees
+    as without it; and blanking one value leaves the other features'
+    histograms of the root untouched."""
+    from synth import make_training_set
+    ds = make_training_set(1, n_events=3000)
+    _, xb = O.bin_features(ds["x"], 16)
+    x2 = np.concatenate([ds["x"], np.full((1, 3000), np.nan, np.float32)])
+    _, xb2 = O.bin_features(x2, 16)
+    assert (xb2[-1] == 255).all() and np.array_equal(xb2[:-1], xb)
+    m1 = O.fit(xb, ds["y"], ds["v"], 3, 3, 0.1, 1.0, 0, 16)
+    m2 = O.fit(xb2, ds["y"], ds["v"], 3, 3, 0.1, 1.0, 0, 16)
+    assert np.array_equal(m1.cut_feature, m2.cut_feature)
+    assert np.array_equal(m1.cut_bin, m2.cut_bin)
+    assert np.allclose(m1.leaf, m2.leaf, rtol=1e-12)
+    x3 = ds["x"].copy()
+    x3[2, 17] = np.nan
+    _, xb3 = O.bin_features(x3, 16)
+    w = np.ones(3000, np.float32)
+    H1 = O.histogram(xb, np.ones(3000, np.int64), w, ds["y"] > 0, 0, 16)
+    H3 = O.histogram(xb3, np.ones(3000, np.int64), w, ds["y"] > 0, 0, 16)
+    others = [j for j in range(xb.shape[0]) if j != 2]
+    assert np.array_equal(H1[:, others], H3[:, others])
+    assert H3[0, 2].sum() == H1[0, 2].sum() - 1.0
 
 
 def test_hand_example_event_importance():
