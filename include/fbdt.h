@@ -46,7 +46,7 @@ enum fbdt_status {
     FBDT_OK = 0,
     FBDT_E_INVAL = -1,  /* null pointer, size or parameter out of range      */
     FBDT_E_LABEL = -2,  /* a label not in {+1, -1}, or a class with no weight */
-    FBDT_E_NAN = -3,    /* NaN among the float features                       */
+    FBDT_E_NAN = -3,    /* NaN among the float features with 256 bins         */
     FBDT_E_WEIGHT = -4, /* a weight not finite                                */
     FBDT_E_SHAPE = -5,  /* too few features for the model                     */
     FBDT_E_DEVICE = -6  /* HIP runtime error or out of device memory          */
@@ -72,25 +72,36 @@ typedef struct {
     const double *gain;         /* host [T][2^D - 1] separation gain, or NULL */
     const double *leaf;         /* host [T][2^D], boost weight times eta      */
     const float *boundaries;    /* host [d][B - 1] bin boundaries, or NULL    */
+    /* host [T][2^D - 1] boost weight times eta of every inner node, or NULL.
+     * Present when the model handles missing values (section 4.2): with at
+     * most 255 bins, bin code 255 marks a missing value, and an event whose
+     * code (apply) or value (apply_float: NaN) of a node's cut feature is
+     * missing stops at that node and takes its weight. */
+    const double *inner;
 } fbdt_model_view;
 
 /*
  * Equal-frequency binning of a training sample (section 2.2, Fig. 3).
- * For each feature j, with s the ascending sort of x[j][0..n), boundary k
- * (k = 1..B-1) is s[floor(k n / B)] and a value goes to bin
- * #{k : boundary_k <= value}.  Tied values share a bin; repeated boundaries
- * leave empty bins.  x: device float32 [d][ldx]; boundaries: host float32
- * [d][B-1] (output); xb: device uint8 [d][ldb] (output).  1 <= d <= 255,
- * 2 <= n_bins <= 256, n >= 1.  The sort runs on the host; the call
- * synchronises the stream.  Returns FBDT_E_NAN if any value is NaN.
+ * For each feature j, with s the ascending sort of the m non-NaN values of
+ * x[j][0..n), boundary k (k = 1..B-1) is s[floor(k m / B)] (+inf when m = 0)
+ * and a value goes to bin #{k : boundary_k <= value}.  Tied values share a
+ * bin; repeated boundaries leave empty bins.  NaN values are missing
+ * (section 4.2): with n_bins <= 255 they take the reserved code 255, with
+ * 256 bins they are an error (FBDT_E_NAN).  x: device float32 [d][ldx];
+ * boundaries: host float32 [d][B-1] (output); xb: device uint8 [d][ldb]
+ * (output; only the first n bytes of each row are written).  1 <= d <= 255,
+ * 2 <= n_bins <= 256, n >= 1.  The sort runs on the device (one radix sort
+ * per batch of features, scratch held by the library); the call
+ * synchronises the stream.
  */
 int fbdt_bin(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
              float *boundaries, uint8_t *xb, int64_t ldb, void *stream);
 
 /*
  * Bin fresh events with the boundaries of a training sample (section 2.2).
- * Same layouts as fbdt_bin; boundaries is host input.  Synchronises the
- * stream to report NaN inputs (FBDT_E_NAN).
+ * Same layouts as fbdt_bin; boundaries is host input.  A NaN value takes
+ * code 255 with n_bins <= 255 and is an error (FBDT_E_NAN) with 256 bins;
+ * the stream is synchronised to report it.
  */
 int fbdt_bin_transform(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
                        const float *boundaries, uint8_t *xb, int64_t ldb, void *stream);
@@ -104,8 +115,14 @@ int fbdt_bin_transform(const float *x, int64_t n, int32_t d, int64_t ldx, int32_
  * weights.  xb: device uint8 [d][ldb]; y: device int8 [n]; w: device
  * float32 [n] or NULL (event weights, any sign; each class's total must be
  * positive, else FBDT_E_LABEL); score_out: optional device float64 [n] that receives
- * the final score F of every event.  *out receives a new model (free with
- * fbdt_model_free).  Synchronises the stream before returning.
+ * the final score F of every event.  Codes must be < n_bins, except that
+ * with n_bins <= 255 code 255 marks a missing value (section 4.2): it stays
+ * out of its feature's histograms, an event stops at the node that cuts on
+ * a feature it misses, and every node, inner or leaf, gets a boost weight
+ * over the sampled events that reached it (the model's inner weights;
+ * depth <= 6, else FBDT_E_INVAL).  Other codes >= n_bins give FBDT_E_INVAL.
+ * *out receives a new model (free with fbdt_model_free).  Synchronises the
+ * stream before returning.
  */
 int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bins,
              const int8_t *y, const float *w, const fbdt_fit_params *params,
@@ -114,9 +131,11 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
 /*
  * Score events (Fig. 1, section 1.3): F = f0 + sum over trees of the leaf
  * reached, accumulated in float64 in tree order; prob = 1 / (1 + exp(-2F))
- * rounded to float32.  xb: device uint8 [d][ldb] with d >= the model's
- * feature count (else FBDT_E_SHAPE); prob: device float32 [n] (output);
- * score: optional device float64 [n] (output).  Stream-ordered.
+ * rounded to float32.  A model with inner weights (missing values) stops an
+ * event at the node whose cut feature has code 255 and adds that node's
+ * weight.  xb: device uint8 [d][ldb] with d >= the model's feature count
+ * (else FBDT_E_SHAPE); prob: device float32 [n] (output); score: optional
+ * device float64 [n] (output).  Stream-ordered.
  */
 int fbdt_apply(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
                float *prob, double *score, void *stream);
@@ -129,9 +148,10 @@ int fbdt_apply(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d, int
  * fbdt_apply on fbdt_bin_transform's codes bit for bit.  The model needs its
  * boundaries (fbdt_model_set_boundaries or fbdt_model_import), else
  * FBDT_E_INVAL.  x: device float32 [d][ldx], ldx >= n, d >= the model's
- * feature count (else FBDT_E_SHAPE); NaN values are not supported (a NaN
- * fails every test and takes the left branch).  prob, score as for
- * fbdt_apply.  Stream-ordered.
+ * feature count (else FBDT_E_SHAPE).  A NaN value stops the event at the
+ * node that cuts on it when the model has inner weights (as code 255 does
+ * in fbdt_apply); in other models it fails every test and takes the left
+ * branch.  prob, score as for fbdt_apply.  Stream-ordered.
  */
 int fbdt_apply_float(const fbdt_model *m, const float *x, int64_t n, int32_t d, int64_t ldx,
                      float *prob, double *score, void *stream);
@@ -146,7 +166,9 @@ int fbdt_feature_importance(const fbdt_model *m, double *importance);
 /*
  * Importance of every feature for every event (section 4.3): the gains of
  * the nodes on the event's path through the trees summed per cut feature,
- * tree by tree in float64.  xb: device uint8 [d][ldb] (as fbdt_apply);
+ * tree by tree in float64; with missing values a path ends at the node
+ * whose cut feature the event misses, without that node's gain.  xb: device
+ * uint8 [d][ldb] (as fbdt_apply);
  * importance: device float64 [d][ldi] (output, ldi >= n; rows of features
  * beyond the model's are zero).  Stream-ordered.
  */
@@ -175,6 +197,9 @@ void fbdt_model_free(fbdt_model *m);
 const char *fbdt_last_error(void);
 
 /* ---- The steps of one boosting iteration, callable one at a time ------- */
+/* With n_bins <= 255, fbdt_histogram leaves code 255 (a missing value) out
+ * of its sums; fbdt_route and fbdt_leaf_values know no stops at missing
+ * values, which fbdt_fit handles itself. */
 
 /*
  * Re-weighting of one tree (sections 1.3, 1.4): for every event,

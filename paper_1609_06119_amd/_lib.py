@@ -41,7 +41,7 @@ class ModelView(C.Structure):
                 ("n_bins", C.c_int32), ("f0", C.c_double),
                 ("cut_feature", C.POINTER(C.c_uint8)), ("cut_bin", C.POINTER(C.c_uint8)),
                 ("gain", C.POINTER(C.c_double)), ("leaf", C.POINTER(C.c_double)),
-                ("boundaries", C.POINTER(C.c_float))]
+                ("boundaries", C.POINTER(C.c_float)), ("inner", C.POINTER(C.c_double))]
 
 
 class FbdtError(RuntimeError):

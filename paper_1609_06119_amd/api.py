@@ -114,6 +114,8 @@ class Model:
         if v.boundaries:
             out["boundaries"] = arr(v.boundaries, v.n_features * (v.n_bins - 1),
                                     np.float32).reshape(v.n_features, v.n_bins - 1)
+        if v.inner:   # missing values: boost weights of the inner nodes
+            out["inner"] = arr(v.inner, T * nin, np.float64).reshape(T, nin)
         return out
 
     def set_boundaries(self, boundaries) -> "Model":
@@ -125,7 +127,7 @@ class Model:
 
     @staticmethod
     def from_arrays(cut_feature, cut_bin, leaf, f0: float, n_features: int, n_bins: int,
-                    gain=None, boundaries=None) -> "Model":
+                    gain=None, boundaries=None, inner=None) -> "Model":
         cf = np.ascontiguousarray(cut_feature, np.uint8)
         cb = np.ascontiguousarray(cut_bin, np.uint8)
         lf = np.ascontiguousarray(leaf, np.float64)
@@ -147,6 +149,12 @@ class Model:
             b = np.ascontiguousarray(boundaries, np.float32)
             keep.append(b)
             v.boundaries = b.ctypes.data_as(C.POINTER(C.c_float))
+        if inner is not None:
+            iv = np.ascontiguousarray(inner, np.float64)
+            if iv.shape != cf.shape:
+                raise ValueError("inner must have the shape of cut_feature")
+            keep.append(iv)
+            v.inner = iv.ctypes.data_as(C.POINTER(C.c_double))
         h = C.c_void_p()
         check("fbdt_model_import", lib().fbdt_model_import(C.byref(v), C.byref(h)))
         del keep

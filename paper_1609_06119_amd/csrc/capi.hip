@@ -23,6 +23,10 @@ struct fbdt_model {
     double f0 = 0.0;
     std::vector<uint8_t> cut_feature, cut_bin;
     std::vector<double> gain, leaf;
+    // missing values (section 4.2): boost weights of the inner nodes [T][2^D - 1];
+    // an event whose code of a node's cut feature is the missing code stops there
+    bool missing = false;
+    std::vector<double> inner;
     std::vector<float> boundaries;
     // device copies of the forest for apply, one per device used
     struct DeviceCopy {
@@ -156,13 +160,13 @@ struct GraphKey {
     double eta, alpha;
     uint64_t seed;
     int64_t fpg, chunks, threads, copies;
-    bool signed_w;
+    bool signed_w, missing;
     bool operator==(const GraphKey &o) const {
         return xb == o.xb && y == o.y && w == o.w && n == o.n && ldb == o.ldb && d == o.d &&
                n_bins == o.n_bins && depth == o.depth && n_trees == o.n_trees &&
                scale == o.scale && lblocks == o.lblocks && eta == o.eta && alpha == o.alpha &&
                seed == o.seed && fpg == o.fpg && chunks == o.chunks && threads == o.threads &&
-               copies == o.copies && signed_w == o.signed_w;
+               copies == o.copies && signed_w == o.signed_w && missing == o.missing;
     }
 };
 
@@ -245,7 +249,8 @@ int read_err(int *err_dev, hipStream_t s, int *out) {
     return FBDT_OK;
 }
 
-double hist_algorithmic_bytes(int64_t n, int d, int n_bins, int layer, bool routed) {
+double hist_algorithmic_bytes(int64_t n, int d, int n_bins, int layer, bool routed,
+                              bool sibling) {
     double b = (double)n * d + 4.0 * n;                 // bin codes + weights
     if (routed) {
         if (layer >= 2) b += (double)n;                 // parent ids
@@ -253,9 +258,9 @@ double hist_algorithmic_bytes(int64_t n, int d, int n_bins, int layer, bool rout
     } else {
         b += (double)n;                                 // node ids
     }
-    // the histograms written: below the root a routed pass writes one child
+    // the histograms written: below the root a sibling pass writes one child
     // per parent (the other is parent - child)
-    const int hnodes = routed && layer >= 1 ? 1 << (layer - 1) : 1 << layer;
+    const int hnodes = sibling && layer >= 1 ? 1 << (layer - 1) : 1 << layer;
     b += (double)hnodes * d * n_bins * 2 * 8;
     return b;
 }
@@ -359,7 +364,7 @@ static int encode_with(const float *x, int64_t n, int32_t d, int64_t ldx, int32_
     }
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;
-    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values");
+    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values needs n_bins <= 255");
     return FBDT_OK;
 }
 
@@ -405,21 +410,24 @@ int fbdt_bin(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
     Carver cv;
     uint64_t *keys_a, *keys_b;
     char *temp;
+    unsigned long long *nan_count;
     float *bounds;
     int *err;
     cv.add(&keys_a, qs.key_elems);
     cv.add(&keys_b, qs.key_elems);
     cv.add(&temp, std::max<size_t>(qs.temp_bytes, 1));
+    cv.add(&nan_count, (size_t)d);
     cv.add(&bounds, nb);
     cv.add(&err, 1);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     HIP_TRY(launch_fill_u32(err, 0u, 1, s));
-    HIP_TRY(launch_quantile_boundaries(x, ldx, n, d, n_bins, qs, keys_a, keys_b, temp, bounds, err,
-                                       s));
+    HIP_TRY(launch_quantile_boundaries(x, ldx, n, d, n_bins, qs, keys_a, keys_b, temp, nan_count,
+                                       bounds, err, s));
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;
-    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values");
+    if (h_err & kErrNan)
+        return fail(FBDT_E_NAN, "NaN among the feature values needs n_bins <= 255");
     {
         Timed t(FBDT_K_ENCODE, s, (double)n * d * 5.0);
         HIP_TRY(launch_encode(x, ldx, n, d, bounds, n_bins, xb, ldb, err, s));
@@ -428,7 +436,7 @@ int fbdt_bin(const float *x, int64_t n, int32_t d, int64_t ldx, int32_t n_bins,
     std::vector<float> host(nb);
     HIP_TRY(hipMemcpyAsync(host.data(), bounds, nb * sizeof(float), hipMemcpyDeviceToHost, s));
     if ((rc = read_err(err, s, &h_err))) return rc;
-    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values");
+    if (h_err & kErrNan) return fail(FBDT_E_NAN, "NaN among the feature values needs n_bins <= 255");
     std::memcpy(boundaries, host.data(), nb * sizeof(float));
     return FBDT_OK;
 }
@@ -472,19 +480,33 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     const int nin = (1 << D) - 1, nleaf = 1 << D;
     const int64_t npad = (n + 15) & ~(int64_t)15;
 
-    std::vector<HistShape> plans(D);
+    // missing values (section 4.2) are possible with at most 255 bins; the
+    // scan of the codes decides, so the plans and buffers below fit either mode
+    const bool may_miss = n_bins <= kMissingCode;
+    // below the root the routed pass histograms one child per parent (the
+    // other is parent - child), except with missing values: an event that
+    // stops at a parent is in the parent's histograms but in neither child's,
+    // so both children are histogrammed
+    std::vector<HistShape> plans_sib(D), plans_both(may_miss ? D : 0);
     size_t partial_elems = 0;
-    for (int l = 0; l < D; ++l) {
-        // below the root the routed pass histograms one child per parent
-        plans[l] = plan_histogram(n, d, n_bins, l, true, di.cu_count, di.max_lds, hist_overrides());
-        const size_t hnodes = l >= 1 ? (size_t)1 << (l - 1) : 1;
-        partial_elems = std::max(partial_elems,
-                                 (size_t)plans[l].chunks * hnodes * d * n_bins * 2);
-        if (plans[l].lds_bytes + kHistStaticLdsReserve > di.max_lds)
-            return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", l,
-                        plans[l].lds_bytes, di.max_lds);
+    for (int mode = 0; mode < (may_miss ? 2 : 1); ++mode) {
+        std::vector<HistShape> &pl = mode == 0 ? plans_sib : plans_both;
+        for (int l = 0; l < D; ++l) {
+            pl[l] = plan_histogram(n, d, n_bins, l, mode == 0, di.cu_count, di.max_lds,
+                                   hist_overrides());
+            const size_t hnodes = pl[l].sibling ? (size_t)1 << (l - 1) : (size_t)1 << l;
+            partial_elems =
+                std::max(partial_elems, (size_t)pl[l].chunks * hnodes * d * n_bins * 2);
+            if (pl[l].lds_bytes + kHistStaticLdsReserve > di.max_lds)
+                return fail(FBDT_E_INVAL, "layer %d needs %zu bytes of LDS, the device has %zu", l,
+                            pl[l].lds_bytes, di.max_lds);
+        }
     }
-    const int lblocks = leaf_blocks(n, D, di.cu_count);
+    const int lblocks_plain = leaf_blocks(n, D, false, di.cu_count);
+    const int lblocks_miss = may_miss ? leaf_blocks(n, D, true, di.cu_count) : 0;
+    const size_t slots_max = may_miss ? (size_t)2 * nleaf - 1 : (size_t)nleaf;
+    const size_t leaf_partial_elems =
+        std::max((size_t)lblocks_plain * 2 * nleaf, (size_t)lblocks_miss * 2 * slots_max);
     const bool fused = D <= kFusedLeafDepth;
     const int max_nodes = 1 << (D - 1);
 
@@ -512,14 +534,14 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     const int S = cut_slices(n_bins);
     cv.add(&fb.cand_gain, (size_t)max_nodes * d * S);
     cv.add(&fb.cand_cut, (size_t)max_nodes * d * S);
-    cv.add(&fb.leaf_partial, (size_t)lblocks * 2 * nleaf);
+    cv.add(&fb.leaf_partial, leaf_partial_elems);
     cv.add(&fb.class_partial, 3 * kValidateBlocks);
     cv.add(&fb.f0, 2);
     cv.add(&fb.err, 1);
     cv.add(&fb.cut_feature, (size_t)T * nin);
     cv.add(&fb.cut_bin, (size_t)T * nin);
     cv.add(&fb.gain, (size_t)T * nin);
-    cv.add(&fb.leaf, (size_t)T * nleaf);
+    cv.add(&fb.leaf, (size_t)T * slots_max);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
 
@@ -535,6 +557,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
         HIP_TRY(hipMemcpyAsync(fb.v, w, (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, s));
     }
     HIP_TRY(launch_validate(y, w, n, fb.class_partial, fb.err, s));
+    if (may_miss) HIP_TRY(launch_find_code(xb, ldb, n, d, (uint8_t)kMissingCode, kHasMissing, fb.err, s));
     HIP_TRY(launch_initial_score(fb.class_partial, fb.f0, fb.err, s));
     int h_err = 0;
     double h_f0[2] = {0.0, 0.0};
@@ -550,8 +573,15 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     // negative event weights (section 4.1): their signs travel in bytes
     // beside the weights, and the histogram passes subtract those events
     const bool signed_w = (h_err & kNegWeights) != 0;
+    const bool missing = may_miss && (h_err & kHasMissing) != 0;
+    if (missing && leaf_lds_bytes(D, true) > kLeafMaxLds)
+        return fail(FBDT_E_INVAL, "missing values (code %d) are supported up to depth 6",
+                    kMissingCode);
+    const int nslots = missing ? 2 * nleaf - 1 : nleaf;   // boost weights per tree
+    const int lblocks = missing ? lblocks_miss : lblocks_plain;
     if (signed_w) HIP_TRY(launch_sign_bytes(w, n, npad, fb.vsign, s));
     const uint8_t *vsign = signed_w ? fb.vsign : nullptr;
+    const std::vector<HistShape> &plans = missing ? plans_both : plans_sib;
 
     const uint64_t seed = p->seed;
     const double alpha = p->subsample, eta = p->shrinkage;
@@ -563,12 +593,12 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 // the previous tree's boost weights: summed here from the leaf
                 // pass partials (shallow trees; workgroup 0 records them), or
                 // from the model after leaf_finalize
-                double *prev = t == 0 ? nullptr : fb.leaf + (size_t)(t - 1) * nleaf;
+                double *prev = t == 0 ? nullptr : fb.leaf + (size_t)(t - 1) * nslots;
                 HIP_TRY(launch_tree_prep(y, w, fb.F, t == 0 ? fb.f0 : nullptr,
                                          t == 0 ? nullptr : fb.node[D & 1], fused ? nullptr : prev,
                                          t > 0 && fused ? fb.leaf_partial : nullptr, lblocks, eta,
-                                         fused ? prev : nullptr, D, n, seed, t, alpha, fb.w,
-                                         fb.yts, nullptr, di.cu_count, st));
+                                         fused ? prev : nullptr, D, missing, n, seed, t, alpha,
+                                         fb.w, fb.yts, nullptr, di.cu_count, st));
                 tm.done();
             }
             uint8_t *cf = fb.cut_feature + (size_t)t * nin;
@@ -583,7 +613,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                     pc = ParentCuts{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
                 const int gl = t * D + l;   // side histograms alternate by gl's parity
                 {
-                    Timed tm(FBDT_K_HISTOGRAM, st, hist_algorithmic_bytes(n, d, n_bins, l, true));
+                    Timed tm(FBDT_K_HISTOGRAM, st,
+                             hist_algorithmic_bytes(n, d, n_bins, l, true, plans[l].sibling));
                     HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
                                              l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
                                              l >= 1 ? fb.node[l & 1] : nullptr, fb.w, vsign, pc, l,
@@ -593,17 +624,20 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 }
                 {
                     Timed tm(FBDT_K_BEST_CUTS, st);
-                    // right children below the root: parent - left child; the
-                    // next layer's side histogram (next tree's root after the
-                    // last layer) is cleared on the way
+                    // right children below the root: parent - left child (the
+                    // parents' summed rows are kept for that); the next layer's
+                    // side histogram (next tree's root after the last layer) is
+                    // cleared on the way
+                    const bool sib = plans[l].sibling;
                     const size_t next_count =
                         (size_t)(l + 1 < D ? 1 << (l + 1) : 1) * d * n_bins * 2;
                     HIP_TRY(launch_cut_scan(fb.partial, plans[l].chunks, scale, fb.small[gl & 1],
                                             fb.small[(gl + 1) & 1], next_count,
-                                            l >= 1 ? 1 << (l - 1) : 1, d, n_bins, l >= 1,
+                                            sib ? 1 << (l - 1) : 1 << l, d, n_bins, sib,
                                             fb.cand_gain, fb.cand_cut,
-                                            l >= 1 ? fb.hfull[(l - 1) & 1] : nullptr,
-                                            l + 1 < D ? fb.hfull[l & 1] : nullptr, st));
+                                            sib ? fb.hfull[(l - 1) & 1] : nullptr,
+                                            l + 1 < D && !missing ? fb.hfull[l & 1] : nullptr,
+                                            st));
                     tm.done();
                 }
             }
@@ -612,11 +646,11 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 const ParentCuts pc{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
                 Timed tm(FBDT_K_LEAF, st);
                 HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
-                                    fb.node[D & 1], pc, D, true, fb.v, fb.yts, lblocks,
+                                    fb.node[D & 1], pc, D, missing, true, fb.v, fb.yts, lblocks,
                                     fb.leaf_partial, fb.err, st));
                 if (!fused || t == T - 1)
-                    HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, eta,
-                                                 fb.leaf + (size_t)t * nleaf, st));
+                    HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, missing, eta,
+                                                 fb.leaf + (size_t)t * nslots, st));
                 tm.done();
             }
         }
@@ -627,7 +661,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     if (opt_fit_graphs.load() && !(g_timing.load() & timed_kinds)) {
         const GraphKey key{xb, y, w, n, ldb, d, n_bins, D, T, scale, lblocks, eta, alpha, seed,
                            opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load(),
-                           opt_hist_copies.load(), signed_w};
+                           opt_hist_copies.load(), signed_w, missing};
         hipGraphExec_t exec = nullptr;
         for (auto &g : a.graphs)
             if (g.first == key) exec = g.second;
@@ -663,8 +697,9 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     }
     if (score_out)
         HIP_TRY(launch_tree_prep(y, w, fb.F, nullptr, fb.node[D & 1],
-                                 fb.leaf + (size_t)(T - 1) * nleaf, nullptr, 0, 0.0, nullptr, D, n,
-                                 seed, T, alpha, nullptr, nullptr, score_out, di.cu_count, s));
+                                 fb.leaf + (size_t)(T - 1) * nslots, nullptr, 0, 0.0, nullptr, D,
+                                 missing, n, seed, T, alpha, nullptr, nullptr, score_out,
+                                 di.cu_count, s));
 
     fbdt_model *m = new (std::nothrow) fbdt_model;
     if (!m) return fail(FBDT_E_DEVICE, "out of host memory");
@@ -675,7 +710,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     m->cut_feature.resize((size_t)T * nin);
     m->cut_bin.resize((size_t)T * nin);
     m->gain.resize((size_t)T * nin);
-    m->leaf.resize((size_t)T * nleaf);
+    // the boost weights of every node (missing values) or of the leaves
+    std::vector<double> values((size_t)T * nslots);
     auto cleanup = [&](int code) {
         delete m;
         return code;
@@ -686,7 +722,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                        s) != hipSuccess ||
         hipMemcpyAsync(m->gain.data(), fb.gain, (size_t)T * nin * sizeof(double),
                        hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipMemcpyAsync(m->leaf.data(), fb.leaf, (size_t)T * nleaf * sizeof(double),
+        hipMemcpyAsync(values.data(), fb.leaf, values.size() * sizeof(double),
                        hipMemcpyDeviceToHost, s) != hipSuccess ||
         hipMemcpyAsync(&m->f0, fb.f0, sizeof(double), hipMemcpyDeviceToHost, s) != hipSuccess ||
         hipMemcpyAsync(&h_err, fb.err, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess) {
@@ -698,6 +734,18 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
         return cleanup(fail(FBDT_E_DEVICE, "fit failed: %s", hipGetErrorString(se)));
     if (h_err & kErrBin) return cleanup(fail(FBDT_E_INVAL, "a bin code is >= n_bins"));
     if (h_err & kErrRoute) return cleanup(fail(FBDT_E_DEVICE, "internal routing error"));
+    m->missing = missing;
+    m->leaf.resize((size_t)T * nleaf);
+    if (missing) m->inner.resize((size_t)T * nin);
+    for (size_t t = 0; t < (size_t)T; ++t) {
+        const double *row = values.data() + t * nslots;
+        if (missing) {   // heap order: the inner nodes, then the leaves
+            std::copy(row, row + nin, m->inner.begin() + t * nin);
+            std::copy(row + nin, row + nin + nleaf, m->leaf.begin() + t * nleaf);
+        } else {
+            std::copy(row, row + nleaf, m->leaf.begin() + t * nleaf);
+        }
+    }
     *out = m;
     return FBDT_OK;
 }
@@ -715,6 +763,7 @@ int fbdt_model_export(const fbdt_model *m, fbdt_model_view *v) {
     v->gain = m->gain.data();
     v->leaf = m->leaf.data();
     v->boundaries = m->boundaries.empty() ? nullptr : m->boundaries.data();
+    v->inner = m->missing ? m->inner.data() : nullptr;
     return FBDT_OK;
 }
 
@@ -725,6 +774,9 @@ int fbdt_model_import(const fbdt_model_view *v, fbdt_model **out) {
         return fail(FBDT_E_INVAL, "model dimensions out of range");
     if (!v->cut_feature || !v->cut_bin || !v->leaf)
         return fail(FBDT_E_INVAL, "cut_feature, cut_bin and leaf are required");
+    if (v->inner && v->n_bins > kMissingCode)
+        return fail(FBDT_E_INVAL, "inner boost weights (missing values) need n_bins <= %d",
+                    kMissingCode);
     if (!std::isfinite(v->f0)) return fail(FBDT_E_INVAL, "f0 is not finite");
     const size_t T = v->n_trees, nin = ((size_t)1 << v->depth) - 1, nleaf = (size_t)1 << v->depth;
     for (size_t k = 0; k < T * nin; ++k) {
@@ -754,6 +806,10 @@ int fbdt_model_import(const fbdt_model_view *v, fbdt_model **out) {
     if (v->boundaries)
         m->boundaries.assign(v->boundaries,
                              v->boundaries + (size_t)v->n_features * (v->n_bins - 1));
+    if (v->inner) {
+        m->missing = true;
+        m->inner.assign(v->inner, v->inner + T * nin);
+    }
     *out = m;
     return FBDT_OK;
 }
@@ -794,6 +850,46 @@ void fbdt_model_free(fbdt_model *m) {
 }
 
 // ---- apply ----------------------------------------------------------------
+// The model's device copy on `dev`, created on first use: the packed cuts and
+// the boost weights per tree (the leaves, or with missing values every node
+// in heap order).  Call with m->mu held.
+static int device_copy(fbdt_model *m, int dev, fbdt_model::DeviceCopy **out) {
+    for (auto &c : m->copies)
+        if (c.device == dev) {
+            *out = &c;
+            return FBDT_OK;
+        }
+    const size_t T = m->n_trees, nin = ((size_t)1 << m->depth) - 1;
+    const size_t nleaf = (size_t)1 << m->depth;
+    const size_t per_tree = m->missing ? nin + nleaf : nleaf;
+    std::vector<uint16_t> packed(T * nin);
+    for (size_t k = 0; k < packed.size(); ++k)
+        packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
+    std::vector<double> values(T * per_tree);
+    for (size_t t = 0; t < T; ++t) {
+        double *row = values.data() + t * per_tree;
+        if (m->missing) {
+            std::copy(m->inner.begin() + t * nin, m->inner.begin() + (t + 1) * nin, row);
+            row += nin;
+        }
+        std::copy(m->leaf.begin() + t * nleaf, m->leaf.begin() + (t + 1) * nleaf, row);
+    }
+    fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
+    HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
+    if (hipMalloc(&c.leaves, values.size() * sizeof(double)) != hipSuccess) {
+        (void)hipFree(c.cuts);
+        return fail(FBDT_E_DEVICE, "out of device memory");
+    }
+    m->copies.push_back(c);
+    fbdt_model::DeviceCopy *cp = &m->copies.back();
+    HIP_TRY(hipMemcpy(cp->cuts, packed.data(), packed.size() * sizeof(uint16_t),
+                      hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(cp->leaves, values.data(), values.size() * sizeof(double),
+                      hipMemcpyHostToDevice));
+    *out = cp;
+    return FBDT_OK;
+}
+
 int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
                float *prob, double *score, void *stream) {
     int rc;
@@ -808,8 +904,8 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     if ((rc = current_device(&dev, &di))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = m->n_trees, D = m->depth;
-    const size_t nin = ((size_t)1 << D) - 1, nleaf = (size_t)1 << D;
-    ApplyShape as = plan_apply(n, m->n_features, T, D, di.cu_count, di.max_lds,
+    const size_t nin = ((size_t)1 << D) - 1;
+    ApplyShape as = plan_apply(n, m->n_features, T, D, m->missing, di.cu_count, di.max_lds,
                                (int)opt_apply_threads.load());
     if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
         return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
@@ -820,25 +916,7 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     {
         std::lock_guard<std::mutex> lk(m->mu);
         fbdt_model::DeviceCopy *copy = nullptr;
-        for (auto &c : m->copies)
-            if (c.device == dev) copy = &c;
-        if (!copy) {
-            std::vector<uint16_t> packed((size_t)T * nin);
-            for (size_t k = 0; k < packed.size(); ++k)
-                packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
-            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
-            HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
-            if (hipMalloc(&c.leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
-                (void)hipFree(c.cuts);
-                return fail(FBDT_E_DEVICE, "out of device memory");
-            }
-            m->copies.push_back(c);
-            copy = &m->copies.back();
-            HIP_TRY(hipMemcpy(copy->cuts, packed.data(), packed.size() * sizeof(uint16_t),
-                              hipMemcpyHostToDevice));
-            HIP_TRY(hipMemcpy(copy->leaves, m->leaf.data(), (size_t)T * nleaf * sizeof(double),
-                              hipMemcpyHostToDevice));
-        }
+        if ((rc = device_copy(m, dev, &copy))) return rc;
         if (as.shallow && copy->nodes_stride != apply_node_stride(as)) {
             // node records for this launch's tile stride
             const int xs = apply_node_stride(as);
@@ -861,35 +939,6 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
     Timed tm(FBDT_K_APPLY, s, (double)n * (m->n_features + 4));
     HIP_TRY(launch_apply(as, xb, ldb, n, cuts, nodes, leaves, T, D, m->f0, prob, score, s));
     tm.done();
-    return FBDT_OK;
-}
-
-// The model's device copy on `dev` (cuts and leaves), created on first use.
-// Call with m->mu held.
-static int device_copy(fbdt_model *m, int dev, fbdt_model::DeviceCopy **out) {
-    for (auto &c : m->copies)
-        if (c.device == dev) {
-            *out = &c;
-            return FBDT_OK;
-        }
-    const size_t T = m->n_trees, nin = ((size_t)1 << m->depth) - 1;
-    const size_t nleaf = (size_t)1 << m->depth;
-    fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
-    std::vector<uint16_t> packed(T * nin);
-    for (size_t k = 0; k < packed.size(); ++k)
-        packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
-    HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
-    if (hipMalloc(&c.leaves, T * nleaf * sizeof(double)) != hipSuccess) {
-        (void)hipFree(c.cuts);
-        return fail(FBDT_E_DEVICE, "out of device memory");
-    }
-    m->copies.push_back(c);
-    fbdt_model::DeviceCopy *cp = &m->copies.back();
-    HIP_TRY(hipMemcpy(cp->cuts, packed.data(), packed.size() * sizeof(uint16_t),
-                      hipMemcpyHostToDevice));
-    HIP_TRY(hipMemcpy(cp->leaves, m->leaf.data(), T * nleaf * sizeof(double),
-                      hipMemcpyHostToDevice));
-    *out = cp;
     return FBDT_OK;
 }
 
@@ -918,7 +967,8 @@ int fbdt_event_importance(const fbdt_model *mc, const uint8_t *xb, int64_t n, in
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = m->n_trees, D = m->depth;
     const size_t nin = ((size_t)1 << D) - 1;
-    const ApplyShape as = plan_importance(n, m->n_features, T, D, di.cu_count, di.max_lds);
+    const ApplyShape as =
+        plan_importance(n, m->n_features, T, D, m->missing, di.cu_count, di.max_lds);
     if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
         return fail(FBDT_E_INVAL, "event importance needs %zu bytes of LDS, the device has %zu",
                     as.lds_bytes, di.max_lds);
@@ -955,9 +1005,9 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
     if ((rc = current_device(&dev, &di))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = m->n_trees, D = m->depth;
-    const size_t nin = ((size_t)1 << D) - 1, nleaf = (size_t)1 << D;
-    const ApplyShape as = plan_apply_float(n, m->n_features, T, D, di.cu_count, di.max_lds,
-                                           (int)opt_apply_threads.load());
+    const size_t nin = ((size_t)1 << D) - 1;
+    const ApplyShape as = plan_apply_float(n, m->n_features, T, D, m->missing, di.cu_count,
+                                           di.max_lds, (int)opt_apply_threads.load());
     if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
         return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
                     "apply_threads)", as.lds_bytes, di.max_lds);
@@ -968,25 +1018,7 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
         if (m->boundaries.empty())
             return fail(FBDT_E_INVAL, "the model has no bin boundaries (fbdt_model_set_boundaries)");
         fbdt_model::DeviceCopy *copy = nullptr;
-        for (auto &c : m->copies)
-            if (c.device == dev) copy = &c;
-        if (!copy) {
-            fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
-            std::vector<uint16_t> packed((size_t)T * nin);
-            for (size_t k = 0; k < packed.size(); ++k)
-                packed[k] = (uint16_t)(m->cut_feature[k] | (m->cut_bin[k] << 8));
-            HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
-            if (hipMalloc(&c.leaves, (size_t)T * nleaf * sizeof(double)) != hipSuccess) {
-                (void)hipFree(c.cuts);
-                return fail(FBDT_E_DEVICE, "out of device memory");
-            }
-            m->copies.push_back(c);
-            copy = &m->copies.back();
-            HIP_TRY(hipMemcpy(copy->cuts, packed.data(), packed.size() * sizeof(uint16_t),
-                              hipMemcpyHostToDevice));
-            HIP_TRY(hipMemcpy(copy->leaves, m->leaf.data(), (size_t)T * nleaf * sizeof(double),
-                              hipMemcpyHostToDevice));
-        }
+        if ((rc = device_copy(m, dev, &copy))) return rc;
         if (!copy->frec) {
             // cut "bin >= c" of feature j = "x >= boundary c of feature j"
             // (boundary index c - 1 of its row)
@@ -1026,7 +1058,7 @@ int fbdt_tree_weights(const int8_t *y, const float *v, const double *F, int64_t 
     hipStream_t s = static_cast<hipStream_t>(stream);
     Timed tm(FBDT_K_TREE_PREP, s, (double)n * 17.0);
     HIP_TRY(launch_tree_prep(y, v, const_cast<double *>(F), nullptr, nullptr, nullptr, nullptr, 0,
-                             0.0, nullptr, 1, n, seed, tree, alpha, w_out, nullptr, nullptr,
+                             0.0, nullptr, 1, false, n, seed, tree, alpha, w_out, nullptr, nullptr,
                              di.cu_count, s));
     tm.done();
     return FBDT_OK;
@@ -1084,7 +1116,7 @@ int fbdt_histogram(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t
     if (!std::isfinite(h_wsum)) return fail(FBDT_E_WEIGHT, "weights must be finite");
     const int scale = histogram_scale(h_wsum * (1.0 + 1e-6));
     {
-        Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, layer, false));
+        Timed tm(FBDT_K_HISTOGRAM, s, hist_algorithmic_bytes(n, d, n_bins, layer, false, false));
         HIP_TRY(launch_histogram(hs, xb, ldb, n, d, n_bins, node_pad, nullptr, w_pad, nullptr,
                                  ParentCuts{}, layer, false, scale, partial, small, err, s));
         tm.done();
@@ -1164,7 +1196,7 @@ int fbdt_leaf_values(const uint8_t *node, const int8_t *y, const float *v, const
     DeviceInfo di;
     if ((rc = current_device(&dev, &di))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int blocks = leaf_blocks(n, depth, di.cu_count);
+    const int blocks = leaf_blocks(n, depth, false, di.cu_count);
     // the leaf pass reads whole steps of events: padded copies of the leaf
     // ids and weights, and y~ of the sampled events (0 beyond n) from the
     // re-weighting pass
@@ -1192,11 +1224,11 @@ int fbdt_leaf_values(const uint8_t *node, const int8_t *y, const float *v, const
         HIP_TRY(hipMemcpyAsync(v_pad, v, (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, s));
     }
     HIP_TRY(launch_tree_prep(y, v, const_cast<double *>(F), nullptr, nullptr, nullptr, nullptr, 0,
-                             0.0, nullptr, depth, n, seed, tree, alpha, nullptr, yts, nullptr,
-                             di.cu_count, s));
-    HIP_TRY(launch_leaf(nullptr, 0, n, 1, node_pad, nullptr, ParentCuts{}, depth, false, v_pad,
-                        yts, blocks, lp, err, s));
-    HIP_TRY(launch_leaf_finalize(lp, blocks, depth, eta, leaf, s));
+                             0.0, nullptr, depth, false, n, seed, tree, alpha, nullptr, yts,
+                             nullptr, di.cu_count, s));
+    HIP_TRY(launch_leaf(nullptr, 0, n, 1, node_pad, nullptr, ParentCuts{}, depth, false, false,
+                        v_pad, yts, blocks, lp, err, s));
+    HIP_TRY(launch_leaf_finalize(lp, blocks, depth, false, eta, leaf, s));
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;
     if (h_err & kErrRoute) return fail(FBDT_E_INVAL, "a node id is not a leaf id (skipped)");

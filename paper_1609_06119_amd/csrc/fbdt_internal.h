@@ -18,7 +18,14 @@ enum : int {
     kErrRoute = 16,    // cut or node id out of range met while routing
     kErrClass = 32,    // a class has no positive total weight
     kNegWeights = 64,  // (not an error) some event weight is negative
+    kHasMissing = 128, // (not an error) some bin code is the missing code
 };
+
+// Missing values (section 4.2): with at most kMissingCode bins a NaN value
+// takes the bin code kMissingCode; it stays out of the feature's histograms,
+// and an event whose code of a node's cut feature is kMissingCode stops at
+// that node (its terminal node, whose boost weight it takes).
+constexpr int kMissingCode = 255;
 
 // Launch shape of one histogram pass.
 struct HistShape {
@@ -36,6 +43,8 @@ struct HistShape {
                               // lane l adds into copy l % copies
     int copy_stride;          // bytes between copies (the histograms plus a bank shift)
     size_t lds_bytes;         // dynamic LDS per workgroup
+    bool sibling;             // routed pass below the root histograms the left child of
+                              // each parent only (right = parent - left)
 };
 
 // Launch-shape overrides of the histogram pass (0 = the planner's choice).
@@ -100,6 +109,9 @@ hipError_t launch_fill_u32(void *p, uint32_t value, size_t count, hipStream_t s)
 
 hipError_t launch_validate(const int8_t *y, const float *v, int64_t n, double *class_partial,
                            int *err, hipStream_t s);
+// err |= flag if any of the first n codes of a row equals `code`.
+hipError_t launch_find_code(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t code,
+                            int flag, int *err, hipStream_t s);
 hipError_t launch_initial_score(const double *class_partial, double *f0, int *err,
                                 hipStream_t s);
 
@@ -118,8 +130,9 @@ constexpr int kFusedLeafDepth = 4;
 hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const double *f0,
                             const uint8_t *leaf_node, const double *leaf_prev,
                             const double *leaf_partial, int lblocks, double eta, double *leaf_rec,
-                            int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
-                            double *yts, double *score_out, int cu_count, hipStream_t s);
+                            int depth, bool missing, int64_t n, uint64_t seed, int tree,
+                            double alpha, float *w, double *yts, double *score_out, int cu_count,
+                            hipStream_t s);
 
 // ov: launch-shape overrides (0 = the planner's choice).  sibling: the
 // routed fit pass, which for layer >= 1 histograms one child per parent.
@@ -214,13 +227,21 @@ hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int 
 // writes eta * num / den per leaf.  node_in, v (or null: unit weights) and
 // yts hold round_up(n, 8) elements with yts = 0 beyond n; node_out receives
 // round_up(n, 8) ids.
-int leaf_blocks(int64_t n, int depth, int cu_count);
+// missing (section 4.2): the terminal nodes are every node of the tree, in
+// heap order (slot k - 1 = node k), and an event whose code of its node's
+// cut feature is kMissingCode stays at that node; launch_leaf_finalize then
+// writes the boost weight of every node, an inner node's over all the
+// sampled events that reached it.  The leaf pass of depth 7 with missing
+// values needs more LDS than a CU has (hipErrorInvalidValue).
+int leaf_blocks(int64_t n, int depth, bool missing, int cu_count);
+size_t leaf_lds_bytes(int depth, bool missing);
+constexpr size_t kLeafMaxLds = 136 * 1024;
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
-                       uint8_t *node_out, const ParentCuts &pc, int depth, bool routed,
-                       const float *v, const double *yts, int blocks, double *leaf_partial,
-                       int *err, hipStream_t s);
-hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, double eta,
-                                double *leaf_out, hipStream_t s);
+                       uint8_t *node_out, const ParentCuts &pc, int depth, bool missing,
+                       bool routed, const float *v, const double *yts, int blocks,
+                       double *leaf_partial, int *err, hipStream_t s);
+hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, bool missing,
+                                double eta, double *leaf_out, hipStream_t s);
 
 hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *node,
                         const uint8_t *cut_f, const uint8_t *cut_c, int layer, int *err,
@@ -233,14 +254,16 @@ hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_
 constexpr int kApplyShallowDepth = 3;
 struct ApplyShape {
     bool shallow;          // depth <= kApplyShallowDepth: apply_shallow_kernel
+    bool missing;          // missing values: boost weights of every node per tree (heap
+                           // order) and the missing code stops an event at its node
     int threads;
     int blocks;
     int trees_per_chunk;   // trees whose leaf values (and cuts) are staged in LDS at once
     int d_used;
     size_t lds_bytes;
 };
-ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_count,
-                      size_t max_lds, int threads);
+ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, bool missing,
+                      int cu_count, size_t max_lds, int threads);
 inline int apply_node_stride(const ApplyShape &as) { return 2 * as.threads + 8; }
 hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
                         const uint16_t *cuts, const uint32_t *nodes, const double *leaves,
@@ -250,8 +273,8 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
 // Per-event importance [d_out][ldi] (float64) of binned events: the gains of
 // the nodes on each event's path summed per cut feature, tree by tree.
 // cuts: [T][2^D-1] packed (feature | bin << 8); gains: [T][2^D-1].
-ApplyShape plan_importance(int64_t n, int d_used, int n_trees, int depth, int cu_count,
-                           size_t max_lds);
+ApplyShape plan_importance(int64_t n, int d_used, int n_trees, int depth, bool missing,
+                           int cu_count, size_t max_lds);
 hipError_t launch_importance(const ApplyShape &as, const uint8_t *xb, int64_t ldb, int64_t n,
                              const uint16_t *cuts, const double *gains, int n_trees, int depth,
                              double *imp, int64_t ldi, int d_out, hipStream_t s);
@@ -259,8 +282,8 @@ hipError_t launch_importance(const ApplyShape &as, const uint8_t *xb, int64_t ld
 // Traversal of float32 events [d][ldx] with value thresholds.  rec: [T][2^D-1]
 // (feature, float bits of the threshold) per heap node.  as.shallow marks
 // depth <= kApplyShallowDepth (every node tested, records by scalar loads).
-ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, int cu_count,
-                            size_t max_lds, int threads);
+ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, bool missing,
+                            int cu_count, size_t max_lds, int threads);
 hipError_t launch_apply_float(const ApplyShape &as, const float *x, int64_t ldx, int64_t n,
                               const uint2 *rec, const double *leaves, int n_trees, int depth,
                               double f0, float *prob, double *score, hipStream_t s);
@@ -276,11 +299,13 @@ struct QuantileScratch {
 };
 int quantile_batch_features(int64_t n, int d);
 hipError_t quantile_scratch(int64_t n, int d, QuantileScratch *qs);
-// x: device float32 [d][ldx]; bounds: device float32 [d][n_bins - 1]; err
-// receives kErrNan if any value is NaN (the boundaries are then undefined).
+// x: device float32 [d][ldx]; bounds: device float32 [d][n_bins - 1], over
+// the non-NaN values of each feature; nan_count: device [d] scratch; err
+// receives kErrNan if a value is NaN and n_bins > kMissingCode.
 hipError_t launch_quantile_boundaries(const float *x, int64_t ldx, int64_t n, int d, int n_bins,
                                       const QuantileScratch &qs, uint64_t *keys_a,
-                                      uint64_t *keys_b, void *temp, float *bounds, int *err,
+                                      uint64_t *keys_b, void *temp,
+                                      unsigned long long *nan_count, float *bounds, int *err,
                                       hipStream_t s);
 
 hipError_t launch_encode(const float *x, int64_t ldx, int64_t n, int d, const float *bounds,

@@ -176,12 +176,34 @@ __global__ __launch_bounds__(256) void initial_score_kernel(const double *__rest
 // / nv, then the stripes are added pairwise.
 constexpr int kLeafReduceThreads = 1024;
 
+// With missing values (section 4.2) the slots are all nodes of the tree in
+// heap order (slot k - 1 = node k) holding (num, den) of the events whose
+// terminal node it is: every inner node (the first `inner` slots) adds its
+// children's sums, bottom up in a fixed order, and then every slot becomes
+// eta * num / den (0 where den = 0).  s[2 slot] = num, s[2 slot + 1] = den
+// on entry; s[slot] = the weight on exit.
+__device__ void node_sums_to_weights(double *s, int nslots, int inner, double eta) {
+#pragma clang fp contract(off)
+    if (threadIdx.x == 0) {
+        for (int k = inner; k >= 1; --k) {   // node k's children: nodes 2k, 2k + 1
+            s[2 * (k - 1)] += s[2 * (2 * k - 1)] + s[2 * (2 * k)];
+            s[2 * (k - 1) + 1] += s[2 * (2 * k - 1) + 1] + s[2 * (2 * k) + 1];
+        }
+        for (int k = 0; k < nslots; ++k) {
+            const double num = s[2 * k], den = s[2 * k + 1];
+            s[k] = den == 0.0 ? 0.0 : eta * (num / den);
+        }
+    }
+    __syncthreads();
+}
+
 __device__ void reduce_leaf_partials(const double *__restrict__ leaf_partial, int nblocks,
-                                     int nleaf, double eta, double *red, double *s_leaf) {
+                                     int nleaf, double eta, double *red, double *s_leaf,
+                                     int bottom_up_inner = 0) {
 #pragma clang fp contract(off)
     const int nv = 2 * nleaf;
     const int t = threadIdx.x;
-    if (nv <= kWave) {
+    if (nv <= kWave && (nv & (nv - 1)) == 0) {   // a power of two: lanes share a wavefront
         const int lane = t % kWave, wave = t / kWave;
         const int per_wave = kWave / nv;
         const int stripes = (kLeafReduceThreads / kWave) * per_wave;
@@ -205,12 +227,19 @@ __device__ void reduce_leaf_partials(const double *__restrict__ leaf_partial, in
                 num += red[w * nv + 2 * t];
                 den += red[w * nv + 2 * t + 1];
             }
-            s_leaf[t] = den == 0.0 ? 0.0 : eta * (num / den);
+            if (bottom_up_inner) {
+                s_leaf[2 * t] = num;
+                s_leaf[2 * t + 1] = den;
+            } else {
+                s_leaf[t] = den == 0.0 ? 0.0 : eta * (num / den);
+            }
         }
         lds_barrier();
+        if (bottom_up_inner) node_sums_to_weights(s_leaf, nleaf, bottom_up_inner, eta);
         return;
     }
-    const int stripes = kLeafReduceThreads / nv;
+    int stripes = 1;   // a power of two
+    while (2 * stripes * nv <= kLeafReduceThreads) stripes *= 2;
     if (t < stripes * nv) {
         const int val = t % nv, st = t / nv;
         double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
@@ -232,9 +261,15 @@ __device__ void reduce_leaf_partials(const double *__restrict__ leaf_partial, in
     }
     if (t < nleaf) {
         const double num = red[2 * t], den = red[2 * t + 1];
-        s_leaf[t] = den == 0.0 ? 0.0 : eta * (num / den);
+        if (bottom_up_inner) {
+            s_leaf[2 * t] = num;
+            s_leaf[2 * t + 1] = den;
+        } else {
+            s_leaf[t] = den == 0.0 ? 0.0 : eta * (num / den);
+        }
     }
     __syncthreads();
+    if (bottom_up_inner) node_sums_to_weights(s_leaf, nleaf, bottom_up_inner, eta);
 }
 
 // ---------------------------------------------------------------------------
@@ -258,12 +293,16 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     const int8_t *__restrict__ y, const float *__restrict__ v, double *__restrict__ F,
     const double *__restrict__ f0, const uint8_t *__restrict__ leaf_node,
     const double *__restrict__ leaf_prev, const double *__restrict__ leaf_partial,
-    int lblocks, double eta, double *__restrict__ leaf_rec, int depth, int64_t n,
+    int lblocks, double eta, double *__restrict__ leaf_rec, int depth, bool missing, int64_t n,
     uint64_t seed, int tree, double alpha, float *__restrict__ w, double *__restrict__ yts,
     double *__restrict__ score_out, int64_t xcd_events) {
     __shared__ double red[kLeafReduceThreads];
-    __shared__ double s_leaf[128];
+    __shared__ double s_leaf[256];
+    // boost weights of the terminal nodes: the leaves (heap ids from 2^D), or
+    // with missing values every node (heap ids from 1)
     const unsigned nleaf = 1u << depth;
+    const unsigned nslots = missing ? 2u * nleaf - 1u : nleaf;
+    const unsigned first_id = missing ? 1u : nleaf;
     const bool have_leaf = leaf_prev || leaf_partial;
     const bool read_F = have_leaf || !f0;
     // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
@@ -284,18 +323,20 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     PrepStep A, B;
     if (ia < xend) load(A, ia);
     if (leaf_partial) {
-        reduce_leaf_partials(leaf_partial, lblocks, (int)nleaf, eta, red, s_leaf);
-        if (blockIdx.x == 0 && leaf_rec && threadIdx.x < nleaf) leaf_rec[threadIdx.x] = s_leaf[threadIdx.x];
+        reduce_leaf_partials(leaf_partial, lblocks, (int)nslots, eta, red, s_leaf,
+                             missing ? (int)nleaf - 1 : 0);
+        if (blockIdx.x == 0 && leaf_rec && threadIdx.x < nslots)
+            leaf_rec[threadIdx.x] = s_leaf[threadIdx.x];
     } else if (leaf_prev) {
-        for (unsigned t = threadIdx.x; t < nleaf; t += blockDim.x) s_leaf[t] = leaf_prev[t];
+        for (unsigned t = threadIdx.x; t < nslots; t += blockDim.x) s_leaf[t] = leaf_prev[t];
         lds_barrier();
     }
     const double f0v = (f0 && !have_leaf) ? *f0 : 0.0;
     auto step = [&](const PrepStep &st, int64_t i) {
         double Fi;
         if (have_leaf) {
-            unsigned li = st.leaf - nleaf;
-            if (li >= nleaf) li = 0;  // unreachable: leaf ids come from the leaf pass
+            unsigned li = st.leaf - first_id;
+            if (li >= nslots) li = 0;  // unreachable: terminal ids come from the leaf pass
             Fi = st.F + s_leaf[li];
             F[i] = Fi;
         } else if (f0) {
@@ -509,6 +550,8 @@ struct HistArgs {
     const uint8_t *xb;
     int64_t ldb, n;
     int d, nbins, layer, nodes, half, j0, nf, k0, nk, scale;
+    bool miss;                        // n_bins <= kMissingCode: code kMissingCode is missing
+    bool sib;                         // left children only (right = parent - left)
     uint32_t tau_bits;                // bits of the smallest weight on the fixed-point grid
     const uint8_t *node_in;
     uint8_t *node_out;
@@ -557,10 +600,12 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
     // Per event: slot = index of the histogrammed node within the group
     // (>= nk: not this group's), nl = node of this layer - nodes (side
     // histogram index), counted = the event's node is histogrammed here.
-    // Routed passes below the root histogram the left child of every parent
-    // only (slot = parent index); the right child's fixed-point histogram is
-    // parent - left.  Weights below the grid go to the side histogram of
-    // every node, left or right.
+    // Routed passes below the root with sib histogram the left child of
+    // every parent only (slot = parent index); the right child's fixed-point
+    // histogram is parent - left.  Without sib (fits with missing values,
+    // where events that stop at a parent are in its histograms but in
+    // neither child's) both children are histogrammed.  Weights below the
+    // grid go to the side histogram of every node, left or right.
     uint32_t slot[kHistE], nl[kHistE];
     bool counted[kHistE];
     uint32_t bad = 0u;
@@ -584,6 +629,7 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
 #pragma unroll
         for (int e = 0; e < kHistE; ++e) {
             uint32_t par, k, code, c;
+            bool stop = false;   // the event stays at its node (missing value)
             if (NP == 1) {   // layer 1: the root is the only parent
                 par = 1u;
                 k = 0u;
@@ -592,10 +638,14 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
             } else {
                 par = byte8(st.node, e);
                 k = par - (uint32_t)a.half;
-                if (k >= (uint32_t)a.half) {   // unreachable for ids written by this library
-                    bad = 1u;
+                if (k >= (uint32_t)a.half) {
+                    // below the layer: stopped earlier at a missing value;
+                    // above it: unreachable for ids written by this library
+                    const bool earlier = a.miss & (par < (uint32_t)a.half);
+                    stop = earlier;
+                    bad |= earlier ? 0u : 1u;
                     k = 0u;
-                    par = (uint32_t)a.half;
+                    par = earlier ? par : (uint32_t)a.half;
                 }
                 if (NP > 0) {
                     code = byte8(st.rows[0], e);
@@ -612,12 +662,14 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
                     c = s_cc[k];
                 }
             }
+            stop |= a.miss & (code == (uint32_t)kMissingCode);
             const uint32_t right = code >= c ? 1u : 0u;
-            const uint32_t ne = 2u * par + right;
+            const uint32_t ne = stop ? par : 2u * par + right;
             o[e >> 2] |= ne << (8 * (e & 3));
             nl[e] = ne - (uint32_t)a.nodes;
-            slot[e] = k - (uint32_t)a.k0;
-            counted[e] = right == 0u;
+            // stopped: counted nowhere
+            slot[e] = stop ? 0xffffffffu : (a.sib ? k : nl[e]) - (uint32_t)a.k0;
+            counted[e] = !stop & (!a.sib | (right == 0u));
         }
         // padded events get ids too, so that the next layer reads valid parents
         if (writer) *reinterpret_cast<uint2 *>(a.node_out + i0) = make_uint2(o[0], o[1]);
@@ -657,7 +709,8 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
 #pragma unroll
                 for (int ff = 0; ff < FPG; ++ff) {
                     const uint32_t bin = byte8(st.codes[ff], e);
-                    if (ff < a.nf && bin >= (uint32_t)a.nbins) eflag |= kErrBin;
+                    const bool missing = a.miss & (bin == (uint32_t)kMissingCode);
+                    if (ff < a.nf && bin >= (uint32_t)a.nbins && !missing) eflag |= kErrBin;
                     if (ff < a.nf && bin < (uint32_t)a.nbins) {
                         const size_t gi =
                             ((((size_t)nl[e] * a.d + a.j0 + ff) * a.nbins + bin) * 2) +
@@ -677,7 +730,8 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const float *__restrict__ w, const uint8_t *__restrict__ vsign,
     const double *__restrict__ cand_gain,
     const int *__restrict__ cand_cut, int cslices, uint8_t *__restrict__ rec_f,
-    uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, int G, int npg, int NG,
+    uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, bool sib, int G, int npg,
+    int NG,
     int chunks, int64_t chunk_events, int64_t xcd_events, int scale, int copies,
     int copy_stride, uint64_t *__restrict__ partial, double *__restrict__ small,
     int *__restrict__ err) {
@@ -702,10 +756,12 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     a.n = n;
     a.d = d;
     a.nbins = nbins;
+    a.miss = nbins <= kMissingCode;
     a.layer = layer;
     a.nodes = 1 << layer;
     a.half = a.nodes >> 1;
-    const int hnodes = ROUTED && layer >= 1 ? a.half : a.nodes;   // histogrammed nodes
+    a.sib = ROUTED && layer >= 1 && sib;
+    const int hnodes = a.sib ? a.half : a.nodes;   // histogrammed nodes
     a.j0 = g * FPG;
     a.nf = min(FPG, d - a.j0);
     a.k0 = h * npg;
@@ -828,7 +884,8 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         const int f = rr - k * a.nf;
         const uint4 *src = reinterpret_cast<const uint4 *>(lds + (k * FPG + f) * kRow);
         uint4 *dst = out + ((size_t)(a.k0 + k) * d + a.j0 + f) * nbins;
-        for (int t = nbins + lane; t < 256; t += kWave) {
+        // bins >= n_bins must be empty, but for the missing code's
+        for (int t = nbins + lane; t < (a.miss ? kMissingCode : 256); t += kWave) {
             const uint4 v = src[t];
             if (v.x | v.y | v.z | v.w) eflag |= kErrBin;
         }
@@ -1222,9 +1279,15 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
 // issued before the current step's arithmetic.
 constexpr int kLeafE = 8;
 
-__host__ __device__ constexpr int leaf_threads(int depth) {
-    // acc takes threads * 2^(depth + 1) doubles: at most 128 KiB
-    return depth <= 5 ? 256 : depth == 6 ? 128 : 64;
+// Terminal-node slots of the leaf pass: the 2^D leaves, or with missing
+// values every node of the tree (2^(D+1) - 1).
+__host__ __device__ constexpr int leaf_slots(int depth, bool missing) {
+    return missing ? (2 << depth) - 1 : 1 << depth;
+}
+
+__host__ __device__ constexpr int leaf_threads(int depth, bool missing) {
+    // acc takes threads * 2 slots doubles: at most ~133 KiB
+    return 2 * leaf_slots(depth, missing) <= 64 ? 256 : 2 * leaf_slots(depth, missing) <= 128 ? 128 : 64;
 }
 
 template <int NP>
@@ -1279,14 +1342,19 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
-    int depth, const float *__restrict__ v, const double *__restrict__ yts,
+    int depth, bool missing, const float *__restrict__ v, const double *__restrict__ yts,
     double *__restrict__ leaf_partial, int *__restrict__ err, int64_t xcd_events) {
 #pragma clang fp contract(off)
-    extern __shared__ double acc[];   // [2 nleaf][T + 1], then the segment sums
+    // Sums per terminal node: the leaves, and with missing values (section
+    // 4.2) every node, since an event stops at the node that cuts on its
+    // missing value; slot = heap id - first_id.
+    extern __shared__ double acc[];   // [2 nslots][T + 1], then the segment sums
     __shared__ uint8_t s_cf[64], s_cc[64];
     const int T = blockDim.x;
     const int nleaf = 1 << depth;
-    const int nv = 2 * nleaf;
+    const uint32_t first_id = missing ? 1u : (uint32_t)nleaf;
+    const int nslots = missing ? 2 * nleaf - 1 : nleaf;
+    const int nv = 2 * nslots;
     const int half = nleaf >> 1;
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
@@ -1343,10 +1411,15 @@ __global__ __launch_bounds__(256) void leaf_kernel(
             if (ROUTED) {
                 uint32_t par = byte8(st.node, e);
                 uint32_t k = par - (uint32_t)half;
-                if (k >= (uint32_t)half) {   // unreachable for ids written by this library
-                    eflag |= kErrRoute;
+                bool stop = false;
+                if (k >= (uint32_t)half) {
+                    // below the layer: stopped earlier at a missing value;
+                    // above it: unreachable for ids written by this library
+                    const bool earlier = missing & (par < (uint32_t)half);
+                    stop = earlier;
+                    if (!earlier) eflag |= kErrRoute;
                     k = 0u;
-                    par = (uint32_t)half;
+                    par = earlier ? par : (uint32_t)half;
                 }
                 uint32_t x, c;
                 if (NP > 0) {
@@ -1363,15 +1436,16 @@ __global__ __launch_bounds__(256) void leaf_kernel(
                     x = xb[(int64_t)min((int)s_cf[k], d - 1) * ldb + i0 + e];
                     c = s_cc[k];
                 }
-                leaf = 2u * par + (x >= c ? 1u : 0u);
+                stop |= missing & (x == (uint32_t)kMissingCode);
+                leaf = stop ? par : 2u * par + (x >= c ? 1u : 0u);
                 o[e >> 2] |= leaf << (8 * (e & 3));
             } else {
                 leaf = byte8(st.node, e);
             }
-            const uint32_t li = leaf - (uint32_t)nleaf;
+            const uint32_t li = leaf - first_id;
             const double yt = st.yt[e];
             if (yt != 0.0) {   // sampled
-                if (li >= (uint32_t)nleaf) {   // unreachable for ids written by this library
+                if (li >= (uint32_t)nslots) {   // unreachable for ids written by this library
                     eflag |= kErrRoute;
                     continue;
                 }
@@ -1401,8 +1475,10 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     }
     lds_barrier();
     // columns added in a fixed order: G segments of T / G columns per value,
-    // then the G segment sums
-    const int G = T >= nv ? T / nv : 1;
+    // then the G segment sums; G is a power of two (nv need not be one, so
+    // T / nv may not divide T) with G nv <= T
+    int G = 1;
+    while (2 * G * nv <= T) G *= 2;
     const int seg = T / G;
     double *segsum = acc + (size_t)nv * TP;   // [G][nv]
     for (int idx = threadIdx.x; idx < nv * G; idx += T) {
@@ -1425,12 +1501,12 @@ __global__ __launch_bounds__(256) void leaf_kernel(
 }
 
 __global__ __launch_bounds__(kLeafReduceThreads) void leaf_finalize_kernel(
-    const double *__restrict__ leaf_partial, int nblocks, int nleaf, double eta,
+    const double *__restrict__ leaf_partial, int nblocks, int nslots, int inner, double eta,
     double *__restrict__ leaf_out) {
     __shared__ double red[kLeafReduceThreads];
-    __shared__ double s_leaf[128];
-    reduce_leaf_partials(leaf_partial, nblocks, nleaf, eta, red, s_leaf);
-    if ((int)threadIdx.x < nleaf) leaf_out[threadIdx.x] = s_leaf[threadIdx.x];
+    __shared__ double s_leaf[256];
+    reduce_leaf_partials(leaf_partial, nblocks, nslots, eta, red, s_leaf, inner);
+    for (int t = threadIdx.x; t < nslots; t += blockDim.x) leaf_out[t] = s_leaf[t];
 }
 
 // node <- 2 node + [xb[f][i] >= c] with (f, c) the cut of the node.
@@ -1468,10 +1544,13 @@ __global__ __launch_bounds__(256) void route_kernel(const uint8_t *__restrict__ 
 __global__ __launch_bounds__(1024) void apply_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d_used,
     const uint16_t *__restrict__ cuts, const double *__restrict__ leaves, int T, int depth,
-    int tpc, double f0, float *__restrict__ prob, double *__restrict__ score) {
+    bool missing, int tpc, double f0, float *__restrict__ prob, double *__restrict__ score) {
     extern __shared__ double smem[];
     const int nin = (1 << depth) - 1;
-    const int nleaf = 1 << depth;
+    // boost weights per tree: the leaves, or with missing values (section
+    // 4.2) every node in heap order, for events that stop at an inner node
+    const int nleaf = missing ? 2 * nin + 1 : 1 << depth;
+    const int first_id = missing ? 1 : 1 << depth;
     double *s_leaf = smem;
     uint16_t *s_cut = reinterpret_cast<uint16_t *>(s_leaf + (size_t)tpc * nleaf);
     uint8_t *s_x = reinterpret_cast<uint8_t *>(s_cut + (((size_t)tpc * nin + 3) & ~(size_t)3));
@@ -1503,9 +1582,11 @@ __global__ __launch_bounds__(1024) void apply_kernel(
                     const uint16_t cc = s_cut[t * nin + node - 1];
                     const int f = cc & 0xff;
                     const int c = cc >> 8;
-                    node = 2 * node + (s_x[f * XS + threadIdx.x] >= c ? 1 : 0);
+                    const int code = s_x[f * XS + threadIdx.x];
+                    if (missing && code == kMissingCode) break;   // stops at this node
+                    node = 2 * node + (code >= c ? 1 : 0);
                 }
-                Fv += s_leaf[t * nleaf + node - nleaf];
+                Fv += s_leaf[t * nleaf + node - first_id];
             }
         }
         if (i < n) {
@@ -1661,7 +1742,7 @@ __global__ __launch_bounds__(1024) void apply_shallow_kernel(
 __global__ __launch_bounds__(256) void importance_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d_used,
     const uint16_t *__restrict__ cuts, const double *__restrict__ gains, int T, int depth,
-    int tpc, double *__restrict__ imp, int64_t ldi, int d_out) {
+    bool missing, int tpc, double *__restrict__ imp, int64_t ldi, int d_out) {
     extern __shared__ double smem[];
     const int nin = (1 << depth) - 1;
     const int nt = blockDim.x;
@@ -1694,8 +1775,10 @@ __global__ __launch_bounds__(256) void importance_kernel(
                     const int k = t * nin + node - 1;
                     const uint16_t cc = s_cut[k];
                     const int f = cc & 0xff;
+                    const int code = s_x[f * XS + threadIdx.x];
+                    if (missing && code == kMissingCode) break;   // the cut does not apply
                     s_acc[f * nt + threadIdx.x] += s_gain[k];
-                    node = 2 * node + (s_x[f * XS + threadIdx.x] >= (cc >> 8) ? 1 : 0);
+                    node = 2 * node + (code >= (cc >> 8) ? 1 : 0);
                 }
             }
         }
@@ -1733,15 +1816,19 @@ __device__ __forceinline__ uint32_t float_leaf(const float *xme, int XS, const u
 template <int D>
 __global__ __launch_bounds__(1024) void apply_float_kernel(
     const float *__restrict__ x, int64_t ldx, int64_t n, int d_used,
-    const uint2 *__restrict__ rec, const double *__restrict__ leaves, int T, int tpc, double f0,
-    float *__restrict__ prob, double *__restrict__ score) {
-    constexpr int NLEAF = 1 << D;
+    const uint2 *__restrict__ rec, const double *__restrict__ leaves, int T, bool missing,
+    int tpc, double f0, float *__restrict__ prob, double *__restrict__ score) {
     constexpr int NIN = (1 << D) - 1;
-    constexpr bool kAll = D <= kApplyShallowDepth;
+    // boost weights per tree: the leaves, or with missing values every node
+    // in heap order (a NaN value stops its event at the node cutting on it);
+    // missing values take the walk below, which stages the records in LDS
+    const int NLEAF = missing ? 2 * NIN + 1 : 1 << D;
+    const int first_id = missing ? 1 : 1 << D;
+    const bool all = (D <= kApplyShallowDepth) && !missing;
     extern __shared__ double smem[];
     double *s_leaf = smem;                                                    // [tpc][NLEAF]
     uint2 *s_rec = reinterpret_cast<uint2 *>(s_leaf + (size_t)tpc * NLEAF);   // [tpc][NIN]
-    float *s_x = reinterpret_cast<float *>(s_rec + (kAll ? 0 : (size_t)tpc * NIN));
+    float *s_x = reinterpret_cast<float *>(s_rec + (all ? 0 : (size_t)tpc * NIN));
     const int XS = blockDim.x;   // [d_used][XS]
     const int nchunks = (T + tpc - 1) / tpc;
     const int64_t ntiles = (n + blockDim.x - 1) / blockDim.x;
@@ -1759,7 +1846,7 @@ __global__ __launch_bounds__(1024) void apply_float_kernel(
                 __syncthreads();
                 for (int q = threadIdx.x; q < tc * NLEAF; q += blockDim.x)
                     s_leaf[q] = leaves[(size_t)t0 * NLEAF + q];
-                if (!kAll)
+                if (!all)
                     for (int q = threadIdx.x; q < tc * NIN; q += blockDim.x) {
                         const uint2 r = rec[(size_t)t0 * NIN + q];
                         s_rec[q] = make_uint2(r.x * (uint32_t)XS, r.y);   // row offset
@@ -1767,7 +1854,7 @@ __global__ __launch_bounds__(1024) void apply_float_kernel(
                 staged = true;
             }
             __syncthreads();
-            if constexpr (kAll) {
+            if (D <= kApplyShallowDepth && all) {
                 int t = 0;
                 for (; t + kApplyBatch <= tc; t += kApplyBatch) {
                     uint2 r[kApplyBatch][NIN];
@@ -1778,7 +1865,7 @@ __global__ __launch_bounds__(1024) void apply_float_kernel(
                     double lv[kApplyBatch];
 #pragma unroll
                     for (int u = 0; u < kApplyBatch; ++u)
-                        lv[u] = s_leaf[(t + u) * NLEAF + float_leaf<D>(xme, XS, r[u])];
+                        lv[u] = s_leaf[(t + u) * NLEAF + float_leaf<(D < 3 ? D : 3)>(xme, XS, r[u])];
 #pragma unroll
                     for (int u = 0; u < kApplyBatch; ++u) Fv += lv[u];
                 }
@@ -1786,7 +1873,7 @@ __global__ __launch_bounds__(1024) void apply_float_kernel(
                     uint2 r[NIN];
 #pragma unroll
                     for (int k = 0; k < NIN; ++k) r[k] = rec[(size_t)(t0 + t) * NIN + k];
-                    Fv += s_leaf[t * NLEAF + float_leaf<D>(xme, XS, r)];
+                    Fv += s_leaf[t * NLEAF + float_leaf<(D < 3 ? D : 3)>(xme, XS, r)];
                 }
             } else {
                 for (int t = 0; t < tc; ++t) {
@@ -1794,9 +1881,11 @@ __global__ __launch_bounds__(1024) void apply_float_kernel(
 #pragma unroll
                     for (int lvl = 0; lvl < D; ++lvl) {
                         const uint2 r = s_rec[t * NIN + node - 1];
-                        node = 2 * node + (xme[r.x] >= __uint_as_float(r.y) ? 1 : 0);
+                        const float xv = xme[r.x];
+                        if (missing && xv != xv) break;   // NaN: stops at this node
+                        node = 2 * node + (xv >= __uint_as_float(r.y) ? 1 : 0);
                     }
-                    Fv += s_leaf[t * NLEAF + node - NLEAF];
+                    Fv += s_leaf[t * NLEAF + node - first_id];
                 }
             }
         }
@@ -1824,7 +1913,12 @@ __global__ __launch_bounds__(256) void encode_kernel(const float *__restrict__ x
         uint8_t code = 0;
         const float val = x[(int64_t)j * ldx + i];
         if (val != val) {
-            eflag |= kErrNan;
+            // a missing value: the reserved code with at most 255 bins
+            // (section 4.2), else an error
+            if (nbins <= kMissingCode)
+                code = (uint8_t)kMissingCode;
+            else
+                eflag |= kErrNan;
         } else {
             int lo = 0, len = nb;
             while (len > 0) {
@@ -1945,12 +2039,13 @@ hipError_t launch_initial_score(const double *class_partial, double *f0, int *er
 hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const double *f0,
                             const uint8_t *leaf_node, const double *leaf_prev,
                             const double *leaf_partial, int lblocks, double eta, double *leaf_rec,
-                            int depth, int64_t n, uint64_t seed, int tree, double alpha, float *w,
-                            double *yts, double *score_out, int cu_count, hipStream_t s) {
+                            int depth, bool missing, int64_t n, uint64_t seed, int tree,
+                            double alpha, float *w, double *yts, double *score_out, int cu_count,
+                            hipStream_t s) {
     if (leaf_partial && depth > kFusedLeafDepth) return hipErrorInvalidValue;
     tree_prep_kernel<<<xcd_grid(n, kLeafReduceThreads, cu_count), kLeafReduceThreads, 0, s>>>(
-        y, v, F, f0, leaf_node, leaf_prev, leaf_partial, lblocks, eta, leaf_rec, depth, n, seed,
-        tree, alpha, w, yts, score_out, xcd_range(n));
+        y, v, F, f0, leaf_node, leaf_prev, leaf_partial, lblocks, eta, leaf_rec, depth, missing, n,
+        seed, tree, alpha, w, yts, score_out, xcd_range(n));
     return hipGetLastError();
 }
 
@@ -2058,6 +2153,7 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     hs.copies = copies;
     hs.copy_stride = copies > 1 ? (int)(one + kHistCopyShift) : (int)one;
     hs.lds_bytes = copies > 1 ? (size_t)copies * hs.copy_stride : one;
+    hs.sibling = sibling && layer >= 1;
     return hs;
 }
 
@@ -2078,9 +2174,9 @@ hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, i
                           uint64_t *partial, double *small, int *err, hipStream_t s) {
     hist_kernel<ROUTED, NP, FPG, SIGNED><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices,
-        pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.feature_groups, hs.nodes_per_group, hs.node_groups,
-        hs.chunks, hs.chunk_events, hs.xcd_events, scale, hs.copies, hs.copy_stride, partial, small,
-        err);
+        pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.sibling, hs.feature_groups, hs.nodes_per_group,
+        hs.node_groups, hs.chunks, hs.chunk_events, hs.xcd_events, scale, hs.copies,
+        hs.copy_stride, partial, small, err);
     return hipGetLastError();
 }
 
@@ -2163,6 +2259,24 @@ hipError_t launch_merge_partials(const uint64_t *partial, int chunks, size_t cou
     return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void find_code_kernel(const uint8_t *__restrict__ xb,
+                                                        int64_t ldb, int64_t n, uint8_t code,
+                                                        int flag, int *__restrict__ err) {
+    const int j = blockIdx.y;
+    bool found = false;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        found |= xb[(int64_t)j * ldb + i] == code;
+    if (__any(found) && threadIdx.x % kWave == 0) atomicOr(err, flag);
+}
+
+hipError_t launch_find_code(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t code,
+                            int flag, int *err, hipStream_t s) {
+    const dim3 grid((unsigned)grid_for(n, 256, 256), (unsigned)d);
+    find_code_kernel<<<grid, 256, 0, s>>>(xb, ldb, n, code, flag, err);
+    return hipGetLastError();
+}
+
 hipError_t launch_abs_sum(const float *w, int64_t n, double *block_partial, double *out,
                           hipStream_t s) {
     abs_sum_kernel<<<kValidateBlocks, 256, 0, s>>>(w, n, block_partial);
@@ -2203,46 +2317,52 @@ hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int 
     return hipGetLastError();
 }
 
-int leaf_blocks(int64_t n, int depth, int cu_count) {
-    return xcd_grid(n, (int64_t)kLeafE * leaf_threads(depth), cu_count);
+int leaf_blocks(int64_t n, int depth, bool missing, int cu_count) {
+    return xcd_grid(n, (int64_t)kLeafE * leaf_threads(depth, missing), cu_count);
 }
 
-size_t leaf_lds_bytes(int depth) {
-    const size_t T = (size_t)leaf_threads(depth), nv = (size_t)2 << depth;
+size_t leaf_lds_bytes(int depth, bool missing) {
+    const size_t T = (size_t)leaf_threads(depth, missing);
+    const size_t nv = 2 * (size_t)leaf_slots(depth, missing);
     return (nv * (T + 1) + (T >= nv ? T : nv)) * sizeof(double);
 }
 
 template <bool ROUTED, int NP>
 void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t n, int d,
              const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
-             const float *v, const double *yts, double *leaf_partial, int *err) {
-    leaf_kernel<ROUTED, NP><<<blocks, leaf_threads(depth), leaf_lds_bytes(depth), s>>>(
-        xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut, pc.slices, pc.rec_f,
-        pc.rec_c, pc.rec_g, depth, v, yts, leaf_partial, err, xcd_range(n));
+             bool missing, const float *v, const double *yts, double *leaf_partial, int *err) {
+    leaf_kernel<ROUTED, NP><<<blocks, leaf_threads(depth, missing), leaf_lds_bytes(depth, missing),
+                              s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut,
+                                   pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, depth, missing, v, yts,
+                                   leaf_partial, err, xcd_range(n));
 }
 
 hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const uint8_t *node_in,
-                       uint8_t *node_out, const ParentCuts &pc, int depth, bool routed,
-                       const float *v, const double *yts, int blocks, double *leaf_partial,
-                       int *err, hipStream_t s) {
+                       uint8_t *node_out, const ParentCuts &pc, int depth, bool missing,
+                       bool routed, const float *v, const double *yts, int blocks,
+                       double *leaf_partial, int *err, hipStream_t s) {
+    if (missing && leaf_lds_bytes(depth, missing) > kLeafMaxLds) return hipErrorInvalidValue;
+#define FBDT_LEAF(R, NPV, NI, NO, PC)                                                           \
+    leaf_go<R, NPV>(blocks, s, xb, ldb, n, d, NI, NO, PC, depth, missing, v, yts, leaf_partial, err)
     if (!routed) {
-        leaf_go<false, 0>(blocks, s, xb, ldb, n, d, node_in, nullptr, ParentCuts{}, depth, v, yts,
-                          leaf_partial, err);
+        FBDT_LEAF(false, 0, node_in, nullptr, ParentCuts{});
     } else {
         switch (1 << (depth - 1)) {   // parents of the leaves
-        case 1: leaf_go<true, 1>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
-        case 2: leaf_go<true, 2>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
-        case 4: leaf_go<true, 4>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
-        default: leaf_go<true, 0>(blocks, s, xb, ldb, n, d, node_in, node_out, pc, depth, v, yts, leaf_partial, err); break;
+        case 1: FBDT_LEAF(true, 1, node_in, node_out, pc); break;
+        case 2: FBDT_LEAF(true, 2, node_in, node_out, pc); break;
+        case 4: FBDT_LEAF(true, 4, node_in, node_out, pc); break;
+        default: FBDT_LEAF(true, 0, node_in, node_out, pc); break;
         }
     }
+#undef FBDT_LEAF
     return hipGetLastError();
 }
 
-hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, double eta,
-                                double *leaf_out, hipStream_t s) {
-    leaf_finalize_kernel<<<1, kLeafReduceThreads, 0, s>>>(leaf_partial, blocks, 1 << depth, eta,
-                                                          leaf_out);
+hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, bool missing,
+                                double eta, double *leaf_out, hipStream_t s) {
+    leaf_finalize_kernel<<<1, kLeafReduceThreads, 0, s>>>(
+        leaf_partial, blocks, leaf_slots(depth, missing), missing ? (1 << depth) - 1 : 0, eta,
+        leaf_out);
     return hipGetLastError();
 }
 
@@ -2254,13 +2374,15 @@ hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_
     return hipGetLastError();
 }
 
-ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, int cu_count,
-                      size_t max_lds, int threads) {
+ApplyShape plan_apply(int64_t n, int d_used, int n_trees, int depth, bool missing,
+                      int cu_count, size_t max_lds, int threads) {
     ApplyShape as{};
     as.d_used = d_used;
-    const int nin = (1 << depth) - 1, nleaf = 1 << depth;
+    as.missing = missing;
+    // boost weights per tree: the leaves, or with missing values every node
+    const int nin = (1 << depth) - 1, nleaf = missing ? 2 * nin + 1 : 1 << depth;
     const size_t lds_cap = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
-    as.shallow = depth <= kApplyShallowDepth;
+    as.shallow = depth <= kApplyShallowDepth && !missing;
     if (as.shallow) {
         // workgroups of 512 threads (two per CU for 40 features and 400
         // trees of depth 3, measured best); the tile of codes takes at most
@@ -2322,15 +2444,16 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
         return hipGetLastError();
     }
     apply_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(xb, ldb, n, as.d_used, cuts, leaves,
-                                                            n_trees, depth, as.trees_per_chunk,
-                                                            f0, prob, score);
+                                                            n_trees, depth, as.missing,
+                                                            as.trees_per_chunk, f0, prob, score);
     return hipGetLastError();
 }
 
-ApplyShape plan_importance(int64_t n, int d_used, int n_trees, int depth, int cu_count,
-                           size_t max_lds) {
+ApplyShape plan_importance(int64_t n, int d_used, int n_trees, int depth, bool missing,
+                           int cu_count, size_t max_lds) {
     ApplyShape as{};
     as.d_used = d_used;
+    as.missing = missing;
     const int nin = (1 << depth) - 1;
     const size_t lds_cap = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
     // one event per thread: its float64 accumulator column and code column
@@ -2359,16 +2482,18 @@ hipError_t launch_importance(const ApplyShape &as, const uint8_t *xb, int64_t ld
                              const uint16_t *cuts, const double *gains, int n_trees, int depth,
                              double *imp, int64_t ldi, int d_out, hipStream_t s) {
     importance_kernel<<<as.blocks, as.threads, as.lds_bytes, s>>>(
-        xb, ldb, n, as.d_used, cuts, gains, n_trees, depth, as.trees_per_chunk, imp, ldi, d_out);
+        xb, ldb, n, as.d_used, cuts, gains, n_trees, depth, as.missing, as.trees_per_chunk, imp,
+        ldi, d_out);
     return hipGetLastError();
 }
 
-ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, int cu_count,
-                            size_t max_lds, int threads) {
+ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, bool missing,
+                            int cu_count, size_t max_lds, int threads) {
     ApplyShape as{};
     as.d_used = d_used;
-    as.shallow = depth <= kApplyShallowDepth;
-    const int nin = (1 << depth) - 1, nleaf = 1 << depth;
+    as.missing = missing;
+    as.shallow = depth <= kApplyShallowDepth && !missing;
+    const int nin = (1 << depth) - 1, nleaf = missing ? 2 * nin + 1 : 1 << depth;
     const size_t lds_cap = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
     // one event per thread, 768 threads (measured best on 8M events x 40
     // features at depths 3 and 6): the tile of float32 values takes at most
@@ -2397,7 +2522,8 @@ hipError_t launch_apply_float(const ApplyShape &as, const float *x, int64_t ldx,
                               double f0, float *prob, double *score, hipStream_t s) {
 #define FBDT_APPLY_F(DV)                                                                        \
     apply_float_kernel<DV><<<as.blocks, as.threads, as.lds_bytes, s>>>(                         \
-        x, ldx, n, as.d_used, rec, leaves, n_trees, as.trees_per_chunk, f0, prob, score)
+        x, ldx, n, as.d_used, rec, leaves, n_trees, as.missing, as.trees_per_chunk, f0, prob,  \
+        score)
     switch (depth) {
     case 1: FBDT_APPLY_F(1); break;
     case 2: FBDT_APPLY_F(2); break;

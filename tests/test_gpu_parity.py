@@ -97,15 +97,46 @@ def test_bin_with_row_stride_and_transform():
     assert np.array_equal(c2.numpy(), ref)
 
 
-def test_bin_rejects_nan():
+def test_bin_rejects_nan_with_256_bins():
+    """NaN takes the reserved code 255 (section 4.2), so it is an error only
+    when all 256 codes are bins."""
     x = np.ones((2, 100), np.float32)
     x[1, 50] = np.nan
     with pytest.raises(fb.FbdtError) as ei:
-        fb.bin(dev(x), 16)
+        fb.bin(dev(x), 256)
     assert ei.value.status == "FBDT_E_NAN"
     with pytest.raises(fb.FbdtError) as ei:
-        fb.bin_transform(dev(x), np.zeros((2, 15), np.float32))
+        fb.bin_transform(dev(x), np.zeros((2, 255), np.float32))
     assert ei.value.status == "FBDT_E_NAN"
+
+
+def _with_missing(x, seed):
+    """A copy of x [d][n] with NaN values (section 4.2): features in turn
+    hold none, 3 %, 20 % and 60 % NaN; the last feature is NaN throughout."""
+    rng = np.random.default_rng(seed)
+    x = np.array(x, np.float32)
+    d, n = x.shape
+    for j in range(d):
+        frac = (0.0, 0.03, 0.2, 0.6)[j % 4]
+        x[j, rng.random(n) < frac] = np.nan
+    x[d - 1] = np.nan
+    return x
+
+
+@pytest.mark.parametrize("cfg,n,B", [(1, None, 16), (4, 50_001, 255), (2, 30_011, 2)])
+def test_bin_with_missing_values_matches_oracle(cfg, n, B):
+    x = _with_missing(make_training_set(cfg, n_events=n)["x"], cfg)
+    x[0, :5] = -np.nan                                  # a NaN with the sign bit set
+    say(f"bin with NaN: workload {cfg} d={x.shape[0]} n={x.shape[1]} B={B}")
+    bounds, codes = fb.bin(dev(x), B)
+    ob, oc = O.bin_features(x, B)
+    assert np.array_equal(bounds, ob)
+    assert np.array_equal(codes.numpy(), oc)
+    assert np.isinf(bounds[-1]).all() and (oc[-1] == O.MISSING).all()
+    fresh = _with_missing(make_apply_chunk(1, 20_001)["x"][: x.shape[0]], 99)
+    c2 = fb.bin_transform(dev(fresh), bounds)
+    ref = np.stack([O.encode(fresh[j], ob[j]) for j in range(x.shape[0])])
+    assert np.array_equal(c2.numpy(), ref)
 
 
 # ------------------------------------------------------------ single steps
@@ -299,7 +330,7 @@ def test_leaf_values_match_oracle():
 # --------------------------------------------------------------- full fit
 def _oracle_model(m):
     return O.Model(m["depth"], m["n_bins"], m["n_features"], m["f0"], m["cut_feature"],
-                   m["cut_bin"], m["gain"], m["leaf"])
+                   m["cut_bin"], m["gain"], m["leaf"], m.get("inner"))
 
 
 FIT_CASES = {
@@ -360,6 +391,96 @@ def test_fit_and_apply_match_oracle(case):
     op, oF = O.apply(om, xb)
     assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
     assert np.allclose(ascore.cpu().numpy(), oF, rtol=1e-9, atol=1e-12)
+
+
+MISSING_CASES = {
+    "config1-nan": dict(cfg=1),
+    "config2-nan-30k-weighted": dict(cfg=2, n_events=30_011, n_trees=8, n_bins=200,
+                                     weights=True),
+    "config4-nan-60k-depth6-B255": dict(cfg=4, n_events=60_013, n_bins=255, n_trees=3),
+    "nan-depth1-B2": dict(cfg=1, n_events=1237, depth=1, n_bins=2, n_trees=5),
+    "nan-negative-weights": dict(cfg=2, n_events=30_011, depth=4, n_trees=4, n_bins=64,
+                                 weights="signed"),
+}
+
+
+@pytest.mark.parametrize("case", list(MISSING_CASES))
+def test_fit_with_missing_values_matches_oracle(case):
+    """Section 4.2: NaN values take the missing code, stay out of their
+    feature's histograms, and stop an event at the node that cuts on them;
+    every node gets a boost weight.  The fitted model (cuts, gains, leaf and
+    inner-node weights), the fit's final scores, and the binned apply, float
+    apply and event importance of that model against the oracle."""
+    c = MISSING_CASES[case]
+    spec = CONFIGS[c["cfg"]]
+    ds = make_training_set(c["cfg"], n_events=c.get("n_events"))
+    x = _with_missing(ds["x"], 7)
+    d, n = x.shape
+    B = c.get("n_bins", spec.n_bins)
+    D = c.get("depth", spec.depth)
+    T = c.get("n_trees", spec.n_trees)
+    eta, alpha, seed = spec.shrinkage, spec.subsample, spec.fit_seed
+    v = ds["v"]
+    if c.get("weights") == "signed":
+        v = np.random.default_rng(9).uniform(-0.6, 2.5, n).astype(np.float32)
+    elif c.get("weights"):
+        v = np.random.default_rng(9).uniform(0.2, 3.0, n).astype(np.float32)
+    say(f"missing-value fit {case}: n={n} d={d} B={B} D={D} T={T}")
+    bounds, codes = fb.bin(dev(x), B)
+    ob, xb = O.bin_features(x, B)
+    assert np.array_equal(codes.numpy(), xb)
+    score = torch.empty(n, dtype=torch.float64, device="cuda")
+    model = fb.fit(codes, dev(ds["y"]), B, D, T, eta, alpha, seed, w=dev(v), score_out=score)
+    gm = model.export()
+    assert "inner" in gm and gm["inner"].shape == gm["gain"].shape
+    say(f"  oracle fit {case}")
+    log = O.TieLog()
+    om, F = O.fit(xb, ds["y"], v, D, T, eta, alpha, seed, B, reference=_oracle_model(gm),
+                  tie_log=log, final_score=True)
+    say(f"  near-ties adopted: {len(log.adopted)}  rejected: {len(log.rejected)}")
+    assert log.rejected == []
+    assert om.inner is not None
+    assert np.array_equal(gm["cut_feature"], om.cut_feature)
+    assert np.array_equal(gm["cut_bin"], om.cut_bin)
+    assert abs(gm["f0"] - om.f0) <= 1e-12
+    assert np.allclose(gm["gain"], om.gain, rtol=1e-9, atol=1e-12 * n)
+    assert np.allclose(gm["leaf"], om.leaf, rtol=1e-9, atol=1e-13)
+    assert np.allclose(gm["inner"], om.inner, rtol=1e-9, atol=1e-13)
+    Fg = score.cpu().numpy()
+    assert np.allclose(Fg, F, rtol=1e-9, atol=1e-12)
+    say(f"  apply {case}")
+    ascore = torch.empty(n, dtype=torch.float64, device="cuda")
+    p = fb.apply(model, codes, score=ascore).cpu().numpy()
+    assert np.array_equal(ascore.cpu().numpy(), Fg)
+    op, oF = O.apply(om, xb)
+    assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
+    assert np.allclose(ascore.cpu().numpy(), oF, rtol=1e-9, atol=1e-12)
+    say(f"  apply_float {case}")
+    model.set_boundaries(bounds)
+    fscore = torch.empty(n, dtype=torch.float64, device="cuda")
+    pf = fb.apply_float(model, dev(x), score=fscore).cpu().numpy()
+    assert np.array_equal(fscore.cpu().numpy(), Fg)
+    assert np.array_equal(pf, p)
+    tp, tF = O.apply_thresholds(om, x, ob)
+    assert np.array_equal(tF, oF)
+    say(f"  event importance {case}")
+    ei = fb.event_importance(model, codes).cpu().numpy()
+    oe = O.event_importance(om, xb)
+    assert np.allclose(ei, oe, rtol=1e-9, atol=1e-12 * n)
+    assert np.allclose(fb.feature_importance(model), O.feature_importance(om), rtol=1e-9,
+                       atol=1e-12 * n)
+
+
+def test_missing_values_need_depth_at_most_6_and_plain_data_stays_plain():
+    ds = make_training_set(1)
+    x = _with_missing(ds["x"], 3)
+    _, codes = fb.bin(dev(x), 16)
+    y = dev(ds["y"])
+    with pytest.raises(fb.FbdtError) as ei:
+        fb.fit(codes, y, 16, 7, 2)
+    assert ei.value.status == "FBDT_E_INVAL"
+    _, plain = fb.bin(dev(ds["x"]), 16)                 # B <= 255 but no NaN
+    assert "inner" not in fb.fit(plain, y, 16, 3, 2).export()
 
 
 def test_fit_graph_replays_match_eager_fit():
