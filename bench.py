@@ -96,11 +96,12 @@ def measure_fit_workload(cfg, fb, torch):
     fit()
     torch.cuda.synchronize()
     fit_s = time.perf_counter() - ts
-    fb.timing_enable(("histogram", "best_cuts"))
+    fb.timing_enable(("histogram", "best_cuts", "route"))
     fit()
     torch.cuda.synchronize()
     hl, hms, hb = fb.timing_read("histogram")
     cl, cms, _ = fb.timing_read("best_cuts")
+    rl, rms, _ = fb.timing_read("route")
     fb.timing_enable(())
     del codes, y
     torch.cuda.empty_cache()
@@ -114,6 +115,9 @@ def measure_fit_workload(cfg, fb, torch):
             "hist_achieved_gbs": achieved,
             "hist_frac": achieved / HBM_PEAK_GBS,
             "cut_scan_mean_launch_us": cms * 1e3 / max(cl, 1),
+            # layers with more than 4 parents: routing as a pass of its own
+            "route_launches": rl,
+            "route_mean_launch_us": rms * 1e3 / rl if rl else None,
             "setup_s": round(time.time() - t0, 1)}
 
 

@@ -262,13 +262,16 @@ int fbdt_leaf_values(const uint8_t *node, const int8_t *y, const float *v, const
 /* ---- Measurement and tuning -------------------------------------------- */
 
 enum fbdt_kernel_kind {
-    FBDT_K_HISTOGRAM = 0, /* per-layer histogram pass (with fused routing)   */
+    FBDT_K_HISTOGRAM = 0, /* per-layer histogram pass (routing fused up to 4  */
+                          /* parents)                                         */
     FBDT_K_BEST_CUTS = 1, /* CPH scan, gain and argmax of one layer          */
     FBDT_K_TREE_PREP = 2, /* score update and re-weighting of one tree       */
     FBDT_K_LEAF = 3,      /* last routing and terminal boost weights          */
     FBDT_K_APPLY = 4,     /* forest traversal                                */
     FBDT_K_ENCODE = 5,    /* float -> bin code                                */
-    FBDT_K_COUNT = 6
+    FBDT_K_ROUTE = 6,     /* routing of a layer as a pass of its own (layers  */
+                          /* with more than 4 parents; fbdt_route)            */
+    FBDT_K_COUNT = 7
 };
 
 /*
@@ -277,8 +280,9 @@ enum fbdt_kernel_kind {
  * 0 turns timing off, the default).  The call resets the tallies.
  * fbdt_timing_read waits for the recorded events and returns
  * the number of launches of a kind, their summed duration in milliseconds
- * and, for the histogram kind, the summed algorithmic bytes those launches
- * move (features, node ids, weights, routing and the histogram written).
+ * and the summed algorithmic bytes those launches move (histogram: codes,
+ * node ids, weights, routing and the histogram written; route: parent id,
+ * one code and the new id per event; 0 where not counted).
  */
 int fbdt_timing_enable(int32_t kinds);
 int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *bytes);

@@ -20,7 +20,7 @@ STATUS = {
     -6: "FBDT_E_DEVICE",
 }
 KERNEL_KINDS = {"histogram": 0, "best_cuts": 1, "tree_prep": 2, "leaf": 3, "apply": 4,
-                "encode": 5}
+                "encode": 5, "route": 6}
 
 EXPORTED = (
     "fbdt_bin", "fbdt_bin_transform", "fbdt_fit", "fbdt_apply", "fbdt_apply_float",

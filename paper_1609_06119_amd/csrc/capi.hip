@@ -494,6 +494,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
         for (int l = 0; l < D; ++l) {
             pl[l] = plan_histogram(n, d, n_bins, l, mode == 0, di.cu_count, di.max_lds,
                                    hist_overrides());
+            pl[l].prefix = true;   // the cut scan reads prefix-summed rows
             const size_t hnodes = pl[l].sibling ? (size_t)1 << (l - 1) : (size_t)1 << l;
             partial_elems =
                 std::max(partial_elems, (size_t)pl[l].chunks * hnodes * d * n_bins * 2);
@@ -612,14 +613,26 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 if (l >= 1)
                     pc = ParentCuts{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
                 const int gl = t * D + l;   // side histograms alternate by gl's parity
+                // layers with many parents are routed by a pass of their own
+                // (one code gather per event instead of one per feature group)
+                const bool own_route = l >= 1 && (1 << (l - 1)) > kRoutedMaxParents;
+                if (own_route) {
+                    Timed tm(FBDT_K_ROUTE, st, 3.0 * (double)n);
+                    HIP_TRY(launch_route_layer(xb, ldb, n, d, fb.node[(l - 1) & 1],
+                                               fb.node[l & 1], pc, l, n_bins <= kMissingCode,
+                                               fb.err, di.cu_count, st));
+                    tm.done();
+                }
                 {
                     Timed tm(FBDT_K_HISTOGRAM, st,
-                             hist_algorithmic_bytes(n, d, n_bins, l, true, plans[l].sibling));
-                    HIP_TRY(launch_histogram(plans[l], xb, ldb, n, d, n_bins,
-                                             l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
-                                             l >= 1 ? fb.node[l & 1] : nullptr, fb.w, vsign, pc, l,
-                                             true, scale, fb.partial, fb.small[gl & 1], fb.err,
-                                             st));
+                             hist_algorithmic_bytes(n, d, n_bins, l, !own_route,
+                                                    plans[l].sibling));
+                    HIP_TRY(launch_histogram(
+                        plans[l], xb, ldb, n, d, n_bins,
+                        own_route ? fb.node[l & 1] : l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
+                        !own_route && l >= 1 ? fb.node[l & 1] : nullptr, fb.w, vsign,
+                        own_route ? ParentCuts{} : pc, l, !own_route, scale, fb.partial,
+                        fb.small[gl & 1], fb.err, st));
                     tm.done();
                 }
                 {
@@ -657,7 +670,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
         return FBDT_OK;
     };
     const int timed_kinds = (1 << FBDT_K_TREE_PREP) | (1 << FBDT_K_HISTOGRAM) |
-                            (1 << FBDT_K_BEST_CUTS) | (1 << FBDT_K_LEAF);
+                            (1 << FBDT_K_BEST_CUTS) | (1 << FBDT_K_LEAF) | (1 << FBDT_K_ROUTE);
     if (opt_fit_graphs.load() && !(g_timing.load() & timed_kinds)) {
         const GraphKey key{xb, y, w, n, ldb, d, n_bins, D, T, scale, lblocks, eta, alpha, seed,
                            opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load(),
@@ -1176,7 +1189,11 @@ int fbdt_route(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, uint8_t *no
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     HIP_TRY(launch_fill_u32(err, 0u, 1, s));
-    HIP_TRY(launch_route(xb, ldb, n, d, node, cut_feature, cut_bin, layer, err, s));
+    {
+        Timed tm(FBDT_K_ROUTE, s, 3.0 * (double)n);
+        HIP_TRY(launch_route(xb, ldb, n, d, node, cut_feature, cut_bin, layer, err, s));
+        tm.done();
+    }
     int h_err = 0;
     if ((rc = read_err(err, s, &h_err))) return rc;
     if (h_err & kErrRoute)

@@ -45,6 +45,9 @@ struct HistShape {
     size_t lds_bytes;         // dynamic LDS per workgroup
     bool sibling;             // routed pass below the root histograms the left child of
                               // each parent only (right = parent - left)
+    bool prefix;              // partial rows written as inclusive prefix sums over bins
+                              // (the fit's passes, read by the cut scan); the planner
+                              // leaves it false (plain rows, for merge_partials)
 };
 
 // Launch-shape overrides of the histogram pass (0 = the planner's choice).
@@ -165,14 +168,17 @@ int histogram_scale(double total_weight_bound);
 // parent (the right child is the parent minus the left child, formed by
 // best_cuts): partial: [chunks][2^(layer-1)][d][B][2], indexed by parent.
 // routed = false: node_in holds the ids of the layer itself; partial:
-// [chunks][2^layer][d][B][2].
+// [chunks][2^layer][d][B][2], or with hs.sibling (layer >= 1, ids written by
+// launch_route_layer) [chunks][2^(layer-1)][d][B][2] of the left children
+// only, indexed by parent.  Ids below the layer (events stopped earlier at
+// a missing value) count nowhere.
 // small: [2^layer][d][B][2] float64 sums of the weights below the grid, for
 // every node of the layer (accumulated into, not cleared).
 // Every step reads kHistE = 8 whole events: w and node_in must hold
 // round_up(n, 8) elements, with weight 0 beyond n (those events count
 // nowhere), code rows ldb >= round_up(n, 8) bytes, and node_out room for
 // round_up(n, 8) ids (the padded events are routed too).
-// vsign (routed passes only, else null): [round_up(n, 8)] bytes, 1 where the
+// vsign (or null): [round_up(n, 8)] bytes, 1 where the
 // event's weight is negative; w then holds |w| with the class in the sign
 // bit and the pass adds -|w| for those events (two's complement fixed point).
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
@@ -246,6 +252,21 @@ hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int dept
 hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *node,
                         const uint8_t *cut_f, const uint8_t *cut_c, int layer, int *err,
                         hipStream_t s);
+
+// The histogram pass routes the events itself while the layer has at most
+// this many parents (it loads the parents' cut-feature rows with the codes);
+// deeper layers are routed by launch_route_layer first.
+constexpr int kRoutedMaxParents = 4;
+
+// Routing of layer `layer` (>= 1) on its own: the parents' cuts from the
+// candidates in pc (recorded in the model through pc.rec_*), then
+// node_out[i] = 2 node_in[i] + [code >= cut] for every event up to
+// round_up(n, 8); with miss (n_bins <= kMissingCode) an event whose code of
+// the cut feature is kMissingCode, or whose id lies below the parents'
+// layer, keeps its id.
+hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
+                              const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc,
+                              int layer, bool miss, int *err, int cu_count, hipStream_t s);
 
 // Forest traversal.  cuts: [T][2^D-1] packed (feature | bin << 8), for the
 // general kernel; nodes: [T][16] for depth <= kApplyShallowDepth, for heap

@@ -561,7 +561,7 @@ struct HistArgs {
 };
 
 // codes of the parents' cut features (the cut table must be in LDS)
-template <bool ROUTED, int NP, int FPG, bool SIGNED>
+template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
 __device__ __forceinline__ void hist_load_rows(HistStep<NP, FPG> &st, const HistArgs &a,
                                                const uint8_t *s_cf, int64_t i0) {
     if (ROUTED && NP > 0 && a.layer >= 1) {
@@ -576,7 +576,7 @@ __device__ __forceinline__ void hist_load_rows(HistStep<NP, FPG> &st, const Hist
 // The per-event arrays (weights, node ids) are padded to a multiple of
 // kHistE with zero weights, and code rows to ldb >= that padding, so every
 // step loads kHistE whole events; padded events weigh 0 and count nowhere.
-template <bool ROUTED, int NP, int FPG, bool SIGNED>
+template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
 __device__ __forceinline__ void hist_load(HistStep<NP, FPG> &st, const HistArgs &a,
                                           const uint8_t *s_cf, int64_t i0, bool with_rows) {
     const uint4 x = reinterpret_cast<const uint4 *>(a.w + i0)[0];
@@ -589,10 +589,10 @@ __device__ __forceinline__ void hist_load(HistStep<NP, FPG> &st, const HistArgs 
         st.codes[ff] = *reinterpret_cast<const uint2 *>(
             a.xb + (int64_t)min(a.j0 + ff, a.d - 1) * a.ldb + i0);
     if (SIGNED) st.vs = *reinterpret_cast<const uint2 *>(a.vsign + i0);
-    if (with_rows) hist_load_rows<ROUTED, NP, FPG, SIGNED>(st, a, s_cf, i0);
+    if (with_rows) hist_load_rows<ROUTED, NP, FPG, SIGNED, MISS>(st, a, s_cf, i0);
 }
 
-template <bool ROUTED, int NP, int FPG, bool SIGNED>
+template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
 __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const HistArgs &a,
                                          uint64_t *lds, bool writer, const uint8_t *s_cf,
                                          const uint8_t *s_cc, const uint32_t (&cut)[4],
@@ -610,12 +610,15 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
     bool counted[kHistE];
     uint32_t bad = 0u;
     if (!ROUTED) {
+        // ids of this layer; with sib the left child 2k is histogrammed in
+        // slot k and the right child is parent - left; ids below the layer
+        // (stopped earlier) fall outside every slot
 #pragma unroll
         for (int e = 0; e < kHistE; ++e) {
             const uint32_t node = byte8(st.node, e);
             nl[e] = node - (uint32_t)a.nodes;
-            slot[e] = nl[e] - (uint32_t)a.k0;
-            counted[e] = true;
+            slot[e] = (a.sib ? nl[e] >> 1 : nl[e]) - (uint32_t)a.k0;
+            counted[e] = !a.sib | ((nl[e] & 1u) == 0u);
         }
     } else if (a.layer == 0) {
 #pragma unroll
@@ -641,7 +644,7 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
                 if (k >= (uint32_t)a.half) {
                     // below the layer: stopped earlier at a missing value;
                     // above it: unreachable for ids written by this library
-                    const bool earlier = a.miss & (par < (uint32_t)a.half);
+                    const bool earlier = MISS && par < (uint32_t)a.half;
                     stop = earlier;
                     bad |= earlier ? 0u : 1u;
                     k = 0u;
@@ -662,14 +665,20 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
                     c = s_cc[k];
                 }
             }
-            stop |= a.miss & (code == (uint32_t)kMissingCode);
+            if (MISS) stop |= code == (uint32_t)kMissingCode;
             const uint32_t right = code >= c ? 1u : 0u;
             const uint32_t ne = stop ? par : 2u * par + right;
             o[e >> 2] |= ne << (8 * (e & 3));
             nl[e] = ne - (uint32_t)a.nodes;
-            // stopped: counted nowhere
-            slot[e] = stop ? 0xffffffffu : (a.sib ? k : nl[e]) - (uint32_t)a.k0;
-            counted[e] = !stop & (!a.sib | (right == 0u));
+            // stopped: counted nowhere; routed passes take sibling
+            // subtraction exactly when no event can stop (!MISS)
+            if (MISS) {
+                slot[e] = stop ? 0xffffffffu : nl[e] - (uint32_t)a.k0;
+                counted[e] = !stop;
+            } else {
+                slot[e] = k - (uint32_t)a.k0;
+                counted[e] = right == 0u;
+            }
         }
         // padded events get ids too, so that the next layer reads valid parents
         if (writer) *reinterpret_cast<uint2 *>(a.node_out + i0) = make_uint2(o[0], o[1]);
@@ -723,15 +732,15 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
     }
 }
 
-template <bool ROUTED, int NP, int FPG, bool SIGNED>
+template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
 __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const float *__restrict__ w, const uint8_t *__restrict__ vsign,
     const double *__restrict__ cand_gain,
     const int *__restrict__ cand_cut, int cslices, uint8_t *__restrict__ rec_f,
-    uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, bool sib, int G, int npg,
-    int NG,
+    uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, bool sib, bool prefix,
+    int G, int npg, int NG,
     int chunks, int64_t chunk_events, int64_t xcd_events, int scale, int copies,
     int copy_stride, uint64_t *__restrict__ partial, double *__restrict__ small,
     int *__restrict__ err) {
@@ -760,7 +769,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     a.layer = layer;
     a.nodes = 1 << layer;
     a.half = a.nodes >> 1;
-    a.sib = ROUTED && layer >= 1 && sib;
+    a.sib = layer >= 1 && sib;
     const int hnodes = a.sib ? a.half : a.nodes;   // histogrammed nodes
     a.j0 = g * FPG;
     a.nf = min(FPG, d - a.j0);
@@ -805,7 +814,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     if (pwave) cand_load(cs, wave, lane, cr);
     HistStep<NP, FPG> A, B;
     int64_t ia = start + (int64_t)kHistE * threadIdx.x;
-    if (ia < end) hist_load<ROUTED, NP, FPG, SIGNED>(A, a, s_cf, ia, false);
+    if (ia < end) hist_load<ROUTED, NP, FPG, SIGNED, MISS>(A, a, s_cf, ia, false);
 
     {
         uint4 *l4 = reinterpret_cast<uint4 *>(lds);
@@ -845,17 +854,17 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     // adds of step s.  They are issued unconditionally (the last step
     // reloads its own events) so that the waits for step s never cover them.
     if (ia < end) {
-        hist_load_rows<ROUTED, NP, FPG, SIGNED>(A, a, s_cf, ia);
+        hist_load_rows<ROUTED, NP, FPG, SIGNED, MISS>(A, a, s_cf, ia);
         for (;;) {
             const int64_t ib = ia + stride;
             const bool more_b = ib < end;
-            hist_load<ROUTED, NP, FPG, SIGNED>(B, a, s_cf, more_b ? ib : ia, true);
-            hist_add<ROUTED, NP, FPG, SIGNED>(A, a, lds_lane, writer, s_cf, s_cc, cut, ia, eflag);
+            hist_load<ROUTED, NP, FPG, SIGNED, MISS>(B, a, s_cf, more_b ? ib : ia, true);
+            hist_add<ROUTED, NP, FPG, SIGNED, MISS>(A, a, lds_lane, writer, s_cf, s_cc, cut, ia, eflag);
             if (!more_b) break;
             ia = ib + stride;
             const bool more_a = ia < end;
-            hist_load<ROUTED, NP, FPG, SIGNED>(A, a, s_cf, more_a ? ia : ib, true);
-            hist_add<ROUTED, NP, FPG, SIGNED>(B, a, lds_lane, writer, s_cf, s_cc, cut, ib, eflag);
+            hist_load<ROUTED, NP, FPG, SIGNED, MISS>(A, a, s_cf, more_a ? ia : ib, true);
+            hist_add<ROUTED, NP, FPG, SIGNED, MISS>(B, a, lds_lane, writer, s_cf, s_cc, cut, ib, eflag);
             if (!more_a) break;
         }
     }
@@ -871,8 +880,8 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     }
 
     // partial[p][node][feature][bin][class]: one (node, feature) row per
-    // wavefront step; bins >= n_bins must be empty.  Routed (fit) passes
-    // write every row as inclusive prefix sums over bins, P(b) = sum of the
+    // wavefront step; bins >= n_bins must be empty.  With prefix (the fit's
+    // passes) every row is written as inclusive prefix sums over bins, P(b) = sum of the
     // bins <= b per class: summed over chunks these are the cumulative
     // histograms, which best_cuts then reads slice by slice.  Lane l holds
     // bins 4l..4l+3 (both classes), prefix in the lane, then an exclusive
@@ -889,7 +898,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
             const uint4 v = src[t];
             if (v.x | v.y | v.z | v.w) eflag |= kErrBin;
         }
-        if (ROUTED) {   // the row is scanned in place (this wavefront's row only)
+        if (prefix) {   // the row is scanned in place (this wavefront's row only)
             ulonglong2 *s2 = reinterpret_cast<ulonglong2 *>(lds + (k * FPG + f) * kRow) + 4 * lane;
             ulonglong2 v[4] = {s2[0], s2[1], s2[2], s2[3]};
 #pragma unroll
@@ -1509,6 +1518,85 @@ __global__ __launch_bounds__(kLeafReduceThreads) void leaf_finalize_kernel(
     for (int t = threadIdx.x; t < nslots; t += blockDim.x) leaf_out[t] = s_leaf[t];
 }
 
+// Routing of one layer as a pass of its own, for layers with more parents
+// than the histogram pass routes itself.  There each event would gather one
+// code byte from the row of its parent's cut feature (a cache line per lane
+// of the load, as the parents of a wavefront's events differ), once in every
+// feature group's workgroup; here the gather happens once per event.  Every
+// workgroup forms the parents' cuts from their candidates (workgroup 0
+// records them in the model), then moves each event of its XCD's range to
+// its node of this layer, node <- 2 node + [code >= cut] (section 1.1).
+// With miss, an event whose code of the cut feature is the missing code, or
+// which stopped at an earlier layer, keeps its node (section 4.2).  Whole
+// steps of kHistE events: padded events get ids too.
+__global__ __launch_bounds__(256) void route_layer_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
+    const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
+    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
+    uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
+    int layer, bool miss, int *__restrict__ err, int64_t xcd_events) {
+    __shared__ uint8_t s_cf[64], s_cc[64];
+    const uint32_t half = 1u << (layer - 1);
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nwaves = blockDim.x / kWave;
+    int eflag = 0;
+    const CandSet cs{cand_gain, cand_cut, d, cslices};
+    for (int k = wave; k < (int)half; k += nwaves) {
+        int bf, bc;
+        double bg;
+        bool ok;
+        node_best(cs, k, lane, &bf, &bc, &bg, &ok);
+        if (lane == 0) {
+            s_cf[k] = (uint8_t)bf;
+            s_cc[k] = (uint8_t)bc;
+            if (!ok) eflag |= kErrRoute;
+            if (blockIdx.x == 0 && rec_f) {
+                rec_f[k] = (uint8_t)bf;
+                rec_c[k] = (uint8_t)bc;
+                rec_g[k] = bg;
+            }
+        }
+    }
+    __syncthreads();
+    // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
+    const int64_t xlo = (int64_t)(blockIdx.x % kXcds) * xcd_events;
+    const int64_t xend = min(n, xlo + xcd_events);
+    const int64_t stride = (int64_t)(gridDim.x / kXcds) * blockDim.x * kHistE;
+    for (int64_t i0 = xlo + ((int64_t)(blockIdx.x / kXcds) * blockDim.x + threadIdx.x) * kHistE;
+         i0 < xend; i0 += stride) {
+        const uint2 pin = *reinterpret_cast<const uint2 *>(node_in + i0);
+        uint32_t par[kHistE], k[kHistE], code[kHistE];
+        // the step's gathers first, all in flight together
+#pragma unroll
+        for (int e = 0; e < kHistE; ++e) {
+            par[e] = byte8(pin, e);
+            k[e] = par[e] - half;
+            const uint32_t kk = k[e] < half ? k[e] : 0u;
+            code[e] = xb[(int64_t)min((int)s_cf[kk], d - 1) * ldb + i0 + e];
+        }
+        uint32_t o[2] = {0u, 0u};
+#pragma unroll
+        for (int e = 0; e < kHistE; ++e) {
+            uint32_t p = par[e], kk = k[e];
+            bool stop = false;
+            if (kk >= half) {
+                // below the layer: stopped earlier at a missing value; above
+                // it: unreachable for ids written by this library
+                const bool earlier = miss & (p < half);
+                stop = earlier;
+                if (!earlier) eflag |= kErrRoute;
+                kk = 0u;
+                p = earlier ? p : half;
+            }
+            stop |= miss & (code[e] == (uint32_t)kMissingCode);
+            const uint32_t ne = stop ? p : 2u * p + (code[e] >= s_cc[kk] ? 1u : 0u);
+            o[e >> 2] |= ne << (8 * (e & 3));
+        }
+        *reinterpret_cast<uint2 *>(node_out + i0) = make_uint2(o[0], o[1]);
+    }
+    if (eflag) atomicOr(err, eflag);
+}
+
 // node <- 2 node + [xb[f][i] >= c] with (f, c) the cut of the node.
 __global__ __launch_bounds__(256) void route_kernel(const uint8_t *__restrict__ xb, int64_t ldb,
                                                     int64_t n, int d, uint8_t *__restrict__ node,
@@ -1978,15 +2066,24 @@ hipError_t allow_lds(K kernel, size_t max_lds) {
 // ===========================================================================
 template <int FPG>
 hipError_t allow_hist_lds(size_t max_lds) {
-    const hipError_t e[] = {allow_lds(hist_kernel<false, 0, FPG, false>, max_lds),
-                            allow_lds(hist_kernel<true, 0, FPG, false>, max_lds),
-                            allow_lds(hist_kernel<true, 1, FPG, false>, max_lds),
-                            allow_lds(hist_kernel<true, 2, FPG, false>, max_lds),
-                            allow_lds(hist_kernel<true, 4, FPG, false>, max_lds),
-                            allow_lds(hist_kernel<true, 0, FPG, true>, max_lds),
-                            allow_lds(hist_kernel<true, 1, FPG, true>, max_lds),
-                            allow_lds(hist_kernel<true, 2, FPG, true>, max_lds),
-                            allow_lds(hist_kernel<true, 4, FPG, true>, max_lds)};
+    const hipError_t e[] = {allow_lds(hist_kernel<false, 0, FPG, false, false>, max_lds),
+                            allow_lds(hist_kernel<false, 0, FPG, true, false>, max_lds),
+                            allow_lds(hist_kernel<true, 0, FPG, false, false>, max_lds),
+                            allow_lds(hist_kernel<true, 1, FPG, false, false>, max_lds),
+                            allow_lds(hist_kernel<true, 2, FPG, false, false>, max_lds),
+                            allow_lds(hist_kernel<true, 4, FPG, false, false>, max_lds),
+                            allow_lds(hist_kernel<true, 0, FPG, true, false>, max_lds),
+                            allow_lds(hist_kernel<true, 1, FPG, true, false>, max_lds),
+                            allow_lds(hist_kernel<true, 2, FPG, true, false>, max_lds),
+                            allow_lds(hist_kernel<true, 4, FPG, true, false>, max_lds),
+                            allow_lds(hist_kernel<true, 0, FPG, false, true>, max_lds),
+                            allow_lds(hist_kernel<true, 1, FPG, false, true>, max_lds),
+                            allow_lds(hist_kernel<true, 2, FPG, false, true>, max_lds),
+                            allow_lds(hist_kernel<true, 4, FPG, false, true>, max_lds),
+                            allow_lds(hist_kernel<true, 0, FPG, true, true>, max_lds),
+                            allow_lds(hist_kernel<true, 1, FPG, true, true>, max_lds),
+                            allow_lds(hist_kernel<true, 2, FPG, true, true>, max_lds),
+                            allow_lds(hist_kernel<true, 4, FPG, true, true>, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -2167,20 +2264,21 @@ int histogram_scale(double total_weight_bound) {
     return sc;
 }
 
-template <bool ROUTED, int NP, int FPG, bool SIGNED>
+template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
 hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
                           const uint8_t *vsign, const ParentCuts &pc, int layer, int scale,
                           uint64_t *partial, double *small, int *err, hipStream_t s) {
-    hist_kernel<ROUTED, NP, FPG, SIGNED><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+    hist_kernel<ROUTED, NP, FPG, SIGNED, MISS><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices,
-        pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.sibling, hs.feature_groups, hs.nodes_per_group,
+        pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.sibling, hs.prefix, hs.feature_groups,
+        hs.nodes_per_group,
         hs.node_groups, hs.chunks, hs.chunk_events, hs.xcd_events, scale, hs.copies,
         hs.copy_stride, partial, small, err);
     return hipGetLastError();
 }
 
-template <int FPG, bool SIGNED>
+template <int FPG, bool SIGNED, bool MISS>
 hipError_t launch_hist_routed(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                               int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                               const float *w, const uint8_t *vsign, const ParentCuts &pc,
@@ -2188,8 +2286,9 @@ hipError_t launch_hist_routed(const HistShape &hs, const uint8_t *xb, int64_t ld
                               hipStream_t s) {
     const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
 #define FBDT_HIST(NPV)                                                                          \
-    launch_hist_np<true, NPV, FPG, SIGNED>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,     \
-                                           vsign, pc, layer, scale, partial, small, err, s)
+    launch_hist_np<true, NPV, FPG, SIGNED, MISS>(hs, xb, ldb, n, d, n_bins, node_in, node_out, \
+                                                 w, vsign, pc, layer, scale, partial, small,   \
+                                                 err, s)
     switch (parents) {
     case 0:
     case 1: return FBDT_HIST(1);
@@ -2208,16 +2307,25 @@ hipError_t launch_hist_fpg(const HistShape &hs, const uint8_t *xb, int64_t ldb, 
                            hipStream_t s) {
     const ParentCuts none{};
     if (!routed) {
-        if (vsign) return hipErrorInvalidValue;   // signed weights: routed (fit) passes only
-        return launch_hist_np<false, 0, FPG, false>(hs, xb, ldb, n, d, n_bins, node_in, nullptr,
-                                                    w, nullptr, none, layer, scale, partial,
-                                                    small, err, s);
+        if (vsign)
+            return launch_hist_np<false, 0, FPG, true, false>(hs, xb, ldb, n, d, n_bins, node_in,
+                                                              nullptr, w, vsign, none, layer,
+                                                              scale, partial, small, err, s);
+        return launch_hist_np<false, 0, FPG, false, false>(hs, xb, ldb, n, d, n_bins, node_in,
+                                                           nullptr, w, nullptr, none, layer,
+                                                           scale, partial, small, err, s);
     }
-    if (vsign)
-        return launch_hist_routed<FPG, true>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,
-                                             vsign, pc, layer, scale, partial, small, err, s);
-    return launch_hist_routed<FPG, false>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,
-                                          nullptr, pc, layer, scale, partial, small, err, s);
+    // routed passes below the root subtract siblings exactly when no event
+    // can stop at a missing value; a fit with missing values histograms both
+    // children and takes the stop logic (MISS)
+    const bool miss = layer >= 1 && !hs.sibling;
+#define FBDT_HIST_R(SG, MS)                                                                     \
+    launch_hist_routed<FPG, SG, MS>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,            \
+                                    SG ? vsign : nullptr, pc, layer, scale, partial, small,    \
+                                    err, s)
+    if (vsign) return miss ? FBDT_HIST_R(true, true) : FBDT_HIST_R(true, false);
+    return miss ? FBDT_HIST_R(false, true) : FBDT_HIST_R(false, false);
+#undef FBDT_HIST_R
 }
 
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
@@ -2363,6 +2471,23 @@ hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int dept
     leaf_finalize_kernel<<<1, kLeafReduceThreads, 0, s>>>(
         leaf_partial, blocks, leaf_slots(depth, missing), missing ? (1 << depth) - 1 : 0, eta,
         leaf_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
+                              const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc,
+                              int layer, bool miss, int *err, int cu_count, hipStream_t s) {
+    if (layer < 1 || (1 << (layer - 1)) > 64) return hipErrorInvalidValue;
+    // up to 4 workgroups of 256 threads per CU: the gathers are
+    // latency-bound, so many wavefronts keep loads in flight
+    const int64_t R = xcd_range(n);
+    int64_t per = (R + (int64_t)kHistE * 256 - 1) / ((int64_t)kHistE * 256);
+    const int64_t cap = 4 * (cu_count / kXcds > 0 ? cu_count / kXcds : 1);
+    if (per > cap) per = cap;
+    if (per < 1) per = 1;
+    route_layer_kernel<<<(unsigned)(kXcds * per), 256, 0, s>>>(
+        xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut, pc.slices, pc.rec_f,
+        pc.rec_c, pc.rec_g, layer, miss, err, R);
     return hipGetLastError();
 }
 
