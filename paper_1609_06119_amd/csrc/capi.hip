@@ -657,10 +657,23 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
             {
                 const int plo = (1 << (D - 1)) - 1;
                 const ParentCuts pc{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
+                // the leaves of deep trees are routed by a pass of their own,
+                // like the deep layers
+                const bool own_route = (1 << (D - 1)) > kRoutedMaxParents;
+                if (own_route) {
+                    Timed tm(FBDT_K_ROUTE, st, 3.0 * (double)n);
+                    HIP_TRY(launch_route_layer(xb, ldb, n, d, fb.node[(D - 1) & 1],
+                                               fb.node[D & 1], pc, D, n_bins <= kMissingCode,
+                                               fb.err, di.cu_count, st));
+                    tm.done();
+                }
                 Timed tm(FBDT_K_LEAF, st);
-                HIP_TRY(launch_leaf(xb, ldb, n, d, D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
-                                    fb.node[D & 1], pc, D, missing, true, fb.v, fb.yts, lblocks,
-                                    fb.leaf_partial, fb.err, st));
+                HIP_TRY(launch_leaf(xb, ldb, n, d,
+                                    own_route ? fb.node[D & 1]
+                                              : D >= 2 ? fb.node[(D - 1) & 1] : nullptr,
+                                    own_route ? nullptr : fb.node[D & 1],
+                                    own_route ? ParentCuts{} : pc, D, missing, !own_route, fb.v,
+                                    fb.yts, lblocks, fb.leaf_partial, fb.err, st));
                 if (!fused || t == T - 1)
                     HIP_TRY(launch_leaf_finalize(fb.leaf_partial, lblocks, D, missing, eta,
                                                  fb.leaf + (size_t)t * nslots, st));

@@ -1279,10 +1279,13 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
 // parents' cut features are loaded with the step's other data, so routing
 // costs no dependent load.
 //
-// Every thread owns the 2 * 2^depth accumulators of its column of the
-// LDS array acc[value][thread] and adds its events in order (non-returning
-// LDS float64 adds on addresses no other thread touches: exact order, no
-// bank conflicts); the workgroup then adds its columns in a fixed order.
+// Every column of the LDS array acc[value][column] holds the 2 * slots
+// accumulators of `share` consecutive threads, which add their events in
+// turn (non-returning LDS float64 adds: each address has one writer at a
+// time, in a fixed order, and no bank conflicts); the workgroup then adds
+// its columns in a fixed order.  The columns take up to ~130 KiB, so deep
+// trees have few of them: up to 8 threads share one there, which keeps 512
+// threads (8 wavefronts) per CU instead of 128 or 64.
 // kLeafE consecutive events per thread and step on padded arrays (weights,
 // yts, node ids: zero pseudo-response beyond n), the next step's loads
 // issued before the current step's arithmetic.
@@ -1294,9 +1297,18 @@ __host__ __device__ constexpr int leaf_slots(int depth, bool missing) {
     return missing ? (2 << depth) - 1 : 1 << depth;
 }
 
-__host__ __device__ constexpr int leaf_threads(int depth, bool missing) {
-    // acc takes threads * 2 slots doubles: at most ~133 KiB
+__host__ __device__ constexpr int leaf_columns(int depth, bool missing) {
+    // acc takes columns * 2 slots doubles: at most ~133 KiB
     return 2 * leaf_slots(depth, missing) <= 64 ? 256 : 2 * leaf_slots(depth, missing) <= 128 ? 128 : 64;
+}
+
+// threads per accumulator column
+__host__ __device__ constexpr int leaf_share(int depth, bool missing) {
+    return leaf_columns(depth, missing) >= 256 ? 1 : 512 / leaf_columns(depth, missing);
+}
+
+__host__ __device__ constexpr int leaf_threads(int depth, bool missing) {
+    return leaf_columns(depth, missing) * leaf_share(depth, missing);
 }
 
 template <int NP>
@@ -1346,7 +1358,7 @@ __device__ __forceinline__ void leaf_load(LeafStep<NP> &st, const uint8_t *__res
 }
 
 template <bool ROUTED, int NP>
-__global__ __launch_bounds__(256) void leaf_kernel(
+__global__ __launch_bounds__(512) void leaf_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
@@ -1357,9 +1369,12 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     // Sums per terminal node: the leaves, and with missing values (section
     // 4.2) every node, since an event stops at the node that cuts on its
     // missing value; slot = heap id - first_id.
-    extern __shared__ double acc[];   // [2 nslots][T + 1], then the segment sums
+    extern __shared__ double acc[];   // [2 nslots][ncol + 1], then the segment sums
     __shared__ uint8_t s_cf[64], s_cc[64];
     const int T = blockDim.x;
+    const int share = leaf_share(depth, missing);   // threads per column
+    const int ncol = T / share;
+    const int sub = threadIdx.x & (share - 1);
     const int nleaf = 1 << depth;
     const uint32_t first_id = missing ? 1u : (uint32_t)nleaf;
     const int nslots = missing ? 2 * nleaf - 1 : nleaf;
@@ -1381,7 +1396,7 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     if (pwave) cand_load(cs, wave, lane, cr);
     LeafStep<NP> A, B;
     if (ia < xend) leaf_load<ROUTED, NP>(A, xb, ldb, d, node_in, v, yts, s_cf, ia, false);
-    const int TP = T + 1;   // row stride: rows start two LDS banks apart
+    const int TP = ncol + 1;   // row stride: rows start two LDS banks apart
     for (int t = threadIdx.x; t < nv * TP; t += T) acc[t] = 0.0;
     if (ROUTED) {
         for (int k = wave; k < half; k += nwaves) {
@@ -1410,10 +1425,11 @@ __global__ __launch_bounds__(256) void leaf_kernel(
 #pragma unroll
         for (int k = 0; k < (NP > 0 ? NP : 1); ++k) cut[k] = s_cc[k];
     }
-    double *mine = acc + threadIdx.x;   // this thread's column, value stride TP
+    double *mine = acc + threadIdx.x / share;   // this thread's column, value stride TP
 
     auto add = [&](const LeafStep<NP> &st, int64_t i0) {
         uint32_t o[2] = {0u, 0u};
+        uint32_t lid[kLeafE];
 #pragma unroll
         for (int e = 0; e < kLeafE; ++e) {
             uint32_t leaf;
@@ -1451,21 +1467,28 @@ __global__ __launch_bounds__(256) void leaf_kernel(
             } else {
                 leaf = byte8(st.node, e);
             }
-            const uint32_t li = leaf - first_id;
-            const double yt = st.yt[e];
-            if (yt != 0.0) {   // sampled
-                if (li >= (uint32_t)nslots) {   // unreachable for ids written by this library
-                    eflag |= kErrRoute;
-                    continue;
-                }
-                const double vi = (double)st.v[e];
-                const double a = fabs(yt);
-                unsafeAtomicAdd(mine + (size_t)(2 * li) * TP, vi * yt);
-                unsafeAtomicAdd(mine + (size_t)(2 * li + 1) * TP, vi * a * (2.0 - a));
-            }
+            lid[e] = leaf - first_id;
+            // unreachable for ids written by this library
+            if (st.yt[e] != 0.0 && lid[e] >= (uint32_t)nslots) eflag |= kErrRoute;
         }
         // padded events get leaf ids too (the arrays hold whole steps)
         if (ROUTED) *reinterpret_cast<uint2 *>(node_out + i0) = make_uint2(o[0], o[1]);
+        // the threads of a column add their sampled events in turn
+        for (int r = 0; r < share; ++r) {
+            if (sub == r) {
+#pragma unroll
+                for (int e = 0; e < kLeafE; ++e) {
+                    const double yt = st.yt[e];
+                    const uint32_t li = lid[e];
+                    if (yt != 0.0 && li < (uint32_t)nslots) {   // sampled
+                        const double vi = (double)st.v[e];
+                        const double a = fabs(yt);
+                        unsafeAtomicAdd(mine + (size_t)(2 * li) * TP, vi * yt);
+                        unsafeAtomicAdd(mine + (size_t)(2 * li + 1) * TP, vi * a * (2.0 - a));
+                    }
+                }
+            }
+        }
     };
     if (ia < xend) {
         leaf_load_rows<ROUTED, NP>(A, xb, ldb, d, s_cf, ia);
@@ -1487,8 +1510,8 @@ __global__ __launch_bounds__(256) void leaf_kernel(
     // then the G segment sums; G is a power of two (nv need not be one, so
     // T / nv may not divide T) with G nv <= T
     int G = 1;
-    while (2 * G * nv <= T) G *= 2;
-    const int seg = T / G;
+    while (2 * G * nv <= ncol) G *= 2;
+    const int seg = ncol / G;
     double *segsum = acc + (size_t)nv * TP;   // [G][nv]
     for (int idx = threadIdx.x; idx < nv * G; idx += T) {
         const int val = idx % nv, g = idx / nv;
@@ -2430,9 +2453,9 @@ int leaf_blocks(int64_t n, int depth, bool missing, int cu_count) {
 }
 
 size_t leaf_lds_bytes(int depth, bool missing) {
-    const size_t T = (size_t)leaf_threads(depth, missing);
+    const size_t C = (size_t)leaf_columns(depth, missing);
     const size_t nv = 2 * (size_t)leaf_slots(depth, missing);
-    return (nv * (T + 1) + (T >= nv ? T : nv)) * sizeof(double);
+    return (nv * (C + 1) + (C >= nv ? C : nv)) * sizeof(double);
 }
 
 template <bool ROUTED, int NP>
