@@ -344,6 +344,10 @@ FIT_CASES = {
     # negative event weights (section 4.1): about a fifth of the events
     "negative-weights": dict(cfg=2, n_events=30_011, n_trees=8, weights="signed"),
     "negative-weights-depth6": dict(cfg=4, n_events=60_013, depth=6, n_trees=2, weights="signed"),
+    # tiny samples: fewer events than one step of a pass, most nodes empty
+    "two-events-depth3": dict(cfg=1, n_events=2, depth=3, n_trees=3, subsample=1.0),
+    "17-events-depth6-B4": dict(cfg=4, n_events=17, depth=6, n_bins=4, n_trees=2),
+    "1001-events-depth7-B255": dict(cfg=3, n_events=1001, depth=7, n_bins=255, n_trees=2),
 }
 
 
@@ -401,6 +405,7 @@ MISSING_CASES = {
     "nan-depth1-B2": dict(cfg=1, n_events=1237, depth=1, n_bins=2, n_trees=5),
     "nan-negative-weights": dict(cfg=2, n_events=30_011, depth=4, n_trees=4, n_bins=64,
                                  weights="signed"),
+    "nan-33-events-depth5": dict(cfg=1, n_events=33, depth=5, n_trees=3),
 }
 
 
