@@ -37,6 +37,12 @@ struct fbdt_model {
         uint32_t *nodes;    // [T][16] node records of shallow forests, or null
         uint2 *frec;        // [T][2^D - 1] (feature, threshold) for float apply, or null
         double *gains;      // [T][2^D - 1] separation gains, or null
+        // float apply of shallow forests: per-feature threshold table and the
+        // node records (threshold ranks) for the tile stride fnodes_stride
+        uint32_t *ftab;
+        int ftab_words;
+        uint32_t *fnodes;
+        int fnodes_stride;
     };
     std::mutex mu;
     std::vector<DeviceCopy> copies;
@@ -850,9 +856,15 @@ int fbdt_model_set_boundaries(fbdt_model *m, const float *boundaries) {
     int cur = -1;
     (void)hipGetDevice(&cur);
     for (auto &c : m->copies)
-        if (c.frec && hipSetDevice(c.device) == hipSuccess) {
-            (void)hipFree(c.frec);
+        if (hipSetDevice(c.device) == hipSuccess) {
+            if (c.frec) (void)hipFree(c.frec);
+            if (c.ftab) (void)hipFree(c.ftab);
+            if (c.fnodes) (void)hipFree(c.fnodes);
             c.frec = nullptr;
+            c.ftab = nullptr;
+            c.fnodes = nullptr;
+            c.ftab_words = 0;
+            c.fnodes_stride = 0;
         }
     if (cur >= 0) (void)hipSetDevice(cur);
     return FBDT_OK;
@@ -869,6 +881,8 @@ void fbdt_model_free(fbdt_model *m) {
             if (c.nodes) (void)hipFree(c.nodes);
             if (c.frec) (void)hipFree(c.frec);
             if (c.gains) (void)hipFree(c.gains);
+            if (c.ftab) (void)hipFree(c.ftab);
+            if (c.fnodes) (void)hipFree(c.fnodes);
         }
     }
     if (cur >= 0) (void)hipSetDevice(cur);
@@ -1032,12 +1046,11 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = m->n_trees, D = m->depth;
     const size_t nin = ((size_t)1 << D) - 1;
-    const ApplyShape as = plan_apply_float(n, m->n_features, T, D, m->missing, di.cu_count,
-                                           di.max_lds, (int)opt_apply_threads.load());
-    if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
-        return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
-                    "apply_threads)", as.lds_bytes, di.max_lds);
+    const bool shallow = D <= kApplyShallowDepth && !m->missing;
+    ApplyShape as{};
     const uint2 *rec = nullptr;
+    const uint32_t *fnodes = nullptr, *ftab = nullptr;
+    int ftab_words = 0;
     const double *leaves = nullptr;
     {
         std::lock_guard<std::mutex> lk(m->mu);
@@ -1045,28 +1058,98 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
             return fail(FBDT_E_INVAL, "the model has no bin boundaries (fbdt_model_set_boundaries)");
         fbdt_model::DeviceCopy *copy = nullptr;
         if ((rc = device_copy(m, dev, &copy))) return rc;
-        if (!copy->frec) {
-            // cut "bin >= c" of feature j = "x >= boundary c of feature j"
-            // (boundary index c - 1 of its row)
-            std::vector<uint2> table((size_t)T * nin);
-            const size_t nb = (size_t)m->n_bins - 1;
-            for (size_t k = 0; k < table.size(); ++k) {
-                const uint32_t f = m->cut_feature[k], c = m->cut_bin[k];
-                float thr;
-                std::memcpy(&thr, &m->boundaries[f * nb + c - 1], sizeof thr);
-                uint32_t bits;
-                std::memcpy(&bits, &thr, sizeof bits);
-                table[k] = make_uint2(f, bits);
+        const size_t nb = (size_t)m->n_bins - 1;
+        // cut "bin >= c" of feature j = "x >= boundary c of feature j"
+        // (boundary index c - 1 of its row)
+        auto threshold = [&](size_t k) {
+            return m->boundaries[(size_t)m->cut_feature[k] * nb + m->cut_bin[k] - 1];
+        };
+        std::vector<uint32_t> rank;   // per node: rank of its threshold (shallow)
+        if (shallow && !copy->ftab) {
+            // per feature, the ascending distinct thresholds its cuts test
+            // (equal values, +0 and -0 included, decide alike: one entry)
+            const int d_used = m->n_features;
+            std::vector<std::vector<float>> per(d_used);
+            for (size_t k = 0; k < (size_t)T * nin; ++k)
+                per[m->cut_feature[k]].push_back(threshold(k));
+            std::vector<uint32_t> table(d_used + 1, 0u);
+            for (int f = 0; f < d_used; ++f) {
+                auto &v = per[f];
+                std::sort(v.begin(), v.end());
+                v.erase(std::unique(v.begin(), v.end(),
+                                    [](float a, float b) { return a == b; }),
+                        v.end());
+                table[f + 1] = table[f] + (uint32_t)v.size();
             }
-            HIP_TRY(hipMalloc(&copy->frec, table.size() * sizeof(uint2)));
-            HIP_TRY(hipMemcpy(copy->frec, table.data(), table.size() * sizeof(uint2),
+            for (int f = 0; f < d_used; ++f)
+                for (float t : per[f]) {
+                    uint32_t bits;
+                    std::memcpy(&bits, &t, sizeof bits);
+                    table.push_back(bits);
+                }
+            HIP_TRY(hipMalloc(&copy->ftab, table.size() * sizeof(uint32_t)));
+            HIP_TRY(hipMemcpy(copy->ftab, table.data(), table.size() * sizeof(uint32_t),
                               hipMemcpyHostToDevice));
+            copy->ftab_words = (int)table.size();
+            copy->fnodes_stride = 0;
         }
-        rec = copy->frec;
+        if (shallow) {
+            as = plan_apply_float(n, m->n_features, T, D, false, di.cu_count, di.max_lds,
+                                  (int)opt_apply_threads.load(),
+                                  (size_t)copy->ftab_words * sizeof(uint32_t));
+            if (copy->fnodes_stride != apply_node_stride(as)) {
+                // node records for this launch's tile stride, with threshold ranks
+                std::vector<uint32_t> ttab((size_t)copy->ftab_words);
+                HIP_TRY(hipMemcpy(ttab.data(), copy->ftab, ttab.size() * sizeof(uint32_t),
+                                  hipMemcpyDeviceToHost));
+                const int xs = apply_node_stride(as);
+                std::vector<uint32_t> table((size_t)T * 16, 0u);
+                const uint32_t *off = ttab.data();
+                const float *thr = reinterpret_cast<const float *>(ttab.data() + m->n_features + 1);
+                for (size_t t = 0; t < (size_t)T; ++t)
+                    for (size_t k = 0; k < nin; ++k) {
+                        const size_t q = t * nin + k;
+                        const uint32_t f = m->cut_feature[q];
+                        const float v = threshold(q);
+                        const float *lo = thr + off[f], *hi = thr + off[f + 1];
+                        const uint32_t r = (uint32_t)(std::lower_bound(lo, hi, v) - lo) + 1u;
+                        table[t * 16 + k] = f * (uint32_t)xs;
+                        table[t * 16 + 8 + k] = (256u - r) * 0x10001u;
+                    }
+                if (!copy->fnodes)
+                    HIP_TRY(hipMalloc(&copy->fnodes, table.size() * sizeof(uint32_t)));
+                HIP_TRY(hipMemcpy(copy->fnodes, table.data(), table.size() * sizeof(uint32_t),
+                                  hipMemcpyHostToDevice));
+                copy->fnodes_stride = xs;
+            }
+            fnodes = copy->fnodes;
+            ftab = copy->ftab;
+            ftab_words = copy->ftab_words;
+        } else {
+            as = plan_apply_float(n, m->n_features, T, D, m->missing, di.cu_count, di.max_lds,
+                                  (int)opt_apply_threads.load(), 0);
+            if (!copy->frec) {
+                std::vector<uint2> table((size_t)T * nin);
+                for (size_t k = 0; k < table.size(); ++k) {
+                    const float thr = threshold(k);
+                    uint32_t bits;
+                    std::memcpy(&bits, &thr, sizeof bits);
+                    table[k] = make_uint2(m->cut_feature[k], bits);
+                }
+                HIP_TRY(hipMalloc(&copy->frec, table.size() * sizeof(uint2)));
+                HIP_TRY(hipMemcpy(copy->frec, table.data(), table.size() * sizeof(uint2),
+                                  hipMemcpyHostToDevice));
+            }
+            rec = copy->frec;
+        }
         leaves = copy->leaves;
     }
+    if (as.lds_bytes + kHistStaticLdsReserve > di.max_lds)
+        return fail(FBDT_E_INVAL, "apply needs %zu bytes of LDS, the device has %zu (fewer "
+                    "apply_threads)", as.lds_bytes, di.max_lds);
     Timed tm(FBDT_K_APPLY, s, (double)n * (4.0 * m->n_features + 4));
-    HIP_TRY(launch_apply_float(as, x, ldx, n, rec, leaves, T, D, m->f0, prob, score, s));
+    HIP_TRY(launch_apply_float(as, x, ldx, n, rec, fnodes, ftab, ftab_words, leaves, T, D, m->f0,
+                               prob, score, s));
     tm.done();
     return FBDT_OK;
 }

@@ -300,13 +300,20 @@ hipError_t launch_importance(const ApplyShape &as, const uint8_t *xb, int64_t ld
                              const uint16_t *cuts, const double *gains, int n_trees, int depth,
                              double *imp, int64_t ldi, int d_out, hipStream_t s);
 
-// Traversal of float32 events [d][ldx] with value thresholds.  rec: [T][2^D-1]
-// (feature, float bits of the threshold) per heap node.  as.shallow marks
-// depth <= kApplyShallowDepth (every node tested, records by scalar loads).
+// Traversal of float32 events [d][ldx] with value thresholds.  Forests of
+// depth <= kApplyShallowDepth without missing values (as.shallow) take the
+// binned shallow traversal with its code tile staged from the values:
+// ftab = [d_used + 1] offsets, then per feature the ascending distinct
+// thresholds its cuts test (float bits), ftab_words words in all (table_bytes
+// of LDS); fnodes = node records as for the binned traversal (stride
+// apply_node_stride(as)) with word 8 + k = (256 - c') * 0x10001, c' the rank
+// (from 1) of the node's threshold among its feature's.  Other forests walk
+// rec: [T][2^D-1] (feature, float bits of the threshold) per heap node.
 ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, bool missing,
-                            int cu_count, size_t max_lds, int threads);
+                            int cu_count, size_t max_lds, int threads, size_t table_bytes);
 hipError_t launch_apply_float(const ApplyShape &as, const float *x, int64_t ldx, int64_t n,
-                              const uint2 *rec, const double *leaves, int n_trees, int depth,
+                              const uint2 *rec, const uint32_t *fnodes, const uint32_t *ftab,
+                              int ftab_words, const double *leaves, int n_trees, int depth,
                               double f0, float *prob, double *score, hipStream_t s);
 
 // Equal-frequency boundaries on the device: for every feature the value of

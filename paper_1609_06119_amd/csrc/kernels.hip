@@ -1750,9 +1750,19 @@ __device__ __forceinline__ uint32_t shallow_leaf2(const uint8_t *xpair, const ui
     return ((r1 & kBits) >> 6) | ((r2 & kBits) >> 7) | ((r3 & kBits) >> 8);
 }
 
-template <int D>
+// With FLOATS the tile is staged from float32 values (section 2.2's
+// inverse transform, fused): ftab holds, per feature, the ascending distinct
+// thresholds that the forest's cuts on it test (offsets [d_used + 1], then
+// the thresholds' float bits), and a value's code is the number of those
+// thresholds at or below it, found by a binary search in LDS; the node
+// records then carry, instead of the bin c, the rank c' of the node's
+// threshold among its feature's (code >= c' exactly when x >= threshold).
+// NaN compares false with every threshold: code 0, the left branch of every
+// cut, as the threshold test gives.
+template <int D, bool FLOATS>
 __global__ __launch_bounds__(1024) void apply_shallow_kernel(
-    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d_used,
+    const uint8_t *__restrict__ xb, int64_t ldb, const float *__restrict__ xf, int64_t ldx,
+    const uint32_t *__restrict__ ftab, int ftab_words, int64_t n, int d_used,
     const uint32_t *__restrict__ nodes, const double *__restrict__ leaves, int T, int tpc,
     double f0, float *__restrict__ prob, double *__restrict__ score) {
     constexpr int NLEAF = 1 << D;
@@ -1762,6 +1772,12 @@ __global__ __launch_bounds__(1024) void apply_shallow_kernel(
     uint8_t *s_x = reinterpret_cast<uint8_t *>(s_leaf + (size_t)tpc * NLEAF);   // [d_used][XS]
     const int tile_events = 2 * blockDim.x;
     const int XS = tile_events + 8;   // the stride the node records were prepared for
+    // FLOATS: thresholds per feature, after the code tile (XS is a multiple of 8)
+    uint32_t *s_tab = reinterpret_cast<uint32_t *>(s_x + (size_t)d_used * XS);
+    const float *s_thr = reinterpret_cast<const float *>(s_tab + d_used + 1);
+    if (FLOATS) {
+        for (int q = threadIdx.x; q < ftab_words; q += blockDim.x) s_tab[q] = ftab[q];
+    }
     const int nchunks = (T + tpc - 1) / tpc;
     const int64_t ntiles = (n + tile_events - 1) / tile_events;
     const uint8_t *xpair = s_x + 2 * threadIdx.x;
@@ -1769,14 +1785,42 @@ __global__ __launch_bounds__(1024) void apply_shallow_kernel(
     for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t i0 = tile * tile_events + 2 * threadIdx.x;   // this thread's events
         __syncthreads();
-        for (int f = 0; f < d_used; ++f) {
-            const uint8_t *src = xb + (int64_t)f * ldb + i0;
-            uint16_t pair = 0;
-            if (i0 + 1 < n)
-                pair = *reinterpret_cast<const uint16_t *>(src);
-            else if (i0 < n)
-                pair = src[0];
-            *reinterpret_cast<uint16_t *>(s_x + f * XS + 2 * threadIdx.x) = pair;
+        if (FLOATS) {
+            // 8 features' values loaded at a time, then their codes searched
+            for (int fb = 0; fb < d_used; fb += 8) {
+                float va[8], vb[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const float *src = xf + (int64_t)min(fb + u, d_used - 1) * ldx + i0;
+                    va[u] = i0 < n ? src[0] : 0.0f;
+                    vb[u] = i0 + 1 < n ? src[1] : 0.0f;
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int f = fb + u;
+                    if (f >= d_used) break;
+                    const int lo = (int)s_tab[f], m = (int)s_tab[f + 1] - lo;
+                    int ca = 0, cb = 0;
+                    // count of thresholds <= value (binary lifting over m entries)
+                    for (int step = m > 0 ? 1 << (31 - __clz(m)) : 0; step > 0; step >>= 1) {
+                        const int ta = ca + step, tb = cb + step;
+                        if (ta <= m && s_thr[lo + ta - 1] <= va[u]) ca = ta;
+                        if (tb <= m && s_thr[lo + tb - 1] <= vb[u]) cb = tb;
+                    }
+                    *reinterpret_cast<uint16_t *>(s_x + f * XS + 2 * threadIdx.x) =
+                        (uint16_t)(ca | (cb << 8));
+                }
+            }
+        } else {
+            for (int f = 0; f < d_used; ++f) {
+                const uint8_t *src = xb + (int64_t)f * ldb + i0;
+                uint16_t pair = 0;
+                if (i0 + 1 < n)
+                    pair = *reinterpret_cast<const uint16_t *>(src);
+                else if (i0 < n)
+                    pair = src[0];
+                *reinterpret_cast<uint16_t *>(s_x + f * XS + 2 * threadIdx.x) = pair;
+            }
         }
         double Fa = f0, Fb = f0;
         for (int ch = 0; ch < nchunks; ++ch) {
@@ -1899,31 +1943,13 @@ __global__ __launch_bounds__(256) void importance_kernel(
     }
 }
 
-// Leaf (0 .. 2^D - 1) of a tree of depth D <= 3 reached by this thread's
-// event: every node tested (x >= threshold), then the path picked from the
-// decisions; r[k] = (feature, threshold bits) of heap node k + 1.
-template <int D>
-__device__ __forceinline__ uint32_t float_leaf(const float *xme, int XS, const uint2 *r) {
-    constexpr int NIN = (1 << D) - 1;
-    uint32_t b[NIN];
-#pragma unroll
-    for (int k = 0; k < NIN; ++k) b[k] = xme[r[k].x * XS] >= __uint_as_float(r[k].y) ? 1u : 0u;
-    const uint32_t r1 = b[0];
-    if (D == 1) return r1;
-    const uint32_t r2 = r1 ? b[2] : b[1];
-    if (D == 2) return 2u * r1 + r2;
-    const uint32_t r3 = r1 ? (r2 ? b[6] : b[5]) : (r2 ? b[4] : b[3]);
-    return 4u * r1 + 2u * r2 + r3;
-}
-
 // Forest traversal of float32 events with value thresholds (section 2.2:
 // the cut "bin >= c" of feature j is the test x >= b_j,c, the c-th training
-// boundary, since a value's bin counts the boundaries at or below it).  A
-// workgroup stages a tile of one event per thread, feature-major, in LDS.
-// rec: [T][2^D - 1] pairs (feature, threshold bits).  Depth <= 3: every
-// node of a tree is tested (records read with scalar loads, a batch of
-// trees at a time) and the leaf is picked from the decisions without a
-// branch; deeper trees: each event walks its path with records in LDS.
+// boundary, since a value's bin counts the boundaries at or below it), for
+// trees deeper than kApplyShallowDepth or with missing values.  A workgroup
+// stages a tile of one event per thread, feature-major, in LDS, and chunks
+// of the forest's records rec: [T][2^D - 1] pairs (feature, threshold bits);
+// each event walks its path.
 template <int D>
 __global__ __launch_bounds__(1024) void apply_float_kernel(
     const float *__restrict__ x, int64_t ldx, int64_t n, int d_used,
@@ -1931,15 +1957,13 @@ __global__ __launch_bounds__(1024) void apply_float_kernel(
     int tpc, double f0, float *__restrict__ prob, double *__restrict__ score) {
     constexpr int NIN = (1 << D) - 1;
     // boost weights per tree: the leaves, or with missing values every node
-    // in heap order (a NaN value stops its event at the node cutting on it);
-    // missing values take the walk below, which stages the records in LDS
+    // in heap order (a NaN value stops its event at the node cutting on it)
     const int NLEAF = missing ? 2 * NIN + 1 : 1 << D;
     const int first_id = missing ? 1 : 1 << D;
-    const bool all = (D <= kApplyShallowDepth) && !missing;
     extern __shared__ double smem[];
     double *s_leaf = smem;                                                    // [tpc][NLEAF]
     uint2 *s_rec = reinterpret_cast<uint2 *>(s_leaf + (size_t)tpc * NLEAF);   // [tpc][NIN]
-    float *s_x = reinterpret_cast<float *>(s_rec + (all ? 0 : (size_t)tpc * NIN));
+    float *s_x = reinterpret_cast<float *>(s_rec + (size_t)tpc * NIN);
     const int XS = blockDim.x;   // [d_used][XS]
     const int nchunks = (T + tpc - 1) / tpc;
     const int64_t ntiles = (n + blockDim.x - 1) / blockDim.x;
@@ -1957,47 +1981,23 @@ __global__ __launch_bounds__(1024) void apply_float_kernel(
                 __syncthreads();
                 for (int q = threadIdx.x; q < tc * NLEAF; q += blockDim.x)
                     s_leaf[q] = leaves[(size_t)t0 * NLEAF + q];
-                if (!all)
-                    for (int q = threadIdx.x; q < tc * NIN; q += blockDim.x) {
-                        const uint2 r = rec[(size_t)t0 * NIN + q];
-                        s_rec[q] = make_uint2(r.x * (uint32_t)XS, r.y);   // row offset
-                    }
+                for (int q = threadIdx.x; q < tc * NIN; q += blockDim.x) {
+                    const uint2 r = rec[(size_t)t0 * NIN + q];
+                    s_rec[q] = make_uint2(r.x * (uint32_t)XS, r.y);   // row offset
+                }
                 staged = true;
             }
             __syncthreads();
-            if (D <= kApplyShallowDepth && all) {
-                int t = 0;
-                for (; t + kApplyBatch <= tc; t += kApplyBatch) {
-                    uint2 r[kApplyBatch][NIN];
+            for (int t = 0; t < tc; ++t) {
+                int node = 1;
 #pragma unroll
-                    for (int u = 0; u < kApplyBatch; ++u)
-#pragma unroll
-                        for (int k = 0; k < NIN; ++k) r[u][k] = rec[(size_t)(t0 + t + u) * NIN + k];
-                    double lv[kApplyBatch];
-#pragma unroll
-                    for (int u = 0; u < kApplyBatch; ++u)
-                        lv[u] = s_leaf[(t + u) * NLEAF + float_leaf<(D < 3 ? D : 3)>(xme, XS, r[u])];
-#pragma unroll
-                    for (int u = 0; u < kApplyBatch; ++u) Fv += lv[u];
+                for (int lvl = 0; lvl < D; ++lvl) {
+                    const uint2 r = s_rec[t * NIN + node - 1];
+                    const float xv = xme[r.x];
+                    if (missing && xv != xv) break;   // NaN: stops at this node
+                    node = 2 * node + (xv >= __uint_as_float(r.y) ? 1 : 0);
                 }
-                for (; t < tc; ++t) {
-                    uint2 r[NIN];
-#pragma unroll
-                    for (int k = 0; k < NIN; ++k) r[k] = rec[(size_t)(t0 + t) * NIN + k];
-                    Fv += s_leaf[t * NLEAF + float_leaf<(D < 3 ? D : 3)>(xme, XS, r)];
-                }
-            } else {
-                for (int t = 0; t < tc; ++t) {
-                    int node = 1;
-#pragma unroll
-                    for (int lvl = 0; lvl < D; ++lvl) {
-                        const uint2 r = s_rec[t * NIN + node - 1];
-                        const float xv = xme[r.x];
-                        if (missing && xv != xv) break;   // NaN: stops at this node
-                        node = 2 * node + (xv >= __uint_as_float(r.y) ? 1 : 0);
-                    }
-                    Fv += s_leaf[t * NLEAF + node - first_id];
-                }
+                Fv += s_leaf[t * NLEAF + node - first_id];
             }
         }
         if (i < n) {
@@ -2121,9 +2121,12 @@ hipError_t prepare_kernels(size_t max_lds) {
                             allow_lds(leaf_kernel<true, 1>, max_lds),
                             allow_lds(leaf_kernel<true, 2>, max_lds),
                             allow_lds(leaf_kernel<true, 4>, max_lds),
-                            allow_lds(apply_shallow_kernel<1>, max_lds),
-                            allow_lds(apply_shallow_kernel<2>, max_lds),
-                            allow_lds(apply_shallow_kernel<3>, max_lds),
+                            allow_lds(apply_shallow_kernel<1, false>, max_lds),
+                            allow_lds(apply_shallow_kernel<2, false>, max_lds),
+                            allow_lds(apply_shallow_kernel<3, false>, max_lds),
+                            allow_lds(apply_shallow_kernel<1, true>, max_lds),
+                            allow_lds(apply_shallow_kernel<2, true>, max_lds),
+                            allow_lds(apply_shallow_kernel<3, true>, max_lds),
                             allow_lds(apply_float_kernel<1>, max_lds),
                             allow_lds(apply_float_kernel<2>, max_lds),
                             allow_lds(apply_float_kernel<3>, max_lds),
@@ -2580,8 +2583,9 @@ hipError_t launch_apply(const ApplyShape &as, const uint8_t *xb, int64_t ldb, in
     if (as.shallow) {
         if (!nodes) return hipErrorInvalidValue;
 #define FBDT_APPLY_S(DV)                                                                        \
-    apply_shallow_kernel<DV><<<as.blocks, as.threads, as.lds_bytes, s>>>(                       \
-        xb, ldb, n, as.d_used, nodes, leaves, n_trees, as.trees_per_chunk, f0, prob, score)
+    apply_shallow_kernel<DV, false><<<as.blocks, as.threads, as.lds_bytes, s>>>(                \
+        xb, ldb, nullptr, 0, nullptr, 0, n, as.d_used, nodes, leaves, n_trees,                 \
+        as.trees_per_chunk, f0, prob, score)
         switch (depth) {
         case 1: FBDT_APPLY_S(1); break;
         case 2: FBDT_APPLY_S(2); break;
@@ -2636,11 +2640,20 @@ hipError_t launch_importance(const ApplyShape &as, const uint8_t *xb, int64_t ld
 }
 
 ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, bool missing,
-                            int cu_count, size_t max_lds, int threads) {
+                            int cu_count, size_t max_lds, int threads, size_t table_bytes) {
+    if (depth <= kApplyShallowDepth && !missing) {
+        // the binned shallow traversal, its tile staged from the values with
+        // the threshold table beside it in LDS
+        const size_t tb = (table_bytes + 15) & ~(size_t)15;
+        ApplyShape as = plan_apply(n, d_used, n_trees, depth, false, cu_count,
+                                   max_lds > tb ? max_lds - tb : 0, threads);
+        as.lds_bytes += tb;
+        return as;
+    }
     ApplyShape as{};
     as.d_used = d_used;
     as.missing = missing;
-    as.shallow = depth <= kApplyShallowDepth && !missing;
+    as.shallow = false;
     const int nin = (1 << depth) - 1, nleaf = missing ? 2 * nin + 1 : 1 << depth;
     const size_t lds_cap = max_lds > kHistStaticLdsReserve ? max_lds - kHistStaticLdsReserve : 0;
     // one event per thread, 768 threads (measured best on 8M events x 40
@@ -2650,7 +2663,7 @@ ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, bool 
     while (t > 64 && (size_t)d_used * t * 4 > 124 * 1024) t -= 64;
     as.threads = t;
     const size_t xtile = (size_t)d_used * t * 4;
-    const size_t per_tree = (size_t)nleaf * 8 + (as.shallow ? 0 : (size_t)nin * 8);
+    const size_t per_tree = (size_t)nleaf * 8 + (size_t)nin * 8;
     const size_t room = lds_cap > xtile + 64 ? lds_cap - xtile - 64 : 0;
     int64_t tpc = (int64_t)(room / per_tree);
     if (tpc < 1) tpc = 1;
@@ -2666,8 +2679,24 @@ ApplyShape plan_apply_float(int64_t n, int d_used, int n_trees, int depth, bool 
 }
 
 hipError_t launch_apply_float(const ApplyShape &as, const float *x, int64_t ldx, int64_t n,
-                              const uint2 *rec, const double *leaves, int n_trees, int depth,
+                              const uint2 *rec, const uint32_t *fnodes, const uint32_t *ftab,
+                              int ftab_words, const double *leaves, int n_trees, int depth,
                               double f0, float *prob, double *score, hipStream_t s) {
+    if (as.shallow) {
+        if (!fnodes || !ftab) return hipErrorInvalidValue;
+#define FBDT_APPLY_FS(DV)                                                                       \
+    apply_shallow_kernel<DV, true><<<as.blocks, as.threads, as.lds_bytes, s>>>(                 \
+        nullptr, 0, x, ldx, ftab, ftab_words, n, as.d_used, fnodes, leaves, n_trees,           \
+        as.trees_per_chunk, f0, prob, score)
+        switch (depth) {
+        case 1: FBDT_APPLY_FS(1); break;
+        case 2: FBDT_APPLY_FS(2); break;
+        case 3: FBDT_APPLY_FS(3); break;
+        default: return hipErrorInvalidValue;
+        }
+#undef FBDT_APPLY_FS
+        return hipGetLastError();
+    }
 #define FBDT_APPLY_F(DV)                                                                        \
     apply_float_kernel<DV><<<as.blocks, as.threads, as.lds_bytes, s>>>(                         \
         x, ldx, n, as.d_used, rec, leaves, n_trees, as.missing, as.trees_per_chunk, f0, prob,  \
