@@ -58,3 +58,15 @@ def test_argument_errors_need_no_device():
     assert L.fbdt_set_option(b"hist_copies", 3) == -1
     assert L.fbdt_set_option(b"hist_copies", 4) == 0
     assert L.fbdt_set_option(b"hist_copies", 0) == 0
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus 2 exits with status 2 and says so,
+    before any device work."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stdout + r.stderr
