@@ -18,7 +18,9 @@ HBM.  Prints one JSON line:
 Also reported, outside the step: "apply" = the 400-tree forest applied to 50M
 fresh events (events/s); "fit_workloads" = full fits of the 2M x 40 (200
 trees) and 10M x 40 (depth 6, 100 trees) workloads, with the histogram
-kernel's mean launch and roofline fraction on each.
+kernel's mean launch and roofline fraction on each; "section4" = on the
+2M x 40 sample, fits with negative event weights and with missing values
+against the plain fit, and the per-event and global feature importance.
 """
 from __future__ import annotations
 
@@ -64,6 +66,8 @@ def parse():
                     help="fresh events of the apply workload (0 skips it)")
     ap.add_argument("--apply-steps", type=int, default=3,
                     help="timed applies of the 400-tree forest to the fresh events")
+    ap.add_argument("--section4", type=int, default=1,
+                    help="also time negative weights, missing values and importance (1/0)")
     ap.add_argument("--fit-workloads", default="3,4",
                     help="larger fit workloads also timed and reported (comma list, '' for none)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -118,6 +122,63 @@ def measure_fit_workload(cfg, fb, torch):
             # layers with more than 4 parents: routing as a pass of its own
             "route_launches": rl,
             "route_mean_launch_us": rms * 1e3 / rl if rl else None,
+            "setup_s": round(time.time() - t0, 1)}
+
+
+def measure_section4(fb, torch):
+    """The features of sections 4.1-4.3 on workload 3's sample (2M x 40, 256
+    bins, 200 trees of depth 3), each against the plain fit of the same
+    sample: a fit with negative event weights (v uniform in [-0.6, 2.5]), a
+    fit with missing values (NaN in the float features, features in turn
+    0%, 3%, 20% and 60% missing, 255 bins so that code 255 marks them), and
+    the per-event and global importance of the plain model.  Times are one
+    fit (or call) after a warm-up, host clock around a synchronised call."""
+    import numpy as np
+    from synth import CONFIGS, make_training_set
+    spec = CONFIGS[3]
+    t0 = time.time()
+    ds = make_training_set(3)
+    d, n = ds["x"].shape
+    y = torch.from_numpy(ds["y"]).cuda()
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        out = fn()
+        torch.cuda.synchronize()
+        return out, (time.perf_counter() - ts) * 1e3
+
+    def fit(codes, n_bins, w=None):
+        return lambda: fb.fit(codes, y, n_bins, spec.depth, spec.n_trees, spec.shrinkage,
+                              spec.subsample, spec.fit_seed, w=w)
+
+    _, codes = fb.bin(torch.from_numpy(ds["x"]).cuda(), spec.n_bins)
+    plain, plain_ms = timed(fit(codes, spec.n_bins))
+    v = np.random.default_rng(9).uniform(-0.6, 2.5, n).astype(np.float32)
+    _, signed_ms = timed(fit(codes, spec.n_bins, torch.from_numpy(v).cuda()))
+    xm = ds["x"].copy()
+    rng = np.random.default_rng(7)
+    for j in range(d):
+        xm[j, rng.random(n) < (0.0, 0.03, 0.2, 0.6)[j % 4]] = np.nan
+    _, mcodes = fb.bin(torch.from_numpy(xm).cuda(), 255)
+    del xm
+    mmodel, missing_ms = timed(fit(mcodes, 255))
+    has_inner = "inner" in mmodel.export()
+    ei = torch.empty((d, n), dtype=torch.float64, device="cuda")
+    _, ei_ms = timed(lambda: fb.event_importance(plain, codes, out=ei))
+    _, fi_ms = timed(lambda: fb.feature_importance(plain))
+    del ei, codes, mcodes, y
+    torch.cuda.empty_cache()
+    return {"workload": f"fit {n} x {d}, depth {spec.depth}, {spec.n_trees} trees "
+                        f"({spec.name})",
+            "plain_fit_ms": plain_ms,
+            "negative_weights_fit_ms": signed_ms,
+            "missing_values_fit_ms": missing_ms,
+            "missing_values_model_has_inner_weights": has_inner,
+            "event_importance_ms": ei_ms,
+            "event_importance_events_per_s": n / (ei_ms / 1e3),
+            "feature_importance_ms": fi_ms,
             "setup_s": round(time.time() - t0, 1)}
 
 
@@ -280,6 +341,10 @@ def main():
         print(f"# fit workload {c}: {fits[f'workload{int(c)}']['fit_ms']:.1f} ms", file=sys.stderr,
               flush=True)
 
+    section4 = measure_section4(fb, torch) if args.section4 else None
+    if section4:
+        print(f"# section 4 features: {section4}", file=sys.stderr, flush=True)
+
     apply_out = {"events_per_s": apply_events_per_s, "launches": a_launches,
                  "mean_launch_us": a_ms * 1e3 / max(a_launches, 1),
                  "workload": f"{n} binned events x {T} trees of depth {D} (the step's apply)"}
@@ -330,6 +395,7 @@ def main():
         },
         "apply": apply_out,
         "fit_workloads": fits,
+        "section4": section4,
         "bin_ms": bin_ms,
         "cpu_baseline": {
             "value": cpu_value,
