@@ -97,9 +97,19 @@ def measure_fit_workload(cfg, fb, torch):
     fit()   # warm-up (records the graph)
     torch.cuda.synchronize()
     ts = time.perf_counter()
-    fit()
+    model = fit()
     torch.cuda.synchronize()
     fit_s = time.perf_counter() - ts
+    # the fitted forest applied to the training events (the general
+    # traversal for depth > 3, the two-events-per-lane one below)
+    prob = torch.empty(n, dtype=torch.float32, device="cuda")
+    fb.apply(model, codes, prob=prob)
+    torch.cuda.synchronize()
+    ta = time.perf_counter()
+    fb.apply(model, codes, prob=prob)
+    torch.cuda.synchronize()
+    apply_s = time.perf_counter() - ta
+    del prob, model
     fb.timing_enable(("histogram", "best_cuts", "route"))
     fit()
     torch.cuda.synchronize()
@@ -119,6 +129,8 @@ def measure_fit_workload(cfg, fb, torch):
             "hist_achieved_gbs": achieved,
             "hist_frac": achieved / HBM_PEAK_GBS,
             "cut_scan_mean_launch_us": cms * 1e3 / max(cl, 1),
+            "apply_ms": apply_s * 1e3,
+            "apply_events_per_s": n / apply_s,
             # layers with more than 4 parents: routing as a pass of its own
             "route_launches": rl,
             "route_mean_launch_us": rms * 1e3 / rl if rl else None,
