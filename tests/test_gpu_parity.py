@@ -488,6 +488,34 @@ def test_missing_values_need_depth_at_most_6_and_plain_data_stays_plain():
     assert "inner" not in fb.fit(plain, y, 16, 3, 2).export()
 
 
+@pytest.mark.parametrize("d,n,B,D,T", [(255, 5003, 256, 4, 3), (3, 20_011, 3, 5, 4),
+                                       (8, 3001, 16, 2, 300)])
+def test_fit_extreme_shapes_match_oracle(d, n, B, D, T):
+    """The most features a code byte can name (255), three bins, and a
+    300-tree boosting loop (one captured graph of 300 x 6 launches), against
+    the oracle: random features, labels from a noisy linear rule."""
+    rng = np.random.default_rng(d + n)
+    x = rng.normal(size=(d, n)).astype(np.float32)
+    score = x[: min(d, 4)].sum(axis=0) + rng.normal(scale=1.0, size=n)
+    y = np.where(score > 0, 1, -1).astype(np.int8)
+    v = np.ones(n, np.float32)
+    say(f"extreme fit: d={d} n={n} B={B} D={D} T={T}")
+    _, codes = fb.bin(dev(x), B)
+    _, xb = O.bin_features(x, B)
+    assert np.array_equal(codes.numpy(), xb)
+    sc = torch.empty(n, dtype=torch.float64, device="cuda")
+    gm = fb.fit(codes, dev(y), B, D, T, 0.1, 0.5, 3, score_out=sc).export()
+    log = O.TieLog()
+    om, F = O.fit(xb, y, v, D, T, 0.1, 0.5, 3, B, reference=_oracle_model(gm), tie_log=log,
+                  final_score=True)
+    say(f"  near-ties adopted: {len(log.adopted)}  rejected: {len(log.rejected)}")
+    assert log.rejected == []
+    assert np.array_equal(gm["cut_feature"], om.cut_feature)
+    assert np.array_equal(gm["cut_bin"], om.cut_bin)
+    assert np.allclose(gm["leaf"], om.leaf, rtol=1e-9, atol=1e-13)
+    assert np.allclose(sc.cpu().numpy(), F, rtol=1e-9, atol=1e-12)
+
+
 def test_fit_graph_replays_match_eager_fit():
     """The boosting loop is captured once per argument set and replayed; every
     replay, with other device work and other fits in between, gives the model
