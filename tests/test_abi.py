@@ -70,3 +70,32 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stdout + r.stderr
+
+
+def test_degenerate_arguments_are_rejected_before_device_work():
+    """Empty and out-of-range inputs are FBDT_E_INVAL before any HIP call:
+    no events, no or too many features, 1 or 257 bins, depth 0 or 8, no
+    trees, shrinkage not finite and > 0, subsample outside (0, 1]."""
+    from paper_1609_06119_amd._lib import FitParams, lib
+    L = lib()
+    h = ctypes.c_void_p()
+    buf = ctypes.create_string_buffer(4096 + 16)
+    xb = ctypes.c_void_p((ctypes.addressof(buf) + 15) // 16 * 16)
+    y = ctypes.create_string_buffer(64)
+
+    def fit(n=10, d=2, ldb=16, n_bins=16, params=(3, 10, 0.1, 0.5, 0)):
+        p = FitParams(*params)
+        return L.fbdt_fit(xb, n, d, ldb, n_bins, y, None, ctypes.byref(p), ctypes.byref(h),
+                          None, None)
+
+    for kw, needle in [(dict(n=0), b"n = 0"), (dict(d=0), b"d = 0"), (dict(d=256), b"d = 256"),
+                       (dict(n_bins=1), b"n_bins"), (dict(n_bins=257), b"n_bins"),
+                       (dict(params=(0, 10, 0.1, 0.5, 0)), b"depth"),
+                       (dict(params=(8, 10, 0.1, 0.5, 0)), b"depth"),
+                       (dict(params=(3, 0, 0.1, 0.5, 0)), b"n_trees"),
+                       (dict(params=(3, 10, 0.0, 0.5, 0)), b"shrinkage"),
+                       (dict(params=(3, 10, float("inf"), 0.5, 0)), b"shrinkage"),
+                       (dict(params=(3, 10, 0.1, 0.0, 0)), b"subsample"),
+                       (dict(params=(3, 10, 0.1, 1.5, 0)), b"subsample")]:
+        assert fit(**kw) == -1, kw
+        assert needle in L.fbdt_last_error(), (kw, L.fbdt_last_error())
