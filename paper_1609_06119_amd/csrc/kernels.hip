@@ -498,7 +498,12 @@ __global__ __launch_bounds__(64) void select_cuts_kernel(const double *__restric
 // stores the new ids.  With NP > 0 (NP = number of parents) the code rows of
 // the parents' cut features are loaded for the step up front, so routing
 // costs no dependent load; with NP = 0 each event's routing code is
-// gathered after its parent id arrives (deep layers).
+// gathered after its parent id arrives.  The fit routes layers with more
+// than kRoutedMaxParents parents by a pass of its own (route_layer_kernel)
+// and histograms them with ROUTED = false from the new ids.  MISS (routed
+// passes of fits with missing values) adds the stops at the missing code
+// and histograms both children; otherwise layers below the root histogram
+// the left children only (sibling subtraction), in both modes.
 //
 // An LDS row of (node, feature) holds 256 bins x 2 classes (4 KiB) whatever
 // n_bins; codes >= n_bins land in bins that are checked at the end and
