@@ -168,7 +168,7 @@ def bin(x: torch.Tensor, n_bins: int, codes: Codes | None = None):
     d, n = int(x.shape[0]), int(x.shape[1])
     codes = codes or Codes.empty(d, n, x.device)
     bounds = np.zeros((d, n_bins - 1), np.float32)
-    check("fbdt_bin", lib().fbdt_bin(_ptr(x), n, d, x.stride(0), n_bins,
+    check("fbdt_bin", lib().fbdt_bin(_ptr(x), n, d, _row_stride(x), n_bins,
                                      bounds.ctypes.data_as(C.c_void_p), _ptr(codes.data),
                                      codes.ldb, _stream()))
     return bounds, codes
@@ -177,8 +177,13 @@ def bin(x: torch.Tensor, n_bins: int, codes: Codes | None = None):
 def _need_rows(x: torch.Tensor):
     if not isinstance(x, torch.Tensor) or not x.is_cuda or x.dtype != torch.float32:
         raise TypeError("x must be a float32 CUDA (HIP) tensor [d][n]")
-    if x.dim() != 2 or x.stride(1) != 1:
+    if x.dim() != 2 or (x.stride(1) != 1 and x.shape[1] > 1):
         raise ValueError("x must be 2-D [d][n] with unit stride along events")
+
+
+def _row_stride(x: torch.Tensor) -> int:
+    """Elements between feature rows; a single row may report any stride."""
+    return int(x.stride(0)) if x.shape[0] > 1 else int(x.shape[1])
 
 
 def bin_transform(x: torch.Tensor, boundaries: np.ndarray, codes: Codes | None = None) -> Codes:
@@ -190,7 +195,7 @@ def bin_transform(x: torch.Tensor, boundaries: np.ndarray, codes: Codes | None =
         raise ValueError("boundaries must have one row per feature")
     codes = codes or Codes.empty(d, n, x.device)
     check("fbdt_bin_transform",
-          lib().fbdt_bin_transform(_ptr(x), n, d, x.stride(0), b.shape[1] + 1,
+          lib().fbdt_bin_transform(_ptr(x), n, d, _row_stride(x), b.shape[1] + 1,
                                    b.ctypes.data_as(C.c_void_p), _ptr(codes.data), codes.ldb,
                                    _stream()))
     return codes
@@ -239,7 +244,7 @@ def apply_float(model: Model, x: torch.Tensor, prob: torch.Tensor | None = None,
     _need(prob, torch.float32, "prob", n)
     if score is not None:
         _need(score, torch.float64, "score", n)
-    check("fbdt_apply_float", lib().fbdt_apply_float(model.handle, _ptr(x), n, d, x.stride(0),
+    check("fbdt_apply_float", lib().fbdt_apply_float(model.handle, _ptr(x), n, d, _row_stride(x),
                                                      _ptr(prob), _ptr(score), _stream()))
     return prob
 

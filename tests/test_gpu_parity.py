@@ -718,6 +718,66 @@ def test_feature_and_event_importance_match_oracle():
     assert not ei[d:].any()
 
 
+# ------------------------------------------------ hand-worked examples
+def test_hand_worked_examples_on_the_gpu():
+    """The fixtures worked by hand from the paper's definitions, through the
+    C ABI: the depth-1 example (binning, the cut, the boost weights and P of
+    two trees), its missing-value variant (section 4.2: code 255, the root's
+    boost weight for the stopped event), and the exclusive-or table of
+    section 4.3 (a zero-gain root cut, gains 0.5 below it, importance)."""
+    from tests.golden_io import read_fixture
+    _, ex = read_fixture("hand_depth1.txt")
+    x = np.array(ex["x"], np.float32)[None, :]
+    y = np.array(ex["y"], np.int8)
+    bounds, codes = fb.bin(dev(x), 4)
+    assert bounds[0].tolist() == ex["boundaries"]
+    assert codes.numpy()[0].tolist() == ex["bins"]
+    m = fb.fit(codes, dev(y), 4, 1, 2, 1.0, 1.0, 0).export()
+    assert int(m["cut_bin"][0, 0]) == int(ex["tree1_cut"][0])
+    assert np.allclose(m["leaf"][0], ex["tree1_leaves"], rtol=1e-15)
+    assert np.allclose(m["gain"][0, 0], ex["tree1_gains"][0], rtol=1e-15)
+    assert int(m["cut_bin"][1, 0]) == int(ex["tree2_cut_eta1"][0])
+    assert np.allclose(m["leaf"][1], ex["tree2_leaves_eta1"], atol=1e-6)
+    p = fb.apply(fb.fit(codes, dev(y), 4, 1, 2, 1.0, 1.0, 0), codes).cpu().numpy()
+    assert np.allclose(p[[0, 2, 4]], ex["tree2_p_eta1"], atol=1e-6)
+
+    _, ex = read_fixture("hand_missing.txt")
+    x = np.array(ex["x"], np.float32)[None, :]
+    y = np.array(ex["y"], np.int8)
+    bounds, codes = fb.bin(dev(x), 4)
+    assert bounds[0].tolist() == ex["boundaries"]
+    assert codes.numpy()[0].tolist() == [int(v) for v in ex["bins"]]
+    model = fb.fit(codes, dev(y), 4, 1, 1, 1.0, 1.0, 0)
+    m = model.export()
+    assert int(m["cut_bin"][0, 0]) == int(ex["cut"][0])
+    assert np.allclose(m["leaf"][0], ex["leaves"], rtol=1e-15)
+    assert np.allclose(m["inner"][0], ex["root_value"], atol=1e-15)
+    assert np.allclose(fb.apply(model, codes).cpu().numpy(), ex["p"], atol=1e-7)
+    model.set_boundaries(bounds)
+    assert np.allclose(fb.apply_float(model, dev(x)).cpu().numpy(), ex["p"], atol=1e-7)
+
+    rows, ex = read_fixture("xor_table3.txt")
+    t = np.array(rows, np.float32)
+    x = np.ascontiguousarray(t[:, :2].T)
+    y = np.where(t[:, 2] > 0, 1, -1).astype(np.int8)
+    bounds, codes = fb.bin(dev(x), 2)
+    model = fb.fit(codes, dev(y), 2, 2, 1, 1.0, 1.0, 0)
+    m = model.export()
+    assert (int(m["cut_feature"][0, 0]), int(m["cut_bin"][0, 0])) == tuple(
+        int(v) for v in ex["root_cut"])
+    assert m["gain"][0, 0] == ex["root_gain"][0]
+    for k in (1, 2):
+        assert (int(m["cut_feature"][0, k]), int(m["cut_bin"][0, k])) == tuple(
+            int(v) for v in ex["layer2_cut"])
+        assert np.isclose(m["gain"][0, k], ex["layer2_gain"][0], rtol=1e-15)
+    p = fb.apply(model, codes).cpu().numpy()
+    assert np.allclose(p[y > 0], ex["p_signal"][0], atol=1e-7)
+    assert np.allclose(p[y < 0], ex["p_background"][0], atol=1e-7)
+    assert np.allclose(fb.feature_importance(model), ex["importance"], rtol=1e-15)
+    ei = fb.event_importance(model, codes).cpu().numpy()
+    assert np.allclose(ei, np.array(ex["event_importance"])[:, None], rtol=1e-15)
+
+
 # ------------------------------------------------------------------ errors
 def test_errors_are_reported():
     n, d, B = 1000, 3, 16
