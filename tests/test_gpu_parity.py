@@ -516,6 +516,30 @@ def test_fit_extreme_shapes_match_oracle(d, n, B, D, T):
     assert np.allclose(sc.cpu().numpy(), F, rtol=1e-9, atol=1e-12)
 
 
+def test_fit_on_constant_features_takes_zero_gain_cuts():
+    """Degenerate sample: every feature constant, so every boundary equals the
+    value and every code is the top bin; every candidate cut has gain 0 and
+    every node takes (feature 0, bin 1), which sends all its events right:
+    only the rightmost leaf has events, the others keep boost weight 0
+    (section 1.1's cut rule, the empty-node reading), against the oracle."""
+    n, d, B, D, T = 1000, 3, 16, 3, 2
+    x = np.full((d, n), 2.5, np.float32)
+    y = np.where(np.arange(n) % 3 == 0, 1, -1).astype(np.int8)
+    _, codes = fb.bin(dev(x), B)
+    _, xb = O.bin_features(x, B)
+    assert np.array_equal(codes.numpy(), xb)
+    sc = torch.empty(n, dtype=torch.float64, device="cuda")
+    gm = fb.fit(codes, dev(y), B, D, T, 0.1, 0.5, 1, score_out=sc).export()
+    om, F = O.fit(xb, y, np.ones(n, np.float32), D, T, 0.1, 0.5, 1, B, final_score=True)
+    assert (gm["cut_feature"] == 0).all() and (gm["cut_bin"] == 1).all()
+    assert np.array_equal(gm["cut_feature"], om.cut_feature)
+    assert np.array_equal(gm["cut_bin"], om.cut_bin)
+    assert (gm["gain"] == 0.0).all()
+    assert np.allclose(gm["leaf"], om.leaf, rtol=1e-12, atol=1e-15)
+    assert (gm["leaf"][:, :-1] == 0.0).all()         # only the rightmost leaf has events
+    assert np.allclose(sc.cpu().numpy(), F, rtol=1e-12)
+
+
 def test_fit_graph_replays_match_eager_fit():
     """The boosting loop is captured once per argument set and replayed; every
     replay, with other device work and other fits in between, gives the model
