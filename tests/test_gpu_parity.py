@@ -348,6 +348,11 @@ FIT_CASES = {
     "two-events-depth3": dict(cfg=1, n_events=2, depth=3, n_trees=3, subsample=1.0),
     "17-events-depth6-B4": dict(cfg=4, n_events=17, depth=6, n_bins=4, n_trees=2),
     "1001-events-depth7-B255": dict(cfg=3, n_events=1001, depth=7, n_bins=255, n_trees=2),
+    # event weights over 15 orders of magnitude: the smallest fall below the
+    # fixed-point grid into the float64 side histograms inside the fit
+    "weights-1e-12-to-1e3": dict(cfg=2, n_events=30_011, n_trees=5, weights="wide"),
+    # one signal event in 20,000: F0 = -4.95, extreme pseudo-responses
+    "one-signal-in-20000": dict(cfg=1, n_events=20_000, n_trees=5, labels="one-signal"),
 }
 
 
@@ -366,8 +371,13 @@ def test_fit_and_apply_match_oracle(case):
     v = ds["v"]
     if c.get("weights") == "signed":
         v = np.random.default_rng(9).uniform(-0.6, 2.5, n).astype(np.float32)
+    elif c.get("weights") == "wide":
+        v = (10.0 ** np.random.default_rng(9).uniform(-12, 3, n)).astype(np.float32)
     elif c.get("weights"):
         v = np.random.default_rng(9).uniform(0.2, 3.0, n).astype(np.float32)
+    if c.get("labels") == "one-signal":
+        ds["y"] = np.full(n, -1, np.int8)
+        ds["y"][n // 3] = 1
     say(f"fit parity {case}: n={n} d={ds['x'].shape[0]} B={B} D={D} T={T} alpha={alpha}")
     bounds, codes = fb.bin(dev(ds["x"]), B)
     ob, xb = O.bin_features(ds["x"], B)
