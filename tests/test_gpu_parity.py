@@ -62,10 +62,15 @@ def _bin_cases():
     cases.append(("inf-and-signed-zero", x, 32))
     cases.append(("one-event", np.array([[1.5]], np.float32), 2))
     cases.append(("more-bins-than-events", rng.normal(size=(2, 5)).astype(np.float32), 256))
+    # subnormal, tiny, huge and signed-zero values mixed (the order-preserving
+    # keys of the device sort against the oracle's comparison sort)
+    edge = np.array([1e-45, -1e-45, 1e-40, -1e-40, 1.17549435e-38, 0.0, -0.0, 3.4028235e38,
+                     -3.4028235e38, 1.0, -1.0], np.float32)
+    cases.append(("subnormal-and-huge", edge[rng.integers(0, len(edge), (3, 4001))], 64))
     return cases
 
 
-@pytest.mark.parametrize("case", range(6))
+@pytest.mark.parametrize("case", range(7))
 def test_bin_matches_oracle(case):
     name, x, B = _bin_cases()[case]
     say(f"bin parity: {name} d={x.shape[0]} n={x.shape[1]} B={B}")
