@@ -555,25 +555,32 @@ def test_fit_on_constant_features_takes_zero_gain_cuts():
     assert np.allclose(sc.cpu().numpy(), F, rtol=1e-12)
 
 
-def test_fit_graph_replays_match_eager_fit():
+@pytest.mark.parametrize("mode", ["plain", "missing-signed-depth5"])
+def test_fit_graph_replays_match_eager_fit(mode):
     """The boosting loop is captured once per argument set and replayed; every
     replay, with other device work and other fits in between, gives the model
-    and scores of a fit that launches its kernels one by one."""
+    and scores of a fit that launches its kernels one by one; also for a fit
+    with missing values, negative weights and route passes (depth 5)."""
     spec = CONFIGS[2]
     ds = make_training_set(2, n_events=60_013)
     n = ds["x"].shape[1]
-    _, codes = fb.bin(dev(ds["x"]), spec.n_bins)
+    x, B, D, w = ds["x"], spec.n_bins, 3, None
+    if mode != "plain":
+        x, B, D = _with_missing(x, 5), 200, 5
+        w = dev(np.random.default_rng(9).uniform(-0.6, 2.5, n).astype(np.float32))
+    _, codes = fb.bin(dev(x), B)
     y = dev(ds["y"])
-    args = (spec.n_bins, 3, 12, spec.shrinkage, spec.subsample)
+    args = (B, D, 12, spec.shrinkage, spec.subsample)
 
     def run(seed):
         score = torch.empty(n, dtype=torch.float64, device="cuda")
-        m = fb.fit(codes, y, *args, seed, score_out=score).export()
+        m = fb.fit(codes, y, *args, seed, w=w, score_out=score).export()
         return m, score.cpu().numpy()
 
     def same(a, b):
         (ma, fa), (mb, fb_) = a, b
-        for k in ("cut_feature", "cut_bin", "gain", "leaf"):
+        assert ("inner" in ma) == (mode != "plain") == ("inner" in mb)
+        for k in ("cut_feature", "cut_bin", "gain", "leaf") + (("inner",) if "inner" in ma else ()):
             assert np.array_equal(ma[k], mb[k]), k
         assert ma["f0"] == mb["f0"]
         assert np.array_equal(fa, fb_)
