@@ -135,7 +135,10 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
  * event at the node whose cut feature has code 255 and adds that node's
  * weight.  xb: device uint8 [d][ldb] with d >= the model's feature count
  * (else FBDT_E_SHAPE); prob: device float32 [n] (output); score: optional
- * device float64 [n] (output).  Stream-ordered.
+ * device float64 [n] (output).  Stream-ordered, except that the first call
+ * for a model on a device (or launch shape) uploads the model's arrays
+ * with a synchronous copy and allocates their device copy, which the model
+ * owns until fbdt_model_free.
  */
 int fbdt_apply(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
                float *prob, double *score, void *stream);
