@@ -344,9 +344,22 @@ def is_near_tie(best_gain: float, other_gain: float, parent_gini: float,
     return best_gain - other_gain <= rtol * abs(best_gain) + noise * abs(parent_gini)
 
 
+def _near_tie_candidates(H, g, best, parent, k):
+    """Every (feature, cut, gain) of node k that ``is_near_tie`` admits beside
+    the best, leaving out cuts c >= 2 whose bin c - 1 is empty in the node
+    (they make the same partition as cut c - 1, whose gain they share)."""
+    nc = g.shape[2]
+    # bin c - 1 of cut c (column c - 1 of g) empty in both classes
+    empty = (H[k, :, :nc, 0] == 0.0) & (H[k, :, :nc, 1] == 0.0)
+    empty[:, 0] = False                       # cut 1 is never a repeat
+    near = is_near_tie(float(best[k]), g[k], float(parent[k])) & ~empty
+    return [(int(j), int(c0) + 1, float(g[k, j, c0])) for j, c0 in zip(*np.nonzero(near))]
+
+
 def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
         seed: int, n_bins: int, reference: Model | None = None, tie_log: TieLog | None = None,
-        trace: list | None = None, final_score: bool = False):
+        trace: list | None = None, final_score: bool = False, start=None,
+        near_ties: list | None = None):
     """Stochastic gradient-boosted trees on binned features (sections 1.1-1.4, 2.1).
 
     ``reference`` (optional) holds another implementation's cuts.  Where that
@@ -356,6 +369,12 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
     genuine ties; any other difference is recorded as rejected and this
     function keeps its own cut.  ``trace`` (optional list) receives one dict
     per layer with the histogram and chosen cuts.
+    ``start`` (optional) = (t0, F): resume the boosting loop at tree t0 with
+    the scores F that trees 0..t0-1 left (e.g. ``apply`` of those trees on
+    the same events, which reproduces the loop's F exactly); the model's rows
+    of the trees before t0 stay zero.  ``near_ties`` (optional list) receives,
+    for every node whose near-tie set holds more than its best cut, a tuple
+    (tree, heap node, [(feature, cut, gain), ...]) of that set.
     Returns the Model, and the final score F when ``final_score``.
     """
     xb = np.asarray(xb)
@@ -366,6 +385,9 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
     n_inner = (1 << depth) - 1
     f0 = initial_score(y, v)
     F = np.full(n, f0)
+    t_first = 0
+    if start is not None:
+        t_first, F = int(start[0]), np.array(start[1], dtype=np.float64)
     cut_feature = np.zeros((n_trees, n_inner), np.uint8)
     cut_bin = np.zeros((n_trees, n_inner), np.uint8)
     gain_out = np.zeros((n_trees, n_inner))
@@ -373,7 +395,7 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
     # missing values (section 4.2): NaN codes in data binned with B <= 255
     missing = missing_allowed(n_bins) and bool((xb == MISSING).any())
     inner_out = np.zeros((n_trees, (1 << depth) - 1)) if missing else None
-    for t in range(n_trees):
+    for t in range(t_first, n_trees):
         mask = subsample_mask(seed, t, n, subsample)
         yt = pseudo_response(y, F)
         w = histogram_weights(y, v, yt, mask)
@@ -384,6 +406,12 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
             g = split_gains(S, Bk)
             feat, cut, best = best_cuts(g)
             lo = (1 << layer) - 1
+            if near_ties is not None:
+                parent = gini(S[:, 0, n_bins], Bk[:, 0, n_bins])
+                for k in range(1 << layer):
+                    cands = _near_tie_candidates(H, g, best, parent, k)
+                    if len(cands) > 1:
+                        near_ties.append((t, (1 << layer) + k, cands))
             if reference is not None:
                 parent = gini(S[:, 0, n_bins], Bk[:, 0, n_bins])
                 for k in range(1 << layer):

@@ -14,13 +14,58 @@ from tests.golden_io import read_fixture
 
 
 # ---------------------------------------------------------------- SplitMix64
+_SM64_1234567 = [6457827717110365317, 3203168211198807973, 9817491932198370423,
+                 4593380528125082431, 16408922859458223821]
+
+
 def test_splitmix64_published_outputs():
     # Reference outputs of SplitMix64 (Steele, Lea & Flood 2014) as published
     # with the reference C implementation: seed 0 and seed 1234567.
     assert int(O.splitmix64(0, [0])[0]) == 0xE220A8397B1DCDAF
     got = [int(z) for z in O.splitmix64(1234567, np.arange(5))]
-    assert got == [6457827717110365317, 3203168211198807973, 9817491932198370423,
-                   4593380528125082431, 16408922859458223821]
+    assert got == _SM64_1234567
+
+
+def _u_by_hand(out: int) -> float:
+    # the top 53 bits of a published output, as an exact integer times 2^-53
+    return float(out >> 11) * 2.0 ** -53
+
+
+def test_subsample_mask_pins_the_53_bit_mapping_and_counter_layout():
+    """The reading of section 1.4: event i of tree t is sampled iff
+    u(t N + i) < alpha, with u the top 53 bits of SplitMix64 output number
+    t N + i over 2^53.  Derived by hand from the published outputs for seed
+    1234567 (outputs 0..4): alpha just above each u samples the event, alpha
+    equal to it or just below does not.  Fails for the low 53 bits, for a
+    rounding of the top bits, and for an i T + t or i + t counter."""
+    u = [_u_by_hand(o) for o in _SM64_1234567]
+    assert np.array_equal(O.uniform53(1234567, np.arange(5)), np.array(u))
+    seed = 1234567
+
+    def above(x):
+        return float(np.nextafter(x, 2.0))
+
+    def below(x):
+        return float(np.nextafter(x, -1.0))
+
+    # one event per tree: tree t reads output t
+    for t in range(5):
+        assert bool(O.subsample_mask(seed, t, 1, above(u[t]))[0])
+        assert not bool(O.subsample_mask(seed, t, 1, u[t])[0])
+        assert not bool(O.subsample_mask(seed, t, 1, below(u[t]))[0])
+    # five events of tree 0: event i reads output i
+    for i in range(5):
+        m_hi = O.subsample_mask(seed, 0, 5, above(u[i]))
+        m_at = O.subsample_mask(seed, 0, 5, u[i])
+        assert m_hi.tolist() == [u[k] < above(u[i]) for k in range(5)]
+        assert m_at.tolist() == [u[k] < u[i] for k in range(5)]
+        assert bool(m_hi[i]) and not bool(m_at[i])
+    # tree 1 of two events reads outputs 2 and 3; tree 2 of one event output 2
+    for a in sorted(u):
+        assert O.subsample_mask(seed, 1, 2, above(a)).tolist() == [u[2] <= a, u[3] <= a]
+        assert O.subsample_mask(seed, 2, 1, above(a)).tolist() == [u[2] <= a]
+    # the published outputs differ from their low-53-bit images here
+    assert any(float(o & ((1 << 53) - 1)) * 2.0 ** -53 != x for o, x in zip(_SM64_1234567, u))
 
 
 def test_subsample_mask_statistics():
@@ -540,6 +585,55 @@ def test_apply_reproduces_fit_score():
     m, F = _fit_small(xb, y, v, T=8)
     _, Fa = O.apply(m, xb)
     assert np.array_equal(F, Fa)
+
+
+def test_resume_from_applied_scores_reproduces_later_trees():
+    """Resuming the loop at tree t0 with the scores that apply gives for
+    trees 0..t0-1 (equal to the loop's own, pinned above) fits the same later
+    trees and final score: the sub-sample depends on the tree index only."""
+    xb, y, v = _small_problem()
+    m, F = _fit_small(xb, y, v, T=8)
+    for t0 in (1, 5):
+        head = O.Model(m.depth, m.n_bins, m.n_features, m.f0, m.cut_feature[:t0],
+                       m.cut_bin[:t0], m.gain[:t0], m.leaf[:t0])
+        _, Ft = O.apply(head, xb)
+        m2, F2 = O.fit(xb, y, v, m.depth, 8, 0.1, 0.5, 3, m.n_bins, final_score=True,
+                       start=(t0, Ft))
+        assert np.array_equal(m2.cut_feature[t0:], m.cut_feature[t0:])
+        assert np.array_equal(m2.cut_bin[t0:], m.cut_bin[t0:])
+        assert np.array_equal(m2.leaf[t0:], m.leaf[t0:])
+        assert not m2.leaf[:t0].any()
+        assert np.array_equal(F2, F)
+
+
+def test_near_tie_sets_on_the_xor_table():
+    """Table 3 (section 4.3): at the root both features have gain 0, so the
+    root's near-tie set holds both cuts; each layer-2 node has one best cut
+    (gain 0.5 against 0)."""
+    rows, _ = read_fixture("xor_table3.txt")
+    rows = np.array(rows)
+    xb = rows[:, :2].T.astype(np.uint8)
+    y = np.where(rows[:, 2] > 0, 1, -1).astype(np.int8)
+    near = []
+    O.fit(xb, y, np.ones(4, np.float32), depth=2, n_trees=1, shrinkage=1.0, subsample=1.0,
+          seed=0, n_bins=2, near_ties=near)
+    assert len(near) == 1
+    t, node, cands = near[0]
+    assert (t, node) == (0, 1)
+    assert sorted((f, c) for f, c, _ in cands) == [(0, 1), (1, 1)]
+    assert all(g == 0.0 for _, _, g in cands)
+
+
+def test_near_tie_sets_leave_out_repeated_partitions():
+    """A feature with an empty bin: cut c whose bin c - 1 is empty makes the
+    partition of cut c - 1 and is not a separate candidate."""
+    xb = np.array([[0, 0, 2, 2, 3, 3]], np.uint8)      # bin 1 empty: cuts 1 and 2 alike
+    y = np.array([-1, -1, 1, 1, 1, -1], np.int8)
+    near = []
+    m = O.fit(xb, y, np.ones(6, np.float32), depth=1, n_trees=1, shrinkage=1.0, subsample=1.0,
+              seed=0, n_bins=4, near_ties=near)
+    assert (int(m.cut_feature[0, 0]), int(m.cut_bin[0, 0])) == (0, 1)
+    assert near == []
 
 
 def test_model_invariant_under_monotone_feature_transform():
