@@ -242,6 +242,20 @@ int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bin
                    uint8_t *cut_feature, uint8_t *cut_bin, double *gain, void *stream);
 
 /*
+ * fbdt_best_cuts for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same result, bit for bit, from the same kernels, but the candidate
+ * cuts live in a fixed device array of the library (192 KiB per device, held
+ * until the process ends) instead of its allocated scratch.  The call makes
+ * no allocation and does not synchronise (stream-ordered).  Limit: n_nodes *
+ * d <= 16384, which n_nodes <= 64 and d <= 255 always meet.  Every call on a
+ * device shares that device's array: calls that overlap on one device (other
+ * streams, other threads) race and must be ordered by the caller.
+ */
+int fbdt_best_cuts_noalloc(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bins,
+                           uint8_t *cut_feature, uint8_t *cut_bin, double *gain, void *stream);
+
+/*
  * Route every event one layer down (section 1.1): node <- 2 node +
  * [xb[f][i] >= c] with (f, c) the cut of its node.  node: device uint8 [n],
  * updated in place (ids of `layer` on entry); cut_feature, cut_bin: device

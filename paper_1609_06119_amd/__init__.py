@@ -9,6 +9,7 @@ from .api import (  # noqa: F401
     apply,
     apply_float,
     best_cuts,
+    best_cuts_noalloc,
     bin,
     bin_transform,
     event_importance,

@@ -26,7 +26,8 @@ EXPORTED = (
     "fbdt_bin", "fbdt_bin_transform", "fbdt_fit", "fbdt_apply", "fbdt_apply_float",
     "fbdt_model_export", "fbdt_model_import", "fbdt_model_set_boundaries", "fbdt_model_free",
     "fbdt_last_error", "fbdt_tree_weights", "fbdt_feature_importance", "fbdt_event_importance",
-    "fbdt_histogram", "fbdt_best_cuts", "fbdt_route", "fbdt_leaf_values",
+    "fbdt_histogram", "fbdt_best_cuts", "fbdt_best_cuts_noalloc", "fbdt_route",
+    "fbdt_leaf_values",
     "fbdt_timing_enable", "fbdt_timing_read", "fbdt_set_option",
 )
 
@@ -78,6 +79,7 @@ def _declare(lib):
         "fbdt_tree_weights": (C.c_int, [P, P, P, I64, C.c_uint64, I32, C.c_double, P, P]),
         "fbdt_histogram": (C.c_int, [P, I64, I32, I64, I32, P, P, I32, P, P]),
         "fbdt_best_cuts": (C.c_int, [P, I32, I32, I32, P, P, P, P]),
+        "fbdt_best_cuts_noalloc": (C.c_int, [P, I32, I32, I32, P, P, P, P]),
         "fbdt_route": (C.c_int, [P, I64, I32, I64, P, P, P, I32, P]),
         "fbdt_leaf_values": (C.c_int, [P, P, P, P, I64, I32, C.c_uint64, I32, C.c_double,
                                        C.c_double, P, P]),

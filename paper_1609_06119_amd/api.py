@@ -16,8 +16,8 @@ import torch
 from ._lib import FitParams, FbdtError, KERNEL_KINDS, ModelView, check, lib
 
 __all__ = ["Codes", "Model", "bin", "bin_transform", "fit", "apply", "tree_weights",
-           "histogram", "best_cuts", "route", "leaf_values", "timing_enable", "timing_read",
-           "set_option", "FbdtError", "padded_stride"]
+           "histogram", "best_cuts", "best_cuts_noalloc", "route", "leaf_values",
+           "timing_enable", "timing_read", "set_option", "FbdtError", "padded_stride"]
 
 
 def padded_stride(n: int) -> int:
@@ -312,6 +312,22 @@ def best_cuts(hist: torch.Tensor):
     check("fbdt_best_cuts", lib().fbdt_best_cuts(_ptr(hist), n_nodes, d, n_bins, _ptr(f),
                                                  _ptr(c), _ptr(g), _stream()))
     return f, c, g
+
+
+def best_cuts_noalloc(hist: torch.Tensor, cut_feature: torch.Tensor, cut_bin: torch.Tensor,
+                      gain: torch.Tensor):
+    """fbdt_best_cuts_noalloc into caller-allocated outputs (uint8, uint8,
+    float64, one entry per node); stream-ordered, allocates nothing."""
+    _need(hist, torch.float64, "hist")
+    n_nodes, d, n_bins, two = hist.shape
+    if two != 2:
+        raise ValueError("hist must be [nodes][d][B][2]")
+    _need(cut_feature, torch.uint8, "cut_feature", n_nodes)
+    _need(cut_bin, torch.uint8, "cut_bin", n_nodes)
+    _need(gain, torch.float64, "gain", n_nodes)
+    check("fbdt_best_cuts_noalloc",
+          lib().fbdt_best_cuts_noalloc(_ptr(hist), n_nodes, d, n_bins, _ptr(cut_feature),
+                                       _ptr(cut_bin), _ptr(gain), _stream()))
 
 
 def route(codes: Codes, node: torch.Tensor, cut_feature: torch.Tensor, cut_bin: torch.Tensor,

@@ -69,9 +69,24 @@ int fail(int code, const char *fmt, ...) {
             return fail(FBDT_E_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));   \
     } while (0)
 
+// Scratch of fbdt_best_cuts_noalloc, the entry point that allocates nothing:
+// the candidate cut of every (node, feature) of a call, float64 gains
+// [n_nodes][d] then int32 cut bins [n_nodes][d] from byte offset
+// kNoAllocGainBytes.  A file-scope device array, so each device holds its
+// own copy for the life of the process.  In host code the name `scratch`
+// is a host-side stand-in: kernels and copies take the device address that
+// hipGetSymbolAddress returned for the current device (DeviceInfo::scratch).
+constexpr size_t kNoAllocCandidates = 64 * 256;
+constexpr size_t kNoAllocGainBytes = kNoAllocCandidates * sizeof(double);
+constexpr size_t kNoAllocScratchBytes = kNoAllocGainBytes + kNoAllocCandidates * sizeof(int32_t);
+static_assert(kNoAllocGainBytes % 256 == 0, "the cut array starts 256-byte aligned");
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 struct DeviceInfo {
     int cu_count = 0;
     size_t max_lds = 0;
+    void *scratch = nullptr;                  // device address of `scratch` on this device
+    hipError_t scratch_status = hipSuccess;   // hipGetSymbolAddress's result
 };
 
 std::mutex g_dev_mu;
@@ -86,6 +101,11 @@ int device_info(int dev, DeviceInfo *out) {
         HIP_TRY(hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev));
         HIP_TRY(hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
         HIP_TRY(prepare_kernels((size_t)lds));
+        // the no-allocation scratch of this device (dev is the current
+        // device here: callers pass the id hipGetDevice returned)
+        void *sp = nullptr;
+        di.scratch_status = hipGetSymbolAddress(&sp, HIP_SYMBOL(scratch));
+        di.scratch = di.scratch_status == hipSuccess ? sp : nullptr;
         di.cu_count = cu;
         di.max_lds = (size_t)lds;
     }
@@ -1264,6 +1284,34 @@ int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bin
     HIP_TRY(launch_select_cuts(cg, cc, n_nodes, d, 1, cut_feature, cut_bin, gain, s));
     tm.done();
     HIP_TRY(hipStreamSynchronize(s));
+    return FBDT_OK;
+}
+
+int fbdt_best_cuts_noalloc(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bins,
+                           uint8_t *cut_feature, uint8_t *cut_bin, double *gain, void *stream) {
+    int rc;
+    if (!hist || !cut_feature || !cut_bin || !gain) return fail(FBDT_E_INVAL, "NULL argument");
+    if (n_nodes < 1 || n_nodes > 64) return fail(FBDT_E_INVAL, "n_nodes not in [1, 64]");
+    if (d < 1 || d > 255) return fail(FBDT_E_INVAL, "d not in [1, 255]");
+    if ((rc = check_bins(n_bins))) return rc;
+    if ((reinterpret_cast<uintptr_t>(hist) & 15u) != 0)
+        return fail(FBDT_E_INVAL, "hist must be 16-byte aligned");
+    if ((size_t)n_nodes * (size_t)d > kNoAllocCandidates)
+        return fail(FBDT_E_INVAL, "%d nodes x %d features exceed the %zu candidates of the "
+                    "no-allocation scratch", n_nodes, d, kNoAllocCandidates);
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    if (!di.scratch)
+        return fail(FBDT_E_DEVICE, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev,
+                    hipGetErrorString(di.scratch_status));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // every candidate entry [node][feature] is written before it is read:
+    // nothing left in the scratch by an earlier call needs clearing
+    double *cg = static_cast<double *>(di.scratch);
+    int *cc = reinterpret_cast<int *>(static_cast<char *>(di.scratch) + kNoAllocGainBytes);
+    HIP_TRY(launch_best_cuts_f64(hist, n_nodes, d, n_bins, cg, cc, s));
+    HIP_TRY(launch_select_cuts(cg, cc, n_nodes, d, 1, cut_feature, cut_bin, gain, s));
     return FBDT_OK;
 }
 
