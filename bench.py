@@ -70,6 +70,8 @@ def parse():
                     help="also time negative weights, missing values and importance (1/0)")
     ap.add_argument("--fit-workloads", default="3,4",
                     help="larger fit workloads also timed and reported (comma list, '' for none)")
+    ap.add_argument("--phases", type=int, default=1,
+                    help="histogram phase timeline and reference passes (1/0)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this size on the device three "
                          "times (reference kernel for hardware byte counters)")
@@ -135,6 +137,82 @@ def measure_fit_workload(cfg, fb, torch):
             "route_launches": rl,
             "route_mean_launch_us": rms * 1e3 / rl if rl else None,
             "setup_s": round(time.time() - t0, 1)}
+
+
+def measure_hist_phases(fb, torch, codes, y, spec):
+    """Where a histogram launch of the bench workload spends its time.
+
+    One fit with the library's phase timeline on: every workgroup of every
+    histogram launch stamps the device's constant-rate clock at entry, once
+    the parents' cuts are in LDS, after its first step of events is added,
+    after every add and after its partial rows are written.  Per layer, the
+    stamps relative to the launch's first entry are averaged over the
+    workgroups and then over the trees; "last_*" is the latest workgroup.
+    Beside it, the reference passes on the same launch shape (empty
+    workgroups; workgroups that only read what the pass reads), timed with
+    HIP events like the histogram launches, with the histogram launches of
+    the same layer timed the same way."""
+    import numpy as np
+    B, D, T = spec.n_bins, spec.depth, spec.n_trees
+    fb.set_option("hist_timeline", 1)
+    try:
+        fb.fit(codes, y, B, D, T, spec.shrinkage, spec.subsample, spec.fit_seed)
+        torch.cuda.synchronize()
+        st, blocks, rate_khz = fb.hist_timeline()
+    finally:
+        fb.set_option("hist_timeline", 0)
+    us = 1e3 / rate_khz
+    # stamp columns: entry, cuts in LDS, first step added, adds done, rows
+    # written, last wavefront's entry, LDS cleared (wavefront 0)
+    cols = {"entry": 0, "last_wave_entry": 5, "lds_cleared": 6, "table": 1, "first_step": 2,
+            "adds_done": 3, "rows_written": 4}
+    layers = {}
+    for layer in range(D):
+        acc = {k: [] for k in list(cols) + ["last_entry", "last_rows_written"]}
+        for t in range(T):
+            rows = st[t * D + layer, :blocks[t * D + layer]].astype(np.int64)
+            rows = rows[rows[:, 0] != 0]
+            t0 = rows[:, 0].min()
+            rel = (rows - t0) * us
+            for k, i in cols.items():
+                col = rel[:, i][rows[:, i] != 0]
+                acc[k].append(col.mean())
+            acc["last_entry"].append(rel[:, 0].max())
+            acc["last_rows_written"].append(rel[:, 4].max())
+        layers[f"layer{layer}"] = {k + "_us": float(np.mean(v)) for k, v in acc.items()}
+        layers[f"layer{layer}"]["workgroups"] = int(blocks[layer])
+    # reference passes on the launch shapes of layer 0 (no node ids) and of
+    # the last layer (node ids read), against the histogram launches
+    n = codes.n
+    npad = (n + 7) // 8 * 8
+    w = torch.zeros(npad, dtype=torch.float32, device="cuda")
+    node = torch.zeros(npad, dtype=torch.uint8, device="cuda")
+    refs = {}
+    for layer in (0, D - 1):
+        out = {}
+        for kind, name in ((0, "empty"), (1, "read"), (2, "read_up_front")):
+            for _ in range(3):
+                fb.reference_pass(kind, codes, B, layer, w, node if layer >= 1 else None)
+            torch.cuda.synchronize()
+            fb.timing_enable(("reference",))
+            for _ in range(50):
+                fb.reference_pass(kind, codes, B, layer, w, node if layer >= 1 else None)
+            torch.cuda.synchronize()
+            k, ms, by = fb.timing_read("reference")
+            fb.timing_enable(())
+            out[f"{name}_mean_launch_us"] = ms * 1e3 / k
+            if kind >= 1:
+                out[f"{name}_bytes_per_launch"] = by / k
+                out[f"{name}_gbs"] = by / (ms / 1e3) / 1e9
+        refs[f"layer{layer}"] = out
+    fb.timing_enable(("histogram",))
+    fb.fit(codes, y, B, D, T, spec.shrinkage, spec.subsample, spec.fit_seed)
+    torch.cuda.synchronize()
+    hl, hms, _ = fb.timing_read("histogram")
+    fb.timing_enable(())
+    return {"clock_khz": rate_khz, "phases": layers, "reference": refs,
+            "hist_mean_launch_us_same_timing": hms * 1e3 / hl,
+            "note": "phase stamps in microseconds after the launch's first workgroup entry"}
 
 
 def measure_section4(fb, torch):
@@ -343,6 +421,10 @@ def main():
     achieved = hist_avg_bytes / (hist_avg_ms / 1e3) / 1e9
     apply_events_per_s = n * a_launches / (a_ms / 1e3) if a_ms > 0 else None
 
+    phases = measure_hist_phases(fb, torch, codes, y, spec) if args.phases else None
+    if phases:
+        print(f"# histogram phases: {json.dumps(phases)}", file=sys.stderr, flush=True)
+
     # CPU oracle on a bounded sample of the same workload (first trees, all events)
     from oracle import fbdt_oracle as O
     _, xb = O.bin_features(ds["x"], B)
@@ -410,6 +492,7 @@ def main():
             "mean_launch_us": hist_avg_ms * 1e3,
             "algorithmic_bytes_per_launch": hist_avg_bytes,
         },
+        "hist_phases": phases,
         "apply": apply_out,
         "fit_workloads": fits,
         "section4": section4,

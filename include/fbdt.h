@@ -288,7 +288,8 @@ enum fbdt_kernel_kind {
     FBDT_K_ENCODE = 5,    /* float -> bin code                                */
     FBDT_K_ROUTE = 6,     /* routing of a layer as a pass of its own (layers  */
                           /* with more than 4 parents; fbdt_route)            */
-    FBDT_K_COUNT = 7
+    FBDT_K_REFERENCE = 7, /* fbdt_reference_pass                              */
+    FBDT_K_COUNT = 8
 };
 
 /*
@@ -315,9 +316,44 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
  * calls with the same set; up to 4 graphs per device are kept, and growing the
  * device workspace drops them.  0 launches every kernel one by one.  Graphs
  * are not used while any fit kernel kind is being timed.
+ * "hist_timeline" (default 0): 1 makes fbdt_fit record the phase timeline
+ * of every histogram launch (see fbdt_hist_timeline); fits then launch
+ * kernel by kernel.
  * Returns FBDT_E_INVAL for an unknown name.
  */
 int fbdt_set_option(const char *name, int64_t value);
+
+/*
+ * Phase timeline of the histogram launches of the last fbdt_fit made while
+ * option "hist_timeline" was 1 (measurement of the layer pass of sections
+ * 1.1 and 2.1).  Launch k = tree * D + layer ran blocks[k] workgroups;
+ * workgroup b of it wrote stamps[(k * max_blocks + b) * 5 + p], the value
+ * of the device's constant-rate clock (rate_khz ticks per millisecond) at
+ * phase p: 0 entry, 1 the parents' cuts in LDS, 2 first step of events
+ * added (wavefront 0), 3 every add done, 4 partial rows written (wavefront
+ * 0).  A row is 0 for workgroups beyond the launch's work and phase 2 is 0
+ * for a workgroup without events.  The arrays belong to the library and
+ * stay valid until the next such fit (or the end of the process); launches
+ * = 0 if there was none.
+ */
+int fbdt_hist_timeline(int64_t *launches, int32_t *max_blocks, const int32_t **blocks,
+                       const uint64_t **stamps, int64_t *rate_khz);
+
+/*
+ * Reference passes for the histogram pass's roofline (measurement of the
+ * layer pass of sections 1.1 and 2.1): launched with the grid, workgroup
+ * size and dynamic LDS that fbdt_fit uses for `layer` of n events x d
+ * features at n_bins, kind 0 runs workgroups that return at once (launch
+ * cost) and kind 1 workgroups that read what the pass reads (the weights,
+ * the node ids if node is not NULL, and the codes of their features over
+ * their event chunk) and write nothing.  xb as for fbdt_histogram; w
+ * (float32) and node (uint8, or NULL) on the device, holding round_up(n, 8)
+ * elements, 16-byte aligned.  Timed as FBDT_K_REFERENCE with the bytes read.
+ * Stream-ordered.
+ */
+int fbdt_reference_pass(int32_t kind, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
+                        int32_t n_bins, int32_t layer, const uint8_t *node, const float *w,
+                        void *stream);
 
 #ifdef __cplusplus
 }

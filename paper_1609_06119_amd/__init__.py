@@ -15,9 +15,11 @@ from .api import (  # noqa: F401
     event_importance,
     feature_importance,
     fit,
+    hist_timeline,
     histogram,
     leaf_values,
     padded_stride,
+    reference_pass,
     route,
     set_option,
     timing_enable,

@@ -20,7 +20,7 @@ STATUS = {
     -6: "FBDT_E_DEVICE",
 }
 KERNEL_KINDS = {"histogram": 0, "best_cuts": 1, "tree_prep": 2, "leaf": 3, "apply": 4,
-                "encode": 5, "route": 6}
+                "encode": 5, "route": 6, "reference": 7}
 
 EXPORTED = (
     "fbdt_bin", "fbdt_bin_transform", "fbdt_fit", "fbdt_apply", "fbdt_apply_float",
@@ -28,7 +28,8 @@ EXPORTED = (
     "fbdt_last_error", "fbdt_tree_weights", "fbdt_feature_importance", "fbdt_event_importance",
     "fbdt_histogram", "fbdt_best_cuts", "fbdt_best_cuts_noalloc", "fbdt_route",
     "fbdt_leaf_values",
-    "fbdt_timing_enable", "fbdt_timing_read", "fbdt_set_option",
+    "fbdt_timing_enable", "fbdt_timing_read", "fbdt_set_option", "fbdt_hist_timeline",
+    "fbdt_reference_pass",
 )
 
 
@@ -87,6 +88,10 @@ def _declare(lib):
         "fbdt_timing_read": (C.c_int, [I32, C.POINTER(I64), C.POINTER(C.c_double),
                                        C.POINTER(C.c_double)]),
         "fbdt_set_option": (C.c_int, [C.c_char_p, I64]),
+        "fbdt_hist_timeline": (C.c_int, [C.POINTER(I64), C.POINTER(I32),
+                                         C.POINTER(C.POINTER(I32)),
+                                         C.POINTER(C.POINTER(C.c_uint64)), C.POINTER(I64)]),
+        "fbdt_reference_pass": (C.c_int, [I32, P, I64, I32, I64, I32, I32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)

@@ -17,7 +17,8 @@ from ._lib import FitParams, FbdtError, KERNEL_KINDS, ModelView, check, lib
 
 __all__ = ["Codes", "Model", "bin", "bin_transform", "fit", "apply", "tree_weights",
            "histogram", "best_cuts", "best_cuts_noalloc", "route", "leaf_values",
-           "timing_enable", "timing_read", "set_option", "FbdtError", "padded_stride"]
+           "timing_enable", "timing_read", "set_option", "hist_timeline", "reference_pass",
+           "FbdtError", "padded_stride"]
 
 
 def padded_stride(n: int) -> int:
@@ -374,6 +375,38 @@ def timing_read(kind: str):
     check("fbdt_timing_read", lib().fbdt_timing_read(KERNEL_KINDS[kind], C.byref(k),
                                                      C.byref(ms), C.byref(by)))
     return int(k.value), float(ms.value), float(by.value)
+
+
+def hist_timeline():
+    """Phase timeline of the histogram launches of the last fit made with
+    option hist_timeline = 1: (stamps uint64 [launches][max_blocks][8],
+    blocks int32 [launches], clock rate in kHz); None if there was none."""
+    launches, mb, rate = C.c_int64(), C.c_int32(), C.c_int64()
+    blocks = C.POINTER(C.c_int32)()
+    stamps = C.POINTER(C.c_uint64)()
+    check("fbdt_hist_timeline", lib().fbdt_hist_timeline(C.byref(launches), C.byref(mb),
+                                                          C.byref(blocks), C.byref(stamps),
+                                                          C.byref(rate)))
+    if launches.value == 0:
+        return None
+    k, m = launches.value, mb.value
+    st = np.ctypeslib.as_array(stamps, shape=(k * m * 8,)).reshape(k, m, 8).copy()
+    bl = np.ctypeslib.as_array(blocks, shape=(k,)).copy()
+    return st, bl, rate.value
+
+
+def reference_pass(kind: int, codes: Codes, n_bins: int, layer: int, w: torch.Tensor,
+                   node: torch.Tensor | None = None):
+    """fbdt_reference_pass: kind 0 (empty) or 1 (read only) on the histogram
+    pass's launch shape for `layer`; w float32 and node uint8 padded to a
+    multiple of 8 events."""
+    npad = (codes.n + 7) // 8 * 8
+    _need(w, torch.float32, "w", npad)
+    if node is not None:
+        _need(node, torch.uint8, "node", npad)
+    check("fbdt_reference_pass",
+          lib().fbdt_reference_pass(int(kind), _ptr(codes.data), codes.n, codes.d, codes.ldb,
+                                    int(n_bins), int(layer), _ptr(node), _ptr(w), _stream()))
 
 
 def set_option(name: str, value: int):

@@ -22,6 +22,10 @@ HIPCC_FLAGS = [
     # evaluated as written (no fused multiply-add contraction)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-ffp-contract=off",
+    # kernel arguments preloaded into scalar registers at wave launch (the
+    # first 16 dwords), so that a kernel's first loads need no scalar load
+    # of its argument segment
+    "-mllvm", "-amdgpu-kernarg-preload-count=16",
     "-Wall",
     "-Wno-unused-command-line-argument",
 ]

@@ -115,7 +115,19 @@ int device_info(int dev, DeviceInfo *out) {
 
 // ---- options --------------------------------------------------------------
 std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0}, opt_hist_copies{0},
-    opt_apply_threads{0}, opt_fit_graphs{1};
+    opt_apply_threads{0}, opt_fit_graphs{1}, opt_hist_timeline{0};
+
+// Phase timeline of the histogram launches of the last fit made with option
+// hist_timeline (host copy): [launches][max_blocks][kTimelineStamps].
+struct Timeline {
+    std::mutex mu;
+    int64_t launches = 0;
+    int32_t max_blocks = 0;
+    int64_t rate_khz = 0;
+    std::vector<int32_t> blocks;          // grid of each launch
+    std::vector<uint64_t> stamps;
+};
+Timeline g_timeline;
 
 HistOverrides hist_overrides() {
     HistOverrides ov;
@@ -315,6 +327,8 @@ int fbdt_set_option(const char *name, int64_t value) {
         if (value != 0 && value != 1 && value != 2 && value != 4)
             return fail(FBDT_E_INVAL, "hist_copies must be 0, 1, 2 or 4");
         opt_hist_copies = value;
+    } else if (!strcmp(name, "hist_timeline")) {
+        opt_hist_timeline = value != 0;
     } else if (!strcmp(name, "fit_graphs")) {
         opt_fit_graphs = value != 0;
     } else if (!strcmp(name, "apply_threads")) {
@@ -569,8 +583,18 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.cut_bin, (size_t)T * nin);
     cv.add(&fb.gain, (size_t)T * nin);
     cv.add(&fb.leaf, (size_t)T * slots_max);
+    // phase timeline of every histogram launch (measurement option)
+    const bool timeline = opt_hist_timeline.load() != 0;
+    int tl_blocks = 0;
+    for (int mode = 0; mode < (may_miss ? 2 : 1); ++mode)
+        for (const HistShape &h : mode == 0 ? plans_sib : plans_both)
+            tl_blocks = std::max(tl_blocks, h.blocks);
+    const size_t tl_count = timeline ? (size_t)T * D * tl_blocks * kTimelineStamps : 0;
+    unsigned long long *tl = nullptr;
+    if (timeline) cv.add(&tl, tl_count);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
+    if (timeline) HIP_TRY(launch_fill_u32(tl, 0u, 2 * tl_count, s));
 
     HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
     HIP_TRY(launch_fill_u32(fb.small[0], 0u, 2 * small_elems, s));
@@ -658,7 +682,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                         own_route ? fb.node[l & 1] : l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
                         !own_route && l >= 1 ? fb.node[l & 1] : nullptr, fb.w, vsign,
                         own_route ? ParentCuts{} : pc, l, !own_route, scale, fb.partial,
-                        fb.small[gl & 1], fb.err, st));
+                        fb.small[gl & 1], fb.err, st,
+                        tl ? tl + (size_t)(t * D + l) * tl_blocks * kTimelineStamps : nullptr));
                     tm.done();
                 }
                 {
@@ -710,7 +735,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     };
     const int timed_kinds = (1 << FBDT_K_TREE_PREP) | (1 << FBDT_K_HISTOGRAM) |
                             (1 << FBDT_K_BEST_CUTS) | (1 << FBDT_K_LEAF) | (1 << FBDT_K_ROUTE);
-    if (opt_fit_graphs.load() && !(g_timing.load() & timed_kinds)) {
+    if (opt_fit_graphs.load() && !timeline && !(g_timing.load() & timed_kinds)) {
         const GraphKey key{xb, y, w, n, ldb, d, n_bins, D, T, scale, lblocks, eta, alpha, seed,
                            opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load(),
                            opt_hist_copies.load(), signed_w, missing};
@@ -786,6 +811,20 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
         return cleanup(fail(FBDT_E_DEVICE, "fit failed: %s", hipGetErrorString(se)));
     if (h_err & kErrBin) return cleanup(fail(FBDT_E_INVAL, "a bin code is >= n_bins"));
     if (h_err & kErrRoute) return cleanup(fail(FBDT_E_DEVICE, "internal routing error"));
+    if (timeline) {
+        int rate = 0;
+        HIP_TRY(hipDeviceGetAttribute(&rate, hipDeviceAttributeWallClockRate, dev));
+        std::lock_guard<std::mutex> tlk(g_timeline.mu);
+        g_timeline.stamps.resize(tl_count);
+        HIP_TRY(hipMemcpy(g_timeline.stamps.data(), tl, tl_count * sizeof(uint64_t),
+                          hipMemcpyDeviceToHost));
+        g_timeline.launches = (int64_t)T * D;
+        g_timeline.max_blocks = tl_blocks;
+        g_timeline.rate_khz = rate;
+        g_timeline.blocks.assign((size_t)T * D, 0);
+        for (int t = 0; t < T; ++t)
+            for (int l = 0; l < D; ++l) g_timeline.blocks[(size_t)t * D + l] = plans[l].blocks;
+    }
     m->missing = missing;
     m->leaf.resize((size_t)T * nleaf);
     if (missing) m->inner.resize((size_t)T * nin);
@@ -1284,6 +1323,49 @@ int fbdt_best_cuts(const double *hist, int32_t n_nodes, int32_t d, int32_t n_bin
     HIP_TRY(launch_select_cuts(cg, cc, n_nodes, d, 1, cut_feature, cut_bin, gain, s));
     tm.done();
     HIP_TRY(hipStreamSynchronize(s));
+    return FBDT_OK;
+}
+
+int fbdt_hist_timeline(int64_t *launches, int32_t *max_blocks, const int32_t **blocks,
+                       const uint64_t **stamps, int64_t *rate_khz) {
+    if (!launches || !max_blocks || !blocks || !stamps || !rate_khz)
+        return fail(FBDT_E_INVAL, "NULL argument");
+    std::lock_guard<std::mutex> lk(g_timeline.mu);
+    *launches = g_timeline.launches;
+    *max_blocks = g_timeline.max_blocks;
+    *blocks = g_timeline.blocks.empty() ? nullptr : g_timeline.blocks.data();
+    *stamps = g_timeline.stamps.empty() ? nullptr : g_timeline.stamps.data();
+    *rate_khz = g_timeline.rate_khz;
+    return FBDT_OK;
+}
+
+int fbdt_reference_pass(int32_t kind, const uint8_t *xb, int64_t n, int32_t d, int64_t ldb,
+                        int32_t n_bins, int32_t layer, const uint8_t *node, const float *w,
+                        void *stream) {
+    int rc;
+    if (kind < 0 || kind > 2) return fail(FBDT_E_INVAL, "reference kind %d not 0, 1 or 2", kind);
+    if ((rc = check_codes(xb, n, d, ldb)) || (rc = check_bins(n_bins))) return rc;
+    if (!w) return fail(FBDT_E_INVAL, "w is NULL");
+    if (!aligned16(w) || (node && !aligned16(node)))
+        return fail(FBDT_E_INVAL, "node and w must be 16-byte aligned");
+    if (layer < 0 || layer > 6) return fail(FBDT_E_INVAL, "layer %d not in [0, 6]", layer);
+    int dev;
+    DeviceInfo di;
+    if ((rc = current_device(&dev, &di))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const HistShape hs = plan_histogram(n, d, n_bins, layer, true, di.cu_count, di.max_lds,
+                                        hist_overrides());
+    Arena &a = g_arena[dev];
+    std::lock_guard<std::mutex> lk(a.mu);
+    Carver cv;
+    uint32_t *sink;
+    cv.add(&sink, (size_t)hs.blocks);
+    if ((rc = arena_reserve(a, cv.off))) return rc;
+    cv.assign(a.ptr);
+    const double bytes = kind == 0 ? 0.0 : (double)n * d + 4.0 * n + (node ? (double)n : 0.0);
+    Timed tm(FBDT_K_REFERENCE, s, bytes);
+    HIP_TRY(launch_hist_reference(kind, hs, xb, ldb, n, d, node, w, sink, s));
+    tm.done();
     return FBDT_OK;
 }
 

@@ -181,11 +181,21 @@ int histogram_scale(double total_weight_bound);
 // vsign (or null): [round_up(n, 8)] bytes, 1 where the
 // event's weight is negative; w then holds |w| with the class in the sign
 // bit and the pass adds -|w| for those events (two's complement fixed point).
+// tl (optional, measurement): kTimelineStamps clock values per workgroup of
+// the launch (hs.blocks rows), see fbdt_hist_timeline.
+constexpr int kTimelineStamps = 8;
 hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                             const float *w, const uint8_t *vsign, const ParentCuts &pc,
                             int layer, bool routed, int scale, uint64_t *partial, double *small,
-                            int *err, hipStream_t s);
+                            int *err, hipStream_t s, unsigned long long *tl = nullptr);
+
+// Reference passes of the histogram pass (measurement): the pass's grid,
+// workgroup size and LDS for shape hs; kind 0 returns at once, kind 1 reads
+// the weights, node ids (node may be null) and its features' codes.
+hipError_t launch_hist_reference(int kind, const HistShape &hs, const uint8_t *xb, int64_t ldb,
+                                 int64_t n, int d, const uint8_t *node, const float *w,
+                                 uint32_t *sink, hipStream_t s);
 
 // vs[i] = 1 where v[i] < 0 (i < n), else 0, for i < npad.
 hipError_t launch_sign_bytes(const float *v, int64_t n, int64_t npad, uint8_t *vs, hipStream_t s);

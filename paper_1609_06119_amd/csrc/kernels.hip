@@ -738,26 +738,44 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
 }
 
 template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
+// The arguments that the first loads need come first, so that they fit the
+// kernel arguments preloaded into scalar registers at wave launch (16
+// dwords): the code, weight and id arrays, the event ranges, and two packed
+// words, geo = d | G << 8 | NG << 16 | chunks per XCD << 24 and mode =
+// layer | sib << 3 | prefix << 4 | npg << 8 | cut slices << 16 | copies << 24.
 __global__ __launch_bounds__(1024) void hist_kernel(
-    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
-    const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
-    const float *__restrict__ w, const uint8_t *__restrict__ vsign,
-    const double *__restrict__ cand_gain,
-    const int *__restrict__ cand_cut, int cslices, uint8_t *__restrict__ rec_f,
-    uint8_t *__restrict__ rec_c, double *__restrict__ rec_g, int layer, bool sib, bool prefix,
-    int G, int npg, int NG,
-    int chunks, int64_t chunk_events, int64_t xcd_events, int scale, int copies,
-    int copy_stride, uint64_t *__restrict__ partial, double *__restrict__ small,
-    int *__restrict__ err) {
+    const uint8_t *__restrict__ xb, const float *__restrict__ w,
+    const uint8_t *__restrict__ node_in, int64_t ldb, int64_t n, int64_t chunk_events,
+    int64_t xcd_events, uint32_t geo, uint32_t mode, const double *__restrict__ cand_gain,
+    const int *__restrict__ cand_cut, int nbins, int scale, int copy_stride,
+    const uint8_t *__restrict__ vsign, uint8_t *__restrict__ node_out,
+    uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
+    uint64_t *__restrict__ partial, double *__restrict__ small, int *__restrict__ err,
+    unsigned long long *__restrict__ tl) {
+    const int d = (int)(geo & 0xffu), G = (int)((geo >> 8) & 0xffu);
+    const int NG = (int)((geo >> 16) & 0xffu), cpx = (int)(geo >> 24);
+    const int chunks = cpx * kXcds;
+    const int layer = (int)(mode & 7u);
+    const bool sib = ((mode >> 3) & 1u) != 0, prefix = ((mode >> 4) & 1u) != 0;
+    const int npg = (int)((mode >> 8) & 0xffu), cslices = (int)((mode >> 16) & 0xffu);
+    const int copies = (int)(mode >> 24);
     extern __shared__ uint64_t lds[];
     __shared__ uint8_t s_cf[64], s_cc[64];
+    // phase timeline (measurement, tl != null): the device's constant-rate
+    // clock at entry, cut table in LDS, first step added (wavefront 0), every
+    // add done and partial rows written (wavefront 0), one row of
+    // kTimelineStamps per workgroup
+    const bool stamp = tl != nullptr && threadIdx.x == 0;
+    const unsigned long long t_entry = stamp ? (unsigned long long)wall_clock64() : 0ull;
+    if (tl != nullptr && threadIdx.x == blockDim.x - kWave)   // the last wavefront's entry
+        tl[(size_t)blockIdx.x * kTimelineStamps + 5] = (unsigned long long)wall_clock64();
 
     // Consecutive work items (same event chunk, different feature groups) go
     // to the same XCD so that the chunk's node ids and weights are fetched
     // into that XCD's L2 once and re-read from there.
-    const int per_xcd = gridDim.x / kXcds;
-    const int q = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
     const int groups = G * NG;
+    const int per_xcd = cpx * groups;   // the grid is kXcds * cpx * groups workgroups
+    const int q = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
     if (q >= chunks * groups) return;
     const int p = q / groups;
     const int r = q - p * groups;
@@ -801,7 +819,6 @@ __global__ __launch_bounds__(1024) void hist_kernel(
 
     // chunk p is chunk k of XCD x's event range [x R, (x + 1) R) (the range
     // every per-event pass of the fit gives that XCD)
-    const int cpx = chunks / kXcds;
     const int64_t xlo = (int64_t)(p / cpx) * xcd_events;
     const int64_t start = xlo + (int64_t)(p % cpx) * chunk_events;
     const int64_t end = min(min(n, xlo + xcd_events), start + chunk_events);
@@ -826,6 +843,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         const int n16 = copies > 1 ? copies * copy_stride / 16 : lds_n / 2;
         for (int t = threadIdx.x; t < n16; t += blockDim.x) l4[t] = make_uint4(0u, 0u, 0u, 0u);
     }
+    if (stamp) tl[(size_t)blockIdx.x * kTimelineStamps + 6] = (unsigned long long)wall_clock64();
     if (ROUTED && layer >= 1) {
         // cut of parent k from its candidates; workgroup 0 records it in the model
         for (int k = wave; k < a.half; k += nwaves) {
@@ -849,6 +867,8 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         }
     }
     lds_barrier();
+    const unsigned long long t_table = stamp ? (unsigned long long)wall_clock64() : 0ull;
+    unsigned long long t_first = 0ull;
     uint32_t cut[4] = {0u, 0u, 0u, 0u};
     if (ROUTED && NP > 0 && layer >= 1) {
 #pragma unroll
@@ -865,6 +885,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
             const bool more_b = ib < end;
             hist_load<ROUTED, NP, FPG, SIGNED, MISS>(B, a, s_cf, more_b ? ib : ia, true);
             hist_add<ROUTED, NP, FPG, SIGNED, MISS>(A, a, lds_lane, writer, s_cf, s_cc, cut, ia, eflag);
+            if (stamp && t_first == 0ull) t_first = (unsigned long long)wall_clock64();
             if (!more_b) break;
             ia = ib + stride;
             const bool more_a = ia < end;
@@ -874,6 +895,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         }
     }
     lds_barrier();
+    const unsigned long long t_adds = stamp ? (unsigned long long)wall_clock64() : 0ull;
     if (copies > 1) {   // copy 0 += the others
         const int cs = copy_stride / 8;
         for (int t = threadIdx.x; t < lds_n; t += blockDim.x) {
@@ -919,6 +941,79 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         for (int t = lane; t < nbins; t += kWave) dst[t] = src[t];
     }
     if (eflag) atomicOr(err, eflag);
+    if (stamp) {
+        unsigned long long *row = tl + (size_t)blockIdx.x * kTimelineStamps;
+        row[0] = t_entry;
+        row[1] = t_table;
+        row[2] = t_first;
+        row[3] = t_adds;
+        row[4] = (unsigned long long)wall_clock64();
+    }
+}
+
+// Reference passes of the histogram pass's roofline (measurement only),
+// launched with the pass's own grid, workgroup size and dynamic LDS.  kind
+// 0: every workgroup returns at once (launch and teardown cost).  kind 1:
+// every workgroup reads what the pass reads for its (event chunk, feature
+// group), kHistE events per thread and step: the weights, the node ids (if
+// any) and the codes of its features, folded into an XOR that is stored only
+// if it equals a constant, so that the loads stay and nothing is written.
+__global__ __launch_bounds__(1024) void hist_reference_kernel(
+    int kind, const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int fpg,
+    const uint8_t *__restrict__ node, const float *__restrict__ w, int G, int NG, int chunks,
+    int64_t chunk_events, int64_t xcd_events, uint32_t *__restrict__ sink) {
+    if (kind == 0) return;
+    const int groups = G * NG;
+    const int cpx = chunks / kXcds;
+    const int per_xcd = cpx * groups;   // the grid is kXcds * cpx * groups workgroups
+    const int q = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (q >= chunks * groups) return;
+    const int p = q / groups;
+    const int g = (q - p * groups) % G;
+    const int64_t xlo = (int64_t)(p / cpx) * xcd_events;
+    const int64_t start = xlo + (int64_t)(p % cpx) * chunk_events;
+    const int64_t end = min(min(n, xlo + xcd_events), start + chunk_events);
+    const int64_t stride = (int64_t)kHistE * blockDim.x;
+    uint32_t acc = 0u;
+    if (kind == 2 && fpg <= 2) {
+        // up to 4 steps per thread, all loads issued before any is used
+        uint4 x[4], y[4];
+        uint2 nd[4], c0[4], c1[4];
+        if (end <= start) return;
+        const int64_t i0 = start + (int64_t)kHistE * threadIdx.x;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            // a whole step inside the chunk's padded range (start is a multiple of 8)
+            const int64_t i = min(i0 + k * stride, end - 1) / kHistE * kHistE;
+            x[k] = reinterpret_cast<const uint4 *>(w + i)[0];
+            y[k] = reinterpret_cast<const uint4 *>(w + i)[1];
+            nd[k] = node ? *reinterpret_cast<const uint2 *>(node + i) : make_uint2(0u, 0u);
+            c0[k] = *reinterpret_cast<const uint2 *>(xb + (int64_t)min(g * fpg, d - 1) * ldb + i);
+            c1[k] = *reinterpret_cast<const uint2 *>(xb + (int64_t)min(g * fpg + 1, d - 1) * ldb + i);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (i0 + k * stride < end)
+                acc ^= x[k].x ^ x[k].y ^ x[k].z ^ x[k].w ^ y[k].x ^ y[k].y ^ y[k].z ^ y[k].w ^
+                       nd[k].x ^ nd[k].y ^ c0[k].x ^ c0[k].y ^ c1[k].x ^ c1[k].y;
+        if (acc == 0x9E3779B9u) sink[blockIdx.x] = acc;
+        return;
+    }
+    for (int64_t i = start + (int64_t)kHistE * threadIdx.x; i < end; i += stride) {
+        const uint4 x = reinterpret_cast<const uint4 *>(w + i)[0];
+        const uint4 y = reinterpret_cast<const uint4 *>(w + i)[1];
+        acc ^= x.x ^ x.y ^ x.z ^ x.w ^ y.x ^ y.y ^ y.z ^ y.w;
+        if (node) {
+            const uint2 nd = *reinterpret_cast<const uint2 *>(node + i);
+            acc ^= nd.x ^ nd.y;
+        }
+        for (int ff = 0; ff < fpg; ++ff) {
+            const uint2 c = *reinterpret_cast<const uint2 *>(
+                xb + (int64_t)min(g * fpg + ff, d - 1) * ldb + i);
+            acc ^= c.x ^ c.y;
+        }
+    }
+    if (acc == 0x9E3779B9u) sink[blockIdx.x] = acc;
 }
 
 // Sum of the fixed-point chunk partials (exact) converted to float64, plus
@@ -2139,7 +2234,8 @@ hipError_t prepare_kernels(size_t max_lds) {
                             allow_lds(apply_float_kernel<5>, max_lds),
                             allow_lds(apply_float_kernel<6>, max_lds),
                             allow_lds(apply_float_kernel<7>, max_lds),
-                            allow_lds(importance_kernel, max_lds)};
+                            allow_lds(importance_kernel, max_lds),
+                            allow_lds(hist_reference_kernel, max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -2262,6 +2358,7 @@ HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, 
     int64_t c8 = chunks > 0 ? (chunks + kXcds - 1) / kXcds
                : c8_pick > 0 ? c8_pick : (int64_t)cu_count / kXcds / groups;
     if (chunks <= 0 && c8 > c8max) c8 = c8max;
+    if (c8 > 255) c8 = 255;   // the kernel takes chunks per XCD in 8 bits
     if (c8 < 1) c8 = 1;
     int64_t ce = (R + c8 - 1) / c8;
     ce = (ce + kHistE - 1) / kHistE * kHistE;
@@ -2299,13 +2396,22 @@ template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
 hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, int64_t n, int d,
                           int n_bins, const uint8_t *node_in, uint8_t *node_out, const float *w,
                           const uint8_t *vsign, const ParentCuts &pc, int layer, int scale,
-                          uint64_t *partial, double *small, int *err, hipStream_t s) {
+                          uint64_t *partial, double *small, int *err, unsigned long long *tl,
+                          hipStream_t s) {
+    const int cpx = hs.chunks / kXcds;
+    if (d > 255 || hs.feature_groups > 255 || hs.node_groups > 255 || cpx > 255 ||
+        hs.chunks != cpx * kXcds || hs.blocks != hs.chunks * hs.feature_groups * hs.node_groups ||
+        layer > 7 || hs.nodes_per_group > 255 || pc.slices > 255 || hs.copies > 255)
+        return hipErrorInvalidValue;
+    const uint32_t geo = (uint32_t)d | (uint32_t)hs.feature_groups << 8 |
+                         (uint32_t)hs.node_groups << 16 | (uint32_t)cpx << 24;
+    const uint32_t mode = (uint32_t)layer | (hs.sibling ? 8u : 0u) | (hs.prefix ? 16u : 0u) |
+                          (uint32_t)hs.nodes_per_group << 8 | (uint32_t)pc.slices << 16 |
+                          (uint32_t)hs.copies << 24;
     hist_kernel<ROUTED, NP, FPG, SIGNED, MISS><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
-        xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices,
-        pc.rec_f, pc.rec_c, pc.rec_g, layer, hs.sibling, hs.prefix, hs.feature_groups,
-        hs.nodes_per_group,
-        hs.node_groups, hs.chunks, hs.chunk_events, hs.xcd_events, scale, hs.copies,
-        hs.copy_stride, partial, small, err);
+        xb, w, node_in, ldb, n, hs.chunk_events, hs.xcd_events, geo, mode, pc.cand_gain,
+        pc.cand_cut, n_bins, scale, hs.copy_stride, vsign, node_out, pc.rec_f, pc.rec_c,
+        pc.rec_g, partial, small, err, tl);
     return hipGetLastError();
 }
 
@@ -2314,12 +2420,12 @@ hipError_t launch_hist_routed(const HistShape &hs, const uint8_t *xb, int64_t ld
                               int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                               const float *w, const uint8_t *vsign, const ParentCuts &pc,
                               int layer, int scale, uint64_t *partial, double *small, int *err,
-                              hipStream_t s) {
+                              unsigned long long *tl, hipStream_t s) {
     const int parents = layer >= 1 ? 1 << (layer - 1) : 0;
 #define FBDT_HIST(NPV)                                                                          \
     launch_hist_np<true, NPV, FPG, SIGNED, MISS>(hs, xb, ldb, n, d, n_bins, node_in, node_out, \
                                                  w, vsign, pc, layer, scale, partial, small,   \
-                                                 err, s)
+                                                 err, tl, s)
     switch (parents) {
     case 0:
     case 1: return FBDT_HIST(1);
@@ -2335,16 +2441,16 @@ hipError_t launch_hist_fpg(const HistShape &hs, const uint8_t *xb, int64_t ldb, 
                            int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                            const float *w, const uint8_t *vsign, const ParentCuts &pc, int layer,
                            bool routed, int scale, uint64_t *partial, double *small, int *err,
-                           hipStream_t s) {
+                           unsigned long long *tl, hipStream_t s) {
     const ParentCuts none{};
     if (!routed) {
         if (vsign)
             return launch_hist_np<false, 0, FPG, true, false>(hs, xb, ldb, n, d, n_bins, node_in,
                                                               nullptr, w, vsign, none, layer,
-                                                              scale, partial, small, err, s);
+                                                              scale, partial, small, err, tl, s);
         return launch_hist_np<false, 0, FPG, false, false>(hs, xb, ldb, n, d, n_bins, node_in,
                                                            nullptr, w, nullptr, none, layer,
-                                                           scale, partial, small, err, s);
+                                                           scale, partial, small, err, tl, s);
     }
     // routed passes below the root subtract siblings exactly when no event
     // can stop at a missing value; a fit with missing values histograms both
@@ -2353,7 +2459,7 @@ hipError_t launch_hist_fpg(const HistShape &hs, const uint8_t *xb, int64_t ldb, 
 #define FBDT_HIST_R(SG, MS)                                                                     \
     launch_hist_routed<FPG, SG, MS>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w,            \
                                     SG ? vsign : nullptr, pc, layer, scale, partial, small,    \
-                                    err, s)
+                                    err, tl, s)
     if (vsign) return miss ? FBDT_HIST_R(true, true) : FBDT_HIST_R(true, false);
     return miss ? FBDT_HIST_R(false, true) : FBDT_HIST_R(false, false);
 #undef FBDT_HIST_R
@@ -2363,10 +2469,10 @@ hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb,
                             int d, int n_bins, const uint8_t *node_in, uint8_t *node_out,
                             const float *w, const uint8_t *vsign, const ParentCuts &pc,
                             int layer, bool routed, int scale, uint64_t *partial, double *small,
-                            int *err, hipStream_t s) {
+                            int *err, hipStream_t s, unsigned long long *tl) {
 #define FBDT_HIST_F(F)                                                                          \
     launch_hist_fpg<F>(hs, xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc, layer,       \
-                       routed, scale, partial, small, err, s)
+                       routed, scale, partial, small, err, tl, s)
     switch (hs.features_per_group) {
     case 1: return FBDT_HIST_F(1);
     case 2: return FBDT_HIST_F(2);
@@ -2376,6 +2482,15 @@ hipError_t launch_histogram(const HistShape &hs, const uint8_t *xb, int64_t ldb,
     default: return hipErrorInvalidValue;
     }
 #undef FBDT_HIST_F
+}
+
+hipError_t launch_hist_reference(int kind, const HistShape &hs, const uint8_t *xb, int64_t ldb,
+                                 int64_t n, int d, const uint8_t *node, const float *w,
+                                 uint32_t *sink, hipStream_t s) {
+    hist_reference_kernel<<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
+        kind, xb, ldb, n, d, hs.features_per_group, node, w, hs.feature_groups, hs.node_groups,
+        hs.chunks, hs.chunk_events, hs.xcd_events, sink);
+    return hipGetLastError();
 }
 
 // vs[i] = 1 where v[i] < 0, 0 elsewhere and for the padding [n, npad)
