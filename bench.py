@@ -35,6 +35,9 @@ sys.path.insert(0, ROOT)
 
 METRIC = ("fit: binned event·features/s per tree layer (HBM GB/s); apply: events/s")
 HBM_PEAK_GBS = 8000.0
+# integer VALU peak of MI355X: 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz
+VALU_PEAK_GOPS = 256 * 64 * 2.4
+APPLY_OPS_PER_NODE_STEP = 4
 
 
 def measured_traffic():
@@ -332,10 +335,22 @@ def measure_apply_workload(args, apply_x, fb, torch):
                  "workload": f"the same forest and events as float32 values [{d}][{n}], "
                              "value thresholds (fbdt_apply_float)",
                  "prob_equal_to_binned_apply": same}
+    # ALU roofline: the traversal's algorithmic integer work is 4 lane
+    # operations per node step (fetch the node's code, compare with the cut,
+    # form the child index, select), T * D node steps per event; the peak is
+    # MI355X's integer VALU issue rate, 256 CUs x 64 lanes per clock x 2.4 GHz
+    ops = n * s5.n_trees * s5.depth * APPLY_OPS_PER_NODE_STEP
+    achieved = ops / (mean_ms / 1e3) / 1e9
     return {"events_per_s": n / (mean_ms / 1e3), "launches": launches,
             "mean_launch_us": mean_ms * 1e3,
             "bytes_per_event": d + 4,
             "hbm_gbs": n * (d + 4) / (mean_ms / 1e3) / 1e9,
+            "hbm_frac": n * (d + 4) / (mean_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "roofline": {"bound": "alu", "kernel": "apply_shallow_kernel<3> (binned)",
+                         "achieved": achieved, "peak": VALU_PEAK_GOPS,
+                         "unit": "G int32 lane-ops/s", "frac": achieved / VALU_PEAK_GOPS,
+                         "ops_per_node_step": APPLY_OPS_PER_NODE_STEP,
+                         "node_steps_per_event": s5.n_trees * s5.depth},
             "workload": f"{s5.n_trees}-tree depth-{s5.depth} forest fitted on workload 3 "
                         f"({s3.n_events} x {s3.n_features}, {s5.n_bins} bins) applied to {n} "
                         f"fresh events x {d} uint8 codes; prob float32 out",
