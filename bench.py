@@ -73,6 +73,8 @@ def parse():
                     help="also time negative weights, missing values and importance (1/0)")
     ap.add_argument("--fit-workloads", default="3,4",
                     help="larger fit workloads also timed and reported (comma list, '' for none)")
+    ap.add_argument("--oracle-baseline", type=int, default=1,
+                    help="time the CPU oracle per phase on bounded samples of every workload (1/0)")
     ap.add_argument("--phases", type=int, default=1,
                     help="histogram phase timeline and reference passes (1/0)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -218,6 +220,114 @@ def measure_hist_phases(fb, torch, codes, y, spec):
             "note": "phase stamps in microseconds after the launch's first workgroup entry"}
 
 
+def host_info():
+    """CPU model, core counts and numpy version of this host."""
+    import platform
+    import numpy as np
+    model = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    usable = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cores": usable,
+            "numpy": np.__version__, "threads_used": 1}
+
+
+def _stats(xs):
+    import numpy as np
+    return {"min": float(np.min(xs)), "mean": float(np.mean(xs)), "max": float(np.max(xs)),
+            "repeats": len(xs)}
+
+
+def measure_oracle_baseline(apply_model=None):
+    """The CPU oracle (single-threaded numpy, as it stands) timed per phase
+    on bounded samples of every workload: binning of a few features of the
+    full sample, a few trees of the fit (per layer: histogram, cumulative
+    sums + gains + best cut, routing), and apply; repeated up to 5 times
+    (min/mean/max).  The samples are stated with each workload."""
+    import numpy as np
+    from oracle import fbdt_oracle as O
+    from synth import CONFIGS, make_apply_chunk, make_training_set
+    # workload -> (events used, features binned, trees fitted, repeats)
+    plan = {1: (None, None, None, 5), 2: (None, 2, 5, 5), 3: (None, 2, 1, 5),
+            4: (1_000_000, 2, 1, 1)}
+    out = {}
+    for cfg, (n_ev, nbf, trees, reps) in plan.items():
+        spec = CONFIGS[cfg]
+        t0 = time.time()
+        ds = make_training_set(cfg, n_events=n_ev)
+        d, n = ds["x"].shape
+        B, D = spec.n_bins, spec.depth
+        T = spec.n_trees if trees is None else trees
+        jb = d if nbf is None else nbf
+        bin_s, fit_s, app_s, steps = [], [], [], []
+        for _ in range(reps):
+            tb = time.perf_counter()
+            O.bin_features(ds["x"][:jb], B)
+            bin_s.append((time.perf_counter() - tb) * d / jb)
+        _, xb = O.bin_features(ds["x"], B) if jb == d else (None, None)
+        if xb is None:
+            xb = np.stack([O.encode(ds["x"][j], O.quantile_boundaries(ds["x"][j], B))
+                           for j in range(d)])
+        del ds["x"]
+        for _ in range(reps):
+            tm = {}
+            tf = time.perf_counter()
+            m = O.fit(xb, ds["y"], ds["v"], D, T, spec.shrinkage, spec.subsample,
+                      spec.fit_seed, B, timings=tm)
+            fit_s.append((time.perf_counter() - tf) / T)
+            steps.append(tm)
+            ta = time.perf_counter()
+            O.apply(m, xb)
+            app_s.append((time.perf_counter() - ta) / T)
+        layer_us = {}
+        for key in steps[0]:
+            layer_us[key + "_us_per_tree"] = float(np.mean([st[key] for st in steps])) / T * 1e6
+        per_tree = _stats(fit_s)
+        out[f"workload{cfg}"] = {
+            "sample": ((f"all {n} events" if n == spec.n_events else
+                        f"{n} events drawn from the {spec.n_events}-event workload's "
+                        f"distribution (same seed)") +
+                       f" x {d} features; binning timed on {jb} feature(s) and scaled to {d}; "
+                       f"fit of the first {T} of {spec.n_trees} trees; apply of those trees to "
+                       f"the {n} events"),
+            "bin_s_all_features": _stats(bin_s),
+            "fit_s_per_tree": per_tree,
+            "fit_s_all_trees_est": per_tree["mean"] * spec.n_trees * spec.n_events / n,
+            "value": n * d * D / per_tree["mean"],
+            "unit": "event*features/s per tree layer",
+            "steps": layer_us,
+            "apply_s_per_tree": _stats(app_s),
+            "apply_events_per_s_all_trees": n / (np.mean(app_s) * spec.n_trees),
+            "setup_s": round(time.time() - t0, 1)}
+        print(f"# oracle baseline workload {cfg}: {per_tree['mean']:.3f} s per tree",
+              file=sys.stderr, flush=True)
+    if apply_model is not None:
+        s5 = CONFIGS[5]
+        m = 200_000
+        xf = make_apply_chunk(0, m)["x"]
+        xb = np.stack([O.encode(xf[j], apply_model["boundaries"][j]) for j in range(xf.shape[0])])
+        om = O.Model(apply_model["depth"], apply_model["n_bins"], apply_model["n_features"],
+                     apply_model["f0"], apply_model["cut_feature"], apply_model["cut_bin"],
+                     apply_model["gain"], apply_model["leaf"])
+        app = []
+        for _ in range(3):
+            ta = time.perf_counter()
+            O.apply(om, xb)
+            app.append(time.perf_counter() - ta)
+        out["workload5"] = {
+            "sample": f"apply of the fitted {s5.n_trees}-tree forest to {m} of the "
+                      f"{s5.apply_events} fresh events (binned by the oracle)",
+            "apply_s": _stats(app), "events_per_s": m / float(np.mean(app)),
+            "unit": "events/s"}
+    return {"host": host_info(), "kind": "oracle", "workloads": out}
+
+
 def measure_section4(fb, torch):
     """The features of sections 4.1-4.3 on workload 3's sample (2M x 40, 256
     bins, 200 trees of depth 3), each against the plain fit of the same
@@ -329,6 +439,10 @@ def measure_apply_workload(args, apply_x, fb, torch):
     same = bool(torch.equal(prob, prob_binned))
     del xf, prob_binned
     f_ms = fms / max(fl, 1)
+    gm = model.export()
+    oracle_model = {k: gm[k] for k in ("depth", "n_bins", "n_features", "f0", "cut_feature",
+                                       "cut_bin", "gain", "leaf")}
+    oracle_model["boundaries"] = bounds
     float_out = {"events_per_s": n / (f_ms / 1e3), "launches": fl, "mean_launch_us": f_ms * 1e3,
                  "bytes_per_event": 4 * d + 4,
                  "hbm_gbs": n * (4 * d + 4) / (f_ms / 1e3) / 1e9,
@@ -354,7 +468,7 @@ def measure_apply_workload(args, apply_x, fb, torch):
             "workload": f"{s5.n_trees}-tree depth-{s5.depth} forest fitted on workload 3 "
                         f"({s3.n_events} x {s3.n_features}, {s5.n_bins} bins) applied to {n} "
                         f"fresh events x {d} uint8 codes; prob float32 out",
-            "setup_s": round(fit_s, 1), "float": float_out}
+            "setup_s": round(fit_s, 1), "float": float_out, "_oracle_model": oracle_model}
 
 
 def main():
@@ -465,6 +579,9 @@ def main():
     if apply_x:
         apply_out = measure_apply_workload(args, apply_x, fb, torch)
 
+    oracle_model = apply_out.pop("_oracle_model", None)
+    oracle_baseline = measure_oracle_baseline(oracle_model) if args.oracle_baseline else None
+
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20
         src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
@@ -513,10 +630,12 @@ def main():
         "section4": section4,
         "bin_ms": bin_ms,
         "bin_warm_ms": bin_warm_ms,
+        "oracle_baseline": oracle_baseline,
         "cpu_baseline": {
             "value": cpu_value,
             "unit": "event*features/s per tree layer",
             "cores": 1,
+            "host": host_info(),
             "kind": "oracle",
             "sample": f"numpy oracle fit of the first {cpu_T} of the 100 trees on all 500k "
                       f"events (bins precomputed), {cpu_s:.1f} s",

@@ -30,6 +30,7 @@ l (0-based) holds nodes [2^l, 2^(l+1)), leaves are [2^D, 2^(D+1)).
 from __future__ import annotations
 
 import dataclasses
+import time
 
 import numpy as np
 
@@ -356,10 +357,28 @@ def _near_tie_candidates(H, g, best, parent, k):
     return [(int(j), int(c0) + 1, float(g[k, j, c0])) for j, c0 in zip(*np.nonzero(near))]
 
 
+class _Clock:
+    """Wall-clock seconds per named step, summed into a dict (or nothing)."""
+
+    def __init__(self, into: dict | None):
+        self.into = into
+        self.t = 0.0
+
+    def start(self):
+        if self.into is not None:
+            self.t = time.perf_counter()
+
+    def stop(self, name: str):
+        if self.into is not None:
+            now = time.perf_counter()
+            self.into[name] = self.into.get(name, 0.0) + (now - self.t)
+            self.t = now
+
+
 def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
         seed: int, n_bins: int, reference: Model | None = None, tie_log: TieLog | None = None,
         trace: list | None = None, final_score: bool = False, start=None,
-        near_ties: list | None = None):
+        near_ties: list | None = None, timings: dict | None = None):
     """Stochastic gradient-boosted trees on binned features (sections 1.1-1.4, 2.1).
 
     ``reference`` (optional) holds another implementation's cuts.  Where that
@@ -375,6 +394,10 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
     of the trees before t0 stay zero.  ``near_ties`` (optional list) receives,
     for every node whose near-tie set holds more than its best cut, a tuple
     (tree, heap node, [(feature, cut, gain), ...]) of that set.
+    ``timings`` (optional dict) accumulates wall seconds per step: "reweight"
+    (sub-sample, pseudo-response, weights), "histogram_l<layer>",
+    "scan_l<layer>" (cumulative sums, gains, best cut), "route_l<layer>" and
+    "leaf" (boost weights and score update).
     Returns the Model, and the final score F when ``final_score``.
     """
     xb = np.asarray(xb)
@@ -395,16 +418,21 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
     # missing values (section 4.2): NaN codes in data binned with B <= 255
     missing = missing_allowed(n_bins) and bool((xb == MISSING).any())
     inner_out = np.zeros((n_trees, (1 << depth) - 1)) if missing else None
+    clock = _Clock(timings)
     for t in range(t_first, n_trees):
+        clock.start()
         mask = subsample_mask(seed, t, n, subsample)
         yt = pseudo_response(y, F)
         w = histogram_weights(y, v, yt, mask)
         node = np.ones(n, dtype=np.int64)
+        clock.stop("reweight")
         for layer in range(depth):
             H = histogram(xb, node, w, is_signal, layer, n_bins)
+            clock.stop(f"histogram_l{layer}")
             S, Bk = cumulative(H)
             g = split_gains(S, Bk)
             feat, cut, best = best_cuts(g)
+            clock.stop(f"scan_l{layer}")
             lo = (1 << layer) - 1
             if near_ties is not None:
                 parent = gini(S[:, 0, n_bins], Bk[:, 0, n_bins])
@@ -435,7 +463,9 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
             if trace is not None:
                 trace.append({"tree": t, "layer": layer, "H": H, "node": node.copy(),
                               "w": w, "feat": feat.copy(), "cut": cut.copy()})
+            clock.start()
             node = route(node, xb, feat, cut, layer, missing)
+            clock.stop(f"route_l{layer}")
         leaf_local = node - (1 << depth)
         if missing:
             values = shrinkage * node_values(node, yt, v, mask, depth)
@@ -446,6 +476,7 @@ def fit(xb, y, v, depth: int, n_trees: int, shrinkage: float, subsample: float,
             gamma = leaf_values(leaf_local, yt, v, mask, 1 << depth)
             leaf_out[t] = shrinkage * gamma
             F = F + leaf_out[t][leaf_local]
+        clock.stop("leaf")
     model = Model(depth, n_bins, d, f0, cut_feature, cut_bin, gain_out, leaf_out, inner_out)
     return (model, F) if final_score else model
 
