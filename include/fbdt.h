@@ -147,14 +147,16 @@ int fbdt_apply(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d, int
  * Score float32 events without binning them (section 2.2, the inverse of the
  * bin transform): the cut "bin >= c" of feature j is the test
  * x >= boundaries[j][c - 1], which holds exactly when the value's bin (the
- * number of boundaries at or below it) is >= c, so the result equals
- * fbdt_apply on fbdt_bin_transform's codes bit for bit.  The model needs its
+ * number of boundaries at or below it) is >= c, so for events without NaN
+ * values the result equals fbdt_apply on fbdt_bin_transform's codes bit for
+ * bit (NaN: see below; fbdt_bin_transform gives NaN code 255, which in a
+ * model without inner weights goes right at every cut).  The model needs its
  * boundaries (fbdt_model_set_boundaries or fbdt_model_import), else
  * FBDT_E_INVAL.  x: device float32 [d][ldx], ldx >= n, d >= the model's
  * feature count (else FBDT_E_SHAPE).  A NaN value stops the event at the
  * node that cuts on it when the model has inner weights (as code 255 does
  * in fbdt_apply); in other models it fails every test and takes the left
- * branch.  prob, score as for fbdt_apply.  Stream-ordered.
+ * branch, as code 0 would.  prob, score as for fbdt_apply.  Stream-ordered.
  */
 int fbdt_apply_float(const fbdt_model *m, const float *x, int64_t n, int32_t d, int64_t ldx,
                      float *prob, double *score, void *stream);
@@ -178,12 +180,15 @@ int fbdt_feature_importance(const fbdt_model *m, double *importance);
 int fbdt_event_importance(const fbdt_model *m, const uint8_t *xb, int64_t n, int32_t d,
                           int64_t ldb, double *importance, int64_t ldi, void *stream);
 
-/* Borrowed host view of a model, valid until fbdt_model_free. */
+/* Borrowed host view of a model, valid until fbdt_model_free: the forest of
+ * Fig. 1 (cuts in heap order, terminal boost weights of section 1.3), f0,
+ * the separation gains (section 4.3) and the bin boundaries (section 2.2). */
 int fbdt_model_export(const fbdt_model *m, fbdt_model_view *view);
 
-/* New model from host arrays (copied); gain and boundaries may be NULL.
- * Boundaries, if given, must hold no NaN and ascend (non-strictly) per
- * feature, else FBDT_E_INVAL. */
+/* New model from host arrays (copied), in the layout of fbdt_model_export;
+ * gain and boundaries may be NULL.  Cut features must be < n_features and
+ * cut bins in 1..n_bins-1, else FBDT_E_INVAL.  Boundaries, if given, must
+ * hold no NaN and ascend (non-strictly) per feature, else FBDT_E_INVAL. */
 int fbdt_model_import(const fbdt_model_view *view, fbdt_model **out);
 
 /*
@@ -194,9 +199,13 @@ int fbdt_model_import(const fbdt_model_view *view, fbdt_model **out);
  */
 int fbdt_model_set_boundaries(fbdt_model *m, const float *boundaries);
 
+/* Frees a model made by fbdt_fit or fbdt_model_import and its device
+ * copies; NULL is ignored.  Not to be called while the model is in use. */
 void fbdt_model_free(fbdt_model *m);
 
-/* Message of the last failed call on this thread ("" if none). */
+/* Message of the last failed call on this thread ("" if none): the argument
+ * or device condition behind the FBDT_E_* code the call returned.  Owned by
+ * the library, valid until the thread's next failing call. */
 const char *fbdt_last_error(void);
 
 /* ---- The steps of one boosting iteration, callable one at a time ------- */
@@ -316,6 +325,12 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
  * calls with the same set; up to 4 graphs per device are kept, and growing the
  * device workspace drops them.  0 launches every kernel one by one.  Graphs
  * are not used while any fit kernel kind is being timed.
+ * "fail_alloc" (default 0, for tests of the error path): the next `value`
+ * device allocations the library would make (its scratch, a model's device
+ * copy) fail instead, and the calls that needed them return FBDT_E_DEVICE;
+ * a positive value first releases the scratch the library holds (waiting
+ * for the devices to finish with it), so the next call that needs scratch
+ * allocates.
  * "hist_timeline" (default 0): 1 makes fbdt_fit record the phase timeline
  * of every histogram launch (see fbdt_hist_timeline); fits then launch
  * kernel by kernel.

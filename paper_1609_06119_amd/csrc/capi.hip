@@ -114,6 +114,22 @@ int device_info(int dev, DeviceInfo *out) {
 }
 
 // ---- options --------------------------------------------------------------
+// Forced allocation failure (tests of the error path): while positive, each
+// device allocation the library would make fails instead, as an exhausted
+// device would make it fail, and the count goes down by one.
+std::atomic<int64_t> opt_fail_alloc{0};
+
+hipError_t device_alloc(void **p, size_t bytes) {
+    int64_t left = opt_fail_alloc.load();
+    while (left > 0) {
+        if (opt_fail_alloc.compare_exchange_weak(left, left - 1)) {
+            *p = nullptr;
+            return hipErrorOutOfMemory;
+        }
+    }
+    return hipMalloc(p, bytes);
+}
+
 std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0}, opt_hist_copies{0},
     opt_apply_threads{0}, opt_fit_graphs{1}, opt_hist_timeline{0};
 
@@ -232,8 +248,31 @@ int arena_reserve(Arena &a, size_t bytes) {
         a.size = 0;
     }
     size_t want = bytes + bytes / 4 + (1 << 20);
-    HIP_TRY(hipMalloc(&a.ptr, want));
+    HIP_TRY(device_alloc(&a.ptr, want));
     a.size = want;
+    return FBDT_OK;
+}
+
+// Frees the scratch of every device (after the device has finished with it:
+// hipFree waits) and the fit graphs that point into it.
+int release_scratch() {
+    int cur = -1;
+    HIP_TRY(hipGetDevice(&cur));
+    for (int dev = 0; dev < 64; ++dev) {
+        Arena &a = g_arena[dev];
+        std::lock_guard<std::mutex> lk(a.mu);
+        if (!a.ptr) continue;
+        HIP_TRY(hipSetDevice(dev));
+        drop_graphs(a);
+        const hipError_t e = hipFree(a.ptr);
+        a.ptr = nullptr;
+        a.size = 0;
+        if (e != hipSuccess) {
+            (void)hipSetDevice(cur);
+            return fail(FBDT_E_DEVICE, "hipFree of the scratch failed: %s", hipGetErrorString(e));
+        }
+    }
+    HIP_TRY(hipSetDevice(cur));
     return FBDT_OK;
 }
 
@@ -329,6 +368,14 @@ int fbdt_set_option(const char *name, int64_t value) {
         opt_hist_copies = value;
     } else if (!strcmp(name, "hist_timeline")) {
         opt_hist_timeline = value != 0;
+    } else if (!strcmp(name, "fail_alloc")) {
+        // the scratch the library holds is released first, so that the next
+        // call that needs scratch allocates (and fails)
+        if (value > 0) {
+            const int rc = release_scratch();
+            if (rc) return rc;
+        }
+        opt_fail_alloc = value;
     } else if (!strcmp(name, "fit_graphs")) {
         opt_fit_graphs = value != 0;
     } else if (!strcmp(name, "apply_threads")) {
@@ -974,8 +1021,9 @@ static int device_copy(fbdt_model *m, int dev, fbdt_model::DeviceCopy **out) {
         std::copy(m->leaf.begin() + t * nleaf, m->leaf.begin() + (t + 1) * nleaf, row);
     }
     fbdt_model::DeviceCopy c{dev, nullptr, nullptr, 0, nullptr, nullptr, nullptr};
-    HIP_TRY(hipMalloc(&c.cuts, packed.size() * sizeof(uint16_t)));
-    if (hipMalloc(&c.leaves, values.size() * sizeof(double)) != hipSuccess) {
+    HIP_TRY(device_alloc(reinterpret_cast<void **>(&c.cuts), packed.size() * sizeof(uint16_t)));
+    if (device_alloc(reinterpret_cast<void **>(&c.leaves), values.size() * sizeof(double)) !=
+        hipSuccess) {
         (void)hipFree(c.cuts);
         return fail(FBDT_E_DEVICE, "out of device memory");
     }
@@ -1026,7 +1074,8 @@ int fbdt_apply(const fbdt_model *mc, const uint8_t *xb, int64_t n, int32_t d, in
                     table[t * 16 + 8 + k] = (256u - m->cut_bin[t * nin + k]) * 0x10001u;
                 }
             if (!copy->nodes)
-                HIP_TRY(hipMalloc(&copy->nodes, table.size() * sizeof(uint32_t)));
+                HIP_TRY(device_alloc(reinterpret_cast<void **>(&copy->nodes),
+                                     table.size() * sizeof(uint32_t)));
             HIP_TRY(hipMemcpy(copy->nodes, table.data(), table.size() * sizeof(uint32_t),
                               hipMemcpyHostToDevice));
             copy->nodes_stride = xs;
@@ -1078,7 +1127,8 @@ int fbdt_event_importance(const fbdt_model *mc, const uint8_t *xb, int64_t n, in
         fbdt_model::DeviceCopy *copy = nullptr;
         if ((rc = device_copy(m, dev, &copy))) return rc;
         if (!copy->gains) {
-            HIP_TRY(hipMalloc(&copy->gains, (size_t)T * nin * sizeof(double)));
+            HIP_TRY(device_alloc(reinterpret_cast<void **>(&copy->gains),
+                                 (size_t)T * nin * sizeof(double)));
             HIP_TRY(hipMemcpy(copy->gains, m->gain.data(), (size_t)T * nin * sizeof(double),
                               hipMemcpyHostToDevice));
         }
@@ -1146,7 +1196,8 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
                     std::memcpy(&bits, &t, sizeof bits);
                     table.push_back(bits);
                 }
-            HIP_TRY(hipMalloc(&copy->ftab, table.size() * sizeof(uint32_t)));
+            HIP_TRY(device_alloc(reinterpret_cast<void **>(&copy->ftab),
+                                 table.size() * sizeof(uint32_t)));
             HIP_TRY(hipMemcpy(copy->ftab, table.data(), table.size() * sizeof(uint32_t),
                               hipMemcpyHostToDevice));
             copy->ftab_words = (int)table.size();
@@ -1176,7 +1227,8 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
                         table[t * 16 + 8 + k] = (256u - r) * 0x10001u;
                     }
                 if (!copy->fnodes)
-                    HIP_TRY(hipMalloc(&copy->fnodes, table.size() * sizeof(uint32_t)));
+                    HIP_TRY(device_alloc(reinterpret_cast<void **>(&copy->fnodes),
+                                         table.size() * sizeof(uint32_t)));
                 HIP_TRY(hipMemcpy(copy->fnodes, table.data(), table.size() * sizeof(uint32_t),
                                   hipMemcpyHostToDevice));
                 copy->fnodes_stride = xs;
@@ -1195,7 +1247,8 @@ int fbdt_apply_float(const fbdt_model *mc, const float *x, int64_t n, int32_t d,
                     std::memcpy(&bits, &thr, sizeof bits);
                     table[k] = make_uint2(m->cut_feature[k], bits);
                 }
-                HIP_TRY(hipMalloc(&copy->frec, table.size() * sizeof(uint2)));
+                HIP_TRY(device_alloc(reinterpret_cast<void **>(&copy->frec),
+                                     table.size() * sizeof(uint2)));
                 HIP_TRY(hipMemcpy(copy->frec, table.data(), table.size() * sizeof(uint2),
                                   hipMemcpyHostToDevice));
             }

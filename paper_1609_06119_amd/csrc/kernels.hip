@@ -1288,9 +1288,15 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     // holds anything, picked at this lane's window bin; sb = the bin itself
     double sp = 0.0, sb = 0.0, stot = 0.0;
     bool any = false;
+    int side_last = -1;   // highest bin with side weight (either class), exact
 #pragma unroll
-    for (int e = 0; e < 8; ++e) any |= sd[e] != 0.0;
+    for (int e = 0; e < 8; ++e) {
+        any |= sd[e] != 0.0;
+        if (sd[e] != 0.0) side_last = max(side_last, 4 * lane + (e >> 1));
+    }
     if (__any(any)) {
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) side_last = max(side_last, __shfl_xor(side_last, o));
         double pr[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) pr[e] = sd[e] + (e >= 2 ? pr[e - 2] : 0.0);
@@ -1335,8 +1341,11 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     const int c = kCutSlice * q + wi;
     double g = -INFINITY;
     if (cls == 0 && wi >= 1 && c <= nbins - 1) {
+        // empty sides from exact quantities: the fixed-point sums, and for the
+        // side histogram a zero prefix below c, or no weight in a bin at or
+        // above c (side_last)
         const bool left_empty = Ps == 0 && Pb == 0 && sPs == 0.0 && sPb == 0.0;
-        const bool right_empty = Ps == Ts && Pb == Tb && sPs == sTs && sPb == sTb;
+        const bool right_empty = Ps == Ts && Pb == Tb && c > side_last;
         const bool bin_empty = Ps == Qs && Pb == Qb && sBs == 0.0 && sBb == 0.0;
         if (c >= 2 && bin_empty) {
             g = -INFINITY;   // same partition as cut c-1

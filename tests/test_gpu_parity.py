@@ -868,3 +868,76 @@ def test_errors_are_reported():
         fb.Model.from_arrays(np.array([[5]], np.uint8), np.array([[1]], np.uint8),
                              np.zeros((1, 2)), 0.0, 3, 16)
     assert ei.value.status == "FBDT_E_INVAL"
+
+
+def test_allocation_failure_reports_device_error_and_leaves_the_library_usable():
+    """Option fail_alloc makes the library's next device allocations fail as
+    an exhausted device would: the fit (its scratch, released by the option
+    so that the fit must allocate) and the first apply of a new model (its
+    device copy) return FBDT_E_DEVICE, with their outputs untouched; once the
+    count is spent the same calls succeed and match the oracle."""
+    ds = make_training_set(1)
+    spec = CONFIGS[1]
+    B, D, T = spec.n_bins, spec.depth, spec.n_trees
+    ob, xb = O.bin_features(ds["x"], B)
+    codes = fb.Codes.from_numpy(xb)
+    y = dev(ds["y"])
+    say("allocation failure: fit")
+    fb.set_option("fail_alloc", 1)
+    try:
+        with pytest.raises(fb.FbdtError) as ei:
+            fb.fit(codes, y, B, D, T, spec.shrinkage, spec.subsample, spec.fit_seed)
+        assert ei.value.status == "FBDT_E_DEVICE"
+    finally:
+        fb.set_option("fail_alloc", 0)
+    model = fb.fit(codes, y, B, D, T, spec.shrinkage, spec.subsample, spec.fit_seed)
+    gm = model.export()
+    om = O.fit(xb, ds["y"], ds["v"], D, T, spec.shrinkage, spec.subsample, spec.fit_seed, B)
+    assert np.array_equal(gm["cut_feature"], om.cut_feature)
+    assert np.array_equal(gm["cut_bin"], om.cut_bin)
+    say("allocation failure: first apply of a new model")
+    fresh = fb.Model.from_arrays(gm["cut_feature"], gm["cut_bin"], gm["leaf"], gm["f0"],
+                                 gm["n_features"], B)
+    prob = torch.full((codes.n,), -1.0, dtype=torch.float32, device="cuda")
+    fb.set_option("fail_alloc", 1)
+    try:
+        with pytest.raises(fb.FbdtError) as ei:
+            fb.apply(fresh, codes, prob=prob)
+        assert ei.value.status == "FBDT_E_DEVICE"
+    finally:
+        fb.set_option("fail_alloc", 0)
+    assert bool((prob == -1.0).all())
+    p = fb.apply(fresh, codes, prob=prob).cpu().numpy()
+    op, _ = O.apply(om, xb)
+    assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
+
+
+def test_apply_float_nan_without_inner_weights_takes_the_left_branch():
+    """In a model without inner weights a NaN value fails every threshold
+    test x >= b (section 2.2) and goes left at every node that cuts on it:
+    fbdt_apply_float equals fbdt_apply on codes where NaN is code 0 (not the
+    code 255 of fbdt_bin_transform, which goes right), bit for bit, and the
+    oracle's threshold apply."""
+    B, D, T, d, n = 64, 3, 50, 6, 5001
+    rng = np.random.default_rng(12)
+    clean = rng.normal(size=(d, 20_000)).astype(np.float32)
+    gb = np.stack([O.quantile_boundaries(clean[j], B) for j in range(d)])
+    x = rng.normal(size=(d, n)).astype(np.float32)
+    x[rng.random(x.shape) < 0.1] = np.nan
+    f = random_forest(T, D, d, B, seed=11)
+    model = fb.Model.from_arrays(f["cut_feature"], f["cut_bin"], f["leaf"], f["f0"], d, B,
+                                 boundaries=gb)
+    say(f"apply_float with NaN, no inner weights: n={n} d={d} T={T}")
+    sf = torch.empty(n, dtype=torch.float64, device="cuda")
+    pf = fb.apply_float(model, dev(x), score=sf).cpu().numpy()
+    codes = np.stack([O.encode(x[j], gb[j]) for j in range(d)])
+    assert (codes[np.isnan(x)] == 255).all()
+    codes[np.isnan(x)] = 0
+    sb = torch.empty(n, dtype=torch.float64, device="cuda")
+    pb = fb.apply(model, fb.Codes.from_numpy(codes), score=sb).cpu().numpy()
+    assert np.array_equal(pf, pb) and torch.equal(sf, sb)
+    om = O.Model(D, B, d, f["f0"], f["cut_feature"], f["cut_bin"],
+                 np.zeros_like(f["leaf"][:, 1:]), f["leaf"])
+    op, oF = O.apply_thresholds(om, x, gb)
+    assert np.array_equal(sf.cpu().numpy(), oF)
+    np.testing.assert_array_max_ulp(pf, op, maxulp=1)
