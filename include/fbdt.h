@@ -119,8 +119,8 @@ int fbdt_bin_transform(const float *x, int64_t n, int32_t d, int64_t ldx, int32_
  * with n_bins <= 255 code 255 marks a missing value (section 4.2): it stays
  * out of its feature's histograms, an event stops at the node that cuts on
  * a feature it misses, and every node, inner or leaf, gets a boost weight
- * over the sampled events that reached it (the model's inner weights;
- * depth <= 6, else FBDT_E_INVAL).  Other codes >= n_bins give FBDT_E_INVAL.
+ * over the sampled events that reached it (the model's inner weights).
+ * Other codes >= n_bins give FBDT_E_INVAL.
  * *out receives a new model (free with fbdt_model_free).  Synchronises the
  * stream before returning.
  */

@@ -673,8 +673,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     const bool signed_w = (h_err & kNegWeights) != 0;
     const bool missing = may_miss && (h_err & kHasMissing) != 0;
     if (missing && leaf_lds_bytes(D, true) > kLeafMaxLds)
-        return fail(FBDT_E_INVAL, "missing values (code %d) are supported up to depth 6",
-                    kMissingCode);
+        return fail(FBDT_E_INVAL, "the leaf pass of depth %d with missing values (code %d) "
+                    "needs more LDS than the device has", D, kMissingCode);
     const int nslots = missing ? 2 * nleaf - 1 : nleaf;   // boost weights per tree
     const int lblocks = missing ? lblocks_miss : lblocks_plain;
     if (signed_w) HIP_TRY(launch_sign_bytes(w, n, npad, fb.vsign, s));

@@ -175,6 +175,9 @@ __global__ __launch_bounds__(256) void initial_score_kernel(const double *__rest
 // Larger nv: thread t takes value t % nv over stripes of kLeafReduceThreads
 // / nv, then the stripes are added pairwise.
 constexpr int kLeafReduceThreads = 1024;
+// (num, den) pairs of every terminal slot of the deepest tree: with missing
+// values at depth 7, 255 nodes
+constexpr int kLeafSumSlots = 2 * ((2 << 7) - 1);
 
 // With missing values (section 4.2) the slots are all nodes of the tree in
 // heap order (slot k - 1 = node k) holding (num, den) of the events whose
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
     uint64_t seed, int tree, double alpha, float *__restrict__ w, double *__restrict__ yts,
     double *__restrict__ score_out, int64_t xcd_events) {
     __shared__ double red[kLeafReduceThreads];
-    __shared__ double s_leaf[256];
+    __shared__ double s_leaf[kLeafSumSlots];
     // boost weights of the terminal nodes: the leaves (heap ids from 2^D), or
     // with missing values every node (heap ids from 1)
     const unsigned nleaf = 1u << depth;
@@ -1407,8 +1410,12 @@ __host__ __device__ constexpr int leaf_slots(int depth, bool missing) {
 }
 
 __host__ __device__ constexpr int leaf_columns(int depth, bool missing) {
-    // acc takes columns * 2 slots doubles: at most ~133 KiB
-    return 2 * leaf_slots(depth, missing) <= 64 ? 256 : 2 * leaf_slots(depth, missing) <= 128 ? 128 : 64;
+    // acc takes columns * 2 slots doubles: at most ~136 KiB (depth 7 with
+    // missing values: 255 slots in 32 columns)
+    return 2 * leaf_slots(depth, missing) <= 64    ? 256
+           : 2 * leaf_slots(depth, missing) <= 128 ? 128
+           : 2 * leaf_slots(depth, missing) <= 256 ? 64
+                                                    : 32;
 }
 
 // threads per accumulator column
@@ -1645,7 +1652,7 @@ __global__ __launch_bounds__(kLeafReduceThreads) void leaf_finalize_kernel(
     const double *__restrict__ leaf_partial, int nblocks, int nslots, int inner, double eta,
     double *__restrict__ leaf_out) {
     __shared__ double red[kLeafReduceThreads];
-    __shared__ double s_leaf[256];
+    __shared__ double s_leaf[kLeafSumSlots];
     reduce_leaf_partials(leaf_partial, nblocks, nslots, eta, red, s_leaf, inner);
     for (int t = threadIdx.x; t < nslots; t += blockDim.x) leaf_out[t] = s_leaf[t];
 }
@@ -2623,6 +2630,7 @@ hipError_t launch_leaf(const uint8_t *xb, int64_t ldb, int64_t n, int d, const u
 
 hipError_t launch_leaf_finalize(const double *leaf_partial, int blocks, int depth, bool missing,
                                 double eta, double *leaf_out, hipStream_t s) {
+    if (2 * leaf_slots(depth, missing) > kLeafSumSlots) return hipErrorInvalidValue;
     leaf_finalize_kernel<<<1, kLeafReduceThreads, 0, s>>>(
         leaf_partial, blocks, leaf_slots(depth, missing), missing ? (1 << depth) - 1 : 0, eta,
         leaf_out);

@@ -421,6 +421,7 @@ MISSING_CASES = {
     "nan-negative-weights": dict(cfg=2, n_events=30_011, depth=4, n_trees=4, n_bins=64,
                                  weights="signed"),
     "nan-33-events-depth5": dict(cfg=1, n_events=33, depth=5, n_trees=3),
+    "nan-depth7-B64": dict(cfg=2, n_events=40_009, depth=7, n_bins=64, n_trees=3),
 }
 
 
@@ -491,14 +492,9 @@ def test_fit_with_missing_values_matches_oracle(case):
                        atol=1e-12 * n)
 
 
-def test_missing_values_need_depth_at_most_6_and_plain_data_stays_plain():
+def test_plain_data_with_fewer_than_256_bins_stays_plain():
     ds = make_training_set(1)
-    x = _with_missing(ds["x"], 3)
-    _, codes = fb.bin(dev(x), 16)
     y = dev(ds["y"])
-    with pytest.raises(fb.FbdtError) as ei:
-        fb.fit(codes, y, 16, 7, 2)
-    assert ei.value.status == "FBDT_E_INVAL"
     _, plain = fb.bin(dev(ds["x"]), 16)                 # B <= 255 but no NaN
     assert "inner" not in fb.fit(plain, y, 16, 3, 2).export()
 
