@@ -132,6 +132,12 @@ hipError_t device_alloc(void **p, size_t bytes) {
 
 std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0}, opt_hist_copies{0},
     opt_apply_threads{0}, opt_fit_graphs{1}, opt_hist_timeline{0};
+// event lists below the root: 0 = the fit decides (kListAutoEvents), 1 =
+// never, 2 = always; and the list pass's launch-shape overrides
+std::atomic<int64_t> opt_hist_lists{0}, opt_list_fpg{0}, opt_list_parts{0}, opt_list_copies{0};
+// fits of at least this many events histogram the layers below the root
+// from event lists
+constexpr int64_t kListAutoEvents = 4000000;
 
 // Phase timeline of the histogram launches of the last fit made with option
 // hist_timeline (host copy): [launches][max_blocks][kTimelineStamps].
@@ -215,12 +221,16 @@ struct GraphKey {
     uint64_t seed;
     int64_t fpg, chunks, threads, copies;
     bool signed_w, missing;
+    bool lists;
+    int64_t list_fpg, list_parts, list_copies;
     bool operator==(const GraphKey &o) const {
         return xb == o.xb && y == o.y && w == o.w && n == o.n && ldb == o.ldb && d == o.d &&
                n_bins == o.n_bins && depth == o.depth && n_trees == o.n_trees &&
                scale == o.scale && lblocks == o.lblocks && eta == o.eta && alpha == o.alpha &&
                seed == o.seed && fpg == o.fpg && chunks == o.chunks && threads == o.threads &&
-               copies == o.copies && signed_w == o.signed_w && missing == o.missing;
+               copies == o.copies && signed_w == o.signed_w && missing == o.missing &&
+               lists == o.lists && list_fpg == o.list_fpg && list_parts == o.list_parts &&
+               list_copies == o.list_copies;
     }
 };
 
@@ -342,6 +352,16 @@ double hist_algorithmic_bytes(int64_t n, int d, int n_bins, int layer, bool rout
     return b;
 }
 
+// Bytes a list pass of layer `layer` needs at the least: for each expected
+// entry (a sampled event, alpha n of them at the root, at most half of them
+// in the shorter children with sib) its 8-byte entry and d codes, plus the
+// histograms written.
+double list_algorithmic_bytes(int64_t n, double alpha, int d, int n_bins, int layer, bool sib) {
+    const double entries = alpha * (double)n * (sib ? 0.5 : 1.0);
+    const int hnodes = sib ? 1 << (layer - 1) : 1 << layer;
+    return entries * (8.0 + d) + (double)hnodes * d * n_bins * 2 * 8;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -366,6 +386,21 @@ int fbdt_set_option(const char *name, int64_t value) {
         if (value != 0 && value != 1 && value != 2 && value != 4)
             return fail(FBDT_E_INVAL, "hist_copies must be 0, 1, 2 or 4");
         opt_hist_copies = value;
+    } else if (!strcmp(name, "hist_lists")) {
+        if (value > 2) return fail(FBDT_E_INVAL, "hist_lists must be 0 (auto), 1 (off) or 2 (on)");
+        opt_hist_lists = value;
+    } else if (!strcmp(name, "list_features_per_group")) {
+        if (value != 0 && !list_fpg_supported((int)value))
+            return fail(FBDT_E_INVAL,
+                        "list_features_per_group must be 0, 4, 8, 12, 20, 28, 36 or 40");
+        opt_list_fpg = value;
+    } else if (!strcmp(name, "list_parts")) {
+        if (value > 4096) return fail(FBDT_E_INVAL, "list_parts must be <= 4096");
+        opt_list_parts = value;
+    } else if (!strcmp(name, "list_copies")) {
+        if (value != 0 && value != 1 && value != 2 && value != 4)
+            return fail(FBDT_E_INVAL, "list_copies must be 0, 1, 2 or 4");
+        opt_list_copies = value;
     } else if (!strcmp(name, "hist_timeline")) {
         opt_hist_timeline = value != 0;
     } else if (!strcmp(name, "fail_alloc")) {
@@ -590,6 +625,25 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                             pl[l].lds_bytes, di.max_lds);
         }
     }
+    // layers 1 .. D-1 of large fits histogram event lists (the shorter child
+    // of every parent, or with missing values every node of the layer)
+    const int64_t lists_opt = opt_hist_lists.load();
+    const bool lists = D >= 2 && npad <= kListMaxEvents &&
+                       (lists_opt == 2 || (lists_opt == 0 && n >= kListAutoEvents));
+    std::vector<ListShape> lplans_sib(lists ? D : 0), lplans_both(lists && may_miss ? D : 0);
+    for (int l = 1; lists && l < D; ++l) {
+        for (int mode = 0; mode < (may_miss ? 2 : 1); ++mode) {
+            const int nl = mode == 0 ? 1 << (l - 1) : 1 << l;
+            ListShape &ls = (mode == 0 ? lplans_sib : lplans_both)[l];
+            ls = plan_list_histogram(d, nl, di.cu_count, di.max_lds, (int)opt_list_fpg.load(),
+                                     (int)opt_list_parts.load(), (int)opt_list_copies.load());
+            partial_elems =
+                std::max(partial_elems, (size_t)ls.parts * d * n_bins * 2);
+            if (ls.lds_bytes > di.max_lds)
+                return fail(FBDT_E_INVAL, "the list pass of layer %d needs %zu bytes of LDS", l,
+                            ls.lds_bytes);
+        }
+    }
     const int lblocks_plain = leaf_blocks(n, D, false, di.cu_count);
     const int lblocks_miss = may_miss ? leaf_blocks(n, D, true, di.cu_count) : 0;
     const size_t slots_max = may_miss ? (size_t)2 * nleaf - 1 : (size_t)nleaf;
@@ -630,6 +684,22 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.cut_bin, (size_t)T * nin);
     cv.add(&fb.gain, (size_t)T * nin);
     cv.add(&fb.leaf, (size_t)T * slots_max);
+    // event lists: the event-major codes, the lists (each node's list holds
+    // at most its parent's sampled events, so two per sampled event), per
+    // layer 64 cursors + 64 node counts, the lists' starts and caps, and the
+    // histogrammed lists' partial rows for the cut scan
+    uint8_t *xr = nullptr;
+    uint2 *list = nullptr, *lchunks = nullptr;
+    uint32_t *lctr = nullptr, *lstart = nullptr, *lcap = nullptr;
+    const size_t lctr_count = (size_t)D * 2 * kListMaxSlots;
+    if (lists) {
+        cv.add(&xr, list_codes_bytes(n, d));
+        cv.add(&list, (size_t)2 * npad);
+        cv.add(&lctr, lctr_count);
+        cv.add(&lstart, kListMaxSlots);
+        cv.add(&lcap, kListMaxSlots);
+        cv.add(&lchunks, kListMaxSlots);
+    }
     // phase timeline of every histogram launch (measurement option)
     const bool timeline = opt_hist_timeline.load() != 0;
     int tl_blocks = 0;
@@ -680,6 +750,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     if (signed_w) HIP_TRY(launch_sign_bytes(w, n, npad, fb.vsign, s));
     const uint8_t *vsign = signed_w ? fb.vsign : nullptr;
     const std::vector<HistShape> &plans = missing ? plans_both : plans_sib;
+    const std::vector<ListShape> &lplans = missing ? lplans_both : lplans_sib;
+    if (lists) HIP_TRY(launch_transpose_codes(xb, ldb, n, d, xr, s));
 
     const uint64_t seed = p->seed;
     const double alpha = p->subsample, eta = p->shrinkage;
@@ -699,6 +771,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                                          fb.w, fb.yts, nullptr, di.cu_count, st));
                 tm.done();
             }
+            if (lists) HIP_TRY(launch_fill_u32(lctr, 0u, lctr_count, st));
             uint8_t *cf = fb.cut_feature + (size_t)t * nin;
             uint8_t *cc = fb.cut_bin + (size_t)t * nin;
             double *cg = fb.gain + (size_t)t * nin;
@@ -710,6 +783,44 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 if (l >= 1)
                     pc = ParentCuts{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
                 const int gl = t * D + l;   // side histograms alternate by gl's parity
+                if (lists && l >= 1) {
+                    // route with list output, then histogram the lists
+                    const ListShape &ls = lplans[l];
+                    uint32_t *ctr = lctr + (size_t)l * 2 * kListMaxSlots;
+                    const uint32_t *cap_prev =
+                        l >= 2 ? lctr + (size_t)(l - 1) * 2 * kListMaxSlots + kListMaxSlots : nullptr;
+                    {
+                        Timed tm(FBDT_K_ROUTE, st, 3.0 * (double)n);
+                        HIP_TRY(launch_route_list(
+                            xb, ldb, n, d, n_bins, l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
+                            fb.node[l & 1], fb.w, vsign, pc, l, n_bins <= kMissingCode, scale,
+                            cap_prev, (uint32_t)npad, l + 1 < D ? ctr + kListMaxSlots : nullptr,
+                            ctr, lstart, lcap, list, fb.small[gl & 1], fb.err, st));
+                        tm.done();
+                    }
+                    {
+                        Timed tm(FBDT_K_HISTOGRAM, st,
+                                 list_algorithmic_bytes(n, alpha, d, n_bins, l, !missing));
+                        HIP_TRY(launch_hist_list(ls, !missing, list, lstart, lcap, ctr, xr, d,
+                                                 n_bins, vsign != nullptr, scale, lchunks,
+                                                 fb.partial, fb.err, st));
+                        tm.done();
+                    }
+                    {
+                        Timed tm(FBDT_K_BEST_CUTS, st);
+                        const bool sib = !missing;
+                        const size_t next_count =
+                            (size_t)(l + 1 < D ? 1 << (l + 1) : 1) * d * n_bins * 2;
+                        HIP_TRY(launch_cut_scan(fb.partial, 0, scale, fb.small[gl & 1],
+                                                fb.small[(gl + 1) & 1], next_count, ls.lists, d,
+                                                n_bins, sib, fb.cand_gain, fb.cand_cut,
+                                                sib ? fb.hfull[(l - 1) & 1] : nullptr,
+                                                l + 1 < D && !missing ? fb.hfull[l & 1] : nullptr,
+                                                st, lchunks));
+                        tm.done();
+                    }
+                    continue;
+                }
                 // layers with many parents are routed by a pass of their own
                 // (one code gather per event instead of one per feature group)
                 const bool own_route = l >= 1 && (1 << (l - 1)) > kRoutedMaxParents;
@@ -785,7 +896,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     if (opt_fit_graphs.load() && !timeline && !(g_timing.load() & timed_kinds)) {
         const GraphKey key{xb, y, w, n, ldb, d, n_bins, D, T, scale, lblocks, eta, alpha, seed,
                            opt_hist_fpg.load(), opt_hist_chunks.load(), opt_hist_threads.load(),
-                           opt_hist_copies.load(), signed_w, missing};
+                           opt_hist_copies.load(), signed_w, missing, lists,
+                           opt_list_fpg.load(), opt_list_parts.load(), opt_list_copies.load()};
         hipGraphExec_t exec = nullptr;
         for (auto &g : a.graphs)
             if (g.first == key) exec = g.second;

@@ -225,11 +225,15 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
 // hparent [hnodes][d][B][2] their summed prefix rows; the right child is
 // parent - left.  hout (optional) receives the summed prefix rows of every
 // node of the layer.  Clears small_next[0, small_next_count) (the next
-// layer's side histogram).
+// layer's side histogram).  lchunks (list passes): the partials of
+// histogrammed node k are the rows [x_k, x_k + (y_k & 0x7fffffff)) of
+// [*][d][B][2], and with sibling bit 31 of y_k tells that they hold the
+// right child (the left is parent - right).
 hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
                            double *small_next, size_t small_next_count, int hnodes, int d,
                            int n_bins, bool sibling, double *cand_gain, int *cand_cut,
-                           const uint64_t *hparent, uint64_t *hout, hipStream_t s);
+                           const uint64_t *hparent, uint64_t *hout, hipStream_t s,
+                           const uint2 *lchunks = nullptr);
 
 // Best cut of each node over its candidates (d features x slices entries).
 hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,
@@ -277,6 +281,69 @@ constexpr int kRoutedMaxParents = 4;
 hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
                               const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc,
                               int layer, bool miss, int *err, int cu_count, hipStream_t s);
+
+// Event lists of the histogrammed nodes ("slots": the left child of every
+// parent, or with missing values every node of the layer), for layers 1 ..
+// depth - 1 of large fits.  launch_route_list routes a layer (as
+// launch_route_layer) and appends each sampled event that the layer's
+// histograms count and whose weight is on the fixed-point grid to its
+// slot's list, {event | negative << 31, weight bits}; launch_hist_list then
+// histograms the lists, reading each event's codes from an event-major copy
+// of the code matrix (launch_transpose_codes).  Lists need n < 2^31 and at
+// most kListMaxSlots slots.
+constexpr int kListMaxSlots = 64;
+constexpr int64_t kListMaxEvents = ((int64_t)1 << 31) - 1;
+// features per workgroup of the list pass it is built for (multiples of 4:
+// a workgroup reads an entry's codes as words)
+constexpr int kListFpgSizes[] = {4, 8, 12, 20, 28, 36, 40};
+bool list_fpg_supported(int f);
+// bytes per event of the event-major copy (d rounded up to 4), and the
+// copy's size (events rounded up to 256)
+int list_row_bytes(int d);
+size_t list_codes_bytes(int64_t n, int d);
+hipError_t launch_transpose_codes(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *xr,
+                                  hipStream_t s);
+
+struct ListShape {
+    int fpg;            // features per workgroup
+    int groups;         // ceil(d / fpg)
+    int parts;          // workgroups per feature group that share the lists' entries (> lists)
+    int lists;          // histogrammed lists of the layer
+    int per_xcd;        // workgroups per XCD
+    int blocks;         // kXcds * per_xcd
+    int copies;         // LDS copies of the rows (lane l adds into copy l % copies)
+    int copy_stride;    // bytes between copies
+    size_t lds_bytes;   // dynamic LDS per workgroup
+};
+// fpg / parts / copies: overrides (0 = the planner's choice).
+ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, int fpg,
+                              int parts, int copies);
+
+// Routing of layer `layer` in [1, 6] with list output: every node of the
+// layer gets a list.  node_in: ids of layer - 1 (null at layer 1: all
+// events at the root); node_out receives the ids of the layer for
+// round_up(n, 8) events.  w, vsign as for launch_histogram.  cap_prev:
+// sampled events per node of layer - 1 (null at layer 1: cap_root for the
+// root); cnt_out (optional, zeroed): receives the sampled events per node
+// of this layer; cursor [2^layer] (zeroed): receives the entries per list;
+// lstart / lcap [2^layer]: each list's range in `list` (2 cap_root entries
+// at most); small: the layer's side histogram [2^layer][d][B][2].
+hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, int n_bins,
+                             const uint8_t *node_in, uint8_t *node_out, const float *w,
+                             const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
+                             int scale, const uint32_t *cap_prev, uint32_t cap_root,
+                             uint32_t *cnt_out, uint32_t *cursor, uint32_t *lstart,
+                             uint32_t *lcap, uint2 *list, double *small, int *err,
+                             hipStream_t s);
+// Histograms of the lists of launch_route_list (sib: of the shorter child
+// of each of ls.lists parents; else of all ls.lists nodes) into
+// prefix-summed partials [ls.parts][d][B][2], with lchunks
+// [ls.lists] = {first part, parts | right child histogrammed << 31} for the
+// cut scan.
+hipError_t launch_hist_list(const ListShape &ls, bool sib, const uint2 *list,
+                            const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
+                            const uint8_t *xr, int d, int n_bins, bool signed_w, int scale,
+                            uint2 *lchunks, uint64_t *partial, int *err, hipStream_t s);
 
 // Forest traversal.  cuts: [T][2^D-1] packed (feature | bin << 8), for the
 // general kernel; nodes: [T][16] for depth <= kApplyShallowDepth, for heap

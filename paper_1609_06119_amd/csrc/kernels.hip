@@ -740,6 +740,60 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
     }
 }
 
+// The end of a histogram workgroup, after its adds (and an LDS barrier):
+// the LDS copies are summed into copy 0, bins >= n_bins are checked to be
+// empty (but for the missing code's with miss), and the rows (k, f), k < nk,
+// f < nf (LDS row k * fpg + f) are written to out[(k0 + k) * d + j0 + f]
+// [bin], the two classes of a bin in one 16-byte element: one row per
+// wavefront step.  With prefix (the fit's passes) every row is written as
+// inclusive prefix sums over bins, P(b) = sum of the bins <= b per class:
+// summed over chunks these are the cumulative histograms, which the cut
+// scan reads slice by slice.  Lane l holds bins 4l..4l+3 (both classes),
+// prefix in the lane, then an exclusive scan of the lane totals across the
+// wavefront.
+__device__ __forceinline__ void hist_write_rows(uint64_t *lds, int copies, int copy_stride,
+                                                int lds_n, int nk, int nf, int fpg, int k0,
+                                                int j0, int d, int nbins, bool miss, bool prefix,
+                                                uint4 *out, int &eflag) {
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nwaves = blockDim.x / kWave;
+    if (copies > 1) {   // copy 0 += the others
+        const int cs = copy_stride / 8;
+        for (int t = threadIdx.x; t < lds_n; t += blockDim.x) {
+            uint64_t v = lds[t];
+            for (int c = 1; c < copies; ++c) v += lds[c * cs + t];
+            lds[t] = v;
+        }
+        lds_barrier();
+    }
+    const int nrows = nk * nf;
+    for (int rr = wave; rr < nrows; rr += nwaves) {
+        const int k = rr / nf;
+        const int f = rr - k * nf;
+        const uint4 *src = reinterpret_cast<const uint4 *>(lds + (k * fpg + f) * kRow);
+        uint4 *dst = out + ((size_t)(k0 + k) * d + j0 + f) * nbins;
+        // bins >= n_bins must be empty, but for the missing code's
+        for (int t = nbins + lane; t < (miss ? kMissingCode : 256); t += kWave) {
+            const uint4 v = src[t];
+            if (v.x | v.y | v.z | v.w) eflag |= kErrBin;
+        }
+        if (prefix) {   // the row is scanned in place (this wavefront's row only)
+            ulonglong2 *s2 = reinterpret_cast<ulonglong2 *>(lds + (k * fpg + f) * kRow) + 4 * lane;
+            ulonglong2 v[4] = {s2[0], s2[1], s2[2], s2[3]};
+#pragma unroll
+            for (int e = 1; e < 4; ++e) {
+                v[e].x += v[e - 1].x;
+                v[e].y += v[e - 1].y;
+            }
+            const unsigned long long xs = wave_inclusive_scan_u64(v[3].x) - v[3].x;   // exclusive
+            const unsigned long long xb = wave_inclusive_scan_u64(v[3].y) - v[3].y;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) s2[e] = make_ulonglong2(v[e].x + xs, v[e].y + xb);
+        }
+        for (int t = lane; t < nbins; t += kWave) dst[t] = src[t];
+    }
+}
+
 template <bool ROUTED, int NP, int FPG, bool SIGNED, bool MISS>
 // The arguments that the first loads need come first, so that they fit the
 // kernel arguments preloaded into scalar registers at wave launch (16
@@ -899,50 +953,9 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     }
     lds_barrier();
     const unsigned long long t_adds = stamp ? (unsigned long long)wall_clock64() : 0ull;
-    if (copies > 1) {   // copy 0 += the others
-        const int cs = copy_stride / 8;
-        for (int t = threadIdx.x; t < lds_n; t += blockDim.x) {
-            uint64_t v = lds[t];
-            for (int c = 1; c < copies; ++c) v += lds[c * cs + t];
-            lds[t] = v;
-        }
-        lds_barrier();
-    }
-
-    // partial[p][node][feature][bin][class]: one (node, feature) row per
-    // wavefront step; bins >= n_bins must be empty.  With prefix (the fit's
-    // passes) every row is written as inclusive prefix sums over bins, P(b) = sum of the
-    // bins <= b per class: summed over chunks these are the cumulative
-    // histograms, which best_cuts then reads slice by slice.  Lane l holds
-    // bins 4l..4l+3 (both classes), prefix in the lane, then an exclusive
-    // scan of the lane totals across the wavefront.
-    const int nrows = a.nk * a.nf;
-    uint4 *out = reinterpret_cast<uint4 *>(partial + (size_t)p * hnodes * d * nbins * 2);
-    for (int rr = wave; rr < nrows; rr += nwaves) {
-        const int k = rr / a.nf;
-        const int f = rr - k * a.nf;
-        const uint4 *src = reinterpret_cast<const uint4 *>(lds + (k * FPG + f) * kRow);
-        uint4 *dst = out + ((size_t)(a.k0 + k) * d + a.j0 + f) * nbins;
-        // bins >= n_bins must be empty, but for the missing code's
-        for (int t = nbins + lane; t < (a.miss ? kMissingCode : 256); t += kWave) {
-            const uint4 v = src[t];
-            if (v.x | v.y | v.z | v.w) eflag |= kErrBin;
-        }
-        if (prefix) {   // the row is scanned in place (this wavefront's row only)
-            ulonglong2 *s2 = reinterpret_cast<ulonglong2 *>(lds + (k * FPG + f) * kRow) + 4 * lane;
-            ulonglong2 v[4] = {s2[0], s2[1], s2[2], s2[3]};
-#pragma unroll
-            for (int e = 1; e < 4; ++e) {
-                v[e].x += v[e - 1].x;
-                v[e].y += v[e - 1].y;
-            }
-            const unsigned long long xs = wave_inclusive_scan_u64(v[3].x) - v[3].x;   // exclusive
-            const unsigned long long xb = wave_inclusive_scan_u64(v[3].y) - v[3].y;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) s2[e] = make_ulonglong2(v[e].x + xs, v[e].y + xb);
-        }
-        for (int t = lane; t < nbins; t += kWave) dst[t] = src[t];
-    }
+    hist_write_rows(lds, copies, copy_stride, lds_n, a.nk, a.nf, FPG, a.k0, a.j0, d, nbins,
+                    a.miss, prefix, reinterpret_cast<uint4 *>(partial + (size_t)p * hnodes * d * nbins * 2),
+                    eflag);
     if (eflag) atomicOr(err, eflag);
     if (stamp) {
         unsigned long long *row = tl + (size_t)blockIdx.x * kTimelineStamps;
@@ -1206,7 +1219,8 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     const uint64_t *__restrict__ partial, int chunks, int scale, const double *__restrict__ small,
     double *__restrict__ small_next, size_t small_next_count, int hnodes, int d, int nbins, int S,
     double *__restrict__ cand_gain, int *__restrict__ cand_cut,
-    const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout) {
+    const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout,
+    const uint2 *__restrict__ lchunks) {
 #pragma clang fp contract(off)
     __shared__ uint64_t red[kCutWaves][kWave + 2];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
@@ -1218,12 +1232,29 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     const int wi = lane >> 1, cls = lane & 1;
     const int b = kCutSlice * q - 1 + wi;   // this lane's window bin
     const bool inb = b >= 0 && b < nbins;
+    // partials of the streaming pass: [chunks][hnodes][d][B][2]; of the
+    // list pass (lchunks): chunk c of list k at [base_k + c][d][B][2], and
+    // with SIB the flag tells that the right child was histogrammed
+    uint32_t lbase = 0u, flag = 0u;
+    if (lchunks) {
+        const uint2 lc = lchunks[k];
+        lbase = lc.x;
+        chunks = (int)(lc.y & 0x7fffffffu);
+        flag = lc.y >> 31;
+    }
+    // offsets of this lane's window bin and of the row total within a row
+    // [k][j] of the parents' rows, and within the first chunk's partial row
     const size_t off = ((size_t)k * d + j) * row;
     const size_t offv = off + (size_t)(inb ? b : 0) * 2 + cls;
     const size_t offt = off + (size_t)(nbins - 1) * 2 + cls;
-    const size_t stride_p = (size_t)hnodes * d * row;
-    // node of this wavefront's candidates, as an index within the layer
+    const size_t poff = lchunks ? ((size_t)lbase * d + j) * row : off;
+    const size_t pv_off = poff + (size_t)(inb ? b : 0) * 2 + cls;
+    const size_t pt_off = poff + (size_t)(nbins - 1) * 2 + cls;
+    const size_t stride_p = lchunks ? (size_t)d * row : (size_t)hnodes * d * row;
+    // node of this wavefront's candidates, as an index within the layer; with
+    // SIB wavefront `sub` forms its node as parent - the histogrammed child
     const int node = SIB ? 2 * k + (wave & 1) : k;
+    const int sub = flag ? 0 : 1;
     const size_t noff = ((size_t)node * d + j) * row;
 
     // side histogram row of the candidate wavefronts' node: lane l holds bins
@@ -1237,8 +1268,8 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
             sd[e] = bb < nbins ? small[noff + 2 * bb + (e & 1)] : 0.0;
         }
     }
-    uint64_t pv = 0, pt = 0;   // parent row (right child = parent - left)
-    if (SIB && wave == 1) {
+    uint64_t pv = 0, pt = 0;   // parent row (other child = parent - histogrammed child)
+    if (SIB && wave == sub) {
         pv = hparent[offv];
         pt = hparent[offt];
     }
@@ -1251,14 +1282,14 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
             const uint64_t *b1 = b0 + kCutWaves * stride_p;
             const uint64_t *b2 = b1 + kCutWaves * stride_p;
             const uint64_t *b3 = b2 + kCutWaves * stride_p;
-            const uint64_t x0 = b0[offv], x1 = b1[offv], x2 = b2[offv], x3 = b3[offv];
-            const uint64_t t0 = b0[offt], t1 = b1[offt], t2 = b2[offt], t3 = b3[offt];
+            const uint64_t x0 = b0[pv_off], x1 = b1[pv_off], x2 = b2[pv_off], x3 = b3[pv_off];
+            const uint64_t t0 = b0[pt_off], t1 = b1[pt_off], t2 = b2[pt_off], t3 = b3[pt_off];
             v += (x0 + x1) + (x2 + x3);
             vt += (t0 + t1) + (t2 + t3);
         }
         for (; p < chunks; p += kCutWaves) {
-            v += partial[(size_t)p * stride_p + offv];
-            vt += partial[(size_t)p * stride_p + offt];
+            v += partial[(size_t)p * stride_p + pv_off];
+            vt += partial[(size_t)p * stride_p + pt_off];
         }
     }
     red[wave][lane] = v;
@@ -1279,7 +1310,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         T += red[w][kWave + cls];
     }
     if (!inb) P = 0;
-    if (SIB && wave == 1) {   // right child = parent - left child (exact)
+    if (SIB && wave == sub) {   // the other child = parent - histogrammed child (exact)
         P = (inb ? pv : 0) - P;
         T = pt - T;
     }
@@ -1733,6 +1764,384 @@ __global__ __launch_bounds__(256) void route_layer_kernel(
         }
         *reinterpret_cast<uint2 *>(node_out + i0) = make_uint2(o[0], o[1]);
     }
+    if (eflag) atomicOr(err, eflag);
+}
+
+// ---------------------------------------------------------------------------
+// Event lists of the histogrammed nodes (layers >= 1 of large fits).
+//
+// The streaming pass reads every event once per (feature group, node group)
+// workgroup and adds it with a half-empty wavefront when the sub-sample or
+// the sibling rule leaves it out.  Below the root the list-driven pass
+// instead reads, per histogrammed node ("slot": the left child of each
+// parent, or with missing values each child), the list of the sampled
+// events that the node's histogram counts, and takes their codes from an
+// event-major copy of the code matrix: every LDS add then has all its lanes
+// busy, and an event is read once per feature group.
+
+// xr[i * dr + j] = xb[j * ldb + i] for i < n and j < d, else 0, for the
+// 256 events of each workgroup (dr a multiple of 4, <= 256).
+__global__ __launch_bounds__(256) void transpose_codes_kernel(const uint8_t *__restrict__ xb,
+                                                              int64_t ldb, int64_t n, int d,
+                                                              uint8_t *__restrict__ xr, int dr) {
+    __shared__ uint32_t tile[256 * 64];   // [256 events][dr bytes]
+    uint8_t *tb = reinterpret_cast<uint8_t *>(tile);
+    const int64_t i0 = (int64_t)blockIdx.x * 256;
+    const int64_t i = i0 + threadIdx.x;
+    for (int j = 0; j < dr; ++j)
+        tb[threadIdx.x * dr + j] = (j < d && i < n) ? xb[(int64_t)j * ldb + i] : (uint8_t)0;
+    __syncthreads();
+    uint32_t *dst = reinterpret_cast<uint32_t *>(xr + (size_t)i0 * dr);
+    for (int t = threadIdx.x; t < 64 * dr; t += 256) dst[t] = tile[t];
+}
+
+// Routing of layer `layer` (>= 1) for the list-driven histogram pass.  The
+// parents' cuts come from their candidates as in route_layer_kernel, and
+// every event (node_in = null at layer 1: all at the root) gets its node of
+// this layer, node <- 2 node + [code >= cut] (section 1.1); with miss, an
+// event whose code of the cut feature is the missing code, or which stopped
+// earlier, keeps its node (section 4.2).  A sampled event that has not
+// stopped is counted into cnt_out[node - 2^layer] (the caps of the next
+// layer's lists) and, if its weight is on the fixed-point grid (|w| >= tau),
+// appended to its node's list as {event | negative << 31, weight bits}
+// (both children are listed: the histogram pass picks the shorter list of
+// each parent).  Node k's list is the range [start_k, start_k + cap_k) of
+// `list`: cap_k = the sampled events of its parent (cap_prev, or cap_root at
+// layer 1), start_k = the caps of the nodes below k; workgroup 0 records
+// both (lstart, lcap).  Each workgroup counts its entries per node in LDS
+// and reserves them with one atomic add per node on cursor[k], so a list
+// holds its events in no fixed order (the
+// fixed-point sums do not depend on it).  Sampled weights below the grid go
+// to the float64 side histogram `small` [2^layer][d][B][2] here, for either
+// child and every feature, as the streaming pass adds them.
+constexpr int kRouteListThreads = 1024;
+constexpr int kRouteListSteps = 2;
+constexpr int kRouteListEvents = kRouteListThreads * kRouteListSteps * kHistE;
+template <bool SIGNED>
+__global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 4) void route_list_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
+    const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
+    const float *__restrict__ w, const uint8_t *__restrict__ vsign,
+    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
+    uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
+    int layer, bool miss, uint32_t tau_bits, const uint32_t *__restrict__ cap_prev,
+    uint32_t cap_root, uint32_t *__restrict__ cnt_out, uint32_t *__restrict__ cursor,
+    uint32_t *__restrict__ lstart, uint32_t *__restrict__ lcap, uint2 *__restrict__ list,
+    double *__restrict__ small, int *__restrict__ err, int64_t xcd_events) {
+    __shared__ uint8_t s_cf[64], s_cc[64];
+    __shared__ uint32_t s_cnt[kListMaxSlots], s_ncnt[kListMaxSlots];
+    __shared__ uint32_t s_start[kListMaxSlots], s_cap[kListMaxSlots], s_base[kListMaxSlots];
+    const uint32_t half = 1u << (layer - 1), nodes = 1u << layer;
+    const int nslots = (int)nodes;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nwaves = blockDim.x / kWave;
+    int eflag = 0;
+    const CandSet cs{cand_gain, cand_cut, d, cslices};
+    for (int k = wave; k < (int)half; k += nwaves) {
+        int bf, bc;
+        double bg;
+        bool ok;
+        node_best(cs, k, lane, &bf, &bc, &bg, &ok);
+        if (lane == 0) {
+            s_cf[k] = (uint8_t)bf;
+            s_cc[k] = (uint8_t)bc;
+            if (!ok) eflag |= kErrRoute;
+            if (blockIdx.x == 0 && rec_f) {
+                rec_f[k] = (uint8_t)bf;
+                rec_c[k] = (uint8_t)bc;
+                rec_g[k] = bg;
+            }
+        }
+    }
+    if (wave == nwaves - 1) {
+        // caps and starts of the lists: an exclusive scan of the caps
+        uint32_t cap = 0u;
+        if (lane < nslots) cap = cap_prev ? cap_prev[lane >> 1] : cap_root;
+        uint32_t x = cap;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const uint32_t y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+        }
+        if (lane < nslots) {
+            s_start[lane] = x - cap;
+            s_cap[lane] = cap;
+            if (blockIdx.x == 0) {
+                lstart[lane] = x - cap;
+                lcap[lane] = cap;
+            }
+        }
+        s_cnt[lane] = 0u;
+        s_ncnt[lane] = 0u;
+    }
+    __syncthreads();
+
+    // per event of the thread's steps: node << 16 | rank within the
+    // workgroup's entries of that node, or ~0 (no entry)
+    uint32_t rec[kRouteListSteps][kHistE];
+    uint32_t negs[kRouteListSteps];
+    // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
+    // (the range every per-event pass of the fit gives that XCD), in turn
+    const int64_t xlo = (int64_t)(blockIdx.x % kXcds) * xcd_events;
+    const int64_t base_i = xlo + (int64_t)(blockIdx.x / kXcds) * kRouteListEvents;
+    const int64_t end_i = min(min(n, xlo + xcd_events), base_i + kRouteListEvents);
+#pragma unroll
+    for (int st = 0; st < kRouteListSteps; ++st) {
+        const int64_t i0 = base_i + ((int64_t)st * kRouteListThreads + threadIdx.x) * kHistE;
+        negs[st] = 0u;
+#pragma unroll
+        for (int e = 0; e < kHistE; ++e) rec[st][e] = ~0u;
+        if (i0 < end_i) {
+            const uint2 pin = node_in ? *reinterpret_cast<const uint2 *>(node_in + i0)
+                                      : make_uint2(0x01010101u, 0x01010101u);
+            uint32_t par[kHistE], k[kHistE], code[kHistE];
+#pragma unroll
+            for (int e = 0; e < kHistE; ++e) {
+                par[e] = byte8(pin, e);
+                k[e] = par[e] - half;
+                const uint32_t kk = k[e] < half ? k[e] : 0u;
+                code[e] = xb[(int64_t)min((int)s_cf[kk], d - 1) * ldb + i0 + e];
+            }
+            const uint4 wx = reinterpret_cast<const uint4 *>(w + i0)[0];
+            const uint4 wy = reinterpret_cast<const uint4 *>(w + i0)[1];
+            const uint32_t wb[kHistE] = {wx.x, wx.y, wx.z, wx.w, wy.x, wy.y, wy.z, wy.w};
+            uint2 vs = make_uint2(0u, 0u);
+            if (SIGNED) vs = *reinterpret_cast<const uint2 *>(vsign + i0);
+            uint32_t o[2] = {0u, 0u};
+            uint32_t below = 0u;
+#pragma unroll
+            for (int e = 0; e < kHistE; ++e) {
+                uint32_t p = par[e], kk = k[e];
+                bool stop = false;
+                if (kk >= half) {
+                    const bool earlier = miss & (p < half);
+                    stop = earlier;
+                    if (!earlier) eflag |= kErrRoute;
+                    kk = 0u;
+                    p = earlier ? p : half;
+                }
+                stop |= miss & (code[e] == (uint32_t)kMissingCode);
+                const uint32_t ne = stop ? p : 2u * p + (code[e] >= s_cc[kk] ? 1u : 0u);
+                o[e >> 2] |= ne << (8 * (e & 3));
+                const uint32_t ab = wb[e] & 0x7fffffffu;
+                if (ab != 0u && !stop) {
+                    // counted once: the node's entries (on the grid) or,
+                    // rarely, its events below the grid
+                    const uint32_t nl = ne - nodes;
+                    if (ab < tau_bits) {
+                        below |= 1u << e;
+                        atomicAdd(&s_ncnt[nl], 1u);
+                    } else {
+                        rec[st][e] = nl << 16 | atomicAdd(&s_cnt[nl], 1u);
+                    }
+                }
+                if (SIGNED && byte8(vs, e)) negs[st] |= 1u << e;
+            }
+            *reinterpret_cast<uint2 *>(node_out + i0) = make_uint2(o[0], o[1]);
+            if (below) {   // rare: weights below the grid, every feature's side histogram
+                for (int e = 0; e < kHistE; ++e) {
+                    if (!((below >> e) & 1u)) continue;
+                    const uint32_t ne = byte8(make_uint2(o[0], o[1]), e);
+                    const uint32_t bits = __float_as_uint(w[i0 + e]);
+                    double wa = (double)__uint_as_float(bits & 0x7fffffffu);
+                    if ((negs[st] >> e) & 1u) wa = -wa;
+                    for (int j = 0; j < d; ++j) {
+                        const uint32_t bin = xb[(int64_t)j * ldb + i0 + e];
+                        if (bin < (uint32_t)nbins) {
+                            const size_t gi =
+                                ((((size_t)(ne - nodes) * d + j) * nbins + bin) * 2) + (bits >> 31);
+                            atomicAdd(&small[gi], wa);
+                        } else if (!(miss && bin == (uint32_t)kMissingCode)) {
+                            eflag |= kErrBin;
+                        }
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < (unsigned)nslots) {
+        const uint32_t c = s_cnt[threadIdx.x];
+        s_base[threadIdx.x] = c ? atomicAdd(&cursor[threadIdx.x], c) : 0u;
+    } else if (cnt_out && threadIdx.x >= kListMaxSlots &&
+               threadIdx.x < kListMaxSlots + (unsigned)nodes) {
+        const uint32_t t = threadIdx.x - kListMaxSlots;
+        const uint32_t c = s_cnt[t] + s_ncnt[t];
+        if (c) atomicAdd(&cnt_out[t], c);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int st = 0; st < kRouteListSteps; ++st) {
+        const int64_t i0 = base_i + ((int64_t)st * kRouteListThreads + threadIdx.x) * kHistE;
+        if (i0 < end_i) {
+            // the weights again (in L2), rather than held in registers across
+            // the reservation
+            const uint4 wx = reinterpret_cast<const uint4 *>(w + i0)[0];
+            const uint4 wy = reinterpret_cast<const uint4 *>(w + i0)[1];
+            const uint32_t wb[kHistE] = {wx.x, wx.y, wx.z, wx.w, wy.x, wy.y, wy.z, wy.w};
+#pragma unroll
+            for (int e = 0; e < kHistE; ++e) {
+                const uint32_t r = rec[st][e];
+                if (r != ~0u) {
+                    const uint32_t slot = r >> 16;
+                    const uint32_t pos = s_base[slot] + (r & 0xffffu);
+                    // the caps bound every count; an entry beyond one is an error
+                    if (pos < s_cap[slot])
+                        list[(size_t)s_start[slot] + pos] = make_uint2(
+                            (uint32_t)(i0 + e) | (((negs[st] >> e) & 1u) << 31), wb[e]);
+                    else
+                        eflag |= kErrRoute;
+                }
+            }
+        }
+    }
+    if (eflag) atomicOr(err, eflag);
+}
+
+// Histogram pass over the lists.  The histogrammed lists: with sib the
+// shorter of the two children's lists of each parent (flag = the right one;
+// the other child is parent - child, formed by the cut scan), else every
+// node's.  Each feature group's `parts` workgroups (parts > lists) share
+// the entries of those lists: with E entries in all, list k of m_k entries
+// gets C_k = ceil(m_k / ceil(E / (parts - lists))) equal parts (none when
+// empty), numbered from base_k = C_0 + ... + C_(k-1); the C_k add up to at
+// most parts.  Workgroup 0 records {base_k, C_k | flag << 31} in lchunks
+// for the cut scan.  Workgroup (part, feature group g) adds its part of its list
+// for the features [g FPG, g FPG + FPG) into its LDS rows (one per feature,
+// 256 bins x 2 classes of 64-bit fixed-point counters, as in the streaming
+// pass); each entry's codes are FPG / 4 words of the event's row in xr
+// (stride dr).  Every entry is on the grid (route_list_kernel sends the
+// others to the side histogram).  Rows are written out prefix-summed to
+// partial[base_k + part][feature][bin][class].  The feature groups of one
+// part run on one XCD, so that the event rows the first reads are in that
+// XCD's L2 for the others.
+template <int FPG, bool SIGNED>
+__global__ __launch_bounds__(1024) void hist_list_kernel(
+    const uint2 *__restrict__ list, const uint32_t *__restrict__ lstart,
+    const uint32_t *__restrict__ lcap, const uint32_t *__restrict__ cursor,
+    const uint8_t *__restrict__ xr, int dr, int d, int nbins, bool miss, int G, int parts,
+    int nlists, bool sib, int per_xcd, int scale, int copies, int copy_stride,
+    uint2 *__restrict__ lchunks, uint64_t *__restrict__ partial, int *__restrict__ err) {
+    constexpr int NQ = FPG / 4;
+    // the rows take all of the LDS (40 features: 160 KiB); the prologue's
+    // few words sit at its start until the rows are cleared
+    extern __shared__ uint64_t lds[];
+    uint32_t *hdr = reinterpret_cast<uint32_t *>(lds);
+    const int q = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int w = q / G;   // part slot of this workgroup
+    if (wave == 0) {
+        // list k's length, first entry and flag; parts per list from the total
+        uint32_t m = 0u, first = 0u, flag = 0u;
+        if (lane < nlists) {
+            const int a = sib ? 2 * lane : lane;
+            const uint32_t ma = min(cursor[a], lcap[a]);
+            m = ma;
+            first = lstart[a];
+            if (sib) {
+                const uint32_t mb = min(cursor[a + 1], lcap[a + 1]);
+                flag = mb < ma ? 1u : 0u;
+                if (flag) {
+                    m = mb;
+                    first = lstart[a + 1];
+                }
+            }
+        }
+        uint64_t tot = m;
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) tot += __shfl_xor(tot, o);
+        const uint64_t target = tot > 0 ? (tot + (parts - nlists) - 1) / (parts - nlists) : 1;
+        const uint32_t c = (uint32_t)((m + target - 1) / target);
+        uint32_t x = c;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const uint32_t y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+        }
+        if (lane < nlists && blockIdx.x == 0) lchunks[lane] = make_uint2(x - c, c | flag << 31);
+        // the list whose parts hold part slot w, if any
+        const bool mine = lane < nlists && (uint32_t)w >= x - c && (uint32_t)w < x;
+        const uint64_t any = __ballot(mine);   // every lane of the wavefront votes
+        if (lane == 0) hdr[0] = any != 0ull ? 1u : 0u;
+        if (mine) {
+            hdr[1] = w - (x - c);   // part within the list
+            hdr[2] = c;
+            hdr[3] = m;
+            hdr[4] = first;
+            hdr[5] = x - c;
+        }
+    }
+    __syncthreads();
+    const bool used = hdr[0] != 0u && q < G * parts;
+    const uint32_t c = hdr[1], pbase = hdr[5];
+    const uint64_t m = hdr[3], C = hdr[2], first = hdr[4];
+    __syncthreads();   // the header is read before the rows are cleared over it
+    if (!used) return;   // an unused part slot
+    const int g = q % G;
+    const int j0 = g * FPG;
+    const int nf = min(FPG, d - j0);
+    const int qbase = j0 / 4, qmax = dr / 4 - 1;
+    const int lds_n = FPG * kRow;
+    uint64_t *const lds_lane = reinterpret_cast<uint64_t *>(
+        reinterpret_cast<char *>(lds) + (lane & (copies - 1)) * copy_stride);
+    {
+        uint4 *l4 = reinterpret_cast<uint4 *>(lds);
+        const int n16 = copies > 1 ? copies * copy_stride / 16 : lds_n / 2;
+        for (int t = threadIdx.x; t < n16; t += blockDim.x) l4[t] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    const int64_t lo = (int64_t)(first + m * c / C);
+    const int64_t hi = (int64_t)(first + m * (c + 1) / C);
+    const int64_t T = blockDim.x;
+    lds_barrier();
+
+    char *ldsb = reinterpret_cast<char *>(lds_lane);
+    auto add = [&](const uint2 en, const uint32_t (&cw)[NQ]) {
+        const uint32_t bits = en.y;
+        const uint32_t ab = bits & 0x7fffffffu;
+        const int sh = (int)(ab >> 23) - 150 + scale;   // >= 0 on the grid
+        uint64_t fx = (uint64_t)((ab & 0x7fffffu) | 0x800000u) << sh;
+        if (SIGNED && (en.x >> 31)) fx = 0ull - fx;
+        const uint32_t base = (bits >> 28) & 8u;
+#pragma unroll
+        for (int ff = 0; ff < FPG; ++ff) {
+            if (ff < nf) {   // (uniform) the last group may hold fewer features
+                const uint32_t off = base + (((cw[ff >> 2] >> (8 * (ff & 3))) & 0xffu) << 4);
+                atomicAdd(reinterpret_cast<uint64_t *>(ldsb + off) + ff * kRow, fx);
+            }
+        }
+    };
+    auto codes = [&](const uint2 en, uint32_t (&cw)[NQ]) {
+        const uint32_t *row =
+            reinterpret_cast<const uint32_t *>(xr + (size_t)(en.x & 0x7fffffffu) * dr);
+#pragma unroll
+        for (int qq = 0; qq < NQ; ++qq) cw[qq] = row[min(qbase + qq, qmax)];
+    };
+    // two entries per thread and step; the next step's entries are loaded
+    // while this step's codes arrive and are added
+    int64_t ja = lo + threadIdx.x;
+    uint2 ea = make_uint2(0u, 0u), eb = make_uint2(0u, 0u);
+    if (ja < hi) ea = list[ja];
+    if (ja + T < hi) eb = list[ja + T];
+    while (ja < hi) {
+        const bool has_b = ja + T < hi;
+        uint32_t ca[NQ], cb[NQ];
+        codes(ea, ca);
+        if (has_b) codes(eb, cb);
+        const int64_t jn = ja + 2 * T;
+        uint2 na = make_uint2(0u, 0u), nb = make_uint2(0u, 0u);
+        if (jn < hi) na = list[jn];
+        if (jn + T < hi) nb = list[jn + T];
+        add(ea, ca);
+        if (has_b) add(eb, cb);
+        ja = jn;
+        ea = na;
+        eb = nb;
+    }
+    lds_barrier();
+    int eflag = 0;
+    hist_write_rows(lds, copies, copy_stride, lds_n, 1, nf, FPG, 0, j0, d, nbins, miss, true,
+                    reinterpret_cast<uint4 *>(partial + (size_t)(pbase + c) * d * nbins * 2),
+                    eflag);
     if (eflag) atomicOr(err, eflag);
 }
 
@@ -2228,6 +2637,12 @@ hipError_t allow_hist_lds(size_t max_lds) {
     return hipSuccess;
 }
 
+template <int FPG>
+hipError_t allow_list_lds(size_t max_lds) {
+    const hipError_t a = allow_lds(hist_list_kernel<FPG, false>, max_lds);
+    return a != hipSuccess ? a : allow_lds(hist_list_kernel<FPG, true>, max_lds);
+}
+
 hipError_t prepare_kernels(size_t max_lds) {
     const hipError_t e[] = {allow_hist_lds<1>(max_lds), allow_hist_lds<2>(max_lds),
                             allow_hist_lds<4>(max_lds), allow_hist_lds<5>(max_lds),
@@ -2251,7 +2666,11 @@ hipError_t prepare_kernels(size_t max_lds) {
                             allow_lds(apply_float_kernel<6>, max_lds),
                             allow_lds(apply_float_kernel<7>, max_lds),
                             allow_lds(importance_kernel, max_lds),
-                            allow_lds(hist_reference_kernel, max_lds)};
+                            allow_lds(hist_reference_kernel, max_lds),
+                            allow_list_lds<4>(max_lds), allow_list_lds<8>(max_lds),
+                            allow_list_lds<12>(max_lds), allow_list_lds<20>(max_lds),
+                            allow_list_lds<28>(max_lds), allow_list_lds<36>(max_lds),
+                            allow_list_lds<40>(max_lds)};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;
@@ -2565,17 +2984,18 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
 hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
                            double *small_next, size_t small_next_count, int hnodes, int d,
                            int n_bins, bool sibling, double *cand_gain, int *cand_cut,
-                           const uint64_t *hparent, uint64_t *hout, hipStream_t s) {
+                           const uint64_t *hparent, uint64_t *hout, hipStream_t s,
+                           const uint2 *lchunks) {
     const int S = cut_slices(n_bins);
     const int blocks = hnodes * d * S;
     if (sibling)
         cut_scan_kernel<true><<<blocks, kCutWaves * kWave, 0, s>>>(
             partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,
-            cand_gain, cand_cut, hparent, hout);
+            cand_gain, cand_cut, hparent, hout, lchunks);
     else
         cut_scan_kernel<false><<<blocks, kCutWaves * kWave, 0, s>>>(
             partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,
-            cand_gain, cand_cut, nullptr, hout);
+            cand_gain, cand_cut, nullptr, hout, lchunks);
     return hipGetLastError();
 }
 
@@ -2651,6 +3071,134 @@ hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
     route_layer_kernel<<<(unsigned)(kXcds * per), 256, 0, s>>>(
         xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut, pc.slices, pc.rec_f,
         pc.rec_c, pc.rec_g, layer, miss, err, R);
+    return hipGetLastError();
+}
+
+bool list_fpg_supported(int f) {
+    for (int c : kListFpgSizes)
+        if (c == f) return true;
+    return false;
+}
+
+int list_row_bytes(int d) { return (d + 3) & ~3; }
+
+size_t list_codes_bytes(int64_t n, int d) {
+    return (size_t)((n + 255) / 256) * 256 * (size_t)list_row_bytes(d);
+}
+
+hipError_t launch_transpose_codes(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *xr,
+                                  hipStream_t s) {
+    const int dr = list_row_bytes(d);
+    if (d < 1 || dr > 256 || n < 1) return hipErrorInvalidValue;
+    transpose_codes_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(xb, ldb, n, d, xr, dr);
+    return hipGetLastError();
+}
+
+ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, int fpg,
+                              int parts, int copies) {
+    ListShape ls{};
+    // the fewest feature groups whose rows fit the LDS (one row of 256 bins
+    // x 2 classes per feature; the kernel has no static LDS), then the
+    // smallest built group size that covers d in that many groups
+    int f = fpg;
+    if (f <= 0) {
+        int fmax = kListFpgSizes[0];
+        for (int c : kListFpgSizes)
+            if ((size_t)c * kRowBytes <= max_lds) fmax = c;
+        const int g = (d + fmax - 1) / fmax;
+        const int need = (d + g - 1) / g;
+        f = fmax;
+        for (int c : kListFpgSizes)
+            if (c >= need) {
+                f = c;
+                break;
+            }
+    }
+    ls.fpg = f;
+    ls.groups = (d + f - 1) / f;
+    ls.lists = lists;
+    // about one workgroup per CU (parts per feature group), shared among the
+    // lists in proportion to their lengths; more than `lists` of them
+    int c = parts > 0 ? parts : cu_count / ls.groups;
+    if (c < lists + 1) c = lists + 1;
+    ls.parts = c;
+    const int total = c * ls.groups;
+    ls.per_xcd = (total + kXcds - 1) / kXcds;
+    ls.blocks = kXcds * ls.per_xcd;
+    const size_t one = (size_t)f * kRowBytes;
+    int cp = copies > 0 ? copies : 1;
+    while (cp > 1 && (size_t)cp * (one + kHistCopyShift) > max_lds) cp >>= 1;
+    ls.copies = cp;
+    ls.copy_stride = cp > 1 ? (int)(one + kHistCopyShift) : (int)one;
+    ls.lds_bytes = cp > 1 ? (size_t)cp * ls.copy_stride : one;
+    return ls;
+}
+
+hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, int n_bins,
+                             const uint8_t *node_in, uint8_t *node_out, const float *w,
+                             const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
+                             int scale, const uint32_t *cap_prev, uint32_t cap_root,
+                             uint32_t *cnt_out, uint32_t *cursor, uint32_t *lstart,
+                             uint32_t *lcap, uint2 *list, double *small, int *err,
+                             hipStream_t s) {
+    if (layer < 1 || layer > 6 || n < 1 || n > kListMaxEvents) return hipErrorInvalidValue;
+    if ((layer == 1) != (node_in == nullptr) || (layer == 1) != (cap_prev == nullptr))
+        return hipErrorInvalidValue;
+    if ((1 << layer) > kListMaxSlots) return hipErrorInvalidValue;
+    const uint32_t tau_bits = (uint32_t)(127 + 23 - scale) << 23;   // 2^(23 - scale)
+    if (23 - scale < -126) return hipErrorInvalidValue;
+    const int64_t R = xcd_range(n);
+    const unsigned blocks = (unsigned)(kXcds * ((R + kRouteListEvents - 1) / kRouteListEvents));
+    if (vsign)
+        route_list_kernel<true><<<blocks, kRouteListThreads, 0, s>>>(
+            xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut,
+            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, tau_bits, cap_prev,
+            cap_root, cnt_out, cursor, lstart, lcap, list, small, err, R);
+    else
+        route_list_kernel<false><<<blocks, kRouteListThreads, 0, s>>>(
+            xb, ldb, n, d, n_bins, node_in, node_out, w, nullptr, pc.cand_gain, pc.cand_cut,
+            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, tau_bits, cap_prev,
+            cap_root, cnt_out, cursor, lstart, lcap, list, small, err, R);
+    return hipGetLastError();
+}
+
+template <int FPG>
+void hist_list_go(const ListShape &ls, bool sib, bool signed_w, hipStream_t s, const uint2 *list,
+                  const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
+                  const uint8_t *xr, int dr, int d, int nbins, int scale, uint2 *lchunks,
+                  uint64_t *partial, int *err) {
+    const bool miss = nbins <= kMissingCode;
+    if (signed_w)
+        hist_list_kernel<FPG, true><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
+            list, lstart, lcap, cursor, xr, dr, d, nbins, miss, ls.groups, ls.parts, ls.lists,
+            sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+    else
+        hist_list_kernel<FPG, false><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
+            list, lstart, lcap, cursor, xr, dr, d, nbins, miss, ls.groups, ls.parts, ls.lists,
+            sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+}
+
+hipError_t launch_hist_list(const ListShape &ls, bool sib, const uint2 *list,
+                            const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
+                            const uint8_t *xr, int d, int n_bins, bool signed_w, int scale,
+                            uint2 *lchunks, uint64_t *partial, int *err, hipStream_t s) {
+    // sib: lists of 2 lists nodes (the shorter child of each parent is histogrammed)
+    if (ls.lists < 1 || (sib ? 2 : 1) * ls.lists > kListMaxSlots || ls.groups * ls.fpg < d ||
+        ls.parts <= ls.lists || ls.blocks != kXcds * ls.per_xcd ||
+        ls.per_xcd * kXcds < ls.parts * ls.groups ||
+        (ls.copies & (ls.copies - 1)) != 0 || ls.lds_bytes < (size_t)ls.fpg * kRowBytes)
+        return hipErrorInvalidValue;
+    const int dr = list_row_bytes(d);
+    switch (ls.fpg) {
+    case 4: hist_list_go<4>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 8: hist_list_go<8>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 12: hist_list_go<12>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 20: hist_list_go<20>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 28: hist_list_go<28>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 36: hist_list_go<36>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 40: hist_list_go<40>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

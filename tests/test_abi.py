@@ -58,6 +58,16 @@ def test_argument_errors_need_no_device():
     assert L.fbdt_set_option(b"hist_copies", 3) == -1
     assert L.fbdt_set_option(b"hist_copies", 4) == 0
     assert L.fbdt_set_option(b"hist_copies", 0) == 0
+    # event lists below the root: auto, off or on; list passes are built for
+    # 4, 8, 12, 20, 28 or 36 features per workgroup
+    assert L.fbdt_set_option(b"hist_lists", 3) == -1
+    assert L.fbdt_set_option(b"hist_lists", 0) == 0
+    assert L.fbdt_set_option(b"list_features_per_group", 5) == -1
+    assert L.fbdt_set_option(b"list_features_per_group", 20) == 0
+    assert L.fbdt_set_option(b"list_features_per_group", 0) == 0
+    assert L.fbdt_set_option(b"list_copies", 3) == -1
+    assert L.fbdt_set_option(b"list_parts", 4097) == -1
+    assert L.fbdt_set_option(b"list_parts", 0) == 0
 
 
 def test_bench_refuses_more_than_one_gpu():

@@ -1,0 +1,174 @@
+"""Parity of the list-driven histogram layers (the layers below the root of
+large fits: a route pass that appends each counted event to its node's list,
+then a pass over the lists with the codes read from an event-major copy)
+with the CPU oracle, and with the streaming pass on the same data.
+
+The fits here force the lists on (option hist_lists = 2) at sizes where the
+library would stream; the full-size fits of 10M events take them by
+default.  Tolerances as in test_gpu_parity: cuts exact (up to adopted
+near-ties), gains, boost weights and scores to relative 1e-9, P to 1e-5.
+With the fixed-point sums exact and order-free, a list fit and a streaming
+fit of the same sample give the same model bit for bit unless weights fall
+below the fixed-point grid (float64 side histograms, summed in another
+order).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_1609_06119_amd as fb
+from oracle import fbdt_oracle as O
+from synth import CONFIGS, make_training_set
+
+pytestmark = pytest.mark.gpu
+
+LIST_OPTIONS = ("hist_lists", "list_features_per_group", "list_parts", "list_copies")
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.fixture(autouse=True)
+def _defaults():
+    for name in LIST_OPTIONS:
+        fb.set_option(name, 0)
+    fb.set_option("fit_graphs", 1)
+    yield
+    for name in LIST_OPTIONS:
+        fb.set_option(name, 0)
+    fb.set_option("fit_graphs", 1)
+
+
+def _with_missing(x, seed):
+    """NaN in features in turn 0 %, 3 %, 20 % and 60 % of the time, and the
+    last feature NaN throughout (section 4.2)."""
+    rng = np.random.default_rng(seed)
+    x = np.array(x, np.float32)
+    d, n = x.shape
+    for j in range(d):
+        x[j, rng.random(n) < (0.0, 0.03, 0.2, 0.6)[j % 4]] = np.nan
+    x[d - 1] = np.nan
+    return x
+
+
+def _oracle_model(m):
+    return O.Model(m["depth"], m["n_bins"], m["n_features"], m["f0"], m["cut_feature"],
+                   m["cut_bin"], m["gain"], m["leaf"], m.get("inner"))
+
+
+CASES = {
+    "config4-200k-depth6": dict(cfg=4, n_events=200_000, n_trees=3),
+    "config3-100k-depth3": dict(cfg=3, n_events=100_000, n_trees=12),
+    "config2-30k-depth2": dict(cfg=2, n_events=30_011, depth=2, n_trees=6),
+    "depth7-B128": dict(cfg=3, n_events=40_013, depth=7, n_bins=128, n_trees=2, subsample=1.0),
+    "negative-weights-depth6": dict(cfg=4, n_events=60_013, depth=6, n_trees=2,
+                                    weights="signed"),
+    # the smallest weights fall below the fixed-point grid: the route pass
+    # adds them to the side histograms of both children
+    "weights-1e-12-to-1e3": dict(cfg=2, n_events=30_011, n_trees=5, weights="wide"),
+    "17-events-depth6-B4": dict(cfg=4, n_events=17, depth=6, n_bins=4, n_trees=2),
+    "two-events-depth3": dict(cfg=1, n_events=2, depth=3, n_trees=3, subsample=1.0),
+    # parts of the lists and feature groups other than the planner's: 40
+    # features in groups of 12 (the last holds 4) with 37 parts per group;
+    # groups of 4 with the fewest parts (one more than the lists) and 4 LDS
+    # copies
+    "config4-60k-fpg12-parts37": dict(cfg=4, n_events=60_013, depth=5, n_trees=2, fpg=12,
+                                      parts=37),
+    "config2-30k-fpg4-parts1-copies4": dict(cfg=2, n_events=30_011, depth=4, n_trees=3, fpg=4,
+                                            parts=1, copies=4),
+    # missing values: both children histogrammed, stopped events in no list
+    "nan-config4-60k-depth6-B255": dict(cfg=4, n_events=60_013, n_bins=255, n_trees=3,
+                                        missing=True),
+    "nan-depth7-B64": dict(cfg=2, n_events=40_009, depth=7, n_bins=64, n_trees=2,
+                           missing=True),
+    "nan-negative-weights-depth4": dict(cfg=2, n_events=30_011, depth=4, n_trees=4, n_bins=64,
+                                        weights="signed", missing=True),
+}
+
+
+def _weights(kind, n, v):
+    if kind == "signed":
+        return np.random.default_rng(9).uniform(-0.6, 2.5, n).astype(np.float32)
+    if kind == "wide":
+        return (10.0 ** np.random.default_rng(9).uniform(-12, 3, n)).astype(np.float32)
+    return v
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_list_fit_matches_oracle_and_streaming_fit(case):
+    c = CASES[case]
+    spec = CONFIGS[c["cfg"]]
+    ds = make_training_set(c["cfg"], n_events=c.get("n_events"))
+    x = _with_missing(ds["x"], 7) if c.get("missing") else ds["x"]
+    d, n = x.shape
+    B = c.get("n_bins", spec.n_bins)
+    D = c.get("depth", spec.depth)
+    T = c.get("n_trees", spec.n_trees)
+    alpha = c.get("subsample", spec.subsample)
+    eta, seed = spec.shrinkage, spec.fit_seed
+    v = _weights(c.get("weights"), n, ds["v"])
+    say(f"list fit {case}: n={n} d={d} B={B} D={D} T={T} alpha={alpha}")
+    _, codes = fb.bin(dev(x), B)
+    _, xb = O.bin_features(x, B)
+    assert np.array_equal(codes.numpy(), xb)
+    y = dev(ds["y"])
+    runs = {}
+    for mode in ("lists", "streaming"):
+        fb.set_option("hist_lists", 2 if mode == "lists" else 1)
+        fb.set_option("list_features_per_group", c.get("fpg", 0) if mode == "lists" else 0)
+        fb.set_option("list_parts", c.get("parts", 0) if mode == "lists" else 0)
+        fb.set_option("list_copies", c.get("copies", 0) if mode == "lists" else 0)
+        score = torch.empty(n, dtype=torch.float64, device="cuda")
+        model = fb.fit(codes, y, B, D, T, eta, alpha, seed, w=dev(v), score_out=score)
+        runs[mode] = (model, model.export(), score.cpu().numpy())
+    model, gm, Fg = runs["lists"]
+    _, sm, Fs = runs["streaming"]
+    exact = c.get("weights") != "wide"
+    for key in ("cut_feature", "cut_bin"):
+        assert np.array_equal(gm[key], sm[key]), key
+    for key in ("gain", "leaf") + (("inner",) if c.get("missing") else ()):
+        if exact:
+            assert np.array_equal(gm[key], sm[key]), key
+        else:
+            assert np.allclose(gm[key], sm[key], rtol=1e-12, atol=0.0), key
+    assert np.array_equal(Fg, Fs) if exact else np.allclose(Fg, Fs, rtol=1e-12, atol=1e-15)
+    say(f"  oracle fit {case}")
+    log = O.TieLog()
+    om, F = O.fit(xb, ds["y"], v, D, T, eta, alpha, seed, B, reference=_oracle_model(gm),
+                  tie_log=log, final_score=True)
+    say(f"  near-ties adopted: {len(log.adopted)}  rejected: {len(log.rejected)}")
+    assert log.rejected == []
+    assert np.array_equal(gm["cut_feature"], om.cut_feature)
+    assert np.array_equal(gm["cut_bin"], om.cut_bin)
+    assert abs(gm["f0"] - om.f0) <= 1e-12
+    assert np.allclose(gm["gain"], om.gain, rtol=1e-9, atol=1e-12 * n)
+    assert np.allclose(gm["leaf"], om.leaf, rtol=1e-9, atol=1e-13)
+    if c.get("missing"):
+        assert np.allclose(gm["inner"], om.inner, rtol=1e-9, atol=1e-13)
+    assert np.allclose(Fg, F, rtol=1e-9, atol=1e-12)
+    p = fb.apply(model, codes).cpu().numpy()
+    op, _ = O.apply(om, xb)
+    assert np.max(np.abs(p.astype(np.float64) - op)) <= 1e-5
+
+
+def test_list_fit_graph_replays_match_eager_fit():
+    """The list layers inside the captured boosting loop (the per-tree
+    counter fill is a kernel) give the eager fit's model on every replay."""
+    ds = make_training_set(4, n_events=60_013)
+    _, codes = fb.bin(dev(ds["x"]), 256)
+    y, v = dev(ds["y"]), dev(ds["v"])
+    fb.set_option("hist_lists", 2)
+    fb.set_option("fit_graphs", 0)
+    ref = fb.fit(codes, y, 256, 6, 3, 0.1, 0.5, 4, w=v).export()
+    fb.set_option("fit_graphs", 1)
+    for rep in range(3):
+        got = fb.fit(codes, y, 256, 6, 3, 0.1, 0.5, 4, w=v).export()
+        torch.cuda.synchronize()
+        for key in ("cut_feature", "cut_bin", "gain", "leaf"):
+            assert np.array_equal(got[key], ref[key]), (rep, key)
+
