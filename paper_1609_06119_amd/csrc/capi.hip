@@ -353,8 +353,8 @@ double hist_algorithmic_bytes(int64_t n, int d, int n_bins, int layer, bool rout
 }
 
 // Bytes a list pass of layer `layer` needs at the least: for each expected
-// entry (a sampled event, alpha n of them at the root, at most half of them
-// in the shorter children with sib) its 8-byte entry and d codes, plus the
+// entry (a sampled event, alpha n of them at the root, about half of them
+// in the listed children with sib) its 8-byte entry and d codes, plus the
 // histograms written.
 double list_algorithmic_bytes(int64_t n, double alpha, int d, int n_bins, int layer, bool sib) {
     const double entries = alpha * (double)n * (sib ? 0.5 : 1.0);
@@ -625,7 +625,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                             pl[l].lds_bytes, di.max_lds);
         }
     }
-    // layers 1 .. D-1 of large fits histogram event lists (the shorter child
+    // layers 1 .. D-1 of large fits histogram event lists (the lighter child
     // of every parent, or with missing values every node of the layer)
     const int64_t lists_opt = opt_hist_lists.load();
     const bool lists = D >= 2 && npad <= kListMaxEvents &&
@@ -684,20 +684,22 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     cv.add(&fb.cut_bin, (size_t)T * nin);
     cv.add(&fb.gain, (size_t)T * nin);
     cv.add(&fb.leaf, (size_t)T * slots_max);
-    // event lists: the event-major codes, the lists (each node's list holds
-    // at most its parent's sampled events, so two per sampled event), per
-    // layer 64 cursors + 64 node counts, the lists' starts and caps, and the
-    // histogrammed lists' partial rows for the cut scan
+    // event lists: the event-major codes, the lists (a list holds at most
+    // the sampled events of its node's parent: one list per parent, or with
+    // missing values two), per layer 64 cursors + 64 node counts, the lists'
+    // starts, caps and listed children, and their partial rows for the cut
+    // scan
     uint8_t *xr = nullptr;
     uint2 *list = nullptr, *lchunks = nullptr;
-    uint32_t *lctr = nullptr, *lstart = nullptr, *lcap = nullptr;
+    uint32_t *lctr = nullptr, *lstart = nullptr, *lcap = nullptr, *lside = nullptr;
     const size_t lctr_count = (size_t)D * 2 * kListMaxSlots;
     if (lists) {
         cv.add(&xr, list_codes_bytes(n, d));
-        cv.add(&list, (size_t)2 * npad);
+        cv.add(&list, (size_t)(may_miss ? 2 : 1) * npad);
         cv.add(&lctr, lctr_count);
         cv.add(&lstart, kListMaxSlots);
         cv.add(&lcap, kListMaxSlots);
+        cv.add(&lside, kListMaxSlots);
         cv.add(&lchunks, kListMaxSlots);
     }
     // phase timeline of every histogram launch (measurement option)
@@ -793,16 +795,17 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                         Timed tm(FBDT_K_ROUTE, st, 3.0 * (double)n);
                         HIP_TRY(launch_route_list(
                             xb, ldb, n, d, n_bins, l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
-                            fb.node[l & 1], fb.w, vsign, pc, l, n_bins <= kMissingCode, scale,
-                            cap_prev, (uint32_t)npad, l + 1 < D ? ctr + kListMaxSlots : nullptr,
-                            ctr, lstart, lcap, list, fb.small[gl & 1], fb.err, st));
+                            fb.node[l & 1], fb.w, vsign, pc, l, n_bins <= kMissingCode,
+                            missing ? nullptr : fb.hfull[(l - 1) & 1], scale, cap_prev,
+                            (uint32_t)npad, l + 1 < D ? ctr + kListMaxSlots : nullptr, ctr,
+                            lstart, lcap, lside, list, fb.small[gl & 1], fb.err, st));
                         tm.done();
                     }
                     {
                         Timed tm(FBDT_K_HISTOGRAM, st,
                                  list_algorithmic_bytes(n, alpha, d, n_bins, l, !missing));
-                        HIP_TRY(launch_hist_list(ls, !missing, list, lstart, lcap, ctr, xr, d,
-                                                 n_bins, vsign != nullptr, scale, lchunks,
+                        HIP_TRY(launch_hist_list(ls, !missing, list, lstart, lcap, ctr, lside, xr,
+                                                 d, n_bins, vsign != nullptr, scale, lchunks,
                                                  fb.partial, fb.err, st));
                         tm.done();
                     }

@@ -319,31 +319,35 @@ struct ListShape {
 ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, int fpg,
                               int parts, int copies);
 
-// Routing of layer `layer` in [1, 6] with list output: every node of the
-// layer gets a list.  node_in: ids of layer - 1 (null at layer 1: all
-// events at the root); node_out receives the ids of the layer for
-// round_up(n, 8) events.  w, vsign as for launch_histogram.  cap_prev:
-// sampled events per node of layer - 1 (null at layer 1: cap_root for the
-// root); cnt_out (optional, zeroed): receives the sampled events per node
-// of this layer; cursor [2^layer] (zeroed): receives the entries per list;
-// lstart / lcap [2^layer]: each list's range in `list` (2 cap_root entries
-// at most); small: the layer's side histogram [2^layer][d][B][2].
+// Routing of layer `layer` in [1, 6] with list output.  node_in: ids of
+// layer - 1 (null at layer 1: all events at the root); node_out receives the
+// ids of the layer for round_up(n, 8) events.  w, vsign as for
+// launch_histogram.  hparent (fits without missing values): the summed
+// prefix rows [2^(layer-1)][d][B][2] of the parents; one child per parent
+// is listed, the lighter one (lside[k] = 1: the right child of parent k),
+// list k = parent k; hparent null: every node of the layer is listed.
+// cap_prev: sampled events per node of layer - 1 (null at layer 1: cap_root
+// for the root); cnt_out (optional, zeroed): receives the sampled events per
+// node of this layer; cursor [lists] (zeroed): receives the entries per
+// list; lstart / lcap [lists]: each list's range in `list` (at most cap_root
+// entries with hparent, else 2 cap_root); small: the layer's side histogram
+// [2^layer][d][B][2].
 hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, int n_bins,
                              const uint8_t *node_in, uint8_t *node_out, const float *w,
                              const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
-                             int scale, const uint32_t *cap_prev, uint32_t cap_root,
-                             uint32_t *cnt_out, uint32_t *cursor, uint32_t *lstart,
-                             uint32_t *lcap, uint2 *list, double *small, int *err,
-                             hipStream_t s);
-// Histograms of the lists of launch_route_list (sib: of the shorter child
-// of each of ls.lists parents; else of all ls.lists nodes) into
-// prefix-summed partials [ls.parts][d][B][2], with lchunks
-// [ls.lists] = {first part, parts | right child histogrammed << 31} for the
-// cut scan.
+                             const uint64_t *hparent, int scale, const uint32_t *cap_prev,
+                             uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
+                             uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
+                             double *small, int *err, hipStream_t s);
+// Histograms of the ls.lists lists of launch_route_list (sib: one child per
+// parent, lside from the route pass; else every node) into prefix-summed
+// partials [ls.parts][d][B][2], with lchunks [ls.lists] = {first part,
+// parts | right child histogrammed << 31} for the cut scan.
 hipError_t launch_hist_list(const ListShape &ls, bool sib, const uint2 *list,
                             const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
-                            const uint8_t *xr, int d, int n_bins, bool signed_w, int scale,
-                            uint2 *lchunks, uint64_t *partial, int *err, hipStream_t s);
+                            const uint32_t *lside, const uint8_t *xr, int d, int n_bins,
+                            bool signed_w, int scale, uint2 *lchunks, uint64_t *partial, int *err,
+                            hipStream_t s);
 
 // Forest traversal.  cuts: [T][2^D-1] packed (feature | bin << 8), for the
 // general kernel; nodes: [T][16] for depth <= kApplyShallowDepth, for heap

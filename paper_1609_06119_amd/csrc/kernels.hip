@@ -1802,15 +1802,19 @@ __global__ __launch_bounds__(256) void transpose_codes_kernel(const uint8_t *__r
 // event whose code of the cut feature is the missing code, or which stopped
 // earlier, keeps its node (section 4.2).  A sampled event that has not
 // stopped is counted into cnt_out[node - 2^layer] (the caps of the next
-// layer's lists) and, if its weight is on the fixed-point grid (|w| >= tau),
-// appended to its node's list as {event | negative << 31, weight bits}
-// (both children are listed: the histogram pass picks the shorter list of
-// each parent).  Node k's list is the range [start_k, start_k + cap_k) of
-// `list`: cap_k = the sampled events of its parent (cap_prev, or cap_root at
-// layer 1), start_k = the caps of the nodes below k; workgroup 0 records
-// both (lstart, lcap).  Each workgroup counts its entries per node in LDS
-// and reserves them with one atomic add per node on cursor[k], so a list
-// holds its events in no fixed order (the
+// layer's lists) and, if its weight is on the fixed-point grid (|w| >= tau)
+// and its node is listed, appended to the node's list as {event | negative
+// << 31, weight bits}.  Listed: with sib one child of every parent, the one
+// whose fixed-point weight in the parent's summed rows hparent is smaller
+// (lside[k] = 1: the right child; the histogram pass takes it and the cut
+// scan forms the other as parent - child), list k = parent k; else every
+// node of the layer, list k = node k.  List k is the range [start_k,
+// start_k + cap_k) of `list`: cap_k = the sampled events of its node's
+// parent (cap_prev, or cap_root at layer 1), start_k = the caps of the lists
+// below k; workgroup 0 records both (lstart, lcap) and lside.  Each
+// workgroup counts its entries per list in LDS and reserves them with one
+// atomic add per list on cursor[k], so a list holds its events in no fixed
+// order (the
 // fixed-point sums do not depend on it).  Sampled weights below the grid go
 // to the float64 side histogram `small` [2^layer][d][B][2] here, for either
 // child and every feature, as the streaming pass adds them.
@@ -1824,15 +1828,16 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     const float *__restrict__ w, const uint8_t *__restrict__ vsign,
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
-    int layer, bool miss, uint32_t tau_bits, const uint32_t *__restrict__ cap_prev,
-    uint32_t cap_root, uint32_t *__restrict__ cnt_out, uint32_t *__restrict__ cursor,
-    uint32_t *__restrict__ lstart, uint32_t *__restrict__ lcap, uint2 *__restrict__ list,
-    double *__restrict__ small, int *__restrict__ err, int64_t xcd_events) {
-    __shared__ uint8_t s_cf[64], s_cc[64];
+    int layer, bool miss, bool sib, const uint64_t *__restrict__ hparent, uint32_t tau_bits,
+    const uint32_t *__restrict__ cap_prev, uint32_t cap_root, uint32_t *__restrict__ cnt_out,
+    uint32_t *__restrict__ cursor, uint32_t *__restrict__ lstart, uint32_t *__restrict__ lcap,
+    uint32_t *__restrict__ lside, uint2 *__restrict__ list, double *__restrict__ small,
+    int *__restrict__ err, int64_t xcd_events) {
+    __shared__ uint8_t s_cf[64], s_cc[64], s_side[64];
     __shared__ uint32_t s_cnt[kListMaxSlots], s_ncnt[kListMaxSlots];
     __shared__ uint32_t s_start[kListMaxSlots], s_cap[kListMaxSlots], s_base[kListMaxSlots];
     const uint32_t half = 1u << (layer - 1), nodes = 1u << layer;
-    const int nslots = (int)nodes;
+    const int nslots = sib ? (int)half : (int)nodes;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int nwaves = blockDim.x / kWave;
     int eflag = 0;
@@ -1851,12 +1856,23 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
                 rec_c[k] = (uint8_t)bc;
                 rec_g[k] = bg;
             }
+            uint32_t side = 0u;
+            if (sib) {
+                // weights (signal + background, fixed point) left of the cut
+                // and in all, from the parent's prefix-summed row of its feature
+                const uint64_t *row = hparent + ((size_t)k * d + bf) * nbins * 2;
+                const int64_t left = (int64_t)(row[2 * (bc - 1)] + row[2 * (bc - 1) + 1]);
+                const int64_t all = (int64_t)(row[2 * (nbins - 1)] + row[2 * (nbins - 1) + 1]);
+                side = all - left < left ? 1u : 0u;
+            }
+            s_side[k] = (uint8_t)side;
+            if (blockIdx.x == 0 && sib) lside[k] = side;
         }
     }
     if (wave == nwaves - 1) {
         // caps and starts of the lists: an exclusive scan of the caps
         uint32_t cap = 0u;
-        if (lane < nslots) cap = cap_prev ? cap_prev[lane >> 1] : cap_root;
+        if (lane < nslots) cap = cap_prev ? cap_prev[sib ? lane : lane >> 1] : cap_root;
         uint32_t x = cap;
 #pragma unroll
         for (int o = 1; o < kWave; o <<= 1) {
@@ -1925,14 +1941,16 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
                 o[e >> 2] |= ne << (8 * (e & 3));
                 const uint32_t ab = wb[e] & 0x7fffffffu;
                 if (ab != 0u && !stop) {
-                    // counted once: the node's entries (on the grid) or,
-                    // rarely, its events below the grid
+                    // counted once: as an entry of its list (listed node, on
+                    // the grid), else into its node's other events
                     const uint32_t nl = ne - nodes;
-                    if (ab < tau_bits) {
-                        below |= 1u << e;
-                        atomicAdd(&s_ncnt[nl], 1u);
+                    const bool listed = !sib || (nl & 1u) == s_side[kk];
+                    if (ab < tau_bits) below |= 1u << e;
+                    if (listed && ab >= tau_bits) {
+                        const uint32_t slot = sib ? kk : nl;
+                        rec[st][e] = slot << 16 | atomicAdd(&s_cnt[slot], 1u);
                     } else {
-                        rec[st][e] = nl << 16 | atomicAdd(&s_cnt[nl], 1u);
+                        atomicAdd(&s_ncnt[nl], 1u);
                     }
                 }
                 if (SIGNED && byte8(vs, e)) negs[st] |= 1u << e;
@@ -1966,7 +1984,10 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     } else if (cnt_out && threadIdx.x >= kListMaxSlots &&
                threadIdx.x < kListMaxSlots + (unsigned)nodes) {
         const uint32_t t = threadIdx.x - kListMaxSlots;
-        const uint32_t c = s_cnt[t] + s_ncnt[t];
+        // node t's sampled events: its other events, plus its list's entries
+        // if it is the listed node
+        const bool listed = !sib || (t & 1u) == s_side[t >> 1];
+        const uint32_t c = s_ncnt[t] + (listed ? s_cnt[sib ? t >> 1 : t] : 0u);
         if (c) atomicAdd(&cnt_out[t], c);
     }
     __syncthreads();
@@ -1998,10 +2019,9 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     if (eflag) atomicOr(err, eflag);
 }
 
-// Histogram pass over the lists.  The histogrammed lists: with sib the
-// shorter of the two children's lists of each parent (flag = the right one;
-// the other child is parent - child, formed by the cut scan), else every
-// node's.  Each feature group's `parts` workgroups (parts > lists) share
+// Histogram pass over the lists of route_list_kernel: with sib one child
+// of every parent (lside[k] = 1: the right one; the cut scan forms the other
+// as parent - child), else every node of the layer.  Each feature group's `parts` workgroups (parts > lists) share
 // the entries of those lists: with E entries in all, list k of m_k entries
 // gets C_k = ceil(m_k / ceil(E / (parts - lists))) equal parts (none when
 // empty), numbered from base_k = C_0 + ... + C_(k-1); the C_k add up to at
@@ -2019,9 +2039,10 @@ template <int FPG, bool SIGNED>
 __global__ __launch_bounds__(1024) void hist_list_kernel(
     const uint2 *__restrict__ list, const uint32_t *__restrict__ lstart,
     const uint32_t *__restrict__ lcap, const uint32_t *__restrict__ cursor,
-    const uint8_t *__restrict__ xr, int dr, int d, int nbins, bool miss, int G, int parts,
-    int nlists, bool sib, int per_xcd, int scale, int copies, int copy_stride,
-    uint2 *__restrict__ lchunks, uint64_t *__restrict__ partial, int *__restrict__ err) {
+    const uint32_t *__restrict__ lside, const uint8_t *__restrict__ xr, int dr, int d,
+    int nbins, bool miss, int G, int parts, int nlists, bool sib, int per_xcd, int scale,
+    int copies, int copy_stride, uint2 *__restrict__ lchunks, uint64_t *__restrict__ partial,
+    int *__restrict__ err) {
     constexpr int NQ = FPG / 4;
     // the rows take all of the LDS (40 features: 160 KiB); the prologue's
     // few words sit at its start until the rows are cleared
@@ -2034,18 +2055,9 @@ __global__ __launch_bounds__(1024) void hist_list_kernel(
         // list k's length, first entry and flag; parts per list from the total
         uint32_t m = 0u, first = 0u, flag = 0u;
         if (lane < nlists) {
-            const int a = sib ? 2 * lane : lane;
-            const uint32_t ma = min(cursor[a], lcap[a]);
-            m = ma;
-            first = lstart[a];
-            if (sib) {
-                const uint32_t mb = min(cursor[a + 1], lcap[a + 1]);
-                flag = mb < ma ? 1u : 0u;
-                if (flag) {
-                    m = mb;
-                    first = lstart[a + 1];
-                }
-            }
+            m = min(cursor[lane], lcap[lane]);
+            first = lstart[lane];
+            flag = sib ? lside[lane] : 0u;
         }
         uint64_t tot = m;
 #pragma unroll
@@ -3137,10 +3149,10 @@ ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, in
 hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, int n_bins,
                              const uint8_t *node_in, uint8_t *node_out, const float *w,
                              const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
-                             int scale, const uint32_t *cap_prev, uint32_t cap_root,
-                             uint32_t *cnt_out, uint32_t *cursor, uint32_t *lstart,
-                             uint32_t *lcap, uint2 *list, double *small, int *err,
-                             hipStream_t s) {
+                             const uint64_t *hparent, int scale, const uint32_t *cap_prev,
+                             uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
+                             uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
+                             double *small, int *err, hipStream_t s) {
     if (layer < 1 || layer > 6 || n < 1 || n > kListMaxEvents) return hipErrorInvalidValue;
     if ((layer == 1) != (node_in == nullptr) || (layer == 1) != (cap_prev == nullptr))
         return hipErrorInvalidValue;
@@ -3152,51 +3164,53 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
     if (vsign)
         route_list_kernel<true><<<blocks, kRouteListThreads, 0, s>>>(
             xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut,
-            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, tau_bits, cap_prev,
-            cap_root, cnt_out, cursor, lstart, lcap, list, small, err, R);
+            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, hparent != nullptr, hparent,
+            tau_bits, cap_prev, cap_root, cnt_out, cursor, lstart, lcap, lside, list, small, err,
+            R);
     else
         route_list_kernel<false><<<blocks, kRouteListThreads, 0, s>>>(
             xb, ldb, n, d, n_bins, node_in, node_out, w, nullptr, pc.cand_gain, pc.cand_cut,
-            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, tau_bits, cap_prev,
-            cap_root, cnt_out, cursor, lstart, lcap, list, small, err, R);
+            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, hparent != nullptr, hparent,
+            tau_bits, cap_prev, cap_root, cnt_out, cursor, lstart, lcap, lside, list, small, err,
+            R);
     return hipGetLastError();
 }
 
 template <int FPG>
 void hist_list_go(const ListShape &ls, bool sib, bool signed_w, hipStream_t s, const uint2 *list,
                   const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
-                  const uint8_t *xr, int dr, int d, int nbins, int scale, uint2 *lchunks,
-                  uint64_t *partial, int *err) {
+                  const uint32_t *lside, const uint8_t *xr, int dr, int d, int nbins, int scale,
+                  uint2 *lchunks, uint64_t *partial, int *err) {
     const bool miss = nbins <= kMissingCode;
     if (signed_w)
         hist_list_kernel<FPG, true><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
-            list, lstart, lcap, cursor, xr, dr, d, nbins, miss, ls.groups, ls.parts, ls.lists,
-            sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+            list, lstart, lcap, cursor, lside, xr, dr, d, nbins, miss, ls.groups, ls.parts,
+            ls.lists, sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
     else
         hist_list_kernel<FPG, false><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
-            list, lstart, lcap, cursor, xr, dr, d, nbins, miss, ls.groups, ls.parts, ls.lists,
-            sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+            list, lstart, lcap, cursor, lside, xr, dr, d, nbins, miss, ls.groups, ls.parts,
+            ls.lists, sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
 }
 
 hipError_t launch_hist_list(const ListShape &ls, bool sib, const uint2 *list,
                             const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
-                            const uint8_t *xr, int d, int n_bins, bool signed_w, int scale,
-                            uint2 *lchunks, uint64_t *partial, int *err, hipStream_t s) {
-    // sib: lists of 2 lists nodes (the shorter child of each parent is histogrammed)
-    if (ls.lists < 1 || (sib ? 2 : 1) * ls.lists > kListMaxSlots || ls.groups * ls.fpg < d ||
+                            const uint32_t *lside, const uint8_t *xr, int d, int n_bins,
+                            bool signed_w, int scale, uint2 *lchunks, uint64_t *partial, int *err,
+                            hipStream_t s) {
+    if (ls.lists < 1 || ls.lists > kListMaxSlots || ls.groups * ls.fpg < d ||
         ls.parts <= ls.lists || ls.blocks != kXcds * ls.per_xcd ||
         ls.per_xcd * kXcds < ls.parts * ls.groups ||
         (ls.copies & (ls.copies - 1)) != 0 || ls.lds_bytes < (size_t)ls.fpg * kRowBytes)
         return hipErrorInvalidValue;
     const int dr = list_row_bytes(d);
     switch (ls.fpg) {
-    case 4: hist_list_go<4>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 8: hist_list_go<8>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 12: hist_list_go<12>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 20: hist_list_go<20>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 28: hist_list_go<28>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 36: hist_list_go<36>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 40: hist_list_go<40>(ls, sib, signed_w, s, list, lstart, lcap, cursor, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 4: hist_list_go<4>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 8: hist_list_go<8>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 12: hist_list_go<12>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 20: hist_list_go<20>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 28: hist_list_go<28>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 36: hist_list_go<36>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 40: hist_list_go<40>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
