@@ -338,11 +338,12 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
  * builds the histograms of the layers below the root (sections 1.1, 2.1).
  * 1 streams every event through every layer's pass; 2 has each layer's
  * routing pass append the sampled events of one child of every parent (the
- * one with less weight in the parent's histograms) to per-parent lists, or
- * with missing values those of every node, and histograms the lists, the
- * codes read from an event-major copy of the code matrix (n * round_up(d, 4)
- * bytes of device workspace, plus 8 bytes per event for the lists, 16 with
- * missing values); fits need n < 2^31 for it.  Both give the same model bit
+ * one with less weight in the parent's histograms) to per-parent lists,
+ * with missing values (section 4.2) also the events that stop at the parent
+ * to a list of their own, and histograms the lists, the codes read from an
+ * event-major copy of the code matrix (n * round_up(d, 4) bytes of device
+ * workspace, plus 8 bytes per event for the lists, 16 with missing values);
+ * the other child is the parent minus the lists.  Fits need n < 2^31 for it.  Both give the same model bit
  * for bit, except for the rounding of sums of weights below the
  * fixed-point grid.  "list_features_per_group" (4, 8, 12, 20, 28, 36 or
  * 40), "list_parts" (workgroups per feature group, at most 4096) and

@@ -788,6 +788,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 if (lists && l >= 1) {
                     // route with list output, then histogram the lists
                     const ListShape &ls = lplans[l];
+                    const int lmode = missing ? kCutStopped : kCutSibling;
                     uint32_t *ctr = lctr + (size_t)l * 2 * kListMaxSlots;
                     const uint32_t *cap_prev =
                         l >= 2 ? lctr + (size_t)(l - 1) * 2 * kListMaxSlots + kListMaxSlots : nullptr;
@@ -795,31 +796,30 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                         Timed tm(FBDT_K_ROUTE, st, 3.0 * (double)n);
                         HIP_TRY(launch_route_list(
                             xb, ldb, n, d, n_bins, l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
-                            fb.node[l & 1], fb.w, vsign, pc, l, n_bins <= kMissingCode,
-                            missing ? nullptr : fb.hfull[(l - 1) & 1], scale, cap_prev,
-                            (uint32_t)npad, l + 1 < D ? ctr + kListMaxSlots : nullptr, ctr,
-                            lstart, lcap, lside, list, fb.small[gl & 1], fb.err, st));
+                            fb.node[l & 1], fb.w, vsign, pc, l, n_bins <= kMissingCode, lmode,
+                            fb.hfull[(l - 1) & 1], scale, cap_prev, (uint32_t)npad,
+                            l + 1 < D ? ctr + kListMaxSlots : nullptr, ctr, lstart, lcap, lside,
+                            list, fb.small[gl & 1], fb.err, st));
                         tm.done();
                     }
                     {
                         Timed tm(FBDT_K_HISTOGRAM, st,
                                  list_algorithmic_bytes(n, alpha, d, n_bins, l, !missing));
-                        HIP_TRY(launch_hist_list(ls, !missing, list, lstart, lcap, ctr, lside, xr,
-                                                 d, n_bins, vsign != nullptr, scale, lchunks,
+                        HIP_TRY(launch_hist_list(ls, lmode, list, lstart, lcap, ctr, lside, xr, d,
+                                                 n_bins, vsign != nullptr, scale, lchunks,
                                                  fb.partial, fb.err, st));
                         tm.done();
                     }
                     {
                         Timed tm(FBDT_K_BEST_CUTS, st);
-                        const bool sib = !missing;
                         const size_t next_count =
                             (size_t)(l + 1 < D ? 1 << (l + 1) : 1) * d * n_bins * 2;
                         HIP_TRY(launch_cut_scan(fb.partial, 0, scale, fb.small[gl & 1],
                                                 fb.small[(gl + 1) & 1], next_count, ls.lists, d,
-                                                n_bins, sib, fb.cand_gain, fb.cand_cut,
-                                                sib ? fb.hfull[(l - 1) & 1] : nullptr,
-                                                l + 1 < D && !missing ? fb.hfull[l & 1] : nullptr,
-                                                st, lchunks));
+                                                n_bins, lmode, fb.cand_gain, fb.cand_cut,
+                                                fb.hfull[(l - 1) & 1],
+                                                l + 1 < D ? fb.hfull[l & 1] : nullptr, st,
+                                                lchunks));
                         tm.done();
                     }
                     continue;
@@ -850,19 +850,20 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                 {
                     Timed tm(FBDT_K_BEST_CUTS, st);
                     // right children below the root: parent - left child (the
-                    // parents' summed rows are kept for that); the next layer's
-                    // side histogram (next tree's root after the last layer) is
+                    // parents' summed rows are kept for that; fits with missing
+                    // values histogram both children); the next layer's side
+                    // histogram (next tree's root after the last layer) is
                     // cleared on the way
                     const bool sib = plans[l].sibling;
+                    const int cmode = sib ? kCutSibling : kCutPlain;
                     const size_t next_count =
                         (size_t)(l + 1 < D ? 1 << (l + 1) : 1) * d * n_bins * 2;
                     HIP_TRY(launch_cut_scan(fb.partial, plans[l].chunks, scale, fb.small[gl & 1],
                                             fb.small[(gl + 1) & 1], next_count,
-                                            sib ? 1 << (l - 1) : 1 << l, d, n_bins, sib,
+                                            sib ? 1 << (l - 1) : 1 << l, d, n_bins, cmode,
                                             fb.cand_gain, fb.cand_cut,
-                                            sib ? fb.hfull[(l - 1) & 1] : nullptr,
-                                            l + 1 < D && !missing ? fb.hfull[l & 1] : nullptr,
-                                            st));
+                                            cmode != kCutPlain ? fb.hfull[(l - 1) & 1] : nullptr,
+                                            l + 1 < D ? fb.hfull[l & 1] : nullptr, st));
                     tm.done();
                 }
             }

@@ -218,20 +218,27 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
                                 double *cand_gain, int *cand_cut, hipStream_t s);
 
 // Best cuts of a layer in the fit from the prefix-summed fixed-point chunk
-// partials of the routed histogram pass (hnodes histogrammed nodes, chunks
-// partials) plus the float64 side histogram `small` of the layer, into
-// cand_gain/cand_cut [layer nodes][d * cut_slices(B)].  sibling (layers
-// below the root): the partials are the left children of hnodes parents and
-// hparent [hnodes][d][B][2] their summed prefix rows; the right child is
-// parent - left.  hout (optional) receives the summed prefix rows of every
-// node of the layer.  Clears small_next[0, small_next_count) (the next
-// layer's side histogram).  lchunks (list passes): the partials of
-// histogrammed node k are the rows [x_k, x_k + (y_k & 0x7fffffff)) of
-// [*][d][B][2], and with sibling bit 31 of y_k tells that they hold the
-// right child (the left is parent - right).
+// partials of the histogram pass (hnodes slots, chunks partials) plus the
+// float64 side histogram `small` of the layer, into cand_gain/cand_cut
+// [layer nodes][d * cut_slices(B)].  mode kCutSibling (layers below the
+// root): slot k holds the left child of parent k and hparent [parents][d][B]
+// [2] the parents' summed prefix rows; the right child is parent - left.
+// kCutStopped: slot 2k the left child, slot 2k + 1 the events that stopped
+// at parent k; the right child is parent - left - stopped.  hout (optional)
+// receives the summed prefix rows of every node of the layer.  Clears
+// small_next[0, small_next_count) (the next layer's side histogram).
+// lchunks (list passes): the partials of slot k are the rows [x_k, x_k +
+// (y_k & 0x7fffffff)) of [*][d][B][2], and bit 31 of y_k tells that a
+// child slot holds the right child (the left is then the one formed).
+enum CutMode : int {
+    kCutPlain = 0,     // slot k holds node k
+    kCutSibling = 1,   // slot k holds one child of parent k, the other is parent - child
+    kCutStopped = 2,   // slot 2k holds one child of parent k, slot 2k + 1 the events that
+                       // stopped at k; the other child is parent - child - stopped
+};
 hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
                            double *small_next, size_t small_next_count, int hnodes, int d,
-                           int n_bins, bool sibling, double *cand_gain, int *cand_cut,
+                           int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
                            const uint2 *lchunks = nullptr);
 
@@ -322,10 +329,11 @@ ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, in
 // Routing of layer `layer` in [1, 6] with list output.  node_in: ids of
 // layer - 1 (null at layer 1: all events at the root); node_out receives the
 // ids of the layer for round_up(n, 8) events.  w, vsign as for
-// launch_histogram.  hparent (fits without missing values): the summed
-// prefix rows [2^(layer-1)][d][B][2] of the parents; one child per parent
-// is listed, the lighter one (lside[k] = 1: the right child of parent k),
-// list k = parent k; hparent null: every node of the layer is listed.
+// launch_histogram.  lmode kCutSibling: one child per parent is listed, the
+// lighter one in the parents' summed prefix rows hparent [2^(layer-1)][d]
+// [B][2] (lside[k] = 1: the right child of parent k), list k = parent k;
+// kCutStopped (missing values): that child in list 2k and the events that
+// stop at parent k in list 2k + 1; kCutPlain: every node of the layer.
 // cap_prev: sampled events per node of layer - 1 (null at layer 1: cap_root
 // for the root); cnt_out (optional, zeroed): receives the sampled events per
 // node of this layer; cursor [lists] (zeroed): receives the entries per
@@ -335,15 +343,16 @@ ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, in
 hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, int n_bins,
                              const uint8_t *node_in, uint8_t *node_out, const float *w,
                              const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
-                             const uint64_t *hparent, int scale, const uint32_t *cap_prev,
+                             int lmode, const uint64_t *hparent, int scale,
+                             const uint32_t *cap_prev,
                              uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
                              uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
                              double *small, int *err, hipStream_t s);
-// Histograms of the ls.lists lists of launch_route_list (sib: one child per
-// parent, lside from the route pass; else every node) into prefix-summed
-// partials [ls.parts][d][B][2], with lchunks [ls.lists] = {first part,
-// parts | right child histogrammed << 31} for the cut scan.
-hipError_t launch_hist_list(const ListShape &ls, bool sib, const uint2 *list,
+// Histograms of the ls.lists lists of launch_route_list (lmode as there,
+// lside from the route pass) into prefix-summed partials [ls.parts][d][B]
+// [2], with lchunks [ls.lists] = {first part, parts | right child
+// histogrammed << 31} for the cut scan.
+hipError_t launch_hist_list(const ListShape &ls, int lmode, const uint2 *list,
                             const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
                             const uint32_t *lside, const uint8_t *xr, int d, int n_bins,
                             bool signed_w, int scale, uint2 *lchunks, uint64_t *partial, int *err,

@@ -1196,10 +1196,14 @@ __global__ __launch_bounds__(kWave) void best_cuts_f64_kernel(const double *__re
 // The workgroup's wavefronts sum the chunks round-robin (integer sums: exact
 // in any order); wavefront 0 then evaluates the slice's cuts and writes the
 // slice's candidate (entry j * S + q of the node, gain highest, then lowest
-// bin).  With SIB (layers below the root) the partials are the left children
-// of the parents and wavefront 1 evaluates the right child, parent - left,
-// from the parents' summed rows (hparent).  hout receives the summed rows of
-// every node of the layer (the next layer's parents).
+// bin).  Below the root (kCutSibling) a workgroup takes a parent: the
+// partials are one child of each parent (the left one, or as the list pass
+// flags it the right one), wavefronts 0 and 1 evaluate the left and right
+// children, and the other child is formed as parent - child from the
+// parents' summed rows (hparent).  With missing values (kCutStopped, section
+// 4.2) the events that stopped at the parent have partials of their own and
+// the other child is parent - child - stopped.  hout receives the summed
+// rows of every node of the layer (the next layer's parents).
 //
 // The side histogram (float64 sums of the weights below the fixed-point
 // grid, per node of the layer, plain bins) is added after a prefix scan when
@@ -1214,7 +1218,7 @@ __global__ __launch_bounds__(kWave) void best_cuts_f64_kernel(const double *__re
 constexpr int kCutSlice = 31;
 constexpr int kCutWaves = 4;
 
-template <bool SIB>
+template <int MODE>   // CutMode
 __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     const uint64_t *__restrict__ partial, int chunks, int scale, const double *__restrict__ small,
     double *__restrict__ small_next, size_t small_next_count, int hnodes, int d, int nbins, int S,
@@ -1222,45 +1226,54 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout,
     const uint2 *__restrict__ lchunks) {
 #pragma clang fp contract(off)
+    constexpr bool PAIR = MODE != kCutPlain;   // both children of a parent per workgroup
     __shared__ uint64_t red[kCutWaves][kWave + 2];
+    __shared__ uint64_t red_stop[MODE == kCutStopped ? kCutWaves : 1][kWave + 2];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int q = blockIdx.x % S;
     const int kj = blockIdx.x / S;
     const int j = kj % d;
-    const int k = kj / d;   // histogrammed node (the parent with SIB)
+    const int k = kj / d;   // histogrammed node, or with PAIR the parent
     const size_t row = (size_t)nbins * 2;
     const int wi = lane >> 1, cls = lane & 1;
     const int b = kCutSlice * q - 1 + wi;   // this lane's window bin
     const bool inb = b >= 0 && b < nbins;
-    // partials of the streaming pass: [chunks][hnodes][d][B][2]; of the
-    // list pass (lchunks): chunk c of list k at [base_k + c][d][B][2], and
-    // with SIB the flag tells that the right child was histogrammed
-    uint32_t lbase = 0u, flag = 0u;
+    // slots: the histogrammed child (or node) and, with kCutStopped, the
+    // events that stopped at the parent.  Partials of the streaming pass:
+    // [chunks][hnodes][d][B][2]; of the list pass (lchunks): chunk c of slot
+    // s at [base_s + c][d][B][2], and the flag of a child slot tells that it
+    // holds the right child
+    const int cslot = MODE == kCutStopped ? 2 * k : k;
+    uint32_t cbase = (uint32_t)cslot, sbase = (uint32_t)cslot + 1u, flag = 0u;
+    int cchunks = chunks, schunks = MODE == kCutStopped ? chunks : 0;
     if (lchunks) {
-        const uint2 lc = lchunks[k];
-        lbase = lc.x;
-        chunks = (int)(lc.y & 0x7fffffffu);
+        const uint2 lc = lchunks[cslot];
+        cbase = lc.x;
+        cchunks = (int)(lc.y & 0x7fffffffu);
         flag = lc.y >> 31;
+        if (MODE == kCutStopped) {
+            const uint2 ls = lchunks[cslot + 1];
+            sbase = ls.x;
+            schunks = (int)(ls.y & 0x7fffffffu);
+        }
     }
     // offsets of this lane's window bin and of the row total within a row
-    // [k][j] of the parents' rows, and within the first chunk's partial row
+    // [k][j] of the parents' rows, and within the first chunk's partial rows
     const size_t off = ((size_t)k * d + j) * row;
-    const size_t offv = off + (size_t)(inb ? b : 0) * 2 + cls;
-    const size_t offt = off + (size_t)(nbins - 1) * 2 + cls;
-    const size_t poff = lchunks ? ((size_t)lbase * d + j) * row : off;
-    const size_t pv_off = poff + (size_t)(inb ? b : 0) * 2 + cls;
-    const size_t pt_off = poff + (size_t)(nbins - 1) * 2 + cls;
+    const size_t wv = (size_t)(inb ? b : 0) * 2 + cls, wt = (size_t)(nbins - 1) * 2 + cls;
+    const size_t coff = ((size_t)cbase * d + j) * row, soff = ((size_t)sbase * d + j) * row;
     const size_t stride_p = lchunks ? (size_t)d * row : (size_t)hnodes * d * row;
     // node of this wavefront's candidates, as an index within the layer; with
-    // SIB wavefront `sub` forms its node as parent - the histogrammed child
-    const int node = SIB ? 2 * k + (wave & 1) : k;
+    // PAIR wavefront `sub` forms its node as parent - the histogrammed child
+    // (- the stopped events)
+    const int node = PAIR ? 2 * k + (wave & 1) : k;
     const int sub = flag ? 0 : 1;
     const size_t noff = ((size_t)node * d + j) * row;
 
     // side histogram row of the candidate wavefronts' node: lane l holds bins
     // 4l..4l+3, both classes (loaded first, in flight with the chunk sums)
     double sd[8];
-    const bool cwave = wave < (SIB ? 2 : 1);
+    const bool cwave = wave < (PAIR ? 2 : 1);
     if (cwave) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -1269,31 +1282,39 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         }
     }
     uint64_t pv = 0, pt = 0;   // parent row (other child = parent - histogrammed child)
-    if (SIB && wave == sub) {
-        pv = hparent[offv];
-        pt = hparent[offt];
+    if (PAIR && wave == sub) {
+        pv = hparent[off + wv];
+        pt = hparent[off + wt];
     }
     // chunk sums: wavefront w takes chunks w, w + kCutWaves, ...
-    uint64_t v = 0, vt = 0;
-    {
+    auto chunk_sums = [&](size_t base_off, int nch, uint64_t &v, uint64_t &vt) {
+        const size_t ov = base_off + wv, ot = base_off + wt;
         int p = wave;
-        for (; p + 3 * kCutWaves < chunks; p += 4 * kCutWaves) {
+        for (; p + 3 * kCutWaves < nch; p += 4 * kCutWaves) {
             const uint64_t *b0 = partial + (size_t)p * stride_p;
             const uint64_t *b1 = b0 + kCutWaves * stride_p;
             const uint64_t *b2 = b1 + kCutWaves * stride_p;
             const uint64_t *b3 = b2 + kCutWaves * stride_p;
-            const uint64_t x0 = b0[pv_off], x1 = b1[pv_off], x2 = b2[pv_off], x3 = b3[pv_off];
-            const uint64_t t0 = b0[pt_off], t1 = b1[pt_off], t2 = b2[pt_off], t3 = b3[pt_off];
+            const uint64_t x0 = b0[ov], x1 = b1[ov], x2 = b2[ov], x3 = b3[ov];
+            const uint64_t t0 = b0[ot], t1 = b1[ot], t2 = b2[ot], t3 = b3[ot];
             v += (x0 + x1) + (x2 + x3);
             vt += (t0 + t1) + (t2 + t3);
         }
-        for (; p < chunks; p += kCutWaves) {
-            v += partial[(size_t)p * stride_p + pv_off];
-            vt += partial[(size_t)p * stride_p + pt_off];
+        for (; p < nch; p += kCutWaves) {
+            v += partial[(size_t)p * stride_p + ov];
+            vt += partial[(size_t)p * stride_p + ot];
         }
-    }
+    };
+    uint64_t v = 0, vt = 0;
+    chunk_sums(coff, cchunks, v, vt);
     red[wave][lane] = v;
     if (lane < 2) red[wave][kWave + lane] = vt;
+    if (MODE == kCutStopped) {
+        uint64_t sv = 0, st = 0;
+        chunk_sums(soff, schunks, sv, st);
+        red_stop[wave][lane] = sv;
+        if (lane < 2) red_stop[wave][kWave + lane] = st;
+    }
     // this workgroup's share of the next layer's side histogram
     {
         const size_t per = (small_next_count + gridDim.x - 1) / gridDim.x;
@@ -1309,11 +1330,18 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         P += red[w][lane];
         T += red[w][kWave + cls];
     }
-    if (!inb) P = 0;
-    if (SIB && wave == sub) {   // the other child = parent - histogrammed child (exact)
-        P = (inb ? pv : 0) - P;
+    if (PAIR && wave == sub) {   // the other child = parent - histogrammed child (exact)
+        P = pv - P;
         T = pt - T;
+        if (MODE == kCutStopped) {   // - the events that stopped at the parent (exact)
+#pragma unroll
+            for (int w = 0; w < kCutWaves; ++w) {
+                P -= red_stop[w][lane];
+                T -= red_stop[w][kWave + cls];
+            }
+        }
     }
+    if (!inb) P = 0;
     if (hout && wi >= 1 && inb) hout[noff + 2 * b + cls] = P;
     // the row total P(B-1), which the windows do not reach when B > 31 S
     if (hout && q == S - 1 && lane < 2) hout[noff + 2 * (nbins - 1) + cls] = T;
@@ -1804,11 +1832,14 @@ __global__ __launch_bounds__(256) void transpose_codes_kernel(const uint8_t *__r
 // stopped is counted into cnt_out[node - 2^layer] (the caps of the next
 // layer's lists) and, if its weight is on the fixed-point grid (|w| >= tau)
 // and its node is listed, appended to the node's list as {event | negative
-// << 31, weight bits}.  Listed: with sib one child of every parent, the one
-// whose fixed-point weight in the parent's summed rows hparent is smaller
-// (lside[k] = 1: the right child; the histogram pass takes it and the cut
-// scan forms the other as parent - child), list k = parent k; else every
-// node of the layer, list k = node k.  List k is the range [start_k,
+// << 31, weight bits}.  Listed: with lmode kCutSibling one child of every
+// parent, the one whose fixed-point weight in the parent's summed rows
+// hparent is smaller (lside[k] = 1: the right child; the histogram pass
+// takes it and the cut scan forms the other as parent - child), list k =
+// parent k; with kCutStopped that child in list 2k and the events that stop
+// at parent k here (on the grid) in list 2k + 1 (the other child is parent -
+// child - stopped); with kCutPlain every node of the layer, list k = node k.
+// List k is the range [start_k,
 // start_k + cap_k) of `list`: cap_k = the sampled events of its node's
 // parent (cap_prev, or cap_root at layer 1), start_k = the caps of the lists
 // below k; workgroup 0 records both (lstart, lcap) and lside.  Each
@@ -1828,7 +1859,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     const float *__restrict__ w, const uint8_t *__restrict__ vsign,
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
-    int layer, bool miss, bool sib, const uint64_t *__restrict__ hparent, uint32_t tau_bits,
+    int layer, bool miss, int lmode, const uint64_t *__restrict__ hparent, uint32_t tau_bits,
     const uint32_t *__restrict__ cap_prev, uint32_t cap_root, uint32_t *__restrict__ cnt_out,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ lstart, uint32_t *__restrict__ lcap,
     uint32_t *__restrict__ lside, uint2 *__restrict__ list, double *__restrict__ small,
@@ -1837,6 +1868,8 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     __shared__ uint32_t s_cnt[kListMaxSlots], s_ncnt[kListMaxSlots];
     __shared__ uint32_t s_start[kListMaxSlots], s_cap[kListMaxSlots], s_base[kListMaxSlots];
     const uint32_t half = 1u << (layer - 1), nodes = 1u << layer;
+    const bool sib = lmode == kCutSibling, stops = lmode == kCutStopped;
+    const bool pick = sib || stops;   // one child of each parent listed
     const int nslots = sib ? (int)half : (int)nodes;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int nwaves = blockDim.x / kWave;
@@ -1857,7 +1890,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
                 rec_g[k] = bg;
             }
             uint32_t side = 0u;
-            if (sib) {
+            if (pick) {
                 // weights (signal + background, fixed point) left of the cut
                 // and in all, from the parent's prefix-summed row of its feature
                 const uint64_t *row = hparent + ((size_t)k * d + bf) * nbins * 2;
@@ -1866,7 +1899,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
                 side = all - left < left ? 1u : 0u;
             }
             s_side[k] = (uint8_t)side;
-            if (blockIdx.x == 0 && sib) lside[k] = side;
+            if (blockIdx.x == 0 && pick) lside[k] = side;
         }
     }
     if (wave == nwaves - 1) {
@@ -1928,9 +1961,9 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
 #pragma unroll
             for (int e = 0; e < kHistE; ++e) {
                 uint32_t p = par[e], kk = k[e];
-                bool stop = false;
+                bool stop = false, earlier = false;
                 if (kk >= half) {
-                    const bool earlier = miss & (p < half);
+                    earlier = miss & (p < half);
                     stop = earlier;
                     if (!earlier) eflag |= kErrRoute;
                     kk = 0u;
@@ -1944,14 +1977,17 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
                     // counted once: as an entry of its list (listed node, on
                     // the grid), else into its node's other events
                     const uint32_t nl = ne - nodes;
-                    const bool listed = !sib || (nl & 1u) == s_side[kk];
+                    const bool listed = !pick || (nl & 1u) == s_side[kk];
                     if (ab < tau_bits) below |= 1u << e;
                     if (listed && ab >= tau_bits) {
-                        const uint32_t slot = sib ? kk : nl;
+                        const uint32_t slot = sib ? kk : stops ? 2u * kk : nl;
                         rec[st][e] = slot << 16 | atomicAdd(&s_cnt[slot], 1u);
                     } else {
                         atomicAdd(&s_ncnt[nl], 1u);
                     }
+                } else if (stops && stop && !earlier && ab >= tau_bits) {
+                    // stops at parent kk here: its list of stopped events
+                    rec[st][e] = (2u * kk + 1u) << 16 | atomicAdd(&s_cnt[2u * kk + 1u], 1u);
                 }
                 if (SIGNED && byte8(vs, e)) negs[st] |= 1u << e;
             }
@@ -1986,8 +2022,8 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
         const uint32_t t = threadIdx.x - kListMaxSlots;
         // node t's sampled events: its other events, plus its list's entries
         // if it is the listed node
-        const bool listed = !sib || (t & 1u) == s_side[t >> 1];
-        const uint32_t c = s_ncnt[t] + (listed ? s_cnt[sib ? t >> 1 : t] : 0u);
+        const bool listed = !pick || (t & 1u) == s_side[t >> 1];
+        const uint32_t c = s_ncnt[t] + (listed ? s_cnt[sib ? t >> 1 : stops ? t & ~1u : t] : 0u);
         if (c) atomicAdd(&cnt_out[t], c);
     }
     __syncthreads();
@@ -2019,9 +2055,11 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     if (eflag) atomicOr(err, eflag);
 }
 
-// Histogram pass over the lists of route_list_kernel: with sib one child
-// of every parent (lside[k] = 1: the right one; the cut scan forms the other
-// as parent - child), else every node of the layer.  Each feature group's `parts` workgroups (parts > lists) share
+// Histogram pass over the lists of route_list_kernel: with lmode
+// kCutSibling one child of every parent (lside[k] = 1: the right one; the
+// cut scan forms the other as parent - child), with kCutStopped that child
+// and the events that stopped at the parent (lists 2k and 2k + 1), with
+// kCutPlain every node of the layer.  Each feature group's `parts` workgroups (parts > lists) share
 // the entries of those lists: with E entries in all, list k of m_k entries
 // gets C_k = ceil(m_k / ceil(E / (parts - lists))) equal parts (none when
 // empty), numbered from base_k = C_0 + ... + C_(k-1); the C_k add up to at
@@ -2040,7 +2078,7 @@ __global__ __launch_bounds__(1024) void hist_list_kernel(
     const uint2 *__restrict__ list, const uint32_t *__restrict__ lstart,
     const uint32_t *__restrict__ lcap, const uint32_t *__restrict__ cursor,
     const uint32_t *__restrict__ lside, const uint8_t *__restrict__ xr, int dr, int d,
-    int nbins, bool miss, int G, int parts, int nlists, bool sib, int per_xcd, int scale,
+    int nbins, bool miss, int G, int parts, int nlists, int lmode, int per_xcd, int scale,
     int copies, int copy_stride, uint2 *__restrict__ lchunks, uint64_t *__restrict__ partial,
     int *__restrict__ err) {
     constexpr int NQ = FPG / 4;
@@ -2057,7 +2095,9 @@ __global__ __launch_bounds__(1024) void hist_list_kernel(
         if (lane < nlists) {
             m = min(cursor[lane], lcap[lane]);
             first = lstart[lane];
-            flag = sib ? lside[lane] : 0u;
+            flag = lmode == kCutSibling                         ? lside[lane]
+                   : lmode == kCutStopped && (lane & 1) == 0 ? lside[lane >> 1]
+                                                             : 0u;
         }
         uint64_t tot = m;
 #pragma unroll
@@ -2995,19 +3035,23 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
 
 hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
                            double *small_next, size_t small_next_count, int hnodes, int d,
-                           int n_bins, bool sibling, double *cand_gain, int *cand_cut,
+                           int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
                            const uint2 *lchunks) {
     const int S = cut_slices(n_bins);
-    const int blocks = hnodes * d * S;
-    if (sibling)
-        cut_scan_kernel<true><<<blocks, kCutWaves * kWave, 0, s>>>(
-            partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,
-            cand_gain, cand_cut, hparent, hout, lchunks);
-    else
-        cut_scan_kernel<false><<<blocks, kCutWaves * kWave, 0, s>>>(
-            partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,
-            cand_gain, cand_cut, nullptr, hout, lchunks);
+    // one workgroup per (histogrammed node, or parent, feature, slice)
+    const int groups = mode == kCutStopped ? hnodes / 2 : hnodes;
+    if ((mode == kCutStopped && hnodes % 2 != 0) || (mode != kCutPlain && !hparent))
+        return hipErrorInvalidValue;
+    const int blocks = groups * d * S;
+#define FBDT_CUT(M)                                                                                 cut_scan_kernel<M><<<blocks, kCutWaves * kWave, 0, s>>>(                                            partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,              cand_gain, cand_cut, M == kCutPlain ? nullptr : hparent, hout, lchunks)
+    switch (mode) {
+    case kCutPlain: FBDT_CUT(kCutPlain); break;
+    case kCutSibling: FBDT_CUT(kCutSibling); break;
+    case kCutStopped: FBDT_CUT(kCutStopped); break;
+    default: return hipErrorInvalidValue;
+    }
+#undef FBDT_CUT
     return hipGetLastError();
 }
 
@@ -3149,14 +3193,16 @@ ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, in
 hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, int n_bins,
                              const uint8_t *node_in, uint8_t *node_out, const float *w,
                              const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
-                             const uint64_t *hparent, int scale, const uint32_t *cap_prev,
+                             int lmode, const uint64_t *hparent, int scale, const uint32_t *cap_prev,
                              uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
                              uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
                              double *small, int *err, hipStream_t s) {
     if (layer < 1 || layer > 6 || n < 1 || n > kListMaxEvents) return hipErrorInvalidValue;
     if ((layer == 1) != (node_in == nullptr) || (layer == 1) != (cap_prev == nullptr))
         return hipErrorInvalidValue;
-    if ((1 << layer) > kListMaxSlots) return hipErrorInvalidValue;
+    if ((1 << layer) > kListMaxSlots || (lmode != kCutPlain && !hparent) || lmode < kCutPlain ||
+        lmode > kCutStopped)
+        return hipErrorInvalidValue;
     const uint32_t tau_bits = (uint32_t)(127 + 23 - scale) << 23;   // 2^(23 - scale)
     if (23 - scale < -126) return hipErrorInvalidValue;
     const int64_t R = xcd_range(n);
@@ -3164,20 +3210,20 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
     if (vsign)
         route_list_kernel<true><<<blocks, kRouteListThreads, 0, s>>>(
             xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut,
-            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, hparent != nullptr, hparent,
+            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent,
             tau_bits, cap_prev, cap_root, cnt_out, cursor, lstart, lcap, lside, list, small, err,
             R);
     else
         route_list_kernel<false><<<blocks, kRouteListThreads, 0, s>>>(
             xb, ldb, n, d, n_bins, node_in, node_out, w, nullptr, pc.cand_gain, pc.cand_cut,
-            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, hparent != nullptr, hparent,
+            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent,
             tau_bits, cap_prev, cap_root, cnt_out, cursor, lstart, lcap, lside, list, small, err,
             R);
     return hipGetLastError();
 }
 
 template <int FPG>
-void hist_list_go(const ListShape &ls, bool sib, bool signed_w, hipStream_t s, const uint2 *list,
+void hist_list_go(const ListShape &ls, int lmode, bool signed_w, hipStream_t s, const uint2 *list,
                   const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
                   const uint32_t *lside, const uint8_t *xr, int dr, int d, int nbins, int scale,
                   uint2 *lchunks, uint64_t *partial, int *err) {
@@ -3185,14 +3231,14 @@ void hist_list_go(const ListShape &ls, bool sib, bool signed_w, hipStream_t s, c
     if (signed_w)
         hist_list_kernel<FPG, true><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
             list, lstart, lcap, cursor, lside, xr, dr, d, nbins, miss, ls.groups, ls.parts,
-            ls.lists, sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+            ls.lists, lmode, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
     else
         hist_list_kernel<FPG, false><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
             list, lstart, lcap, cursor, lside, xr, dr, d, nbins, miss, ls.groups, ls.parts,
-            ls.lists, sib, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+            ls.lists, lmode, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
 }
 
-hipError_t launch_hist_list(const ListShape &ls, bool sib, const uint2 *list,
+hipError_t launch_hist_list(const ListShape &ls, int lmode, const uint2 *list,
                             const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
                             const uint32_t *lside, const uint8_t *xr, int d, int n_bins,
                             bool signed_w, int scale, uint2 *lchunks, uint64_t *partial, int *err,
@@ -3204,13 +3250,13 @@ hipError_t launch_hist_list(const ListShape &ls, bool sib, const uint2 *list,
         return hipErrorInvalidValue;
     const int dr = list_row_bytes(d);
     switch (ls.fpg) {
-    case 4: hist_list_go<4>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 8: hist_list_go<8>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 12: hist_list_go<12>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 20: hist_list_go<20>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 28: hist_list_go<28>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 36: hist_list_go<36>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 40: hist_list_go<40>(ls, sib, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 4: hist_list_go<4>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 8: hist_list_go<8>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 12: hist_list_go<12>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 20: hist_list_go<20>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 28: hist_list_go<28>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 36: hist_list_go<36>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 40: hist_list_go<40>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -81,7 +81,8 @@ CASES = {
                                       parts=37),
     "config2-30k-fpg4-parts1-copies4": dict(cfg=2, n_events=30_011, depth=4, n_trees=3, fpg=4,
                                             parts=1, copies=4),
-    # missing values: both children histogrammed, stopped events in no list
+    # missing values: one child and the events that stop at the parent are
+    # listed, the other child is parent - child - stopped
     "nan-config4-60k-depth6-B255": dict(cfg=4, n_events=60_013, n_bins=255, n_trees=3,
                                         missing=True),
     "nan-depth7-B64": dict(cfg=2, n_events=40_009, depth=7, n_bins=64, n_trees=2,
