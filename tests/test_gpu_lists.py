@@ -89,6 +89,13 @@ CASES = {
                            missing=True),
     "nan-negative-weights-depth4": dict(cfg=2, n_events=30_011, depth=4, n_trees=4, n_bins=64,
                                         weights="signed", missing=True),
+    # layer 6 of a depth-7 fit with missing values: 64 lists (the most), most
+    # of them short or empty
+    "nan-depth7-B200-weighted": dict(cfg=4, n_events=50_021, depth=7, n_bins=200, n_trees=2,
+                                     weights="signed", missing=True),
+    # 255 features: seven groups of 40, the last holding 15
+    "255-features-depth4": dict(cfg=3, n_events=5003, d=255, depth=4, n_trees=3),
+    "3-bins-depth5": dict(cfg=2, n_events=20_011, depth=5, n_bins=3, n_trees=4),
 }
 
 
@@ -105,6 +112,12 @@ def test_list_fit_matches_oracle_and_streaming_fit(case):
     c = CASES[case]
     spec = CONFIGS[c["cfg"]]
     ds = make_training_set(c["cfg"], n_events=c.get("n_events"))
+    if c.get("d"):   # more features: the workload's, repeated with seeded noise
+        reps = -(-c["d"] // ds["x"].shape[0])
+        rng = np.random.default_rng(11)
+        ds["x"] = np.concatenate(
+            [ds["x"] + rng.normal(0.0, 0.5 * r, ds["x"].shape).astype(np.float32)
+             for r in range(reps)])[:c["d"]]
     x = _with_missing(ds["x"], 7) if c.get("missing") else ds["x"]
     d, n = x.shape
     B = c.get("n_bins", spec.n_bins)
