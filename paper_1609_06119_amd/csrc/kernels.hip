@@ -1807,20 +1807,50 @@ __global__ __launch_bounds__(256) void route_layer_kernel(
 // event-major copy of the code matrix: every LDS add then has all its lanes
 // busy, and an event is read once per feature group.
 
-// xr[i * dr + j] = xb[j * ldb + i] for i < n and j < d, else 0, for the
-// 256 events of each workgroup (dr a multiple of 4, <= 256).
-__global__ __launch_bounds__(256) void transpose_codes_kernel(const uint8_t *__restrict__ xb,
-                                                              int64_t ldb, int64_t n, int d,
-                                                              uint8_t *__restrict__ xr, int dr) {
-    __shared__ uint32_t tile[256 * 64];   // [256 events][dr bytes]
-    uint8_t *tb = reinterpret_cast<uint8_t *>(tile);
-    const int64_t i0 = (int64_t)blockIdx.x * 256;
-    const int64_t i = i0 + threadIdx.x;
-    for (int j = 0; j < dr; ++j)
-        tb[threadIdx.x * dr + j] = (j < d && i < n) ? xb[(int64_t)j * ldb + i] : (uint8_t)0;
+// xr[i * dr + j] = xb[j * ldb + i] for i < n (j >= d: 0), E events per
+// workgroup (dr a multiple of 4, <= 256; E a multiple of 4).  A thread reads
+// the words of 4 consecutive events in 4 feature rows, transposes the 4 x 4
+// bytes in registers and stores one word per event into an LDS tile
+// [E][dr / 4 + 1] (the extra word spreads the stores over the banks); the
+// tile's rows of events < n are then written out as consecutive words.
+constexpr int kTransposeThreads = 256;
+__global__ __launch_bounds__(kTransposeThreads) void transpose_codes_kernel(
+    const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, uint8_t *__restrict__ xr,
+    int dr, int E) {
+    extern __shared__ uint32_t tile[];
+    const int W = dr / 4, WS = W + 1;
+    const int64_t i0 = (int64_t)blockIdx.x * E;
+    for (int t = threadIdx.x; t < E / 4; t += blockDim.x) {
+        const int64_t ie = i0 + 4 * t;
+        // bytes of events >= n within the last word read as 0 (rows are
+        // padded to ldb >= round_up(n, 16), so the word is in bounds)
+        const uint32_t keep = ie + 4 <= n ? 0xffffffffu
+                            : ie < n      ? (1u << (8 * (int)(n - ie))) - 1u
+                                          : 0u;
+        for (int q = 0; q < W; ++q) {
+            uint32_t r[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int j = 4 * q + k;
+                r[k] = (j < d && keep) ? *reinterpret_cast<const uint32_t *>(xb + (int64_t)j * ldb + ie) & keep
+                                       : 0u;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int sh = 8 * e;
+                tile[(4 * t + e) * WS + q] = ((r[0] >> sh) & 0xffu) | (((r[1] >> sh) & 0xffu) << 8) |
+                                             (((r[2] >> sh) & 0xffu) << 16) |
+                                             (((r[3] >> sh) & 0xffu) << 24);
+            }
+        }
+    }
     __syncthreads();
+    const int ev = (int)min((int64_t)E, n - i0);
     uint32_t *dst = reinterpret_cast<uint32_t *>(xr + (size_t)i0 * dr);
-    for (int t = threadIdx.x; t < 64 * dr; t += 256) dst[t] = tile[t];
+    for (int o = threadIdx.x; o < ev * W; o += blockDim.x) {   // ev * W <= 65536 / 4
+        const int e = o / W;
+        dst[o] = tile[e * WS + (o - e * W)];
+    }
 }
 
 // Routing of layer `layer` (>= 1) for the list-driven histogram pass.  The
@@ -3146,7 +3176,12 @@ hipError_t launch_transpose_codes(const uint8_t *xb, int64_t ldb, int64_t n, int
                                   hipStream_t s) {
     const int dr = list_row_bytes(d);
     if (d < 1 || dr > 256 || n < 1) return hipErrorInvalidValue;
-    transpose_codes_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(xb, ldb, n, d, xr, dr);
+    // events per workgroup: up to 1024, as many as a 64 KiB tile holds
+    const size_t row = (size_t)(dr / 4 + 1) * 4;
+    int E = (int)std::min<size_t>(1024, 65536 / row) & ~63;
+    if (E < 64) return hipErrorInvalidValue;
+    transpose_codes_kernel<<<(unsigned)((n + E - 1) / E), kTransposeThreads, (size_t)E * row, s>>>(
+        xb, ldb, n, d, xr, dr, E);
     return hipGetLastError();
 }
 
