@@ -341,7 +341,7 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
  * one with less weight in the parent's histograms) to per-parent lists,
  * with missing values (section 4.2) also the events that stop at the parent
  * to a list of their own, and histograms the lists, the codes read from an
- * event-major copy of the code matrix (n * round_up(d, 4) bytes of device
+ * event-major copy of the code matrix (n * round_up(d, 16) bytes of device
  * workspace, plus 8 bytes per event for the lists, 16 with missing values);
  * the other child is the parent minus the lists.  Fits need n < 2^31 for it.  Both give the same model bit
  * for bit, except for the rounding of sums of weights below the

@@ -773,7 +773,6 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                                          fb.w, fb.yts, nullptr, di.cu_count, st));
                 tm.done();
             }
-            if (lists) HIP_TRY(launch_fill_u32(lctr, 0u, lctr_count, st));
             uint8_t *cf = fb.cut_feature + (size_t)t * nin;
             uint8_t *cc = fb.cut_bin + (size_t)t * nin;
             double *cg = fb.gain + (size_t)t * nin;
@@ -858,12 +857,16 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                     const int cmode = sib ? kCutSibling : kCutPlain;
                     const size_t next_count =
                         (size_t)(l + 1 < D ? 1 << (l + 1) : 1) * d * n_bins * 2;
+                    // the root's scan also clears the counters of the tree's
+                    // list passes (layers 1 .. D-1 follow it)
+                    const bool clear = lists && l == 0;
                     HIP_TRY(launch_cut_scan(fb.partial, plans[l].chunks, scale, fb.small[gl & 1],
                                             fb.small[(gl + 1) & 1], next_count,
                                             sib ? 1 << (l - 1) : 1 << l, d, n_bins, cmode,
                                             fb.cand_gain, fb.cand_cut,
                                             cmode != kCutPlain ? fb.hfull[(l - 1) & 1] : nullptr,
-                                            l + 1 < D ? fb.hfull[l & 1] : nullptr, st));
+                                            l + 1 < D ? fb.hfull[l & 1] : nullptr, st, nullptr,
+                                            clear ? lctr : nullptr, clear ? (int)lctr_count : 0));
                     tm.done();
                 }
             }

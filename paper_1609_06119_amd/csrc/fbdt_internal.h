@@ -230,6 +230,7 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
 // lchunks (list passes): the partials of slot k are the rows [x_k, x_k +
 // (y_k & 0x7fffffff)) of [*][d][B][2], and bit 31 of y_k tells that a
 // child slot holds the right child (the left is then the one formed).
+// clear_words (optional): clear_count words zeroed on the way.
 enum CutMode : int {
     kCutPlain = 0,     // slot k holds node k
     kCutSibling = 1,   // slot k holds one child of parent k, the other is parent - child
@@ -240,7 +241,8 @@ hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const
                            double *small_next, size_t small_next_count, int hnodes, int d,
                            int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
-                           const uint2 *lchunks = nullptr);
+                           const uint2 *lchunks = nullptr, uint32_t *clear_words = nullptr,
+                           int clear_count = 0);
 
 // Best cut of each node over its candidates (d features x slices entries).
 hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,
@@ -304,8 +306,9 @@ constexpr int64_t kListMaxEvents = ((int64_t)1 << 31) - 1;
 // a workgroup reads an entry's codes as words)
 constexpr int kListFpgSizes[] = {4, 8, 12, 20, 28, 36, 40};
 bool list_fpg_supported(int f);
-// bytes per event of the event-major copy (d rounded up to 4), and the
-// copy's size (events rounded up to 256)
+// bytes per event of the event-major copy (d rounded up to 16, so that a
+// row is whole 16-byte words), and the copy's size (events rounded up to
+// 256)
 int list_row_bytes(int d);
 size_t list_codes_bytes(int64_t n, int d);
 hipError_t launch_transpose_codes(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *xr,

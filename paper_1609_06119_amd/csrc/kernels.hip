@@ -1224,7 +1224,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     double *__restrict__ small_next, size_t small_next_count, int hnodes, int d, int nbins, int S,
     double *__restrict__ cand_gain, int *__restrict__ cand_cut,
     const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout,
-    const uint2 *__restrict__ lchunks) {
+    const uint2 *__restrict__ lchunks, uint32_t *__restrict__ clear_words, int clear_count) {
 #pragma clang fp contract(off)
     constexpr bool PAIR = MODE != kCutPlain;   // both children of a parent per workgroup
     __shared__ uint64_t red[kCutWaves][kWave + 2];
@@ -1315,12 +1315,15 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         red_stop[wave][lane] = sv;
         if (lane < 2) red_stop[wave][kWave + lane] = st;
     }
-    // this workgroup's share of the next layer's side histogram
+    // this workgroup's share of the next layer's side histogram; workgroup
+    // 0 also clears clear_words (counters of the next passes)
     {
         const size_t per = (small_next_count + gridDim.x - 1) / gridDim.x;
         const size_t lo = per * blockIdx.x;
         const size_t hi = min(small_next_count, lo + per);
         for (size_t t = lo + threadIdx.x; t < hi; t += blockDim.x) small_next[t] = 0.0;
+        if (clear_words && blockIdx.x == 0)
+            for (int t = threadIdx.x; t < clear_count; t += blockDim.x) clear_words[t] = 0u;
     }
     lds_barrier();
     if (!cwave) return;
@@ -1808,7 +1811,7 @@ __global__ __launch_bounds__(256) void route_layer_kernel(
 // busy, and an event is read once per feature group.
 
 // xr[i * dr + j] = xb[j * ldb + i] for i < n (j >= d: 0), E events per
-// workgroup (dr a multiple of 4, <= 256; E a multiple of 4).  A thread reads
+// workgroup (dr a multiple of 16, <= 256; E a multiple of 4).  A thread reads
 // the words of 4 consecutive events in 4 feature rows, transposes the 4 x 4
 // bytes in registers and stores one word per event into an LDS tile
 // [E][dr / 4 + 1] (the extra word spreads the stores over the banks); the
@@ -2192,11 +2195,26 @@ __global__ __launch_bounds__(1024) void hist_list_kernel(
             }
         }
     };
+    // a group that starts the row and whose words fit it reads them as
+    // 16-byte words (rows are a multiple of 16 bytes long)
+    constexpr int NV = (NQ + 3) / 4;
+    const bool vec = j0 == 0 && NV * 16 <= dr;
     auto codes = [&](const uint2 en, uint32_t (&cw)[NQ]) {
-        const uint32_t *row =
-            reinterpret_cast<const uint32_t *>(xr + (size_t)(en.x & 0x7fffffffu) * dr);
+        const uint8_t *rb = xr + (size_t)(en.x & 0x7fffffffu) * dr;
+        if (vec) {
+            uint4 v[NV];
 #pragma unroll
-        for (int qq = 0; qq < NQ; ++qq) cw[qq] = row[min(qbase + qq, qmax)];
+            for (int i = 0; i < NV; ++i) v[i] = reinterpret_cast<const uint4 *>(rb)[i];
+#pragma unroll
+            for (int qq = 0; qq < NQ; ++qq) {
+                const uint4 &u = v[qq >> 2];
+                cw[qq] = (qq & 3) == 0 ? u.x : (qq & 3) == 1 ? u.y : (qq & 3) == 2 ? u.z : u.w;
+            }
+        } else {
+            const uint32_t *row = reinterpret_cast<const uint32_t *>(rb);
+#pragma unroll
+            for (int qq = 0; qq < NQ; ++qq) cw[qq] = row[min(qbase + qq, qmax)];
+        }
     };
     // two entries per thread and step; the next step's entries are loaded
     // while this step's codes arrive and are added
@@ -3067,14 +3085,18 @@ hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const
                            double *small_next, size_t small_next_count, int hnodes, int d,
                            int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
-                           const uint2 *lchunks) {
+                           const uint2 *lchunks, uint32_t *clear_words, int clear_count) {
     const int S = cut_slices(n_bins);
     // one workgroup per (histogrammed node, or parent, feature, slice)
     const int groups = mode == kCutStopped ? hnodes / 2 : hnodes;
     if ((mode == kCutStopped && hnodes % 2 != 0) || (mode != kCutPlain && !hparent))
         return hipErrorInvalidValue;
     const int blocks = groups * d * S;
-#define FBDT_CUT(M)                                                                                 cut_scan_kernel<M><<<blocks, kCutWaves * kWave, 0, s>>>(                                            partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,              cand_gain, cand_cut, M == kCutPlain ? nullptr : hparent, hout, lchunks)
+#define FBDT_CUT(M)                                                                             \
+    cut_scan_kernel<M><<<blocks, kCutWaves * kWave, 0, s>>>(                                    \
+        partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,      \
+        cand_gain, cand_cut, M == kCutPlain ? nullptr : hparent, hout, lchunks, clear_words,     \
+        clear_count)
     switch (mode) {
     case kCutPlain: FBDT_CUT(kCutPlain); break;
     case kCutSibling: FBDT_CUT(kCutSibling); break;
@@ -3166,7 +3188,7 @@ bool list_fpg_supported(int f) {
     return false;
 }
 
-int list_row_bytes(int d) { return (d + 3) & ~3; }
+int list_row_bytes(int d) { return (d + 15) & ~15; }
 
 size_t list_codes_bytes(int64_t n, int d) {
     return (size_t)((n + 255) / 256) * 256 * (size_t)list_row_bytes(d);
