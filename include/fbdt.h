@@ -334,7 +334,7 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
  * "hist_timeline" (default 0): 1 makes fbdt_fit record the phase timeline
  * of every histogram launch (see fbdt_hist_timeline); fits then launch
  * kernel by kernel.
- * "hist_lists" (default 0: fits of at least 4,000,000 events): how fbdt_fit
+ * "hist_lists" (default 0: fits with n * (depth - 2) >= 10,000,000): how fbdt_fit
  * builds the histograms of the layers below the root (sections 1.1, 2.1).
  * 1 streams every event through every layer's pass; 2 has each layer's
  * routing pass append the sampled events of one child of every parent (the

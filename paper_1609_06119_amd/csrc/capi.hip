@@ -132,12 +132,17 @@ hipError_t device_alloc(void **p, size_t bytes) {
 
 std::atomic<int64_t> opt_hist_fpg{0}, opt_hist_chunks{0}, opt_hist_threads{0}, opt_hist_copies{0},
     opt_apply_threads{0}, opt_fit_graphs{1}, opt_hist_timeline{0};
-// event lists below the root: 0 = the fit decides (kListAutoEvents), 1 =
+// event lists below the root: 0 = the fit decides (kListAutoWork), 1 =
 // never, 2 = always; and the list pass's launch-shape overrides
 std::atomic<int64_t> opt_hist_lists{0}, opt_list_fpg{0}, opt_list_parts{0}, opt_list_copies{0};
-// fits of at least this many events histogram the layers below the root
-// from event lists
-constexpr int64_t kListAutoEvents = 4000000;
+// fits with events x (depth - 2) of at least this histogram the layers below
+// the root from event lists.  Measured on 10M x 40 events (fits of 20 trees,
+// streaming / lists): depth 3 breaks even near 10M events (1.18 at 2M, 0.98
+// at 10M), depth 4 near 4-5M (0.99 at 4M), depth 6 near 2.5M (1.04 at 2M,
+// 0.93 at 3M, 0.77 at 10M): the deeper layers that lists speed up most
+// grow with the depth, while the extra route pass per layer costs about
+// the same at every layer.
+constexpr int64_t kListAutoWork = 10000000;
 
 // Phase timeline of the histogram launches of the last fit made with option
 // hist_timeline (host copy): [launches][max_blocks][kTimelineStamps].
@@ -629,7 +634,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     // of every parent, or with missing values every node of the layer)
     const int64_t lists_opt = opt_hist_lists.load();
     const bool lists = D >= 2 && npad <= kListMaxEvents &&
-                       (lists_opt == 2 || (lists_opt == 0 && n >= kListAutoEvents));
+                       (lists_opt == 2 || (lists_opt == 0 && n * (D - 2) >= kListAutoWork));
     std::vector<ListShape> lplans_sib(lists ? D : 0), lplans_both(lists && may_miss ? D : 0);
     for (int l = 1; lists && l < D; ++l) {
         for (int mode = 0; mode < (may_miss ? 2 : 1); ++mode) {
