@@ -333,7 +333,7 @@ int fbdt_timing_read(int32_t kind, int64_t *launches, double *total_ms, double *
  * allocates.
  * "hist_timeline" (default 0): 1 makes fbdt_fit record the phase timeline
  * of every histogram launch (see fbdt_hist_timeline); fits then launch
- * kernel by kernel.
+ * kernel by kernel and stream every layer (no event lists).
  * "hist_lists" (default 0: fits with n * (depth - 2) >= 10,000,000): how fbdt_fit
  * builds the histograms of the layers below the root (sections 1.1, 2.1).
  * 1 streams every event through every layer's pass; 2 has each layer's

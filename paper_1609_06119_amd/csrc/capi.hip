@@ -632,8 +632,10 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     }
     // layers 1 .. D-1 of large fits histogram event lists (the lighter child
     // of every parent, or with missing values every node of the layer)
+    // (the phase timeline measures the streaming pass: a fit that records
+    // it streams every layer)
     const int64_t lists_opt = opt_hist_lists.load();
-    const bool lists = D >= 2 && npad <= kListMaxEvents &&
+    const bool lists = D >= 2 && npad <= kListMaxEvents && opt_hist_timeline.load() == 0 &&
                        (lists_opt == 2 || (lists_opt == 0 && n * (D - 2) >= kListAutoWork));
     std::vector<ListShape> lplans_sib(lists ? D : 0), lplans_both(lists && may_miss ? D : 0);
     for (int l = 1; lists && l < D; ++l) {
