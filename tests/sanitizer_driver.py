@@ -92,8 +92,13 @@ expect(L.fbdt_set_option(b"hist_features_per_group", 3), INVAL)
 expect(L.fbdt_set_option(b"hist_copies", 3), INVAL)
 expect(L.fbdt_set_option(b"apply_threads", 2048), INVAL)
 expect(L.fbdt_set_option(b"fit_graphs", -1), INVAL)
+expect(L.fbdt_set_option(b"hist_lists", 3), INVAL)
+expect(L.fbdt_set_option(b"list_features_per_group", 16), INVAL)
+expect(L.fbdt_set_option(b"list_parts", 5000), INVAL)
+expect(L.fbdt_set_option(b"list_copies", 8), INVAL)
 for name in (b"hist_features_per_group", b"hist_event_chunks", b"hist_threads", b"hist_copies",
-             b"apply_threads", b"hist_timeline", b"fail_alloc"):
+             b"apply_threads", b"hist_timeline", b"fail_alloc", b"hist_lists",
+             b"list_features_per_group", b"list_parts", b"list_copies"):
     expect(L.fbdt_set_option(name, 0), 0)
 expect(L.fbdt_set_option(b"fit_graphs", 1), 0)
 expect(L.fbdt_timing_enable(0), 0)
