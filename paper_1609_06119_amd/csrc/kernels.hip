@@ -1730,7 +1730,8 @@ __global__ __launch_bounds__(kLeafReduceThreads) void leaf_finalize_kernel(
 // With miss, an event whose code of the cut feature is the missing code, or
 // which stopped at an earlier layer, keeps its node (section 4.2).  Whole
 // steps of kHistE events: padded events get ids too.
-__global__ __launch_bounds__(256) void route_layer_kernel(
+constexpr int kRouteLayerThreads = 1024;
+__global__ __launch_bounds__(kRouteLayerThreads) void route_layer_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
@@ -1883,8 +1884,14 @@ __global__ __launch_bounds__(kTransposeThreads) void transpose_codes_kernel(
 // to the float64 side histogram `small` [2^layer][d][B][2] here, for either
 // child and every feature, as the streaming pass adds them.
 constexpr int kRouteListThreads = 1024;
-constexpr int kRouteListSteps = 2;
-constexpr int kRouteListEvents = kRouteListThreads * kRouteListSteps * kHistE;
+// steps of kHistE events per thread: three (24,576 events per workgroup, so
+// that a 10M-event layer needs one round of two workgroups per CU: 41-46 ->
+// 37-42 us per layer on workload 4) where the ranks fit the 64 VGPRs that
+// occupancy allows, two with signed weights (their sign bits spill at three)
+template <bool SIGNED>
+constexpr int route_list_steps() { return SIGNED ? 2 : 3; }
+template <bool SIGNED>
+constexpr int route_list_events() { return kRouteListThreads * route_list_steps<SIGNED>() * kHistE; }
 template <bool SIGNED>
 __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 4) void route_list_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
@@ -1960,15 +1967,17 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
 
     // per event of the thread's steps: node << 16 | rank within the
     // workgroup's entries of that node, or ~0 (no entry)
-    uint32_t rec[kRouteListSteps][kHistE];
-    uint32_t negs[kRouteListSteps];
+    constexpr int STEPS = route_list_steps<SIGNED>();
+    constexpr int64_t EVENTS = route_list_events<SIGNED>();
+    uint32_t rec[STEPS][kHistE];
+    uint32_t negs[STEPS];
     // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
     // (the range every per-event pass of the fit gives that XCD), in turn
     const int64_t xlo = (int64_t)(blockIdx.x % kXcds) * xcd_events;
-    const int64_t base_i = xlo + (int64_t)(blockIdx.x / kXcds) * kRouteListEvents;
-    const int64_t end_i = min(min(n, xlo + xcd_events), base_i + kRouteListEvents);
+    const int64_t base_i = xlo + (int64_t)(blockIdx.x / kXcds) * EVENTS;
+    const int64_t end_i = min(min(n, xlo + xcd_events), base_i + EVENTS);
 #pragma unroll
-    for (int st = 0; st < kRouteListSteps; ++st) {
+    for (int st = 0; st < STEPS; ++st) {
         const int64_t i0 = base_i + ((int64_t)st * kRouteListThreads + threadIdx.x) * kHistE;
         negs[st] = 0u;
 #pragma unroll
@@ -1976,12 +1985,12 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
         if (i0 < end_i) {
             const uint2 pin = node_in ? *reinterpret_cast<const uint2 *>(node_in + i0)
                                       : make_uint2(0x01010101u, 0x01010101u);
-            uint32_t par[kHistE], k[kHistE], code[kHistE];
+            // the parents are taken from pin again below rather than held
+            uint32_t code[kHistE];
 #pragma unroll
             for (int e = 0; e < kHistE; ++e) {
-                par[e] = byte8(pin, e);
-                k[e] = par[e] - half;
-                const uint32_t kk = k[e] < half ? k[e] : 0u;
+                const uint32_t k = byte8(pin, e) - half;
+                const uint32_t kk = k < half ? k : 0u;
                 code[e] = xb[(int64_t)min((int)s_cf[kk], d - 1) * ldb + i0 + e];
             }
             const uint4 wx = reinterpret_cast<const uint4 *>(w + i0)[0];
@@ -1993,7 +2002,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
             uint32_t below = 0u;
 #pragma unroll
             for (int e = 0; e < kHistE; ++e) {
-                uint32_t p = par[e], kk = k[e];
+                uint32_t p = byte8(pin, e), kk = p - half;
                 bool stop = false, earlier = false;
                 if (kk >= half) {
                     earlier = miss & (p < half);
@@ -2061,7 +2070,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     }
     __syncthreads();
 #pragma unroll
-    for (int st = 0; st < kRouteListSteps; ++st) {
+    for (int st = 0; st < STEPS; ++st) {
         const int64_t i0 = base_i + ((int64_t)st * kRouteListThreads + threadIdx.x) * kHistE;
         if (i0 < end_i) {
             // the weights again (in L2), rather than held in registers across
@@ -3169,14 +3178,18 @@ hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
                               const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc,
                               int layer, bool miss, int *err, int cu_count, hipStream_t s) {
     if (layer < 1 || (1 << (layer - 1)) > 64) return hipErrorInvalidValue;
-    // up to 4 workgroups of 256 threads per CU: the gathers are
-    // latency-bound, so many wavefronts keep loads in flight
+    // one workgroup of 1024 threads per CU: every workgroup forms the
+    // parents' cuts from their candidates (up to 64 wavefront reductions
+    // over d x slices entries), so few, wide workgroups spread that over
+    // 16 wavefronts and read the candidates a quarter as often as four
+    // workgroups of 256 (workload 4's leaf routing: 41 -> 34 us)
     const int64_t R = xcd_range(n);
-    int64_t per = (R + (int64_t)kHistE * 256 - 1) / ((int64_t)kHistE * 256);
-    const int64_t cap = 4 * (cu_count / kXcds > 0 ? cu_count / kXcds : 1);
+    int64_t per = (R + (int64_t)kHistE * kRouteLayerThreads - 1) /
+                  ((int64_t)kHistE * kRouteLayerThreads);
+    const int64_t cap = cu_count / kXcds > 0 ? cu_count / kXcds : 1;
     if (per > cap) per = cap;
     if (per < 1) per = 1;
-    route_layer_kernel<<<(unsigned)(kXcds * per), 256, 0, s>>>(
+    route_layer_kernel<<<(unsigned)(kXcds * per), kRouteLayerThreads, 0, s>>>(
         xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut, pc.slices, pc.rec_f,
         pc.rec_c, pc.rec_g, layer, miss, err, R);
     return hipGetLastError();
@@ -3263,7 +3276,8 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
     const uint32_t tau_bits = (uint32_t)(127 + 23 - scale) << 23;   // 2^(23 - scale)
     if (23 - scale < -126) return hipErrorInvalidValue;
     const int64_t R = xcd_range(n);
-    const unsigned blocks = (unsigned)(kXcds * ((R + kRouteListEvents - 1) / kRouteListEvents));
+    const int64_t E = vsign ? route_list_events<true>() : route_list_events<false>();
+    const unsigned blocks = (unsigned)(kXcds * ((R + E - 1) / E));
     if (vsign)
         route_list_kernel<true><<<blocks, kRouteListThreads, 0, s>>>(
             xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut,
