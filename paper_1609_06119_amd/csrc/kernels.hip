@@ -1884,15 +1884,20 @@ __global__ __launch_bounds__(kTransposeThreads) void transpose_codes_kernel(
 // to the float64 side histogram `small` [2^layer][d][B][2] here, for either
 // child and every feature, as the streaming pass adds them.
 constexpr int kRouteListThreads = 1024;
-// steps of kHistE events per thread: three (24,576 events per workgroup, so
+// Steps of kHistE events per thread: three (24,576 events per workgroup, so
 // that a 10M-event layer needs one round of two workgroups per CU: 41-46 ->
 // 37-42 us per layer on workload 4) where the ranks fit the 64 VGPRs that
-// occupancy allows, two with signed weights (their sign bits spill at three)
-template <bool SIGNED>
-constexpr int route_list_steps() { return SIGNED ? 2 : 3; }
-template <bool SIGNED>
-constexpr int route_list_events() { return kRouteListThreads * route_list_steps<SIGNED>() * kHistE; }
-template <bool SIGNED>
+// this occupancy allows, two otherwise (more live registers: the sign bits
+// of signed weights, or 64-bit gather addresses).  OFF32: the code matrix
+// spans less than 4 GiB (d * ldb < 2^32), so the gathers take 32-bit
+// offsets from its base.
+template <bool SIGNED, bool OFF32>
+constexpr int route_list_steps() { return OFF32 && !SIGNED ? 3 : 2; }
+template <bool SIGNED, bool OFF32>
+constexpr int route_list_events() {
+    return kRouteListThreads * route_list_steps<SIGNED, OFF32>() * kHistE;
+}
+template <bool SIGNED, bool OFF32>
 __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 4) void route_list_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
@@ -1967,8 +1972,8 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
 
     // per event of the thread's steps: node << 16 | rank within the
     // workgroup's entries of that node, or ~0 (no entry)
-    constexpr int STEPS = route_list_steps<SIGNED>();
-    constexpr int64_t EVENTS = route_list_events<SIGNED>();
+    constexpr int STEPS = route_list_steps<SIGNED, OFF32>();
+    constexpr int64_t EVENTS = route_list_events<SIGNED, OFF32>();
     uint32_t rec[STEPS][kHistE];
     uint32_t negs[STEPS];
     // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
@@ -1991,7 +1996,9 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
             for (int e = 0; e < kHistE; ++e) {
                 const uint32_t k = byte8(pin, e) - half;
                 const uint32_t kk = k < half ? k : 0u;
-                code[e] = xb[(int64_t)min((int)s_cf[kk], d - 1) * ldb + i0 + e];
+                code[e] = OFF32 ? xb[(uint32_t)min((int)s_cf[kk], d - 1) * (uint32_t)ldb +
+                                     (uint32_t)(i0 + e)]
+                                : xb[(int64_t)min((int)s_cf[kk], d - 1) * ldb + i0 + e];
             }
             const uint4 wx = reinterpret_cast<const uint4 *>(w + i0)[0];
             const uint4 wy = reinterpret_cast<const uint4 *>(w + i0)[1];
@@ -3276,20 +3283,24 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
     const uint32_t tau_bits = (uint32_t)(127 + 23 - scale) << 23;   // 2^(23 - scale)
     if (23 - scale < -126) return hipErrorInvalidValue;
     const int64_t R = xcd_range(n);
-    const int64_t E = vsign ? route_list_events<true>() : route_list_events<false>();
+    const bool off32 = (uint64_t)d * (uint64_t)ldb <= 0xffffffffull;
+    const int64_t E = vsign ? (off32 ? route_list_events<true, true>() : route_list_events<true, false>())
+                            : (off32 ? route_list_events<false, true>() : route_list_events<false, false>());
     const unsigned blocks = (unsigned)(kXcds * ((R + E - 1) / E));
-    if (vsign)
-        route_list_kernel<true><<<blocks, kRouteListThreads, 0, s>>>(
-            xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut,
-            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent,
-            tau_bits, cap_prev, cap_root, cnt_out, cursor, lstart, lcap, lside, list, small, err,
-            R);
+#define FBDT_ROUTE_LIST(SG, O32)                                                                \
+    route_list_kernel<SG, O32><<<blocks, kRouteListThreads, 0, s>>>(                            \
+        xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices, \
+        pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent, tau_bits, cap_prev, cap_root,  \
+        cnt_out, cursor, lstart, lcap, lside, list, small, err, R)
+    if (vsign && off32)
+        FBDT_ROUTE_LIST(true, true);
+    else if (vsign)
+        FBDT_ROUTE_LIST(true, false);
+    else if (off32)
+        FBDT_ROUTE_LIST(false, true);
     else
-        route_list_kernel<false><<<blocks, kRouteListThreads, 0, s>>>(
-            xb, ldb, n, d, n_bins, node_in, node_out, w, nullptr, pc.cand_gain, pc.cand_cut,
-            pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent,
-            tau_bits, cap_prev, cap_root, cnt_out, cursor, lstart, lcap, lside, list, small, err,
-            R);
+        FBDT_ROUTE_LIST(false, false);
+#undef FBDT_ROUTE_LIST
     return hipGetLastError();
 }
 

@@ -186,3 +186,29 @@ def test_list_fit_graph_replays_match_eager_fit():
         for key in ("cut_feature", "cut_bin", "gain", "leaf"):
             assert np.array_equal(got[key], ref[key]), (rep, key)
 
+
+
+def test_list_fit_on_codes_beyond_4_gib():
+    """A code matrix of more than 2^32 bytes (128 features x 34M events): the
+    route pass then addresses its gathers with 64-bit offsets.  The list fit
+    must give the streaming fit's model bit for bit."""
+    d, n = 128, 34_000_000
+    assert d * n > 2 ** 32
+    g = torch.Generator(device="cuda").manual_seed(17)
+    codes = fb.Codes.empty(d, n)
+    codes.data[:, :n] = torch.randint(0, 256, (d, n), dtype=torch.uint8, device="cuda",
+                                      generator=g)
+    noise = torch.randint(0, 64, (n,), dtype=torch.int32, device="cuda", generator=g)
+    s = codes.data[0, :n].to(torch.int32) + codes.data[d - 1, :n].to(torch.int32) + noise
+    y = torch.where(s >= 286, 1, -1).to(torch.int8)
+    del s, noise
+    say(f"list fit beyond 4 GiB: n={n} d={d}")
+    runs = {}
+    for mode in (2, 1):
+        fb.set_option("hist_lists", mode)
+        runs[mode] = fb.fit(codes, y, 256, 4, 2, 0.1, 0.5, 3).export()
+        torch.cuda.synchronize()
+    for key in ("cut_feature", "cut_bin", "gain", "leaf"):
+        assert np.array_equal(runs[2][key], runs[1][key]), key
+    # the cuts use the informative features
+    assert set(runs[2]["cut_feature"][:, 0].tolist()) <= {0, d - 1}
