@@ -718,6 +718,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     const size_t tl_count = timeline ? (size_t)T * D * tl_blocks * kTimelineStamps : 0;
     unsigned long long *tl = nullptr;
     if (timeline) cv.add(&tl, tl_count);
+    cv.add(&fb.sany, 2);   // last: the other buffers keep their offsets
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     if (timeline) HIP_TRY(launch_fill_u32(tl, 0u, 2 * tl_count, s));
@@ -725,6 +726,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     HIP_TRY(launch_fill_u32(fb.err, 0u, 1, s));
     HIP_TRY(launch_fill_u32(fb.small[0], 0u, 2 * small_elems, s));
     HIP_TRY(launch_fill_u32(fb.small[1], 0u, 2 * small_elems, s));
+    HIP_TRY(launch_fill_u32(fb.sany, 0u, 2, s));
     // the histogram and leaf passes read whole steps of events: padded events
     // weigh 0 and have no pseudo-response
     HIP_TRY(launch_fill_u32(fb.w, 0u, (size_t)npad, s));
@@ -805,7 +807,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                             fb.node[l & 1], fb.w, vsign, pc, l, n_bins <= kMissingCode, lmode,
                             fb.hfull[(l - 1) & 1], scale, cap_prev, (uint32_t)npad,
                             l + 1 < D ? ctr + kListMaxSlots : nullptr, ctr, lstart, lcap, lside,
-                            list, fb.small[gl & 1], fb.err, st));
+                            list, fb.small[gl & 1], fb.sany + (gl & 1), fb.err, st));
                         tm.done();
                     }
                     {
@@ -821,7 +823,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                         const size_t next_count =
                             (size_t)(l + 1 < D ? 1 << (l + 1) : 1) * d * n_bins * 2;
                         HIP_TRY(launch_cut_scan(fb.partial, 0, scale, fb.small[gl & 1],
-                                                fb.small[(gl + 1) & 1], next_count, ls.lists, d,
+                                                fb.sany + (gl & 1), fb.small[(gl + 1) & 1],
+                                                fb.sany + ((gl + 1) & 1), next_count, ls.lists, d,
                                                 n_bins, lmode, fb.cand_gain, fb.cand_cut,
                                                 fb.hfull[(l - 1) & 1],
                                                 l + 1 < D ? fb.hfull[l & 1] : nullptr, st,
@@ -868,7 +871,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                     // list passes (layers 1 .. D-1 follow it)
                     const bool clear = lists && l == 0;
                     HIP_TRY(launch_cut_scan(fb.partial, plans[l].chunks, scale, fb.small[gl & 1],
-                                            fb.small[(gl + 1) & 1], next_count,
+                                            nullptr, fb.small[(gl + 1) & 1],
+                                            fb.sany + ((gl + 1) & 1), next_count,
                                             sib ? 1 << (l - 1) : 1 << l, d, n_bins, cmode,
                                             fb.cand_gain, fb.cand_cut,
                                             cmode != kCutPlain ? fb.hfull[(l - 1) & 1] : nullptr,

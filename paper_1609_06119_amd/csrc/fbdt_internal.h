@@ -67,6 +67,8 @@ struct FitBuffers {
                           // [nodes][d][B][2], by layer parity (the next layer's parents)
     double *small[2];     // float64 histograms of the weights below the fixed-point grid,
                           // [nodes][d][B][2], by the parity of tree * D + layer
+    uint32_t *sany;       // [2] non-zero once a list route pass added to small[p] (cleared
+                          // with it)
     double *cand_gain;    // [max nodes][d * slices] best gain of every (node, feature, slice)
     int *cand_cut;        // [max nodes][d * slices] and its bin
     double *leaf_partial;   // [leaf blocks][2^D][2]
@@ -226,7 +228,9 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
 // kCutStopped: slot 2k the left child, slot 2k + 1 the events that stopped
 // at parent k; the right child is parent - left - stopped.  hout (optional)
 // receives the summed prefix rows of every node of the layer.  Clears
-// small_next[0, small_next_count) (the next layer's side histogram).
+// small_next[0, small_next_count) (the next layer's side histogram) and
+// *sany_next (if given).  sany (list layers, or null): the side histogram
+// is read only if *sany is non-zero (the route pass added to it).
 // lchunks (list passes): the partials of slot k are the rows [x_k, x_k +
 // (y_k & 0x7fffffff)) of [*][d][B][2], and bit 31 of y_k tells that a
 // child slot holds the right child (the left is then the one formed).
@@ -238,7 +242,8 @@ enum CutMode : int {
                        // stopped at k; the other child is parent - child - stopped
 };
 hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
-                           double *small_next, size_t small_next_count, int hnodes, int d,
+                           const uint32_t *sany, double *small_next, uint32_t *sany_next,
+                           size_t small_next_count, int hnodes, int d,
                            int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
                            const uint2 *lchunks = nullptr, uint32_t *clear_words = nullptr,
@@ -350,7 +355,8 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
                              const uint32_t *cap_prev,
                              uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
                              uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
-                             double *small, int *err, hipStream_t s);
+                             double *small, uint32_t *sany, int *err, hipStream_t s);
+// (sany: set non-zero when a weight goes to small)
 // Histograms of the ls.lists lists of launch_route_list (lmode as there,
 // lside from the route pass) into prefix-summed partials [ls.parts][d][B]
 // [2], with lchunks [ls.lists] = {first part, parts | right child

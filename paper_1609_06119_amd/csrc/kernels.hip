@@ -1224,7 +1224,8 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     double *__restrict__ small_next, size_t small_next_count, int hnodes, int d, int nbins, int S,
     double *__restrict__ cand_gain, int *__restrict__ cand_cut,
     const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout,
-    const uint2 *__restrict__ lchunks, uint32_t *__restrict__ clear_words, int clear_count) {
+    const uint2 *__restrict__ lchunks, uint32_t *__restrict__ clear_words, int clear_count,
+    const uint32_t *__restrict__ sany, uint32_t *__restrict__ sany_next) {
 #pragma clang fp contract(off)
     constexpr bool PAIR = MODE != kCutPlain;   // both children of a parent per workgroup
     __shared__ uint64_t red[kCutWaves][kWave + 2];
@@ -1271,16 +1272,23 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     const size_t noff = ((size_t)node * d + j) * row;
 
     // side histogram row of the candidate wavefronts' node: lane l holds bins
-    // 4l..4l+3, both classes (loaded first, in flight with the chunk sums)
+    // 4l..4l+3, both classes.  Without sany it is loaded first, in flight
+    // with the chunk sums; with sany (list layers, where the nine slices of
+    // a row would each read all of it and the row is nearly always empty)
+    // only after them, and only if *sany says a weight went to the layer's
+    // side histogram
     double sd[8];
     const bool cwave = wave < (PAIR ? 2 : 1);
-    if (cwave) {
+    auto side_load = [&]() {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int bb = 4 * lane + (e >> 1);
             sd[e] = bb < nbins ? small[noff + 2 * bb + (e & 1)] : 0.0;
         }
-    }
+    };
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sd[e] = 0.0;
+    if (cwave && !sany) side_load();
     uint64_t pv = 0, pt = 0;   // parent row (other child = parent - histogrammed child)
     if (PAIR && wave == sub) {
         pv = hparent[off + wv];
@@ -1309,6 +1317,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     chunk_sums(coff, cchunks, v, vt);
     red[wave][lane] = v;
     if (lane < 2) red[wave][kWave + lane] = vt;
+    if (cwave && sany && *sany != 0u) side_load();
     if (MODE == kCutStopped) {
         uint64_t sv = 0, st = 0;
         chunk_sums(soff, schunks, sv, st);
@@ -1322,6 +1331,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         const size_t lo = per * blockIdx.x;
         const size_t hi = min(small_next_count, lo + per);
         for (size_t t = lo + threadIdx.x; t < hi; t += blockDim.x) small_next[t] = 0.0;
+        if (sany_next && blockIdx.x == 0 && threadIdx.x == 0) *sany_next = 0u;
         if (clear_words && blockIdx.x == 0)
             for (int t = threadIdx.x; t < clear_count; t += blockDim.x) clear_words[t] = 0u;
     }
@@ -1908,7 +1918,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     const uint32_t *__restrict__ cap_prev, uint32_t cap_root, uint32_t *__restrict__ cnt_out,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ lstart, uint32_t *__restrict__ lcap,
     uint32_t *__restrict__ lside, uint2 *__restrict__ list, double *__restrict__ small,
-    int *__restrict__ err, int64_t xcd_events) {
+    int *__restrict__ err, int64_t xcd_events, uint32_t *__restrict__ sany) {
     __shared__ uint8_t s_cf[64], s_cc[64], s_side[64];
     __shared__ uint32_t s_cnt[kListMaxSlots], s_ncnt[kListMaxSlots];
     __shared__ uint32_t s_start[kListMaxSlots], s_cap[kListMaxSlots], s_base[kListMaxSlots];
@@ -2059,6 +2069,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
                         }
                     }
                 }
+                atomicOr(sany, 1u);
             }
         }
     }
@@ -3098,7 +3109,8 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
 }
 
 hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const double *small,
-                           double *small_next, size_t small_next_count, int hnodes, int d,
+                           const uint32_t *sany, double *small_next, uint32_t *sany_next,
+                           size_t small_next_count, int hnodes, int d,
                            int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
                            const uint2 *lchunks, uint32_t *clear_words, int clear_count) {
@@ -3112,7 +3124,7 @@ hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const
     cut_scan_kernel<M><<<blocks, kCutWaves * kWave, 0, s>>>(                                    \
         partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,      \
         cand_gain, cand_cut, M == kCutPlain ? nullptr : hparent, hout, lchunks, clear_words,     \
-        clear_count)
+        clear_count, sany, sany_next)
     switch (mode) {
     case kCutPlain: FBDT_CUT(kCutPlain); break;
     case kCutSibling: FBDT_CUT(kCutSibling); break;
@@ -3273,7 +3285,7 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
                              int lmode, const uint64_t *hparent, int scale, const uint32_t *cap_prev,
                              uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
                              uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
-                             double *small, int *err, hipStream_t s) {
+                             double *small, uint32_t *sany, int *err, hipStream_t s) {
     if (layer < 1 || layer > 6 || n < 1 || n > kListMaxEvents) return hipErrorInvalidValue;
     if ((layer == 1) != (node_in == nullptr) || (layer == 1) != (cap_prev == nullptr))
         return hipErrorInvalidValue;
@@ -3291,7 +3303,7 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
     route_list_kernel<SG, O32><<<blocks, kRouteListThreads, 0, s>>>(                            \
         xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices, \
         pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent, tau_bits, cap_prev, cap_root,  \
-        cnt_out, cursor, lstart, lcap, lside, list, small, err, R)
+        cnt_out, cursor, lstart, lcap, lside, list, small, err, R, sany)
     if (vsign && off32)
         FBDT_ROUTE_LIST(true, true);
     else if (vsign)
