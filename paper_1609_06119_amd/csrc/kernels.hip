@@ -1231,8 +1231,17 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     __shared__ uint64_t red[kCutWaves][kWave + 2];
     __shared__ uint64_t red_stop[MODE == kCutStopped ? kCutWaves : 1][kWave + 2];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int q = blockIdx.x % S;
-    const int kj = blockIdx.x / S;
+    // row kj = (node or parent, feature) and slice q.  The S slices of a row
+    // run on one XCD (workgroup b runs on XCD b % 8), so that the cache
+    // lines that adjacent slices' windows share, and the row totals that
+    // every slice reads, come from that XCD's L2; the grid is padded to
+    // whole rounds of 8 rows
+    const int rows = (MODE == kCutStopped ? hnodes / 2 : hnodes) * d;
+    const int xq = blockIdx.x % kXcds, pq = blockIdx.x / kXcds;
+    const int q = pq % S;
+    const int kj0 = (pq / S) * kXcds + xq;
+    const bool valid = kj0 < rows;
+    const int kj = valid ? kj0 : 0;
     const int j = kj % d;
     const int k = kj / d;   // histogrammed node, or with PAIR the parent
     const size_t row = (size_t)nbins * 2;
@@ -1246,8 +1255,8 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     // holds the right child
     const int cslot = MODE == kCutStopped ? 2 * k : k;
     uint32_t cbase = (uint32_t)cslot, sbase = (uint32_t)cslot + 1u, flag = 0u;
-    int cchunks = chunks, schunks = MODE == kCutStopped ? chunks : 0;
-    if (lchunks) {
+    int cchunks = valid ? chunks : 0, schunks = valid && MODE == kCutStopped ? chunks : 0;
+    if (lchunks && valid) {
         const uint2 lc = lchunks[cslot];
         cbase = lc.x;
         cchunks = (int)(lc.y & 0x7fffffffu);
@@ -1288,7 +1297,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     };
 #pragma unroll
     for (int e = 0; e < 8; ++e) sd[e] = 0.0;
-    if (cwave && !sany) side_load();
+    if (cwave && valid && !sany) side_load();
     uint64_t pv = 0, pt = 0;   // parent row (other child = parent - histogrammed child)
     if (PAIR && wave == sub) {
         pv = hparent[off + wv];
@@ -1317,7 +1326,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     chunk_sums(coff, cchunks, v, vt);
     red[wave][lane] = v;
     if (lane < 2) red[wave][kWave + lane] = vt;
-    if (cwave && sany && *sany != 0u) side_load();
+    if (cwave && valid && sany && *sany != 0u) side_load();
     if (MODE == kCutStopped) {
         uint64_t sv = 0, st = 0;
         chunk_sums(soff, schunks, sv, st);
@@ -1336,7 +1345,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
             for (int t = threadIdx.x; t < clear_count; t += blockDim.x) clear_words[t] = 0u;
     }
     lds_barrier();
-    if (!cwave) return;
+    if (!cwave || !valid) return;
     uint64_t P = 0, T = 0;
 #pragma unroll
     for (int w = 0; w < kCutWaves; ++w) {
@@ -3119,7 +3128,8 @@ hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const
     const int groups = mode == kCutStopped ? hnodes / 2 : hnodes;
     if ((mode == kCutStopped && hnodes % 2 != 0) || (mode != kCutPlain && !hparent))
         return hipErrorInvalidValue;
-    const int blocks = groups * d * S;
+    // rows padded to a multiple of the XCD count (see the kernel)
+    const int blocks = (groups * d + kXcds - 1) / kXcds * kXcds * S;
 #define FBDT_CUT(M)                                                                             \
     cut_scan_kernel<M><<<blocks, kCutWaves * kWave, 0, s>>>(                                    \
         partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,      \
