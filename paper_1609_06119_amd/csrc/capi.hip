@@ -805,9 +805,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                         HIP_TRY(launch_route_list(
                             xb, ldb, n, d, n_bins, l >= 2 ? fb.node[(l - 1) & 1] : nullptr,
                             fb.node[l & 1], fb.w, vsign, pc, l, n_bins <= kMissingCode, lmode,
-                            fb.hfull[(l - 1) & 1], scale, cap_prev, (uint32_t)npad,
-                            l + 1 < D ? ctr + kListMaxSlots : nullptr, ctr, lstart, lcap, lside,
-                            list, fb.small[gl & 1], fb.sany + (gl & 1), fb.err, st));
+                            fb.hfull[(l - 1) & 1], scale, cap_prev, (uint32_t)npad, ctr, lstart,
+                            lcap, lside, list, fb.small[gl & 1], fb.sany + (gl & 1), fb.err, st));
                         tm.done();
                     }
                     {
@@ -815,7 +814,8 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                                  list_algorithmic_bytes(n, alpha, d, n_bins, l, !missing));
                         HIP_TRY(launch_hist_list(ls, lmode, list, lstart, lcap, ctr, lside, xr, d,
                                                  n_bins, vsign != nullptr, scale, lchunks,
-                                                 fb.partial, fb.err, st));
+                                                 fb.partial, fb.err,
+                                                 l + 1 < D ? ctr + kListMaxSlots : nullptr, st));
                         tm.done();
                     }
                     {

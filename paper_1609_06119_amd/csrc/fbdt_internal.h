@@ -342,30 +342,34 @@ ListShape plan_list_histogram(int d, int lists, int cu_count, size_t max_lds, in
 // [B][2] (lside[k] = 1: the right child of parent k), list k = parent k;
 // kCutStopped (missing values): that child in list 2k and the events that
 // stop at parent k in list 2k + 1; kCutPlain: every node of the layer.
-// cap_prev: sampled events per node of layer - 1 (null at layer 1: cap_root
-// for the root); cnt_out (optional, zeroed): receives the sampled events per
-// node of this layer; cursor [lists] (zeroed): receives the entries per
-// list; lstart / lcap [lists]: each list's range in `list` (at most cap_root
-// entries with hparent, else 2 cap_root); small: the layer's side histogram
+// cap_prev: bounds on the on-grid sampled events per node of layer - 1
+// (launch_hist_list's cnt_out of that layer; null at layer 1: cap_root for
+// the root); cursor [lists] (zeroed): receives the entries per list; lstart
+// / lcap [lists]: each list's range in `list` (at most cap_root entries with
+// hparent, else 2 cap_root); small: the layer's side histogram
 // [2^layer][d][B][2].
 hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, int n_bins,
                              const uint8_t *node_in, uint8_t *node_out, const float *w,
                              const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
                              int lmode, const uint64_t *hparent, int scale,
                              const uint32_t *cap_prev,
-                             uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
+                             uint32_t cap_root, uint32_t *cursor,
                              uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
                              double *small, uint32_t *sany, int *err, hipStream_t s);
 // (sany: set non-zero when a weight goes to small)
 // Histograms of the ls.lists lists of launch_route_list (lmode as there,
 // lside from the route pass) into prefix-summed partials [ls.parts][d][B]
 // [2], with lchunks [ls.lists] = {first part, parts | right child
-// histogrammed << 31} for the cut scan.
+// histogrammed << 31} for the cut scan.  cnt_out (optional) [2^layer]
+// receives bounds on the on-grid sampled events of every node of the layer
+// (the next layer's cap_prev): a listed node's entries, the other child of
+// a parent its capacity minus the listed child's entries (and minus the
+// events that stopped at the parent).
 hipError_t launch_hist_list(const ListShape &ls, int lmode, const uint2 *list,
                             const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
                             const uint32_t *lside, const uint8_t *xr, int d, int n_bins,
                             bool signed_w, int scale, uint2 *lchunks, uint64_t *partial, int *err,
-                            hipStream_t s);
+                            uint32_t *cnt_out, hipStream_t s);
 
 // Forest traversal.  cuts: [T][2^D-1] packed (feature | bin << 8), for the
 // general kernel; nodes: [T][16] for depth <= kApplyShallowDepth, for heap

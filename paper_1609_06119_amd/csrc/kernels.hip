@@ -1882,10 +1882,10 @@ __global__ __launch_bounds__(kTransposeThreads) void transpose_codes_kernel(
 // this layer, node <- 2 node + [code >= cut] (section 1.1); with miss, an
 // event whose code of the cut feature is the missing code, or which stopped
 // earlier, keeps its node (section 4.2).  A sampled event that has not
-// stopped is counted into cnt_out[node - 2^layer] (the caps of the next
-// layer's lists) and, if its weight is on the fixed-point grid (|w| >= tau)
-// and its node is listed, appended to the node's list as {event | negative
-// << 31, weight bits}.  Listed: with lmode kCutSibling one child of every
+// stopped, whose weight is on the fixed-point grid (|w| >= tau) and whose
+// node is listed, is appended to the node's list as {event | negative << 31,
+// weight bits}; the other events are counted nowhere (the list pass derives
+// the next layer's capacities from the lists).  Listed: with lmode kCutSibling one child of every
 // parent, the one whose fixed-point weight in the parent's summed rows
 // hparent is smaller (lside[k] = 1: the right child; the histogram pass
 // takes it and the cut scan forms the other as parent - child), list k =
@@ -1893,8 +1893,8 @@ __global__ __launch_bounds__(kTransposeThreads) void transpose_codes_kernel(
 // at parent k here (on the grid) in list 2k + 1 (the other child is parent -
 // child - stopped); with kCutPlain every node of the layer, list k = node k.
 // List k is the range [start_k,
-// start_k + cap_k) of `list`: cap_k = the sampled events of its node's
-// parent (cap_prev, or cap_root at layer 1), start_k = the caps of the lists
+// start_k + cap_k) of `list`: cap_k = a bound on the on-grid sampled events
+// of its node's parent (cap_prev, or cap_root at layer 1), start_k = the caps of the lists
 // below k; workgroup 0 records both (lstart, lcap) and lside.  Each
 // workgroup counts its entries per list in LDS and reserves them with one
 // atomic add per list on cursor[k], so a list holds its events in no fixed
@@ -1924,12 +1924,12 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
     int layer, bool miss, int lmode, const uint64_t *__restrict__ hparent, uint32_t tau_bits,
-    const uint32_t *__restrict__ cap_prev, uint32_t cap_root, uint32_t *__restrict__ cnt_out,
+    const uint32_t *__restrict__ cap_prev, uint32_t cap_root,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ lstart, uint32_t *__restrict__ lcap,
     uint32_t *__restrict__ lside, uint2 *__restrict__ list, double *__restrict__ small,
     int *__restrict__ err, int64_t xcd_events, uint32_t *__restrict__ sany) {
     __shared__ uint8_t s_cf[64], s_cc[64], s_side[64];
-    __shared__ uint32_t s_cnt[kListMaxSlots], s_ncnt[kListMaxSlots];
+    __shared__ uint32_t s_cnt[kListMaxSlots];
     __shared__ uint32_t s_start[kListMaxSlots], s_cap[kListMaxSlots], s_base[kListMaxSlots];
     const uint32_t half = 1u << (layer - 1), nodes = 1u << layer;
     const bool sib = lmode == kCutSibling, stops = lmode == kCutStopped;
@@ -1985,7 +1985,6 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
             }
         }
         s_cnt[lane] = 0u;
-        s_ncnt[lane] = 0u;
     }
     __syncthreads();
 
@@ -2042,16 +2041,14 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
                 o[e >> 2] |= ne << (8 * (e & 3));
                 const uint32_t ab = wb[e] & 0x7fffffffu;
                 if (ab != 0u && !stop) {
-                    // counted once: as an entry of its list (listed node, on
-                    // the grid), else into its node's other events
+                    // an entry of its list if its node is listed and its
+                    // weight on the grid
                     const uint32_t nl = ne - nodes;
                     const bool listed = !pick || (nl & 1u) == s_side[kk];
                     if (ab < tau_bits) below |= 1u << e;
                     if (listed && ab >= tau_bits) {
                         const uint32_t slot = sib ? kk : stops ? 2u * kk : nl;
                         rec[st][e] = slot << 16 | atomicAdd(&s_cnt[slot], 1u);
-                    } else {
-                        atomicAdd(&s_ncnt[nl], 1u);
                     }
                 } else if (stops && stop && !earlier && ab >= tau_bits) {
                     // stops at parent kk here: its list of stopped events
@@ -2086,14 +2083,6 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     if (threadIdx.x < (unsigned)nslots) {
         const uint32_t c = s_cnt[threadIdx.x];
         s_base[threadIdx.x] = c ? atomicAdd(&cursor[threadIdx.x], c) : 0u;
-    } else if (cnt_out && threadIdx.x >= kListMaxSlots &&
-               threadIdx.x < kListMaxSlots + (unsigned)nodes) {
-        const uint32_t t = threadIdx.x - kListMaxSlots;
-        // node t's sampled events: its other events, plus its list's entries
-        // if it is the listed node
-        const bool listed = !pick || (t & 1u) == s_side[t >> 1];
-        const uint32_t c = s_ncnt[t] + (listed ? s_cnt[sib ? t >> 1 : stops ? t & ~1u : t] : 0u);
-        if (c) atomicAdd(&cnt_out[t], c);
     }
     __syncthreads();
 #pragma unroll
@@ -2149,7 +2138,7 @@ __global__ __launch_bounds__(1024) void hist_list_kernel(
     const uint32_t *__restrict__ lside, const uint8_t *__restrict__ xr, int dr, int d,
     int nbins, bool miss, int G, int parts, int nlists, int lmode, int per_xcd, int scale,
     int copies, int copy_stride, uint2 *__restrict__ lchunks, uint64_t *__restrict__ partial,
-    int *__restrict__ err) {
+    int *__restrict__ err, uint32_t *__restrict__ cnt_out) {
     constexpr int NQ = FPG / 4;
     // the rows take all of the LDS (40 features: 160 KiB); the prologue's
     // few words sit at its start until the rows are cleared
@@ -2180,6 +2169,28 @@ __global__ __launch_bounds__(1024) void hist_list_kernel(
             if (lane >= o) x += y;
         }
         if (lane < nlists && blockIdx.x == 0) lchunks[lane] = make_uint2(x - c, c | flag << 31);
+        if (cnt_out && blockIdx.x == 0) {
+            // bounds on the on-grid sampled events of every node of the layer
+            // (the next layer's list capacities; entries never leave them):
+            // a listed node's entries, and for the other child of a parent
+            // the parent's capacity minus the listed child's entries (and
+            // minus the events that stopped at the parent)
+            const uint32_t m_next = __shfl_down(m, 1);
+            if (lmode == kCutPlain) {
+                if (lane < nlists) cnt_out[lane] = m;
+            } else if (lmode == kCutSibling) {
+                if (lane < nlists) {
+                    const uint32_t cap = lcap[lane];
+                    cnt_out[2 * lane + flag] = m;
+                    cnt_out[2 * lane + 1 - flag] = cap - m;
+                }
+            } else if (lane < nlists && (lane & 1) == 0) {   // kCutStopped: lists 2k, 2k + 1
+                const uint32_t cap = lcap[lane];
+                const int k = lane >> 1;
+                cnt_out[2 * k + flag] = m;
+                cnt_out[2 * k + 1 - flag] = cap - m - m_next;
+            }
+        }
         // the list whose parts hold part slot w, if any
         const bool mine = lane < nlists && (uint32_t)w >= x - c && (uint32_t)w < x;
         const uint64_t any = __ballot(mine);   // every lane of the wavefront votes
@@ -3293,7 +3304,7 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
                              const uint8_t *node_in, uint8_t *node_out, const float *w,
                              const uint8_t *vsign, const ParentCuts &pc, int layer, bool miss,
                              int lmode, const uint64_t *hparent, int scale, const uint32_t *cap_prev,
-                             uint32_t cap_root, uint32_t *cnt_out, uint32_t *cursor,
+                             uint32_t cap_root, uint32_t *cursor,
                              uint32_t *lstart, uint32_t *lcap, uint32_t *lside, uint2 *list,
                              double *small, uint32_t *sany, int *err, hipStream_t s) {
     if (layer < 1 || layer > 6 || n < 1 || n > kListMaxEvents) return hipErrorInvalidValue;
@@ -3313,7 +3324,7 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
     route_list_kernel<SG, O32><<<blocks, kRouteListThreads, 0, s>>>(                            \
         xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices, \
         pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent, tau_bits, cap_prev, cap_root,  \
-        cnt_out, cursor, lstart, lcap, lside, list, small, err, R, sany)
+        cursor, lstart, lcap, lside, list, small, err, R, sany)
     if (vsign && off32)
         FBDT_ROUTE_LIST(true, true);
     else if (vsign)
@@ -3330,23 +3341,25 @@ template <int FPG>
 void hist_list_go(const ListShape &ls, int lmode, bool signed_w, hipStream_t s, const uint2 *list,
                   const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
                   const uint32_t *lside, const uint8_t *xr, int dr, int d, int nbins, int scale,
-                  uint2 *lchunks, uint64_t *partial, int *err) {
+                  uint2 *lchunks, uint64_t *partial, int *err, uint32_t *cnt_out) {
     const bool miss = nbins <= kMissingCode;
     if (signed_w)
         hist_list_kernel<FPG, true><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
             list, lstart, lcap, cursor, lside, xr, dr, d, nbins, miss, ls.groups, ls.parts,
-            ls.lists, lmode, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+            ls.lists, lmode, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err,
+            cnt_out);
     else
         hist_list_kernel<FPG, false><<<ls.blocks, 1024, ls.lds_bytes, s>>>(
             list, lstart, lcap, cursor, lside, xr, dr, d, nbins, miss, ls.groups, ls.parts,
-            ls.lists, lmode, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err);
+            ls.lists, lmode, ls.per_xcd, scale, ls.copies, ls.copy_stride, lchunks, partial, err,
+            cnt_out);
 }
 
 hipError_t launch_hist_list(const ListShape &ls, int lmode, const uint2 *list,
                             const uint32_t *lstart, const uint32_t *lcap, const uint32_t *cursor,
                             const uint32_t *lside, const uint8_t *xr, int d, int n_bins,
                             bool signed_w, int scale, uint2 *lchunks, uint64_t *partial, int *err,
-                            hipStream_t s) {
+                            uint32_t *cnt_out, hipStream_t s) {
     if (ls.lists < 1 || ls.lists > kListMaxSlots || ls.groups * ls.fpg < d ||
         ls.parts <= ls.lists || ls.blocks != kXcds * ls.per_xcd ||
         ls.per_xcd * kXcds < ls.parts * ls.groups ||
@@ -3354,13 +3367,13 @@ hipError_t launch_hist_list(const ListShape &ls, int lmode, const uint2 *list,
         return hipErrorInvalidValue;
     const int dr = list_row_bytes(d);
     switch (ls.fpg) {
-    case 4: hist_list_go<4>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 8: hist_list_go<8>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 12: hist_list_go<12>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 20: hist_list_go<20>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 28: hist_list_go<28>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 36: hist_list_go<36>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
-    case 40: hist_list_go<40>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err); break;
+    case 4: hist_list_go<4>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err, cnt_out); break;
+    case 8: hist_list_go<8>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err, cnt_out); break;
+    case 12: hist_list_go<12>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err, cnt_out); break;
+    case 20: hist_list_go<20>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err, cnt_out); break;
+    case 28: hist_list_go<28>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err, cnt_out); break;
+    case 36: hist_list_go<36>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err, cnt_out); break;
+    case 40: hist_list_go<40>(ls, lmode, signed_w, s, list, lstart, lcap, cursor, lside, xr, dr, d, n_bins, scale, lchunks, partial, err, cnt_out); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
