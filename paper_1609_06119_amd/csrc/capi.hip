@@ -719,6 +719,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     unsigned long long *tl = nullptr;
     if (timeline) cv.add(&tl, tl_count);
     cv.add(&fb.sany, 2);   // last: the other buffers keep their offsets
+    cv.add(&fb.keys, 2 * kKeyWords);
     if ((rc = arena_reserve(a, cv.off))) return rc;
     cv.assign(a.ptr);
     if (timeline) HIP_TRY(launch_fill_u32(tl, 0u, 2 * tl_count, s));
@@ -727,6 +728,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
     HIP_TRY(launch_fill_u32(fb.small[0], 0u, 2 * small_elems, s));
     HIP_TRY(launch_fill_u32(fb.small[1], 0u, 2 * small_elems, s));
     HIP_TRY(launch_fill_u32(fb.sany, 0u, 2, s));
+    HIP_TRY(launch_fill_u32(reinterpret_cast<uint32_t *>(fb.keys), 0u, 2 * 2 * kKeyWords, s));
     // the histogram and leaf passes read whole steps of events: padded events
     // weigh 0 and have no pseudo-response
     HIP_TRY(launch_fill_u32(fb.w, 0u, (size_t)npad, s));
@@ -785,14 +787,16 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
             uint8_t *cf = fb.cut_feature + (size_t)t * nin;
             uint8_t *cc = fb.cut_bin + (size_t)t * nin;
             double *cg = fb.gain + (size_t)t * nin;
+            // best-cut keys of layer gl = t * D + l (by gl's parity)
+            auto keys = [&](int gl) { return fb.keys + (size_t)(gl & 1) * kKeyWords; };
             for (int l = 0; l < D; ++l) {
-                // the previous layer's candidates give the cuts this pass routes
+                const int gl = t * D + l;   // side histograms alternate by gl's parity
+                // the previous layer's best cuts are the ones this pass routes
                 // with; workgroup 0 records them in the model
                 const int plo = l >= 1 ? (1 << (l - 1)) - 1 : 0;
                 ParentCuts pc;
                 if (l >= 1)
-                    pc = ParentCuts{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
-                const int gl = t * D + l;   // side histograms alternate by gl's parity
+                    pc = ParentCuts{fb.cand_gain, keys(gl - 1), S, cf + plo, cc + plo, cg + plo};
                 if (lists && l >= 1) {
                     // route with list output, then histogram the lists
                     const ListShape &ls = lplans[l];
@@ -828,7 +832,7 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                                                 n_bins, lmode, fb.cand_gain, fb.cand_cut,
                                                 fb.hfull[(l - 1) & 1],
                                                 l + 1 < D ? fb.hfull[l & 1] : nullptr, st,
-                                                lchunks));
+                                                lchunks, nullptr, 0, keys(gl), keys(gl + 1)));
                         tm.done();
                     }
                     continue;
@@ -877,13 +881,15 @@ int fbdt_fit(const uint8_t *xb, int64_t n, int32_t d, int64_t ldb, int32_t n_bin
                                             fb.cand_gain, fb.cand_cut,
                                             cmode != kCutPlain ? fb.hfull[(l - 1) & 1] : nullptr,
                                             l + 1 < D ? fb.hfull[l & 1] : nullptr, st, nullptr,
-                                            clear ? lctr : nullptr, clear ? (int)lctr_count : 0));
+                                            clear ? lctr : nullptr, clear ? (int)lctr_count : 0,
+                                            keys(gl), keys(gl + 1)));
                     tm.done();
                 }
             }
             {
                 const int plo = (1 << (D - 1)) - 1;
-                const ParentCuts pc{fb.cand_gain, fb.cand_cut, S, cf + plo, cc + plo, cg + plo};
+                const ParentCuts pc{fb.cand_gain, keys(t * D + D - 1), S, cf + plo, cc + plo,
+                                    cg + plo};
                 // the leaves of deep trees are routed by a pass of their own,
                 // like the deep layers
                 const bool own_route = (1 << (D - 1)) > kRoutedMaxParents;

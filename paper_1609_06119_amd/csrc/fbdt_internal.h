@@ -69,6 +69,8 @@ struct FitBuffers {
                           // [nodes][d][B][2], by the parity of tree * D + layer
     uint32_t *sany;       // [2] non-zero once a list route pass added to small[p] (cleared
                           // with it)
+    unsigned long long *keys;   // [2][kKeyWords] best-cut keys of a layer's nodes, by the
+                                // parity of tree * D + layer
     double *cand_gain;    // [max nodes][d * slices] best gain of every (node, feature, slice)
     int *cand_cut;        // [max nodes][d * slices] and its bin
     double *leaf_partial;   // [leaf blocks][2^D][2]
@@ -144,12 +146,23 @@ hipError_t launch_tree_prep(const int8_t *y, const float *v, double *F, const do
 HistShape plan_histogram(int64_t n, int d, int n_bins, int layer, bool sibling, int cu_count,
                          size_t max_lds, const HistOverrides &ov);
 
-// Candidate cuts of a layer's nodes, one per (node, feature), from which a
-// routed pass takes each parent's cut (best gain, then lowest feature);
-// rec_* (optional) receive those cuts for the model (written by workgroup 0).
+// Best-cut keys of a layer's nodes: the cut scan takes the maximum of every
+// candidate's 64-bit key (gain order, then lowest feature and bin) into
+// keys[(node * kXcds + x) * kKeyStride], a slot per node and XCD x of the
+// candidate's workgroup (one 128-byte line each, so that the atomics of a
+// node spread over 8 lines); the node's key is the maximum of its slots; 0 =
+// no candidate.  Two buffers of kKeyNodes nodes, used by alternate layers.
+constexpr int kKeyStride = 16;
+constexpr int kKeyNodes = 64;
+constexpr size_t kKeyWords = (size_t)kKeyNodes * kXcds * kKeyStride;   // per buffer
+
+// The cuts a routed pass takes for the parents of its layer: their best-cut
+// keys, and the candidates (gain of the best cut of each (node, feature,
+// slice)) whose gain rec_g receives; rec_* (optional) receive the cuts for
+// the model (written by workgroup 0).
 struct ParentCuts {
     const double *cand_gain = nullptr;   // [nodes][d * slices]
-    const int *cand_cut = nullptr;
+    const unsigned long long *keys = nullptr;
     int slices = 1;
     uint8_t *rec_f = nullptr;
     uint8_t *rec_c = nullptr;
@@ -234,7 +247,10 @@ hipError_t launch_best_cuts_f64(const double *hist, int n_nodes, int d, int n_bi
 // lchunks (list passes): the partials of slot k are the rows [x_k, x_k +
 // (y_k & 0x7fffffff)) of [*][d][B][2], and bit 31 of y_k tells that a
 // child slot holds the right child (the left is then the one formed).
-// clear_words (optional): clear_count words zeroed on the way.
+// clear_words (optional): clear_count words zeroed on the way.  keys
+// (optional): each node's best-cut key slots (kKeyWords, zero on entry), the
+// maximum of its candidates' keys; keys_next (optional): the next layer's,
+// cleared on the way.
 enum CutMode : int {
     kCutPlain = 0,     // slot k holds node k
     kCutSibling = 1,   // slot k holds one child of parent k, the other is parent - child
@@ -247,7 +263,8 @@ hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const
                            int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
                            const uint2 *lchunks = nullptr, uint32_t *clear_words = nullptr,
-                           int clear_count = 0);
+                           int clear_count = 0, unsigned long long *keys = nullptr,
+                           unsigned long long *keys_next = nullptr);
 
 // Best cut of each node over its candidates (d features x slices entries).
 hipError_t launch_select_cuts(const double *cand_gain, const int *cand_cut, int n_nodes, int d,
@@ -286,8 +303,8 @@ hipError_t launch_route(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_
 // deeper layers are routed by launch_route_layer first.
 constexpr int kRoutedMaxParents = 4;
 
-// Routing of layer `layer` (>= 1) on its own: the parents' cuts from the
-// candidates in pc (recorded in the model through pc.rec_*), then
+// Routing of layer `layer` (>= 1) on its own: the parents' cuts from their
+// best-cut keys in pc (recorded in the model through pc.rec_*), then
 // node_out[i] = 2 node_in[i] + [code >= cut] for every event up to
 // round_up(n, 8); with miss (n_bins <= kMissingCode) an event whose code of
 // the cut feature is kMissingCode, or whose id lies below the parents'

@@ -384,8 +384,7 @@ __global__ __launch_bounds__(kLeafReduceThreads) void tree_prep_kernel(
 // The best candidate of a node (gain highest, then lowest entry: lowest
 // feature, then lowest bin) is found by one wavefront; lane 0 returns it.  An
 // unusable result (no finite gain) falls back to feature 0 and reports it.
-// Split into the loads of the first kCandRegs * 64 entries and the
-// reduction, so that a kernel can issue the loads early.
+// (The fit's routed passes take their cuts from the best-cut keys below.)
 struct CandSet {
     const double *gain;   // [nodes][E]
     const int *cut;       // [nodes][E]
@@ -393,44 +392,15 @@ struct CandSet {
     int S;                // slices per feature; E = d * S entries per node
 };
 
-constexpr int kCandRegs = 8;
+constexpr int kCutSlice = 31;   // cuts per slice (the cut scan's workgroups)
 
-struct CandRegs {
-    double g[kCandRegs];
-    int c[kCandRegs];
-};
-
-__device__ __forceinline__ void cand_load(const CandSet &cs, int k, int lane, CandRegs &r) {
-    const int E = cs.d * cs.S;
-#pragma unroll
-    for (int q = 0; q < kCandRegs; ++q) {
-        const int e = lane + kWave * q;
-        if (e < E) {
-            r.g[q] = cs.gain[(size_t)k * E + e];
-            r.c[q] = cs.cut[(size_t)k * E + e];
-        } else {
-            r.g[q] = -INFINITY;
-            r.c[q] = 1;
-        }
-    }
-}
-
-__device__ __forceinline__ void cand_reduce(const CandRegs &r, const CandSet &cs, int k, int lane,
-                                            int *bf, int *bc, double *bg, bool *ok) {
+__device__ __forceinline__ void node_best(const CandSet &cs, int k, int lane, int *bf, int *bc,
+                                          double *bg, bool *ok) {
     const int E = cs.d * cs.S;
     double g = -INFINITY;
     int idx = 0x7fffffff, c = 1;
     // each lane visits its entries in rising order: a strict > keeps the lowest
-#pragma unroll
-    for (int q = 0; q < kCandRegs; ++q) {
-        const int e = lane + kWave * q;
-        if (e < E && r.g[q] > g) {
-            g = r.g[q];
-            idx = e;
-            c = r.c[q];
-        }
-    }
-    for (int e = lane + kWave * kCandRegs; e < E; e += kWave) {
+    for (int e = lane; e < E; e += kWave) {
         const double x = cs.gain[(size_t)k * E + e];
         if (x > g) {
             g = x;
@@ -456,11 +426,70 @@ __device__ __forceinline__ void cand_reduce(const CandRegs &r, const CandSet &cs
     *bg = g;
 }
 
-__device__ __forceinline__ void node_best(const CandSet &cs, int k, int lane, int *bf, int *bc,
-                                          double *bg, bool *ok) {
-    CandRegs r;
-    cand_load(cs, k, lane, r);
-    cand_reduce(r, cs, k, lane, bf, bc, bg, ok);
+// Best cut of a node as one 64-bit key, so that the cut scan can take the
+// maximum over all of a node's candidates with atomicMax: the gain's bits
+// mapped to an unsigned order (sign bit set for non-negative values, every
+// bit flipped for negative ones; -0 taken as +0), with the low 16 bits
+// replaced by 0xffff - (256 j + c), so that the higher gain wins, then the
+// lower (feature, bin).  Gains that differ only in those 16 mantissa bits
+// (2^-36 relative) count as tied.  A finite or +inf gain gives a non-zero
+// key; 0 means that the node has no candidate.
+__device__ __forceinline__ unsigned long long cut_key(double g, int j, int c) {
+    const unsigned long long u = (unsigned long long)__double_as_longlong(g == 0.0 ? 0.0 : g);
+    const unsigned long long o = (u >> 63) ? ~u : (u | (1ull << 63));
+    return (o & ~0xffffull) | (0xffffull - (unsigned long long)(j * 256 + c));
+}
+
+// Feature and bin of a key; an absent or unusable key falls back to feature
+// 0, bin 1 and reports it (ok = false).
+__device__ __forceinline__ void key_cut(unsigned long long key, int d, int *bf, int *bc, bool *ok) {
+    const int jc = 0xffff - (int)(key & 0xffffull);
+    const int j = jc >> 8, c = jc & 0xff;
+    *ok = key != 0ull && j < d && c >= 1;
+    *bf = *ok ? j : 0;
+    *bc = *ok ? c : 1;
+}
+
+// The key slots of parent k (one per XCD), loaded so that a kernel can
+// issue them early, and their maximum, the parent's key.
+struct KeySlots {
+    unsigned long long v[kXcds];
+};
+
+__device__ __forceinline__ void key_load(const unsigned long long *keys, int k, KeySlots &r) {
+#pragma unroll
+    for (int x = 0; x < kXcds; ++x) r.v[x] = keys[((size_t)k * kXcds + x) * kKeyStride];
+}
+
+__device__ __forceinline__ unsigned long long key_max(const KeySlots &r) {
+    unsigned long long m = r.v[0];
+#pragma unroll
+    for (int x = 1; x < kXcds; ++x) m = max(m, r.v[x]);
+    return m;
+}
+
+// Cut of parent k of a routed pass from its key slots into the cut table.
+__device__ __forceinline__ void parent_cut(const KeySlots &r, int k, int d, uint8_t *s_cf,
+                                           uint8_t *s_cc, int &eflag) {
+    int bf, bc;
+    bool ok;
+    key_cut(key_max(r), d, &bf, &bc, &ok);
+    s_cf[k] = (uint8_t)bf;
+    s_cc[k] = (uint8_t)bc;
+    if (!ok) eflag |= kErrRoute;
+}
+
+// Parent k's cut recorded in the model once the cut table is in LDS:
+// feature and bin; returns the gain to record, that of the candidate of the
+// slice that holds the cut (a load that the caller stores at its end, so
+// that no wavefront waits for it).
+__device__ __forceinline__ double record_parent_cut(const uint8_t *s_cf, const uint8_t *s_cc,
+                                                    int k, int d, int S, const double *cand_gain,
+                                                    uint8_t *rec_f, uint8_t *rec_c) {
+    const int f = s_cf[k], c = s_cc[k];
+    rec_f[k] = (uint8_t)f;
+    rec_c[k] = (uint8_t)c;
+    return cand_gain[((size_t)k * d + f) * S + (c - 1) / kCutSlice];
 }
 
 // Cuts of n_nodes nodes from their candidates (one wavefront per node).
@@ -804,7 +833,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const uint8_t *__restrict__ xb, const float *__restrict__ w,
     const uint8_t *__restrict__ node_in, int64_t ldb, int64_t n, int64_t chunk_events,
     int64_t xcd_events, uint32_t geo, uint32_t mode, const double *__restrict__ cand_gain,
-    const int *__restrict__ cand_cut, int nbins, int scale, int copy_stride,
+    const unsigned long long *__restrict__ keys, int nbins, int scale, int copy_stride,
     const uint8_t *__restrict__ vsign, uint8_t *__restrict__ node_out,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
     uint64_t *__restrict__ partial, double *__restrict__ small, int *__restrict__ err,
@@ -882,15 +911,13 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     const bool writer = ROUTED && layer >= 1 && g == 0 && h == 0 && node_out != nullptr;
     const int64_t stride = (int64_t)kHistE * blockDim.x;
 
-    // Loads in flight together: the candidates of this wavefront's parent
-    // node (the cut table of a routed pass) first, then the first step's
-    // weights, node ids and codes; the candidates are reduced while the
-    // event data arrives, and the step's routing rows follow once the cut
-    // table is in LDS.
-    CandRegs cr;
-    const CandSet cs{cand_gain, cand_cut, d, cslices};
-    const bool pwave = ROUTED && layer >= 1 && wave < a.half;
-    if (pwave) cand_load(cs, wave, lane, cr);
+    // Loads in flight together: the parents' best-cut keys (the cut table of
+    // a routed pass; lane k of wavefront 0 takes parent k) first, then the
+    // first step's weights, node ids and codes; the step's routing rows
+    // follow once the cut table is in LDS.
+    const bool pwave = ROUTED && layer >= 1 && wave == 0 && lane < a.half;
+    KeySlots ks;
+    if (pwave) key_load(keys, lane, ks);
     HistStep<NP, FPG> A, B;
     int64_t ia = start + (int64_t)kHistE * threadIdx.x;
     if (ia < end) hist_load<ROUTED, NP, FPG, SIGNED, MISS>(A, a, s_cf, ia, false);
@@ -901,29 +928,12 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         for (int t = threadIdx.x; t < n16; t += blockDim.x) l4[t] = make_uint4(0u, 0u, 0u, 0u);
     }
     if (stamp) tl[(size_t)blockIdx.x * kTimelineStamps + 6] = (unsigned long long)wall_clock64();
-    if (ROUTED && layer >= 1) {
-        // cut of parent k from its candidates; workgroup 0 records it in the model
-        for (int k = wave; k < a.half; k += nwaves) {
-            int bf, bc;
-            double bg;
-            bool ok;
-            if (k == wave)
-                cand_reduce(cr, cs, k, lane, &bf, &bc, &bg, &ok);
-            else
-                node_best(cs, k, lane, &bf, &bc, &bg, &ok);
-            if (lane == 0) {
-                s_cf[k] = (uint8_t)bf;
-                s_cc[k] = (uint8_t)bc;
-                if (!ok) eflag |= kErrRoute;
-                if (blockIdx.x == 0 && rec_f) {
-                    rec_f[k] = (uint8_t)bf;
-                    rec_c[k] = (uint8_t)bc;
-                    rec_g[k] = bg;
-                }
-            }
-        }
-    }
+    if (pwave) parent_cut(ks, lane, d, s_cf, s_cc, eflag);
     lds_barrier();
+    // workgroup 0 records the parents' cuts in the model (the gains after the adds)
+    const bool rec = pwave && blockIdx.x == 0 && rec_f;
+    const double rg = rec ? record_parent_cut(s_cf, s_cc, lane, d, cslices, cand_gain, rec_f,
+                                              rec_c) : 0.0;
     const unsigned long long t_table = stamp ? (unsigned long long)wall_clock64() : 0ull;
     unsigned long long t_first = 0ull;
     uint32_t cut[4] = {0u, 0u, 0u, 0u};
@@ -952,6 +962,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(
         }
     }
     lds_barrier();
+    if (rec) rec_g[lane] = rg;
     const unsigned long long t_adds = stamp ? (unsigned long long)wall_clock64() : 0ull;
     hist_write_rows(lds, copies, copy_stride, lds_n, a.nk, a.nf, FPG, a.k0, a.j0, d, nbins,
                     a.miss, prefix, reinterpret_cast<uint4 *>(partial + (size_t)p * hnodes * d * nbins * 2),
@@ -1215,7 +1226,6 @@ __global__ __launch_bounds__(kWave) void best_cuts_f64_kernel(const double *__re
 // sums): a cut with an empty side has gain exactly 0; a cut c >= 2 whose bin
 // c-1 is empty makes the same partition as cut c-1 and is skipped, so the
 // lower cut wins that tie whatever the rounding.
-constexpr int kCutSlice = 31;
 constexpr int kCutWaves = 4;
 
 template <int MODE>   // CutMode
@@ -1225,7 +1235,8 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
     double *__restrict__ cand_gain, int *__restrict__ cand_cut,
     const uint64_t *__restrict__ hparent, uint64_t *__restrict__ hout,
     const uint2 *__restrict__ lchunks, uint32_t *__restrict__ clear_words, int clear_count,
-    const uint32_t *__restrict__ sany, uint32_t *__restrict__ sany_next) {
+    const uint32_t *__restrict__ sany, uint32_t *__restrict__ sany_next,
+    unsigned long long *__restrict__ keys, unsigned long long *__restrict__ keys_next) {
 #pragma clang fp contract(off)
     constexpr bool PAIR = MODE != kCutPlain;   // both children of a parent per workgroup
     __shared__ uint64_t red[kCutWaves][kWave + 2];
@@ -1341,6 +1352,9 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         const size_t hi = min(small_next_count, lo + per);
         for (size_t t = lo + threadIdx.x; t < hi; t += blockDim.x) small_next[t] = 0.0;
         if (sany_next && blockIdx.x == 0 && threadIdx.x == 0) *sany_next = 0u;
+        if (keys_next && blockIdx.x == 0)
+            for (int t = threadIdx.x; t < kKeyNodes * kXcds; t += blockDim.x)
+                keys_next[(size_t)t * kKeyStride] = 0ull;
         if (clear_words && blockIdx.x == 0)
             for (int t = threadIdx.x; t < clear_count; t += blockDim.x) clear_words[t] = 0u;
     }
@@ -1459,6 +1473,8 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
         const size_t e = (size_t)node * d * S + (size_t)j * S + q;
         cand_gain[e] = best;
         cand_cut[e] = bestc;
+        if (keys && best > -INFINITY)   // the slot of this workgroup's XCD
+            atomicMax(keys + ((size_t)node * kXcds + xq) * kKeyStride, cut_key(best, j, bestc));
     }
 }
 
@@ -1467,7 +1483,7 @@ __global__ __launch_bounds__(kCutWaves * kWave) void cut_scan_kernel(
 // sum(v |y~| (2 - |y~|)) over the sampled events, one partial per
 // workgroup, from yts (y~ of the sampled events, 0 for the others, written
 // by the re-weighting pass).  Routed mode first takes the last layer's cuts
-// from their candidates, sends every event from layer depth-1 to its leaf
+// from their best-cut keys, sends every event from layer depth-1 to its leaf
 // and stores the leaf id; with at most four parents the code rows of the
 // parents' cut features are loaded with the step's other data, so routing
 // costs no dependent load.
@@ -1558,7 +1574,7 @@ template <bool ROUTED, int NP>
 __global__ __launch_bounds__(512) void leaf_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
-    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
+    const double *__restrict__ cand_gain, const unsigned long long *__restrict__ keys, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
     int depth, bool missing, const float *__restrict__ v, const double *__restrict__ yts,
     double *__restrict__ leaf_partial, int *__restrict__ err, int64_t xcd_events) {
@@ -1587,36 +1603,21 @@ __global__ __launch_bounds__(512) void leaf_kernel(
     const int64_t stride = (int64_t)(gridDim.x / kXcds) * T * kLeafE;
     int64_t ia = xlo + ((int64_t)(blockIdx.x / kXcds) * T + threadIdx.x) * kLeafE;
 
-    CandRegs cr;
-    const CandSet cs{cand_gain, cand_cut, d, cslices};
-    const bool pwave = ROUTED && wave < half;
-    if (pwave) cand_load(cs, wave, lane, cr);
+    // the parents' best-cut keys (lane k of wavefront 0 takes parent k) in
+    // flight with the first step's data
+    const bool pwave = ROUTED && wave == 0 && lane < half;
+    KeySlots ks;
+    if (pwave) key_load(keys, lane, ks);
     LeafStep<NP> A, B;
     if (ia < xend) leaf_load<ROUTED, NP>(A, xb, ldb, d, node_in, v, yts, s_cf, ia, false);
     const int TP = ncol + 1;   // row stride: rows start two LDS banks apart
     for (int t = threadIdx.x; t < nv * TP; t += T) acc[t] = 0.0;
-    if (ROUTED) {
-        for (int k = wave; k < half; k += nwaves) {
-            int bf, bc;
-            double bg;
-            bool ok;
-            if (k == wave)
-                cand_reduce(cr, cs, k, lane, &bf, &bc, &bg, &ok);
-            else
-                node_best(cs, k, lane, &bf, &bc, &bg, &ok);
-            if (lane == 0) {
-                s_cf[k] = (uint8_t)bf;
-                s_cc[k] = (uint8_t)bc;
-                if (!ok) eflag |= kErrRoute;
-                if (blockIdx.x == 0 && rec_f) {
-                    rec_f[k] = (uint8_t)bf;
-                    rec_c[k] = (uint8_t)bc;
-                    rec_g[k] = bg;
-                }
-            }
-        }
-    }
+    if (pwave) parent_cut(ks, lane, d, s_cf, s_cc, eflag);
     lds_barrier();
+    // workgroup 0 records the parents' cuts in the model (the gains at the end)
+    const bool rec = pwave && blockIdx.x == 0 && rec_f;
+    const double rg = rec ? record_parent_cut(s_cf, s_cc, lane, d, cslices, cand_gain, rec_f,
+                                              rec_c) : 0.0;
     uint32_t cut[4] = {0u, 0u, 0u, 0u};
     if (ROUTED && NP > 0) {
 #pragma unroll
@@ -1703,6 +1704,7 @@ __global__ __launch_bounds__(512) void leaf_kernel(
         }
     }
     lds_barrier();
+    if (rec) rec_g[lane] = rg;
     // columns added in a fixed order: G segments of T / G columns per value,
     // then the G segment sums; G is a power of two (nv need not be one, so
     // T / nv may not divide T) with G nv <= T
@@ -1743,7 +1745,7 @@ __global__ __launch_bounds__(kLeafReduceThreads) void leaf_finalize_kernel(
 // code byte from the row of its parent's cut feature (a cache line per lane
 // of the load, as the parents of a wavefront's events differ), once in every
 // feature group's workgroup; here the gather happens once per event.  Every
-// workgroup forms the parents' cuts from their candidates (workgroup 0
+// workgroup takes the parents' cuts from their best-cut keys (workgroup 0
 // records them in the model), then moves each event of its XCD's range to
 // its node of this layer, node <- 2 node + [code >= cut] (section 1.1).
 // With miss, an event whose code of the cut feature is the missing code, or
@@ -1753,32 +1755,25 @@ constexpr int kRouteLayerThreads = 1024;
 __global__ __launch_bounds__(kRouteLayerThreads) void route_layer_kernel(
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
-    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
+    const double *__restrict__ cand_gain, const unsigned long long *__restrict__ keys, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
     int layer, bool miss, int *__restrict__ err, int64_t xcd_events) {
     __shared__ uint8_t s_cf[64], s_cc[64];
     const uint32_t half = 1u << (layer - 1);
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int nwaves = blockDim.x / kWave;
     int eflag = 0;
-    const CandSet cs{cand_gain, cand_cut, d, cslices};
-    for (int k = wave; k < (int)half; k += nwaves) {
-        int bf, bc;
-        double bg;
-        bool ok;
-        node_best(cs, k, lane, &bf, &bc, &bg, &ok);
-        if (lane == 0) {
-            s_cf[k] = (uint8_t)bf;
-            s_cc[k] = (uint8_t)bc;
-            if (!ok) eflag |= kErrRoute;
-            if (blockIdx.x == 0 && rec_f) {
-                rec_f[k] = (uint8_t)bf;
-                rec_c[k] = (uint8_t)bc;
-                rec_g[k] = bg;
-            }
-        }
+    // the parents' cuts from their best-cut keys (lane k of wavefront 0 takes parent k)
+    const bool pwave = wave == 0 && lane < (int)half;
+    if (pwave) {
+        KeySlots ks;
+        key_load(keys, lane, ks);
+        parent_cut(ks, lane, d, s_cf, s_cc, eflag);
     }
     __syncthreads();
+    // workgroup 0 records them in the model (the gains at the end)
+    const bool rec = pwave && blockIdx.x == 0 && rec_f;
+    const double rg = rec ? record_parent_cut(s_cf, s_cc, lane, d, cslices, cand_gain, rec_f,
+                                              rec_c) : 0.0;
     // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
     const int64_t xlo = (int64_t)(blockIdx.x % kXcds) * xcd_events;
     const int64_t xend = min(n, xlo + xcd_events);
@@ -1815,6 +1810,7 @@ __global__ __launch_bounds__(kRouteLayerThreads) void route_layer_kernel(
         }
         *reinterpret_cast<uint2 *>(node_out + i0) = make_uint2(o[0], o[1]);
     }
+    if (rec) rec_g[lane] = rg;
     if (eflag) atomicOr(err, eflag);
 }
 
@@ -1877,7 +1873,7 @@ __global__ __launch_bounds__(kTransposeThreads) void transpose_codes_kernel(
 }
 
 // Routing of layer `layer` (>= 1) for the list-driven histogram pass.  The
-// parents' cuts come from their candidates as in route_layer_kernel, and
+// parents' cuts come from their best-cut keys as in route_layer_kernel, and
 // every event (node_in = null at layer 1: all at the root) gets its node of
 // this layer, node <- 2 node + [code >= cut] (section 1.1); with miss, an
 // event whose code of the cut feature is the missing code, or which stopped
@@ -1921,7 +1917,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     const uint8_t *__restrict__ xb, int64_t ldb, int64_t n, int d, int nbins,
     const uint8_t *__restrict__ node_in, uint8_t *__restrict__ node_out,
     const float *__restrict__ w, const uint8_t *__restrict__ vsign,
-    const double *__restrict__ cand_gain, const int *__restrict__ cand_cut, int cslices,
+    const double *__restrict__ cand_gain, const unsigned long long *__restrict__ keys, int cslices,
     uint8_t *__restrict__ rec_f, uint8_t *__restrict__ rec_c, double *__restrict__ rec_g,
     int layer, bool miss, int lmode, const uint64_t *__restrict__ hparent, uint32_t tau_bits,
     const uint32_t *__restrict__ cap_prev, uint32_t cap_root,
@@ -1938,33 +1934,30 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int nwaves = blockDim.x / kWave;
     int eflag = 0;
-    const CandSet cs{cand_gain, cand_cut, d, cslices};
-    for (int k = wave; k < (int)half; k += nwaves) {
+    // the parents' cuts from their best-cut keys (lane k of wavefront 0 takes
+    // parent k), and the child listed for each
+    const bool pwave = wave == 0 && lane < (int)half;
+    if (pwave) {
+        const int k = lane;
         int bf, bc;
-        double bg;
         bool ok;
-        node_best(cs, k, lane, &bf, &bc, &bg, &ok);
-        if (lane == 0) {
-            s_cf[k] = (uint8_t)bf;
-            s_cc[k] = (uint8_t)bc;
-            if (!ok) eflag |= kErrRoute;
-            if (blockIdx.x == 0 && rec_f) {
-                rec_f[k] = (uint8_t)bf;
-                rec_c[k] = (uint8_t)bc;
-                rec_g[k] = bg;
-            }
-            uint32_t side = 0u;
-            if (pick) {
-                // weights (signal + background, fixed point) left of the cut
-                // and in all, from the parent's prefix-summed row of its feature
-                const uint64_t *row = hparent + ((size_t)k * d + bf) * nbins * 2;
-                const int64_t left = (int64_t)(row[2 * (bc - 1)] + row[2 * (bc - 1) + 1]);
-                const int64_t all = (int64_t)(row[2 * (nbins - 1)] + row[2 * (nbins - 1) + 1]);
-                side = all - left < left ? 1u : 0u;
-            }
-            s_side[k] = (uint8_t)side;
-            if (blockIdx.x == 0 && pick) lside[k] = side;
+        KeySlots ks;
+        key_load(keys, k, ks);
+        key_cut(key_max(ks), d, &bf, &bc, &ok);
+        s_cf[k] = (uint8_t)bf;
+        s_cc[k] = (uint8_t)bc;
+        if (!ok) eflag |= kErrRoute;
+        uint32_t side = 0u;
+        if (pick) {
+            // weights (signal + background, fixed point) left of the cut
+            // and in all, from the parent's prefix-summed row of its feature
+            const uint64_t *row = hparent + ((size_t)k * d + bf) * nbins * 2;
+            const int64_t left = (int64_t)(row[2 * (bc - 1)] + row[2 * (bc - 1) + 1]);
+            const int64_t all = (int64_t)(row[2 * (nbins - 1)] + row[2 * (nbins - 1) + 1]);
+            side = all - left < left ? 1u : 0u;
         }
+        s_side[k] = (uint8_t)side;
+        if (blockIdx.x == 0 && pick) lside[k] = side;
     }
     if (wave == nwaves - 1) {
         // caps and starts of the lists: an exclusive scan of the caps
@@ -2080,6 +2073,11 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
         }
     }
     __syncthreads();
+    // workgroup 0 records the parents' cuts in the model (the gain's load in
+    // flight with the reservation)
+    const bool crec = pwave && blockIdx.x == 0 && rec_f;
+    const double rg = crec ? record_parent_cut(s_cf, s_cc, lane, d, cslices, cand_gain, rec_f,
+                                               rec_c) : 0.0;
     if (threadIdx.x < (unsigned)nslots) {
         const uint32_t c = s_cnt[threadIdx.x];
         s_base[threadIdx.x] = c ? atomicAdd(&cursor[threadIdx.x], c) : 0u;
@@ -2110,6 +2108,7 @@ __global__ __launch_bounds__(kRouteListThreads, 2 * kRouteListThreads / kWave / 
             }
         }
     }
+    if (crec) rec_g[lane] = rg;
     if (eflag) atomicOr(err, eflag);
 }
 
@@ -2992,7 +2991,7 @@ hipError_t launch_hist_np(const HistShape &hs, const uint8_t *xb, int64_t ldb, i
                           (uint32_t)hs.copies << 24;
     hist_kernel<ROUTED, NP, FPG, SIGNED, MISS><<<hs.blocks, hs.threads, hs.lds_bytes, s>>>(
         xb, w, node_in, ldb, n, hs.chunk_events, hs.xcd_events, geo, mode, pc.cand_gain,
-        pc.cand_cut, n_bins, scale, hs.copy_stride, vsign, node_out, pc.rec_f, pc.rec_c,
+        pc.keys, n_bins, scale, hs.copy_stride, vsign, node_out, pc.rec_f, pc.rec_c,
         pc.rec_g, partial, small, err, tl);
     return hipGetLastError();
 }
@@ -3133,19 +3132,21 @@ hipError_t launch_cut_scan(const uint64_t *partial, int chunks, int scale, const
                            size_t small_next_count, int hnodes, int d,
                            int n_bins, int mode, double *cand_gain, int *cand_cut,
                            const uint64_t *hparent, uint64_t *hout, hipStream_t s,
-                           const uint2 *lchunks, uint32_t *clear_words, int clear_count) {
+                           const uint2 *lchunks, uint32_t *clear_words, int clear_count,
+                           unsigned long long *keys, unsigned long long *keys_next) {
     const int S = cut_slices(n_bins);
     // one workgroup per (histogrammed node, or parent, feature, slice)
     const int groups = mode == kCutStopped ? hnodes / 2 : hnodes;
     if ((mode == kCutStopped && hnodes % 2 != 0) || (mode != kCutPlain && !hparent))
         return hipErrorInvalidValue;
+    if (keys && (mode == kCutPlain ? groups : 2 * groups) > kKeyNodes) return hipErrorInvalidValue;
     // rows padded to a multiple of the XCD count (see the kernel)
     const int blocks = (groups * d + kXcds - 1) / kXcds * kXcds * S;
 #define FBDT_CUT(M)                                                                             \
     cut_scan_kernel<M><<<blocks, kCutWaves * kWave, 0, s>>>(                                    \
         partial, chunks, scale, small, small_next, small_next_count, hnodes, d, n_bins, S,      \
         cand_gain, cand_cut, M == kCutPlain ? nullptr : hparent, hout, lchunks, clear_words,     \
-        clear_count, sany, sany_next)
+        clear_count, sany, sany_next, keys, keys_next)
     switch (mode) {
     case kCutPlain: FBDT_CUT(kCutPlain); break;
     case kCutSibling: FBDT_CUT(kCutSibling); break;
@@ -3179,7 +3180,7 @@ void leaf_go(int blocks, hipStream_t s, const uint8_t *xb, int64_t ldb, int64_t 
              const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc, int depth,
              bool missing, const float *v, const double *yts, double *leaf_partial, int *err) {
     leaf_kernel<ROUTED, NP><<<blocks, leaf_threads(depth, missing), leaf_lds_bytes(depth, missing),
-                              s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut,
+                              s>>>(xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.keys,
                                    pc.slices, pc.rec_f, pc.rec_c, pc.rec_g, depth, missing, v, yts,
                                    leaf_partial, err, xcd_range(n));
 }
@@ -3218,11 +3219,9 @@ hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
                               const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc,
                               int layer, bool miss, int *err, int cu_count, hipStream_t s) {
     if (layer < 1 || (1 << (layer - 1)) > 64) return hipErrorInvalidValue;
-    // one workgroup of 1024 threads per CU: every workgroup forms the
-    // parents' cuts from their candidates (up to 64 wavefront reductions
-    // over d x slices entries), so few, wide workgroups spread that over
-    // 16 wavefronts and read the candidates a quarter as often as four
-    // workgroups of 256 (workload 4's leaf routing: 41 -> 34 us)
+    // one workgroup of 1024 threads per CU (workload 4's leaf routing: 41
+    // -> 34 us against four workgroups of 256, measured when every
+    // workgroup reduced the parents' candidates itself)
     const int64_t R = xcd_range(n);
     int64_t per = (R + (int64_t)kHistE * kRouteLayerThreads - 1) /
                   ((int64_t)kHistE * kRouteLayerThreads);
@@ -3230,7 +3229,7 @@ hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
     if (per > cap) per = cap;
     if (per < 1) per = 1;
     route_layer_kernel<<<(unsigned)(kXcds * per), kRouteLayerThreads, 0, s>>>(
-        xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.cand_cut, pc.slices, pc.rec_f,
+        xb, ldb, n, d, node_in, node_out, pc.cand_gain, pc.keys, pc.slices, pc.rec_f,
         pc.rec_c, pc.rec_g, layer, miss, err, R);
     return hipGetLastError();
 }
@@ -3322,7 +3321,7 @@ hipError_t launch_route_list(const uint8_t *xb, int64_t ldb, int64_t n, int d, i
     const unsigned blocks = (unsigned)(kXcds * ((R + E - 1) / E));
 #define FBDT_ROUTE_LIST(SG, O32)                                                                \
     route_list_kernel<SG, O32><<<blocks, kRouteListThreads, 0, s>>>(                            \
-        xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.cand_cut, pc.slices, \
+        xb, ldb, n, d, n_bins, node_in, node_out, w, vsign, pc.cand_gain, pc.keys, pc.slices, \
         pc.rec_f, pc.rec_c, pc.rec_g, layer, miss, lmode, hparent, tau_bits, cap_prev, cap_root,  \
         cursor, lstart, lcap, lside, list, small, err, R, sany)
     if (vsign && off32)
