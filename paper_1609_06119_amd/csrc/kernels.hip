@@ -900,7 +900,6 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     // LDS addresses and banks; the copies are summed before the write-out.
     uint64_t *const lds_lane = reinterpret_cast<uint64_t *>(
         reinterpret_cast<char *>(lds) + (lane & (copies - 1)) * copy_stride);
-    const int nwaves = blockDim.x / kWave;
     int eflag = 0;
 
     // chunk p is chunk k of XCD x's event range [x R, (x + 1) R) (the range
@@ -1595,7 +1594,6 @@ __global__ __launch_bounds__(512) void leaf_kernel(
     const int half = nleaf >> 1;
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
-    const int nwaves = T / kWave;
     int eflag = 0;
     // the workgroups on XCD x = blockIdx % 8 take the events [x R, (x + 1) R)
     const int64_t xlo = (int64_t)(blockIdx.x % kXcds) * xcd_events;
