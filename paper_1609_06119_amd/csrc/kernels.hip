@@ -3217,13 +3217,14 @@ hipError_t launch_route_layer(const uint8_t *xb, int64_t ldb, int64_t n, int d,
                               const uint8_t *node_in, uint8_t *node_out, const ParentCuts &pc,
                               int layer, bool miss, int *err, int cu_count, hipStream_t s) {
     if (layer < 1 || (1 << (layer - 1)) > 64) return hipErrorInvalidValue;
-    // one workgroup of 1024 threads per CU (workload 4's leaf routing: 41
-    // -> 34 us against four workgroups of 256, measured when every
-    // workgroup reduced the parents' candidates itself)
+    // two workgroups of 1024 threads per CU (workload 4's leaf routing: 31
+    // -> 29.4 us against one; when every workgroup still reduced the
+    // parents' candidates itself, one per CU took 34 us against 41 with
+    // four workgroups of 256)
     const int64_t R = xcd_range(n);
     int64_t per = (R + (int64_t)kHistE * kRouteLayerThreads - 1) /
                   ((int64_t)kHistE * kRouteLayerThreads);
-    const int64_t cap = cu_count / kXcds > 0 ? cu_count / kXcds : 1;
+    const int64_t cap = 2 * cu_count / kXcds > 0 ? 2 * cu_count / kXcds : 1;
     if (per > cap) per = cap;
     if (per < 1) per = 1;
     route_layer_kernel<<<(unsigned)(kXcds * per), kRouteLayerThreads, 0, s>>>(
