@@ -551,6 +551,38 @@ def test_fit_on_constant_features_takes_zero_gain_cuts():
     assert np.allclose(sc.cpu().numpy(), F, rtol=1e-12)
 
 
+@pytest.mark.parametrize("lists", [1, 2], ids=["streaming", "lists"])
+def test_fit_on_duplicated_features_keeps_the_first_copy(lists):
+    """Every feature followed by an exact copy of itself: each cut on a copy
+    has bit for bit the gain of the same cut on the original, so the tie rule
+    (highest gain, then lowest feature, section 1.1) must pick the original
+    at every node, through the fit's best-cut keys, and the forest must be
+    the one fitted on the originals alone (cuts, gains, boost weights and
+    scores bit for bit), in the streaming and the list-driven layers."""
+    ds = make_training_set(4, n_events=40_009)
+    x = ds["x"][:12]
+    d, n = x.shape
+    B, D, T = 256, 5, 4
+    y, v = dev(ds["y"]), dev(ds["v"])
+    _, c1 = fb.bin(dev(x), B)
+    _, c2 = fb.bin(dev(np.concatenate([x, x])), B)
+    assert torch.equal(c2.data[d:2 * d, :n], c1.data[:d, :n])
+    fb.set_option("hist_lists", lists)
+    try:
+        runs = []
+        for codes in (c1, c2):
+            sc = torch.empty(n, dtype=torch.float64, device="cuda")
+            runs.append((fb.fit(codes, y, B, D, T, 0.1, 0.5, 7, w=v, score_out=sc).export(),
+                         sc.cpu().numpy()))
+    finally:
+        fb.set_option("hist_lists", 0)
+    (m1, s1), (m2, s2) = runs
+    assert (m2["cut_feature"] < d).all()
+    for key in ("cut_feature", "cut_bin", "gain", "leaf"):
+        assert np.array_equal(m1[key], m2[key]), key
+    assert np.array_equal(s1, s2)
+
+
 @pytest.mark.parametrize("mode", ["plain", "missing-signed-depth5"])
 def test_fit_graph_replays_match_eager_fit(mode):
     """The boosting loop is captured once per argument set and replayed; every
