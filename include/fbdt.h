@@ -111,8 +111,9 @@ int fbdt_bin_transform(const float *x, int64_t n, int32_t d, int64_t ldx, int32_
  * 2.1) on binned features: two-class LK_TreeBoost with a SplitMix64
  * Bernoulli sub-sample per tree, per-layer signal/background histograms of
  * all nodes and features in one pass, cumulative histograms, weighted Gini
- * separation gain, lowest-(feature, bin) argmax, and Newton-step terminal
- * weights.  xb: device uint8 [d][ldb]; y: device int8 [n]; w: device
+ * separation gain, lowest-(feature, bin) argmax (gains that agree in all
+ * but the last 16 of their 52 mantissa bits count as tied), and Newton-step
+ * terminal weights.  xb: device uint8 [d][ldb]; y: device int8 [n]; w: device
  * float32 [n] or NULL (event weights, any sign; each class's total must be
  * positive, else FBDT_E_LABEL); score_out: optional device float64 [n] that receives
  * the final score F of every event.  Codes must be < n_bins, except that
