@@ -328,9 +328,10 @@ constexpr int64_t kListMaxEvents = ((int64_t)1 << 31) - 1;
 // a workgroup reads an entry's codes as words)
 constexpr int kListFpgSizes[] = {4, 8, 12, 20, 28, 36, 40};
 bool list_fpg_supported(int f);
-// bytes per event of the event-major copy (d rounded up to 16, so that a
-// row is whole 16-byte words), and the copy's size (events rounded up to
-// 256)
+// bytes per event of the event-major copy (d rounded up to 16, 32 or 64,
+// then to a multiple of 64, so that a row is whole 16-byte words and never
+// straddles a 64-byte memory segment), and the copy's size (events rounded
+// up to 256)
 int list_row_bytes(int d);
 size_t list_codes_bytes(int64_t n, int d);
 hipError_t launch_transpose_codes(const uint8_t *xb, int64_t ldb, int64_t n, int d, uint8_t *xr,
