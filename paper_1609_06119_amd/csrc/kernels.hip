@@ -587,6 +587,7 @@ struct HistArgs {
     const uint8_t *xb;
     int64_t ldb, n;
     int d, nbins, layer, nodes, half, j0, nf, k0, nk, scale;
+    int jstep;                        // the group's features: j0, j0 + jstep, ... (nf of them)
     bool miss;                        // n_bins <= kMissingCode: code kMissingCode is missing
     bool sib;                         // left children only (right = parent - left)
     uint32_t tau_bits;                // bits of the smallest weight on the fixed-point grid
@@ -624,7 +625,7 @@ __device__ __forceinline__ void hist_load(HistStep<NP, FPG> &st, const HistArgs 
 #pragma unroll
     for (int ff = 0; ff < FPG; ++ff)
         st.codes[ff] = *reinterpret_cast<const uint2 *>(
-            a.xb + (int64_t)min(a.j0 + ff, a.d - 1) * a.ldb + i0);
+            a.xb + (int64_t)min(a.j0 + ff * a.jstep, a.d - 1) * a.ldb + i0);
     if (SIGNED) st.vs = *reinterpret_cast<const uint2 *>(a.vsign + i0);
     if (with_rows) hist_load_rows<ROUTED, NP, FPG, SIGNED, MISS>(st, a, s_cf, i0);
 }
@@ -759,7 +760,7 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
                     if (ff < a.nf && bin >= (uint32_t)a.nbins && !missing) eflag |= kErrBin;
                     if (ff < a.nf && bin < (uint32_t)a.nbins) {
                         const size_t gi =
-                            ((((size_t)nl[e] * a.d + a.j0 + ff) * a.nbins + bin) * 2) +
+                            ((((size_t)nl[e] * a.d + a.j0 + ff * a.jstep) * a.nbins + bin) * 2) +
                             (bits >> 31);
                         atomicAdd(&a.small[gi], wa);
                     }
@@ -772,7 +773,8 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
 // The end of a histogram workgroup, after its adds (and an LDS barrier):
 // the LDS copies are summed into copy 0, bins >= n_bins are checked to be
 // empty (but for the missing code's with miss), and the rows (k, f), k < nk,
-// f < nf (LDS row k * fpg + f) are written to out[(k0 + k) * d + j0 + f]
+// f < nf (LDS row k * fpg + f, feature j0 + f * jstep) are written to
+// out[(k0 + k) * d + j0 + f * jstep]
 // [bin], the two classes of a bin in one 16-byte element: one row per
 // wavefront step.  With prefix (the fit's passes) every row is written as
 // inclusive prefix sums over bins, P(b) = sum of the bins <= b per class:
@@ -782,8 +784,8 @@ __device__ __forceinline__ void hist_add(const HistStep<NP, FPG> &st, const Hist
 // wavefront.
 __device__ __forceinline__ void hist_write_rows(uint64_t *lds, int copies, int copy_stride,
                                                 int lds_n, int nk, int nf, int fpg, int k0,
-                                                int j0, int d, int nbins, bool miss, bool prefix,
-                                                uint4 *out, int &eflag) {
+                                                int j0, int jstep, int d, int nbins, bool miss,
+                                                bool prefix, uint4 *out, int &eflag) {
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int nwaves = blockDim.x / kWave;
     if (copies > 1) {   // copy 0 += the others
@@ -800,7 +802,7 @@ __device__ __forceinline__ void hist_write_rows(uint64_t *lds, int copies, int c
         const int k = rr / nf;
         const int f = rr - k * nf;
         const uint4 *src = reinterpret_cast<const uint4 *>(lds + (k * fpg + f) * kRow);
-        uint4 *dst = out + ((size_t)(k0 + k) * d + j0 + f) * nbins;
+        uint4 *dst = out + ((size_t)(k0 + k) * d + j0 + f * jstep) * nbins;
         // bins >= n_bins must be empty, but for the missing code's
         for (int t = nbins + lane; t < (miss ? kMissingCode : 256); t += kWave) {
             const uint4 v = src[t];
@@ -880,8 +882,14 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     a.half = a.nodes >> 1;
     a.sib = layer >= 1 && sib;
     const int hnodes = a.sib ? a.half : a.nodes;   // histogrammed nodes
-    a.j0 = g * FPG;
-    a.nf = min(FPG, d - a.j0);
+    // features dealt to the G groups in turn (feature j in group j % G), so
+    // that features of few distinct codes, whose atomics pile onto a few
+    // counters and which data sets tend to hold side by side, spread over the
+    // groups instead of making one group the slowest (workload 4's eight
+    // discrete features 32-39 in groups of 5: layer 0 145 -> 134 us)
+    a.j0 = g;
+    a.jstep = G;
+    a.nf = (d - g + G - 1) / G;
     a.k0 = h * npg;
     a.nk = min(npg, hnodes - a.k0);
     a.scale = scale;
@@ -963,9 +971,9 @@ __global__ __launch_bounds__(1024) void hist_kernel(
     lds_barrier();
     if (rec) rec_g[lane] = rg;
     const unsigned long long t_adds = stamp ? (unsigned long long)wall_clock64() : 0ull;
-    hist_write_rows(lds, copies, copy_stride, lds_n, a.nk, a.nf, FPG, a.k0, a.j0, d, nbins,
-                    a.miss, prefix, reinterpret_cast<uint4 *>(partial + (size_t)p * hnodes * d * nbins * 2),
-                    eflag);
+    hist_write_rows(lds, copies, copy_stride, lds_n, a.nk, a.nf, FPG, a.k0, a.j0, a.jstep, d,
+                    nbins, a.miss, prefix,
+                    reinterpret_cast<uint4 *>(partial + (size_t)p * hnodes * d * nbins * 2), eflag);
     if (eflag) atomicOr(err, eflag);
     if (stamp) {
         unsigned long long *row = tl + (size_t)blockIdx.x * kTimelineStamps;
@@ -1014,8 +1022,8 @@ __global__ __launch_bounds__(1024) void hist_reference_kernel(
             x[k] = reinterpret_cast<const uint4 *>(w + i)[0];
             y[k] = reinterpret_cast<const uint4 *>(w + i)[1];
             nd[k] = node ? *reinterpret_cast<const uint2 *>(node + i) : make_uint2(0u, 0u);
-            c0[k] = *reinterpret_cast<const uint2 *>(xb + (int64_t)min(g * fpg, d - 1) * ldb + i);
-            c1[k] = *reinterpret_cast<const uint2 *>(xb + (int64_t)min(g * fpg + 1, d - 1) * ldb + i);
+            c0[k] = *reinterpret_cast<const uint2 *>(xb + (int64_t)min(g, d - 1) * ldb + i);
+            c1[k] = *reinterpret_cast<const uint2 *>(xb + (int64_t)min(g + G, d - 1) * ldb + i);
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k)
@@ -1035,7 +1043,7 @@ __global__ __launch_bounds__(1024) void hist_reference_kernel(
         }
         for (int ff = 0; ff < fpg; ++ff) {
             const uint2 c = *reinterpret_cast<const uint2 *>(
-                xb + (int64_t)min(g * fpg + ff, d - 1) * ldb + i);
+                xb + (int64_t)min(g + ff * G, d - 1) * ldb + i);
             acc ^= c.x ^ c.y;
         }
     }
@@ -2283,7 +2291,7 @@ __global__ __launch_bounds__(1024) void hist_list_kernel(
     }
     lds_barrier();
     int eflag = 0;
-    hist_write_rows(lds, copies, copy_stride, lds_n, 1, nf, FPG, 0, j0, d, nbins, miss, true,
+    hist_write_rows(lds, copies, copy_stride, lds_n, 1, nf, FPG, 0, j0, 1, d, nbins, miss, true,
                     reinterpret_cast<uint4 *>(partial + (size_t)(pbase + c) * d * nbins * 2),
                     eflag);
     if (eflag) atomicOr(err, eflag);
