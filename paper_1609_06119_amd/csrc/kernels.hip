@@ -1872,7 +1872,7 @@ __global__ __launch_bounds__(kTransposeThreads) void transpose_codes_kernel(
     __syncthreads();
     const int ev = (int)min((int64_t)E, n - i0);
     uint32_t *dst = reinterpret_cast<uint32_t *>(xr + (size_t)i0 * dr);
-    for (int o = threadIdx.x; o < ev * W; o += blockDim.x) {   // ev * W <= 65536 / 4
+    for (int o = threadIdx.x; o < ev * W; o += blockDim.x) {   // ev * W <= 32768 / 4
         const int e = o / W;
         dst[o] = tile[e * WS + (o - e * W)];
     }
@@ -3266,9 +3266,11 @@ hipError_t launch_transpose_codes(const uint8_t *xb, int64_t ldb, int64_t n, int
                                   hipStream_t s) {
     const int dr = list_row_bytes(d);
     if (d < 1 || dr > 256 || n < 1) return hipErrorInvalidValue;
-    // events per workgroup: up to 1024, as many as a 64 KiB tile holds
+    // events per workgroup: up to 1024, as many as a 32 KiB tile holds, so
+    // that several workgroups share a CU (10M x 40 in 64-byte rows: 0.62 ms
+    // with 64 KiB tiles, 0.52 ms with 32 KiB, 0.64 ms with 16 KiB)
     const size_t row = (size_t)(dr / 4 + 1) * 4;
-    int E = (int)std::min<size_t>(1024, 65536 / row) & ~63;
+    int E = (int)std::min<size_t>(1024, 32768 / row) & ~63;
     if (E < 64) return hipErrorInvalidValue;
     transpose_codes_kernel<<<(unsigned)((n + E - 1) / E), kTransposeThreads, (size_t)E * row, s>>>(
         xb, ldb, n, d, xr, dr, E);
