@@ -95,6 +95,11 @@ CASES = {
                                      weights="signed", missing=True),
     # 255 features: seven groups of 40, the last holding 15
     "255-features-depth4": dict(cfg=3, n_events=5003, d=255, depth=4, n_trees=3),
+    # event-major rows of 32 bytes (17 features: one group of 20), and of
+    # 128 bytes (65 features: groups of 36 and 29, the second read word by
+    # word from the middle of the row)
+    "17-features-depth5": dict(cfg=4, n_events=20_011, d=17, depth=5, n_trees=3),
+    "65-features-depth4": dict(cfg=3, n_events=12_007, d=65, depth=4, n_trees=3),
     "3-bins-depth5": dict(cfg=2, n_events=20_011, depth=5, n_bins=3, n_trees=4),
 }
 
